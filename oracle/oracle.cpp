@@ -1,0 +1,416 @@
+// CPU oracle for the PackServe window scorer.  TEST INFRASTRUCTURE ONLY:
+// only the tests, the smoke check and the benchmark's CPU-baseline leg may
+// load or call it.  The GPU library never links, includes or calls it, and
+// it shares no code, header, table or constant generator with that library.
+//
+// It is the plain, slow, obviously correct reading of the paper's method:
+// Algorithm 1 (KVC-first, SLO-aware request packing) taken step by step for
+// one request at a time, in fp64 (fp32 interface values are widened
+// exactly), with a naive block-by-block prefix walk over a hash set per
+// instance and an exhaustive selection over all instances.
+//
+// Functions and what pins them (tests under tests/ marked "not gpu"):
+//   prefix_hit      - longest cached prefix (Sec. 7, local prefix tree; the
+//                     N new / C cached split of Sec. 5.2).  Pinned by brute-
+//                     force token-level longest-common-prefix on tiny windows
+//                     and by the generator's construction (owner hits).
+//   t_prefill       - Eq. 7 plus the empirical C and C^2 terms of Sec. 5.3.
+//                     Pinned by hand-computed cases and special cases.
+//   recompute_cost, cache_benefit, filter - Eq. 9 with Alg. 1's KVC-first
+//                     stage.  Pinned by the hand-worked example and the
+//                     eta = 0 / Z = 0 special cases the paper states.
+//   predict_tpot    - Eq. 10 with the per-segment decode model of Eq. 8 and
+//                     the EMA factor of Sec. 5.3.  Pinned by hand cases, the
+//                     A = 0 special case and the single-segment reduction.
+//   select          - decode-batch-size-centric key (Sec. 6.2, Table 4's
+//                     D-C-Q) and the cache-aware load-balancing fallback
+//                     (LMetric product, Sec. 8.1 baselines).  Pinned by hand
+//                     cases, exhaustive brute force and invariants.
+//   commit          - sequential application of decisions (Sec. 7: state is
+//                     updated along the request path).  Pinned by a
+//                     hand-traced sequence.
+//
+// parity unpinned (the paper leaves these open; the oracle follows the
+// readings listed in the design notes and only hand cases of those readings
+// pin it): the capacity rule behind CapacityCandidates (A_i + 1 <= B_max and
+// S_i + L_r <= M_KV), the projected context S+ = S_i + L_r, the queueing
+// estimate alpha0 * Q_i + alpha1 * P_i inside predicted TTFT, snapshot
+// semantics within a window, and the outputs of a rejected request.
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <unordered_set>
+#include <vector>
+
+#include <omp.h>
+
+extern "C" {
+
+// Oracle-local model/policy description (fp64).  The Python wrapper widens
+// the fp32 interface coefficients into it exactly.
+typedef struct {
+  double alpha[6];      // T_pf(N, C) = a0 + a1 N + a2 N C + a3 N^2 + a4 C + a5 C^2
+  int32_t n_seg;        // decode segments
+  int32_t seg_ub[32];   // inclusive upper batch size of each segment, ascending
+  double beta[32][3];   // T_iter(B, S) = b0 + b1 B + b2 S, per segment
+  double gamma[32];     // EMA factor per segment
+  double eta;           // recomputation budget
+  double tau;           // TPOT target
+  double ttft_floor;    // minimum TTFT budget
+  double lout;          // recent median output length
+  int32_t block_tokens; // tokens per block
+  int32_t b_max;        // engine batch limit
+  int64_t kv_cap;       // KV capacity, tokens
+  uint32_t flags;       // 1 TTFT admission, 2 no KVC filter, 4 no TPOT filter
+} orc_model;
+
+}  // extern "C"
+
+namespace {
+
+constexpr uint32_t F_TTFT_ADMIT = 1u, F_NO_KVC = 2u, F_NO_TPOT = 4u;
+constexpr uint32_t R_REJECT = 1u, R_FALLBACK = 2u, R_TTFT_MISS = 4u;
+constexpr uint32_t NB_RHO = 1u, NB_TPOT = 2u, NB_TTFT = 4u, NB_Z = 8u, NB_MISSFLAG = 16u;
+constexpr double NB_REL = 1e-5;
+
+struct Snapshot {
+  int32_t n_inst = 0;
+  int32_t cap = 0;
+  std::vector<std::unordered_set<uint64_t>> sets;
+  std::vector<int32_t> D, Q;
+  std::vector<int64_t> P, S;
+};
+
+struct Chain {
+  const uint64_t* a;
+  int32_t na;
+  const uint64_t* b;
+  int32_t nb;
+  int32_t len() const { return na + nb; }
+  uint64_t at(int32_t j) const { return j < na ? a[j] : b[j - na]; }
+};
+
+// Longest cached prefix, in blocks: walk the chain from its first block and
+// stop at the first block the instance does not hold.
+int64_t prefix_hit(const std::unordered_set<uint64_t>& set, const Chain& ch) {
+  int32_t j = 0;
+  while (j < ch.len() && set.count(ch.at(j)) != 0) ++j;
+  return j;
+}
+
+// Eq. 7 with the two empirical cache terms: N new tokens, C cached tokens.
+double t_prefill(const orc_model& m, double N, double C) {
+  const double* a = m.alpha;
+  return a[0] + a[1] * N + a[2] * N * C + a[3] * N * N + a[4] * C + a[5] * C * C;
+}
+
+// Decode segment for a projected batch size: the first segment whose
+// inclusive upper bound covers it, else the last one.
+int segment_of(const orc_model& m, int64_t B) {
+  for (int s = 0; s < m.n_seg; ++s)
+    if (B <= m.seg_ub[s]) return s;
+  return m.n_seg - 1;
+}
+
+struct Cand {
+  int32_t i;
+  int64_t hit;  // blocks
+  int64_t n, c; // new / cached tokens
+  double W;     // recomputation cost
+  double rho;
+  double tpot, ttft;
+  bool inC, inT;
+};
+
+struct Decision {
+  int32_t inst;
+  int32_t hit;
+  double ttft, tpot;
+  uint32_t flags;
+  uint32_t nA, nC, nT;
+  uint32_t nb;
+};
+
+// Algorithm 1 for one request against the snapshot.  Fills every
+// capacity-eligible candidate (with its memberships) into A and returns the
+// decision.
+Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std::vector<Cand>& A) {
+  Decision d{-1, 0, 0.0, 0.0, R_REJECT, 0, 0, 0, 0};
+  const int64_t L = (int64_t)ch.len() * m.block_tokens;
+  const double Ld = (double)L;
+
+  // Capacity guard: instances that can take one more active request and the
+  // request's tokens.
+  A.clear();
+  for (int32_t i = 0; i < sn.n_inst; ++i) {
+    int64_t active = (int64_t)sn.D[i] + sn.Q[i];
+    if (active + 1 <= m.b_max && sn.S[i] + L <= m.kv_cap) {
+      Cand c{};
+      c.i = i;
+      A.push_back(c);
+    }
+  }
+  d.nA = (uint32_t)A.size();
+  if (A.empty()) return d;
+
+  // KVC-first recomputation filtering.
+  const double tpf_cached = t_prefill(m, 0.0, Ld);  // fully cached input
+  const double tpf_cold = t_prefill(m, Ld, 0.0);    // fully uncached input
+  double Wmin = INFINITY;
+  int64_t hit_at_min = -1;  // hit of the first minimiser (for the near-boundary rule)
+  for (Cand& c : A) {
+    c.hit = prefix_hit(sn.sets[c.i], ch);
+    c.c = c.hit * m.block_tokens;
+    c.n = L - c.c;
+    c.W = std::max(0.0, t_prefill(m, (double)c.n, (double)c.c) - tpf_cached);
+    if (c.W < Wmin) {
+      Wmin = c.W;
+      hit_at_min = c.hit;
+    }
+  }
+  const double Z = tpf_cold - tpf_cached;
+  const bool kvc_on = !(m.flags & F_NO_KVC);
+  if (kvc_on && std::fabs(Z) <= NB_REL * std::fabs(tpf_cold)) d.nb |= NB_Z;
+  for (Cand& c : A) {
+    if (!kvc_on || Z <= 0.0) {
+      c.rho = 0.0;
+      c.inC = true;
+    } else {
+      c.rho = (c.W - Wmin) / Z;
+      c.inC = c.rho <= m.eta;
+      // A candidate with the minimiser's own hit has rho = 0 exactly under
+      // any rounding; every other rho within the relative window of eta is
+      // decided by rounding.
+      const bool exact_zero = c.W == Wmin && c.hit == hit_at_min;
+      if (!exact_zero && std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0)) d.nb |= NB_RHO;
+    }
+  }
+
+  // SLO-aware admission (Eq. 10) and the TTFT estimate (Eq. 4).
+  const double slo = std::max(m.ttft_floor, tpf_cold);
+  for (Cand& c : A) {
+    const int32_t i = c.i;
+    const int64_t active = (int64_t)sn.D[i] + sn.Q[i];
+    const int64_t Bp = active + 1;
+    const double Sp = (double)(sn.S[i] + L);
+    const int s = segment_of(m, Bp);
+    const double t_iter = m.gamma[s] * (m.beta[s][0] + m.beta[s][1] * (double)Bp + m.beta[s][2] * Sp);
+    const double tpf = t_prefill(m, (double)c.n, (double)c.c);
+    const double interference = active > 0 ? tpf / std::max(1.0, m.lout) : 0.0;
+    c.tpot = t_iter + interference;
+    c.ttft = tpf + m.alpha[0] * (double)sn.Q[i] + m.alpha[1] * (double)sn.P[i];
+    const bool tpot_ok = (m.flags & F_NO_TPOT) || c.tpot < m.tau;
+    const bool ttft_ok = !(m.flags & F_TTFT_ADMIT) || c.ttft <= slo;
+    c.inT = c.inC && tpot_ok && ttft_ok;
+    if (!(m.flags & F_NO_TPOT) && std::fabs(c.tpot - m.tau) <= NB_REL * m.tau) d.nb |= NB_TPOT;
+    if ((m.flags & F_TTFT_ADMIT) && std::fabs(c.ttft - slo) <= NB_REL * slo) d.nb |= NB_TTFT;
+  }
+  for (const Cand& c : A) {
+    d.nC += c.inC;
+    d.nT += c.inT;
+  }
+
+  // Decode-batch-size-centric packing: most decoding requests, then most
+  // cached blocks, then fewest queued, then lowest instance id.
+  const Cand* best = nullptr;
+  for (const Cand& c : A) {
+    if (!c.inT) continue;
+    if (!best) { best = &c; continue; }
+    const int32_t Dc = sn.D[c.i], Db = sn.D[best->i];
+    const int32_t Qc = sn.Q[c.i], Qb = sn.Q[best->i];
+    bool better;
+    if (Dc != Db) better = Dc > Db;
+    else if (c.hit != best->hit) better = c.hit > best->hit;
+    else if (Qc != Qb) better = Qc < Qb;
+    else better = c.i < best->i;
+    if (better) best = &c;
+  }
+  d.flags = 0;
+  if (!best) {
+    // Cache-aware load balancing over the KVC-admissible set: the product of
+    // pending uncached prefill tokens and active requests, both counting the
+    // arriving request; ties to the lowest id.
+    unsigned __int128 bestv = 0;
+    for (const Cand& c : A) {
+      if (!c.inC) continue;
+      const int64_t active = (int64_t)sn.D[c.i] + sn.Q[c.i];
+      unsigned __int128 v = (unsigned __int128)(uint64_t)(sn.P[c.i] + c.n) *
+                            (unsigned __int128)(uint64_t)(active + 1);
+      if (!best || v < bestv || (v == bestv && c.i < best->i)) {
+        best = &c;
+        bestv = v;
+      }
+    }
+    d.flags |= R_FALLBACK;
+  }
+  d.inst = best->i;
+  d.hit = (int32_t)best->hit;
+  d.ttft = best->ttft;
+  d.tpot = best->tpot;
+  if (best->ttft > slo) d.flags |= R_TTFT_MISS;
+  if (std::fabs(best->ttft - slo) <= NB_REL * slo) d.nb |= NB_MISSFLAG;
+  return d;
+}
+
+Chain chain_of(const uint64_t* pool, const int64_t* pre_off, const int32_t* pre_len,
+               const int64_t* tail_off, const int32_t* tail_len, int32_t r) {
+  return Chain{pool + pre_off[r], pre_len[r], pool + tail_off[r], tail_len[r]};
+}
+
+}  // namespace
+
+extern "C" {
+
+// Build a snapshot: a hash set per instance from the CSR block lists, plus a
+// copy of the load counters.  Returns 0, or -2 on allocation failure.
+int orc_load(int32_t n_inst, int32_t cap, const int64_t* blk_off, const uint64_t* blk,
+             const int32_t* D, const int32_t* Q, const int64_t* P, const int64_t* S, void** out) {
+  *out = nullptr;
+  Snapshot* sn = new (std::nothrow) Snapshot();
+  if (!sn) return -2;
+  try {
+    sn->n_inst = n_inst;
+    sn->cap = cap;
+    sn->sets.resize((size_t)n_inst);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t i = 0; i < n_inst; ++i) {
+      auto& st = sn->sets[(size_t)i];
+      st.reserve((size_t)(blk_off[i + 1] - blk_off[i]) * 2 + 16);
+      for (int64_t k = blk_off[i]; k < blk_off[i + 1]; ++k) st.insert(blk[k]);
+    }
+    sn->D.assign(D, D + n_inst);
+    sn->Q.assign(Q, Q + n_inst);
+    sn->P.assign(P, P + n_inst);
+    sn->S.assign(S, S + n_inst);
+  } catch (const std::bad_alloc&) {
+    delete sn;
+    return -2;
+  }
+  *out = sn;
+  return 0;
+}
+
+void orc_free(void* h) { delete static_cast<Snapshot*>(h); }
+
+// Prefix hit of every request on every instance (no capacity test):
+// hits[r * n_inst + i].
+int orc_hits(void* h, const uint64_t* pool, const int64_t* pre_off, const int32_t* pre_len,
+             const int64_t* tail_off, const int32_t* tail_len, int32_t n_req, uint32_t* hits,
+             int32_t nthreads) {
+  const Snapshot& sn = *static_cast<Snapshot*>(h);
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int32_t r = 0; r < n_req; ++r) {
+    Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, r);
+    for (int32_t i = 0; i < sn.n_inst; ++i)
+      hits[(size_t)r * sn.n_inst + i] = (uint32_t)prefix_hit(sn.sets[(size_t)i], ch);
+  }
+  return 0;
+}
+
+// Algorithm 1 for every request of the window against the same snapshot.
+// sizes (optional) receives |A|, |C|, |T| per request; nb (optional) the
+// near-boundary bits.
+int orc_score(void* h, const orc_model* m, const uint64_t* pool, const int64_t* pre_off,
+              const int32_t* pre_len, const int64_t* tail_off, const int32_t* tail_len,
+              int32_t n_req, int32_t* inst, int32_t* hit, double* ttft, double* tpot,
+              uint32_t* flags, uint32_t* sizes, uint32_t* nb, int32_t nthreads) {
+  const Snapshot& sn = *static_cast<Snapshot*>(h);
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int32_t r = 0; r < n_req; ++r) {
+    Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, r);
+    std::vector<Cand> A;
+    Decision d = score_one(sn, *m, ch, A);
+    inst[r] = d.inst;
+    hit[r] = d.hit;
+    ttft[r] = d.ttft;
+    tpot[r] = d.tpot;
+    flags[r] = d.flags;
+    if (sizes) {
+      sizes[3 * (size_t)r] = d.nA;
+      sizes[3 * (size_t)r + 1] = d.nC;
+      sizes[3 * (size_t)r + 2] = d.nT;
+    }
+    if (nb) nb[r] = d.nb;
+  }
+  return 0;
+}
+
+// Per-candidate detail of one request (for tests): for every instance,
+// elig[i] = 1 if capacity-eligible; for those, hit, W, rho, TPOT, TTFT and
+// C / T membership.  Returns the chosen instance (-1 on reject).
+int orc_explain(void* h, const orc_model* m, const uint64_t* chain, int32_t len,
+                uint8_t* elig, uint32_t* hit, double* W, double* rho, double* tpot,
+                double* ttft, uint8_t* inC, uint8_t* inT) {
+  const Snapshot& sn = *static_cast<Snapshot*>(h);
+  Chain ch{chain, len, chain, 0};
+  std::vector<Cand> A;
+  Decision d = score_one(sn, *m, ch, A);
+  for (int32_t i = 0; i < sn.n_inst; ++i) {
+    elig[i] = 0; hit[i] = 0; W[i] = rho[i] = tpot[i] = ttft[i] = 0.0; inC[i] = inT[i] = 0;
+  }
+  for (const Cand& c : A) {
+    elig[c.i] = 1;
+    hit[c.i] = (uint32_t)c.hit;
+    W[c.i] = c.W;
+    rho[c.i] = c.rho;
+    tpot[c.i] = c.tpot;
+    ttft[c.i] = c.ttft;
+    inC[c.i] = c.inC;
+    inT[c.i] = c.inT;
+  }
+  return d.inst;
+}
+
+// Apply decisions in array order: the arriving request joins the queue of
+// its instance (Q += 1), adds its uncached tokens to the pending prefill
+// work (measured against the table as left by the earlier entries), adds its
+// tokens to the context sum, and its blocks enter the instance's set in
+// chain order until the cap is reached.  Entries with instance -1 are
+// skipped.  Returns the number of blocks refused at the cap in *dropped.
+int orc_commit(void* h, const uint64_t* pool, const int64_t* pre_off, const int32_t* pre_len,
+               const int64_t* tail_off, const int32_t* tail_len, const int32_t* inst, int32_t n,
+               int32_t block_tokens, int64_t* dropped) {
+  Snapshot& sn = *static_cast<Snapshot*>(h);
+  int64_t drop = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t i = inst[k];
+    if (i < 0) continue;
+    Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, k);
+    auto& set = sn.sets[(size_t)i];
+    const int64_t L = (int64_t)ch.len() * block_tokens;
+    const int64_t hitb = prefix_hit(set, ch);
+    sn.Q[i] += 1;
+    sn.P[i] += L - hitb * block_tokens;
+    sn.S[i] += L;
+    for (int32_t j = 0; j < ch.len(); ++j) {
+      uint64_t key = ch.at(j);
+      if (set.count(key)) continue;
+      if ((int64_t)set.size() < sn.cap) set.insert(key);
+      else ++drop;
+    }
+  }
+  *dropped = drop;
+  return 0;
+}
+
+// Read back the load counters and set sizes.
+int orc_state(void* h, int32_t* D, int32_t* Q, int64_t* P, int64_t* S, int64_t* set_size) {
+  const Snapshot& sn = *static_cast<Snapshot*>(h);
+  for (int32_t i = 0; i < sn.n_inst; ++i) {
+    D[i] = sn.D[i];
+    Q[i] = sn.Q[i];
+    P[i] = sn.P[i];
+    S[i] = sn.S[i];
+    set_size[i] = (int64_t)sn.sets[(size_t)i].size();
+  }
+  return 0;
+}
+
+int orc_max_threads(void) { return omp_get_max_threads(); }
+
+}  // extern "C"

@@ -1,0 +1,282 @@
+"""Seeded synthetic scheduling windows (shared input generator).
+
+This package draws the inputs that both the CPU oracle and the GPU library
+score: chained 64-bit block hashes of agent sessions, per-instance cached
+block sets, per-instance load counters and fp32 latency-model coefficients.
+It holds none of the scheduler's arithmetic.  The native part is
+``psgen.cpp`` (built into ``libpsgen.so`` by :func:`build`).
+
+The named workloads ``c1`` .. ``c5`` are the five scheduling windows the
+benchmarks and parity tests run on:
+
+==== ========= ========= ======== ============== ======= ===================================
+name instances requests sessions  prefix blocks  cap     notes
+==== ========= ========= ======== ============== ======= ===================================
+c1   16        1,024     64       64-128         4,096   uniform owner, TPOT 50 ms, B_max 64
+c2   64        16,384    1,024    512-4,096      65,536  owner Zipf(1.1), TPOT 30/50 ms
+c3   1,024     65,536    8,192    256-8,192      65,536  40% share a 128-block system prompt
+c4   256       32,768    512      2,048-12,500   65,536  request Zipf(1.4), 85% saturated
+c5   4,096     262,144   32,768   64-4,096       32,768  uniform scatter, early misses
+==== ========= ========= ======== ============== ======= ===================================
+
+Load and model constants follow the paper's testbed where it states them:
+B_max 64 and about one million KV tokens per instance (Sec. 8.1, testbed
+paragraph) for c1, and the 3x host tier on top for the larger windows
+(B_max 512, 4,194,304 tokens); eta = 0.5 (the default budget of Sec. 8.2);
+a recent median output length of 556 tokens (mean output of Table 2);
+decode segments bounded at batch sizes 8..512 with gamma = 1 up to 16 and
+U[1.05, 1.25] above (underestimation above batch size 16, Sec. 8.3.3).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass, field
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libpsgen.so")
+_lib = None
+
+
+def build(verbose: bool = False) -> str:
+    """Compile ``psgen.cpp`` into ``libpsgen.so`` (always recompiles)."""
+    src = os.path.join(_HERE, "psgen.cpp")
+    tmp = _LIB_PATH + ".tmp"
+    cmd = ["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-o", tmp, src]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    global _lib
+    _lib = None
+    return _LIB_PATH
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [
+        ("n_inst", ctypes.c_int32), ("n_req", ctypes.c_int32), ("n_sess", ctypes.c_int32),
+        ("ps_min", ctypes.c_int32), ("ps_max", ctypes.c_int32),
+        ("fresh_min", ctypes.c_int32), ("fresh_max", ctypes.c_int32),
+        ("n_steps", ctypes.c_int32), ("step_blocks", ctypes.c_int32),
+        ("owner_zipf", ctypes.c_int32), ("owner_zipf_s", ctypes.c_double),
+        ("req_zipf", ctypes.c_int32), ("req_zipf_s", ctypes.c_double),
+        ("sp_frac", ctypes.c_double), ("sp_blocks", ctypes.c_int32),
+        ("cache_u_min", ctypes.c_double), ("cache_u_max", ctypes.c_double),
+        ("cap", ctypes.c_int32),
+        ("d_min", ctypes.c_int32), ("d_max", ctypes.c_int32),
+        ("q_min", ctypes.c_int32), ("q_max", ctypes.c_int32),
+        ("ctx_min", ctypes.c_int32), ("ctx_max", ctypes.c_int32),
+        ("p_max", ctypes.c_int64),
+        ("sat_frac", ctypes.c_double),
+        ("sat_d_min", ctypes.c_int32), ("sat_d_max", ctypes.c_int32),
+        ("sat_s_min", ctypes.c_int64), ("sat_s_max", ctypes.c_int64),
+        ("n_seg", ctypes.c_int32), ("seg_ub", ctypes.c_int32 * 32),
+        ("gamma_unit_ub", ctypes.c_int32),
+        ("gamma_min", ctypes.c_double), ("gamma_max", ctypes.c_double),
+        ("alpha_nom", ctypes.c_double * 6), ("beta_nom", ctypes.c_double * 3),
+        ("coef_jitter", ctypes.c_double),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is missing: run synth.build() first")
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.psg_generate.argtypes = [ctypes.POINTER(_Params), ctypes.POINTER(ctypes.c_void_p)]
+    lib.psg_generate.restype = ctypes.c_int
+    lib.psg_free.argtypes = [ctypes.c_void_p]
+    lib.psg_free.restype = None
+    lib.psg_sizes.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]
+    lib.psg_sizes.restype = None
+    lib.psg_field.argtypes = [ctypes.c_void_p, ctypes.c_char_p]
+    lib.psg_field.restype = ctypes.c_void_p
+    lib.psg_splitmix64.argtypes = [ctypes.c_uint64]
+    lib.psg_splitmix64.restype = ctypes.c_uint64
+    _lib = lib
+    return lib
+
+
+# Default generation parameters (c1); other workloads override fields.
+_DEFAULTS = dict(
+    n_inst=16, n_req=1024, n_sess=64, ps_min=64, ps_max=128, fresh_min=1, fresh_max=4,
+    n_steps=8, step_blocks=8, owner_zipf=0, owner_zipf_s=1.0, req_zipf=0, req_zipf_s=1.0,
+    sp_frac=0.0, sp_blocks=0, cache_u_min=0.3, cache_u_max=1.0, cap=4096,
+    d_min=0, d_max=64, q_min=0, q_max=4, ctx_min=2048, ctx_max=16384, p_max=8192,
+    sat_frac=0.0, sat_d_min=0, sat_d_max=0, sat_s_min=0, sat_s_max=0,
+    seg_ub=(8, 16, 32, 64, 128, 256, 512), gamma_unit_ub=16, gamma_min=1.05, gamma_max=1.25,
+    alpha_nom=(0.02, 1e-4, 1.5e-9, 7.5e-10, 1e-7, 1e-14), beta_nom=(0.010, 1e-4, 1e-8),
+    coef_jitter=0.1, seed=0,
+)
+
+# Policy constants per workload (not drawn).
+_POLICY_DEFAULTS = dict(eta=0.5, tpot_slo=0.050, ttft_floor=2.0, lout=556.0,
+                        block_tokens=16, b_max=64, kv_cap_tokens=1_048_576, flags=0)
+
+WORKLOADS: Dict[str, dict] = {
+    "c1": dict(gen={}, policy={}),
+    "c2": dict(gen=dict(n_inst=64, n_req=16384, n_sess=1024, ps_min=512, ps_max=4096,
+                        fresh_min=1, fresh_max=64, owner_zipf=1, owner_zipf_s=1.1, cap=65536,
+                        d_min=0, d_max=256),
+               policy=dict(tpot_slo=0.030, b_max=512, kv_cap_tokens=4_194_304)),
+    "c3": dict(gen=dict(n_inst=1024, n_req=65536, n_sess=8192, ps_min=256, ps_max=8192,
+                        sp_frac=0.4, sp_blocks=128, cap=65536, p_max=32768),
+               policy=dict(tpot_slo=0.030, ttft_floor=3.0, b_max=512, kv_cap_tokens=4_194_304)),
+    "c4": dict(gen=dict(n_inst=256, n_req=32768, n_sess=512, ps_min=2048, ps_max=12500,
+                        req_zipf=1, req_zipf_s=1.4, cap=65536, d_min=0, d_max=128,
+                        sat_frac=0.85, sat_d_min=192, sat_d_max=256,
+                        sat_s_min=2_000_000, sat_s_max=3_000_000),
+               policy=dict(tpot_slo=0.050, b_max=512, kv_cap_tokens=4_194_304)),
+    "c5": dict(gen=dict(n_inst=4096, n_req=262144, n_sess=32768, ps_min=64, ps_max=4096,
+                        cap=32768),
+               policy=dict(tpot_slo=0.030, b_max=512, kv_cap_tokens=4_194_304)),
+}
+# The second c2 run at a 50 ms TPOT target.
+WORKLOADS["c2_50"] = dict(gen=WORKLOADS["c2"]["gen"],
+                          policy=dict(WORKLOADS["c2"]["policy"], tpot_slo=0.050))
+
+
+@dataclass
+class Window:
+    """One scheduling window: instance snapshot, model/policy and requests."""
+    # instances
+    n_inst: int
+    cap: int
+    blk_off: np.ndarray  # int64 [n_inst+1]
+    blk: np.ndarray      # uint64 [blk_off[-1]]
+    D: np.ndarray        # int32 decoding
+    Q: np.ndarray        # int32 queued
+    P: np.ndarray        # int64 pending uncached prefill tokens
+    S: np.ndarray        # int64 context tokens of the active requests
+    # model (fp32, interface precision) and policy
+    alpha: np.ndarray    # float32 [6]
+    seg_ub: np.ndarray   # int32 [n_seg]
+    beta: np.ndarray     # float32 [n_seg, 3]
+    gamma: np.ndarray    # float32 [n_seg]
+    policy: dict
+    # requests
+    pool: np.ndarray     # uint64
+    pre_off: np.ndarray  # int64
+    pre_len: np.ndarray  # int32
+    tail_off: np.ndarray # int64
+    tail_len: np.ndarray # int32
+    # generator metadata (ground truth of the construction)
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def n_req(self) -> int:
+        return int(self.pre_off.shape[0])
+
+    def chain(self, r: int) -> np.ndarray:
+        a = self.pool[self.pre_off[r]:self.pre_off[r] + self.pre_len[r]]
+        b = self.pool[self.tail_off[r]:self.tail_off[r] + self.tail_len[r]]
+        return np.concatenate([a, b])
+
+    def subset(self, idx) -> "Window":
+        """The same snapshot with only the requests ``idx`` (pool shared)."""
+        idx = np.asarray(idx, dtype=np.int64)
+        w = Window(**{k: getattr(self, k) for k in self.__dataclass_fields__})
+        w.pre_off = self.pre_off[idx].copy()
+        w.pre_len = self.pre_len[idx].copy()
+        w.tail_off = self.tail_off[idx].copy()
+        w.tail_len = self.tail_len[idx].copy()
+        w.meta = dict(self.meta)
+        for k in ("req_sess", "req_step"):
+            if k in w.meta:
+                w.meta[k] = self.meta[k][idx].copy()
+        return w
+
+
+def _arr(lib, h, name, dtype, n):
+    ptr = lib.psg_field(h, name.encode())
+    if n == 0:
+        return np.zeros(0, dtype=dtype)
+    out = np.empty(n, dtype=dtype)
+    ctypes.memmove(out.ctypes.data, ptr, out.nbytes)
+    return out
+
+
+def generate(workload: str = "c1", seed: int = 0, **overrides) -> Window:
+    """Draw the named window.  ``overrides`` may replace any generation or
+    policy field (e.g. ``n_req=64`` for a smaller slice of the same shape)."""
+    spec = WORKLOADS[workload]
+    gen = dict(_DEFAULTS)
+    gen.update(spec["gen"])
+    pol = dict(_POLICY_DEFAULTS)
+    pol.update(spec["policy"])
+    for k, v in overrides.items():
+        if k in gen:
+            gen[k] = v
+        elif k in pol:
+            pol[k] = v
+        else:
+            raise KeyError(f"unknown window field {k!r}")
+    gen["seed"] = seed
+    lib = _load()
+    p = _Params()
+    for k, v in gen.items():
+        if k == "seg_ub":
+            p.n_seg = len(v)
+            for i in range(32):
+                p.seg_ub[i] = v[i] if i < len(v) else 0
+        elif k in ("alpha_nom", "beta_nom"):
+            arr = getattr(p, k)
+            for i, x in enumerate(v):
+                arr[i] = x
+        else:
+            setattr(p, k, v)
+    h = ctypes.c_void_p()
+    rc = lib.psg_generate(ctypes.byref(p), ctypes.byref(h))
+    if rc != 0:
+        raise RuntimeError(f"psg_generate failed with code {rc}")
+    try:
+        sz = (ctypes.c_int64 * 5)()
+        lib.psg_sizes(h, sz)
+        n_pool, n_blk, n_sess, n_req, n_inst = (int(x) for x in sz)
+        n_seg = p.n_seg
+        win = Window(
+            n_inst=n_inst, cap=int(gen["cap"]),
+            blk_off=_arr(lib, h, "blk_off", np.int64, n_inst + 1),
+            blk=_arr(lib, h, "blk", np.uint64, n_blk),
+            D=_arr(lib, h, "D", np.int32, n_inst), Q=_arr(lib, h, "Q", np.int32, n_inst),
+            P=_arr(lib, h, "P", np.int64, n_inst), S=_arr(lib, h, "S", np.int64, n_inst),
+            alpha=_arr(lib, h, "alpha", np.float32, 6),
+            seg_ub=np.array(gen["seg_ub"], dtype=np.int32),
+            beta=_arr(lib, h, "beta", np.float32, 32 * 3).reshape(32, 3)[:n_seg].copy(),
+            gamma=_arr(lib, h, "gamma", np.float32, 32)[:n_seg].copy(),
+            policy=pol,
+            pool=_arr(lib, h, "pool", np.uint64, n_pool),
+            pre_off=_arr(lib, h, "pre_off", np.int64, n_req),
+            pre_len=_arr(lib, h, "pre_len", np.int32, n_req),
+            tail_off=_arr(lib, h, "tail_off", np.int64, n_req),
+            tail_len=_arr(lib, h, "tail_len", np.int32, n_req),
+            meta=dict(
+                workload=workload, seed=seed,
+                sess_off=_arr(lib, h, "sess_off", np.int64, n_sess),
+                sess_len=_arr(lib, h, "sess_len", np.int32, n_sess),
+                sess_base=_arr(lib, h, "sess_base", np.int32, n_sess),
+                sess_sp=_arr(lib, h, "sess_sp", np.int32, n_sess),
+                sess_owner=_arr(lib, h, "sess_owner", np.int32, n_sess),
+                sess_cached=_arr(lib, h, "sess_cached", np.int32, n_sess),
+                sess_cached_eff=_arr(lib, h, "sess_cached_eff", np.int32, n_sess),
+                inst_sp_have=_arr(lib, h, "inst_sp_have", np.int32, n_inst),
+                req_sess=_arr(lib, h, "req_sess", np.int32, n_req),
+                req_step=_arr(lib, h, "req_step", np.int32, n_req),
+                sp_blocks=int(gen["sp_blocks"]), step_blocks=int(gen["step_blocks"]),
+            ),
+        )
+    finally:
+        lib.psg_free(h)
+    return win
+
+
+def splitmix64(x: int) -> int:
+    """The SplitMix64 output function used for the chains."""
+    return int(_load().psg_splitmix64(ctypes.c_uint64(x & 0xFFFFFFFFFFFFFFFF)))

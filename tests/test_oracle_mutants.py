@@ -1,0 +1,81 @@
+"""Plant plausible mistakes in a copy of the oracle (on the CPU) and check
+that the pins catch every one of them.
+
+Each mutant is a one-token edit of ``oracle/oracle.cpp`` (a dropped term, a
+wrong sign or index, a swapped operand, a flipped comparison); it is built
+into a temporary library and the pin suite is run against it in a child
+process.  A mutant the pins do not kill would mean the oracle could carry
+that mistake unnoticed.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.cpp")
+
+MUTANTS = [
+    ("drop the N*C term", "a[2] * N * C", "0.0 * N * C"),
+    ("C term uses N", "a[4] * C", "a[4] * N"),
+    ("N^2 term uses C", "a[3] * N * N", "a[3] * C * C"),
+    ("W sign", "t_prefill(m, (double)c.n, (double)c.c) - tpf_cached", "t_prefill(m, (double)c.n, (double)c.c) + tpf_cached"),
+    ("no clamp of W", "std::max(0.0, t_prefill(m, (double)c.n, (double)c.c) - tpf_cached)", "(t_prefill(m, (double)c.n, (double)c.c) - tpf_cached)"),
+    ("Z without cached term", "const double Z = tpf_cold - tpf_cached;", "const double Z = tpf_cold;"),
+    ("rho strict", "c.inC = c.rho <= m.eta;", "c.inC = c.rho < m.eta;"),
+    ("Z<=0 ignored", "if (!kvc_on || Z <= 0.0) {", "if (!kvc_on) {"),
+    ("tpot non-strict", "c.tpot < m.tau", "c.tpot <= m.tau"),
+    ("interference always", "active > 0 ? tpf", "active >= 0 ? tpf"),
+    ("interference not amortised", "tpf / std::max(1.0, m.lout)", "tpf"),
+    ("segment exclusive", "if (B <= m.seg_ub[s]) return s;", "if (B < m.seg_ub[s]) return s;"),
+    ("gamma dropped", "m.gamma[s] * (m.beta[s][0]", "1.0 * (m.beta[s][0]"),
+    ("B+ without arrival", "const int64_t Bp = active + 1;", "const int64_t Bp = active;"),
+    ("S+ without request", "const double Sp = (double)(sn.S[i] + L);", "const double Sp = (double)(sn.S[i]);"),
+    ("TTFT queue uses Q for P", "m.alpha[1] * (double)sn.P[i]", "m.alpha[1] * (double)sn.Q[i]"),
+    ("SLO from cached prefill", "std::max(m.ttft_floor, tpf_cold)", "std::max(m.ttft_floor, tpf_cached)"),
+    ("D order", "if (Dc != Db) better = Dc > Db;", "if (Dc != Db) better = Dc < Db;"),
+    ("hit order", "better = c.hit > best->hit;", "better = c.hit < best->hit;"),
+    ("Q order", "better = Qc < Qb;", "better = Qc > Qb;"),
+    ("id order", "else better = c.i < best->i;", "else better = c.i > best->i;"),
+    ("LMetric without arrival", "(unsigned __int128)(uint64_t)(active + 1);", "(unsigned __int128)(uint64_t)(active);"),
+    ("LMetric ignores n", "(uint64_t)(sn.P[c.i] + c.n)", "(uint64_t)(sn.P[c.i])"),
+    ("capacity batch bound", "if (active + 1 <= m.b_max && sn.S[i] + L <= m.kv_cap)", "if (active + 1 < m.b_max && sn.S[i] + L <= m.kv_cap)"),
+    ("capacity ignores tokens", "if (active + 1 <= m.b_max && sn.S[i] + L <= m.kv_cap)", "if (active + 1 <= m.b_max && sn.S[i] <= m.kv_cap)"),
+    ("walk skips last block", "while (j < ch.len() && set.count(ch.at(j)) != 0) ++j;", "while (j + 1 < ch.len() && set.count(ch.at(j)) != 0) ++j;"),
+    ("walk past misses", "while (j < ch.len() && set.count(ch.at(j)) != 0) ++j;", "for (int32_t k = 0; k < ch.len(); ++k) j += set.count(ch.at(k)) != 0;"),
+    ("cached tokens per block", "c.c = c.hit * m.block_tokens;", "c.c = c.hit;"),
+    ("ttft miss non-strict", "if (best->ttft > slo) d.flags |= R_TTFT_MISS;", "if (best->ttft >= slo) d.flags |= R_TTFT_MISS;"),
+    ("commit P counts cached", "sn.P[i] += L - hitb * block_tokens;", "sn.P[i] += L;"),
+    ("commit ignores cap", "if ((int64_t)set.size() < sn.cap) set.insert(key);", "if (true) set.insert(key);"),
+]
+
+
+def _run_mutant(tmp, k, old, new):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation target not found: {old!r}"
+    mut = src.replace(old, new, 1)
+    d = os.path.join(tmp, f"m{k}")
+    os.makedirs(d)
+    cpp = os.path.join(d, "oracle.cpp")
+    so = os.path.join(d, "liboracle.so")
+    with open(cpp, "w") as f:
+        f.write(mut)
+    subprocess.run(["g++", "-O1", "-std=c++17", "-fopenmp", "-shared", "-fPIC", "-o", so, cpp],
+                   check=True, capture_output=True)
+    env = dict(os.environ, PS_ORACLE_MUTANT_LIB=so, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return r.returncode
+
+
+def test_every_planted_mistake_is_caught():
+    with tempfile.TemporaryDirectory() as tmp:
+        with ThreadPoolExecutor(max_workers=6) as ex:
+            codes = list(ex.map(lambda a: _run_mutant(tmp, *a),
+                                [(k, old, new) for k, (_, old, new) in enumerate(MUTANTS)]))
+    survivors = [MUTANTS[k][0] for k, rc in enumerate(codes) if rc == 0]
+    assert not survivors, f"pins missed planted mistakes: {survivors}"

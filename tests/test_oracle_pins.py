@@ -1,0 +1,492 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Nothing here compares the oracle with itself or with a retyped copy of its
+formulas: the expected values are hand-computed (tests/golden), closed forms
+and special cases the paper states, brute force at the token level, and
+invariants of Algorithm 1.
+"""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.tinywin import chain_hashes, make_window
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")
+FLAGS = dict(TTFT_ADMIT=oracle.F_TTFT_ADMIT, NO_KVC_FILTER=oracle.F_NO_KVC_FILTER,
+             NO_TPOT_FILTER=oracle.F_NO_TPOT_FILTER)
+RFLAGS = dict(REJECT=oracle.R_REJECT, FALLBACK=oracle.R_FALLBACK, TTFT_MISS=oracle.R_TTFT_MISS)
+
+
+def _flagbits(v, table):
+    if isinstance(v, list):
+        out = 0
+        for name in v:
+            out |= table[name]
+        return out
+    return int(v)
+
+
+def _worked_window(g, b_max, eta, tau, flags):
+    L = g["chain_blocks"]
+    ch = chain_hashes(L)
+    sets = []
+    for inst in g["instances"]:
+        h = inst["hit"]
+        # instance 4 (hit 0) holds every block but the first one
+        sets.append(ch[:h] if h > 0 else ch[1:])
+    inst = g["instances"]
+    return make_window(
+        sets, [ch], D=[x["D"] for x in inst], Q=[x["Q"] for x in inst],
+        P=[x["P"] for x in inst], S=[x["S"] for x in inst], alpha=g["alpha"],
+        seg_ub=g["seg_ub"], beta=g["beta"], gamma=g["gamma"], eta=eta, tpot_slo=tau,
+        ttft_floor=g["ttft_floor"], lout=g["lout"], block_tokens=g["block_tokens"],
+        b_max=b_max, kv_cap_tokens=g["kv_cap"], flags=flags, cap=16)
+
+
+def _decide(win, **policy):
+    o = oracle.Oracle.from_window(win)
+    try:
+        return o.window_score(win, nthreads=1, **policy)
+    finally:
+        o.close()
+
+
+@pytest.fixture(scope="module")
+def gold():
+    with open(GOLD) as f:
+        return json.load(f)
+
+
+# -- hand-worked example (Algorithm 1, Eqs. 7-10) ---------------------------
+
+def test_worked_example_cases(gold):
+    for case in gold["cases"]:
+        fl = _flagbits(case["flags"], FLAGS)
+        win = _worked_window(gold, case["b_max"], case["eta"], case["tau"], fl)
+        d = _decide(win)
+        assert d.inst[0] == case["inst"], case["name"]
+        assert d.hit[0] == case["hit"], case["name"]
+        assert d.flags[0] == _flagbits(case["rflags"], RFLAGS), case["name"]
+        if case["inst"] >= 0:
+            assert d.ttft[0] == pytest.approx(case["ttft"], rel=1e-6), case["name"]
+            assert d.tpot[0] == pytest.approx(case["tpot"], rel=1e-6), case["name"]
+        if case["sizes"] is not None:
+            assert list(d.sizes[0]) == case["sizes"], case["name"]
+        if case.get("near_boundary"):
+            assert d.nb[0] & oracle.NB_RHO, case["name"]
+        else:
+            assert d.nb[0] & oracle.NB_DECISION == 0, case["name"]
+
+
+def test_worked_example_per_instance_latencies(gold):
+    """Each instance alone, filters off: the decision exposes its TTFT/TPOT."""
+    per = gold["derived"]["per_instance"]
+    for i, inst in enumerate(gold["instances"]):
+        g1 = dict(gold)
+        g1["instances"] = [inst]
+        win = _worked_window(g1, 1000, 0.5, 1.0, oracle.F_NO_KVC_FILTER | oracle.F_NO_TPOT_FILTER)
+        d = _decide(win)
+        assert d.inst[0] == 0 and d.hit[0] == inst["hit"]
+        assert d.tpot[0] == pytest.approx(per[i]["tpot"], rel=1e-9)
+        assert d.ttft[0] == pytest.approx(per[i]["ttft"], rel=1e-9)
+
+
+# -- special cases the paper states -----------------------------------------
+
+SIMPLE_ALPHA = [0.02, 1e-3, 1e-6, 1e-6, 1e-5, 2e-9]
+
+
+def _one_inst(hit, L=8, D=0, Q=0, P=0, S=0, alpha=SIMPLE_ALPHA, seg_ub=(64,),
+              beta=((0.01, 1e-4, 1e-8),), gamma=(1.0,), **pol):
+    ch = chain_hashes(L)
+    pol.setdefault("tpot_slo", 10.0)
+    pol.setdefault("b_max", 10_000)
+    pol.setdefault("kv_cap_tokens", 10**9)
+    return make_window([ch[:hit]], [ch], [D], [Q], [P], [S], alpha, seg_ub, beta, gamma,
+                       cap=max(hit, 1), **pol)
+
+
+def test_interference_term_dropped_when_idle():
+    """Eq. 10: the prefill-interference term is omitted when A_i = 0."""
+    a, b = SIMPLE_ALPHA, (0.01, 1e-4, 1e-8)
+    L, hit, S = 8 * 16, 3, 5000
+    n, c = L - hit * 16, hit * 16
+    tpf = a[0] + a[1] * n + a[2] * n * c + a[3] * n * n + a[4] * c + a[5] * c * c
+    idle = _decide(_one_inst(hit, S=S))
+    assert idle.tpot[0] == pytest.approx(b[0] + b[1] * 1 + b[2] * (S + L), rel=1e-12)
+    busy = _decide(_one_inst(hit, D=1, S=S))
+    assert busy.tpot[0] == pytest.approx(b[0] + b[1] * 2 + b[2] * (S + L) + tpf / 556.0, rel=1e-12)
+
+
+def test_fully_cached_prefill_cost():
+    """n = 0: T_pf(0, L) = a0 + a4 L + a5 L^2; TTFT adds a0 Q + a1 P."""
+    a = SIMPLE_ALPHA
+    L = 8 * 16
+    d = _decide(_one_inst(8, Q=2, P=300, D=1))
+    assert d.hit[0] == 8
+    tpf = a[0] + a[4] * L + a[5] * L * L
+    assert d.ttft[0] == pytest.approx(tpf + a[0] * 2 + a[1] * 300, rel=1e-12)
+
+
+def test_single_segment_reduces_to_eq8():
+    """One segment with gamma = 1: the decode term is Eq. 8 itself, and the
+    EMA factor scales only that term (Sec. 5.3)."""
+    beta = (0.004, 3e-4, 2e-8)
+    d1 = _decide(_one_inst(2, D=0, Q=0, S=1234, seg_ub=(8,), beta=(beta,), gamma=(1.0,)))
+    L = 128
+    assert d1.tpot[0] == pytest.approx(beta[0] + beta[1] * 1 + beta[2] * (1234 + L), rel=1e-12)
+    d2 = _decide(_one_inst(2, D=0, Q=0, S=1234, seg_ub=(8,), beta=(beta,), gamma=(1.5,)))
+    assert d2.tpot[0] == pytest.approx(1.5 * d1.tpot[0], rel=1e-12)
+
+
+def test_segment_bounds_inclusive_and_last_segment():
+    """B+ equal to a bound uses that segment; past the last bound, the last."""
+    beta = ((1.0, 0, 0), (2.0, 0, 0), (3.0, 0, 0))
+    ub = (4, 8, 16)
+    for active, want in [(3, 1.0), (4, 2.0), (7, 2.0), (8, 3.0), (15, 3.0), (40, 3.0)]:
+        d = _decide(_one_inst(0, D=active, Q=0, alpha=[0] * 6, seg_ub=ub, beta=beta,
+                              gamma=(1, 1, 1), tpot_slo=100.0))
+        assert d.tpot[0] == pytest.approx(want), active
+
+
+def _multi(hits, L=8, D=None, Q=None, P=None, S=None, alpha=SIMPLE_ALPHA, **pol):
+    ch = chain_hashes(L)
+    n = len(hits)
+    D = D if D is not None else [0] * n
+    Q = Q if Q is not None else [0] * n
+    P = P if P is not None else [0] * n
+    S = S if S is not None else [0] * n
+    pol.setdefault("tpot_slo", 10.0)
+    pol.setdefault("b_max", 10_000)
+    pol.setdefault("kv_cap_tokens", 10**9)
+    sets = [ch[:h] for h in hits]
+    return make_window(sets, [ch], D, Q, P, S, alpha, (10_000,), ((0.001, 0, 0),), (1.0,),
+                       cap=L, **pol)
+
+
+def test_zero_cache_benefit_keeps_all():
+    """Sec. 6.1: if Z_r = 0 all capacity-eligible candidates remain (here
+    T_pf = a0 + a2 N C, so T_pf(L,0) = T_pf(0,L)), even with eta = 0."""
+    alpha = [0.02, 0, 1e-6, 0, 0, 0]
+    d = _decide(_multi([0, 3, 5, 8], alpha=alpha, eta=0.0))
+    assert list(d.sizes[0]) == [4, 4, 4]
+    assert d.nb[0] & oracle.NB_Z
+
+
+def test_eta_zero_keeps_minimum_cost_only():
+    """Sec. 6.1: eta = 0 retains only minimum-cost candidates."""
+    d = _decide(_multi([2, 6, 6, 5, 0], eta=0.0))
+    assert list(d.sizes[0][:2]) == [5, 2]
+    assert d.hit[0] == 6 and d.inst[0] == 1
+
+
+def test_recompute_cost_clamp_binds():
+    """W is the nonnegative penalty (Sec. 6.1).  With T_pf = N^2/32 + C
+    (alpha3 = 1/32, alpha4 = 1) and L = 128: T_pf(n, L-n) - T_pf(0, L) =
+    n (n/32 - 1), so hits 8, 7, 4, 0 give raw penalties 0, -8, 64, 384 and
+    W = 0, 0, 64, 384; Z = 384, rho = 0, 0, 1/6, 1.  With eta = 0.17 the
+    instance with hit 4 is admissible and, being the only one decoding,
+    wins; without the clamp its rho would be 72/384 > 0.17."""
+    alpha = [0, 0, 0, 1.0 / 32, 1.0, 0]
+    d = _decide(_multi([8, 7, 4, 0], alpha=alpha, eta=0.17, D=[0, 0, 5, 0]))
+    assert list(d.sizes[0][:2]) == [4, 3]
+    assert d.inst[0] == 2 and d.hit[0] == 4
+
+
+def test_rho_boundary_is_inclusive():
+    """Alg. 1 keeps rho <= eta.  With T_pf = N, rho = (n_i - n_min) / L is
+    exact in binary: hits 8 and 4 of 8 blocks give rho = 0.5."""
+    alpha = [0, 1.0, 0, 0, 0, 0]
+    d = _decide(_multi([8, 4], alpha=alpha, eta=0.5, D=[0, 5]))
+    assert list(d.sizes[0][:2]) == [2, 2] and d.inst[0] == 1
+    d = _decide(_multi([8, 4], alpha=alpha, eta=0.49, D=[0, 5]))
+    assert list(d.sizes[0][:2]) == [2, 1] and d.inst[0] == 0
+
+
+def test_tpot_boundary_is_strict():
+    """Alg. 1 keeps predicted TPOT < tau (strict): a TPOT equal to tau fails."""
+    w = _one_inst(0, alpha=[0] * 6, beta=((0.5, 0, 0),), tpot_slo=0.5)
+    d = _decide(w)
+    assert d.flags[0] & oracle.R_FALLBACK and d.sizes[0][2] == 0
+    d = _decide(w, tpot_slo=0.5000001)
+    assert not d.flags[0] & oracle.R_FALLBACK and d.sizes[0][2] == 1
+
+
+def test_ttft_admission_boundary_is_inclusive():
+    """With TTFT admission on, TTFT <= budget passes (budget = max(floor,
+    T_pf(L,0)), Sec. 8.1).  T_pf = 1 + N makes TTFT = 1 + n exactly."""
+    alpha = [1.0, 1.0, 0, 0, 0, 0]
+    # L = 16 tokens, hit 0: TTFT = 17 = T_pf(L,0) = budget -> admitted
+    w = _one_inst(0, L=1, alpha=alpha, beta=((0.001, 0, 0),), flags=oracle.F_TTFT_ADMIT,
+                  ttft_floor=2.0)
+    d = _decide(w)
+    assert d.sizes[0][2] == 1 and d.ttft[0] == 17.0 and not d.flags[0] & oracle.R_TTFT_MISS
+    # one queued request adds a0 = 1 second of queueing: 18 > 17 -> fallback
+    w = _one_inst(0, L=1, Q=1, alpha=alpha, beta=((0.001, 0, 0),), flags=oracle.F_TTFT_ADMIT)
+    d = _decide(w)
+    assert d.sizes[0][2] == 0 and d.flags[0] & oracle.R_FALLBACK and d.flags[0] & oracle.R_TTFT_MISS
+
+
+def test_capacity_bounds_inclusive():
+    """A_i + 1 <= B_max and S_i + L_r <= M_KV (reading of CapacityCandidates
+    from the batch bound of Sec. 3)."""
+    L = 128
+    d = _decide(_multi([0, 0, 0, 0], D=[6, 7, 0, 0], Q=[1, 1, 0, 0], S=[0, 0, 1000 - L, 1001 - L],
+                       b_max=8, kv_cap_tokens=1000))
+    # instance 0: A+1 = 8 ok; 1: 9 > 8; 2: S+L = 1000 ok; 3: 1001 > 1000
+    assert d.sizes[0][0] == 2
+    d = _decide(_multi([0, 0], D=[8, 9], b_max=8))
+    assert d.inst[0] == -1 and d.flags[0] == oracle.R_REJECT and d.hit[0] == 0
+
+
+def test_packing_key_order():
+    """Table 4's D-C-Q: most decoding first, then most cached, then fewest
+    queued, then lowest id; all candidates feasible here."""
+    big = dict(eta=1.0)
+    # D dominates the hit
+    assert _decide(_multi([8, 1], D=[1, 2], **big)).inst[0] == 1
+    # equal D: hit decides
+    assert _decide(_multi([5, 7], D=[2, 2], **big)).inst[0] == 1
+    # equal D and hit: fewer queued
+    assert _decide(_multi([5, 5], D=[2, 2], Q=[3, 1], **big)).inst[0] == 1
+    # full tie: lowest id
+    assert _decide(_multi([5, 5, 5], D=[2, 2, 2], Q=[1, 1, 1], **big)).inst[0] == 0
+
+
+def test_fallback_lmetric_product():
+    """Fallback = min (P_i + n_i)(A_i + 1) over C (LMetric, Sec. 8.1);
+    L = 128 tokens.  Products: (100+128)*1 = 228, (0+64)*4 = 256,
+    (200+0)*1 = 200 -> instance 2."""
+    d = _decide(_multi([0, 4, 8], D=[0, 2, 0], Q=[0, 1, 0], P=[100, 0, 200], eta=1.0,
+                       tpot_slo=1e-9))
+    assert d.flags[0] & oracle.R_FALLBACK and d.inst[0] == 2
+    # tie on the product -> lowest id: (64+64)*1 = 128 and (0+64)*2 = 128
+    d = _decide(_multi([4, 4], D=[0, 1], P=[64, 0], eta=1.0, tpot_slo=1e-9))
+    assert d.inst[0] == 0
+
+
+def test_walk_stops_at_first_miss():
+    """Longest cached prefix: a set holding every block but the second gives
+    hit 1, not 7 (non-prefix-closed set)."""
+    ch = chain_hashes(8)
+    w = make_window([[ch[0]] + ch[2:]], [ch], [0], [0], [0], [0], SIMPLE_ALPHA, (64,),
+                    ((0.01, 0, 0),), (1.0,), cap=8, tpot_slo=10.0)
+    assert _decide(w).hit[0] == 1
+    o = oracle.Oracle.from_window(w)
+    assert o.window_hits(w)[0, 0] == 1
+
+
+# -- brute force at the token level -----------------------------------------
+
+def _block_hashes(tokens, bs=16):
+    h = b"\0" * 8
+    out = []
+    for j in range(len(tokens) // bs):
+        m = hashlib.blake2b(h + np.asarray(tokens[j * bs:(j + 1) * bs], np.int64).tobytes(),
+                            digest_size=8)
+        h = m.digest()
+        v = int.from_bytes(h, "little") or 1
+        out.append(v)
+    return out
+
+
+def test_hits_match_token_level_lcp():
+    """hit = floor(max over cached sequences of LCP(request tokens, seq) / 16),
+    with near-miss blocks that share 15 of 16 tokens."""
+    rng = np.random.default_rng(7)
+    bs = 16
+    for trial in range(6):
+        base = [list(rng.integers(0, 50, size=bs * rng.integers(2, 10))) for _ in range(5)]
+        cached = []   # per instance: list of token sequences
+        for i in range(4):
+            seqs = []
+            for _ in range(rng.integers(1, 4)):
+                b = base[rng.integers(0, len(base))]
+                cut = int(rng.integers(0, len(b) // bs + 1)) * bs
+                s = list(b[:cut])
+                if cut and rng.random() < 0.5:
+                    # near miss: change one token of the last block
+                    s[cut - 1 - int(rng.integers(0, bs))] += 1000
+                seqs.append(s)
+            cached.append(seqs)
+        reqs = []
+        for _ in range(8):
+            b = base[rng.integers(0, len(base))]
+            k = int(rng.integers(1, len(b) // bs + 1)) * bs
+            r = list(b[:k]) + list(rng.integers(100, 200, size=bs * int(rng.integers(0, 3))))
+            reqs.append(r)
+        sets = [sorted({h for s in seqs for h in _block_hashes(s)}) for seqs in cached]
+        chains = [_block_hashes(r) for r in reqs]
+        w = make_window(sets, chains, [0] * 4, [0] * 4, [0] * 4, [0] * 4, SIMPLE_ALPHA, (64,),
+                        ((0.01, 0, 0),), (1.0,), cap=max(len(s) for s in sets) + 1)
+        o = oracle.Oracle.from_window(w)
+        got = o.window_hits(w)
+        for r, toks in enumerate(reqs):
+            for i, seqs in enumerate(cached):
+                best = 0
+                for s in seqs:
+                    lcp = 0
+                    while lcp < min(len(s), len(toks)) and s[lcp] == toks[lcp]:
+                        lcp += 1
+                    best = max(best, lcp // bs)
+                assert got[r, i] == best, (trial, r, i)
+
+
+# -- generator construction (closed form of the owner hit) -------------------
+
+@pytest.mark.parametrize("name,n_req", [("c1", 1024), ("c2", 2048), ("c3", 256)])
+def test_hits_match_generator_construction(name, n_req):
+    """Owner hit = min(P_s + 8k, cached prefix of the session), widened by a
+    shared system prompt held on the instance; every other instance hits only
+    the system prompt (or nothing)."""
+    gen = {"c3": dict(n_inst=64, n_sess=512)}.get(name, {})
+    w = synth.generate(name, n_req=n_req, **gen)
+    o = oracle.Oracle.from_window(w)
+    hits = o.window_hits(w)
+    m = w.meta
+    for r in range(w.n_req):
+        s = m["req_sess"][r]
+        pre = w.pre_len[r]
+        sp = m["sess_sp"][s]
+        for i in range(w.n_inst):
+            have = m["inst_sp_have"][i] if sp else 0
+            own = m["sess_cached_eff"][s] if i == m["sess_owner"][s] else 0
+            assert hits[r, i] == min(pre, max(own, have)), (r, i)
+
+
+def test_hit_invariants_c2():
+    """hit <= chain length; monotone along a session's steps."""
+    w = synth.generate("c2", n_req=4096)
+    o = oracle.Oracle.from_window(w)
+    hits = o.window_hits(w)
+    ell = (w.pre_len + w.tail_len).astype(np.int64)
+    assert (hits <= ell[:, None]).all()
+    sess, step = w.meta["req_sess"], w.meta["req_step"]
+    order = np.lexsort((step, sess))
+    hs, ss = hits[order], sess[order]
+    same = ss[1:] == ss[:-1]
+    assert (hs[1:][same] >= hs[:-1][same]).all()
+
+
+# -- invariants of Algorithm 1 on generated windows --------------------------
+
+def _check_decisions(w, d, hits):
+    D, Q, P = w.D.astype(np.int64), w.Q.astype(np.int64), w.P
+    nA, nC, nT = d.sizes[:, 0], d.sizes[:, 1], d.sizes[:, 2]
+    assert (nT <= nC).all() and (nC <= nA).all()
+    rej = d.inst < 0
+    assert ((nA == 0) == rej).all()
+    assert (d.flags[rej] == oracle.R_REJECT).all() and (d.hit[rej] == 0).all()
+    fb = (d.flags & oracle.R_FALLBACK) != 0
+    assert ((nT == 0) & ~rej == fb).all()
+    ok = ~rej
+    assert (d.hit[ok] == hits[ok, d.inst[ok]]).all()
+
+
+def test_decision_invariants_and_monotonicity():
+    w = synth.generate("c2", n_req=2048)
+    o = oracle.Oracle.from_window(w)
+    hits = o.window_hits(w).astype(np.int64)
+    prev = None
+    for eta in (0.0, 0.25, 0.5, 1.0):
+        d = o.window_score(w, eta=eta)
+        _check_decisions(w, d, hits)
+        if prev is not None:
+            assert (d.sizes[:, 1] >= prev.sizes[:, 1]).all()
+        prev = d
+    prev = None
+    for tau in (0.01, 0.03, 0.05, 0.2):
+        d = o.window_score(w, tpot_slo=tau)
+        _check_decisions(w, d, hits)
+        if prev is not None:
+            assert (d.sizes[:, 2] >= prev.sizes[:, 2]).all()
+            assert (d.sizes[:, 1] == prev.sizes[:, 1]).all()
+        prev = d
+    # the packing choice is in T and beats every other member of T on the
+    # D-C-Q key; a fallback choice is in C
+    d = o.window_score(w)
+    m = oracle.model_of(w)
+    eta = float(np.float32(w.policy["eta"]))
+    tau = float(np.float32(w.policy["tpot_slo"]))
+    for r in range(0, w.n_req, 17):
+        ex = o.explain(m, w.chain(r))
+        i = d.inst[r]
+        assert ex["choice"] == i
+        if i < 0:
+            assert ex["elig"].sum() == 0
+            continue
+        T = np.nonzero(ex["inT"])[0]
+        C = np.nonzero(ex["inC"])[0]
+        assert set(T) <= set(C) <= set(np.nonzero(ex["elig"])[0])
+        if not d.flags[r] & oracle.R_FALLBACK:
+            assert i in T
+            for j in T:
+                assert (-int(w.D[i]), -int(ex["hit"][i]), int(w.Q[i]), i) <= \
+                       (-int(w.D[j]), -int(ex["hit"][j]), int(w.Q[j]), j)
+        else:
+            assert len(T) == 0 and i in C
+        # C is exactly {rho <= eta}; T exactly {TPOT < tau} within C
+        el = ex["elig"] == 1
+        assert (ex["inC"][el] == (ex["rho"][el] <= eta)).all()
+        assert (ex["inT"][el] == (ex["inC"][el] & (ex["tpot"][el] < tau))).all()
+
+
+def test_relabelling_equivariance():
+    """Permuting instance ids permutes decisions, except where the lowest-id
+    tie-break is what decided (then the keys of both choices are equal)."""
+    w = synth.generate("c1")
+    o = oracle.Oracle.from_window(w)
+    d = o.window_score(w)
+    perm = np.random.default_rng(3).permutation(w.n_inst)   # new id of old i = perm[i]
+    inv = np.argsort(perm)
+    w2 = synth.generate("c1")
+    rows = [w.blk[w.blk_off[i]:w.blk_off[i + 1]] for i in inv]
+    w2.blk_off = np.concatenate([[0], np.cumsum([len(x) for x in rows])]).astype(np.int64)
+    w2.blk = np.concatenate(rows).astype(np.uint64)
+    for k in ("D", "Q", "P", "S"):
+        setattr(w2, k, getattr(w, k)[inv].copy())
+    o2 = oracle.Oracle.from_window(w2)
+    d2 = o2.window_score(w2)
+    hits = o.window_hits(w)
+    for r in range(w.n_req):
+        a, b = d.inst[r], d2.inst[r]
+        if a < 0:
+            assert b < 0
+            continue
+        if perm[a] == b:
+            continue
+        b_old = inv[b]
+        if d.flags[r] & oracle.R_FALLBACK:
+            L = int(w.pre_len[r] + w.tail_len[r]) * 16
+            pa = (int(w.P[a]) + L - 16 * int(hits[r, a])) * (int(w.D[a]) + int(w.Q[a]) + 1)
+            pb = (int(w.P[b_old]) + L - 16 * int(hits[r, b_old])) * (int(w.D[b_old]) + int(w.Q[b_old]) + 1)
+            assert pa == pb
+        else:
+            assert (w.D[a], hits[r, a], w.Q[a]) == (w.D[b_old], hits[r, b_old], w.Q[b_old])
+
+
+# -- commit (sequential state update) ----------------------------------------
+
+def test_commit_hand_trace():
+    ch = chain_hashes(6)
+    other = chain_hashes(3, base=50_000)
+    # instance 0 holds the first 2 blocks; instance 1 holds nothing; cap 5
+    w = make_window([ch[:2], []], [ch, ch, other], [1, 0], [0, 2], [10, 20], [100, 200],
+                    SIMPLE_ALPHA, (64,), ((0.01, 0, 0),), (1.0,), cap=5)
+    o = oracle.Oracle.from_window(w)
+    dropped = o.commit(w.pool, w.pre_off, w.pre_len, w.tail_off, w.tail_len, [0, -1, 0])
+    st = o.state()
+    # entry 0: L = 96, hit 2 -> n = 64 tokens; blocks 3..5 enter (set size 5 =
+    # cap) and block 6 is refused; entry 1: skipped; entry 2: L = 48, hit 0 ->
+    # n = 48, all 3 blocks refused
+    assert list(st["Q"]) == [2, 2]
+    assert list(st["P"]) == [10 + 64 + 48, 20]
+    assert list(st["S"]) == [100 + 96 + 48, 200]
+    assert list(st["set_size"]) == [5, 0] and dropped == 1 + 3
+    h = o.window_hits(w)
+    assert list(h[:, 0]) == [5, 5, 0]
