@@ -1,0 +1,222 @@
+/*
+ * packserve.h -- C ABI of the MI355X (gfx950) window scorer for PackServe's
+ * KVC-first, SLO-aware request packing (Algorithm 1 of the paper).
+ *
+ * One call scores a whole scheduling window: for every request of the window
+ * and every serving instance it finds the longest cached block prefix, runs
+ * the white-box latency model (prefill Eq. 7 with the empirical C and C^2
+ * terms of Sec. 5.3, decode Eq. 8 per batch-size segment with its EMA factor,
+ * the TPOT estimate of Eq. 10, the TTFT decomposition of Eq. 4), applies the
+ * capacity guard, the normalised recomputation filter of Eq. 9 and the TPOT
+ * filter, and picks the instance with the decode-batch-size-centric key
+ * (Sec. 6.2, D-C-Q of Table 4) or, when no instance meets the TPOT target,
+ * the cache-aware load-balancing fallback (the LMetric product, Sec. 7 and
+ * Sec. 8.1).  Every request of a window is scored against the same instance
+ * snapshot; ps_commit then applies the chosen placements in order.
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: PS_OK (0) or a negative PS_E_* code.  Nothing is thrown
+ *     or aborted across the ABI; ps_last_error() gives the message.  On an
+ *     error the outputs are unspecified and the context state is unchanged.
+ *   - Host pointers are owned by the caller; the library copies what it
+ *     needs before returning and keeps no pointer to them.
+ *   - "_dev" entry points take device pointers owned by the caller, enqueue
+ *     work on the given HIP stream (NULL = the default stream) and return
+ *     without waiting; the caller synchronises.  They use the context's
+ *     tables and scratch, so two calls on one context must not overlap.
+ *   - A context is not thread-safe; separate contexts are independent.
+ *   - Block hashes are nonzero 64-bit values (0 is the empty-slot sentinel).
+ *     A request's chain is pool[pre_off, pre_off + pre_len) followed by
+ *     pool[tail_off, tail_off + tail_len): chained hashes, so one hash names
+ *     a whole prefix, as a node of a prefix tree does.
+ */
+#ifndef PACKSERVE_H
+#define PACKSERVE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define PS_OK 0
+#define PS_E_INVAL (-1)  /* bad argument: null pointer, zero hash, malformed CSR/model */
+#define PS_E_NOMEM (-2)  /* device or host allocation failed */
+#define PS_E_DEVICE (-3) /* a HIP call failed */
+#define PS_E_STATE (-4)  /* call order: scoring or commit before ps_load_instances */
+#define PS_E_RANGE (-5)  /* a value is outside the limits below */
+
+/* limits (validated) */
+#define PS_MAX_SEG 32          /* decode batch-size segments */
+#define PS_MAX_INST 65536      /* instances: ids fit the 16-bit key field */
+#define PS_MAX_DQ 4095         /* decoding / queued requests per instance */
+#define PS_MAX_CHAIN 16777215  /* blocks per request chain (2^24 - 1) */
+#define PS_MAX_PENDING 17179869184LL  /* pending prefill tokens per instance (2^34) */
+#define PS_MAX_CONTEXT 70368744177664LL /* context tokens per instance (2^46) */
+#define PS_MAX_BLOCK_TOKENS 1024
+#define PS_MAX_BATCH 8191      /* B_max */
+#define PS_MAX_TABLE_CAP 67108864 /* distinct cached blocks per instance (2^26) */
+
+/* ps_model.flags */
+#define PS_F_TTFT_ADMIT 1u     /* also require predicted TTFT <= the TTFT budget for T */
+#define PS_F_NO_KVC_FILTER 2u  /* skip the recomputation filter: C = A */
+#define PS_F_NO_TPOT_FILTER 4u /* skip the TPOT test: T = C (minus TTFT admission if on) */
+
+/* ps_result.flags */
+#define PS_R_REJECT 1u    /* no capacity-eligible instance (Algorithm 1 returns Reject) */
+#define PS_R_FALLBACK 2u  /* T was empty: chosen by the load-balancing fallback over C */
+#define PS_R_TTFT_MISS 4u /* predicted TTFT of the choice exceeds the TTFT budget */
+#define PS_R_INVALID 8u   /* (_dev only) malformed request descriptor; instance -1 */
+
+typedef struct ps_ctx ps_ctx; /* opaque: device tables, instance state, stream */
+typedef int32_t ps_status;
+
+/*
+ * Pool-wide latency profile and policy; copied at load.
+ *  alpha: prefill model T_pf(N, C) = a0 + a1 N + a2 N C + a3 N^2 + a4 C + a5 C^2,
+ *         seconds, N new and C cached tokens (Eq. 7 plus the C, C^2 terms of
+ *         Sec. 5.3).
+ *  seg_ub[0..n_seg): inclusive upper batch size of each decode segment,
+ *         strictly ascending (CUDA-graph capture sizes in the paper, Sec. 5.3);
+ *         a projected batch above the last bound uses the last segment.
+ *  beta[s], gamma[s]: decode iteration T_iter(B, S) = gamma_s (b0 + b1 B + b2 S)
+ *         (Eq. 8 per segment; gamma_s is the EMA factor of Sec. 5.3, > 0).
+ *  eta: recomputation budget (>= 0, Eq. 9); tpot_slo: TPOT target tau (s,
+ *         strict test); ttft_floor: minimum TTFT budget (s; the budget is
+ *         max(floor, T_pf(L, 0)), Sec. 8.1); lout: recent median output length
+ *         (tokens; the interference term divides by max(1, lout), Eq. 10).
+ *  block_tokens: tokens per block; b_max: engine batch limit; kv_cap_tokens:
+ *         KV capacity in tokens (capacity guard: A_i + 1 <= b_max and
+ *         S_i + L <= kv_cap_tokens).
+ *  flags: PS_F_*.
+ */
+typedef struct {
+  float alpha[6];
+  int32_t n_seg;
+  int32_t seg_ub[PS_MAX_SEG];
+  float beta[PS_MAX_SEG][3];
+  float gamma[PS_MAX_SEG];
+  float eta, tpot_slo, ttft_floor, lout;
+  int32_t block_tokens, b_max;
+  int64_t kv_cap_tokens;
+  uint32_t flags;
+} ps_model;
+
+/*
+ * Instance snapshot (host memory).  Instance i caches the block hashes
+ * blk[blk_off[i], blk_off[i+1]) (set semantics: duplicates allowed, order
+ * irrelevant; at most table_cap_blocks per row; blk_off[0] = 0, ascending).
+ * decoding = D_i, queued = Q_i (both in [0, PS_MAX_DQ]; A_i = D_i + Q_i),
+ * pending_tok = P_i (pending uncached prefill tokens), ctx_tok = S_i (context
+ * tokens of the A_i active requests).  table_cap_blocks also bounds later
+ * inserts by ps_commit.
+ */
+typedef struct {
+  int32_t n_inst, table_cap_blocks;
+  const int64_t* blk_off;
+  const uint64_t* blk;
+  const int32_t* decoding;
+  const int32_t* queued;
+  const int64_t* pending_tok;
+  const int64_t* ctx_tok;
+} ps_instances;
+
+/* One request: chain = pool[pre_off..+pre_len) ++ pool[tail_off..+tail_len). */
+typedef struct {
+  int64_t pre_off;
+  int64_t tail_off;
+  int32_t pre_len;
+  int32_t tail_len;
+} ps_req;
+
+/* One decision (20 bytes).  instance -1 = Reject (hit 0, ttft = tpot = 0). */
+typedef struct {
+  int32_t instance;
+  int32_t hit_blocks;
+  float ttft;
+  float tpot;
+  uint32_t flags;
+} ps_result;
+
+/* Create a context on HIP device `device` (owns a default-priority stream). */
+ps_status ps_create(int device, ps_ctx** out);
+
+/* Free every device buffer and the stream.  NULL is accepted. */
+ps_status ps_destroy(ps_ctx* ctx);
+
+/*
+ * Replace the snapshot: build one open-addressing table per instance from the
+ * CSR block lists (buckets of 8 x 64-bit slots, at least 2 * table_cap_blocks
+ * slots, a per-instance salted bucket index) and upload the load counters
+ * and the model.  Synchronous.  PS_E_INVAL on a null pointer, a zero hash, a
+ * malformed CSR or model; PS_E_RANGE when a limit above is exceeded.
+ */
+ps_status ps_load_instances(ps_ctx* ctx, const ps_instances* inst, const ps_model* model);
+
+/*
+ * Score a window held in host memory: copies pool[0, pool_len) and reqs to
+ * the device, runs ps_score_window_dev on the context stream and copies the
+ * n_req results back.  Synchronous.  Descriptors must lie inside the pool,
+ * chains must be at most PS_MAX_CHAIN blocks and the pool free of zero
+ * hashes (PS_E_RANGE / PS_E_INVAL otherwise).  n_req = 0 is a no-op.
+ */
+ps_status ps_score_window(ps_ctx* ctx, const uint64_t* pool, int64_t pool_len,
+                          const ps_req* reqs, int32_t n_req, ps_result* out);
+
+/*
+ * Score a device-resident window into d_out[n_req] (and, if d_sizes is not
+ * NULL, |A|, |C|, |T| per request into d_sizes[3 * n_req]), asynchronously
+ * on `hip_stream`.  Descriptors are checked by the kernel: a malformed one
+ * yields instance -1 with PS_R_INVALID.  A zero hash in a chain never
+ * matches (it ends the prefix walk).
+ */
+ps_status ps_score_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_len,
+                              const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                              uint32_t* d_sizes, void* hip_stream);
+
+/*
+ * Diagnostic: the longest cached prefix (blocks) of every request on every
+ * instance, ignoring capacity, into d_hits[r * n_inst + i], asynchronously on
+ * `hip_stream`.  Same prefix walk as the scorer.  Malformed descriptors give
+ * 0xFFFFFFFF rows.
+ */
+ps_status ps_probe_hits_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_len,
+                            const ps_req* d_reqs, int32_t n_req, uint32_t* d_hits,
+                            void* hip_stream);
+
+/*
+ * Apply placements (host memory) in array order: entry k places request
+ * reqs[k] on instance inst[k] (-1 = skip).  For each placed request, against
+ * the table as left by the earlier entries: Q_i += 1, P_i += uncached tokens
+ * (L - block_tokens * hit), S_i += L, and the chain's blocks enter
+ * the table in chain order until table_cap_blocks distinct blocks are held;
+ * refused blocks are counted in *n_dropped.  No eviction.  Synchronous.
+ * PS_E_RANGE if a counter would leave its limit.
+ */
+ps_status ps_commit(ps_ctx* ctx, const uint64_t* pool, int64_t pool_len, const ps_req* reqs,
+                    const int32_t* inst, int32_t n, int64_t* n_dropped);
+
+/*
+ * Copy the current load counters and per-instance distinct cached-block
+ * counts to host arrays of n_inst entries (any pointer may be NULL).
+ */
+ps_status ps_read_state(ps_ctx* ctx, int32_t* decoding, int32_t* queued, int64_t* pending_tok,
+                        int64_t* ctx_tok, int64_t* cached_blocks);
+
+/*
+ * Layout facts for measurement: slots per instance table, total table bytes,
+ * and whether per-candidate prefix hits stay in LDS (1) or in device scratch
+ * (0) for the loaded instance count.  Any pointer may be NULL.
+ */
+ps_status ps_table_info(ps_ctx* ctx, int64_t* slots_per_table, int64_t* table_bytes,
+                        int32_t* hits_in_lds);
+
+/* Message of the last failed call on ctx (or of ps_create when ctx is NULL). */
+const char* ps_last_error(const ps_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PACKSERVE_H */

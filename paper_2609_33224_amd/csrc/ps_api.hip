@@ -1,0 +1,563 @@
+// Host side of the C ABI declared in include/packserve.h: argument checks,
+// device memory, streams and kernel launches.  Every step of the scoring
+// path runs in the kernels of ps_kernels.hip; nothing here computes a
+// decision.
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ps_device.h"
+
+using namespace ps;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+// Largest dynamic LDS the scoring kernel asks for per workgroup; above it
+// the per-candidate hit rows live in device scratch instead.
+constexpr size_t kLdsBudget = 64 * 1024;
+// Workgroups of the persistent scoring grid when hit rows are in scratch.
+constexpr int kScratchRowsPerCU = 4;
+
+}  // namespace
+
+struct ps_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  int num_cus = 0;
+  std::string err;
+  bool loaded = false;
+  // snapshot
+  int32_t n_inst = 0;
+  int32_t cap = 0;
+  Tables t{};
+  InstState* d_inst = nullptr;
+  DevModel* d_model = nullptr;
+  unsigned long long* d_counter = nullptr;
+  uint32_t* d_scratch = nullptr;
+  int scratch_rows = 0;
+  bool hits_in_lds = true;
+  std::vector<InstState> h_state;
+  std::vector<uint32_t> h_count;
+  DevModel h_model{};
+  // staging for the host-memory entry points
+  void* d_stage[3] = {nullptr, nullptr, nullptr};
+  size_t stage_cap[3] = {0, 0, 0};
+};
+
+namespace {
+
+ps_status fail(ps_ctx* c, ps_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  else g_create_error = buf;
+  return code;
+}
+
+#define HIP_TRY(ctx, call)                                                                  \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail(ctx, e_ == hipErrorOutOfMemory ? PS_E_NOMEM : PS_E_DEVICE, "%s: %s", #call, \
+                  hipGetErrorString(e_));                                                   \
+  } while (0)
+
+// Makes ctx's device current for the scope of an entry point.
+struct DeviceScope {
+  int prev = -1;
+  explicit DeviceScope(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceScope() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+template <class T>
+void dfree(T*& p) {
+  if (p) (void)hipFree((void*)p);
+  p = nullptr;
+}
+
+// Grows staging buffer k to at least `bytes`.
+ps_status stage_buffer(ps_ctx* c, int k, size_t bytes, void** out) {
+  if (bytes > c->stage_cap[k]) {
+    if (c->d_stage[k]) (void)hipFree(c->d_stage[k]);
+    c->d_stage[k] = nullptr;
+    c->stage_cap[k] = 0;
+    size_t want = std::max(bytes, (size_t)4096);
+    HIP_TRY(c, hipMalloc(&c->d_stage[k], want));
+    c->stage_cap[k] = want;
+  }
+  *out = c->d_stage[k];
+  return PS_OK;
+}
+
+int32_t segment_of_host(const ps_model& m, int32_t B) {
+  for (int32_t s = 0; s < m.n_seg; ++s)
+    if (B <= m.seg_ub[s]) return s;
+  return m.n_seg - 1;
+}
+
+bool finite(float x) { return std::isfinite(x); }
+
+ps_status check_model(ps_ctx* c, const ps_model* m) {
+  if (!m) return fail(c, PS_E_INVAL, "model is NULL");
+  if (m->n_seg < 1 || m->n_seg > PS_MAX_SEG)
+    return fail(c, PS_E_RANGE, "n_seg %d outside [1, %d]", m->n_seg, PS_MAX_SEG);
+  for (int k = 0; k < 6; ++k)
+    if (!finite(m->alpha[k])) return fail(c, PS_E_INVAL, "alpha[%d] is not finite", k);
+  for (int s = 0; s < m->n_seg; ++s) {
+    if (m->seg_ub[s] < 1 || (s > 0 && m->seg_ub[s] <= m->seg_ub[s - 1]))
+      return fail(c, PS_E_INVAL, "seg_ub must be positive and strictly ascending (segment %d)", s);
+    for (int k = 0; k < 3; ++k)
+      if (!finite(m->beta[s][k])) return fail(c, PS_E_INVAL, "beta[%d][%d] is not finite", s, k);
+    if (!finite(m->gamma[s]) || !(m->gamma[s] > 0.0f))
+      return fail(c, PS_E_INVAL, "gamma[%d] must be finite and > 0", s);
+  }
+  if (!finite(m->eta) || m->eta < 0.0f) return fail(c, PS_E_INVAL, "eta must be finite and >= 0");
+  if (!finite(m->tpot_slo) || m->tpot_slo < 0.0f)
+    return fail(c, PS_E_INVAL, "tpot_slo must be finite and >= 0");
+  if (!finite(m->ttft_floor) || m->ttft_floor < 0.0f)
+    return fail(c, PS_E_INVAL, "ttft_floor must be finite and >= 0");
+  if (!finite(m->lout) || m->lout < 0.0f) return fail(c, PS_E_INVAL, "lout must be finite and >= 0");
+  if (m->block_tokens < 1 || m->block_tokens > PS_MAX_BLOCK_TOKENS)
+    return fail(c, PS_E_RANGE, "block_tokens %d outside [1, %d]", m->block_tokens, PS_MAX_BLOCK_TOKENS);
+  if (m->b_max < 1 || m->b_max > PS_MAX_BATCH)
+    return fail(c, PS_E_RANGE, "b_max %d outside [1, %d]", m->b_max, PS_MAX_BATCH);
+  if (m->kv_cap_tokens < 0) return fail(c, PS_E_RANGE, "kv_cap_tokens is negative");
+  if (m->flags & ~(PS_F_TTFT_ADMIT | PS_F_NO_KVC_FILTER | PS_F_NO_TPOT_FILTER))
+    return fail(c, PS_E_INVAL, "unknown flag bits 0x%x", m->flags);
+  return PS_OK;
+}
+
+DevModel device_model(const ps_model& m) {
+  DevModel d{};
+  for (int k = 0; k < 6; ++k) d.a[k] = m.alpha[k];
+  const double a1 = m.alpha[1], a2 = m.alpha[2], a3 = m.alpha[3], a4 = m.alpha[4], a5 = m.alpha[5];
+  d.k1 = (float)(a1 - a4);
+  d.k2 = (float)(a2 - 2.0 * a5);
+  d.k3 = (float)(a3 - a2 + a5);
+  d.eta = m.eta;
+  d.tau = m.tpot_slo;
+  d.ttft_floor = m.ttft_floor;
+  d.lout1 = std::max(1.0f, m.lout);
+  d.bs = m.block_tokens;
+  d.b_max = m.b_max;
+  d.kv_cap = m.kv_cap_tokens;
+  d.flags = m.flags;
+  d.n_seg = m.n_seg;
+  for (int s = 0; s < PS_MAX_SEG; ++s) {
+    d.seg_ub[s] = s < m.n_seg ? m.seg_ub[s] : 0;
+    for (int k = 0; k < 3; ++k) d.seg[s][k] = s < m.n_seg ? m.beta[s][k] : 0.0f;
+    d.seg[s][3] = s < m.n_seg ? m.gamma[s] : 1.0f;
+  }
+  return d;
+}
+
+ps_status check_reqs_host(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_req* reqs,
+                          int32_t n) {
+  if (pool_len < 0) return fail(c, PS_E_INVAL, "pool_len is negative");
+  if (n > 0 && !reqs) return fail(c, PS_E_INVAL, "reqs is NULL");
+  if (pool_len > 0 && !pool) return fail(c, PS_E_INVAL, "pool is NULL");
+  for (int32_t r = 0; r < n; ++r) {
+    const ps_req& q = reqs[r];
+    if (q.pre_len < 0 || q.tail_len < 0 || q.pre_off < 0 || q.tail_off < 0 ||
+        q.pre_off > pool_len || q.tail_off > pool_len || q.pre_len > pool_len - q.pre_off ||
+        q.tail_len > pool_len - q.tail_off)
+      return fail(c, PS_E_RANGE, "request %d lies outside the pool", r);
+    if ((int64_t)q.pre_len + q.tail_len > PS_MAX_CHAIN)
+      return fail(c, PS_E_RANGE, "request %d chain longer than %d blocks", r, PS_MAX_CHAIN);
+  }
+  for (int64_t k = 0; k < pool_len; ++k)
+    if (pool[k] == 0) return fail(c, PS_E_INVAL, "zero block hash at pool[%lld]", (long long)k);
+  return PS_OK;
+}
+
+void free_snapshot(ps_ctx* c) {
+  dfree(c->t.keys);
+  dfree(c->t.count);
+  dfree(c->d_inst);
+  dfree(c->d_scratch);
+  c->loaded = false;
+}
+
+}  // namespace
+
+extern "C" {
+
+ps_status ps_create(int device, ps_ctx** out) {
+  if (!out) return fail(nullptr, PS_E_INVAL, "out is NULL");
+  *out = nullptr;
+  int n = 0;
+  hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess)
+    return fail(nullptr, PS_E_DEVICE, "hipGetDeviceCount: %s", hipGetErrorString(e));
+  if (device < 0 || device >= n)
+    return fail(nullptr, PS_E_INVAL, "device %d outside [0, %d)", device, n);
+  ps_ctx* c = new (std::nothrow) ps_ctx();
+  if (!c) return fail(nullptr, PS_E_NOMEM, "host allocation failed");
+  c->device = device;
+  DeviceScope ds(device);
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, device);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipMalloc((void**)&c->d_model, sizeof(DevModel));
+  if (e == hipSuccess) e = hipMalloc((void**)&c->d_counter, sizeof(unsigned long long));
+  if (e != hipSuccess) {
+    ps_destroy(c);
+    return fail(nullptr, PS_E_DEVICE, "device set-up failed: %s", hipGetErrorString(e));
+  }
+  c->num_cus = prop.multiProcessorCount;
+  *out = c;
+  return PS_OK;
+}
+
+ps_status ps_destroy(ps_ctx* c) {
+  if (!c) return PS_OK;
+  DeviceScope ds(c->device);
+  if (c->stream) (void)hipStreamSynchronize(c->stream);
+  free_snapshot(c);
+  dfree(c->d_model);
+  dfree(c->d_counter);
+  for (int k = 0; k < 3; ++k)
+    if (c->d_stage[k]) (void)hipFree(c->d_stage[k]);
+  if (c->stream) (void)hipStreamDestroy(c->stream);
+  delete c;
+  return PS_OK;
+}
+
+const char* ps_last_error(const ps_ctx* c) {
+  return c ? c->err.c_str() : g_create_error.c_str();
+}
+
+ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!in) return fail(c, PS_E_INVAL, "instances is NULL");
+  ps_status st = check_model(c, m);
+  if (st != PS_OK) return st;
+  const int32_t n = in->n_inst;
+  if (n < 1 || n > PS_MAX_INST) return fail(c, PS_E_RANGE, "n_inst %d outside [1, %d]", n, PS_MAX_INST);
+  if (in->table_cap_blocks < 1 || in->table_cap_blocks > PS_MAX_TABLE_CAP)
+    return fail(c, PS_E_RANGE, "table_cap_blocks %d outside [1, %d]", in->table_cap_blocks,
+                PS_MAX_TABLE_CAP);
+  if (!in->blk_off || !in->decoding || !in->queued || !in->pending_tok || !in->ctx_tok)
+    return fail(c, PS_E_INVAL, "instance array is NULL");
+  if (in->blk_off[0] != 0) return fail(c, PS_E_INVAL, "blk_off[0] must be 0");
+  for (int32_t i = 0; i < n; ++i) {
+    const int64_t len = in->blk_off[i + 1] - in->blk_off[i];
+    if (len < 0) return fail(c, PS_E_INVAL, "blk_off not ascending at instance %d", i);
+    if (len > in->table_cap_blocks)
+      return fail(c, PS_E_RANGE, "instance %d lists %lld blocks > table_cap_blocks %d", i,
+                  (long long)len, in->table_cap_blocks);
+    if (in->decoding[i] < 0 || in->decoding[i] > PS_MAX_DQ || in->queued[i] < 0 ||
+        in->queued[i] > PS_MAX_DQ)
+      return fail(c, PS_E_RANGE, "instance %d: decoding/queued outside [0, %d]", i, PS_MAX_DQ);
+    if (in->pending_tok[i] < 0 || in->pending_tok[i] > PS_MAX_PENDING)
+      return fail(c, PS_E_RANGE, "instance %d: pending_tok outside [0, 2^34]", i);
+    if (in->ctx_tok[i] < 0 || in->ctx_tok[i] > PS_MAX_CONTEXT)
+      return fail(c, PS_E_RANGE, "instance %d: ctx_tok outside [0, 2^46]", i);
+  }
+  const int64_t n_blk = in->blk_off[n];
+  if (n_blk > 0 && !in->blk) return fail(c, PS_E_INVAL, "blk is NULL");
+  for (int64_t k = 0; k < n_blk; ++k)
+    if (in->blk[k] == 0) return fail(c, PS_E_INVAL, "zero block hash at blk[%lld]", (long long)k);
+
+  // geometry: >= 2 * cap slots, power of two buckets of 8 slots
+  int64_t slots = 8;
+  while (slots < 2 * (int64_t)in->table_cap_blocks) slots <<= 1;
+  const int64_t buckets = slots / kSlotsPerBucket;
+  int log2b = 0;
+  while ((1ll << log2b) < buckets) ++log2b;
+
+  DeviceScope ds(c->device);
+  ps_ctx fresh;  // new device buffers; swapped in only on success
+  fresh.t.slots = slots;
+  fresh.t.bmask = (uint32_t)(buckets - 1);
+  fresh.t.shift = (uint32_t)(64 - log2b);
+  const size_t tab_bytes = (size_t)n * (size_t)slots * sizeof(uint64_t);
+  const bool lds = ps_score_lds_bytes(n) <= kLdsBudget;
+  const int rows = lds ? 0 : std::max(1, c->num_cus * kScratchRowsPerCU);
+  int64_t* d_off = nullptr;
+  uint64_t* d_blk = nullptr;
+  auto cleanup = [&]() {
+    dfree(fresh.t.keys);
+    dfree(fresh.t.count);
+    dfree(fresh.d_inst);
+    dfree(fresh.d_scratch);
+    dfree(d_off);
+    dfree(d_blk);
+  };
+  hipError_t e = hipMalloc((void**)&fresh.t.keys, tab_bytes);
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.t.count, (size_t)n * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst, (size_t)n * sizeof(InstState));
+  if (e == hipSuccess && rows)
+    e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
+  if (e == hipSuccess && n_blk) e = hipMalloc((void**)&d_blk, (size_t)n_blk * sizeof(uint64_t));
+  if (e != hipSuccess) {
+    cleanup();
+    return fail(c, e == hipErrorOutOfMemory ? PS_E_NOMEM : PS_E_DEVICE,
+                "allocating %.1f MiB of tables: %s", tab_bytes / 1048576.0, hipGetErrorString(e));
+  }
+  std::vector<InstState> hs((size_t)n);
+  for (int32_t i = 0; i < n; ++i) {
+    InstState& s = hs[(size_t)i];
+    s.D = in->decoding[i];
+    s.Q = in->queued[i];
+    s.A1 = s.D + s.Q + 1;
+    s.seg = segment_of_host(*m, s.A1);
+    s.P = in->pending_tok[i];
+    s.S = in->ctx_tok[i];
+  }
+  const DevModel dm = device_model(*m);
+  hipStream_t sm = c->stream;
+  e = hipMemsetAsync(fresh.t.keys, 0, tab_bytes, sm);
+  if (e == hipSuccess) e = hipMemsetAsync(fresh.t.count, 0, (size_t)n * sizeof(uint32_t), sm);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_counter, 0, sizeof(unsigned long long), sm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(d_off, in->blk_off, (size_t)(n + 1) * sizeof(int64_t), hipMemcpyHostToDevice, sm);
+  if (e == hipSuccess && n_blk)
+    e = hipMemcpyAsync(d_blk, in->blk, (size_t)n_blk * sizeof(uint64_t), hipMemcpyHostToDevice, sm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(fresh.d_inst, hs.data(), hs.size() * sizeof(InstState), hipMemcpyHostToDevice, sm);
+  if (e == hipSuccess) {
+    BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter};
+    e = ps_launch_build(ba, sm);
+  }
+  unsigned long long full = 0;
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(&full, c->d_counter, sizeof full, hipMemcpyDeviceToHost, sm);
+  if (e == hipSuccess) e = hipStreamSynchronize(sm);
+  if (e == hipSuccess && full) {
+    cleanup();
+    return fail(c, PS_E_DEVICE, "table build found no free slot for %llu keys", full);
+  }
+  std::vector<uint32_t> hc((size_t)n);
+  if (e == hipSuccess)
+    e = hipMemcpy(hc.data(), fresh.t.count, (size_t)n * sizeof(uint32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) {
+    cleanup();
+    return fail(c, PS_E_DEVICE, "building tables: %s", hipGetErrorString(e));
+  }
+  // The model upload is the last step that can fail; the old snapshot stays
+  // intact until here.
+  e = hipMemcpy(c->d_model, &dm, sizeof dm, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    cleanup();
+    if (c->loaded) (void)hipMemcpy(c->d_model, &c->h_model, sizeof c->h_model, hipMemcpyHostToDevice);
+    return fail(c, PS_E_DEVICE, "model upload: %s", hipGetErrorString(e));
+  }
+  dfree(d_off);
+  dfree(d_blk);
+  free_snapshot(c);
+  c->t = fresh.t;
+  c->d_inst = fresh.d_inst;
+  c->d_scratch = fresh.d_scratch;
+  c->scratch_rows = rows;
+  c->hits_in_lds = lds;
+  c->n_inst = n;
+  c->cap = in->table_cap_blocks;
+  c->h_state = std::move(hs);
+  c->h_count = std::move(hc);
+  c->h_model = dm;
+  c->loaded = true;
+  fresh.t.keys = nullptr;
+  fresh.t.count = nullptr;
+  fresh.d_inst = nullptr;
+  fresh.d_scratch = nullptr;
+  return PS_OK;
+}
+
+static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                              const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                              uint32_t* d_sizes, uint32_t* d_hits, hipStream_t s) {
+  ScoreArgs a{};
+  a.t = c->t;
+  a.inst = c->d_inst;
+  a.model = c->d_model;
+  a.pool = d_pool;
+  a.pool_len = pool_len;
+  a.reqs = d_reqs;
+  a.n_req = n_req;
+  a.n_inst = c->n_inst;
+  a.out = d_out;
+  a.sizes = d_sizes;
+  a.hits_out = d_hits;
+  a.scratch = c->d_scratch;
+  const int grid = c->hits_in_lds ? n_req : std::min(n_req, c->scratch_rows);
+  HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, grid, d_hits != nullptr, s));
+  return PS_OK;
+}
+
+ps_status ps_score_window_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                              const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                              uint32_t* d_sizes, void* hip_stream) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n_req < 0 || pool_len < 0) return fail(c, PS_E_INVAL, "negative n_req or pool_len");
+  if (n_req == 0) return PS_OK;
+  if (!d_reqs || !d_out || (pool_len > 0 && !d_pool))
+    return fail(c, PS_E_INVAL, "device buffer is NULL");
+  DeviceScope ds(c->device);
+  return launch_score(c, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, nullptr,
+                      (hipStream_t)hip_stream);
+}
+
+ps_status ps_probe_hits_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                            const ps_req* d_reqs, int32_t n_req, uint32_t* d_hits,
+                            void* hip_stream) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n_req < 0 || pool_len < 0) return fail(c, PS_E_INVAL, "negative n_req or pool_len");
+  if (n_req == 0) return PS_OK;
+  if (!d_reqs || !d_hits || (pool_len > 0 && !d_pool))
+    return fail(c, PS_E_INVAL, "device buffer is NULL");
+  DeviceScope ds(c->device);
+  return launch_score(c, d_pool, pool_len, d_reqs, n_req, nullptr, nullptr, d_hits,
+                      (hipStream_t)hip_stream);
+}
+
+ps_status ps_score_window(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_req* reqs,
+                          int32_t n_req, ps_result* out) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n_req < 0) return fail(c, PS_E_INVAL, "negative n_req");
+  if (n_req == 0) return PS_OK;
+  if (!out) return fail(c, PS_E_INVAL, "out is NULL");
+  ps_status st = check_reqs_host(c, pool, pool_len, reqs, n_req);
+  if (st != PS_OK) return st;
+  DeviceScope ds(c->device);
+  void *dp, *dr, *dout;
+  if ((st = stage_buffer(c, 0, (size_t)pool_len * sizeof(uint64_t), &dp)) != PS_OK) return st;
+  if ((st = stage_buffer(c, 1, (size_t)n_req * sizeof(ps_req), &dr)) != PS_OK) return st;
+  if ((st = stage_buffer(c, 2, (size_t)n_req * sizeof(ps_result), &dout)) != PS_OK) return st;
+  hipStream_t s = c->stream;
+  if (pool_len)
+    HIP_TRY(c, hipMemcpyAsync(dp, pool, (size_t)pool_len * sizeof(uint64_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(dr, reqs, (size_t)n_req * sizeof(ps_req), hipMemcpyHostToDevice, s));
+  st = launch_score(c, (const uint64_t*)dp, pool_len, (const ps_req*)dr, n_req, (ps_result*)dout,
+                    nullptr, nullptr, s);
+  if (st != PS_OK) return st;
+  HIP_TRY(c, hipMemcpyAsync(out, dout, (size_t)n_req * sizeof(ps_result), hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  return PS_OK;
+}
+
+ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_req* reqs,
+                    const int32_t* inst, int32_t n, int64_t* n_dropped) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n < 0) return fail(c, PS_E_INVAL, "negative n");
+  if (n_dropped) *n_dropped = 0;
+  if (n == 0) return PS_OK;
+  if (!inst) return fail(c, PS_E_INVAL, "inst is NULL");
+  ps_status st = check_reqs_host(c, pool, pool_len, reqs, n);
+  if (st != PS_OK) return st;
+  const int32_t ni = c->n_inst;
+  const int64_t bs = c->h_model.bs;
+  std::vector<int32_t> cnt((size_t)ni, 0);
+  std::vector<int64_t> add((size_t)ni, 0);
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t i = inst[k];
+    if (i < -1 || i >= ni) return fail(c, PS_E_RANGE, "entry %d: instance %d outside [-1, %d)", k, i, ni);
+    if (i < 0) continue;
+    cnt[(size_t)i] += 1;
+    add[(size_t)i] += ((int64_t)reqs[k].pre_len + reqs[k].tail_len) * bs;
+  }
+  std::vector<int32_t> grp_off, grp_inst;
+  for (int32_t i = 0; i < ni; ++i) {
+    const InstState& s = c->h_state[(size_t)i];
+    if (!cnt[(size_t)i]) continue;
+    if (s.Q + cnt[(size_t)i] > PS_MAX_DQ)
+      return fail(c, PS_E_RANGE, "instance %d: queued would exceed %d", i, PS_MAX_DQ);
+    if (s.P + add[(size_t)i] > PS_MAX_PENDING || s.S + add[(size_t)i] > PS_MAX_CONTEXT)
+      return fail(c, PS_E_RANGE, "instance %d: token counters would exceed their limits", i);
+  }
+  // entries grouped by instance, array order kept inside a group
+  std::vector<int32_t> start((size_t)ni + 1, 0);
+  for (int32_t i = 0; i < ni; ++i) start[(size_t)i + 1] = start[(size_t)i] + cnt[(size_t)i];
+  std::vector<int32_t> order((size_t)start[(size_t)ni]);
+  {
+    std::vector<int32_t> fill(start.begin(), start.end() - 1);
+    for (int32_t k = 0; k < n; ++k)
+      if (inst[k] >= 0) order[(size_t)fill[(size_t)inst[k]]++] = k;
+  }
+  for (int32_t i = 0; i < ni; ++i)
+    if (cnt[(size_t)i]) {
+      grp_inst.push_back(i);
+      grp_off.push_back(start[(size_t)i]);
+    }
+  grp_off.push_back((int32_t)order.size());
+  if (grp_inst.empty()) return PS_OK;
+
+  DeviceScope ds(c->device);
+  void *dp, *dr, *dx;
+  const size_t n_grp = grp_inst.size();
+  const size_t aux = (order.size() + 2 * n_grp + 1) * sizeof(int32_t);
+  if ((st = stage_buffer(c, 0, (size_t)pool_len * sizeof(uint64_t), &dp)) != PS_OK) return st;
+  if ((st = stage_buffer(c, 1, (size_t)n * sizeof(ps_req), &dr)) != PS_OK) return st;
+  if ((st = stage_buffer(c, 2, aux, &dx)) != PS_OK) return st;
+  int32_t* d_order = (int32_t*)dx;
+  int32_t* d_grp_off = d_order + order.size();
+  int32_t* d_grp_inst = d_grp_off + n_grp + 1;
+  hipStream_t s = c->stream;
+  HIP_TRY(c, hipMemcpyAsync(dp, pool, (size_t)pool_len * sizeof(uint64_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(dr, reqs, (size_t)n * sizeof(ps_req), hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(d_order, order.data(), order.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(d_grp_off, grp_off.data(), grp_off.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(d_grp_inst, grp_inst.data(), n_grp * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemsetAsync(c->d_counter, 0, sizeof(unsigned long long), s));
+  CommitArgs ca{c->t, c->d_inst, c->d_model, (const uint64_t*)dp, (const ps_req*)dr,
+                d_order, d_grp_off, d_grp_inst, (int32_t)n_grp, (uint32_t)c->cap, c->d_counter};
+  HIP_TRY(c, ps_launch_commit(ca, s));
+  unsigned long long dropped = 0;
+  HIP_TRY(c, hipMemcpyAsync(&dropped, c->d_counter, sizeof dropped, hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(c->h_state.data(), c->d_inst, c->h_state.size() * sizeof(InstState),
+                            hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(c->h_count.data(), c->t.count, c->h_count.size() * sizeof(uint32_t),
+                            hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  if (n_dropped) *n_dropped = (int64_t)dropped;
+  return PS_OK;
+}
+
+ps_status ps_read_state(ps_ctx* c, int32_t* decoding, int32_t* queued, int64_t* pending_tok,
+                        int64_t* ctx_tok, int64_t* cached_blocks) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  for (int32_t i = 0; i < c->n_inst; ++i) {
+    const InstState& s = c->h_state[(size_t)i];
+    if (decoding) decoding[i] = s.D;
+    if (queued) queued[i] = s.Q;
+    if (pending_tok) pending_tok[i] = s.P;
+    if (ctx_tok) ctx_tok[i] = s.S;
+    if (cached_blocks) cached_blocks[i] = c->h_count[(size_t)i];
+  }
+  return PS_OK;
+}
+
+ps_status ps_table_info(ps_ctx* c, int64_t* slots_per_table, int64_t* table_bytes,
+                        int32_t* hits_in_lds) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (slots_per_table) *slots_per_table = c->t.slots;
+  if (table_bytes) *table_bytes = c->t.slots * (int64_t)c->n_inst * (int64_t)sizeof(uint64_t);
+  if (hits_in_lds) *hits_in_lds = c->hits_in_lds ? 1 : 0;
+  return PS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Internal device-side layout and inline helpers of the window scorer
+// (gfx950, wave64).  Shared by the kernels and the host API of this library
+// only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "packserve.h"
+
+namespace ps {
+
+constexpr int kBlock = 256;            // threads per scoring workgroup (4 waves)
+constexpr int kWaves = kBlock / 64;
+constexpr int kStage = 1024;           // chain blocks staged in LDS per request
+constexpr int kSlotsPerBucket = 8;     // 8 x 64-bit keys = one 64-byte bucket
+constexpr uint32_t kInelig = 0xFFFFFFFFu;  // hit slot of a capacity-ineligible instance
+constexpr uint32_t kCont = 0x80000000u;    // hit slot flag: walk continues past the breadth probe
+constexpr int kBreadthRounds = 8;      // octet loads in flight per lane in the breadth probe
+constexpr int kDeepRounds = 16;        // octet loads in flight per lane in a deep walk step
+
+// Per-instance load state, 32 bytes (one pair of 16-byte loads).
+struct alignas(16) InstState {
+  int32_t D;    // decoding
+  int32_t Q;    // queued
+  int32_t A1;   // D + Q + 1: projected decode batch after admission
+  int32_t seg;  // decode segment of A1
+  int64_t P;    // pending uncached prefill tokens
+  int64_t S;    // context tokens of the active requests
+};
+
+// Device copy of the model, with the recomputation-penalty polynomial
+// precomputed: T_pf(n, L - n) - T_pf(0, L) = n (k1 + k2 L + k3 n).
+struct DevModel {
+  float a[6];
+  float k1, k2, k3;
+  float eta, tau, ttft_floor, lout1;  // lout1 = max(1, lout)
+  int32_t bs, b_max;
+  int64_t kv_cap;
+  uint32_t flags;
+  int32_t n_seg;
+  int32_t seg_ub[PS_MAX_SEG];
+  float seg[PS_MAX_SEG][4];  // beta0, beta1, beta2, gamma
+};
+
+// Table geometry: n_inst tables of (1 << log2_buckets) buckets each.
+struct Tables {
+  uint64_t* keys;       // n_inst * slots
+  uint32_t* count;      // distinct keys per instance
+  int64_t slots;        // slots per instance = buckets * 8
+  uint32_t bmask;       // buckets - 1
+  uint32_t shift;       // 64 - log2(buckets) (64 when one bucket)
+};
+
+// Per-instance salted bucket index: a multiply-shift (Fibonacci) hash of the
+// key xor an instance salt, so one hash lands at unrelated offsets in
+// different tables (no two instances' probes for a request share a channel
+// pattern).
+__host__ __device__ __forceinline__ uint32_t bucket_of(uint64_t key, uint32_t inst,
+                                                       uint32_t shift) {
+  uint64_t x = (key ^ (0x9E3779B97F4A7C15ull * (uint64_t)(inst + 1u))) * 0xD6E8FEB86659FD93ull;
+  return shift >= 64 ? 0u : (uint32_t)(x >> shift);
+}
+
+struct ScoreArgs {
+  Tables t;
+  const InstState* inst;
+  const DevModel* model;
+  const uint64_t* pool;
+  int64_t pool_len;
+  const ps_req* reqs;
+  int32_t n_req;
+  int32_t n_inst;
+  ps_result* out;
+  uint32_t* sizes;       // optional |A|,|C|,|T| per request
+  uint32_t* hits_out;    // probe-all diagnostic: n_req * n_inst
+  uint32_t* scratch;     // per-workgroup hit rows when they do not fit LDS
+};
+
+struct CommitArgs {
+  Tables t;
+  InstState* inst;
+  const DevModel* model;
+  const uint64_t* pool;
+  const ps_req* reqs;
+  const int32_t* order;     // entries grouped by instance, array order kept
+  const int32_t* grp_off;   // n_grp + 1
+  const int32_t* grp_inst;  // n_grp
+  int32_t n_grp;
+  uint32_t cap;             // distinct keys allowed per instance
+  unsigned long long* dropped;
+};
+
+struct BuildArgs {
+  Tables t;
+  const int64_t* blk_off;
+  const uint64_t* blk;
+  int32_t n_inst;
+  int64_t n_blk;
+  unsigned long long* full;  // inserts that found no free slot (never for valid caps)
+};
+
+}  // namespace ps
+
+// Kernel launchers (ps_kernels.hip).
+hipError_t ps_launch_build(const ps::BuildArgs& a, hipStream_t s);
+hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
+                           hipStream_t s);
+hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
+size_t ps_score_lds_bytes(int32_t n_inst);

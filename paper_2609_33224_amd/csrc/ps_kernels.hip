@@ -1,0 +1,595 @@
+// HIP kernels of the window scorer for gfx950 (CDNA4, wave64).
+//
+//   build_kernel   - per-instance open-addressing tables from the CSR block
+//                    lists (64-bit atomicCAS inserts).
+//   score_kernel   - the fused hot path, one workgroup per request:
+//                      (1) longest cached prefix of the request's block-hash
+//                          chain on every capacity-eligible instance (a breadth
+//                          probe of the first block with lanes over instances,
+//                          then a deep walk with lanes over chain positions and
+//                          a ballot for the first miss; the chain's head is
+//                          staged in LDS),
+//                      (2) the latency model (Eq. 7 + C, C^2 terms; Eq. 8 per
+//                          segment with its EMA factor; Eq. 10; Eq. 4),
+//                      (3) capacity, recomputation (Eq. 9) and TPOT filters,
+//                      (4) the packed D-C-Q key and the LMetric fallback key,
+//                          reduced with DPP wave minima and an LDS cross-wave
+//                          step.
+//   commit_kernel  - ordered placement of decisions, one wave per instance.
+//
+// The path is bound by HBM (random 64-byte bucket reads); it does no dense
+// contraction, so it uses no MFMA.
+
+#include "ps_device.h"
+
+using namespace ps;
+
+namespace {
+
+// ---------------------------------------------------------------- reductions
+// DPP row shifts and row broadcasts (GFX9 encodings): after the six steps
+// lane 63 holds the reduction over all 64 lanes.  Lanes whose DPP source is
+// out of range keep `old`, which is the identity of the operation.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_src(uint32_t identity, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)identity, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+template <int CTRL, int RM>
+__device__ __forceinline__ void min_step(uint64_t& v) {
+  const uint32_t lo = dpp_src<CTRL, RM>(0xFFFFFFFFu, (uint32_t)v);
+  const uint32_t hi = dpp_src<CTRL, RM>(0xFFFFFFFFu, (uint32_t)(v >> 32));
+  const uint64_t t = ((uint64_t)hi << 32) | lo;
+  v = t < v ? t : v;
+}
+
+template <int CTRL, int RM>
+__device__ __forceinline__ void add_step(uint32_t& v) {
+  v += dpp_src<CTRL, RM>(0u, v);
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+  min_step<0x111, 0xF>(v);  // row_shr:1
+  min_step<0x112, 0xF>(v);  // row_shr:2
+  min_step<0x114, 0xF>(v);  // row_shr:4
+  min_step<0x118, 0xF>(v);  // row_shr:8
+  min_step<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+  min_step<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+  add_step<0x111, 0xF>(v);
+  add_step<0x112, 0xF>(v);
+  add_step<0x114, 0xF>(v);
+  add_step<0x118, 0xF>(v);
+  add_step<0x142, 0xA>(v);
+  add_step<0x143, 0xC>(v);
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+struct Red {
+  uint64_t k[2][kWaves];
+  uint32_t u[3][kWaves];
+};
+
+// ------------------------------------------------------------------- probing
+// Octet probing: the 8 lanes of an octet (lanes 8g .. 8g+7) read the 8 slots
+// of one 64-byte bucket, so every wave-wide load is 8 coalesced 64-byte
+// segments, and two ballots decide all 8 probes of the instruction.
+
+struct Bucket {
+  uint64_t k[kSlotsPerBucket];
+};
+
+__device__ __forceinline__ const uint64_t* table_of(const Tables& t, uint32_t inst) {
+  return t.keys + (size_t)inst * (size_t)t.slots;
+}
+
+// Status of the probe of `key` by the octet of this lane, from the slot
+// value this lane read: 1 found, 0 absent (an empty slot ends the probe
+// sequence), 2 full bucket without the key (the next bucket decides).
+// Inactive octets, and the zero hash (never stored), report 0.  Every lane
+// of the wave must execute this (two ballots).
+__device__ __forceinline__ uint32_t octet_status(uint64_t val, uint64_t key, bool act, int g) {
+  const uint64_t fm = __ballot(act && val == key);
+  const uint64_t em = __ballot(act && val == 0ull);
+  const uint32_t f = (uint32_t)(fm >> (8 * g)) & 0xFFu;
+  const uint32_t e = (uint32_t)(em >> (8 * g)) & 0xFFu;
+  if (!act || key == 0ull) return 0u;
+  return f ? 1u : (e ? 0u : 2u);
+}
+
+// Linear probing past full buckets for the octets still at status 2 (rare
+// at load factor <= 0.5).  Wave-uniform loop, bounded by the bucket count.
+__device__ __forceinline__ uint32_t octet_resolve(const Tables& t, const uint64_t* tab, uint32_t b,
+                                                  uint64_t key, uint32_t status, int s, int g) {
+  for (uint32_t step = 1; step <= t.bmask; ++step) {
+    const bool pend = status == 2u;
+    if (__ballot(pend) == 0ull) break;
+    b = (b + 1) & t.bmask;
+    const uint64_t val = pend ? tab[(size_t)b * kSlotsPerBucket + s] : 0ull;
+    const uint32_t st = octet_status(val, key, pend, g);
+    if (pend) status = st;
+  }
+  return status;
+}
+
+// Single-lane lookup (commit path only).
+__device__ __forceinline__ Bucket load_bucket(const uint64_t* p) {
+  const ulonglong2* q = reinterpret_cast<const ulonglong2*>(p);
+  const ulonglong2 a = q[0], b = q[1], c = q[2], d = q[3];
+  return Bucket{{a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y}};
+}
+
+__device__ bool probe(const Tables& t, uint32_t inst, uint64_t key) {
+  if (key == 0) return false;
+  const uint64_t* tab = table_of(t, inst);
+  uint32_t b = bucket_of(key, inst, t.shift);
+  for (uint32_t step = 0; step <= t.bmask; ++step) {
+    const Bucket bk = load_bucket(tab + (size_t)b * kSlotsPerBucket);
+    bool f = false, e = false;
+#pragma unroll
+    for (int s = 0; s < kSlotsPerBucket; ++s) {
+      f |= bk.k[s] == key;
+      e |= bk.k[s] == 0;
+    }
+    if (f) return true;
+    if (e) return false;
+    b = (b + 1) & t.bmask;
+  }
+  return false;
+}
+
+// 1 inserted, 0 already present, -1 no free slot.  Safe under concurrent
+// inserts: a slot only ever changes from 0 to a key, and every claim of an
+// apparently empty slot goes through a 64-bit compare-and-swap whose result
+// decides.
+__device__ int insert_key(const Tables& t, uint32_t inst, uint64_t key) {
+  uint64_t* tab = t.keys + (size_t)inst * (size_t)t.slots;
+  uint32_t b = bucket_of(key, inst, t.shift);
+  for (uint32_t step = 0; step <= t.bmask; ++step) {
+    uint64_t* bp = tab + (size_t)b * kSlotsPerBucket;
+    const Bucket bk = load_bucket(bp);
+    for (int s = 0; s < kSlotsPerBucket; ++s)
+      if (bk.k[s] == key) return 0;
+    for (int s = 0; s < kSlotsPerBucket; ++s) {
+      if (bk.k[s] != 0) continue;
+      const unsigned long long old =
+          atomicCAS(reinterpret_cast<unsigned long long*>(bp + s), 0ull, (unsigned long long)key);
+      if (old == 0ull) return 1;
+      if (old == key) return 0;
+    }
+    b = (b + 1) & t.bmask;
+  }
+  return -1;
+}
+
+// --------------------------------------------------------------------- chain
+struct ChainRef {
+  const uint64_t* pre;
+  const uint64_t* tail;
+  int32_t pre_len;
+  int32_t len;
+};
+
+__device__ __forceinline__ uint64_t chain_global(const ChainRef& c, int32_t j) {
+  return j < c.pre_len ? c.pre[j] : c.tail[j - c.pre_len];
+}
+
+__device__ __forceinline__ bool req_valid(const ps_req& q, int64_t pool_len) {
+  return q.pre_len >= 0 && q.tail_len >= 0 && q.pre_off >= 0 && q.tail_off >= 0 &&
+         q.pre_off <= pool_len && q.tail_off <= pool_len &&
+         (int64_t)q.pre_len <= pool_len - q.pre_off &&
+         (int64_t)q.tail_len <= pool_len - q.tail_off &&
+         (int64_t)q.pre_len + (int64_t)q.tail_len <= (int64_t)PS_MAX_CHAIN;
+}
+
+// Deep walk of one instance: octets over chain positions.  One step issues
+// kDeepRounds x 8 positions (or half of that on the first step) before any
+// is evaluated, then stops at the first absent position in chain order.
+// Wave-uniform arguments; returns the hit.
+template <bool STAGED>
+__device__ uint32_t deep_walk(const Tables& t, uint32_t inst, const ChainRef& c,
+                              const uint64_t* stage, int32_t pos, int lane) {
+  const int g = lane >> 3, s = lane & 7;
+  const int32_t ell = c.len;
+  const uint64_t* tab = table_of(t, inst);
+  int rounds = kDeepRounds / 2;
+  while (pos < ell) {
+    uint64_t key[kDeepRounds], val[kDeepRounds];
+    uint32_t b[kDeepRounds];
+#pragma unroll
+    for (int r = 0; r < kDeepRounds; ++r) {
+      const int32_t j = pos + r * 8 + g;
+      const bool act = r < rounds && j < ell;
+      key[r] = 0ull;
+      if (act) key[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+      b[r] = bucket_of(key[r], inst, t.shift);
+      val[r] = 0ull;
+      if (act && key[r] != 0ull) val[r] = tab[(size_t)b[r] * kSlotsPerBucket + s];
+    }
+#pragma unroll
+    for (int r = 0; r < kDeepRounds; ++r) {
+      if (r < rounds) {
+        const int32_t j = pos + r * 8 + g;
+        const bool act = j < ell;
+        uint32_t st = octet_status(val[r], key[r], act, g);
+        st = octet_resolve(t, tab, b[r], key[r], st, s, g);
+        const uint64_t miss = __ballot(act && st == 0u && s == 0);
+        if (miss) return (uint32_t)(pos + r * 8 + (__builtin_ctzll(miss) >> 3));
+      }
+    }
+    pos += rounds * 8;
+    rounds = kDeepRounds;
+  }
+  return (uint32_t)ell;
+}
+
+// ------------------------------------------------------------- latency model
+// Eq. 7 with the empirical C and C^2 terms: n new, c cached tokens.
+__device__ __forceinline__ float t_prefill(const DevModel& m, float n, float c) {
+  return m.a[0] + n * (m.a[1] + m.a[2] * c + m.a[3] * n) + c * (m.a[4] + m.a[5] * c);
+}
+
+// T_pf(n, L - n) - T_pf(0, L) as a polynomial in n (no cancellation between
+// two large prefill times).
+__device__ __forceinline__ float recompute_raw(const DevModel& m, float n, float L) {
+  return n * (m.k1 + m.k2 * L + m.k3 * n);
+}
+
+struct Lat {
+  float tpot, ttft;
+};
+
+// Eq. 10 (decode term of Eq. 8 for the projected batch and context, scaled
+// by the segment's EMA factor; prefill interference amortised over the
+// median output length, only on a busy instance) and Eq. 4's TTFT with the
+// queue estimate a0 Q + a1 P.
+__device__ __forceinline__ Lat latency(const DevModel& m, const InstState& st, float n, float c,
+                                       int64_t L) {
+  const float tp = t_prefill(m, n, c);
+  const float* sg = m.seg[st.seg];
+  const float t_iter = sg[3] * (sg[0] + sg[1] * (float)st.A1 + sg[2] * (float)(st.S + L));
+  const float interf = st.A1 > 1 ? tp / m.lout1 : 0.0f;
+  Lat r;
+  r.tpot = t_iter + interf;
+  r.ttft = tp + m.a[0] * (float)st.Q + m.a[1] * (float)st.P;
+  return r;
+}
+
+__device__ __forceinline__ bool eligible(const DevModel& m, int32_t A1, int64_t S, int64_t L) {
+  return A1 <= m.b_max && S + L <= m.kv_cap;
+}
+
+// ------------------------------------------------------------------ kernels
+__global__ void build_kernel(BuildArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < a.n_blk; k += stride) {
+    int32_t lo = 0, hi = a.n_inst;  // last row with blk_off[row] <= k
+    while (hi - lo > 1) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (a.blk_off[mid] <= k) lo = mid;
+      else hi = mid;
+    }
+    const int r = insert_key(a.t, (uint32_t)lo, a.blk[k]);
+    if (r == 1) atomicAdd(&a.t.count[lo], 1u);
+    else if (r < 0) atomicAdd(a.full, 1ull);
+  }
+}
+
+template <bool HITS_IN_LDS, bool PROBE_ALL>
+__global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ Red red;
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
+  uint32_t* hits = HITS_IN_LDS ? reinterpret_cast<uint32_t*>(smem + kStage * sizeof(uint64_t))
+                               : a.scratch + (size_t)blockIdx.x * (size_t)a.n_inst;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const DevModel& m = *a.model;
+  const int32_t n_inst = a.n_inst;
+
+  for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
+    const ps_req q = a.reqs[r];
+    if (!req_valid(q, a.pool_len)) {
+      if (PROBE_ALL) {
+        for (int32_t i = tid; i < n_inst; i += kBlock)
+          a.hits_out[(size_t)r * n_inst + i] = 0xFFFFFFFFu;
+      } else if (tid == 0) {
+        a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
+        if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+      }
+      continue;
+    }
+    const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
+    const int32_t ell = c.len;
+    const int64_t L = (int64_t)ell * m.bs;
+
+    // Stage the head of the chain in LDS (coalesced 8-byte reads).
+    const int32_t nst = ell < kStage ? ell : kStage;
+    for (int32_t j = tid; j < nst; j += kBlock) stage[j] = chain_global(c, j);
+    __syncthreads();
+
+    // (1a) Breadth probe of the chain's first block: octets over instances,
+    // kBreadthRounds x 8 instances per wave per step, all loads in flight
+    // before any is evaluated.
+    const uint64_t k0 = ell > 0 ? stage[0] : 0ull;
+    {
+      const int g = lane >> 3, s = lane & 7;
+      for (int32_t base = wave * (8 * kBreadthRounds); base < n_inst;
+           base += kWaves * 8 * kBreadthRounds) {
+        uint64_t val[kBreadthRounds];
+        uint32_t bkt[kBreadthRounds];
+        bool el[kBreadthRounds];
+#pragma unroll
+        for (int r = 0; r < kBreadthRounds; ++r) {
+          const int32_t i = base + r * 8 + g;
+          el[r] = false;
+          if (i < n_inst) {
+            const InstState* st = a.inst + i;
+            el[r] = PROBE_ALL || eligible(m, st->A1, st->S, L);
+          }
+          bkt[r] = bucket_of(k0, (uint32_t)i, a.t.shift);
+          val[r] = 0ull;
+          if (el[r] && k0 != 0ull)
+            val[r] = table_of(a.t, (uint32_t)i)[(size_t)bkt[r] * kSlotsPerBucket + s];
+        }
+#pragma unroll
+        for (int r = 0; r < kBreadthRounds; ++r) {
+          const int32_t i = base + r * 8 + g;
+          uint32_t st = octet_status(val[r], k0, el[r], g);
+          st = octet_resolve(a.t, table_of(a.t, (uint32_t)i), bkt[r], k0, st, s, g);
+          if (s == 0 && i < n_inst)
+            hits[i] = !el[r] ? kInelig : (st == 1u ? (ell > 1 ? (1u | kCont) : 1u) : 0u);
+        }
+      }
+    }
+    __syncthreads();
+
+    // (1b) Deep walks: each wave takes the surviving instances of its
+    // 64-instance chunks; lanes over chain positions.
+    for (int32_t base = wave * 64; base < n_inst; base += kBlock) {
+      const int32_t i = base + lane;
+      const uint32_t v = i < n_inst ? hits[i] : 0u;
+      uint64_t mask = __ballot(v != kInelig && (v & kCont) != 0u);
+      while (mask) {
+        const int s = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        const uint32_t inst = (uint32_t)(base + s);
+        const uint32_t h = deep_walk<true>(a.t, inst, c, stage, 1, lane);
+        if (lane == 0) hits[inst] = h;
+      }
+    }
+    __syncthreads();
+
+    if (PROBE_ALL) {
+      for (int32_t i = tid; i < n_inst; i += kBlock) a.hits_out[(size_t)r * n_inst + i] = hits[i];
+      __syncthreads();
+      continue;
+    }
+
+    // (2)-(3) Capacity set A and the minimum recomputation penalty over A.
+    const float Lf = (float)L;
+    uint32_t wmin_bits = 0x7F800000u;  // +inf; penalties are >= 0, so bit order = value order
+    uint32_t nA = 0;
+    for (int32_t i = tid; i < n_inst; i += kBlock) {
+      const uint32_t v = hits[i];
+      if (v == kInelig) continue;
+      ++nA;
+      const float n = (float)(L - (int64_t)v * m.bs);
+      const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
+      const uint32_t wb = __float_as_uint(W);
+      wmin_bits = wb < wmin_bits ? wb : wmin_bits;
+    }
+    {
+      const uint64_t wm = wave_min_u64((uint64_t)wmin_bits);
+      const uint32_t na = wave_sum_u32(nA);
+      if (lane == 0) {
+        red.k[0][wave] = wm;
+        red.u[0][wave] = na;
+      }
+    }
+    __syncthreads();
+    uint64_t wmin64 = red.k[0][0];
+    nA = red.u[0][0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) {
+      wmin64 = red.k[0][w] < wmin64 ? red.k[0][w] : wmin64;
+      nA += red.u[0][w];
+    }
+    const float wmin = __uint_as_float((uint32_t)wmin64);
+    __syncthreads();
+
+    // (3)-(4) Filters and keys.
+    const float Z = recompute_raw(m, Lf, Lf);   // T_pf(L, 0) - T_pf(0, L)
+    const float tpf_cold = t_prefill(m, Lf, 0.0f);
+    const float slo = fmaxf(m.ttft_floor, tpf_cold);
+    const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+    const bool tpot_filter = !(m.flags & PS_F_NO_TPOT_FILTER);
+    const bool ttft_admit = (m.flags & PS_F_TTFT_ADMIT) != 0;
+    uint64_t keyT = ~0ull, keyF = ~0ull;
+    uint32_t nC = 0, nT = 0;
+    if (nA > 0) {
+      for (int32_t i = tid; i < n_inst; i += kBlock) {
+        const uint32_t v = hits[i];
+        if (v == kInelig) continue;
+        const int64_t c_tok = (int64_t)v * m.bs;
+        const int64_t n_tok = L - c_tok;
+        const float n = (float)n_tok;
+        if (kvc) {
+          const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
+          if (!((W - wmin) / Z <= m.eta)) continue;
+        }
+        ++nC;
+        const InstState st = a.inst[i];
+        const Lat lt = latency(m, st, n, (float)c_tok, L);
+        const uint64_t lm = (uint64_t)(st.P + n_tok) * (uint64_t)st.A1;
+        const uint64_t kf = (lm << 16) | (uint64_t)i;
+        keyF = kf < keyF ? kf : keyF;
+        const bool inT = (!tpot_filter || lt.tpot < m.tau) && (!ttft_admit || lt.ttft <= slo);
+        if (inT) {
+          ++nT;
+          const uint64_t kt = ((uint64_t)(PS_MAX_DQ - st.D) << 52) |
+                              ((uint64_t)(PS_MAX_CHAIN - v) << 28) | ((uint64_t)st.Q << 16) |
+                              (uint64_t)i;
+          keyT = kt < keyT ? kt : keyT;
+        }
+      }
+    }
+    {
+      const uint64_t kt = wave_min_u64(keyT);
+      const uint64_t kf = wave_min_u64(keyF);
+      const uint32_t nc = wave_sum_u32(nC);
+      const uint32_t nt = wave_sum_u32(nT);
+      if (lane == 0) {
+        red.k[0][wave] = kt;
+        red.k[1][wave] = kf;
+        red.u[1][wave] = nc;
+        red.u[2][wave] = nt;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      uint64_t kt = red.k[0][0], kf = red.k[1][0];
+      nC = red.u[1][0];
+      nT = red.u[2][0];
+      for (int w = 1; w < kWaves; ++w) {
+        kt = red.k[0][w] < kt ? red.k[0][w] : kt;
+        kf = red.k[1][w] < kf ? red.k[1][w] : kf;
+        nC += red.u[1][w];
+        nT += red.u[2][w];
+      }
+      ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+      // With finite arithmetic C holds at least the minimum-penalty
+      // candidate whenever A is non-empty; the second test only keeps a
+      // non-finite model from selecting an out-of-range id.
+      if (nA > 0 && (kt != ~0ull || kf != ~0ull)) {
+        uint32_t fl = 0;
+        uint32_t best;
+        if (kt != ~0ull) {
+          best = (uint32_t)(kt & 0xFFFFu);
+        } else {
+          best = (uint32_t)(kf & 0xFFFFu);
+          fl |= PS_R_FALLBACK;
+        }
+        const uint32_t v = hits[best];
+        const int64_t c_tok = (int64_t)v * m.bs;
+        const InstState st = a.inst[best];
+        const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
+        if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
+        res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot, fl};
+      }
+      a.out[r] = res;
+      if (a.sizes) {
+        a.sizes[3 * (size_t)r] = nA;
+        a.sizes[3 * (size_t)r + 1] = nC;
+        a.sizes[3 * (size_t)r + 2] = nT;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ int32_t segment_of(const DevModel& m, int32_t B) {
+  for (int32_t s = 0; s < m.n_seg; ++s)
+    if (B <= m.seg_ub[s]) return s;
+  return m.n_seg - 1;
+}
+
+// One wave per instance that receives placements; its entries are applied
+// in array order, each measured against the table as the earlier entries
+// left it.
+__global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
+  const int32_t g = blockIdx.x;
+  const int lane = threadIdx.x;
+  const uint32_t inst = (uint32_t)a.grp_inst[g];
+  const DevModel& m = *a.model;
+  InstState st = a.inst[inst];
+  uint32_t count = a.t.count[inst];
+  unsigned long long dropped = 0;
+  for (int32_t k = a.grp_off[g]; k < a.grp_off[g + 1]; ++k) {
+    const ps_req q = a.reqs[a.order[k]];
+    const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
+    const int32_t ell = c.len;
+    const int64_t L = (int64_t)ell * m.bs;
+    const uint32_t h = deep_walk<false>(a.t, inst, c, nullptr, 0, lane);
+    st.Q += 1;
+    st.A1 += 1;
+    st.P += L - (int64_t)h * m.bs;
+    st.S += L;
+    for (int32_t base = 0; base < ell; base += 64) {
+      const int32_t j = base + lane;
+      const bool in = j < ell;
+      const uint64_t key = in ? chain_global(c, j) : 0ull;
+      const bool present = in ? probe(a.t, inst, key) : true;
+      // repeated keys inside this chunk: only the first occurrence counts
+      int first = lane;
+      for (int s = 63; s >= 0; --s) {
+        const uint64_t o = __shfl(key, s);
+        if (s < lane && o == key) first = s;
+      }
+      const bool dup = first != lane;
+      const bool want = in && !present && !dup;
+      const uint64_t wm = __ballot(want);
+      const uint32_t rank = (uint32_t)__popcll(wm & ((1ull << lane) - 1ull));
+      const uint32_t room = a.cap > count ? a.cap - count : 0u;
+      const bool ins = want && rank < room;
+      if (ins) (void)insert_key(a.t, inst, key);
+      const uint64_t im = __ballot(ins);
+      const uint64_t dup_drop = __ballot(in && dup && !present && !((im >> first) & 1ull));
+      const uint32_t nins = (uint32_t)__popcll(im);
+      count += nins;
+      dropped += (unsigned long long)(__popcll(wm) - nins + __popcll(dup_drop));
+      __threadfence();  // later probes of this wave must see these inserts
+    }
+  }
+  st.seg = segment_of(m, st.A1);
+  if (lane == 0) {
+    a.inst[inst] = st;
+    a.t.count[inst] = count;
+    if (dropped) atomicAdd(a.dropped, dropped);
+  }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ launchers
+size_t ps_score_lds_bytes(int32_t n_inst) {
+  return (size_t)kStage * sizeof(uint64_t) + (size_t)n_inst * sizeof(uint32_t);
+}
+
+hipError_t ps_launch_build(const BuildArgs& a, hipStream_t s) {
+  if (a.n_blk == 0) return hipSuccess;
+  int64_t blocks = (a.n_blk + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(build_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
+                           hipStream_t s) {
+  if (a.n_req == 0) return hipSuccess;
+  const size_t lds = hits_in_lds ? ps_score_lds_bytes(a.n_inst) : (size_t)kStage * sizeof(uint64_t);
+  if (hits_in_lds) {
+    if (probe_all)
+      hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(kBlock), lds, s, a);
+    else
+      hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(kBlock), lds, s, a);
+  } else {
+    if (probe_all)
+      hipLaunchKernelGGL((score_kernel<false, true>), dim3(grid), dim3(kBlock), lds, s, a);
+    else
+      hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(kBlock), lds, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t ps_launch_commit(const CommitArgs& a, hipStream_t s) {
+  if (a.n_grp == 0) return hipSuccess;
+  hipLaunchKernelGGL(commit_kernel, dim3(a.n_grp), dim3(64), 0, s, a);
+  return hipGetLastError();
+}

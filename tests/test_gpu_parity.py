@@ -1,0 +1,332 @@
+"""GPU <-> oracle parity through the C ABI (needs an MI355X).
+
+Bar: prefix hits and chosen instances bit-exact; flags and |A|, |C|, |T|
+exact; predicted TTFT/TPOT within 1e-5 relative (fp32 vs fp64); decisions
+whose oracle comparison lies within 1e-5 relative of a boundary are counted
+and excluded from the exact check.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import DeviceWindow, compare_decisions, gpu_model, load_window, reqs_of
+from tests.tinywin import chain_hashes, make_window
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ps():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_33224_amd as ps
+    return ps
+
+
+@pytest.fixture()
+def scorer(ps):
+    s = ps.Scorer(0)
+    yield s
+    s.close()
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+# ------------------------------------------------------------- small windows
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_hits_bit_exact_full_window(ps, scorer, name):
+    _say(f"hits parity {name}")
+    w = synth.generate(name)
+    load_window(scorer, w)
+    dw = DeviceWindow(w)
+    got = dw.hits(scorer, w.n_inst)
+    want = oracle.Oracle.from_window(w).window_hits(w)
+    bad = np.argwhere(got != want)
+    assert len(bad) == 0, f"{len(bad)} hits differ, first {bad[0]}: {got[tuple(bad[0])]} vs {want[tuple(bad[0])]}"
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c2_50"])
+def test_decisions_full_window(ps, scorer, name):
+    _say(f"decision parity {name}")
+    w = synth.generate(name)
+    load_window(scorer, w)
+    res, sizes = DeviceWindow(w).score(scorer)
+    od = oracle.Oracle.from_window(w).window_score(w)
+    nb = compare_decisions(res, sizes, od, label=name)
+    _say(f"{name}: {w.n_req} decisions, {nb} near-boundary excluded")
+    assert nb <= max(5, w.n_req // 200)
+
+
+def test_host_entry_point_matches_device(ps, scorer):
+    w = synth.generate("c1")
+    load_window(scorer, w)
+    a = scorer.score(w.pool, reqs_of(w))
+    b, _ = DeviceWindow(w).score(scorer)
+    assert a.tobytes() == b.tobytes()
+
+
+def test_deterministic(ps, scorer):
+    w = synth.generate("c2", n_req=4096)
+    load_window(scorer, w)
+    dw = DeviceWindow(w)
+    a, sa = dw.score(scorer)
+    b, sb = dw.score(scorer)
+    assert a.tobytes() == b.tobytes() and (sa == sb).all()
+
+
+@pytest.mark.parametrize("policy", [dict(eta=0.0), dict(eta=1.0), dict(eta=0.25),
+                                    dict(tpot_slo=1e-6), dict(tpot_slo=10.0),
+                                    dict(flags=1), dict(flags=2), dict(flags=4), dict(flags=7),
+                                    dict(b_max=1), dict(kv_cap_tokens=0)])
+def test_policy_variants(ps, scorer, policy):
+    _say(f"policy {policy}")
+    w = synth.generate("c1")
+    load_window(scorer, w, **policy)
+    res, sizes = DeviceWindow(w).score(scorer)
+    od = oracle.Oracle.from_window(w).window_score(w, **policy)
+    compare_decisions(res, sizes, od, label=str(policy))
+    if policy.get("b_max") == 1 or policy.get("kv_cap_tokens") == 0:
+        assert (res["instance"] == -1).all() and (res["flags"] == ps.PS_R_REJECT).all()
+    if policy.get("tpot_slo") == 1e-6:
+        assert ((res["flags"] & ps.PS_R_FALLBACK) != 0).all()
+
+
+# ------------------------------------------------------------- edge windows
+ALPHA = [0.02, 1e-4, 1.5e-9, 7.5e-10, 1e-7, 1e-14]
+SEG_UB, BETA, GAMMA = (8, 64, 512), ((0.01, 1e-4, 1e-8),) * 3, (1.0, 1.1, 1.2)
+
+
+def _edge(sets, chains, n=None, **kw):
+    n = len(sets)
+    rng = np.random.default_rng(len(sets) * 7 + len(chains))
+    D = kw.pop("D", rng.integers(0, 64, n))
+    Q = kw.pop("Q", rng.integers(0, 4, n))
+    P = kw.pop("P", rng.integers(0, 8192, n) * (np.asarray(Q) > 0))
+    S = kw.pop("S", rng.integers(0, 500_000, n))
+    cap = kw.pop("cap", max(max((len(s) for s in sets), default=1), 1))
+    kw.setdefault("tpot_slo", 0.05)
+    kw.setdefault("b_max", 512)
+    kw.setdefault("kv_cap_tokens", 4_194_304)
+    return make_window(sets, chains, D, Q, P, S, ALPHA, SEG_UB, BETA, GAMMA, cap=cap, **kw)
+
+
+def _check_edge(ps, scorer, w, label, **policy):
+    w.alpha = np.asarray(w.alpha, np.float32)
+    w.beta = np.asarray(w.beta, np.float32)
+    w.gamma = np.asarray(w.gamma, np.float32)
+    load_window(scorer, w, **policy)
+    dw = DeviceWindow(w)
+    got = dw.hits(scorer, w.n_inst)
+    o = oracle.Oracle.from_window(w)
+    want = o.window_hits(w)
+    assert (got == want).all(), f"{label}: hits differ at {np.argwhere(got != want)[:3]}"
+    res, sizes = dw.score(scorer)
+    od = o.window_score(w, **policy)
+    compare_decisions(res, sizes, od, label=label)
+    return res
+
+
+def test_edge_single_instance_and_ragged_counts(ps, scorer):
+    for n_inst in (1, 63, 100, 257, 1000):
+        ch = chain_hashes(300, base=17)
+        rng = np.random.default_rng(n_inst)
+        sets = [ch[:int(rng.integers(0, 300))] for _ in range(n_inst)]
+        chains = [ch[:k] for k in (1, 2, 65, 150, 300)] + [(ch[:100], chain_hashes(5, base=10**9))]
+        _check_edge(ps, scorer, _edge(sets, chains), f"n_inst={n_inst}")
+
+
+def test_edge_chain_lengths_around_stage(ps, scorer):
+    ch = chain_hashes(5000, base=99)
+    sets = [ch[:h] for h in (0, 1, 63, 64, 65, 1023, 1024, 1025, 2047, 4999, 5000)]
+    chains = [ch[:k] for k in (1, 64, 1023, 1024, 1025, 2048, 5000)]
+    # also split descriptors whose boundary falls inside the staged head
+    chains += [(ch[:700], ch[700:3000]), (ch[:1], ch[1:1500])]
+    _check_edge(ps, scorer, _edge(sets, chains), "stage")
+
+
+def test_edge_fully_cached_and_empty_chain(ps, scorer):
+    ch = chain_hashes(40, base=5)
+    sets = [ch, ch[:20], []]
+    res = _check_edge(ps, scorer, _edge(sets, [ch, [], ch[:1]]), "full/empty")
+    assert res["hit_blocks"][0] in (40, 20, 0)
+
+
+def test_edge_duplicates_and_non_prefix_closed(ps, scorer):
+    ch = chain_hashes(200, base=3)
+    other = chain_hashes(50, base=7 * 10**6)
+    sets = [ch[:50] + ch[:50] + other,          # duplicates in the CSR row
+            ch[1:150],                          # misses the first block
+            ch[:10] + ch[11:200],               # hole at block 10
+            ch[:100][::-1]]                     # order irrelevant
+    _check_edge(ps, scorer, _edge(sets, [ch, ch[:120], other]), "dups/holes", )
+
+
+def test_edge_zero_cache_benefit_and_eta(ps, scorer):
+    ch = chain_hashes(64, base=11)
+    sets = [ch[:h] for h in (0, 10, 20, 40, 64)]
+    w = _edge(sets, [ch, ch[:32]])
+    w.alpha = [0.02, 0.0, 1e-6, 0.0, 0.0, 0.0]   # Z = 0: all of A is kept
+    _check_edge(ps, scorer, w, "Z=0", eta=0.0)
+    for eta in (0.0, 0.3, 1.0):
+        _check_edge(ps, scorer, _edge(sets, [ch, ch[:32]]), f"eta={eta}", eta=eta)
+
+
+def test_edge_large_instance_count_uses_scratch(ps, scorer):
+    n_inst = 20000
+    ch = chain_hashes(128, base=23)
+    rng = np.random.default_rng(1)
+    sets = [ch[:int(h)] for h in rng.integers(0, 129, n_inst)]
+    w = _edge(sets, [ch, ch[:64], ch[:1]], cap=128)
+    res = _check_edge(ps, scorer, w, "n_inst=20000")
+    assert not scorer.table_info()["hits_in_lds"]
+
+
+def test_invalid_descriptor_flagged_on_device(ps, scorer):
+    import torch
+    w = synth.generate("c1", n_req=8)
+    load_window(scorer, w)
+    reqs = reqs_of(w)
+    reqs["pre_off"][3] = len(w.pool) + 5
+    reqs["tail_len"][5] = -1
+    d_pool = ps.to_device_u64(w.pool)
+    d_reqs = ps.to_device_bytes(reqs)
+    d_out = torch.zeros(8 * 20, dtype=torch.uint8, device="cuda")
+    scorer.score_dev(d_pool, len(w.pool), d_reqs, 8, d_out)
+    torch.cuda.synchronize()
+    res = ps.results_from_device(d_out)
+    assert res["flags"][3] == ps.PS_R_INVALID and res["instance"][3] == -1
+    assert res["flags"][5] == ps.PS_R_INVALID
+    assert (res["flags"][[0, 1, 2, 4, 6, 7]] & ps.PS_R_INVALID == 0).all()
+
+
+# ------------------------------------------------------------- commit
+@pytest.mark.parametrize("name,n_req,cap", [("c1", 1024, None), ("c2", 2048, None),
+                                            ("c1", 1024, 1100)])
+def test_commit_sequence(ps, scorer, name, n_req, cap):
+    """Score window 1, apply the oracle's decisions on both sides, compare
+    the state, then score window 2 against the updated snapshot."""
+    _say(f"commit {name} cap={cap}")
+    gen = dict(n_req=n_req)
+    if cap:
+        gen["cap"] = cap
+    w = synth.generate(name, **gen)
+    load_window(scorer, w)
+    o = oracle.Oracle.from_window(w)
+    od = o.window_score(w)
+    dropped_o = o.commit(w.pool, w.pre_off, w.pre_len, w.tail_off, w.tail_len, od.inst)
+    dropped_g = scorer.commit(w.pool, reqs_of(w), od.inst)
+    so, sg = o.state(), scorer.state()
+    for k in ("D", "Q", "P", "S", "set_size"):
+        assert (so[k] == sg[k]).all(), f"{k} differs after commit"
+    assert dropped_o == dropped_g
+    if cap:
+        assert dropped_o > 0
+    w2 = synth.generate(name, seed=1, **gen)
+    # same instances and model as the loaded snapshot; only the requests are new
+    w2.blk_off, w2.blk = w.blk_off, w.blk
+    w2.alpha, w2.beta, w2.gamma = w.alpha, w.beta, w.gamma
+    w2.pool = np.concatenate([w.pool, w2.pool])
+    off = len(w.pool)
+    w2.pre_off = w2.pre_off + off
+    w2.tail_off = w2.tail_off + off
+    # half of window 2 repeats window-1 requests (now cached on their instance)
+    w2.pre_off[::2] = w.pre_off[::2]
+    w2.pre_len[::2] = w.pre_len[::2]
+    w2.tail_off[::2] = w.tail_off[::2]
+    w2.tail_len[::2] = w.tail_len[::2]
+    res, sizes = DeviceWindow(w2).score(scorer)
+    od2 = o.window_score(w2)
+    compare_decisions(res, sizes, od2, label=f"{name} after commit")
+
+
+# ------------------------------------------------------------- ABI errors
+def test_abi_errors(ps, scorer):
+    w = synth.generate("c1", n_req=4)
+    reqs = reqs_of(w)
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.score(w.pool, reqs)
+    assert e.value.code == -4
+    m = gpu_model(w)
+    bad_blk = w.blk.copy()
+    bad_blk[3] = 0
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.load(w.n_inst, w.cap, w.blk_off, bad_blk, w.D, w.Q, w.P, w.S, m)
+    assert e.value.code == -1
+    D = w.D.copy()
+    D[0] = 4096
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.load(w.n_inst, w.cap, w.blk_off, w.blk, D, w.Q, w.P, w.S, m)
+    assert e.value.code == -5
+    m2 = gpu_model(w)
+    m2.seg_ub[2] = m2.seg_ub[1]
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.load(w.n_inst, w.cap, w.blk_off, w.blk, w.D, w.Q, w.P, w.S, m2)
+    assert e.value.code == -1
+    m3 = gpu_model(w, eta=-0.1)
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.load(w.n_inst, w.cap, w.blk_off, w.blk, w.D, w.Q, w.P, w.S, m3)
+    assert e.value.code == -1
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.load(w.n_inst, 3, w.blk_off, w.blk, w.D, w.Q, w.P, w.S, m)
+    assert e.value.code == -5
+    # a good load, then a failing one: the first snapshot stays in force
+    scorer.load(w.n_inst, w.cap, w.blk_off, w.blk, w.D, w.Q, w.P, w.S, m)
+    a = scorer.score(w.pool, reqs)
+    with pytest.raises(ps.PackServeError):
+        scorer.load(w.n_inst, w.cap, w.blk_off, bad_blk, w.D, w.Q, w.P, w.S, m)
+    assert scorer.score(w.pool, reqs).tobytes() == a.tobytes()
+    r2 = reqs.copy()
+    r2["pre_off"][0] = len(w.pool)
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.score(w.pool, r2)
+    assert e.value.code == -5
+    p2 = w.pool.copy()
+    p2[0] = 0
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.score(p2, reqs)
+    assert e.value.code == -1
+    big = np.full((1 << 23) + 1, 7, np.uint64)
+    r3 = ps.pack_reqs([0], [(1 << 23) + 1], [0], [1 << 23])
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.score(big, r3)
+    assert e.value.code == -5
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.commit(w.pool, reqs, np.array([0, 1, w.n_inst, 0], np.int32))
+    assert e.value.code == -5
+    assert len(scorer.score(w.pool, reqs[:0])) == 0
+
+
+# ------------------------------------------------------------- full-size windows
+@pytest.mark.parametrize("name", ["c3", "c4", "c5"])
+def test_full_size_sampled(ps, scorer, name):
+    """Full window on the GPU in the benchmark's launch configuration; the
+    oracle recomputes a seeded sample of requests one by one."""
+    _say(f"full-size {name}: generating")
+    w = synth.generate(name)
+    _say(f"full-size {name}: loading")
+    load_window(scorer, w)
+    dw = DeviceWindow(w)
+    res, sizes = dw.score(scorer)
+    _say(f"full-size {name}: scored {w.n_req}; oracle sample")
+    idx = np.sort(np.random.default_rng(5).choice(w.n_req, 384, replace=False))
+    idx = np.unique(np.concatenate([idx, [0, w.n_req - 1]]))
+    sub = w.subset(idx)
+    o = oracle.Oracle.from_window(w)
+    od = o.window_score(sub)
+    nb = compare_decisions(res, sizes, od, idx=idx, label=name)
+    _say(f"full-size {name}: sample ok, {nb} near-boundary")
+    got = DeviceWindow(sub).hits(scorer, w.n_inst)
+    want = o.window_hits(sub)
+    assert (got == want).all(), f"{name}: sampled hits differ"
+    # whole-window properties
+    assert ((res["instance"] >= -1) & (res["instance"] < w.n_inst)).all()
+    ell = w.pre_len + w.tail_len
+    assert (res["hit_blocks"] <= ell).all()
+    assert (sizes[:, 2] <= sizes[:, 1]).all() and (sizes[:, 1] <= sizes[:, 0]).all()
