@@ -1,0 +1,219 @@
+"""Benchmark of the PackServe window scorer on one MI355X.
+
+A step is one call of ps_score_window_dev over the whole window (prefix
+match, latency model, filters and selection for every request x instance
+pair), inputs resident in HBM.  Default workload: the 64-instance x 16,384-
+request window with a 30 ms TPOT target (c2).  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload c2] [--no-cpu-baseline]
+
+The roofline block counts the algorithmic bytes of a launch: one 64-byte
+bucket per probe, min(hit + 1, chain length) probes per capacity-eligible
+(request, instance) pair, plus the request chain read up to the deepest
+probe, 24 bytes of descriptor and 24 of instance state per request /
+instance, and 20 bytes of result per request.  `traffic` comes from the
+committed rocprofv3 counter summary of the same kernel source, or is null.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("request×instance candidate evals/sec + decisions/sec; "
+          "probe-kernel % of HBM peak")
+HBM_PEAK_GBS = 8000.0
+BUCKET_BYTES = 64
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_33224_amd", "csrc", "ps_kernels.hip")
+
+WORKLOAD_NAMES = {
+    "c1": "16 instances x 1,024 requests, TPOT 50 ms",
+    "c2": "64 instances x 16,384 requests, session prefixes 512-4,096 blocks, owner Zipf(1.1), TPOT 30 ms",
+    "c2_50": "64 instances x 16,384 requests, session prefixes 512-4,096 blocks, owner Zipf(1.1), TPOT 50 ms",
+    "c3": "1,024 instances x 65,536 requests, 40% share a 128-block system prompt, TPOT 30 ms",
+    "c4": "256 instances x 32,768 requests, prefixes 2,048-12,500 blocks, 85% saturated, TPOT 50 ms",
+    "c5": "4,096 instances x 262,144 requests, uniform scatter, TPOT 30 ms",
+}
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        h = hashlib.sha256(f.read())
+    with open(os.path.join(ROOT, "paper_2609_33224_amd", "csrc", "ps_device.h"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(win, hits):
+    """Bytes one launch must move at minimum (see module docstring)."""
+    import numpy as np
+    ell = (win.pre_len.astype(np.int64) + win.tail_len)
+    L = ell * int(win.policy["block_tokens"])
+    A1 = win.D.astype(np.int64) + win.Q + 1
+    elig = (A1[None, :] <= int(win.policy["b_max"])) & \
+           ((win.S[None, :] + L[:, None]) <= int(win.policy["kv_cap_tokens"]))
+    probes = np.minimum(hits.astype(np.int64) + 1, ell[:, None])
+    probes = np.where(ell[:, None] == 0, 0, probes)
+    n_probes = int((probes * elig).sum())
+    deepest = np.where(elig.any(axis=1), (probes * elig).max(axis=1), 0)
+    chain_bytes = int(deepest.sum()) * 8
+    other = win.n_req * (24 + 20) + win.n_inst * 24
+    return n_probes * BUCKET_BYTES + chain_bytes + other, n_probes
+
+
+def traffic_for(workload: str, src_hash: str):
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = t.get(workload)
+    if not ent or ent.get("kernel_source_sha") != src_hash:
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(win, budget_s: float):
+    """The oracle on the host cores, over the same window, repeated (or on a
+    leading slice) to fill roughly `budget_s` seconds."""
+    import oracle
+    o = oracle.Oracle.from_window(win)
+    threads = oracle.max_threads()
+    t0 = time.perf_counter()
+    o.window_score(win)
+    one = time.perf_counter() - t0
+    if one > budget_s:
+        n = max(64, int(win.n_req * budget_s / one))
+        sub = win.subset(range(n))
+        t0 = time.perf_counter()
+        o.window_score(sub)
+        dt = time.perf_counter() - t0
+        return dict(value=n * win.n_inst / dt, unit="candidate evals/s", cores=threads,
+                    kind="oracle", decisions_per_s=n / dt,
+                    sample=f"first {n} of {win.n_req} requests of the window, once")
+    reps = max(1, int(budget_s / max(one, 1e-3)))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        o.window_score(win)
+    dt = (time.perf_counter() - t0) / reps
+    return dict(value=win.n_req * win.n_inst / dt, unit="candidate evals/s", cores=threads,
+                kind="oracle", decisions_per_s=win.n_req / dt,
+                sample=f"whole window ({win.n_req} requests x {win.n_inst} instances), "
+                       f"{reps} repetitions")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the request-sharded multi-GPU design is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    import paper_2609_33224_amd as ps
+
+    print(f"bench: generating {args.workload}", file=sys.stderr, flush=True)
+    win = synth.generate(args.workload, seed=args.seed)
+    sc = ps.Scorer(0)
+    m = ps.make_model(win.alpha, win.seg_ub, win.beta, win.gamma, win.policy["eta"],
+                      win.policy["tpot_slo"], win.policy["ttft_floor"], win.policy["lout"],
+                      win.policy["block_tokens"], win.policy["b_max"],
+                      win.policy["kv_cap_tokens"], win.policy["flags"])
+    t0 = time.perf_counter()
+    sc.load(win.n_inst, win.cap, win.blk_off, win.blk, win.D, win.Q, win.P, win.S, m)
+    load_s = time.perf_counter() - t0
+    reqs = ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
+    d_pool = ps.to_device_u64(win.pool)
+    d_reqs = ps.to_device_bytes(reqs)
+    d_out = torch.empty(win.n_req * 20, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    # untimed: per-pair hits for the byte count, and the end-to-end host call
+    d_hits = torch.empty(win.n_req * win.n_inst, dtype=torch.int32, device="cuda")
+    sc.hits_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_hits)
+    torch.cuda.synchronize()
+    hits = d_hits.cpu().numpy().view(np.uint32).reshape(win.n_req, win.n_inst)
+    del d_hits
+    alg_bytes, n_probes = algorithmic_bytes(win, hits)
+    t0 = time.perf_counter()
+    sc.score(win.pool, reqs)
+    host_call_s = time.perf_counter() - t0
+
+    for _ in range(args.warmup):
+        sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    print(f"bench: timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = wall * 1e3 / args.steps
+    kern_avg = float(np.mean(kern_ms))
+    res = ps.results_from_device(d_out)
+
+    evals = win.n_req * win.n_inst
+    src_hash = kernel_source_hash()
+    traffic = traffic_for(args.workload, src_hash)
+    achieved = alg_bytes / (kern_avg * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": evals / (ms_per_step * 1e-3),
+        "unit": "candidate evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {WORKLOAD_NAMES[args.workload]}",
+                   "n_inst": win.n_inst, "n_req": win.n_req, "seed": args.seed},
+        "decisions_per_s": win.n_req / (ms_per_step * 1e-3),
+        "kernel_ms_avg": kern_avg,
+        "kernel_ms_min": float(np.min(kern_ms)),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+        "algorithmic_bytes_per_launch": alg_bytes,
+        "probes_per_launch": n_probes,
+        "kernel_source_sha": src_hash,
+        "load_instances_s": load_s,
+        "host_call_s_incl_pcie": host_call_s,
+        "placed": int((res["instance"] >= 0).sum()),
+        "fallback": int(((res["flags"] & ps.PS_R_FALLBACK) != 0).sum()),
+    }
+    sc.close()
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(win, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -20,11 +20,9 @@ namespace {
 
 thread_local std::string g_create_error;
 
-// Largest dynamic LDS the scoring kernel asks for per workgroup; above it
-// the per-candidate hit rows live in device scratch instead.
-constexpr size_t kLdsBudget = 64 * 1024;
-// Workgroups of the persistent scoring grid when hit rows are in scratch.
-constexpr int kScratchRowsPerCU = 4;
+// Waves of the persistent scoring grid (per CU) when hit rows live in
+// device scratch instead of LDS.
+constexpr int kScratchRowsPerCU = 16;
 
 }  // namespace
 
@@ -39,9 +37,10 @@ struct ps_ctx {
   int32_t cap = 0;
   Tables t{};
   InstState* d_inst = nullptr;
+  int64_t* d_room = nullptr;
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
-  uint32_t* d_scratch = nullptr;
+  uint16_t* d_scratch = nullptr;
   int scratch_rows = 0;
   bool hits_in_lds = true;
   std::vector<InstState> h_state;
@@ -191,6 +190,7 @@ void free_snapshot(ps_ctx* c) {
   dfree(c->t.keys);
   dfree(c->t.count);
   dfree(c->d_inst);
+  dfree(c->d_room);
   dfree(c->d_scratch);
   c->loaded = false;
 }
@@ -289,7 +289,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.t.bmask = (uint32_t)(buckets - 1);
   fresh.t.shift = (uint32_t)(64 - log2b);
   const size_t tab_bytes = (size_t)n * (size_t)slots * sizeof(uint64_t);
-  const bool lds = ps_score_lds_bytes(n) <= kLdsBudget;
+  const bool lds = ps_hits_fit_lds(n);
   const int rows = lds ? 0 : std::max(1, c->num_cus * kScratchRowsPerCU);
   int64_t* d_off = nullptr;
   uint64_t* d_blk = nullptr;
@@ -297,6 +297,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     dfree(fresh.t.keys);
     dfree(fresh.t.count);
     dfree(fresh.d_inst);
+    dfree(fresh.d_room);
     dfree(fresh.d_scratch);
     dfree(d_off);
     dfree(d_blk);
@@ -304,8 +305,9 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   hipError_t e = hipMalloc((void**)&fresh.t.keys, tab_bytes);
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.t.count, (size_t)n * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst, (size_t)n * sizeof(InstState));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess && rows)
-    e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint32_t));
+    e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint16_t));
   if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
   if (e == hipSuccess && n_blk) e = hipMalloc((void**)&d_blk, (size_t)n_blk * sizeof(uint64_t));
   if (e != hipSuccess) {
@@ -314,6 +316,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
                 "allocating %.1f MiB of tables: %s", tab_bytes / 1048576.0, hipGetErrorString(e));
   }
   std::vector<InstState> hs((size_t)n);
+  std::vector<int64_t> hroom((size_t)n);
   for (int32_t i = 0; i < n; ++i) {
     InstState& s = hs[(size_t)i];
     s.D = in->decoding[i];
@@ -322,6 +325,8 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     s.seg = segment_of_host(*m, s.A1);
     s.P = in->pending_tok[i];
     s.S = in->ctx_tok[i];
+    // capacity guard A_i + 1 <= B_max and S_i + L <= M_KV as one comparison L <= room
+    hroom[(size_t)i] = s.A1 <= m->b_max ? m->kv_cap_tokens - s.S : -1;
   }
   const DevModel dm = device_model(*m);
   hipStream_t sm = c->stream;
@@ -334,6 +339,8 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     e = hipMemcpyAsync(d_blk, in->blk, (size_t)n_blk * sizeof(uint64_t), hipMemcpyHostToDevice, sm);
   if (e == hipSuccess)
     e = hipMemcpyAsync(fresh.d_inst, hs.data(), hs.size() * sizeof(InstState), hipMemcpyHostToDevice, sm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(fresh.d_room, hroom.data(), hroom.size() * sizeof(int64_t), hipMemcpyHostToDevice, sm);
   if (e == hipSuccess) {
     BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter};
     e = ps_launch_build(ba, sm);
@@ -366,6 +373,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   free_snapshot(c);
   c->t = fresh.t;
   c->d_inst = fresh.d_inst;
+  c->d_room = fresh.d_room;
   c->d_scratch = fresh.d_scratch;
   c->scratch_rows = rows;
   c->hits_in_lds = lds;
@@ -378,6 +386,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.t.keys = nullptr;
   fresh.t.count = nullptr;
   fresh.d_inst = nullptr;
+  fresh.d_room = nullptr;
   fresh.d_scratch = nullptr;
   return PS_OK;
 }
@@ -388,6 +397,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   ScoreArgs a{};
   a.t = c->t;
   a.inst = c->d_inst;
+  a.room = c->d_room;
   a.model = c->d_model;
   a.pool = d_pool;
   a.pool_len = pool_len;
@@ -521,7 +531,7 @@ ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_
   HIP_TRY(c, hipMemcpyAsync(d_grp_off, grp_off.data(), grp_off.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
   HIP_TRY(c, hipMemcpyAsync(d_grp_inst, grp_inst.data(), n_grp * sizeof(int32_t), hipMemcpyHostToDevice, s));
   HIP_TRY(c, hipMemsetAsync(c->d_counter, 0, sizeof(unsigned long long), s));
-  CommitArgs ca{c->t, c->d_inst, c->d_model, (const uint64_t*)dp, (const ps_req*)dr,
+  CommitArgs ca{c->t, c->d_inst, c->d_room, c->d_model, (const uint64_t*)dp, (const ps_req*)dr,
                 d_order, d_grp_off, d_grp_inst, (int32_t)n_grp, (uint32_t)c->cap, c->d_counter};
   HIP_TRY(c, ps_launch_commit(ca, s));
   unsigned long long dropped = 0;

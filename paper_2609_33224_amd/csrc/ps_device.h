@@ -10,14 +10,17 @@
 
 namespace ps {
 
-constexpr int kBlock = 256;            // threads per scoring workgroup (4 waves)
-constexpr int kWaves = kBlock / 64;
-constexpr int kStage = 1024;           // chain blocks staged in LDS per request
+constexpr int kStage = 256;            // chain blocks staged in LDS per request (2 KiB)
 constexpr int kSlotsPerBucket = 8;     // 8 x 64-bit keys = one 64-byte bucket
-constexpr uint32_t kInelig = 0xFFFFFFFFu;  // hit slot of a capacity-ineligible instance
-constexpr uint32_t kCont = 0x80000000u;    // hit slot flag: walk continues past the breadth probe
-constexpr int kBreadthRounds = 8;      // octet loads in flight per lane in the breadth probe
-constexpr int kDeepRounds = 16;        // octet loads in flight per lane in a deep walk step
+constexpr int kBreadthRounds = 8;      // octet loads per lane in flight: 64 instances per step
+constexpr int kDeepRounds = 8;         // octet loads per lane in flight: 64 positions per step
+// Per-candidate hit slots (u16 in LDS): exact hits up to kHitMax, then two
+// markers.
+constexpr uint32_t kHitMax = 0xFFFDu;
+constexpr uint32_t kHitOverflow = 0xFFFEu;  // hit > kHitMax: recomputed where needed
+constexpr uint32_t kInelig = 0xFFFFu;       // not capacity-eligible
+// Per-wave dynamic LDS above which hit slots move to device scratch.
+constexpr size_t kLdsHitBudget = 16 * 1024;
 
 // Per-instance load state, 32 bytes (one pair of 16-byte loads).
 struct alignas(16) InstState {
@@ -65,6 +68,7 @@ __host__ __device__ __forceinline__ uint32_t bucket_of(uint64_t key, uint32_t in
 struct ScoreArgs {
   Tables t;
   const InstState* inst;
+  const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
   const DevModel* model;
   const uint64_t* pool;
   int64_t pool_len;
@@ -74,12 +78,13 @@ struct ScoreArgs {
   ps_result* out;
   uint32_t* sizes;       // optional |A|,|C|,|T| per request
   uint32_t* hits_out;    // probe-all diagnostic: n_req * n_inst
-  uint32_t* scratch;     // per-workgroup hit rows when they do not fit LDS
+  uint16_t* scratch;     // per-wave hit rows when they do not fit LDS
 };
 
 struct CommitArgs {
   Tables t;
   InstState* inst;
+  int64_t* room;
   const DevModel* model;
   const uint64_t* pool;
   const ps_req* reqs;
@@ -106,5 +111,6 @@ struct BuildArgs {
 hipError_t ps_launch_build(const ps::BuildArgs& a, hipStream_t s);
 hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s);
+bool ps_hits_fit_lds(int32_t n_inst);
 hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
 size_t ps_score_lds_bytes(int32_t n_inst);

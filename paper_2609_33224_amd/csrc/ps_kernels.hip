@@ -2,19 +2,19 @@
 //
 //   build_kernel   - per-instance open-addressing tables from the CSR block
 //                    lists (64-bit atomicCAS inserts).
-//   score_kernel   - the fused hot path, one workgroup per request:
+//   score_kernel   - the fused hot path, one wave per request (no barriers):
 //                      (1) longest cached prefix of the request's block-hash
-//                          chain on every capacity-eligible instance (a breadth
-//                          probe of the first block with lanes over instances,
-//                          then a deep walk with lanes over chain positions and
-//                          a ballot for the first miss; the chain's head is
-//                          staged in LDS),
+//                          chain on every capacity-eligible instance: a breadth
+//                          probe of the first block, octets of lanes over
+//                          instances, then for each instance holding it a deep
+//                          walk, octets over chain positions, stopping at the
+//                          first absent block (ballot + count-trailing-zeros);
+//                          the chain head is staged in LDS,
 //                      (2) the latency model (Eq. 7 + C, C^2 terms; Eq. 8 per
 //                          segment with its EMA factor; Eq. 10; Eq. 4),
 //                      (3) capacity, recomputation (Eq. 9) and TPOT filters,
 //                      (4) the packed D-C-Q key and the LMetric fallback key,
-//                          reduced with DPP wave minima and an LDS cross-wave
-//                          step.
+//                          reduced with DPP wave minima.
 //   commit_kernel  - ordered placement of decisions, one wave per instance.
 //
 // The path is bound by HBM (random 64-byte bucket reads); it does no dense
@@ -69,11 +69,6 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
   add_step<0x143, 0xC>(v);
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
-
-struct Red {
-  uint64_t k[2][kWaves];
-  uint32_t u[3][kWaves];
-};
 
 // ------------------------------------------------------------------- probing
 // Octet probing: the 8 lanes of an octet (lanes 8g .. 8g+7) read the 8 slots
@@ -187,43 +182,51 @@ __device__ __forceinline__ bool req_valid(const ps_req& q, int64_t pool_len) {
          (int64_t)q.pre_len + (int64_t)q.tail_len <= (int64_t)PS_MAX_CHAIN;
 }
 
-// Deep walk of one instance: octets over chain positions.  One step issues
-// kDeepRounds x 8 positions (or half of that on the first step) before any
-// is evaluated, then stops at the first absent position in chain order.
+// Deep walk of one instance: octets over chain positions.  A step issues
+// the bucket reads of kDeepRounds x 8 positions, then prefetches the next
+// step's chain hashes, then evaluates in chain order and stops at the first
+// absent position.  Positions below kStage read the LDS copy of the chain.
 // Wave-uniform arguments; returns the hit.
 template <bool STAGED>
 __device__ uint32_t deep_walk(const Tables& t, uint32_t inst, const ChainRef& c,
-                              const uint64_t* stage, int32_t pos, int lane) {
-  const int g = lane >> 3, s = lane & 7;
+                              const uint64_t* stage, int32_t pos, int g, int s) {
   const int32_t ell = c.len;
   const uint64_t* tab = table_of(t, inst);
-  int rounds = kDeepRounds / 2;
+  uint64_t nk[kDeepRounds];
+#pragma unroll
+  for (int r = 0; r < kDeepRounds; ++r) {
+    const int32_t j = pos + r * 8 + g;
+    nk[r] = 0ull;
+    if (j < ell) nk[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+  }
   while (pos < ell) {
     uint64_t key[kDeepRounds], val[kDeepRounds];
     uint32_t b[kDeepRounds];
 #pragma unroll
     for (int r = 0; r < kDeepRounds; ++r) {
       const int32_t j = pos + r * 8 + g;
-      const bool act = r < rounds && j < ell;
-      key[r] = 0ull;
-      if (act) key[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+      key[r] = nk[r];
       b[r] = bucket_of(key[r], inst, t.shift);
       val[r] = 0ull;
-      if (act && key[r] != 0ull) val[r] = tab[(size_t)b[r] * kSlotsPerBucket + s];
+      if (j < ell && key[r] != 0ull) val[r] = tab[(size_t)b[r] * kSlotsPerBucket + s];
+    }
+    const int32_t next = pos + kDeepRounds * 8;
+#pragma unroll
+    for (int r = 0; r < kDeepRounds; ++r) {
+      const int32_t j = next + r * 8 + g;
+      nk[r] = 0ull;
+      if (j < ell) nk[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
     }
 #pragma unroll
     for (int r = 0; r < kDeepRounds; ++r) {
-      if (r < rounds) {
-        const int32_t j = pos + r * 8 + g;
-        const bool act = j < ell;
-        uint32_t st = octet_status(val[r], key[r], act, g);
-        st = octet_resolve(t, tab, b[r], key[r], st, s, g);
-        const uint64_t miss = __ballot(act && st == 0u && s == 0);
-        if (miss) return (uint32_t)(pos + r * 8 + (__builtin_ctzll(miss) >> 3));
-      }
+      const int32_t j = pos + r * 8 + g;
+      const bool act = j < ell;
+      uint32_t st = octet_status(val[r], key[r], act, g);
+      st = octet_resolve(t, tab, b[r], key[r], st, s, g);
+      const uint64_t miss = __ballot(act && st == 0u && s == 0);
+      if (miss) return (uint32_t)(pos + r * 8 + (__builtin_ctzll(miss) >> 3));
     }
-    pos += rounds * 8;
-    rounds = kDeepRounds;
+    pos = next;
   }
   return (uint32_t)ell;
 }
@@ -280,16 +283,24 @@ __global__ void build_kernel(BuildArgs a) {
   }
 }
 
+// Bits at positions 0, 8, ..., 56 of x gathered into bits 0..7 (the
+// products of the distinct powers of two never collide or carry).
+__device__ __forceinline__ uint32_t gather_octet_bits(uint64_t x) {
+  return (uint32_t)(((x & 0x0101010101010101ull) * 0x0102040810204080ull) >> 56);
+}
+
+__device__ __forceinline__ uint16_t encode_hit(uint32_t h) {
+  return (uint16_t)(h > kHitMax ? kHitOverflow : h);
+}
+
 template <bool HITS_IN_LDS, bool PROBE_ALL>
-__global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ Red red;
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
-  uint32_t* hits = HITS_IN_LDS ? reinterpret_cast<uint32_t*>(smem + kStage * sizeof(uint64_t))
+  uint16_t* hits = HITS_IN_LDS ? reinterpret_cast<uint16_t*>(smem + kStage * sizeof(uint64_t))
                                : a.scratch + (size_t)blockIdx.x * (size_t)a.n_inst;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int lane = threadIdx.x;
+  const int g = lane >> 3, s = lane & 7;
   const DevModel& m = *a.model;
   const int32_t n_inst = a.n_inst;
 
@@ -297,9 +308,8 @@ __global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
     const ps_req q = a.reqs[r];
     if (!req_valid(q, a.pool_len)) {
       if (PROBE_ALL) {
-        for (int32_t i = tid; i < n_inst; i += kBlock)
-          a.hits_out[(size_t)r * n_inst + i] = 0xFFFFFFFFu;
-      } else if (tid == 0) {
+        for (int32_t i = lane; i < n_inst; i += 64) a.hits_out[(size_t)r * n_inst + i] = 0xFFFFFFFFu;
+      } else if (lane == 0) {
         a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
         if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
       }
@@ -308,103 +318,70 @@ __global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
     const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
     const int32_t ell = c.len;
     const int64_t L = (int64_t)ell * m.bs;
-
-    // Stage the head of the chain in LDS (coalesced 8-byte reads).
-    const int32_t nst = ell < kStage ? ell : kStage;
-    for (int32_t j = tid; j < nst; j += kBlock) stage[j] = chain_global(c, j);
-    __syncthreads();
-
-    // (1a) Breadth probe of the chain's first block: octets over instances,
-    // kBreadthRounds x 8 instances per wave per step, all loads in flight
-    // before any is evaluated.
-    const uint64_t k0 = ell > 0 ? stage[0] : 0ull;
-    {
-      const int g = lane >> 3, s = lane & 7;
-      for (int32_t base = wave * (8 * kBreadthRounds); base < n_inst;
-           base += kWaves * 8 * kBreadthRounds) {
-        uint64_t val[kBreadthRounds];
-        uint32_t bkt[kBreadthRounds];
-        bool el[kBreadthRounds];
-#pragma unroll
-        for (int r = 0; r < kBreadthRounds; ++r) {
-          const int32_t i = base + r * 8 + g;
-          el[r] = false;
-          if (i < n_inst) {
-            const InstState* st = a.inst + i;
-            el[r] = PROBE_ALL || eligible(m, st->A1, st->S, L);
-          }
-          bkt[r] = bucket_of(k0, (uint32_t)i, a.t.shift);
-          val[r] = 0ull;
-          if (el[r] && k0 != 0ull)
-            val[r] = table_of(a.t, (uint32_t)i)[(size_t)bkt[r] * kSlotsPerBucket + s];
-        }
-#pragma unroll
-        for (int r = 0; r < kBreadthRounds; ++r) {
-          const int32_t i = base + r * 8 + g;
-          uint32_t st = octet_status(val[r], k0, el[r], g);
-          st = octet_resolve(a.t, table_of(a.t, (uint32_t)i), bkt[r], k0, st, s, g);
-          if (s == 0 && i < n_inst)
-            hits[i] = !el[r] ? kInelig : (st == 1u ? (ell > 1 ? (1u | kCont) : 1u) : 0u);
-        }
-      }
-    }
-    __syncthreads();
-
-    // (1b) Deep walks: each wave takes the surviving instances of its
-    // 64-instance chunks; lanes over chain positions.
-    for (int32_t base = wave * 64; base < n_inst; base += kBlock) {
-      const int32_t i = base + lane;
-      const uint32_t v = i < n_inst ? hits[i] : 0u;
-      uint64_t mask = __ballot(v != kInelig && (v & kCont) != 0u);
-      while (mask) {
-        const int s = __builtin_ctzll(mask);
-        mask &= mask - 1;
-        const uint32_t inst = (uint32_t)(base + s);
-        const uint32_t h = deep_walk<true>(a.t, inst, c, stage, 1, lane);
-        if (lane == 0) hits[inst] = h;
-      }
-    }
-    __syncthreads();
-
-    if (PROBE_ALL) {
-      for (int32_t i = tid; i < n_inst; i += kBlock) a.hits_out[(size_t)r * n_inst + i] = hits[i];
-      __syncthreads();
-      continue;
-    }
-
-    // (2)-(3) Capacity set A and the minimum recomputation penalty over A.
     const float Lf = (float)L;
+
+    // Stage the head of the chain (coalesced 8-byte reads; same wave reads it).
+    const int32_t nst = ell < kStage ? ell : kStage;
+    for (int32_t j = lane; j < nst; j += 64) stage[j] = chain_global(c, j);
+    __syncthreads();  // one wave per workgroup: orders the LDS writes before the reads
+    const uint64_t k0 = ell > 0 ? stage[0] : 0ull;
+
+    // (1) prefix hits, 64 instances per step; the minimum recomputation
+    // penalty over A is accumulated on the way.
     uint32_t wmin_bits = 0x7F800000u;  // +inf; penalties are >= 0, so bit order = value order
     uint32_t nA = 0;
-    for (int32_t i = tid; i < n_inst; i += kBlock) {
-      const uint32_t v = hits[i];
-      if (v == kInelig) continue;
-      ++nA;
-      const float n = (float)(L - (int64_t)v * m.bs);
-      const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
-      const uint32_t wb = __float_as_uint(W);
-      wmin_bits = wb < wmin_bits ? wb : wmin_bits;
-    }
-    {
-      const uint64_t wm = wave_min_u64((uint64_t)wmin_bits);
-      const uint32_t na = wave_sum_u32(nA);
-      if (lane == 0) {
-        red.k[0][wave] = wm;
-        red.u[0][wave] = na;
+    for (int32_t base = 0; base < n_inst; base += 64) {
+      const int32_t il = base + lane;
+      const int64_t room = il < n_inst ? a.room[il] : -1;
+      const bool elig_l = PROBE_ALL ? il < n_inst : (il < n_inst && L <= room);
+      const uint64_t E = __ballot(elig_l);
+      uint64_t val[kBreadthRounds];
+      uint32_t bkt[kBreadthRounds];
+#pragma unroll
+      for (int rr = 0; rr < kBreadthRounds; ++rr) {
+        const int k = rr * 8 + g;
+        bkt[rr] = bucket_of(k0, (uint32_t)(base + k), a.t.shift);
+        val[rr] = 0ull;
+        if (((E >> k) & 1ull) && k0 != 0ull)
+          val[rr] = table_of(a.t, (uint32_t)(base + k))[(size_t)bkt[rr] * kSlotsPerBucket + s];
+      }
+      uint64_t F = 0ull;  // bit k: instance base + k holds the first block
+#pragma unroll
+      for (int rr = 0; rr < kBreadthRounds; ++rr) {
+        const int k = rr * 8 + g;
+        const bool act = ((E >> k) & 1ull) != 0ull;
+        uint32_t st = octet_status(val[rr], k0, act, g);
+        st = octet_resolve(a.t, table_of(a.t, (uint32_t)(base + k)), bkt[rr], k0, st, s, g);
+        F |= (uint64_t)gather_octet_bits(__ballot(st == 1u && s == 0)) << (8 * rr);
+      }
+      uint32_t h = (uint32_t)((F >> lane) & 1ull);
+      uint64_t deep = ell > 1 ? F : 0ull;
+      while (deep) {
+        const int k = __builtin_ctzll(deep);
+        deep &= deep - 1;
+        const uint32_t hk = deep_walk<true>(a.t, (uint32_t)(base + k), c, stage, 1, g, s);
+        if (lane == k) h = hk;
+      }
+      if (il < n_inst) {
+        if (PROBE_ALL) {
+          a.hits_out[(size_t)r * n_inst + il] = h;
+        } else if (!elig_l) {
+          hits[il] = (uint16_t)kInelig;
+        } else {
+          hits[il] = encode_hit(h);
+          ++nA;
+          const float n = (float)(L - (int64_t)h * m.bs);
+          const uint32_t wb = __float_as_uint(fmaxf(0.0f, recompute_raw(m, n, Lf)));
+          wmin_bits = wb < wmin_bits ? wb : wmin_bits;
+        }
       }
     }
-    __syncthreads();
-    uint64_t wmin64 = red.k[0][0];
-    nA = red.u[0][0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) {
-      wmin64 = red.k[0][w] < wmin64 ? red.k[0][w] : wmin64;
-      nA += red.u[0][w];
-    }
-    const float wmin = __uint_as_float((uint32_t)wmin64);
-    __syncthreads();
+    if (PROBE_ALL) continue;
+    nA = wave_sum_u32(nA);
+    const float wmin = __uint_as_float((uint32_t)wave_min_u64((uint64_t)wmin_bits));
 
-    // (3)-(4) Filters and keys.
+    // (2)-(4) Filters and keys over A; instance state is read only for the
+    // candidates that pass the recomputation filter.
     const float Z = recompute_raw(m, Lf, Lf);   // T_pf(L, 0) - T_pf(0, L)
     const float tpf_cold = t_prefill(m, Lf, 0.0f);
     const float slo = fmaxf(m.ttft_floor, tpf_cold);
@@ -414,8 +391,16 @@ __global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
     uint64_t keyT = ~0ull, keyF = ~0ull;
     uint32_t nC = 0, nT = 0;
     if (nA > 0) {
-      for (int32_t i = tid; i < n_inst; i += kBlock) {
-        const uint32_t v = hits[i];
+      for (int32_t base = 0; base < n_inst; base += 64) {
+        const int32_t i = base + lane;
+        uint32_t v = i < n_inst ? hits[i] : kInelig;
+        uint64_t ovf = __ballot(v == kHitOverflow);
+        while (ovf) {  // hits beyond the u16 slot: walk again (chains > 65533 blocks)
+          const int k = __builtin_ctzll(ovf);
+          ovf &= ovf - 1;
+          const uint32_t hk = deep_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+          if (lane == k) v = hk;
+        }
         if (v == kInelig) continue;
         const int64_t c_tok = (int64_t)v * m.bs;
         const int64_t n_tok = L - c_tok;
@@ -440,49 +425,33 @@ __global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
         }
       }
     }
-    {
-      const uint64_t kt = wave_min_u64(keyT);
-      const uint64_t kf = wave_min_u64(keyF);
-      const uint32_t nc = wave_sum_u32(nC);
-      const uint32_t nt = wave_sum_u32(nT);
-      if (lane == 0) {
-        red.k[0][wave] = kt;
-        red.k[1][wave] = kf;
-        red.u[1][wave] = nc;
-        red.u[2][wave] = nt;
+    keyT = wave_min_u64(keyT);
+    keyF = wave_min_u64(keyF);
+    nC = wave_sum_u32(nC);
+    nT = wave_sum_u32(nT);
+
+    // Decision.  With finite arithmetic C holds at least the minimum-penalty
+    // candidate whenever A is non-empty; the key test only keeps a
+    // non-finite model from selecting an out-of-range id.
+    ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+    if (nA > 0 && (keyT != ~0ull || keyF != ~0ull)) {
+      uint32_t fl = 0;
+      uint32_t best;
+      if (keyT != ~0ull) {
+        best = (uint32_t)(keyT & 0xFFFFu);
+      } else {
+        best = (uint32_t)(keyF & 0xFFFFu);
+        fl |= PS_R_FALLBACK;
       }
+      uint32_t v = hits[best];
+      if (v == kHitOverflow) v = deep_walk<true>(a.t, best, c, stage, 0, g, s);
+      const int64_t c_tok = (int64_t)v * m.bs;
+      const InstState st = a.inst[best];
+      const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
+      if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
+      res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot, fl};
     }
-    __syncthreads();
-    if (tid == 0) {
-      uint64_t kt = red.k[0][0], kf = red.k[1][0];
-      nC = red.u[1][0];
-      nT = red.u[2][0];
-      for (int w = 1; w < kWaves; ++w) {
-        kt = red.k[0][w] < kt ? red.k[0][w] : kt;
-        kf = red.k[1][w] < kf ? red.k[1][w] : kf;
-        nC += red.u[1][w];
-        nT += red.u[2][w];
-      }
-      ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
-      // With finite arithmetic C holds at least the minimum-penalty
-      // candidate whenever A is non-empty; the second test only keeps a
-      // non-finite model from selecting an out-of-range id.
-      if (nA > 0 && (kt != ~0ull || kf != ~0ull)) {
-        uint32_t fl = 0;
-        uint32_t best;
-        if (kt != ~0ull) {
-          best = (uint32_t)(kt & 0xFFFFu);
-        } else {
-          best = (uint32_t)(kf & 0xFFFFu);
-          fl |= PS_R_FALLBACK;
-        }
-        const uint32_t v = hits[best];
-        const int64_t c_tok = (int64_t)v * m.bs;
-        const InstState st = a.inst[best];
-        const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
-        if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
-        res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot, fl};
-      }
+    if (lane == 0) {
       a.out[r] = res;
       if (a.sizes) {
         a.sizes[3 * (size_t)r] = nA;
@@ -490,7 +459,6 @@ __global__ __launch_bounds__(kBlock) void score_kernel(ScoreArgs a) {
         a.sizes[3 * (size_t)r + 2] = nT;
       }
     }
-    __syncthreads();
   }
 }
 
@@ -516,7 +484,7 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
     const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
     const int32_t ell = c.len;
     const int64_t L = (int64_t)ell * m.bs;
-    const uint32_t h = deep_walk<false>(a.t, inst, c, nullptr, 0, lane);
+    const uint32_t h = deep_walk<false>(a.t, inst, c, nullptr, 0, lane >> 3, lane & 7);
     st.Q += 1;
     st.A1 += 1;
     st.P += L - (int64_t)h * m.bs;
@@ -550,6 +518,7 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
   st.seg = segment_of(m, st.A1);
   if (lane == 0) {
     a.inst[inst] = st;
+    a.room[inst] = st.A1 <= m.b_max ? m.kv_cap - st.S : -1;
     a.t.count[inst] = count;
     if (dropped) atomicAdd(a.dropped, dropped);
   }
@@ -559,7 +528,12 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
 
 // ------------------------------------------------------------------ launchers
 size_t ps_score_lds_bytes(int32_t n_inst) {
-  return (size_t)kStage * sizeof(uint64_t) + (size_t)n_inst * sizeof(uint32_t);
+  const size_t hits = ps_hits_fit_lds(n_inst) ? ((size_t)n_inst * sizeof(uint16_t) + 15) / 16 * 16 : 0;
+  return (size_t)kStage * sizeof(uint64_t) + hits;
+}
+
+bool ps_hits_fit_lds(int32_t n_inst) {
+  return (size_t)n_inst * sizeof(uint16_t) <= kLdsHitBudget;
 }
 
 hipError_t ps_launch_build(const BuildArgs& a, hipStream_t s) {
@@ -573,17 +547,17 @@ hipError_t ps_launch_build(const BuildArgs& a, hipStream_t s) {
 hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s) {
   if (a.n_req == 0) return hipSuccess;
-  const size_t lds = hits_in_lds ? ps_score_lds_bytes(a.n_inst) : (size_t)kStage * sizeof(uint64_t);
+  const size_t lds = ps_score_lds_bytes(hits_in_lds ? a.n_inst : PS_MAX_INST);
   if (hits_in_lds) {
     if (probe_all)
-      hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(64), lds, s, a);
     else
-      hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
   } else {
     if (probe_all)
-      hipLaunchKernelGGL((score_kernel<false, true>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((score_kernel<false, true>), dim3(grid), dim3(64), lds, s, a);
     else
-      hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
   }
   return hipGetLastError();
 }
