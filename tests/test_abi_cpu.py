@@ -1,0 +1,62 @@
+"""The C-ABI library loads and exports every entry point its header declares
+(no GPU calls here beyond a device count)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "packserve.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:ps_status|const char\*)\s+(ps_\w+)\s*\(", src, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ("ps_create", "ps_destroy", "ps_load_instances", "ps_score_window",
+              "ps_score_window_dev", "ps_probe_hits_dev", "ps_commit", "ps_read_state",
+              "ps_table_info", "ps_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2609_33224_amd as ps
+    lib = ps.load_library()
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_struct_layouts_match_header():
+    import paper_2609_33224_amd as ps
+    assert ps.PS_REQ_DTYPE.itemsize == 24
+    assert ps.PS_RESULT_DTYPE.itemsize == 20
+    # float alpha[6]; int n_seg; int seg_ub[32]; float beta[32][3]; float gamma[32];
+    # 4 floats; 2 ints; int64 (8-aligned); uint32 -> 712 bytes with tail padding
+    assert ctypes.sizeof(ps.PsModel) == 712
+    assert ctypes.sizeof(ps.binding.PsInstances) == 56
+
+
+def test_errors_without_a_context():
+    import paper_2609_33224_amd as ps
+    lib = ps.load_library()
+    assert lib.ps_create(0, None) == ps.binding.PS_E_INVAL
+    assert lib.ps_destroy(None) == 0
+    assert lib.ps_load_instances(None, None, None) == ps.binding.PS_E_INVAL
+    assert lib.ps_score_window(None, None, 0, None, 0, None) == ps.binding.PS_E_INVAL
+    assert lib.ps_commit(None, None, 0, None, None, 0, None) == ps.binding.PS_E_INVAL
+    assert b"ctx is NULL" in lib.ps_last_error(None)
+
+
+def test_no_device_reports_an_error(monkeypatch):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    import paper_2609_33224_amd as ps
+    with pytest.raises(ps.PackServeError) as e:
+        ps.ps_create(0)
+    assert e.value.code in (ps.binding.PS_E_DEVICE, ps.binding.PS_E_INVAL)
