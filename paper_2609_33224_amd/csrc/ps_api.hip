@@ -38,6 +38,8 @@ struct ps_ctx {
   Tables t{};
   InstState* d_inst = nullptr;
   int64_t* d_room = nullptr;
+  int64_t* d_room_sorted = nullptr;
+  GIndex x{nullptr, nullptr, 0, 64};
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
   uint16_t* d_scratch = nullptr;
@@ -189,10 +191,23 @@ ps_status check_reqs_host(ps_ctx* c, const uint64_t* pool, int64_t pool_len, con
 void free_snapshot(ps_ctx* c) {
   dfree(c->t.keys);
   dfree(c->t.count);
+  dfree(c->t.rows);
+  dfree(c->t.rowpos);
   dfree(c->d_inst);
   dfree(c->d_room);
+  dfree(c->d_room_sorted);
   dfree(c->d_scratch);
+  ps_free_index(&c->x);
   c->loaded = false;
+}
+
+// Per-instance room (kv_cap - S when A + 1 <= B_max, else -1; an instance
+// is capacity-eligible for a request of L tokens iff L <= room) and the same
+// values sorted ascending, so |A| is one binary search.
+std::vector<int64_t> rooms_of(const std::vector<InstState>& hs, const DevModel& m) {
+  std::vector<int64_t> r(hs.size());
+  for (size_t i = 0; i < hs.size(); ++i) r[i] = hs[i].A1 <= m.b_max ? m.kv_cap - hs[i].S : -1;
+  return r;
 }
 
 }  // namespace
@@ -286,6 +301,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   DeviceScope ds(c->device);
   ps_ctx fresh;  // new device buffers; swapped in only on success
   fresh.t.slots = slots;
+  fresh.t.row_cap = in->table_cap_blocks;
   fresh.t.bmask = (uint32_t)(buckets - 1);
   fresh.t.shift = (uint32_t)(64 - log2b);
   const size_t tab_bytes = (size_t)n * (size_t)slots * sizeof(uint64_t);
@@ -293,19 +309,40 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   const int rows = lds ? 0 : std::max(1, c->num_cus * kScratchRowsPerCU);
   int64_t* d_off = nullptr;
   uint64_t* d_blk = nullptr;
+  uint32_t *d_won = nullptr, *d_slot = nullptr, *d_rank = nullptr;
+  auto free_build_temps = [&]() {
+    dfree(d_off);
+    dfree(d_blk);
+    dfree(d_won);
+    dfree(d_slot);
+    dfree(d_rank);
+  };
   auto cleanup = [&]() {
+    free_build_temps();
     dfree(fresh.t.keys);
     dfree(fresh.t.count);
+    dfree(fresh.t.rows);
+    dfree(fresh.t.rowpos);
     dfree(fresh.d_inst);
     dfree(fresh.d_room);
+    dfree(fresh.d_room_sorted);
     dfree(fresh.d_scratch);
+    ps_free_index(&fresh.x);
     dfree(d_off);
     dfree(d_blk);
   };
   hipError_t e = hipMalloc((void**)&fresh.t.keys, tab_bytes);
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.t.count, (size_t)n * sizeof(uint32_t));
+  if (e == hipSuccess)
+    e = hipMalloc((void**)&fresh.t.rowpos, (size_t)n * (size_t)slots * sizeof(uint32_t));
+  if (e == hipSuccess)
+    e = hipMalloc((void**)&fresh.t.rows, (size_t)n * (size_t)fresh.t.row_cap * sizeof(uint64_t));
+  if (e == hipSuccess && n_blk) e = hipMalloc((void**)&d_won, (size_t)n_blk * sizeof(uint32_t));
+  if (e == hipSuccess && n_blk) e = hipMalloc((void**)&d_slot, (size_t)n_blk * sizeof(uint32_t));
+  if (e == hipSuccess && n_blk) e = hipMalloc((void**)&d_rank, (size_t)n_blk * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst, (size_t)n * sizeof(InstState));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room, (size_t)n * sizeof(int64_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room_sorted, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess && rows)
     e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint16_t));
   if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
@@ -316,7 +353,6 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
                 "allocating %.1f MiB of tables: %s", tab_bytes / 1048576.0, hipGetErrorString(e));
   }
   std::vector<InstState> hs((size_t)n);
-  std::vector<int64_t> hroom((size_t)n);
   for (int32_t i = 0; i < n; ++i) {
     InstState& s = hs[(size_t)i];
     s.D = in->decoding[i];
@@ -325,10 +361,11 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     s.seg = segment_of_host(*m, s.A1);
     s.P = in->pending_tok[i];
     s.S = in->ctx_tok[i];
-    // capacity guard A_i + 1 <= B_max and S_i + L <= M_KV as one comparison L <= room
-    hroom[(size_t)i] = s.A1 <= m->b_max ? m->kv_cap_tokens - s.S : -1;
   }
   const DevModel dm = device_model(*m);
+  const std::vector<int64_t> hroom = rooms_of(hs, dm);
+  std::vector<int64_t> hroom_sorted = hroom;
+  std::sort(hroom_sorted.begin(), hroom_sorted.end());
   hipStream_t sm = c->stream;
   e = hipMemsetAsync(fresh.t.keys, 0, tab_bytes, sm);
   if (e == hipSuccess) e = hipMemsetAsync(fresh.t.count, 0, (size_t)n * sizeof(uint32_t), sm);
@@ -341,10 +378,13 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     e = hipMemcpyAsync(fresh.d_inst, hs.data(), hs.size() * sizeof(InstState), hipMemcpyHostToDevice, sm);
   if (e == hipSuccess)
     e = hipMemcpyAsync(fresh.d_room, hroom.data(), hroom.size() * sizeof(int64_t), hipMemcpyHostToDevice, sm);
-  if (e == hipSuccess) {
-    BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter};
-    e = ps_launch_build(ba, sm);
-  }
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(fresh.d_room_sorted, hroom_sorted.data(), hroom_sorted.size() * sizeof(int64_t),
+                       hipMemcpyHostToDevice, sm);
+  BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter, d_won, d_slot, d_rank};
+  if (e == hipSuccess) e = ps_launch_build(ba, sm);
+  if (e == hipSuccess) e = ps_exclusive_scan_u32(d_won, d_rank, n_blk, sm);
+  if (e == hipSuccess) e = ps_launch_rows(ba, sm);
   unsigned long long full = 0;
   if (e == hipSuccess)
     e = hipMemcpyAsync(&full, c->d_counter, sizeof full, hipMemcpyDeviceToHost, sm);
@@ -356,9 +396,11 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   std::vector<uint32_t> hc((size_t)n);
   if (e == hipSuccess)
     e = hipMemcpy(hc.data(), fresh.t.count, (size_t)n * sizeof(uint32_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = ps_build_index(fresh.t, n, hc.data(), &fresh.x, sm);
   if (e != hipSuccess) {
     cleanup();
-    return fail(c, PS_E_DEVICE, "building tables: %s", hipGetErrorString(e));
+    return fail(c, e == hipErrorOutOfMemory ? PS_E_NOMEM : PS_E_DEVICE, "building tables: %s",
+                hipGetErrorString(e));
   }
   // The model upload is the last step that can fail; the old snapshot stays
   // intact until here.
@@ -368,12 +410,13 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     if (c->loaded) (void)hipMemcpy(c->d_model, &c->h_model, sizeof c->h_model, hipMemcpyHostToDevice);
     return fail(c, PS_E_DEVICE, "model upload: %s", hipGetErrorString(e));
   }
-  dfree(d_off);
-  dfree(d_blk);
+  free_build_temps();
   free_snapshot(c);
   c->t = fresh.t;
   c->d_inst = fresh.d_inst;
   c->d_room = fresh.d_room;
+  c->d_room_sorted = fresh.d_room_sorted;
+  c->x = fresh.x;
   c->d_scratch = fresh.d_scratch;
   c->scratch_rows = rows;
   c->hits_in_lds = lds;
@@ -385,8 +428,12 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->loaded = true;
   fresh.t.keys = nullptr;
   fresh.t.count = nullptr;
+  fresh.t.rows = nullptr;
+  fresh.t.rowpos = nullptr;
   fresh.d_inst = nullptr;
   fresh.d_room = nullptr;
+  fresh.d_room_sorted = nullptr;
+  fresh.x = GIndex{nullptr, nullptr, 0, 64};
   fresh.d_scratch = nullptr;
   return PS_OK;
 }
@@ -396,6 +443,8 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                               uint32_t* d_sizes, uint32_t* d_hits, hipStream_t s) {
   ScoreArgs a{};
   a.t = c->t;
+  a.x = c->x;
+  a.room_sorted = c->d_room_sorted;
   a.inst = c->d_inst;
   a.room = c->d_room;
   a.model = c->d_model;
@@ -541,6 +590,10 @@ ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_
   HIP_TRY(c, hipMemcpyAsync(c->h_count.data(), c->t.count, c->h_count.size() * sizeof(uint32_t),
                             hipMemcpyDeviceToHost, s));
   HIP_TRY(c, hipStreamSynchronize(s));
+  std::vector<int64_t> rs = rooms_of(c->h_state, c->h_model);
+  std::sort(rs.begin(), rs.end());
+  HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+  HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
   if (n_dropped) *n_dropped = (int64_t)dropped;
   return PS_OK;
 }

@@ -47,10 +47,18 @@ struct DevModel {
 };
 
 // Table geometry: n_inst tables of (1 << log2_buckets) buckets each.
+// Per-instance tables.  Besides the hash slots, every instance keeps its
+// distinct cached blocks as a row in insertion order (row_cap entries each;
+// row_len = count), and rowpos[slot] gives the row position of the key in
+// that slot, so a walk that finds one block can compare the blocks after it
+// with the row sequentially.
 struct Tables {
   uint64_t* keys;       // n_inst * slots
-  uint32_t* count;      // distinct keys per instance
+  uint32_t* count;      // distinct keys per instance (= row length)
+  uint32_t* rowpos;     // n_inst * slots: row position of each occupied slot
+  uint64_t* rows;       // n_inst * row_cap, insertion order
   int64_t slots;        // slots per instance = buckets * 8
+  int64_t row_cap;      // = table cap
   uint32_t bmask;       // buckets - 1
   uint32_t shift;       // 64 - log2(buckets) (64 when one bucket)
 };
@@ -65,8 +73,28 @@ __host__ __device__ __forceinline__ uint32_t bucket_of(uint64_t key, uint32_t in
   return shift >= 64 ? 0u : (uint32_t)(x >> shift);
 }
 
+// Prefix index: every cached block hash of the pool with the ascending list
+// of instances holding it (the GPU form of a prefix tree over chained hashes:
+// one hash names one prefix).  16-byte entries, buckets of 8 = one 128-byte
+// line, multiply-shift bucket with the salt kIndexSalt, linear probing.
+struct alignas(16) IdxEntry {
+  uint64_t key;   // 0 = empty
+  uint32_t off;   // first holder in `holders`
+  uint32_t cnt;   // number of holders
+};
+constexpr uint32_t kIndexSalt = 0x10000u;  // not an instance id
+
+struct GIndex {
+  IdxEntry* ent;
+  uint16_t* holders;
+  uint32_t bmask;
+  uint32_t shift;
+};
+
 struct ScoreArgs {
   Tables t;
+  GIndex x;
+  const int64_t* room_sorted;  // rooms ascending (eligible count = n - lower_bound(L))
   const InstState* inst;
   const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
   const DevModel* model;
@@ -103,14 +131,24 @@ struct BuildArgs {
   int32_t n_inst;
   int64_t n_blk;
   unsigned long long* full;  // inserts that found no free slot (never for valid caps)
+  uint32_t* won;             // n_blk: 1 where this list entry inserted its key
+  uint32_t* slot_of;         // n_blk: table slot of the entry's key
+  uint32_t* rank;            // n_blk: exclusive scan of `won` (global)
 };
 
 }  // namespace ps
 
 // Kernel launchers (ps_kernels.hip).
-hipError_t ps_launch_build(const ps::BuildArgs& a, hipStream_t s);
+hipError_t ps_launch_build(const ps::BuildArgs& a, hipStream_t s);  // slots, won, slot_of
+hipError_t ps_launch_rows(const ps::BuildArgs& a, hipStream_t s);   // rows, rowpos (needs rank)
+hipError_t ps_exclusive_scan_u32(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t s);
 hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s);
 bool ps_hits_fit_lds(int32_t n_inst);
+// Prefix index build (ps_index.hip): from the per-instance tables.  Frees and
+// replaces *x.  count_host: distinct keys per instance.
+hipError_t ps_build_index(const ps::Tables& t, int32_t n_inst, const uint32_t* count_host,
+                          ps::GIndex* x, hipStream_t s);
+void ps_free_index(ps::GIndex* x);
 hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
 size_t ps_score_lds_bytes(int32_t n_inst);

@@ -1,24 +1,31 @@
 // HIP kernels of the window scorer for gfx950 (CDNA4, wave64).
 //
-//   build_kernel   - per-instance open-addressing tables from the CSR block
-//                    lists (64-bit atomicCAS inserts).
-//   score_kernel   - the fused hot path, one wave per request (no barriers):
-//                      (1) longest cached prefix of the request's block-hash
-//                          chain on every capacity-eligible instance: a breadth
-//                          probe of the first block, octets of lanes over
-//                          instances, then for each instance holding it a deep
-//                          walk, octets over chain positions, stopping at the
-//                          first absent block (ballot + count-trailing-zeros);
-//                          the chain head is staged in LDS,
-//                      (2) the latency model (Eq. 7 + C, C^2 terms; Eq. 8 per
-//                          segment with its EMA factor; Eq. 10; Eq. 4),
-//                      (3) capacity, recomputation (Eq. 9) and TPOT filters,
-//                      (4) the packed D-C-Q key and the LMetric fallback key,
-//                          reduced with DPP wave minima.
-//   commit_kernel  - ordered placement of decisions, one wave per instance.
+//   build_kernel      - per-instance open-addressing tables from the CSR block
+//                       lists (64-bit atomicCAS inserts).
+//   score_kernel      - the fused hot path, one wave per request:
+//                         (1) longest cached prefix on every capacity-eligible
+//                             instance.  One prefix-index lookup of the first
+//                             block gives the instances that hold it; every
+//                             other eligible instance has hit 0.  Up to 64
+//                             holders are walked on their own tables (octets of
+//                             lanes over chain positions, the first absent
+//                             block from a ballot); more holders are walked
+//                             together through the index, position by
+//                             position, with LDS bitmaps of the live set.
+//                             The chain head is staged in LDS.
+//                         (2) the latency model (Eq. 7 + C, C^2 terms; Eq. 8
+//                             per segment with its EMA factor; Eq. 10; Eq. 4),
+//                         (3) capacity, recomputation (Eq. 9) and TPOT filters:
+//                             all hit-0 instances share one penalty, so that
+//                             class is evaluated only if it passes Eq. 9,
+//                         (4) the packed D-C-Q and LMetric keys, reduced with
+//                             DPP wave minima.
+//   probe_all_kernel  - diagnostic: the hit of every request on every
+//                       instance by direct probing of the per-instance tables
+//                       (breadth probe of the first block, then deep walks).
+//   commit_kernel     - ordered placement of decisions, one wave per instance.
 //
-// The path is bound by HBM (random 64-byte bucket reads); it does no dense
-// contraction, so it uses no MFMA.
+// The path does no dense contraction, so it uses no MFMA.
 
 #include "ps_device.h"
 
@@ -112,6 +119,46 @@ __device__ __forceinline__ uint32_t octet_resolve(const Tables& t, const uint64_
   return status;
 }
 
+// Octet lookup in the prefix index: octet g looks up key (if act); the
+// result is valid in every lane of the octet.  Every lane of the wave must
+// call it.  One 16-byte entry per lane, one 128-byte bucket per octet.
+struct IdxHit {
+  bool found;
+  uint32_t off, cnt;
+};
+
+__device__ __forceinline__ IdxHit index_lookup(const GIndex& x, uint64_t key, bool act, int g,
+                                               int s) {
+  IdxHit h{false, 0u, 0u};
+  bool pend = act && key != 0ull;
+  uint32_t b = bucket_of(key, kIndexSalt, x.shift);
+  for (uint32_t step = 0; step <= x.bmask; ++step) {
+    if (__ballot(pend) == 0ull) break;
+    IdxEntry e{0ull, 0u, 0u};
+    if (pend) e = x.ent[(size_t)b * kSlotsPerBucket + s];
+    const uint64_t fm = __ballot(pend && e.key == key);
+    const uint64_t em = __ballot(pend && e.key == 0ull);
+    const uint32_t f = (uint32_t)(fm >> (8 * g)) & 0xFFu;
+    const uint32_t z = (uint32_t)(em >> (8 * g)) & 0xFFu;
+    const int src = 8 * g + (f ? __builtin_ctz(f) : 0);
+    const uint32_t off = __shfl(e.off, src);
+    const uint32_t cnt = __shfl(e.cnt, src);
+    if (pend) {
+      if (f) {
+        h.found = true;
+        h.off = off;
+        h.cnt = cnt;
+        pend = false;
+      } else if (z) {
+        pend = false;
+      } else {
+        b = (b + 1) & x.bmask;
+      }
+    }
+  }
+  return h;
+}
+
 // Single-lane lookup (commit path only).
 __device__ __forceinline__ Bucket load_bucket(const uint64_t* p) {
   const ulonglong2* q = reinterpret_cast<const ulonglong2*>(p);
@@ -138,24 +185,29 @@ __device__ bool probe(const Tables& t, uint32_t inst, uint64_t key) {
   return false;
 }
 
-// 1 inserted, 0 already present, -1 no free slot.  Safe under concurrent
-// inserts: a slot only ever changes from 0 to a key, and every claim of an
-// apparently empty slot goes through a 64-bit compare-and-swap whose result
-// decides.
-__device__ int insert_key(const Tables& t, uint32_t inst, uint64_t key) {
+// 1 inserted, 0 already present, -1 no free slot; *slot = the key's slot
+// within the instance's table.  Safe under concurrent inserts: a slot only
+// ever changes from 0 to a key, and every claim of an apparently empty slot
+// goes through a 64-bit compare-and-swap whose result decides.
+__device__ int insert_key(const Tables& t, uint32_t inst, uint64_t key, uint32_t* slot) {
   uint64_t* tab = t.keys + (size_t)inst * (size_t)t.slots;
   uint32_t b = bucket_of(key, inst, t.shift);
   for (uint32_t step = 0; step <= t.bmask; ++step) {
     uint64_t* bp = tab + (size_t)b * kSlotsPerBucket;
     const Bucket bk = load_bucket(bp);
     for (int s = 0; s < kSlotsPerBucket; ++s)
-      if (bk.k[s] == key) return 0;
+      if (bk.k[s] == key) {
+        *slot = b * kSlotsPerBucket + s;
+        return 0;
+      }
     for (int s = 0; s < kSlotsPerBucket; ++s) {
       if (bk.k[s] != 0) continue;
       const unsigned long long old =
           atomicCAS(reinterpret_cast<unsigned long long*>(bp + s), 0ull, (unsigned long long)key);
-      if (old == 0ull) return 1;
-      if (old == key) return 0;
+      if (old == 0ull || old == key) {
+        *slot = b * kSlotsPerBucket + s;
+        return old == 0ull ? 1 : 0;
+      }
     }
     b = (b + 1) & t.bmask;
   }
@@ -231,6 +283,73 @@ __device__ uint32_t deep_walk(const Tables& t, uint32_t inst, const ChainRef& c,
   return (uint32_t)ell;
 }
 
+// Walk of one instance along its row: one octet probe finds the block at
+// `pos` and its row position; the chain blocks after it are compared with
+// the row entries after it, 256 per step (4 per lane, coalesced), and the
+// first mismatch is probed again (it may begin another run of the row, e.g.
+// after a shared system prompt).  A run shorter than 8 blocks hands the rest
+// of the walk to the octet walk.  Wave-uniform arguments; returns the hit.
+template <bool STAGED>
+__device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, const ChainRef& c,
+                             const uint64_t* stage, int32_t pos, int g, int s) {
+  const int lane = g * 8 + s;
+  const int32_t ell = c.len;
+  const uint64_t* tab = table_of(t, inst);
+  const uint64_t* row = t.rows + (size_t)inst * (size_t)t.row_cap;
+  const int64_t rlen = t.count[inst];
+  while (pos < ell) {
+    const uint64_t key = (STAGED && pos < kStage) ? stage[pos] : chain_global(c, pos);
+    if (key == 0ull) return (uint32_t)pos;
+    uint32_t b = bucket_of(key, inst, t.shift);
+    int64_t rp = -1;
+    bool decided = false;
+    for (uint32_t step = 0; step <= t.bmask && !decided; ++step) {
+      const uint64_t val = g == 0 ? tab[(size_t)b * kSlotsPerBucket + s] : 0ull;
+      const uint64_t fm = __ballot(g == 0 && val == key) & 0xFFull;
+      const uint64_t em = __ballot(g == 0 && val == 0ull) & 0xFFull;
+      if (fm) {
+        rp = t.rowpos[(size_t)inst * t.slots + (size_t)b * kSlotsPerBucket + __builtin_ctzll(fm)];
+        decided = true;
+      } else if (em) {
+        decided = true;
+      } else {
+        b = (b + 1) & t.bmask;
+      }
+    }
+    if (rp < 0) return (uint32_t)pos;
+    const int32_t start = pos + 1;
+    int32_t q = start;
+    int64_t k = rp + 1;
+    int32_t next = -1;
+    while (next < 0) {
+      bool mism[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int32_t j = q + 64 * u + lane;
+        const int64_t kk = k + 64 * u + lane;
+        const bool valid = j < ell;
+        uint64_t cj = 0ull, rk = 0ull;
+        if (valid) cj = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+        if (valid && kk < rlen) rk = row[kk];
+        mism[u] = valid && (kk >= rlen || cj != rk);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint64_t mm = __ballot(mism[u]);
+        if (next < 0 && mm) next = q + 64 * u + __builtin_ctzll(mm);
+      }
+      if (next < 0) {
+        q += 256;
+        k += 256;
+        if (q >= ell) return (uint32_t)ell;
+      }
+    }
+    if (next - start < 8) return deep_walk<STAGED>(t, inst, c, stage, next, g, s);
+    pos = next;
+  }
+  return (uint32_t)ell;
+}
+
 // ------------------------------------------------------------- latency model
 // Eq. 7 with the empirical C and C^2 terms: n new, c cached tokens.
 __device__ __forceinline__ float t_prefill(const DevModel& m, float n, float c) {
@@ -277,9 +396,30 @@ __global__ void build_kernel(BuildArgs a) {
       if (a.blk_off[mid] <= k) lo = mid;
       else hi = mid;
     }
-    const int r = insert_key(a.t, (uint32_t)lo, a.blk[k]);
+    uint32_t slot = 0;
+    const int r = insert_key(a.t, (uint32_t)lo, a.blk[k], &slot);
     if (r == 1) atomicAdd(&a.t.count[lo], 1u);
     else if (r < 0) atomicAdd(a.full, 1ull);
+    a.won[k] = r == 1 ? 1u : 0u;
+    a.slot_of[k] = slot;
+  }
+}
+
+// Rows: the entries that inserted their key, in list order, become the
+// instance's row; rank is the global exclusive scan of `won`.
+__global__ void row_kernel(BuildArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < a.n_blk; k += stride) {
+    if (!a.won[k]) continue;
+    int32_t lo = 0, hi = a.n_inst;
+    while (hi - lo > 1) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (a.blk_off[mid] <= k) lo = mid;
+      else hi = mid;
+    }
+    const uint32_t pos = a.rank[k] - a.rank[a.blk_off[lo]];
+    a.t.rows[(size_t)lo * a.t.row_cap + pos] = a.blk[k];
+    a.t.rowpos[(size_t)lo * a.t.slots + a.slot_of[k]] = pos;
   }
 }
 
@@ -293,48 +433,34 @@ __device__ __forceinline__ uint16_t encode_hit(uint32_t h) {
   return (uint16_t)(h > kHitMax ? kHitOverflow : h);
 }
 
-template <bool HITS_IN_LDS, bool PROBE_ALL>
-__global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
+__device__ __forceinline__ bool test_bit(const uint64_t* bm, uint32_t i) {
+  return ((bm[i >> 6] >> (i & 63)) & 1ull) != 0ull;
+}
+
+// Hit of every request on every instance by direct probing: the first block
+// on all instances (octets of lanes over instances, 64 per step), then a
+// deep walk of each instance that holds it.
+__global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
-  uint16_t* hits = HITS_IN_LDS ? reinterpret_cast<uint16_t*>(smem + kStage * sizeof(uint64_t))
-                               : a.scratch + (size_t)blockIdx.x * (size_t)a.n_inst;
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
-  const DevModel& m = *a.model;
   const int32_t n_inst = a.n_inst;
-
   for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
     const ps_req q = a.reqs[r];
     if (!req_valid(q, a.pool_len)) {
-      if (PROBE_ALL) {
-        for (int32_t i = lane; i < n_inst; i += 64) a.hits_out[(size_t)r * n_inst + i] = 0xFFFFFFFFu;
-      } else if (lane == 0) {
-        a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
-        if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
-      }
+      for (int32_t i = lane; i < n_inst; i += 64) a.hits_out[(size_t)r * n_inst + i] = 0xFFFFFFFFu;
       continue;
     }
     const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
     const int32_t ell = c.len;
-    const int64_t L = (int64_t)ell * m.bs;
-    const float Lf = (float)L;
-
-    // Stage the head of the chain (coalesced 8-byte reads; same wave reads it).
     const int32_t nst = ell < kStage ? ell : kStage;
+    __syncthreads();
     for (int32_t j = lane; j < nst; j += 64) stage[j] = chain_global(c, j);
-    __syncthreads();  // one wave per workgroup: orders the LDS writes before the reads
+    __syncthreads();
     const uint64_t k0 = ell > 0 ? stage[0] : 0ull;
-
-    // (1) prefix hits, 64 instances per step; the minimum recomputation
-    // penalty over A is accumulated on the way.
-    uint32_t wmin_bits = 0x7F800000u;  // +inf; penalties are >= 0, so bit order = value order
-    uint32_t nA = 0;
     for (int32_t base = 0; base < n_inst; base += 64) {
-      const int32_t il = base + lane;
-      const int64_t room = il < n_inst ? a.room[il] : -1;
-      const bool elig_l = PROBE_ALL ? il < n_inst : (il < n_inst && L <= room);
-      const uint64_t E = __ballot(elig_l);
+      const uint64_t E = __ballot(base + lane < n_inst);
       uint64_t val[kBreadthRounds];
       uint32_t bkt[kBreadthRounds];
 #pragma unroll
@@ -362,73 +488,277 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
         const uint32_t hk = deep_walk<true>(a.t, (uint32_t)(base + k), c, stage, 1, g, s);
         if (lane == k) h = hk;
       }
-      if (il < n_inst) {
-        if (PROBE_ALL) {
-          a.hits_out[(size_t)r * n_inst + il] = h;
-        } else if (!elig_l) {
-          hits[il] = (uint16_t)kInelig;
-        } else {
-          hits[il] = encode_hit(h);
-          ++nA;
-          const float n = (float)(L - (int64_t)h * m.bs);
-          const uint32_t wb = __float_as_uint(fmaxf(0.0f, recompute_raw(m, n, Lf)));
+      if (base + lane < n_inst) a.hits_out[(size_t)r * n_inst + base + lane] = h;
+    }
+  }
+}
+
+// Per-lane accumulation of one candidate (instance i, hit v) of A: the
+// recomputation filter, then (for members of C) Eq. 10, Eq. 4, the TPOT /
+// TTFT tests and the two packed keys.
+struct Acc {
+  uint64_t keyT, keyF;
+  uint32_t nC, nT;
+};
+
+__device__ __forceinline__ void evaluate(const ScoreArgs& a, const DevModel& m, Acc& acc,
+                                         uint32_t i, uint32_t v, int64_t L, float Lf, float wmin,
+                                         float Z, bool kvc, float slo) {
+  const int64_t c_tok = (int64_t)v * m.bs;
+  const int64_t n_tok = L - c_tok;
+  const float n = (float)n_tok;
+  if (kvc) {
+    const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
+    if (!((W - wmin) / Z <= m.eta)) return;
+  }
+  ++acc.nC;
+  const InstState st = a.inst[i];
+  const Lat lt = latency(m, st, n, (float)c_tok, L);
+  const uint64_t lm = (uint64_t)(st.P + n_tok) * (uint64_t)st.A1;
+  const uint64_t kf = (lm << 16) | (uint64_t)i;
+  acc.keyF = kf < acc.keyF ? kf : acc.keyF;
+  const bool tpot_ok = (m.flags & PS_F_NO_TPOT_FILTER) || lt.tpot < m.tau;
+  const bool ttft_ok = !(m.flags & PS_F_TTFT_ADMIT) || lt.ttft <= slo;
+  if (tpot_ok && ttft_ok) {
+    ++acc.nT;
+    const uint64_t kt = ((uint64_t)(PS_MAX_DQ - st.D) << 52) |
+                        ((uint64_t)(PS_MAX_CHAIN - v) << 28) | ((uint64_t)st.Q << 16) | (uint64_t)i;
+    acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+  }
+}
+
+// LDS of one scoring wave: chain stage | live bitmap | next bitmap |
+// candidate bitmap (instances holding the first block) | 64 candidate ids |
+// u16 hit slots (or device scratch for large pools).
+template <bool HITS_IN_LDS>
+__global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int32_t n_inst = a.n_inst;
+  const int32_t nw = (n_inst + 63) >> 6;
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
+  uint64_t* bmA = stage + kStage;
+  uint64_t* bmN = bmA + nw;
+  uint64_t* bmC = bmN + nw;
+  uint16_t* cl = reinterpret_cast<uint16_t*>(bmC + nw);
+  uint16_t* hits = HITS_IN_LDS ? cl + 64 : a.scratch + (size_t)blockIdx.x * (size_t)n_inst;
+  const int lane = threadIdx.x;
+  const int g = lane >> 3, s = lane & 7;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  const DevModel& m = *a.model;
+
+  for (int32_t w = lane; w < 3 * nw; w += 64) bmA[w] = 0ull;
+
+  for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
+    const ps_req q = a.reqs[r];
+    if (!req_valid(q, a.pool_len)) {
+      if (lane == 0) {
+        a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
+        if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+      }
+      continue;
+    }
+    const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
+    const int32_t ell = c.len;
+    const int64_t L = (int64_t)ell * m.bs;
+    const float Lf = (float)L;
+    const int32_t nst = ell < kStage ? ell : kStage;
+    __syncthreads();
+    for (int32_t j = lane; j < nst; j += 64) stage[j] = chain_global(c, j);
+    __syncthreads();
+
+    // |A|: capacity-eligible instances are those with room >= L.
+    int32_t lo = 0, hi = n_inst;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (a.room_sorted[mid] < L) lo = mid + 1;
+      else hi = mid;
+    }
+    const uint32_t nA = (uint32_t)(n_inst - lo);
+
+    // (1) Holders of the first block among the eligible instances.
+    uint32_t nCand = 0;
+    if (nA > 0 && ell > 0) {
+      const IdxHit h0 = index_lookup(a.x, stage[0], g == 0, g, s);
+      const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
+      const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
+      if (found0) {
+        for (uint32_t t0 = 0; t0 < cnt0; t0 += 64) {
+          const uint32_t t = t0 + lane;
+          const uint32_t id = t < cnt0 ? a.x.holders[off0 + t] : 0u;
+          const bool el = t < cnt0 && a.room[id] >= L;
+          const uint64_t em = __ballot(el);
+          const uint32_t rank = nCand + (uint32_t)__popcll(em & lt_mask);
+          if (el) {
+            if (rank < 64) cl[rank] = (uint16_t)id;
+            atomicOr(reinterpret_cast<unsigned long long*>(&bmC[id >> 6]), 1ull << (id & 63));
+          }
+          nCand += (uint32_t)__popcll(em);
+        }
+      }
+    }
+    __syncthreads();
+    const bool few = nCand <= 64;
+
+    // Walks.  few: each holder on its own table; else: all live holders
+    // through the index, one position at a time.
+    uint32_t myid = 0, myhit = 0;
+    if (few) {
+      if ((uint32_t)lane < nCand) myid = cl[lane];
+      for (uint32_t k = 0; k < nCand; ++k) {
+        const uint32_t id = (uint32_t)__shfl((int)myid, (int)k);
+        const uint32_t hk = ell > 1 ? run_walk<true>(a.t, id, c, stage, 0, g, s) : 1u;
+        if ((uint32_t)lane == k) myhit = hk;
+      }
+    } else {
+      for (int32_t w = lane; w < nw; w += 64) bmA[w] = bmC[w];
+      __syncthreads();
+      uint32_t nalive = nCand;
+      int32_t p = 1;
+      while (p < ell && nalive > 0) {
+        if (nalive == 1) {  // a single live holder: walk its own table
+          uint32_t who = 0;
+          for (int32_t w0 = 0; w0 < nw; w0 += 64) {
+            const int32_t w = w0 + lane;
+            const uint64_t word = w < nw ? bmA[w] : 0ull;
+            const uint64_t any = __ballot(word != 0ull);
+            if (any) {
+              const int ln = __builtin_ctzll(any);
+              const uint64_t wd = __shfl(word, ln);
+              who = (uint32_t)((w0 + ln) * 64 + __builtin_ctzll(wd));
+              break;
+            }
+          }
+          const uint32_t hk = run_walk<true>(a.t, who, c, stage, p, g, s);
+          if (lane == 0) {
+            hits[who] = encode_hit(hk);
+            bmA[who >> 6] = 0ull;
+          }
+          nalive = 0;
+          __syncthreads();
+          break;
+        }
+        const int32_t jq = p + g;
+        const uint64_t kq = jq < ell ? ((jq < kStage) ? stage[jq] : chain_global(c, jq)) : 0ull;
+        const IdxHit hq = index_lookup(a.x, kq, jq < ell, g, s);
+        int32_t used = 0;
+        for (int t = 0; t < 8; ++t) {
+          const int32_t pos = p + t;
+          if (pos >= ell || nalive <= 1) break;
+          const bool f = __shfl(hq.found ? 1 : 0, 8 * t) != 0;
+          const uint32_t off = __shfl(hq.off, 8 * t), cnt = __shfl(hq.cnt, 8 * t);
+          if (f) {
+            for (uint32_t t0 = 0; t0 < cnt; t0 += 64) {
+              const uint32_t tt = t0 + lane;
+              if (tt < cnt) {
+                const uint32_t id = a.x.holders[off + tt];
+                if (test_bit(bmA, id))
+                  atomicOr(reinterpret_cast<unsigned long long*>(&bmN[id >> 6]), 1ull << (id & 63));
+              }
+            }
+          }
+          __syncthreads();
+          uint32_t live = 0;
+          for (int32_t w = lane; w < nw; w += 64) {
+            const uint64_t aw = bmA[w], nwd = bmN[w];
+            uint64_t d = aw & ~nwd;
+            while (d) {
+              const int b = __builtin_ctzll(d);
+              d &= d - 1;
+              hits[w * 64 + b] = encode_hit((uint32_t)pos);
+            }
+            bmA[w] = nwd;
+            bmN[w] = 0ull;
+            live += (uint32_t)__popcll(nwd);
+          }
+          __syncthreads();
+          nalive = wave_sum_u32(live);
+          used = t + 1;
+        }
+        p += used;
+      }
+      if (nalive > 0) {  // survived to the end of the chain
+        for (int32_t w = lane; w < nw; w += 64) {
+          uint64_t d = bmA[w];
+          while (d) {
+            const int b = __builtin_ctzll(d);
+            d &= d - 1;
+            hits[w * 64 + b] = encode_hit((uint32_t)ell);
+          }
+          bmA[w] = 0ull;
+        }
+      }
+      __syncthreads();
+    }
+
+    // (2)-(3) Minimum recomputation penalty over A.  Every eligible
+    // non-holder has hit 0 and the penalty W(n = L).
+    const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
+    const float W0 = fmaxf(0.0f, Z);
+    const uint32_t n0 = nA - nCand;
+    uint32_t wmin_bits = n0 > 0 ? __float_as_uint(W0) : 0x7F800000u;
+    if (few) {
+      if ((uint32_t)lane < nCand) {
+        const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)myhit * m.bs), Lf));
+        const uint32_t wb = __float_as_uint(W);
+        wmin_bits = wb < wmin_bits ? wb : wmin_bits;
+      }
+    } else {
+      for (int32_t base = 0; base < n_inst; base += 64) {
+        const int32_t i = base + lane;
+        const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
+        uint32_t v = cand ? hits[i] : 0u;
+        uint64_t ovf = __ballot(cand && v == kHitOverflow);
+        while (ovf) {  // hits beyond the u16 slot: walk again
+          const int k = __builtin_ctzll(ovf);
+          ovf &= ovf - 1;
+          const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+          if (lane == k) v = hk;
+        }
+        if (cand) {
+          const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)v * m.bs), Lf));
+          const uint32_t wb = __float_as_uint(W);
           wmin_bits = wb < wmin_bits ? wb : wmin_bits;
         }
       }
     }
-    if (PROBE_ALL) continue;
-    nA = wave_sum_u32(nA);
     const float wmin = __uint_as_float((uint32_t)wave_min_u64((uint64_t)wmin_bits));
 
-    // (2)-(4) Filters and keys over A; instance state is read only for the
-    // candidates that pass the recomputation filter.
-    const float Z = recompute_raw(m, Lf, Lf);   // T_pf(L, 0) - T_pf(0, L)
+    // (3)-(4) Filters and keys.  The hit-0 class is visited only if its
+    // common penalty passes Eq. 9.
     const float tpf_cold = t_prefill(m, Lf, 0.0f);
     const float slo = fmaxf(m.ttft_floor, tpf_cold);
     const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
-    const bool tpot_filter = !(m.flags & PS_F_NO_TPOT_FILTER);
-    const bool ttft_admit = (m.flags & PS_F_TTFT_ADMIT) != 0;
-    uint64_t keyT = ~0ull, keyF = ~0ull;
-    uint32_t nC = 0, nT = 0;
+    const bool admit0 = n0 > 0 && (!kvc || (W0 - wmin) / Z <= m.eta);
+    Acc acc{~0ull, ~0ull, 0u, 0u};
     if (nA > 0) {
-      for (int32_t base = 0; base < n_inst; base += 64) {
-        const int32_t i = base + lane;
-        uint32_t v = i < n_inst ? hits[i] : kInelig;
-        uint64_t ovf = __ballot(v == kHitOverflow);
-        while (ovf) {  // hits beyond the u16 slot: walk again (chains > 65533 blocks)
-          const int k = __builtin_ctzll(ovf);
-          ovf &= ovf - 1;
-          const uint32_t hk = deep_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
-          if (lane == k) v = hk;
-        }
-        if (v == kInelig) continue;
-        const int64_t c_tok = (int64_t)v * m.bs;
-        const int64_t n_tok = L - c_tok;
-        const float n = (float)n_tok;
-        if (kvc) {
-          const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
-          if (!((W - wmin) / Z <= m.eta)) continue;
-        }
-        ++nC;
-        const InstState st = a.inst[i];
-        const Lat lt = latency(m, st, n, (float)c_tok, L);
-        const uint64_t lm = (uint64_t)(st.P + n_tok) * (uint64_t)st.A1;
-        const uint64_t kf = (lm << 16) | (uint64_t)i;
-        keyF = kf < keyF ? kf : keyF;
-        const bool inT = (!tpot_filter || lt.tpot < m.tau) && (!ttft_admit || lt.ttft <= slo);
-        if (inT) {
-          ++nT;
-          const uint64_t kt = ((uint64_t)(PS_MAX_DQ - st.D) << 52) |
-                              ((uint64_t)(PS_MAX_CHAIN - v) << 28) | ((uint64_t)st.Q << 16) |
-                              (uint64_t)i;
-          keyT = kt < keyT ? kt : keyT;
+      if (few) {
+        if ((uint32_t)lane < nCand) evaluate(a, m, acc, myid, myhit, L, Lf, wmin, Z, kvc, slo);
+      }
+      if (admit0 || !few) {
+        for (int32_t base = 0; base < n_inst; base += 64) {
+          const int32_t i = base + lane;
+          const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
+          uint32_t v = (cand && !few) ? hits[i] : 0u;
+          uint64_t ovf = __ballot(cand && !few && v == kHitOverflow);
+          while (ovf) {
+            const int k = __builtin_ctzll(ovf);
+            ovf &= ovf - 1;
+            const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+            if (lane == k) v = hk;
+          }
+          if (i >= n_inst) continue;
+          if (cand) {
+            if (!few) evaluate(a, m, acc, (uint32_t)i, v, L, Lf, wmin, Z, kvc, slo);
+          } else if (admit0 && a.room[i] >= L) {
+            evaluate(a, m, acc, (uint32_t)i, 0u, L, Lf, wmin, Z, kvc, slo);
+          }
         }
       }
     }
-    keyT = wave_min_u64(keyT);
-    keyF = wave_min_u64(keyF);
-    nC = wave_sum_u32(nC);
-    nT = wave_sum_u32(nT);
+    const uint64_t keyT = wave_min_u64(acc.keyT);
+    const uint64_t keyF = wave_min_u64(acc.keyF);
+    const uint32_t nC = wave_sum_u32(acc.nC);
+    const uint32_t nT = wave_sum_u32(acc.nT);
 
     // Decision.  With finite arithmetic C holds at least the minimum-penalty
     // candidate whenever A is non-empty; the key test only keeps a
@@ -443,8 +773,16 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
         best = (uint32_t)(keyF & 0xFFFFu);
         fl |= PS_R_FALLBACK;
       }
-      uint32_t v = hits[best];
-      if (v == kHitOverflow) v = deep_walk<true>(a.t, best, c, stage, 0, g, s);
+      uint32_t v = 0;
+      if (test_bit(bmC, best)) {
+        if (few) {
+          const uint64_t mk = __ballot((uint32_t)lane < nCand && myid == best);
+          v = (uint32_t)__shfl((int)myhit, __builtin_ctzll(mk));
+        } else {
+          v = hits[best];
+          if (v == kHitOverflow) v = run_walk<true>(a.t, best, c, stage, 0, g, s);
+        }
+      }
       const int64_t c_tok = (int64_t)v * m.bs;
       const InstState st = a.inst[best];
       const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
@@ -458,6 +796,13 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
         a.sizes[3 * (size_t)r + 1] = nC;
         a.sizes[3 * (size_t)r + 2] = nT;
       }
+    }
+    // leave the candidate bitmap clear for the next request
+    __syncthreads();
+    if (few) {
+      if ((uint32_t)lane < nCand) bmC[myid >> 6] = 0ull;
+    } else {
+      for (int32_t w = lane; w < nw; w += 64) bmC[w] = 0ull;
     }
   }
 }
@@ -506,7 +851,12 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
       const uint32_t rank = (uint32_t)__popcll(wm & ((1ull << lane) - 1ull));
       const uint32_t room = a.cap > count ? a.cap - count : 0u;
       const bool ins = want && rank < room;
-      if (ins) (void)insert_key(a.t, inst, key);
+      if (ins) {  // new blocks join the row in chain order
+        uint32_t slot = 0;
+        (void)insert_key(a.t, inst, key, &slot);
+        a.t.rows[(size_t)inst * a.t.row_cap + count + rank] = key;
+        a.t.rowpos[(size_t)inst * a.t.slots + slot] = count + rank;
+      }
       const uint64_t im = __ballot(ins);
       const uint64_t dup_drop = __ballot(in && dup && !present && !((im >> first) & 1ull));
       const uint32_t nins = (uint32_t)__popcll(im);
@@ -528,8 +878,10 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
 
 // ------------------------------------------------------------------ launchers
 size_t ps_score_lds_bytes(int32_t n_inst) {
-  const size_t hits = ps_hits_fit_lds(n_inst) ? ((size_t)n_inst * sizeof(uint16_t) + 15) / 16 * 16 : 0;
-  return (size_t)kStage * sizeof(uint64_t) + hits;
+  const size_t nw = ((size_t)n_inst + 63) / 64;
+  const size_t hits = ps_hits_fit_lds(n_inst) ? (size_t)n_inst * sizeof(uint16_t) : 0;
+  return (size_t)kStage * sizeof(uint64_t) + 3 * nw * sizeof(uint64_t) + 64 * sizeof(uint16_t) +
+         (hits + 15) / 16 * 16;
 }
 
 bool ps_hits_fit_lds(int32_t n_inst) {
@@ -544,20 +896,26 @@ hipError_t ps_launch_build(const BuildArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t ps_launch_rows(const BuildArgs& a, hipStream_t s) {
+  if (a.n_blk == 0) return hipSuccess;
+  int64_t blocks = (a.n_blk + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(row_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s) {
   if (a.n_req == 0) return hipSuccess;
-  const size_t lds = ps_score_lds_bytes(hits_in_lds ? a.n_inst : PS_MAX_INST);
-  if (hits_in_lds) {
-    if (probe_all)
-      hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(64), lds, s, a);
-    else
-      hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
+  if (probe_all) {
+    hipLaunchKernelGGL(probe_all_kernel, dim3(grid), dim3(64), (size_t)kStage * sizeof(uint64_t), s,
+                       a);
   } else {
-    if (probe_all)
-      hipLaunchKernelGGL((score_kernel<false, true>), dim3(grid), dim3(64), lds, s, a);
+    const size_t lds = ps_score_lds_bytes(a.n_inst);
+    if (hits_in_lds)
+      hipLaunchKernelGGL(score_kernel<true>, dim3(grid), dim3(64), lds, s, a);
     else
-      hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
+      hipLaunchKernelGGL(score_kernel<false>, dim3(grid), dim3(64), lds, s, a);
   }
   return hipGetLastError();
 }
