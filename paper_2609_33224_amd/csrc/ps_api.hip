@@ -39,7 +39,7 @@ struct ps_ctx {
   InstState* d_inst = nullptr;
   int64_t* d_room = nullptr;
   int64_t* d_room_sorted = nullptr;
-  GIndex x{nullptr, nullptr, 0, 64};
+  GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
   uint16_t* d_scratch = nullptr;
@@ -433,7 +433,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.d_inst = nullptr;
   fresh.d_room = nullptr;
   fresh.d_room_sorted = nullptr;
-  fresh.x = GIndex{nullptr, nullptr, 0, 64};
+  fresh.x = GIndex{nullptr, nullptr, nullptr, 0, 0, 64};
   fresh.d_scratch = nullptr;
   return PS_OK;
 }

@@ -77,16 +77,22 @@ __host__ __device__ __forceinline__ uint32_t bucket_of(uint64_t key, uint32_t in
 // of instances holding it (the GPU form of a prefix tree over chained hashes:
 // one hash names one prefix).  16-byte entries, buckets of 8 = one 128-byte
 // line, multiply-shift bucket with the salt kIndexSalt, linear probing.
+// A hash held by more than kPopular instances keeps its holders as a bitmap
+// of the pool (nw 64-bit words; `off` = bitmap number); otherwise as an
+// ascending list of ids (`off` = first list entry).
 struct alignas(16) IdxEntry {
   uint64_t key;   // 0 = empty
-  uint32_t off;   // first holder in `holders`
+  uint32_t off;   // list offset, or bitmap number when cnt > kPopular
   uint32_t cnt;   // number of holders
 };
 constexpr uint32_t kIndexSalt = 0x10000u;  // not an instance id
+constexpr uint32_t kPopular = 64;
 
 struct GIndex {
   IdxEntry* ent;
   uint16_t* holders;
+  uint64_t* bitmaps;  // n_popular * nw words
+  uint32_t nw;        // words per bitmap = ceil(n_inst / 64)
   uint32_t bmask;
   uint32_t shift;
 };

@@ -30,9 +30,30 @@ __global__ void extract_kernel(Tables t, int32_t n_inst, const int64_t* base, ui
   }
 }
 
+// Popular hashes: set the bits of their holders in their bitmap
+// (bitmap number = exclusive scan of the popular flags).
+__global__ void bitmap_kernel(GIndex x, const uint32_t* uc, const uint32_t* uo,
+                              const uint32_t* pop_rank, const int* n_runs) {
+  const int n = *n_runs;
+  for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n; k += gridDim.x * blockDim.x) {
+    if (uc[k] <= kPopular) continue;
+    uint64_t* bm = x.bitmaps + (size_t)pop_rank[k] * x.nw;
+    for (uint32_t t = 0; t < uc[k]; ++t) {
+      const uint32_t id = x.holders[uo[k] + t];
+      atomicOr(reinterpret_cast<unsigned long long*>(&bm[id >> 6]), 1ull << (id & 63));
+    }
+  }
+}
+
+__global__ void popular_flag_kernel(const uint32_t* uc, uint32_t* flag, const int* n_runs) {
+  const int n = *n_runs;
+  for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n; k += gridDim.x * blockDim.x)
+    flag[k] = uc[k] > kPopular ? 1u : 0u;
+}
+
 __global__ void insert_index_kernel(GIndex x, const uint64_t* uk, const uint32_t* uc,
-                                    const uint32_t* uo, const int* n_runs,
-                                    unsigned long long* full) {
+                                    const uint32_t* uo, const uint32_t* pop_rank,
+                                    const int* n_runs, unsigned long long* full) {
   const int n = *n_runs;
   for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n; k += gridDim.x * blockDim.x) {
     const uint64_t key = uk[k];
@@ -44,7 +65,7 @@ __global__ void insert_index_kernel(GIndex x, const uint64_t* uk, const uint32_t
         unsigned long long old = atomicCAS(reinterpret_cast<unsigned long long*>(&bp[s].key), 0ull,
                                            (unsigned long long)key);
         if (old == 0ull) {
-          bp[s].off = uo[k];
+          bp[s].off = uc[k] > kPopular ? pop_rank[k] : uo[k];
           bp[s].cnt = uc[k];
           done = true;
           break;
@@ -67,6 +88,7 @@ void dfree(T*& p) {
 void ps_free_index(GIndex* x) {
   dfree(x->ent);
   dfree(x->holders);
+  dfree(x->bitmaps);
   x->bmask = 0;
   x->shift = 64;
 }
@@ -87,14 +109,15 @@ hipError_t ps_build_index(const Tables& t, int32_t n_inst, const uint32_t* count
   unsigned int* d_cursor = nullptr;
   uint64_t *pk = nullptr, *sk = nullptr, *uk = nullptr;
   uint16_t *pv = nullptr, *sv = nullptr;
-  uint32_t *uc = nullptr, *uo = nullptr;
+  uint32_t *uc = nullptr, *uo = nullptr, *pflag = nullptr, *prank = nullptr;
+  uint32_t n_pop = 0;
   int* d_runs = nullptr;
   unsigned long long* d_full = nullptr;
   void* tmp = nullptr;
   size_t tmp_bytes = 0, b1 = 0, b2 = 0, b3 = 0;
   int runs = 0;
   unsigned long long full = 0;
-  GIndex nx{nullptr, nullptr, 0, 64};
+  GIndex nx{nullptr, nullptr, nullptr, (uint32_t)((n_inst + 63) / 64), 0, 64};
   const int nn = (int)(n > 0 ? n : 1);
   int64_t buckets = 1;
   int log2b = 0;
@@ -108,6 +131,8 @@ hipError_t ps_build_index(const Tables& t, int32_t n_inst, const uint32_t* count
   TRY(hipMalloc(&sv, (size_t)nn * sizeof(uint16_t)));
   TRY(hipMalloc(&uc, (size_t)nn * sizeof(uint32_t)));
   TRY(hipMalloc(&uo, (size_t)nn * sizeof(uint32_t)));
+  TRY(hipMalloc(&pflag, (size_t)nn * sizeof(uint32_t)));
+  TRY(hipMalloc(&prank, (size_t)nn * sizeof(uint32_t)));
   TRY(hipMalloc(&d_runs, sizeof(int)));
   TRY(hipMalloc(&d_full, sizeof(unsigned long long)));
   TRY(hipMemcpyAsync(d_base, base.data(), base.size() * sizeof(int64_t), hipMemcpyHostToDevice, s));
@@ -131,6 +156,20 @@ hipError_t ps_build_index(const Tables& t, int32_t n_inst, const uint32_t* count
     TRY(hipMemcpyAsync(&runs, d_runs, sizeof(int), hipMemcpyDeviceToHost, s));
     TRY(hipStreamSynchronize(s));
     TRY(hipcub::DeviceScan::ExclusiveSum(tmp, tmp_bytes, uc, uo, runs, s));
+    {
+      int blocks = (runs + 255) / 256;
+      if (blocks > 65536) blocks = 65536;
+      hipLaunchKernelGGL(popular_flag_kernel, dim3(blocks), dim3(256), 0, s, uc, pflag, d_runs);
+      TRY(hipGetLastError());
+    }
+    TRY(hipcub::DeviceScan::ExclusiveSum(tmp, tmp_bytes, pflag, prank, runs, s));
+    {
+      uint32_t last_flag = 0, last_rank = 0;
+      TRY(hipMemcpyAsync(&last_flag, pflag + runs - 1, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+      TRY(hipMemcpyAsync(&last_rank, prank + runs - 1, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+      TRY(hipStreamSynchronize(s));
+      n_pop = last_flag + last_rank;
+    }
   }
   // table of >= 2 * runs entries in buckets of 8
   while (buckets * kSlotsPerBucket < 2 * (int64_t)runs) {
@@ -141,12 +180,21 @@ hipError_t ps_build_index(const Tables& t, int32_t n_inst, const uint32_t* count
   nx.shift = (uint32_t)(64 - log2b);
   TRY(hipMalloc(&nx.ent, (size_t)buckets * kSlotsPerBucket * sizeof(IdxEntry)));
   TRY(hipMemsetAsync(nx.ent, 0, (size_t)buckets * kSlotsPerBucket * sizeof(IdxEntry), s));
+  if (n_pop > 0) {
+    TRY(hipMalloc(&nx.bitmaps, (size_t)n_pop * nx.nw * sizeof(uint64_t)));
+    TRY(hipMemsetAsync(nx.bitmaps, 0, (size_t)n_pop * nx.nw * sizeof(uint64_t), s));
+  }
   if (runs > 0) {
     int blocks = (runs + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(insert_index_kernel, dim3(blocks), dim3(256), 0, s, nx, uk, uc, uo, d_runs,
-                       d_full);
+    nx.holders = sv;  // read by bitmap_kernel
+    hipLaunchKernelGGL(insert_index_kernel, dim3(blocks), dim3(256), 0, s, nx, uk, uc, uo, prank,
+                       d_runs, d_full);
     TRY(hipGetLastError());
+    if (n_pop > 0) {
+      hipLaunchKernelGGL(bitmap_kernel, dim3(blocks), dim3(256), 0, s, nx, uc, uo, prank, d_runs);
+      TRY(hipGetLastError());
+    }
   }
   TRY(hipMemcpyAsync(&full, d_full, sizeof full, hipMemcpyDeviceToHost, s));
   TRY(hipStreamSynchronize(s));
@@ -159,8 +207,10 @@ hipError_t ps_build_index(const Tables& t, int32_t n_inst, const uint32_t* count
   ps_free_index(x);
   *x = nx;
   nx.ent = nullptr;
+  nx.bitmaps = nullptr;
 done:
   if (nx.ent) (void)hipFree(nx.ent);
+  if (nx.bitmaps) (void)hipFree(nx.bitmaps);
   dfree(d_base);
   dfree(d_cursor);
   dfree(pk);
@@ -170,6 +220,8 @@ done:
   dfree(sv);
   dfree(uc);
   dfree(uo);
+  dfree(pflag);
+  dfree(prank);
   dfree(d_runs);
   dfree(d_full);
   if (tmp) (void)hipFree(tmp);

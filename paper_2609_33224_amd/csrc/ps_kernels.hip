@@ -77,6 +77,17 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Exclusive prefix sum of v over the lanes of the wave.
+__device__ __forceinline__ uint32_t wave_exclusive_sum(uint32_t v, int lane) {
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)x, d);
+    if (lane >= d) x += y;
+  }
+  return x - v;
+}
+
 // ------------------------------------------------------------------- probing
 // Octet probing: the 8 lanes of an octet (lanes 8g .. 8g+7) read the 8 slots
 // of one 64-byte bucket, so every wave-wide load is 8 coalesced 64-byte
@@ -581,7 +592,28 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
       const IdxHit h0 = index_lookup(a.x, stage[0], g == 0, g, s);
       const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
       const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
-      if (found0) {
+      if (found0 && cnt0 > kPopular) {  // holders as a bitmap: lanes over its words
+        const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
+        for (int32_t w0 = 0; w0 < nw; w0 += 64) {
+          const int32_t w = w0 + lane;
+          uint64_t d = w < nw ? bm[w] : 0ull, el_bits = 0ull;
+          while (d) {
+            const int b = __builtin_ctzll(d);
+            d &= d - 1;
+            if (a.room[w * 64 + b] >= L) el_bits |= 1ull << b;
+          }
+          const uint32_t cntl = (uint32_t)__popcll(el_bits);
+          uint32_t rank = nCand + wave_exclusive_sum(cntl, lane);
+          if (w < nw) bmC[w] = el_bits;
+          uint64_t e2 = el_bits;
+          while (e2 && rank < 64) {
+            const int b = __builtin_ctzll(e2);
+            e2 &= e2 - 1;
+            cl[rank++] = (uint16_t)(w * 64 + b);
+          }
+          nCand += wave_sum_u32(cntl);
+        }
+      } else if (found0) {
         for (uint32_t t0 = 0; t0 < cnt0; t0 += 64) {
           const uint32_t t = t0 + lane;
           const uint32_t id = t < cnt0 ? a.x.holders[off0 + t] : 0u;
@@ -646,6 +678,25 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
           if (pos >= ell || nalive <= 1) break;
           const bool f = __shfl(hq.found ? 1 : 0, 8 * t) != 0;
           const uint32_t off = __shfl(hq.off, 8 * t), cnt = __shfl(hq.cnt, 8 * t);
+          if (f && cnt > kPopular) {  // live &= holder bitmap, lane-owned words
+            const uint64_t* bm = a.x.bitmaps + (size_t)off * a.x.nw;
+            uint32_t live = 0;
+            for (int32_t w = lane; w < nw; w += 64) {
+              const uint64_t aw = bmA[w];
+              const uint64_t nwd = aw & bm[w];
+              uint64_t d = aw & ~nwd;
+              while (d) {
+                const int b = __builtin_ctzll(d);
+                d &= d - 1;
+                hits[w * 64 + b] = encode_hit((uint32_t)pos);
+              }
+              bmA[w] = nwd;
+              live += (uint32_t)__popcll(nwd);
+            }
+            nalive = wave_sum_u32(live);
+            used = t + 1;
+            continue;
+          }
           if (f) {
             for (uint32_t t0 = 0; t0 < cnt; t0 += 64) {
               const uint32_t tt = t0 + lane;

@@ -140,6 +140,8 @@ def test_edge_single_instance_and_ragged_counts(ps, scorer):
         sets = [ch[:int(rng.integers(0, 300))] for _ in range(n_inst)]
         chains = [ch[:k] for k in (1, 2, 65, 150, 300)] + [(ch[:100], chain_hashes(5, base=10**9))]
         _check_edge(ps, scorer, _edge(sets, chains), f"n_inst={n_inst}")
+        # part of the pool at its batch limit: holders that are not eligible
+        _check_edge(ps, scorer, _edge(sets, chains, b_max=40), f"n_inst={n_inst} b_max=40")
 
 
 def test_edge_chain_lengths_around_stage(ps, scorer):
