@@ -39,6 +39,7 @@ struct ps_ctx {
   InstState* d_inst = nullptr;
   int64_t* d_room = nullptr;
   int64_t* d_room_sorted = nullptr;
+  uint32_t* d_order0 = nullptr;
   GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
@@ -196,6 +197,7 @@ void free_snapshot(ps_ctx* c) {
   dfree(c->d_inst);
   dfree(c->d_room);
   dfree(c->d_room_sorted);
+  dfree(c->d_order0);
   dfree(c->d_scratch);
   ps_free_index(&c->x);
   c->loaded = false;
@@ -208,6 +210,19 @@ std::vector<int64_t> rooms_of(const std::vector<InstState>& hs, const DevModel& 
   std::vector<int64_t> r(hs.size());
   for (size_t i = 0; i < hs.size(); ++i) r[i] = hs[i].A1 <= m.b_max ? m.kv_cap - hs[i].S : -1;
   return r;
+}
+
+// Instance ids in the order of the packing key of a candidate with no cached
+// prefix: most decoding first, then fewest queued, then lowest id.
+std::vector<uint32_t> key_order(const std::vector<InstState>& hs) {
+  std::vector<uint32_t> o(hs.size());
+  for (size_t i = 0; i < o.size(); ++i) o[i] = (uint32_t)i;
+  std::sort(o.begin(), o.end(), [&](uint32_t x, uint32_t y) {
+    if (hs[x].D != hs[y].D) return hs[x].D > hs[y].D;
+    if (hs[x].Q != hs[y].Q) return hs[x].Q < hs[y].Q;
+    return x < y;
+  });
+  return o;
 }
 
 }  // namespace
@@ -326,6 +341,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     dfree(fresh.d_inst);
     dfree(fresh.d_room);
     dfree(fresh.d_room_sorted);
+    dfree(fresh.d_order0);
     dfree(fresh.d_scratch);
     ps_free_index(&fresh.x);
     dfree(d_off);
@@ -343,6 +359,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst, (size_t)n * sizeof(InstState));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room_sorted, (size_t)n * sizeof(int64_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_order0, (size_t)n * sizeof(uint32_t));
   if (e == hipSuccess && rows)
     e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint16_t));
   if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
@@ -366,6 +383,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   const std::vector<int64_t> hroom = rooms_of(hs, dm);
   std::vector<int64_t> hroom_sorted = hroom;
   std::sort(hroom_sorted.begin(), hroom_sorted.end());
+  const std::vector<uint32_t> horder0 = key_order(hs);
   hipStream_t sm = c->stream;
   e = hipMemsetAsync(fresh.t.keys, 0, tab_bytes, sm);
   if (e == hipSuccess) e = hipMemsetAsync(fresh.t.count, 0, (size_t)n * sizeof(uint32_t), sm);
@@ -380,6 +398,9 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     e = hipMemcpyAsync(fresh.d_room, hroom.data(), hroom.size() * sizeof(int64_t), hipMemcpyHostToDevice, sm);
   if (e == hipSuccess)
     e = hipMemcpyAsync(fresh.d_room_sorted, hroom_sorted.data(), hroom_sorted.size() * sizeof(int64_t),
+                       hipMemcpyHostToDevice, sm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(fresh.d_order0, horder0.data(), horder0.size() * sizeof(uint32_t),
                        hipMemcpyHostToDevice, sm);
   BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter, d_won, d_slot, d_rank};
   if (e == hipSuccess) e = ps_launch_build(ba, sm);
@@ -416,6 +437,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->d_inst = fresh.d_inst;
   c->d_room = fresh.d_room;
   c->d_room_sorted = fresh.d_room_sorted;
+  c->d_order0 = fresh.d_order0;
   c->x = fresh.x;
   c->d_scratch = fresh.d_scratch;
   c->scratch_rows = rows;
@@ -433,6 +455,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.d_inst = nullptr;
   fresh.d_room = nullptr;
   fresh.d_room_sorted = nullptr;
+  fresh.d_order0 = nullptr;
   fresh.x = GIndex{nullptr, nullptr, nullptr, 0, 0, 64};
   fresh.d_scratch = nullptr;
   return PS_OK;
@@ -445,6 +468,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.t = c->t;
   a.x = c->x;
   a.room_sorted = c->d_room_sorted;
+  a.order0 = c->d_order0;
   a.inst = c->d_inst;
   a.room = c->d_room;
   a.model = c->d_model;
@@ -593,6 +617,8 @@ ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_
   std::vector<int64_t> rs = rooms_of(c->h_state, c->h_model);
   std::sort(rs.begin(), rs.end());
   HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+  const std::vector<uint32_t> o0 = key_order(c->h_state);
+  HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
   HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
   if (n_dropped) *n_dropped = (int64_t)dropped;
   return PS_OK;

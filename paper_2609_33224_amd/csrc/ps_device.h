@@ -101,6 +101,7 @@ struct ScoreArgs {
   Tables t;
   GIndex x;
   const int64_t* room_sorted;  // rooms ascending (eligible count = n - lower_bound(L))
+  const uint32_t* order0;      // instance ids by (decoding desc, queued asc, id asc)
   const InstState* inst;
   const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
   const DevModel* model;

@@ -88,6 +88,26 @@ __device__ __forceinline__ uint32_t wave_exclusive_sum(uint32_t v, int lane) {
   return x - v;
 }
 
+// Index of the first element >= L of an ascending array, 64 candidates per
+// step: lanes read 64 evenly spaced samples and a ballot narrows the range
+// by 64x (two dependent reads for up to 4096 elements).
+__device__ __forceinline__ int32_t wave_lower_bound(const int64_t* arr, int32_t n, int64_t L,
+                                                    int lane) {
+  int32_t lo = 0, hi = n;
+  while (hi - lo > 64) {
+    const int32_t stride = (hi - lo + 63) / 64;
+    const int32_t idx = lo + (lane + 1) * stride - 1;
+    const bool less = idx < hi && arr[idx] < L;
+    const int32_t c = (int32_t)__popcll(__ballot(less));
+    const int32_t nlo = lo + c * stride;
+    hi = hi < nlo + stride ? hi : nlo + stride;
+    lo = nlo;
+  }
+  const int32_t idx = lo + lane;
+  const bool less = idx < hi && arr[idx] < L;
+  return lo + (int32_t)__popcll(__ballot(less));
+}
+
 // ------------------------------------------------------------------- probing
 // Octet probing: the 8 lanes of an octet (lanes 8g .. 8g+7) read the 8 slots
 // of one 64-byte bucket, so every wave-wide load is 8 coalesced 64-byte
@@ -578,13 +598,7 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
     __syncthreads();
 
     // |A|: capacity-eligible instances are those with room >= L.
-    int32_t lo = 0, hi = n_inst;
-    while (lo < hi) {
-      const int32_t mid = (lo + hi) >> 1;
-      if (a.room_sorted[mid] < L) lo = mid + 1;
-      else hi = mid;
-    }
-    const uint32_t nA = (uint32_t)(n_inst - lo);
+    const uint32_t nA = (uint32_t)(n_inst - wave_lower_bound(a.room_sorted, n_inst, L, lane));
 
     // (1) Holders of the first block among the eligible instances.
     uint32_t nCand = 0;
@@ -784,24 +798,60 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
     if (nA > 0) {
       if (few) {
         if ((uint32_t)lane < nCand) evaluate(a, m, acc, myid, myhit, L, Lf, wmin, Z, kvc, slo);
-      }
-      if (admit0 || !few) {
+      } else {
         for (int32_t base = 0; base < n_inst; base += 64) {
           const int32_t i = base + lane;
           const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
-          uint32_t v = (cand && !few) ? hits[i] : 0u;
-          uint64_t ovf = __ballot(cand && !few && v == kHitOverflow);
+          uint32_t v = cand ? hits[i] : 0u;
+          uint64_t ovf = __ballot(cand && v == kHitOverflow);
           while (ovf) {
             const int k = __builtin_ctzll(ovf);
             ovf &= ovf - 1;
             const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
             if (lane == k) v = hk;
           }
-          if (i >= n_inst) continue;
-          if (cand) {
-            if (!few) evaluate(a, m, acc, (uint32_t)i, v, L, Lf, wmin, Z, kvc, slo);
-          } else if (admit0 && a.room[i] >= L) {
-            evaluate(a, m, acc, (uint32_t)i, 0u, L, Lf, wmin, Z, kvc, slo);
+          if (cand) evaluate(a, m, acc, (uint32_t)i, v, L, Lf, wmin, Z, kvc, slo);
+        }
+      }
+      if (admit0) {
+        // The eligible non-holders (hit 0) share n = L.  Without set sizes
+        // to report, only the best packing key of that class matters: the
+        // first member of T in key order (decoding desc, queued asc, id
+        // asc).  The whole class is evaluated when sizes are requested or
+        // when no member is in T (then the fallback key may come from it).
+        bool done0 = false;
+        if (!a.sizes) {
+          for (int32_t base = 0; base < n_inst && !done0; base += 64) {
+            const int32_t k = base + lane;
+            bool ok = false;
+            uint32_t i = 0;
+            if (k < n_inst) {
+              i = a.order0[k];
+              if (a.room[i] >= L && !test_bit(bmC, i)) {
+                const InstState st = a.inst[i];
+                const Lat lt = latency(m, st, Lf, 0.0f, L);
+                ok = ((m.flags & PS_F_NO_TPOT_FILTER) || lt.tpot < m.tau) &&
+                     (!(m.flags & PS_F_TTFT_ADMIT) || lt.ttft <= slo);
+              }
+            }
+            const uint64_t okm = __ballot(ok);
+            if (okm) {
+              if (lane == __builtin_ctzll(okm)) {
+                const InstState st = a.inst[i];
+                const uint64_t kt = ((uint64_t)(PS_MAX_DQ - st.D) << 52) |
+                                    ((uint64_t)PS_MAX_CHAIN << 28) | ((uint64_t)st.Q << 16) |
+                                    (uint64_t)i;
+                acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+              }
+              done0 = true;
+            }
+          }
+        }
+        if (!done0) {
+          for (int32_t base = 0; base < n_inst; base += 64) {
+            const int32_t i = base + lane;
+            if (i < n_inst && !test_bit(bmC, (uint32_t)i) && a.room[i] >= L)
+              evaluate(a, m, acc, (uint32_t)i, 0u, L, Lf, wmin, Z, kvc, slo);
           }
         }
       }

@@ -57,11 +57,15 @@ def test_decisions_full_window(ps, scorer, name):
     _say(f"decision parity {name}")
     w = synth.generate(name)
     load_window(scorer, w)
-    res, sizes = DeviceWindow(w).score(scorer)
+    dw = DeviceWindow(w)
+    res, sizes = dw.score(scorer)
     od = oracle.Oracle.from_window(w).window_score(w)
     nb = compare_decisions(res, sizes, od, label=name)
     _say(f"{name}: {w.n_req} decisions, {nb} near-boundary excluded")
     assert nb <= max(5, w.n_req // 200)
+    # the path without set sizes (the benchmark's) decides identically
+    res2, _ = dw.score(scorer, with_sizes=False)
+    assert res2.tobytes() == res.tobytes()
 
 
 def test_host_entry_point_matches_device(ps, scorer):
@@ -89,9 +93,12 @@ def test_policy_variants(ps, scorer, policy):
     _say(f"policy {policy}")
     w = synth.generate("c1")
     load_window(scorer, w, **policy)
-    res, sizes = DeviceWindow(w).score(scorer)
+    dw = DeviceWindow(w)
+    res, sizes = dw.score(scorer)
     od = oracle.Oracle.from_window(w).window_score(w, **policy)
     compare_decisions(res, sizes, od, label=str(policy))
+    res2, _ = dw.score(scorer, with_sizes=False)
+    assert res2.tobytes() == res.tobytes()
     if policy.get("b_max") == 1 or policy.get("kv_cap_tokens") == 0:
         assert (res["instance"] == -1).all() and (res["flags"] == ps.PS_R_REJECT).all()
     if policy.get("tpot_slo") == 1e-6:
@@ -130,6 +137,8 @@ def _check_edge(ps, scorer, w, label, **policy):
     res, sizes = dw.score(scorer)
     od = o.window_score(w, **policy)
     compare_decisions(res, sizes, od, label=label)
+    res2, _ = dw.score(scorer, with_sizes=False)
+    assert res2.tobytes() == res.tobytes(), f"{label}: path without sizes differs"
     return res
 
 
@@ -316,6 +325,8 @@ def test_full_size_sampled(ps, scorer, name):
     load_window(scorer, w)
     dw = DeviceWindow(w)
     res, sizes = dw.score(scorer)
+    res2, _ = dw.score(scorer, with_sizes=False)
+    assert res2.tobytes() == res.tobytes(), f"{name}: path without sizes differs"
     _say(f"full-size {name}: scored {w.n_req}; oracle sample")
     idx = np.sort(np.random.default_rng(5).choice(w.n_req, 384, replace=False))
     idx = np.unique(np.concatenate([idx, [0, w.n_req - 1]]))
