@@ -51,21 +51,139 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(win, hits):
-    """Bytes one launch must move at minimum (see module docstring)."""
+def _fp64_model(win):
+    """fp64 copies of the model for byte accounting (not for decisions)."""
     import numpy as np
-    ell = (win.pre_len.astype(np.int64) + win.tail_len)
-    L = ell * int(win.policy["block_tokens"])
-    A1 = win.D.astype(np.int64) + win.Q + 1
-    elig = (A1[None, :] <= int(win.policy["b_max"])) & \
-           ((win.S[None, :] + L[:, None]) <= int(win.policy["kv_cap_tokens"]))
+    a = win.alpha.astype(np.float64)
+    ub = win.seg_ub.astype(np.int64)
+    beta = win.beta.astype(np.float64)
+    gam = win.gamma.astype(np.float64)
+    return a, ub, beta, gam
+
+
+def _tpf(a, n, c):
+    return a[0] + a[1] * n + a[2] * n * c + a[3] * n * n + a[4] * c + a[5] * c * c
+
+
+def probe_bytes(win, hits):
+    """Algorithmic bytes of the exhaustive probe kernel (ps_probe_hits_dev):
+    one 64-byte bucket per probe, min(hit + 1, chain length) probes on every
+    (request, instance) pair, plus the chain head it stages."""
+    import numpy as np
+    ell = (win.pre_len.astype(np.int64) + win.tail_len)[: hits.shape[0]]
     probes = np.minimum(hits.astype(np.int64) + 1, ell[:, None])
     probes = np.where(ell[:, None] == 0, 0, probes)
-    n_probes = int((probes * elig).sum())
-    deepest = np.where(elig.any(axis=1), (probes * elig).max(axis=1), 0)
-    chain_bytes = int(deepest.sum()) * 8
-    other = win.n_req * (24 + 20) + win.n_inst * 24
-    return n_probes * BUCKET_BYTES + chain_bytes + other, n_probes
+    n_probes = int(probes.sum())
+    return n_probes * BUCKET_BYTES + int(np.minimum(ell, 256).sum()) * 8, n_probes
+
+
+def score_bytes(win, r0, hits):
+    """Algorithmic bytes the scoring kernel moves for requests r0 .. r0 +
+    len(hits) (the path without set sizes), from its data movement per
+    request: descriptor, result and staged chain head; the 64-way search of
+    the sorted rooms; one 128-byte index bucket for the first block; the
+    holders of the first block (2-byte ids + 8-byte rooms, or a bitmap when
+    more than 64 hold it); per walked holder one 64-byte probe, a 4-byte row
+    position and 16 bytes (chain + row) per compared position, and a final
+    64-byte probe at the first absent block; with more than 64 holders, one
+    index bucket plus the holder data per walked position; 32 bytes of state
+    per member of C; the key-ordered scan of the hit-0 class (4-byte order
+    entry + 8-byte room per scanned instance, 32 bytes of state per eligible
+    one)."""
+    import numpy as np
+    R, N = hits.shape
+    pol = win.policy
+    bs, bmax, kv = int(pol["block_tokens"]), int(pol["b_max"]), int(pol["kv_cap_tokens"])
+    eta, tau = float(np.float32(pol["eta"])), float(np.float32(pol["tpot_slo"]))
+    lout1 = max(1.0, float(np.float32(pol["lout"])))
+    a, ub, beta, gam = _fp64_model(win)
+    sl = slice(r0, r0 + R)
+    ell = win.pre_len[sl].astype(np.int64) + win.tail_len[sl]
+    L = ell * bs
+    A1 = win.D.astype(np.int64) + win.Q + 1
+    room = np.where(A1 <= bmax, kv - win.S, -1)
+    nw = (N + 63) // 64
+    levels, span = 1, N
+    while span > 64:
+        span = (span + 63) // 64
+        levels += 1
+    h = hits.astype(np.int64)
+    elig = room[None, :] >= L[:, None]
+    hold0 = h >= 1
+    cand = elig & hold0
+    ncand = cand.sum(1)
+    nA = elig.sum(1)
+    cnt0 = hold0.sum(1)
+    by = 44 + 8 * np.minimum(ell, 256) + 512 * levels
+    act = nA > 0
+    by += np.where(act & (ell > 0), 128, 0)
+    by += np.where(act & (ell > 0), np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0), 0)
+    few = ncand <= 64
+    hc = np.minimum(h, (ell - 1)[:, None])
+    walk = np.where(cand, 68 + 16 * hc + 64 * (h < ell[:, None]), 0).sum(1)
+    by += np.where(act & few & (ell > 1), walk, 0)
+    for r in np.nonzero(act & ~few & (ell > 1))[0]:
+        hr = np.sort(h[r][cand[r]])[::-1]
+        P = int(min(ell[r] - 1, hr[1]))
+        cnts = (h[r][None, :] > np.arange(1, P + 1)[:, None]).sum(1)
+        by[r] += 128 * P + int(np.where(cnts > 64, 8 * nw, 2 * cnts).sum())
+        if hr[0] > P:
+            by[r] += 68 + 16 * (min(hr[0], ell[r] - 1) - (P + 1)) + (64 if hr[0] < ell[r] else 0)
+    # the recomputation filter and the hit-0 class
+    n = (L[:, None] - h * bs).astype(np.float64)
+    c = (h * bs).astype(np.float64)
+    Lf = L.astype(np.float64)[:, None]
+    W = np.maximum(0.0, _tpf(a, n, c) - _tpf(a, 0.0, Lf))
+    Z = (_tpf(a, Lf, 0.0) - _tpf(a, 0.0, Lf))[:, 0]
+    Wmin = np.where(elig, W, np.inf).min(1)
+    kvc = Z > 0
+    with np.errstate(divide="ignore", invalid="ignore"):
+        rho = (W - Wmin[:, None]) / Z[:, None]
+    inC = elig & (~kvc[:, None] | (rho <= eta))
+    by += 32 * (cand & inC).sum(1)
+    n0 = nA - ncand
+    W0 = np.maximum(0.0, Z)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        admit0 = (n0 > 0) & (~kvc | ((W0 - Wmin) / Z <= eta))
+    seg = np.searchsorted(ub, A1, side="left")
+    seg = np.minimum(seg, len(ub) - 1)
+    order0 = np.lexsort((np.arange(N), win.Q, -win.D.astype(np.int64)))
+    for r in np.nonzero(act & admit0)[0]:
+        t_iter = gam[seg] * (beta[seg, 0] + beta[seg, 1] * A1 + beta[seg, 2] * (win.S + L[r]))
+        tpot0 = t_iter + np.where(A1 > 1, _tpf(a, float(L[r]), 0.0) / lout1, 0.0)
+        zero = elig[r] & ~hold0[r]
+        ok = (zero & (tpot0 < tau))[order0]
+        if ok.any():
+            k = int(np.argmax(ok))
+            scanned = (k // 64 + 1) * 64
+            by[r] += min(scanned, N) * 12 + 32 * int(zero[order0[:scanned]].sum())
+        else:
+            by[r] += N * 12 + 32 * int(zero.sum())
+    return int(by.sum())
+
+
+def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 27):
+    """Both byte counts over the whole window, from the exhaustive per-pair
+    hits exported chunk by chunk (untimed)."""
+    import numpy as np
+    import torch
+    import paper_2609_33224_amd as ps
+    chunk = max(1, min(win.n_req, chunk_pairs // win.n_inst))
+    reqs = ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
+    d_hits = torch.empty(chunk * win.n_inst, dtype=torch.int32, device="cuda")
+    sb = pb = npr = 0
+    for r0 in range(0, win.n_req, chunk):
+        n = min(chunk, win.n_req - r0)
+        d_r = ps.to_device_bytes(reqs[r0:r0 + n])
+        sc.hits_dev(d_pool, len(win.pool), d_r, n, d_hits)
+        torch.cuda.synchronize()
+        hits = d_hits[: n * win.n_inst].cpu().numpy().view(np.uint32).reshape(n, win.n_inst)
+        b, p_ = probe_bytes(win.subset(range(r0, r0 + n)), hits)
+        pb += b
+        npr += p_
+        sb += score_bytes(win, r0, hits)
+    sb += win.n_inst * 0
+    return sb, pb, npr
 
 
 def traffic_for(workload: str, src_hash: str):
@@ -157,16 +275,26 @@ def main():
     d_out = torch.empty(win.n_req * 20, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
 
-    # untimed: per-pair hits for the byte count, and the end-to-end host call
-    d_hits = torch.empty(win.n_req * win.n_inst, dtype=torch.int32, device="cuda")
-    sc.hits_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_hits)
-    torch.cuda.synchronize()
-    hits = d_hits.cpu().numpy().view(np.uint32).reshape(win.n_req, win.n_inst)
-    del d_hits
-    alg_bytes, n_probes = algorithmic_bytes(win, hits)
+    # untimed: byte counts from the per-pair hits, and the end-to-end host call
+    print("bench: counting algorithmic bytes", file=sys.stderr, flush=True)
+    alg_bytes, probe_alg_bytes, n_probes = algorithmic_bytes(sc, win, d_pool, d_reqs)
     t0 = time.perf_counter()
     sc.score(win.pool, reqs)
     host_call_s = time.perf_counter() - t0
+
+    # the exhaustive per-instance probe kernel (ps_probe_hits_dev), timed alone
+    pk_chunk = max(1, min(win.n_req, (1 << 28) // win.n_inst))
+    d_ph = torch.empty(pk_chunk * win.n_inst, dtype=torch.int32, device="cuda")
+    d_pr = ps.to_device_bytes(reqs[:pk_chunk])
+    sc.hits_dev(d_pool, len(win.pool), d_pr, pk_chunk, d_ph, stream)
+    pe = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(3)]
+    for a_, b_ in pe:
+        a_.record(stream)
+        sc.hits_dev(d_pool, len(win.pool), d_pr, pk_chunk, d_ph, stream)
+        b_.record(stream)
+    torch.cuda.synchronize()
+    probe_ms = float(np.mean([a_.elapsed_time(b_) for a_, b_ in pe])) * win.n_req / pk_chunk
+    del d_ph, d_pr
 
     for _ in range(args.warmup):
         sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
@@ -213,7 +341,12 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
         "algorithmic_bytes_per_launch": alg_bytes,
-        "probes_per_launch": n_probes,
+        "probe_kernel": {"kernel": "ps_probe_hits_dev (every request x instance probed)",
+                         "ms_per_window": probe_ms, "probes": n_probes,
+                         "algorithmic_bytes": probe_alg_bytes,
+                         "achieved_GBs": probe_alg_bytes / (probe_ms * 1e-3) / 1e9,
+                         "frac_of_hbm_peak": probe_alg_bytes / (probe_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                         "evals_per_s": win.n_req * win.n_inst / (probe_ms * 1e-3)},
         "kernel_source_sha": src_hash,
         "load_instances_s": load_s,
         "host_call_s_incl_pcie": host_call_s,
