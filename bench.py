@@ -265,7 +265,7 @@ def main():
     m = ps.make_model(win.alpha, win.seg_ub, win.beta, win.gamma, win.policy["eta"],
                       win.policy["tpot_slo"], win.policy["ttft_floor"], win.policy["lout"],
                       win.policy["block_tokens"], win.policy["b_max"],
-                      win.policy["kv_cap_tokens"], win.policy["flags"])
+                      win.policy["kv_cap_tokens"], win.policy["flags"], win.policy["rand_seed"])
     t0 = time.perf_counter()
     sc.load(win.n_inst, win.cap, win.blk_off, win.blk, win.D, win.Q, win.P, win.S, m)
     load_s = time.perf_counter() - t0

@@ -58,10 +58,33 @@ extern "C" {
 #define PS_MAX_BATCH 8191      /* B_max */
 #define PS_MAX_TABLE_CAP 67108864 /* distinct cached blocks per instance (2^26) */
 
-/* ps_model.flags */
+/*
+ * ps_model.flags.  The admission layers of the paper's layer ablation
+ * (Table 3) are: G = NO_KVC_FILTER | NO_TPOT_FILTER, C = NO_TPOT_FILTER,
+ * T = NO_KVC_FILTER | FALLBACK_DCQ, CT = FALLBACK_DCQ, F (full) = 0.
+ */
 #define PS_F_TTFT_ADMIT 1u     /* also require predicted TTFT <= the TTFT budget for T */
 #define PS_F_NO_KVC_FILTER 2u  /* skip the recomputation filter: C = A */
 #define PS_F_NO_TPOT_FILTER 4u /* skip the TPOT test: T = C (minus TTFT admission if on) */
+#define PS_F_FALLBACK_DCQ 8u   /* when T is empty choose over C by the D-C-Q key, not LMetric */
+/*
+ * Selection order within T (bits 8..11 of flags; the selector ablation of
+ * Table 4, plus LMetric alone).  D = most decoding requests, C = most cached
+ * blocks, Q = fewest queued requests, H = smallest TPOT headroom
+ * (tpot_slo - predicted TPOT); every order ends with the lowest id.  RANDOM
+ * takes the k-th member of T in id order, k = floor(z_hi * |T| / 2^32) with
+ * z the (r + 1)-th output of a SplitMix64 stream seeded with rand_seed for
+ * request r of the window.
+ */
+#define PS_SEL_DCQ 0u
+#define PS_SEL_D 1u
+#define PS_SEL_DQ 2u
+#define PS_SEL_DC 3u
+#define PS_SEL_DQC 4u
+#define PS_SEL_HCQ 5u
+#define PS_SEL_RANDOM 6u
+#define PS_SEL_LMETRIC 7u
+#define PS_F_SELECTOR(sel) ((uint32_t)(sel) << 8)
 
 /* ps_result.flags */
 #define PS_R_REJECT 1u    /* no capacity-eligible instance (Algorithm 1 returns Reject) */
@@ -89,7 +112,8 @@ typedef int32_t ps_status;
  *  block_tokens: tokens per block; b_max: engine batch limit; kv_cap_tokens:
  *         KV capacity in tokens (capacity guard: A_i + 1 <= b_max and
  *         S_i + L <= kv_cap_tokens).
- *  flags: PS_F_*.
+ *  flags: PS_F_* and PS_F_SELECTOR(PS_SEL_*).
+ *  rand_seed: seed of the random selector's stream.
  */
 typedef struct {
   float alpha[6];
@@ -101,6 +125,7 @@ typedef struct {
   int32_t block_tokens, b_max;
   int64_t kv_cap_tokens;
   uint32_t flags;
+  uint64_t rand_seed;
 } ps_model;
 
 /*

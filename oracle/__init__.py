@@ -27,10 +27,15 @@ if os.environ.get("PS_ORACLE_MUTANT_LIB"):
     _LIB_PATH = os.environ["PS_ORACLE_MUTANT_LIB"]
 _lib = None
 
-F_TTFT_ADMIT, F_NO_KVC_FILTER, F_NO_TPOT_FILTER = 1, 2, 4
+F_TTFT_ADMIT, F_NO_KVC_FILTER, F_NO_TPOT_FILTER, F_FALLBACK_DCQ = 1, 2, 4, 8
+SEL_DCQ, SEL_D, SEL_DQ, SEL_DC, SEL_DQC, SEL_HCQ, SEL_RANDOM, SEL_LMETRIC = range(8)
+
+
+def selector_flags(sel: int) -> int:
+    return (int(sel) & 0xF) << 8
 R_REJECT, R_FALLBACK, R_TTFT_MISS = 1, 2, 4
-NB_RHO, NB_TPOT, NB_TTFT, NB_Z, NB_MISSFLAG = 1, 2, 4, 8, 16
-NB_DECISION = NB_RHO | NB_TPOT | NB_TTFT | NB_Z
+NB_RHO, NB_TPOT, NB_TTFT, NB_Z, NB_MISSFLAG, NB_HEADROOM = 1, 2, 4, 8, 16, 32
+NB_DECISION = NB_RHO | NB_TPOT | NB_TTFT | NB_Z | NB_HEADROOM
 
 
 def build(verbose: bool = False) -> str:
@@ -60,11 +65,12 @@ class Model(ctypes.Structure):
         ("block_tokens", ctypes.c_int32), ("b_max", ctypes.c_int32),
         ("kv_cap", ctypes.c_int64),
         ("flags", ctypes.c_uint32),
+        ("rand_seed", ctypes.c_uint64),
     ]
 
 
 def make_model(alpha, seg_ub, beta, gamma, eta, tau, ttft_floor, lout, block_tokens, b_max,
-               kv_cap, flags=0) -> Model:
+               kv_cap, flags=0, rand_seed=0) -> Model:
     """Fill an oracle model.  Values are taken as given (Python floats are
     fp64; pass fp32 arrays to reproduce the interface precision exactly)."""
     m = Model()
@@ -78,6 +84,7 @@ def make_model(alpha, seg_ub, beta, gamma, eta, tau, ttft_floor, lout, block_tok
         m.gamma[s] = float(gamma[s])
     m.eta, m.tau, m.ttft_floor, m.lout = float(eta), float(tau), float(ttft_floor), float(lout)
     m.block_tokens, m.b_max, m.kv_cap, m.flags = int(block_tokens), int(b_max), int(kv_cap), int(flags)
+    m.rand_seed = int(rand_seed) & 0xFFFFFFFFFFFFFFFF
     return m
 
 
@@ -89,7 +96,7 @@ def model_of(win, **policy_overrides) -> Model:
                       win.gamma.astype(np.float64), np.float32(pol["eta"]),
                       np.float32(pol["tpot_slo"]), np.float32(pol["ttft_floor"]),
                       np.float32(pol["lout"]), pol["block_tokens"], pol["b_max"],
-                      pol["kv_cap_tokens"], pol.get("flags", 0))
+                      pol["kv_cap_tokens"], pol.get("flags", 0), pol.get("rand_seed", 0))
 
 
 def _load():

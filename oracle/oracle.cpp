@@ -64,16 +64,21 @@ typedef struct {
   int32_t block_tokens; // tokens per block
   int32_t b_max;        // engine batch limit
   int64_t kv_cap;       // KV capacity, tokens
-  uint32_t flags;       // 1 TTFT admission, 2 no KVC filter, 4 no TPOT filter
+  uint32_t flags;       // 1 TTFT admission, 2 no KVC filter, 4 no TPOT filter,
+                        // 8 fallback by the D-C-Q key; bits 8..11 selector
+  uint64_t rand_seed;   // seed of the random selector's stream
 } orc_model;
 
 }  // extern "C"
 
 namespace {
 
-constexpr uint32_t F_TTFT_ADMIT = 1u, F_NO_KVC = 2u, F_NO_TPOT = 4u;
+constexpr uint32_t F_TTFT_ADMIT = 1u, F_NO_KVC = 2u, F_NO_TPOT = 4u, F_FALLBACK_DCQ = 8u;
+// Selection orders within T (Table 4 of the paper, plus LMetric alone).
+enum Selector : uint32_t { SEL_DCQ = 0, SEL_D, SEL_DQ, SEL_DC, SEL_DQC, SEL_HCQ, SEL_RANDOM, SEL_LMETRIC };
 constexpr uint32_t R_REJECT = 1u, R_FALLBACK = 2u, R_TTFT_MISS = 4u;
-constexpr uint32_t NB_RHO = 1u, NB_TPOT = 2u, NB_TTFT = 4u, NB_Z = 8u, NB_MISSFLAG = 16u;
+constexpr uint32_t NB_RHO = 1u, NB_TPOT = 2u, NB_TTFT = 4u, NB_Z = 8u, NB_MISSFLAG = 16u,
+                   NB_HEADROOM = 32u;
 constexpr double NB_REL = 1e-5;
 
 struct Snapshot {
@@ -137,7 +142,17 @@ struct Decision {
 // Algorithm 1 for one request against the snapshot.  Fills every
 // capacity-eligible candidate (with its memberships) into A and returns the
 // decision.
-Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std::vector<Cand>& A) {
+// SplitMix64 (Steele, Lea, Flood; Vigna's reference): the (r + 1)-th output
+// of the stream seeded with `seed`.
+uint64_t rand_seed_state(uint64_t seed, int64_t r) {
+  uint64_t z = seed + (uint64_t)(r + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std::vector<Cand>& A,
+                   int64_t r_index) {
   Decision d{-1, 0, 0.0, 0.0, R_REJECT, 0, 0, 0, 0};
   const int64_t L = (int64_t)ch.len() * m.block_tokens;
   const double Ld = (double)L;
@@ -213,35 +228,97 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
     d.nT += c.inT;
   }
 
-  // Decode-batch-size-centric packing: most decoding requests, then most
-  // cached blocks, then fewest queued, then lowest instance id.
+  // Packing within T by the selector; D-C-Q by default (most decoding
+  // requests, then most cached blocks, then fewest queued, then lowest id).
+  const uint32_t sel = (m.flags >> 8) & 0xFu;
+  auto lmetric = [&](const Cand& c) {
+    const int64_t active = (int64_t)sn.D[c.i] + sn.Q[c.i];
+    return (unsigned __int128)(uint64_t)(sn.P[c.i] + c.n) * (unsigned __int128)(uint64_t)(active + 1);
+  };
+  // true if a comes before b in selector order s
+  auto before = [&](uint32_t s, const Cand& a, const Cand& b) {
+    const int32_t Da = sn.D[a.i], Db = sn.D[b.i], Qa = sn.Q[a.i], Qb = sn.Q[b.i];
+    switch (s) {
+      case SEL_D:
+        if (Da != Db) return Da > Db;
+        break;
+      case SEL_DQ:
+        if (Da != Db) return Da > Db;
+        if (Qa != Qb) return Qa < Qb;
+        break;
+      case SEL_DC:
+        if (Da != Db) return Da > Db;
+        if (a.hit != b.hit) return a.hit > b.hit;
+        break;
+      case SEL_DQC:
+        if (Da != Db) return Da > Db;
+        if (Qa != Qb) return Qa < Qb;
+        if (a.hit != b.hit) return a.hit > b.hit;
+        break;
+      case SEL_HCQ: {  // smallest TPOT headroom first
+        const double ha = m.tau - a.tpot, hb = m.tau - b.tpot;
+        if (ha != hb) return ha < hb;
+        if (a.hit != b.hit) return a.hit > b.hit;
+        if (Qa != Qb) return Qa < Qb;
+        break;
+      }
+      case SEL_LMETRIC: {
+        const unsigned __int128 la = lmetric(a), lb = lmetric(b);
+        if (la != lb) return la < lb;
+        break;
+      }
+      default:  // SEL_DCQ
+        if (Da != Db) return Da > Db;
+        if (a.hit != b.hit) return a.hit > b.hit;
+        if (Qa != Qb) return Qa < Qb;
+        break;
+    }
+    return a.i < b.i;
+  };
   const Cand* best = nullptr;
-  for (const Cand& c : A) {
-    if (!c.inT) continue;
-    if (!best) { best = &c; continue; }
-    const int32_t Dc = sn.D[c.i], Db = sn.D[best->i];
-    const int32_t Qc = sn.Q[c.i], Qb = sn.Q[best->i];
-    bool better;
-    if (Dc != Db) better = Dc > Db;
-    else if (c.hit != best->hit) better = c.hit > best->hit;
-    else if (Qc != Qb) better = Qc < Qb;
-    else better = c.i < best->i;
-    if (better) best = &c;
+  if (sel == SEL_RANDOM) {
+    // The k-th member of T in id order, k from the (r + 1)-th output of a
+    // SplitMix64 stream seeded with rand_seed: k = floor(z_hi * |T| / 2^32).
+    if (d.nT > 0) {
+      uint64_t z = rand_seed_state(m.rand_seed, r_index);
+      const uint64_t k = ((z >> 32) * (uint64_t)d.nT) >> 32;
+      uint64_t seen = 0;
+      for (const Cand& c : A) {
+        if (!c.inT) continue;
+        if (seen++ == k) {
+          best = &c;
+          break;
+        }
+      }
+    }
+  } else {
+    for (const Cand& c : A) {
+      if (c.inT && (!best || before(sel, c, *best))) best = &c;
+    }
+    if (sel == SEL_HCQ && best) {
+      const double hb = m.tau - best->tpot;
+      for (const Cand& c : A)
+        if (c.inT && &c != best && std::fabs((m.tau - c.tpot) - hb) <= NB_REL * m.tau) d.nb |= NB_HEADROOM;
+    }
   }
   d.flags = 0;
   if (!best) {
-    // Cache-aware load balancing over the KVC-admissible set: the product of
-    // pending uncached prefill tokens and active requests, both counting the
-    // arriving request; ties to the lowest id.
-    unsigned __int128 bestv = 0;
-    for (const Cand& c : A) {
-      if (!c.inC) continue;
-      const int64_t active = (int64_t)sn.D[c.i] + sn.Q[c.i];
-      unsigned __int128 v = (unsigned __int128)(uint64_t)(sn.P[c.i] + c.n) *
-                            (unsigned __int128)(uint64_t)(active + 1);
-      if (!best || v < bestv || (v == bestv && c.i < best->i)) {
-        best = &c;
-        bestv = v;
+    if (m.flags & F_FALLBACK_DCQ) {
+      // fallback by the D-C-Q key over the KVC-admissible set
+      for (const Cand& c : A)
+        if (c.inC && (!best || before(SEL_DCQ, c, *best))) best = &c;
+    } else {
+      // Cache-aware load balancing over the KVC-admissible set: the product
+      // of pending uncached prefill tokens and active requests, both
+      // counting the arriving request; ties to the lowest id.
+      unsigned __int128 bestv = 0;
+      for (const Cand& c : A) {
+        if (!c.inC) continue;
+        const unsigned __int128 v = lmetric(c);
+        if (!best || v < bestv || (v == bestv && c.i < best->i)) {
+          best = &c;
+          bestv = v;
+        }
       }
     }
     d.flags |= R_FALLBACK;
@@ -324,7 +401,7 @@ int orc_score(void* h, const orc_model* m, const uint64_t* pool, const int64_t* 
   for (int32_t r = 0; r < n_req; ++r) {
     Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, r);
     std::vector<Cand> A;
-    Decision d = score_one(sn, *m, ch, A);
+    Decision d = score_one(sn, *m, ch, A, r);
     inst[r] = d.inst;
     hit[r] = d.hit;
     ttft[r] = d.ttft;
@@ -349,7 +426,7 @@ int orc_explain(void* h, const orc_model* m, const uint64_t* chain, int32_t len,
   const Snapshot& sn = *static_cast<Snapshot*>(h);
   Chain ch{chain, len, chain, 0};
   std::vector<Cand> A;
-  Decision d = score_one(sn, *m, ch, A);
+  Decision d = score_one(sn, *m, ch, A, 0);
   for (int32_t i = 0; i < sn.n_inst; ++i) {
     elig[i] = 0; hit[i] = 0; W[i] = rho[i] = tpot[i] = ttft[i] = 0.0; inC[i] = inT[i] = 0;
   }

@@ -26,7 +26,15 @@ PS_MAX_SEG = 32
 PS_MAX_INST = 65536
 PS_MAX_DQ = 4095
 PS_MAX_CHAIN = (1 << 24) - 1
-PS_F_TTFT_ADMIT, PS_F_NO_KVC_FILTER, PS_F_NO_TPOT_FILTER = 1, 2, 4
+PS_F_TTFT_ADMIT, PS_F_NO_KVC_FILTER, PS_F_NO_TPOT_FILTER, PS_F_FALLBACK_DCQ = 1, 2, 4, 8
+(PS_SEL_DCQ, PS_SEL_D, PS_SEL_DQ, PS_SEL_DC, PS_SEL_DQC, PS_SEL_HCQ, PS_SEL_RANDOM,
+ PS_SEL_LMETRIC) = range(8)
+
+
+def PS_F_SELECTOR(sel: int) -> int:
+    return (int(sel) & 0xF) << 8
+
+
 PS_R_REJECT, PS_R_FALLBACK, PS_R_TTFT_MISS, PS_R_INVALID = 1, 2, 4, 8
 
 # struct ps_req (24 bytes) and struct ps_result (20 bytes)
@@ -49,6 +57,7 @@ class PsModel(ctypes.Structure):
         ("block_tokens", ctypes.c_int32), ("b_max", ctypes.c_int32),
         ("kv_cap_tokens", ctypes.c_int64),
         ("flags", ctypes.c_uint32),
+        ("rand_seed", ctypes.c_uint64),
     ]
 
 
@@ -126,7 +135,7 @@ def _stream_handle(stream) -> Optional[int]:
 
 # ------------------------------------------------------------------ structs
 def make_model(alpha, seg_ub, beta, gamma, eta, tpot_slo, ttft_floor, lout, block_tokens,
-               b_max, kv_cap_tokens, flags=0) -> PsModel:
+               b_max, kv_cap_tokens, flags=0, rand_seed=0) -> PsModel:
     m = PsModel()
     for k in range(6):
         m.alpha[k] = float(alpha[k])
@@ -139,6 +148,7 @@ def make_model(alpha, seg_ub, beta, gamma, eta, tpot_slo, ttft_floor, lout, bloc
     m.eta, m.tpot_slo, m.ttft_floor, m.lout = float(eta), float(tpot_slo), float(ttft_floor), float(lout)
     m.block_tokens, m.b_max = int(block_tokens), int(b_max)
     m.kv_cap_tokens, m.flags = int(kv_cap_tokens), int(flags)
+    m.rand_seed = int(rand_seed) & 0xFFFFFFFFFFFFFFFF
     return m
 
 

@@ -141,8 +141,11 @@ ps_status check_model(ps_ctx* c, const ps_model* m) {
   if (m->b_max < 1 || m->b_max > PS_MAX_BATCH)
     return fail(c, PS_E_RANGE, "b_max %d outside [1, %d]", m->b_max, PS_MAX_BATCH);
   if (m->kv_cap_tokens < 0) return fail(c, PS_E_RANGE, "kv_cap_tokens is negative");
-  if (m->flags & ~(PS_F_TTFT_ADMIT | PS_F_NO_KVC_FILTER | PS_F_NO_TPOT_FILTER))
+  if (m->flags & ~(PS_F_TTFT_ADMIT | PS_F_NO_KVC_FILTER | PS_F_NO_TPOT_FILTER | PS_F_FALLBACK_DCQ |
+                   PS_F_SELECTOR(0xF)))
     return fail(c, PS_E_INVAL, "unknown flag bits 0x%x", m->flags);
+  if (((m->flags >> 8) & 0xF) > PS_SEL_LMETRIC)
+    return fail(c, PS_E_INVAL, "unknown selector %u", (m->flags >> 8) & 0xF);
   return PS_OK;
 }
 
@@ -160,7 +163,9 @@ DevModel device_model(const ps_model& m) {
   d.bs = m.block_tokens;
   d.b_max = m.b_max;
   d.kv_cap = m.kv_cap_tokens;
-  d.flags = m.flags;
+  d.flags = m.flags & 0xFFu;
+  d.sel = (m.flags >> 8) & 0xFu;
+  d.rand_seed = m.rand_seed;
   d.n_seg = m.n_seg;
   for (int s = 0; s < PS_MAX_SEG; ++s) {
     d.seg_ub[s] = s < m.n_seg ? m.seg_ub[s] : 0;

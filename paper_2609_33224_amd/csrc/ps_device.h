@@ -40,7 +40,9 @@ struct DevModel {
   float eta, tau, ttft_floor, lout1;  // lout1 = max(1, lout)
   int32_t bs, b_max;
   int64_t kv_cap;
-  uint32_t flags;
+  uint32_t flags;     // PS_F_* admission bits
+  uint32_t sel;       // PS_SEL_*
+  uint64_t rand_seed;
   int32_t n_seg;
   int32_t seg_ub[PS_MAX_SEG];
   float seg[PS_MAX_SEG][4];  // beta0, beta1, beta2, gamma

@@ -524,38 +524,104 @@ __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
   }
 }
 
-// Per-lane accumulation of one candidate (instance i, hit v) of A: the
-// recomputation filter, then (for members of C) Eq. 10, Eq. 4, the TPOT /
-// TTFT tests and the two packed keys.
+// Per-lane accumulation over candidates of A: the selector's key over T
+// (for H-C-Q a sortable headroom plus the rest of the key), the fallback
+// key over C, and |C|, |T|.
 struct Acc {
   uint64_t keyT, keyF;
+  uint32_t hroom;
   uint32_t nC, nT;
 };
+
+// Order-preserving map of a float to u32 (negative values below positive).
+__device__ __forceinline__ uint32_t sortable_bits(float x) {
+  const uint32_t b = __float_as_uint(x);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t dcq_key(const InstState& st, uint32_t v, uint32_t i) {
+  return ((uint64_t)(PS_MAX_DQ - st.D) << 52) | ((uint64_t)(PS_MAX_CHAIN - v) << 28) |
+         ((uint64_t)st.Q << 16) | (uint64_t)i;
+}
+
+// Packed key of a member of T under selector `sel` (smaller = preferred;
+// the id in the low 16 bits ends every order).  H-C-Q: the part after the
+// headroom.
+__device__ __forceinline__ uint64_t select_key(uint32_t sel, const InstState& st, uint32_t v,
+                                               uint32_t i, uint64_t lm) {
+  const uint64_t d = (uint64_t)(PS_MAX_DQ - st.D) << 52;
+  const uint64_t c = (uint64_t)(PS_MAX_CHAIN - v);
+  switch (sel) {
+    case PS_SEL_D: return d | i;
+    case PS_SEL_DQ: return d | ((uint64_t)st.Q << 16) | i;
+    case PS_SEL_DC: return d | (c << 28) | i;
+    case PS_SEL_DQC: return d | ((uint64_t)st.Q << 40) | (c << 16) | i;
+    case PS_SEL_HCQ: return (c << 28) | ((uint64_t)st.Q << 16) | i;
+    case PS_SEL_LMETRIC: return (lm << 16) | i;
+    default: return dcq_key(st, v, i);
+  }
+}
+
+// Membership of candidate (instance i, hit v) of A in C and T, with the
+// state and latencies it needs.
+struct Member {
+  bool inC, inT;
+  InstState st;
+  Lat lt;
+  int64_t n_tok;
+};
+
+__device__ __forceinline__ Member member(const ScoreArgs& a, const DevModel& m, uint32_t i,
+                                         uint32_t v, int64_t L, float Lf, float wmin, float Z,
+                                         bool kvc, float slo) {
+  Member r{};
+  const int64_t c_tok = (int64_t)v * m.bs;
+  r.n_tok = L - c_tok;
+  const float n = (float)r.n_tok;
+  if (kvc) {
+    const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
+    if (!((W - wmin) / Z <= m.eta)) return r;
+  }
+  r.inC = true;
+  r.st = a.inst[i];
+  r.lt = latency(m, r.st, n, (float)c_tok, L);
+  const bool tpot_ok = (m.flags & PS_F_NO_TPOT_FILTER) || r.lt.tpot < m.tau;
+  const bool ttft_ok = !(m.flags & PS_F_TTFT_ADMIT) || r.lt.ttft <= slo;
+  r.inT = tpot_ok && ttft_ok;
+  return r;
+}
 
 __device__ __forceinline__ void evaluate(const ScoreArgs& a, const DevModel& m, Acc& acc,
                                          uint32_t i, uint32_t v, int64_t L, float Lf, float wmin,
                                          float Z, bool kvc, float slo) {
-  const int64_t c_tok = (int64_t)v * m.bs;
-  const int64_t n_tok = L - c_tok;
-  const float n = (float)n_tok;
-  if (kvc) {
-    const float W = fmaxf(0.0f, recompute_raw(m, n, Lf));
-    if (!((W - wmin) / Z <= m.eta)) return;
-  }
+  const Member mb = member(a, m, i, v, L, Lf, wmin, Z, kvc, slo);
+  if (!mb.inC) return;
   ++acc.nC;
-  const InstState st = a.inst[i];
-  const Lat lt = latency(m, st, n, (float)c_tok, L);
-  const uint64_t lm = (uint64_t)(st.P + n_tok) * (uint64_t)st.A1;
-  const uint64_t kf = (lm << 16) | (uint64_t)i;
+  const uint64_t lm = (uint64_t)(mb.st.P + mb.n_tok) * (uint64_t)mb.st.A1;
+  const uint64_t kf = (m.flags & PS_F_FALLBACK_DCQ) ? dcq_key(mb.st, v, i) : ((lm << 16) | i);
   acc.keyF = kf < acc.keyF ? kf : acc.keyF;
-  const bool tpot_ok = (m.flags & PS_F_NO_TPOT_FILTER) || lt.tpot < m.tau;
-  const bool ttft_ok = !(m.flags & PS_F_TTFT_ADMIT) || lt.ttft <= slo;
-  if (tpot_ok && ttft_ok) {
-    ++acc.nT;
-    const uint64_t kt = ((uint64_t)(PS_MAX_DQ - st.D) << 52) |
-                        ((uint64_t)(PS_MAX_CHAIN - v) << 28) | ((uint64_t)st.Q << 16) | (uint64_t)i;
+  if (!mb.inT) return;
+  ++acc.nT;
+  if (m.sel == PS_SEL_RANDOM) return;
+  const uint64_t kt = select_key(m.sel, mb.st, v, i, lm);
+  if (m.sel == PS_SEL_HCQ) {
+    const uint32_t h = sortable_bits(m.tau - mb.lt.tpot);
+    if (h < acc.hroom || (h == acc.hroom && kt < acc.keyT)) {
+      acc.hroom = h;
+      acc.keyT = kt;
+    }
+  } else {
     acc.keyT = kt < acc.keyT ? kt : acc.keyT;
   }
+}
+
+// The (r + 1)-th output of a SplitMix64 stream seeded with `seed`
+// (Steele, Lea, Flood; Vigna's public-domain reference).
+__device__ __forceinline__ uint64_t splitmix64_at(uint64_t seed, int64_t r) {
+  uint64_t z = seed + (uint64_t)(r + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
 }
 
 // LDS of one scoring wave: chain stage | live bitmap | next bitmap |
@@ -655,6 +721,7 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
         const uint32_t hk = ell > 1 ? run_walk<true>(a.t, id, c, stage, 0, g, s) : 1u;
         if ((uint32_t)lane == k) myhit = hk;
       }
+      if ((uint32_t)lane < nCand) hits[myid] = encode_hit(myhit);
     } else {
       for (int32_t w = lane; w < nw; w += 64) bmA[w] = bmC[w];
       __syncthreads();
@@ -794,7 +861,7 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
     const float slo = fmaxf(m.ttft_floor, tpf_cold);
     const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
     const bool admit0 = n0 > 0 && (!kvc || (W0 - wmin) / Z <= m.eta);
-    Acc acc{~0ull, ~0ull, 0u, 0u};
+    Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
     if (nA > 0) {
       if (few) {
         if ((uint32_t)lane < nCand) evaluate(a, m, acc, myid, myhit, L, Lf, wmin, Z, kvc, slo);
@@ -820,7 +887,8 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
         // asc).  The whole class is evaluated when sizes are requested or
         // when no member is in T (then the fallback key may come from it).
         bool done0 = false;
-        if (!a.sizes) {
+        const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
+        if (!a.sizes && keyed) {
           for (int32_t base = 0; base < n_inst && !done0; base += 64) {
             const int32_t k = base + lane;
             bool ok = false;
@@ -838,9 +906,7 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
             if (okm) {
               if (lane == __builtin_ctzll(okm)) {
                 const InstState st = a.inst[i];
-                const uint64_t kt = ((uint64_t)(PS_MAX_DQ - st.D) << 52) |
-                                    ((uint64_t)PS_MAX_CHAIN << 28) | ((uint64_t)st.Q << 16) |
-                                    (uint64_t)i;
+                const uint64_t kt = select_key(m.sel, st, 0u, i, 0ull);
                 acc.keyT = kt < acc.keyT ? kt : acc.keyT;
               }
               done0 = true;
@@ -856,10 +922,45 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
         }
       }
     }
-    const uint64_t keyT = wave_min_u64(acc.keyT);
+    uint64_t keyT;
+    if (m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
+      const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
+      keyT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
+    } else {
+      keyT = wave_min_u64(acc.keyT);
+    }
     const uint64_t keyF = wave_min_u64(acc.keyF);
     const uint32_t nC = wave_sum_u32(acc.nC);
     const uint32_t nT = wave_sum_u32(acc.nT);
+    if (m.sel == PS_SEL_RANDOM && nT > 0) {
+      // the k-th member of T in id order
+      const uint64_t z = splitmix64_at(m.rand_seed, r);
+      const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
+      uint32_t seen = 0;
+      for (int32_t base = 0; base < n_inst; base += 64) {
+        const int32_t i = base + lane;
+        const bool el = i < n_inst && a.room[i] >= L;
+        const bool cand = el && test_bit(bmC, (uint32_t)i);
+        uint32_t v = cand ? hits[i] : 0u;
+        uint64_t ovf = __ballot(cand && v == kHitOverflow);
+        while (ovf) {
+          const int k = __builtin_ctzll(ovf);
+          ovf &= ovf - 1;
+          const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+          if (lane == k) v = hk;
+        }
+        bool inT = false;
+        if (el && (cand || admit0)) inT = member(a, m, (uint32_t)i, v, L, Lf, wmin, Z, kvc, slo).inT;
+        uint64_t mm = __ballot(inT);
+        const uint32_t cnt = (uint32_t)__popcll(mm);
+        if (seen + cnt > kth) {
+          for (uint32_t j = seen; j < kth; ++j) mm &= mm - 1;
+          keyT = (uint64_t)(base + __builtin_ctzll(mm));
+          break;
+        }
+        seen += cnt;
+      }
+    }
 
     // Decision.  With finite arithmetic C holds at least the minimum-penalty
     // candidate whenever A is non-empty; the key test only keeps a

@@ -118,7 +118,7 @@ _DEFAULTS = dict(
 
 # Policy constants per workload (not drawn).
 _POLICY_DEFAULTS = dict(eta=0.5, tpot_slo=0.050, ttft_floor=2.0, lout=556.0,
-                        block_tokens=16, b_max=64, kv_cap_tokens=1_048_576, flags=0)
+                        block_tokens=16, b_max=64, kv_cap_tokens=1_048_576, flags=0, rand_seed=0)
 
 WORKLOADS: Dict[str, dict] = {
     "c1": dict(gen={}, policy={}),

@@ -13,7 +13,7 @@ def gpu_model(win, **policy):
     pol.update(policy)
     return ps.make_model(win.alpha, win.seg_ub, win.beta, win.gamma, pol["eta"], pol["tpot_slo"],
                          pol["ttft_floor"], pol["lout"], pol["block_tokens"], pol["b_max"],
-                         pol["kv_cap_tokens"], pol.get("flags", 0))
+                         pol["kv_cap_tokens"], pol.get("flags", 0), pol.get("rand_seed", 0))
 
 
 def load_window(scorer, win, **policy):

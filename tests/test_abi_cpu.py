@@ -36,8 +36,8 @@ def test_struct_layouts_match_header():
     assert ps.PS_REQ_DTYPE.itemsize == 24
     assert ps.PS_RESULT_DTYPE.itemsize == 20
     # float alpha[6]; int n_seg; int seg_ub[32]; float beta[32][3]; float gamma[32];
-    # 4 floats; 2 ints; int64 (8-aligned); uint32 -> 712 bytes with tail padding
-    assert ctypes.sizeof(ps.PsModel) == 712
+    # 4 floats; 2 ints; int64 (8-aligned); uint32; uint64 -> 720 bytes
+    assert ctypes.sizeof(ps.PsModel) == 720
     assert ctypes.sizeof(ps.binding.PsInstances) == 56
 
 

@@ -343,3 +343,28 @@ def test_full_size_sampled(ps, scorer, name):
     ell = w.pre_len + w.tail_len
     assert (res["hit_blocks"] <= ell).all()
     assert (sizes[:, 2] <= sizes[:, 1]).all() and (sizes[:, 1] <= sizes[:, 0]).all()
+
+
+# ------------------------------------------------------------- policy variants
+SELECTORS = ["DCQ", "D", "DQ", "DC", "DQC", "HCQ", "RANDOM", "LMETRIC"]
+LAYERS = {"G": 2 | 4, "C": 4, "T": 2 | 8, "CT": 8, "F": 0}
+
+
+@pytest.mark.parametrize("name,gen", [("c1", {}), ("c2", dict(n_req=2048)),
+                                      ("c3", dict(n_inst=128, n_sess=256, n_req=1024))])
+def test_selectors_and_layers(ps, scorer, name, gen):
+    """Every selector of Table 4 (plus LMetric) and every admission layer of
+    Table 3, on windows with one and with many holders of the first block."""
+    w = synth.generate(name, **gen)
+    o = oracle.Oracle.from_window(w)
+    dw = DeviceWindow(w)
+    for k, sel in enumerate(SELECTORS):
+        for layer, fl in LAYERS.items():
+            flags = fl | (k << 8)
+            pol = dict(flags=flags, rand_seed=1234567 + k)
+            load_window(scorer, w, **pol)
+            res, sizes = dw.score(scorer)
+            od = o.window_score(w, **pol)
+            compare_decisions(res, sizes, od, label=f"{name} {sel} {layer}")
+            res2, _ = dw.score(scorer, with_sizes=False)
+            assert res2.tobytes() == res.tobytes(), f"{name} {sel} {layer}: no-sizes path differs"

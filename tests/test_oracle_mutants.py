@@ -36,11 +36,11 @@ MUTANTS = [
     ("S+ without request", "const double Sp = (double)(sn.S[i] + L);", "const double Sp = (double)(sn.S[i]);"),
     ("TTFT queue uses Q for P", "m.alpha[1] * (double)sn.P[i]", "m.alpha[1] * (double)sn.Q[i]"),
     ("SLO from cached prefill", "std::max(m.ttft_floor, tpf_cold)", "std::max(m.ttft_floor, tpf_cached)"),
-    ("D order", "if (Dc != Db) better = Dc > Db;", "if (Dc != Db) better = Dc < Db;"),
-    ("hit order", "better = c.hit > best->hit;", "better = c.hit < best->hit;"),
-    ("Q order", "better = Qc < Qb;", "better = Qc > Qb;"),
-    ("id order", "else better = c.i < best->i;", "else better = c.i > best->i;"),
-    ("LMetric without arrival", "(unsigned __int128)(uint64_t)(active + 1);", "(unsigned __int128)(uint64_t)(active);"),
+    ("D order", "default:  // SEL_DCQ\n        if (Da != Db) return Da > Db;", "default:  // SEL_DCQ\n        if (Da != Db) return Da < Db;"),
+    ("hit order", "default:  // SEL_DCQ\n        if (Da != Db) return Da > Db;\n        if (a.hit != b.hit) return a.hit > b.hit;", "default:  // SEL_DCQ\n        if (Da != Db) return Da > Db;\n        if (a.hit != b.hit) return a.hit < b.hit;"),
+    ("Q order", "if (a.hit != b.hit) return a.hit > b.hit;\n        if (Qa != Qb) return Qa < Qb;\n        break;\n    }", "if (a.hit != b.hit) return a.hit > b.hit;\n        if (Qa != Qb) return Qa > Qb;\n        break;\n    }"),
+    ("id order", "return a.i < b.i;\n  };", "return a.i > b.i;\n  };"),
+    ("LMetric without arrival", "* (unsigned __int128)(uint64_t)(active + 1);", "* (unsigned __int128)(uint64_t)(active);"),
     ("LMetric ignores n", "(uint64_t)(sn.P[c.i] + c.n)", "(uint64_t)(sn.P[c.i])"),
     ("capacity batch bound", "if (active + 1 <= m.b_max && sn.S[i] + L <= m.kv_cap)", "if (active + 1 < m.b_max && sn.S[i] + L <= m.kv_cap)"),
     ("capacity ignores tokens", "if (active + 1 <= m.b_max && sn.S[i] + L <= m.kv_cap)", "if (active + 1 <= m.b_max && sn.S[i] <= m.kv_cap)"),
@@ -49,6 +49,11 @@ MUTANTS = [
     ("cached tokens per block", "c.c = c.hit * m.block_tokens;", "c.c = c.hit;"),
     ("ttft miss non-strict", "if (best->ttft > slo) d.flags |= R_TTFT_MISS;", "if (best->ttft >= slo) d.flags |= R_TTFT_MISS;"),
     ("commit P counts cached", "sn.P[i] += L - hitb * block_tokens;", "sn.P[i] += L;"),
+    ("D-Q queued order", "if (Qa != Qb) return Qa < Qb;\n        break;\n      case SEL_DC:", "if (Qa != Qb) return Qa > Qb;\n        break;\n      case SEL_DC:"),
+    ("H-C-Q headroom direction", "if (ha != hb) return ha < hb;", "if (ha != hb) return ha > hb;"),
+    ("random k from low bits", "const uint64_t k = ((z >> 32) * (uint64_t)d.nT) >> 32;", "const uint64_t k = z % (uint64_t)d.nT;"),
+    ("D-C-Q fallback over A", "if (c.inC && (!best || before(SEL_DCQ, c, *best))) best = &c;", "if ((!best || before(SEL_DCQ, c, *best))) best = &c;"),
+    ("LMetric selector order", "if (la != lb) return la < lb;", "if (la != lb) return la > lb;"),
     ("commit ignores cap", "if ((int64_t)set.size() < sn.cap) set.insert(key);", "if (true) set.insert(key);"),
 ]
 

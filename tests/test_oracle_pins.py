@@ -490,3 +490,112 @@ def test_commit_hand_trace():
     assert list(st["set_size"]) == [5, 0] and dropped == 1 + 3
     h = o.window_hits(w)
     assert list(h[:, 0]) == [5, 5, 0]
+
+
+# -- policy variants: selector orders (Table 4) and admission layers (Table 3)
+
+def _sel_window(**pol):
+    """Four instances all in T (no prefill cost, so no KVC effect; tau large).
+    hits 2, 1, 3, 8; D 5, 5, 5, 4; Q 2, 1, 1, 0; S 1000, 5000, 3000, 2000."""
+    ch = chain_hashes(8)
+    hits = [2, 1, 3, 8]
+    pol.setdefault("tpot_slo", 10.0)
+    pol.setdefault("b_max", 10_000)
+    pol.setdefault("kv_cap_tokens", 10**9)
+    return make_window([ch[:h] for h in hits], [ch], [5, 5, 5, 4], [2, 1, 1, 0], [0, 0, 0, 0],
+                       [1000, 5000, 3000, 2000], [0.0] * 6, (10_000,), ((0.01, 0.0, 1e-6),),
+                       (1.0,), cap=8, lout=1e9, **pol)
+
+
+def test_selector_orders():
+    """D: most decoding then lowest id -> 0.  D-Q: then fewest queued -> 1.
+    D-C and D-Q-C and D-C-Q: then most cached -> 2 (D-Q-C: Q ties 1, 2 ->
+    hit 3 wins).  LMetric (P + n)(A + 1): 96*8, 112*7, 80*7, 0*5 -> 3.
+    H-C-Q: smallest headroom tau - TPOT = largest TPOT = largest S -> 1."""
+    want = {oracle.SEL_D: 0, oracle.SEL_DQ: 1, oracle.SEL_DC: 2, oracle.SEL_DQC: 2,
+            oracle.SEL_DCQ: 2, oracle.SEL_LMETRIC: 3, oracle.SEL_HCQ: 1}
+    for sel, inst in want.items():
+        d = _decide(_sel_window(flags=oracle.selector_flags(sel)))
+        assert d.inst[0] == inst, sel
+        assert d.sizes[0][2] == 4 and not d.flags[0] & oracle.R_FALLBACK
+
+
+def test_selector_dq_vs_dqc_order_of_ties():
+    """D-Q-C compares queued before cached, D-C-Q cached before queued:
+    instances (D, Q, hit) = (5, 2, 7) and (5, 1, 3) split them."""
+    ch = chain_hashes(8)
+    w = make_window([ch[:7], ch[:3]], [ch], [5, 5], [2, 1], [0, 0], [0, 0], [0.0] * 6,
+                    (10_000,), ((0.01, 0.0, 0.0),), (1.0,), cap=8, tpot_slo=10.0, b_max=100,
+                    kv_cap_tokens=10**9)
+    assert _decide(w, flags=oracle.selector_flags(oracle.SEL_DCQ)).inst[0] == 0
+    assert _decide(w, flags=oracle.selector_flags(oracle.SEL_DQC)).inst[0] == 1
+
+
+def test_random_selector_uses_splitmix64_stream():
+    """k = floor(z_hi * |T| / 2^32), z = the (r + 1)-th SplitMix64 output of
+    the stream seeded with rand_seed (published definition; the generator's
+    splitmix64 is checked against the reference vector in test_synth)."""
+    gamma = 0x9E3779B97F4A7C15
+    for seed in (0, 1, 12345, 2**63 + 7):
+        w = _sel_window(flags=oracle.selector_flags(oracle.SEL_RANDOM), rand_seed=seed)
+        z = synth.splitmix64(seed)                       # r = 0: state seed + gamma
+        k = ((z >> 32) * 4) >> 32
+        d = _decide(w)
+        assert d.inst[0] == [0, 1, 2, 3][k], seed
+    # request index r uses the (r + 1)-th output
+    ch = chain_hashes(8)
+    w = _sel_window(flags=oracle.selector_flags(oracle.SEL_RANDOM), rand_seed=99)
+    w2 = make_window([ch[:h] for h in [2, 1, 3, 8]], [ch, ch, ch], [5, 5, 5, 4], [2, 1, 1, 0],
+                     [0] * 4, [1000, 5000, 3000, 2000], [0.0] * 6, (10_000,),
+                     ((0.01, 0.0, 1e-6),), (1.0,), cap=8, lout=1e9, tpot_slo=10.0, b_max=10_000,
+                     kv_cap_tokens=10**9, flags=oracle.selector_flags(oracle.SEL_RANDOM),
+                     rand_seed=99)
+    d = _decide(w2)
+    for r in range(3):
+        z = synth.splitmix64((99 + r * gamma) & 0xFFFFFFFFFFFFFFFF)
+        assert d.inst[r] == ((z >> 32) * 4) >> 32
+
+
+def _layer_window(tau, **pol):
+    """T_pf = N, so W = n and rho = n / 128 (L = 128): hits 8, 0, 6 give
+    rho 0, 1, 0.25; eta = 0.5 -> C = {0, 2}.  Decode 0.01 + 1e-6 (S + 128)
+    with S = 20000, 1000, 2000 -> TPOT 0.0301, 0.0111, 0.0121 (interference
+    is negligible: L_out = 1e9).  D = 1, 9, 3; P = 0."""
+    ch = chain_hashes(8)
+    return make_window([ch, [], ch[:6]], [ch], [1, 9, 3], [0, 0, 0], [0, 0, 0],
+                       [20000, 1000, 2000], [0, 1.0, 0, 0, 0, 0], (10_000,),
+                       ((0.01, 0.0, 1e-6),), (1.0,), cap=8, lout=1e9, eta=0.5, tpot_slo=tau,
+                       b_max=10_000, kv_cap_tokens=10**9, **pol)
+
+
+def test_admission_layers_table3():
+    """G = capacity only, C = cache only, T = TPOT only (DCQ fallback over A),
+    CT = cache + TPOT (DCQ fallback over C), F = full (LMetric fallback)."""
+    G = oracle.F_NO_KVC_FILTER | oracle.F_NO_TPOT_FILTER
+    C = oracle.F_NO_TPOT_FILTER
+    T = oracle.F_NO_KVC_FILTER | oracle.F_FALLBACK_DCQ
+    CT = oracle.F_FALLBACK_DCQ
+    F = 0
+    # tau = 0.02: T passes instances 1 and 2
+    want = {G: (1, False), C: (2, False), T: (1, False), CT: (2, False), F: (2, False)}
+    for fl, (inst, fb) in want.items():
+        d = _decide(_layer_window(0.02, flags=fl))
+        assert d.inst[0] == inst and bool(d.flags[0] & oracle.R_FALLBACK) == fb, fl
+    # tau = 0.001: nobody passes TPOT; fallbacks: F -> LMetric over C
+    # (n (A + 1) = 0 * 2 for instance 0), CT -> D-C-Q over C (instance 2),
+    # T -> D-C-Q over A (instance 1)
+    want = {T: 1, CT: 2, F: 0}
+    for fl, inst in want.items():
+        d = _decide(_layer_window(0.001, flags=fl))
+        assert d.inst[0] == inst and d.flags[0] & oracle.R_FALLBACK, fl
+
+
+def test_headroom_near_tie_is_flagged():
+    """H-C-Q: two members of T whose headrooms agree to 1e-5 tau are a
+    near-boundary decision (their order is decided by rounding)."""
+    ch = chain_hashes(8)
+    w = make_window([ch[:2], ch[:3]], [ch], [5, 5], [0, 0], [0, 0], [1000, 1000], [0.0] * 6,
+                    (10_000,), ((0.01, 0.0, 1e-6),), (1.0,), cap=8, tpot_slo=10.0, b_max=100,
+                    kv_cap_tokens=10**9, lout=1e9, flags=oracle.selector_flags(oracle.SEL_HCQ))
+    d = _decide(w)
+    assert d.inst[0] == 1 and d.nb[0] & oracle.NB_HEADROOM

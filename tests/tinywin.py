@@ -9,7 +9,7 @@ import numpy as np
 from synth import Window
 
 DEFAULT_POLICY = dict(eta=0.5, tpot_slo=0.030, ttft_floor=2.0, lout=556.0, block_tokens=16,
-                      b_max=64, kv_cap_tokens=1_000_000, flags=0)
+                      b_max=64, kv_cap_tokens=1_000_000, flags=0, rand_seed=0)
 
 
 def make_window(sets, chains, D, Q, P, S, alpha, seg_ub, beta, gamma, cap=None, **policy):
