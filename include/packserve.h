@@ -237,6 +237,60 @@ ps_status ps_read_state(ps_ctx* ctx, int32_t* decoding, int32_t* queued, int64_t
 ps_status ps_table_info(ps_ctx* ctx, int64_t* slots_per_table, int64_t* table_bytes,
                         int32_t* hits_in_lds);
 
+/*
+ * Response-path feedback (Sec. 5.3 and Sec. 7 of the paper; applied in array
+ * order, between windows, never concurrently with scoring).
+ */
+
+/* Instance state transitions along the response path. */
+#define PS_EV_PREFILL_DONE 1  /* a queued request produced its first token: Q -= 1, D += 1,
+                                 P -= tokens (the request's uncached prefill tokens) */
+#define PS_EV_DECODE_TOKENS 2 /* the instance's decoding requests generated `tokens` tokens:
+                                 S += tokens */
+#define PS_EV_FINISHED 3      /* a decoding request completed: D -= 1, S -= tokens (its final
+                                 context length) */
+typedef struct {
+  int32_t instance;
+  int32_t kind;   /* PS_EV_* */
+  int64_t tokens;
+} ps_event;
+
+/*
+ * Apply events to the load counters in array order, then refresh the derived
+ * per-instance data (capacity room, decode segment, key order).  PS_E_RANGE if
+ * any counter would leave its limits (D, Q in [0, PS_MAX_DQ], P in
+ * [0, PS_MAX_PENDING], S in [0, PS_MAX_CONTEXT]); PS_E_INVAL on an unknown
+ * kind or instance.  On error no event is applied.  Synchronous.
+ */
+ps_status ps_apply_events(ps_ctx* ctx, const ps_event* events, int32_t n);
+
+/*
+ * Online calibration of the decode model (Sec. 5.3).  Sample k is a measured
+ * pure-decode forward: batch size batch[k] >= 1, total context ctx_tok[k]
+ * tokens, duration measured_s[k] > 0 seconds.  For its segment s (the
+ * segment of batch[k]) the base prediction is b0 + b1 B + b2 S (no factor);
+ * ratio = clip(measured / prediction, 0.5, 2); gamma_s = clip(0.98 gamma_s +
+ * 0.02 ratio, 1, 2).  Samples whose base prediction is not positive are
+ * skipped.  The factors are kept in double precision between calls and used
+ * by the scorer in fp32.  PS_E_INVAL on a non-finite or non-positive
+ * duration or a batch below 1.
+ */
+ps_status ps_feedback_decode(ps_ctx* ctx, const int32_t* batch, const int64_t* ctx_tok,
+                             const float* measured_s, int32_t n);
+
+/*
+ * Recent median output length (the L_out of Eq. 10): record completed
+ * requests' output lengths (tokens, >= 0) in order; L_out becomes the lower
+ * median (element floor((m - 1) / 2) of the sorted values) of the last
+ * m = min(recorded, PS_LOUT_WINDOW) lengths.  Before any sample the model's
+ * lout stays.
+ */
+#define PS_LOUT_WINDOW 1024
+ps_status ps_feedback_output(ps_ctx* ctx, const int32_t* out_len, int32_t n);
+
+/* Current EMA factors (n_seg entries) and L_out; either pointer may be NULL. */
+ps_status ps_read_model(ps_ctx* ctx, float* gamma, float* lout, int32_t* n_seg);
+
 /* Message of the last failed call on ctx (or of ps_create when ctx is NULL). */
 const char* ps_last_error(const ps_ctx* ctx);
 

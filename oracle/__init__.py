@@ -122,6 +122,12 @@ def _load():
     lib.orc_state.restype = ctypes.c_int
     lib.orc_explain.argtypes = [vp, ctypes.POINTER(Model), vp, i32] + [vp] * 8
     lib.orc_explain.restype = ctypes.c_int
+    lib.orc_feedback_decode.argtypes = [ctypes.POINTER(Model), vp, vp, vp, i32]
+    lib.orc_feedback_decode.restype = ctypes.c_int
+    lib.orc_feedback_output.argtypes = [vp, ctypes.POINTER(Model), vp, i32, i32]
+    lib.orc_feedback_output.restype = ctypes.c_int
+    lib.orc_apply_events.argtypes = [vp, vp, vp, vp, i32]
+    lib.orc_apply_events.restype = ctypes.c_int
     lib.orc_max_threads.argtypes = []
     lib.orc_max_threads.restype = ctypes.c_int
     _lib = lib
@@ -215,6 +221,17 @@ class Oracle:
                           sz.ctypes.data)
         return dict(D=D, Q=Q, P=P, S=S, set_size=sz)
 
+    def apply_events(self, inst, kind, tokens) -> int:
+        """Response-path transitions; returns 0, -1 (bad event) or -5 (range)."""
+        i_, ip = _c(inst, np.int32)
+        k_, kp = _c(kind, np.int32)
+        t_, tp = _c(tokens, np.int64)
+        return int(_load().orc_apply_events(self._h, ip, kp, tp, len(i_)))
+
+    def feedback_output(self, model: Model, out_len, window=1024) -> None:
+        o_, op = _c(out_len, np.int32)
+        _load().orc_feedback_output(self._h, ctypes.byref(model), op, len(o_), int(window))
+
     def explain(self, model: Model, chain) -> dict:
         """Per-instance detail of one request: elig, hit, W, rho, tpot, ttft,
         inC, inT (zero where not capacity-eligible) and the choice."""
@@ -235,6 +252,14 @@ class Oracle:
     def window_score(self, win, nthreads=0, **policy) -> Decisions:
         return self.score(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,
                           win.tail_off, win.tail_len, nthreads)
+
+
+def feedback_decode(model: Model, batch, ctx_tok, measured) -> None:
+    """EMA calibration of the model's decode factors (in place)."""
+    b_, bp = _c(batch, np.int32)
+    c_, cp = _c(ctx_tok, np.int64)
+    m_, mp = _c(measured, np.float64)
+    _load().orc_feedback_decode(ctypes.byref(model), bp, cp, mp, len(b_))
 
 
 def max_threads() -> int:

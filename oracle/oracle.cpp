@@ -84,6 +84,7 @@ constexpr double NB_REL = 1e-5;
 struct Snapshot {
   int32_t n_inst = 0;
   int32_t cap = 0;
+  std::vector<int32_t> out_lens;  // every recorded output length, in order
   std::vector<std::unordered_set<uint64_t>> sets;
   std::vector<int32_t> D, Q;
   std::vector<int64_t> P, S;
@@ -485,6 +486,74 @@ int orc_state(void* h, int32_t* D, int32_t* Q, int64_t* P, int64_t* S, int64_t* 
     S[i] = sn.S[i];
     set_size[i] = (int64_t)sn.sets[(size_t)i].size();
   }
+  return 0;
+}
+
+// Online calibration (Sec. 5.3): for each measured pure-decode forward, the
+// factor of the segment of its batch size moves towards the
+// measured-to-predicted ratio of the base model (no factor) with weight
+// 0.02; the ratio is clipped to [0.5, 2] and the factor to [1, 2].  Samples
+// with a non-positive base prediction carry no ratio and are skipped.
+int orc_feedback_decode(orc_model* m, const int32_t* batch, const int64_t* ctx_tok,
+                        const double* measured, int32_t n) {
+  const double w = 0.02;
+  for (int32_t k = 0; k < n; ++k) {
+    const int s = segment_of(*m, batch[k]);
+    const double pred = m->beta[s][0] + m->beta[s][1] * (double)batch[k] +
+                        m->beta[s][2] * (double)ctx_tok[k];
+    if (!(pred > 0.0)) continue;
+    double ratio = measured[k] / pred;
+    ratio = std::min(2.0, std::max(0.5, ratio));
+    double f = (1.0 - w) * m->gamma[s] + w * ratio;
+    m->gamma[s] = std::min(2.0, std::max(1.0, f));
+  }
+  return 0;
+}
+
+// Recent median output length: the lower median of the last (at most
+// `window`) recorded lengths becomes the model's L_out.
+int orc_feedback_output(void* h, orc_model* m, const int32_t* out_len, int32_t n, int32_t window) {
+  Snapshot& sn = *static_cast<Snapshot*>(h);
+  for (int32_t k = 0; k < n; ++k) sn.out_lens.push_back(out_len[k]);
+  if (sn.out_lens.empty()) return 0;
+  const size_t cnt = std::min(sn.out_lens.size(), (size_t)window);
+  std::vector<int32_t> recent(sn.out_lens.end() - (long)cnt, sn.out_lens.end());
+  std::sort(recent.begin(), recent.end());
+  m->lout = (double)recent[(cnt - 1) / 2];
+  return 0;
+}
+
+// Response-path transitions (Sec. 7: state follows the request and response
+// paths).  kind 1: a queued request's first token (Q - 1, D + 1, P - tokens);
+// 2: generated tokens of the decoding requests (S + tokens); 3: a decoding
+// request finished (D - 1, S - tokens).  All or nothing: -5 if a counter
+// would go negative, -1 on a bad kind or instance.
+int orc_apply_events(void* h, const int32_t* inst, const int32_t* kind, const int64_t* tokens,
+                     int32_t n) {
+  Snapshot& sn = *static_cast<Snapshot*>(h);
+  std::vector<int32_t> D = sn.D, Q = sn.Q;
+  std::vector<int64_t> P = sn.P, S = sn.S;
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t i = inst[k];
+    if (i < 0 || i >= sn.n_inst || tokens[k] < 0) return -1;
+    if (kind[k] == 1) {
+      Q[i] -= 1;
+      D[i] += 1;
+      P[i] -= tokens[k];
+    } else if (kind[k] == 2) {
+      S[i] += tokens[k];
+    } else if (kind[k] == 3) {
+      D[i] -= 1;
+      S[i] -= tokens[k];
+    } else {
+      return -1;
+    }
+    if (D[i] < 0 || Q[i] < 0 || P[i] < 0 || S[i] < 0) return -5;
+  }
+  sn.D = D;
+  sn.Q = Q;
+  sn.P = P;
+  sn.S = S;
   return 0;
 }
 

@@ -42,7 +42,11 @@ PS_REQ_DTYPE = np.dtype([("pre_off", "<i8"), ("tail_off", "<i8"), ("pre_len", "<
                          ("tail_len", "<i4")])
 PS_RESULT_DTYPE = np.dtype([("instance", "<i4"), ("hit_blocks", "<i4"), ("ttft", "<f4"),
                             ("tpot", "<f4"), ("flags", "<u4")])
+PS_EVENT_DTYPE = np.dtype([("instance", "<i4"), ("kind", "<i4"), ("tokens", "<i8")])
 assert PS_REQ_DTYPE.itemsize == 24 and PS_RESULT_DTYPE.itemsize == 20
+assert PS_EVENT_DTYPE.itemsize == 16
+PS_EV_PREFILL_DONE, PS_EV_DECODE_TOKENS, PS_EV_FINISHED = 1, 2, 3
+PS_LOUT_WINDOW = 1024
 
 
 class PsModel(ctypes.Structure):
@@ -99,6 +103,10 @@ def load_library() -> ctypes.CDLL:
         "ps_read_state": ([vp, vp, vp, vp, vp, vp], i32),
         "ps_table_info": ([vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i32)], i32),
         "ps_last_error": ([vp], ctypes.c_char_p),
+        "ps_apply_events": ([vp, vp, i32], i32),
+        "ps_feedback_decode": ([vp, vp, vp, vp, i32], i32),
+        "ps_feedback_output": ([vp, vp, i32], i32),
+        "ps_read_model": ([vp, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -235,6 +243,33 @@ def ps_table_info(ctx) -> dict:
                 hits_in_lds=bool(lds.value))
 
 
+def ps_apply_events(ctx, inst, kind, tokens) -> None:
+    ev = np.zeros(len(inst), dtype=PS_EVENT_DTYPE)
+    ev["instance"], ev["kind"], ev["tokens"] = inst, kind, tokens
+    _check(ctx, load_library().ps_apply_events(ctx, ev.ctypes.data, len(ev)))
+
+
+def ps_feedback_decode(ctx, batch, ctx_tok, measured_s) -> None:
+    b, bp = _ptr(batch, np.int32)
+    c, cp = _ptr(ctx_tok, np.int64)
+    m, mp = _ptr(measured_s, np.float32)
+    _check(ctx, load_library().ps_feedback_decode(ctx, bp, cp, mp, len(b)))
+
+
+def ps_feedback_output(ctx, out_len) -> None:
+    o, op = _ptr(out_len, np.int32)
+    _check(ctx, load_library().ps_feedback_output(ctx, op, len(o)))
+
+
+def ps_read_model(ctx) -> dict:
+    g = np.zeros(PS_MAX_SEG, np.float32)
+    lout = ctypes.c_float()
+    n = ctypes.c_int32()
+    _check(ctx, load_library().ps_read_model(ctx, g.ctypes.data, ctypes.byref(lout),
+                                             ctypes.byref(n)))
+    return dict(gamma=g[:n.value].copy(), lout=float(lout.value))
+
+
 # ------------------------------------------------------------------ tensors
 def to_device_u64(a: np.ndarray, device="cuda") -> torch.Tensor:
     """uint64 host array -> int64 device tensor holding the same bits."""
@@ -290,3 +325,15 @@ class Scorer:
 
     def table_info(self) -> dict:
         return ps_table_info(self.ctx)
+
+    def apply_events(self, inst, kind, tokens) -> None:
+        ps_apply_events(self.ctx, inst, kind, tokens)
+
+    def feedback_decode(self, batch, ctx_tok, measured_s) -> None:
+        ps_feedback_decode(self.ctx, batch, ctx_tok, measured_s)
+
+    def feedback_output(self, out_len) -> None:
+        ps_feedback_output(self.ctx, out_len)
+
+    def model(self) -> dict:
+        return ps_read_model(self.ctx)

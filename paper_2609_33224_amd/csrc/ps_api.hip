@@ -49,6 +49,11 @@ struct ps_ctx {
   std::vector<InstState> h_state;
   std::vector<uint32_t> h_count;
   DevModel h_model{};
+  // feedback: EMA factors in double between updates; recent output lengths
+  std::vector<double> gamma64;
+  std::vector<int32_t> lout_ring;
+  int64_t lout_seen = 0;
+  float lout_raw = 0.0f;
   // staging for the host-memory entry points
   void* d_stage[3] = {nullptr, nullptr, nullptr};
   size_t stage_cap[3] = {0, 0, 0};
@@ -217,6 +222,12 @@ std::vector<int64_t> rooms_of(const std::vector<InstState>& hs, const DevModel& 
   return r;
 }
 
+int32_t segment_of_dev(const DevModel& m, int32_t B) {
+  for (int32_t s = 0; s < m.n_seg; ++s)
+    if (B <= m.seg_ub[s]) return s;
+  return m.n_seg - 1;
+}
+
 // Instance ids in the order of the packing key of a candidate with no cached
 // prefix: most decoding first, then fewest queued, then lowest id.
 std::vector<uint32_t> key_order(const std::vector<InstState>& hs) {
@@ -228,6 +239,30 @@ std::vector<uint32_t> key_order(const std::vector<InstState>& hs) {
     return x < y;
   });
   return o;
+}
+
+// Upload the host copy of the instance state and everything derived from it
+// (rooms, sorted rooms, key order).
+ps_status refresh_derived(ps_ctx* c) {
+  for (InstState& st : c->h_state) {
+    st.A1 = st.D + st.Q + 1;
+    st.seg = segment_of_dev(c->h_model, st.A1);
+  }
+  const std::vector<int64_t> room = rooms_of(c->h_state, c->h_model);
+  std::vector<int64_t> rs = room;
+  std::sort(rs.begin(), rs.end());
+  const std::vector<uint32_t> o0 = key_order(c->h_state);
+  HIP_TRY(c, hipMemcpy(c->d_inst, c->h_state.data(), c->h_state.size() * sizeof(InstState),
+                       hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemcpy(c->d_room, room.data(), room.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+  return PS_OK;
+}
+
+ps_status upload_model(ps_ctx* c) {
+  HIP_TRY(c, hipMemcpy(c->d_model, &c->h_model, sizeof c->h_model, hipMemcpyHostToDevice));
+  return PS_OK;
 }
 
 }  // namespace
@@ -452,6 +487,11 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->h_state = std::move(hs);
   c->h_count = std::move(hc);
   c->h_model = dm;
+  c->gamma64.assign((size_t)m->n_seg, 0.0);
+  for (int32_t k = 0; k < m->n_seg; ++k) c->gamma64[(size_t)k] = m->gamma[k];
+  c->lout_ring.clear();
+  c->lout_seen = 0;
+  c->lout_raw = m->lout;
   c->loaded = true;
   fresh.t.keys = nullptr;
   fresh.t.count = nullptr;
@@ -626,6 +666,116 @@ ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_
   HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
   HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
   if (n_dropped) *n_dropped = (int64_t)dropped;
+  return PS_OK;
+}
+
+ps_status ps_apply_events(ps_ctx* c, const ps_event* ev, int32_t n) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n < 0 || (n > 0 && !ev)) return fail(c, PS_E_INVAL, "bad event array");
+  std::vector<InstState> st = c->h_state;
+  for (int32_t k = 0; k < n; ++k) {
+    const ps_event& e = ev[k];
+    if (e.instance < 0 || e.instance >= c->n_inst)
+      return fail(c, PS_E_INVAL, "event %d: instance %d outside [0, %d)", k, e.instance, c->n_inst);
+    if (e.tokens < 0) return fail(c, PS_E_INVAL, "event %d: negative tokens", k);
+    InstState& s = st[(size_t)e.instance];
+    switch (e.kind) {
+      case PS_EV_PREFILL_DONE:
+        s.Q -= 1;
+        s.D += 1;
+        s.P -= e.tokens;
+        break;
+      case PS_EV_DECODE_TOKENS:
+        s.S += e.tokens;
+        break;
+      case PS_EV_FINISHED:
+        s.D -= 1;
+        s.S -= e.tokens;
+        break;
+      default:
+        return fail(c, PS_E_INVAL, "event %d: unknown kind %d", k, e.kind);
+    }
+    if (s.D < 0 || s.D > PS_MAX_DQ || s.Q < 0 || s.Q > PS_MAX_DQ || s.P < 0 ||
+        s.P > PS_MAX_PENDING || s.S < 0 || s.S > PS_MAX_CONTEXT)
+      return fail(c, PS_E_RANGE, "event %d leaves instance %d outside the counter limits", k,
+                  e.instance);
+  }
+  DeviceScope ds(c->device);
+  std::vector<InstState> old = c->h_state;
+  c->h_state = st;
+  ps_status rc = refresh_derived(c);
+  if (rc != PS_OK) c->h_state = old;
+  return rc;
+}
+
+ps_status ps_feedback_decode(ps_ctx* c, const int32_t* batch, const int64_t* ctx_tok,
+                             const float* measured_s, int32_t n) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n < 0 || (n > 0 && (!batch || !ctx_tok || !measured_s)))
+    return fail(c, PS_E_INVAL, "bad sample arrays");
+  for (int32_t k = 0; k < n; ++k)
+    if (batch[k] < 1 || ctx_tok[k] < 0 || !std::isfinite(measured_s[k]) || !(measured_s[k] > 0.0f))
+      return fail(c, PS_E_INVAL, "sample %d: batch >= 1, context >= 0, finite positive duration", k);
+  std::vector<double> g = c->gamma64;
+  const DevModel& m = c->h_model;
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t s = segment_of_dev(m, batch[k]);
+    const double pred = (double)m.seg[s][0] + (double)m.seg[s][1] * (double)batch[k] +
+                        (double)m.seg[s][2] * (double)ctx_tok[k];
+    if (!(pred > 0.0)) continue;
+    const double ratio = std::min(2.0, std::max(0.5, (double)measured_s[k] / pred));
+    g[(size_t)s] = std::min(2.0, std::max(1.0, 0.98 * g[(size_t)s] + 0.02 * ratio));
+  }
+  DeviceScope ds(c->device);
+  const DevModel keep = c->h_model;
+  for (int32_t s = 0; s < m.n_seg; ++s) c->h_model.seg[s][3] = (float)g[(size_t)s];
+  const ps_status rc = upload_model(c);
+  if (rc != PS_OK) {
+    c->h_model = keep;
+    return rc;
+  }
+  c->gamma64 = g;
+  return PS_OK;
+}
+
+ps_status ps_feedback_output(ps_ctx* c, const int32_t* out_len, int32_t n) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n < 0 || (n > 0 && !out_len)) return fail(c, PS_E_INVAL, "bad length array");
+  for (int32_t k = 0; k < n; ++k)
+    if (out_len[k] < 0) return fail(c, PS_E_INVAL, "output length %d is negative", k);
+  if (n == 0) return PS_OK;
+  std::vector<int32_t> ring = c->lout_ring;
+  int64_t seen = c->lout_seen;
+  if (ring.size() < (size_t)PS_LOUT_WINDOW) ring.resize(PS_LOUT_WINDOW, 0);
+  for (int32_t k = 0; k < n; ++k) ring[(size_t)((seen++) % PS_LOUT_WINDOW)] = out_len[k];
+  const size_t mlen = (size_t)std::min<int64_t>(seen, PS_LOUT_WINDOW);
+  std::vector<int32_t> win(ring.begin(), ring.begin() + (long)mlen);
+  std::nth_element(win.begin(), win.begin() + (long)((mlen - 1) / 2), win.end());
+  const float lout = (float)win[(mlen - 1) / 2];
+  DeviceScope ds(c->device);
+  const DevModel keep = c->h_model;
+  c->h_model.lout1 = std::max(1.0f, lout);
+  const ps_status rc = upload_model(c);
+  if (rc != PS_OK) {
+    c->h_model = keep;
+    return rc;
+  }
+  c->lout_ring = ring;
+  c->lout_seen = seen;
+  c->lout_raw = lout;
+  return PS_OK;
+}
+
+ps_status ps_read_model(ps_ctx* c, float* gamma, float* lout, int32_t* n_seg) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (gamma)
+    for (int32_t s = 0; s < c->h_model.n_seg; ++s) gamma[s] = c->h_model.seg[s][3];
+  if (lout) *lout = c->lout_raw;
+  if (n_seg) *n_seg = c->h_model.n_seg;
   return PS_OK;
 }
 

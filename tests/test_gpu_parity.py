@@ -368,3 +368,65 @@ def test_selectors_and_layers(ps, scorer, name, gen):
             compare_decisions(res, sizes, od, label=f"{name} {sel} {layer}")
             res2, _ = dw.score(scorer, with_sizes=False)
             assert res2.tobytes() == res.tobytes(), f"{name} {sel} {layer}: no-sizes path differs"
+
+
+# ------------------------------------------------------------- feedback path
+def test_feedback_path(ps, scorer):
+    """EMA calibration, the median output tracker and response-path
+    transitions applied to both sides, then a window scored on the result."""
+    w = synth.generate("c2", n_req=2048)
+    load_window(scorer, w)
+    o = oracle.Oracle.from_window(w)
+    m = oracle.model_of(w)
+    rng = np.random.default_rng(11)
+    n = 600
+    B = rng.integers(1, 700, n).astype(np.int32)
+    S = rng.integers(0, 3_000_000, n).astype(np.int64)
+    meas = rng.uniform(0.005, 0.2, n).astype(np.float32)
+    scorer.feedback_decode(B, S, meas)
+    oracle.feedback_decode(m, B, S, meas.astype(np.float64))
+    g = scorer.model()["gamma"]
+    want = np.array([m.gamma[k] for k in range(len(g))])
+    assert np.allclose(g, want, rtol=1e-6, atol=0), (g, want)
+    assert (g >= 1.0).all() and (g <= 2.0).all() and (np.abs(g - 1.0) > 1e-3).any()
+    outs = rng.integers(1, 4000, 1500).astype(np.int32)
+    scorer.feedback_output(outs)
+    o.feedback_output(m, outs)
+    assert scorer.model()["lout"] == m.lout
+    # valid transitions, drawn against a local copy of the counters
+    st = o.state()
+    D, Q, P, S_ = st["D"].astype(np.int64), st["Q"].astype(np.int64), st["P"].copy(), st["S"].copy()
+    inst, kind, tok = [], [], []
+    for _ in range(400):
+        i = int(rng.integers(0, w.n_inst))
+        k = int(rng.integers(1, 4))
+        if k == 1 and Q[i] > 0:
+            t = int(rng.integers(0, P[i] + 1))
+            Q[i] -= 1; D[i] += 1; P[i] -= t
+        elif k == 2:
+            t = int(rng.integers(0, 5000))
+            S_[i] += t
+        elif k == 3 and D[i] > 0:
+            t = int(rng.integers(0, S_[i] + 1))
+            D[i] -= 1; S_[i] -= t
+        else:
+            continue
+        inst.append(i); kind.append(k); tok.append(t)
+    scorer.apply_events(inst, kind, tok)
+    assert o.apply_events(inst, kind, tok) == 0
+    so, sg = o.state(), scorer.state()
+    for k in ("D", "Q", "P", "S"):
+        assert (so[k] == sg[k]).all(), k
+    # an out-of-range batch is refused as a whole
+    before = scorer.state()
+    j = int(np.argmin(sg["D"]))
+    with pytest.raises(ps.PackServeError) as e:
+        scorer.apply_events([0, j] + [j] * (int(sg["D"][j]) + 1),
+                            [2] + [3] * (int(sg["D"][j]) + 2), [1] * (int(sg["D"][j]) + 3))
+    assert e.value.code == -5
+    after = scorer.state()
+    for k in ("D", "Q", "P", "S"):
+        assert (before[k] == after[k]).all()
+    res, sizes = DeviceWindow(w).score(scorer)
+    od = o.score(m, w.pool, w.pre_off, w.pre_len, w.tail_off, w.tail_len)
+    compare_decisions(res, sizes, od, label="after feedback")

@@ -54,6 +54,11 @@ MUTANTS = [
     ("random k from low bits", "const uint64_t k = ((z >> 32) * (uint64_t)d.nT) >> 32;", "const uint64_t k = z % (uint64_t)d.nT;"),
     ("D-C-Q fallback over A", "if (c.inC && (!best || before(SEL_DCQ, c, *best))) best = &c;", "if ((!best || before(SEL_DCQ, c, *best))) best = &c;"),
     ("LMetric selector order", "if (la != lb) return la < lb;", "if (la != lb) return la > lb;"),
+    ("EMA weight", "const double w = 0.02;", "const double w = 0.2;"),
+    ("EMA ratio clip", "ratio = std::min(2.0, std::max(0.5, ratio));", "ratio = std::min(4.0, std::max(0.5, ratio));"),
+    ("EMA factor floor", "m->gamma[s] = std::min(2.0, std::max(1.0, f));", "m->gamma[s] = std::min(2.0, std::max(0.5, f));"),
+    ("upper median", "m->lout = (double)recent[(cnt - 1) / 2];", "m->lout = (double)recent[cnt / 2];"),
+    ("first token keeps pending", "P[i] -= tokens[k];", "P[i] -= 0;"),
     ("commit ignores cap", "if ((int64_t)set.size() < sn.cap) set.insert(key);", "if (true) set.insert(key);"),
 ]
 

@@ -599,3 +599,67 @@ def test_headroom_near_tie_is_flagged():
                     kv_cap_tokens=10**9, lout=1e9, flags=oracle.selector_flags(oracle.SEL_HCQ))
     d = _decide(w)
     assert d.inst[0] == 1 and d.nb[0] & oracle.NB_HEADROOM
+
+
+# -- feedback path: EMA calibration (Sec. 5.3), median output, transitions ----
+
+def _fb_model(gamma=(1.0, 1.0)):
+    return oracle.make_model([0.02, 1e-4, 0, 0, 0, 0], (8, 64), ((0.01, 1e-3, 1e-6), (0.02, 0.0, 0.0)),
+                             gamma, 0.5, 0.05, 2.0, 556.0, 16, 64, 10**6)
+
+
+def test_ema_update_rule():
+    """Factor f of the sample's segment: f <- clip(0.98 f + 0.02 clip(ratio,
+    0.5, 2), 1, 2), ratio = measured / (b0 + b1 B + b2 S) of the base model.
+    Segment 0 (B <= 8): prediction 0.01 + 0.001*4 + 1e-6*6000 = 0.02."""
+    m = _fb_model()
+    oracle.feedback_decode(m, [4], [6000], [0.03])          # ratio 1.5
+    assert m.gamma[0] == pytest.approx(0.98 + 0.03, rel=1e-12) and m.gamma[1] == 1.0
+    oracle.feedback_decode(m, [4], [6000], [0.2])           # ratio 10 -> clipped to 2
+    assert m.gamma[0] == pytest.approx(0.98 * 1.01 + 0.04, rel=1e-12)
+    m = _fb_model()
+    oracle.feedback_decode(m, [4], [6000], [0.001])         # ratio 0.05 -> 0.5; factor floor 1
+    assert m.gamma[0] == 1.0
+    m = _fb_model((2.0, 1.0))
+    oracle.feedback_decode(m, [4], [6000], [0.04])          # ratio 2 keeps 2 (ceiling)
+    assert m.gamma[0] == 2.0
+    m = _fb_model()
+    oracle.feedback_decode(m, [20], [0], [0.03])            # B = 20 -> segment 1, pred 0.02
+    assert m.gamma[1] == pytest.approx(1.01, rel=1e-12) and m.gamma[0] == 1.0
+    m = _fb_model()
+    oracle.feedback_decode(m, [4] * 2000, [6000] * 2000, [0.04] * 2000)
+    assert 1.99 < m.gamma[0] <= 2.0                        # converges to the clipped ratio
+
+
+def test_median_output_tracker():
+    w = synth.generate("c1", n_req=4)
+    o = oracle.Oracle.from_window(w)
+    m = oracle.model_of(w)
+    o.feedback_output(m, [5, 1, 3])
+    assert m.lout == 3.0                                    # sorted 1 3 5
+    o.feedback_output(m, [4])
+    assert m.lout == 3.0                                    # 1 3 4 5 -> lower median 3
+    o2 = oracle.Oracle.from_window(w)
+    m2 = oracle.model_of(w)
+    o2.feedback_output(m2, list(range(1, 1101)))            # keeps the last 1024: 77..1100
+    assert m2.lout == 77 + 511
+
+
+def test_event_transitions():
+    w = synth.generate("c1", n_req=4)
+    o = oracle.Oracle.from_window(w)
+    st0 = o.state()
+    i = int(np.argmax(st0["Q"]))
+    assert o.apply_events([i, i, i], [1, 2, 3], [100, 5000, 3000]) == 0
+    st = o.state()
+    assert st["Q"][i] == st0["Q"][i] - 1 and st["D"][i] == st0["D"][i]
+    assert st["P"][i] == st0["P"][i] - 100 and st["S"][i] == st0["S"][i] + 2000
+    # all or nothing: the second event would drive D below zero
+    j = int(np.argmin(st["D"]))
+    before = o.state()
+    assert o.apply_events([i, j] + [j] * (int(st["D"][j]) + 1), [2, 3] + [3] * (int(st["D"][j]) + 1),
+                          [1] * (int(st["D"][j]) + 3)) == -5
+    after = o.state()
+    for k in ("D", "Q", "P", "S"):
+        assert (before[k] == after[k]).all()
+    assert o.apply_events([0], [7], [0]) == -1
