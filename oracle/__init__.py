@@ -118,6 +118,12 @@ def _load():
     lib.orc_score.restype = ctypes.c_int
     lib.orc_commit.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.POINTER(i64)]
     lib.orc_commit.restype = ctypes.c_int
+    lib.orc_schedule.argtypes = [vp, ctypes.POINTER(Model), vp, vp, vp, vp, vp, i32,
+                                 vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i64)]
+    lib.orc_schedule.restype = ctypes.c_int
+    lib.orc_replay.argtypes = [vp, ctypes.POINTER(Model), vp, vp, vp, vp, vp, vp, i32,
+                               vp, vp, vp, ctypes.POINTER(i64)]
+    lib.orc_replay.restype = ctypes.c_int
     lib.orc_state.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.orc_state.restype = ctypes.c_int
     lib.orc_explain.argtypes = [vp, ctypes.POINTER(Model), vp, i32] + [vp] * 8
@@ -206,6 +212,35 @@ class Oracle:
                           int(nthreads))
         return d
 
+    def schedule(self, model: Model, pool, pre_off, pre_len, tail_off, tail_len):
+        """Algorithm 1 per arrival (the snapshot moves to the final state).
+        Returns (Decisions, dropped)."""
+        keep, ptrs = self._reqs(pool, pre_off, pre_len, tail_off, tail_len)
+        n = len(keep[1][0])
+        d = Decisions(inst=np.zeros(n, np.int32), hit=np.zeros(n, np.int32),
+                      ttft=np.zeros(n, np.float64), tpot=np.zeros(n, np.float64),
+                      flags=np.zeros(n, np.uint32), sizes=np.zeros((n, 3), np.uint32),
+                      nb=np.zeros(n, np.uint32))
+        dropped = ctypes.c_int64()
+        _load().orc_schedule(self._h, ctypes.byref(model), *ptrs, n, d.inst.ctypes.data,
+                             d.hit.ctypes.data, d.ttft.ctypes.data, d.tpot.ctypes.data,
+                             d.flags.ctypes.data, d.sizes.ctypes.data, d.nb.ctypes.data,
+                             ctypes.byref(dropped))
+        return d, int(dropped.value)
+
+    def replay(self, model: Model, pool, pre_off, pre_len, tail_off, tail_len, inst):
+        """Latencies of given placements at their arrival, committing each.
+        Returns (hit, ttft, tpot, dropped)."""
+        keep, ptrs = self._reqs(pool, pre_off, pre_len, tail_off, tail_len)
+        ia, ip = _c(inst, np.int32)
+        n = len(ia)
+        hit = np.zeros(n, np.int32)
+        ttft, tpot = np.zeros(n), np.zeros(n)
+        dropped = ctypes.c_int64()
+        _load().orc_replay(self._h, ctypes.byref(model), *ptrs, ip, n, hit.ctypes.data,
+                           ttft.ctypes.data, tpot.ctypes.data, ctypes.byref(dropped))
+        return hit, ttft, tpot, int(dropped.value)
+
     def commit(self, pool, pre_off, pre_len, tail_off, tail_len, inst, block_tokens=16) -> int:
         keep, ptrs = self._reqs(pool, pre_off, pre_len, tail_off, tail_len)
         ia, ip = _c(inst, np.int32)
@@ -252,6 +287,14 @@ class Oracle:
     def window_score(self, win, nthreads=0, **policy) -> Decisions:
         return self.score(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,
                           win.tail_off, win.tail_len, nthreads)
+
+    def window_schedule(self, win, **policy):
+        return self.schedule(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,
+                             win.tail_off, win.tail_len)
+
+    def window_replay(self, win, inst, **policy):
+        return self.replay(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,
+                           win.tail_off, win.tail_len, inst)
 
 
 def feedback_decode(model: Model, batch, ctx_tok, measured) -> None:

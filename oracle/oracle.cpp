@@ -29,6 +29,13 @@
 //   commit          - sequential application of decisions (Sec. 7: state is
 //                     updated along the request path).  Pinned by a
 //                     hand-traced sequence.
+//   schedule        - Algorithm 1 per arrival: score, then commit, request
+//                     by request.  Pinned by the round-robin closed form on
+//                     identical instances, capacity exhaustion, a hand-traced
+//                     session that follows its own blocks, and the TPOT
+//                     guarantee of every placement at its arrival.
+//   replay          - latencies of given placements at their arrival, then
+//                     commit.  Pinned by a hand-traced sequence.
 //
 // parity unpinned (the paper leaves these open; the oracle follows the
 // readings listed in the design notes and only hand cases of those readings
@@ -121,6 +128,24 @@ int segment_of(const orc_model& m, int64_t B) {
   return m.n_seg - 1;
 }
 
+// Eq. 10's TPOT and Eq. 4's TTFT of placing a request of L tokens (n new,
+// c cached) on instance i in the current state: the decode step of the
+// projected batch and context scaled by its segment's factor, plus the
+// request's prefill amortised over the median output length when the
+// instance is busy; the prefill plus the queueing estimate.
+void candidate_latency(const Snapshot& sn, const orc_model& m, int32_t i, int64_t n, int64_t c,
+                       int64_t L, double& tpot, double& ttft) {
+  const int64_t active = (int64_t)sn.D[i] + sn.Q[i];
+  const int64_t Bp = active + 1;
+  const double Sp = (double)(sn.S[i] + L);
+  const int s = segment_of(m, Bp);
+  const double t_iter = m.gamma[s] * (m.beta[s][0] + m.beta[s][1] * (double)Bp + m.beta[s][2] * Sp);
+  const double tpf = t_prefill(m, (double)n, (double)c);
+  const double interference = active > 0 ? tpf / std::max(1.0, m.lout) : 0.0;
+  tpot = t_iter + interference;
+  ttft = tpf + m.alpha[0] * (double)sn.Q[i] + m.alpha[1] * (double)sn.P[i];
+}
+
 struct Cand {
   int32_t i;
   int64_t hit;  // blocks
@@ -208,16 +233,7 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
   // SLO-aware admission (Eq. 10) and the TTFT estimate (Eq. 4).
   const double slo = std::max(m.ttft_floor, tpf_cold);
   for (Cand& c : A) {
-    const int32_t i = c.i;
-    const int64_t active = (int64_t)sn.D[i] + sn.Q[i];
-    const int64_t Bp = active + 1;
-    const double Sp = (double)(sn.S[i] + L);
-    const int s = segment_of(m, Bp);
-    const double t_iter = m.gamma[s] * (m.beta[s][0] + m.beta[s][1] * (double)Bp + m.beta[s][2] * Sp);
-    const double tpf = t_prefill(m, (double)c.n, (double)c.c);
-    const double interference = active > 0 ? tpf / std::max(1.0, m.lout) : 0.0;
-    c.tpot = t_iter + interference;
-    c.ttft = tpf + m.alpha[0] * (double)sn.Q[i] + m.alpha[1] * (double)sn.P[i];
+    candidate_latency(sn, m, c.i, c.n, c.c, L, c.tpot, c.ttft);
     const bool tpot_ok = (m.flags & F_NO_TPOT) || c.tpot < m.tau;
     const bool ttft_ok = !(m.flags & F_TTFT_ADMIT) || c.ttft <= slo;
     c.inT = c.inC && tpot_ok && ttft_ok;
@@ -336,6 +352,29 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
 Chain chain_of(const uint64_t* pool, const int64_t* pre_off, const int32_t* pre_len,
                const int64_t* tail_off, const int32_t* tail_len, int32_t r) {
   return Chain{pool + pre_off[r], pre_len[r], pool + tail_off[r], tail_len[r]};
+}
+
+// Place one request on instance i (Sec. 7: the request path updates the
+// instance's counters and its prefix tree as the request is routed): it
+// joins the queue (Q += 1), its uncached tokens, measured against the set
+// as it stands, join the pending prefill work, its tokens join the context
+// sum, and its blocks enter the set in chain order until the cap is
+// reached (refused blocks are counted in drop).  Returns the hit measured
+// before the blocks enter.
+int64_t commit_one(Snapshot& sn, const Chain& ch, int32_t i, int32_t block_tokens, int64_t& drop) {
+  auto& set = sn.sets[(size_t)i];
+  const int64_t L = (int64_t)ch.len() * block_tokens;
+  const int64_t hitb = prefix_hit(set, ch);
+  sn.Q[i] += 1;
+  sn.P[i] += L - hitb * block_tokens;
+  sn.S[i] += L;
+  for (int32_t j = 0; j < ch.len(); ++j) {
+    uint64_t key = ch.at(j);
+    if (set.count(key)) continue;
+    if ((int64_t)set.size() < sn.cap) set.insert(key);
+    else ++drop;
+  }
+  return hitb;
 }
 
 }  // namespace
@@ -459,18 +498,67 @@ int orc_commit(void* h, const uint64_t* pool, const int64_t* pre_off, const int3
     const int32_t i = inst[k];
     if (i < 0) continue;
     Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, k);
-    auto& set = sn.sets[(size_t)i];
-    const int64_t L = (int64_t)ch.len() * block_tokens;
-    const int64_t hitb = prefix_hit(set, ch);
-    sn.Q[i] += 1;
-    sn.P[i] += L - hitb * block_tokens;
-    sn.S[i] += L;
-    for (int32_t j = 0; j < ch.len(); ++j) {
-      uint64_t key = ch.at(j);
-      if (set.count(key)) continue;
-      if ((int64_t)set.size() < sn.cap) set.insert(key);
-      else ++drop;
+    (void)commit_one(sn, ch, i, block_tokens, drop);
+  }
+  *dropped = drop;
+  return 0;
+}
+
+// Algorithm 1 per arrival: the requests are taken in array order; each is
+// scored against the state left by the ones before it and, when placed,
+// committed (as orc_commit) before the next one is scored.  Outputs as
+// orc_score, plus the blocks refused at the cap in *dropped.  The snapshot
+// is left in the final state.
+int orc_schedule(void* h, const orc_model* m, const uint64_t* pool, const int64_t* pre_off,
+                 const int32_t* pre_len, const int64_t* tail_off, const int32_t* tail_len,
+                 int32_t n_req, int32_t* inst, int32_t* hit, double* ttft, double* tpot,
+                 uint32_t* flags, uint32_t* sizes, uint32_t* nb, int64_t* dropped) {
+  Snapshot& sn = *static_cast<Snapshot*>(h);
+  int64_t drop = 0;
+  std::vector<Cand> A;
+  for (int32_t r = 0; r < n_req; ++r) {
+    Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, r);
+    const Decision d = score_one(sn, *m, ch, A, r);
+    inst[r] = d.inst;
+    hit[r] = d.hit;
+    ttft[r] = d.ttft;
+    tpot[r] = d.tpot;
+    flags[r] = d.flags;
+    if (sizes) {
+      sizes[3 * (size_t)r] = d.nA;
+      sizes[3 * (size_t)r + 1] = d.nC;
+      sizes[3 * (size_t)r + 2] = d.nT;
     }
+    if (nb) nb[r] = d.nb;
+    if (d.inst >= 0) (void)commit_one(sn, ch, d.inst, m->block_tokens, drop);
+  }
+  *dropped = drop;
+  return 0;
+}
+
+// Given placements applied in array order (entries with instance -1 are
+// skipped): for each placed request, the hit, TTFT and TPOT its instance
+// offers at its arrival, i.e. in the state left by the entries before it,
+// then the commit of orc_commit.  Skipped entries get hit 0 and zero
+// latencies.
+int orc_replay(void* h, const orc_model* m, const uint64_t* pool, const int64_t* pre_off,
+               const int32_t* pre_len, const int64_t* tail_off, const int32_t* tail_len,
+               const int32_t* inst, int32_t n, int32_t* hit, double* ttft, double* tpot,
+               int64_t* dropped) {
+  Snapshot& sn = *static_cast<Snapshot*>(h);
+  int64_t drop = 0;
+  for (int32_t k = 0; k < n; ++k) {
+    hit[k] = 0;
+    ttft[k] = tpot[k] = 0.0;
+    const int32_t i = inst[k];
+    if (i < 0) continue;
+    Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, k);
+    const int64_t L = (int64_t)ch.len() * m->block_tokens;
+    const int64_t hb = prefix_hit(sn.sets[(size_t)i], ch);
+    const int64_t c = hb * m->block_tokens;
+    candidate_latency(sn, *m, i, L - c, c, L, tpot[k], ttft[k]);
+    hit[k] = (int32_t)hb;
+    (void)commit_one(sn, ch, i, m->block_tokens, drop);
   }
   *dropped = drop;
   return 0;

@@ -60,6 +60,12 @@ MUTANTS = [
     ("upper median", "m->lout = (double)recent[(cnt - 1) / 2];", "m->lout = (double)recent[cnt / 2];"),
     ("first token keeps pending", "P[i] -= tokens[k];", "P[i] -= 0;"),
     ("commit ignores cap", "if ((int64_t)set.size() < sn.cap) set.insert(key);", "if (true) set.insert(key);"),
+    ("schedule without commit", "if (d.inst >= 0) (void)commit_one(sn, ch, d.inst, m->block_tokens, drop);", "(void)0;"),
+    ("commit keeps the queue", "sn.Q[i] += 1;", "sn.Q[i] += 0;"),
+    ("replay measures after commit",
+     "    candidate_latency(sn, *m, i, L - c, c, L, tpot[k], ttft[k]);\n    hit[k] = (int32_t)hb;\n    (void)commit_one(sn, ch, i, m->block_tokens, drop);",
+     "    (void)commit_one(sn, ch, i, m->block_tokens, drop);\n    candidate_latency(sn, *m, i, L - c, c, L, tpot[k], ttft[k]);\n    hit[k] = (int32_t)hb;"),
+    ("replay hit after commit", "const int64_t hb = prefix_hit(sn.sets[(size_t)i], ch);", "const int64_t hb = ch.len();"),
 ]
 
 

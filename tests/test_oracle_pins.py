@@ -663,3 +663,132 @@ def test_event_transitions():
     for k in ("D", "Q", "P", "S"):
         assert (before[k] == after[k]).all()
     assert o.apply_events([0], [7], [0]) == -1
+
+
+# -- Algorithm 1 per arrival (each placement changes the state the next
+#    request sees) and the replay of given placements
+
+def _rr_window(n_inst=5, n_req=23, D=3, b_max=7):
+    """Identical idle-queue instances (same D, nothing cached) and requests of
+    four fresh blocks each (no block shared between requests)."""
+    chains = [chain_hashes(4, base=10_000 * (k + 1)) for k in range(n_req)]
+    return make_window([[] for _ in range(n_inst)], chains, [D] * n_inst, [0] * n_inst,
+                       [0] * n_inst, [0] * n_inst, SIMPLE_ALPHA, (64,), ((0.01, 0.0, 0.0),),
+                       (1.0,), cap=64, tpot_slo=10.0, b_max=b_max, kv_cap_tokens=10**9)
+
+
+def test_sequential_round_robin_closed_form():
+    """Equal D and no cache: each placement adds one to Q, so by D-C-Q the
+    k-th request goes to instance k mod n.  With A = D + Q, an instance takes
+    requests while A + 1 <= B_max, i.e. B_max - D = 4 of them; after n * 4
+    placements A is empty and every later request is rejected.  |A| at
+    request k of the last round, 15 + j, is n - j.  Against the snapshot all
+    of them pick instance 0."""
+    w = _rr_window()
+    o = oracle.Oracle.from_window(w)
+    d, dropped = o.window_schedule(w)
+    want = [k % 5 for k in range(20)] + [-1, -1, -1]
+    assert list(d.inst) == want
+    assert list(d.hit) == [0] * 23 and dropped == 0
+    nA = [5] * 15 + [5, 4, 3, 2, 1] + [0, 0, 0]
+    assert list(d.sizes[:, 0]) == nA
+    assert all(d.flags[20:] == oracle.R_REJECT)
+    st = o.state()
+    assert list(st["Q"]) == [4] * 5 and list(st["P"]) == [4 * 64] * 5
+    assert list(st["S"]) == [4 * 64] * 5 and list(st["set_size"]) == [16] * 5
+    snap = _decide(_rr_window())
+    assert list(snap.inst) == [0] * 23
+
+
+def _session_window():
+    """Two instances with D = 2 and nothing cached; requests: session A's
+    first 4 blocks, session B's first 4, A's first 6, B's first 5, and two
+    blocks of a third session.  eta = 0: only minimum-penalty candidates
+    pass the KVC-first stage."""
+    a = chain_hashes(6, base=1_000)
+    b = chain_hashes(5, base=2_000)
+    c = chain_hashes(2, base=3_000)
+    return make_window([[], []], [a[:4], b[:4], a, b, c], [2, 2], [0, 0], [0, 0], [0, 0],
+                       SIMPLE_ALPHA, (64,), ((0.01, 0.0, 0.0),), (1.0,), cap=64, eta=0.0,
+                       tpot_slo=10.0, b_max=100, kv_cap_tokens=10**9)
+
+
+def test_sequential_session_follows_its_blocks():
+    """Hand trace.  r0 (A, 4 blocks): tie -> instance 0; its blocks enter
+    instance 0, Q0 = 1.  r1 (B, 4): hits 0 / 0, D-C-Q by Q -> instance 1.
+    r2 (A, 6): hit 4 on instance 0, 0 on 1; eta = 0 keeps only instance 0.
+    r3 (B, 5): hit 4 on instance 1 -> 1.  r4 (C, 2): Q0 = Q1 = 2 -> 0.
+    r2's latencies on instance 0 (Q = 1, P = 64, S = 64): n = 32, c = 64
+    tokens, T_pf = 0.02 + 0.032 + 0.002048 + 0.001024 + 0.00064 +
+    0.000008192 = 0.055720192; TTFT = T_pf + 0.02 * 1 + 0.001 * 64;
+    TPOT = 0.01 + T_pf / 556 (busy instance).  The snapshot sends every
+    request to instance 0 with hit 0."""
+    w = _session_window()
+    o = oracle.Oracle.from_window(w)
+    d, _ = o.window_schedule(w)
+    assert list(d.inst) == [0, 1, 0, 1, 0]
+    assert list(d.hit) == [0, 0, 4, 4, 0]
+    tpf = 0.055720192
+    assert d.ttft[2] == pytest.approx(tpf + 0.02 + 0.064, rel=1e-12)
+    assert d.tpot[2] == pytest.approx(0.01 + tpf / 556.0, rel=1e-12)
+    st = o.state()
+    # P: instance 0 gets 64 + 32 + 32 new tokens, instance 1 gets 64 + 16
+    assert list(st["Q"]) == [3, 2] and list(st["P"]) == [128, 80]
+    assert list(st["S"]) == [64 + 96 + 32, 64 + 80] and list(st["set_size"]) == [8, 5]
+    snap = _decide(_session_window())
+    assert list(snap.inst) == [0] * 5 and list(snap.hit) == [0] * 5
+
+
+def test_replay_hand_trace():
+    """The snapshot's placements (all on instance 0) applied in arrival
+    order, each measured in the state the earlier ones left:
+      r0: hit 0, Q 0, P 0:    TTFT = T_pf(64, 0) = 0.088096
+      r1: hit 0, Q 1, P 64:   TTFT = 0.088096 + 0.02 + 0.064
+      r2: hit 4, Q 2, P 128:  TTFT = 0.055720192 + 0.04 + 0.128
+      r3: hit 4, Q 3, P 160:  T_pf(16, 64) = 0.037928192, + 0.06 + 0.16
+      r4: hit 0, Q 4, P 176:  T_pf(32, 0) = 0.053024, + 0.08 + 0.176
+    TPOT = 0.01 plus the interference T_pf / 556 (D = 2: always busy)."""
+    w = _session_window()
+    o = oracle.Oracle.from_window(w)
+    hit, ttft, tpot, dropped = o.window_replay(w, [0] * 5)
+    assert list(hit) == [0, 0, 4, 4, 0] and dropped == 0
+    tpf = [0.088096, 0.088096, 0.055720192, 0.037928192, 0.053024]
+    want = [tpf[0], tpf[1] + 0.084, tpf[2] + 0.168, tpf[3] + 0.22, tpf[4] + 0.256]
+    assert np.allclose(ttft, want, rtol=1e-12, atol=0)
+    assert np.allclose(tpot, [0.01 + t / 556.0 for t in tpf], rtol=1e-12, atol=0)
+    st = o.state()
+    assert list(st["Q"]) == [5, 0] and list(st["P"]) == [176 + 32, 0]
+    # skipped entries report zeros and change nothing
+    o2 = oracle.Oracle.from_window(w)
+    hit2, ttft2, _, _ = o2.window_replay(w, [-1, 1, -1, -1, -1])
+    assert list(hit2) == [0] * 5 and ttft2[0] == 0.0 and ttft2[1] == pytest.approx(0.088096)
+    assert list(o2.state()["Q"]) == [0, 1]
+
+
+def test_sequential_placements_hold_at_arrival():
+    """On a loaded generated window with a binding TPOT target: replaying the
+    per-arrival placements reproduces their hits and latencies exactly, and
+    every placement that is not a fallback meets the TPOT target in the state
+    it arrived to.  The snapshot's placements, replayed the same way, break
+    it (the herding that per-arrival scoring removes)."""
+    w = synth.generate("c1", seed=3)
+    pol = dict(tpot_slo=0.030, b_max=96)
+    o = oracle.Oracle.from_window(w)
+    d, dropped = o.window_schedule(w, **pol)
+    o2 = oracle.Oracle.from_window(w)
+    hit, ttft, tpot, dropped2 = o2.window_replay(w, d.inst, **pol)
+    placed = d.inst >= 0
+    assert placed.sum() > 0.9 * w.n_req
+    assert np.array_equal(hit[placed], d.hit[placed]) and dropped2 == dropped
+    assert np.array_equal(ttft[placed], d.ttft[placed])
+    assert np.array_equal(tpot[placed], d.tpot[placed])
+    tau = float(np.float32(0.030))
+    ok = placed & ((d.flags & oracle.R_FALLBACK) == 0)
+    assert (tpot[ok] < tau).all()
+    for k in ("Q", "P", "S", "set_size"):
+        assert np.array_equal(o.state()[k], o2.state()[k])
+    snap = _decide(w, **pol)
+    o3 = oracle.Oracle.from_window(w)
+    _, _, tpot_s, _ = o3.window_replay(w, snap.inst, **pol)
+    ok_s = (snap.inst >= 0) & ((snap.flags & oracle.R_FALLBACK) == 0)
+    assert (tpot_s[ok_s] >= tau).sum() > 0
