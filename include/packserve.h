@@ -211,6 +211,50 @@ ps_status ps_probe_hits_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_le
                             void* hip_stream);
 
 /*
+ * Algorithm 1 per arrival (Sec. 6 and 7 of the paper: one request at a time,
+ * the request path updating the chosen instance's counters and prefix tree
+ * before the next request is routed).  The device-resident window's
+ * requests are taken in array order; request r is scored against the state
+ * left by requests 0..r-1 (same scoring as ps_score_window_dev) and, when
+ * placed, committed as ps_commit would commit it, before request r + 1 is
+ * scored.  Results into d_out[n_req]; |A|, |C|, |T| into d_sizes[3 * n_req]
+ * if not NULL; blocks refused at the table cap into *n_dropped (host, may
+ * be NULL).  Malformed descriptors yield PS_R_INVALID and change nothing.
+ * Zero hashes in a chain are never inserted (nor counted as refused).
+ * Runs on `hip_stream` and returns once the window is scheduled and the
+ * context holds the final state.  PS_E_RANGE, before any change, if B_max
+ * or M_KV would let a counter leave its limit (B_max - 1 - D_i above
+ * PS_MAX_DQ; P_i or S_i plus M_KV - S_i above its limit).
+ */
+ps_status ps_schedule_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_len,
+                                 const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                                 uint32_t* d_sizes, int64_t* n_dropped, void* hip_stream);
+
+/*
+ * Device memory the two calls above may hold for the hits of the requests
+ * one launch schedules (n_inst x 4 bytes per request): a window whose hits
+ * exceed it is scheduled in several launches, in order, with identical
+ * results.  0 restores the default, 256 MiB; any budget admits at least one
+ * request per launch.  The memory is kept by the context until ps_destroy.
+ */
+ps_status ps_set_schedule_budget(ps_ctx* ctx, int64_t bytes);
+
+/*
+ * Replay given placements (device array d_inst[n_req], -1 = none) in array
+ * order: for each placed request, d_out gets the instance, the hit, TTFT
+ * and TPOT that instance offers at the request's arrival (the state left by
+ * the earlier entries; no capacity test) and PS_R_TTFT_MISS when TTFT
+ * exceeds the request's SLO; then the request is committed as ps_commit
+ * does.  Entries with -1 yield PS_R_REJECT.  Measures what placements made
+ * against one snapshot do to the requests that follow them.  PS_E_RANGE,
+ * before any change, for an instance outside [-1, n_inst) or a counter that
+ * would leave its limit.  Synchronous on `hip_stream` as above.
+ */
+ps_status ps_replay_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_len,
+                               const ps_req* d_reqs, int32_t n_req, const int32_t* d_inst,
+                               ps_result* d_out, int64_t* n_dropped, void* hip_stream);
+
+/*
  * Apply placements (host memory) in array order: entry k places request
  * reqs[k] on instance inst[k] (-1 = skip).  For each placed request, against
  * the table as left by the earlier entries: Q_i += 1, P_i += uncached tokens

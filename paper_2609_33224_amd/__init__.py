@@ -7,6 +7,7 @@ from .binding import (  # noqa: F401
     PS_R_REJECT, PS_R_TTFT_MISS, PS_REQ_DTYPE, PS_RESULT_DTYPE, PackServeError, PsModel, Scorer,
     load_library, make_model, pack_reqs, ps_commit, ps_create, ps_destroy, ps_last_error,
     ps_load_instances, ps_probe_hits_dev, ps_read_state, ps_score_window, ps_score_window_dev,
+    ps_schedule_window_dev, ps_replay_window_dev,
     ps_table_info, results_from_device, to_device_bytes, to_device_u64, ps_apply_events,
     ps_feedback_decode, ps_feedback_output, ps_read_model, PS_EV_PREFILL_DONE,
     PS_EV_DECODE_TOKENS, PS_EV_FINISHED, PS_LOUT_WINDOW,

@@ -100,6 +100,9 @@ def load_library() -> ctypes.CDLL:
         "ps_score_window_dev": ([vp, vp, i64, vp, i32, vp, vp, vp], i32),
         "ps_probe_hits_dev": ([vp, vp, i64, vp, i32, vp, vp], i32),
         "ps_commit": ([vp, vp, i64, vp, vp, i32, ctypes.POINTER(i64)], i32),
+        "ps_schedule_window_dev": ([vp, vp, i64, vp, i32, vp, vp, ctypes.POINTER(i64), vp], i32),
+        "ps_replay_window_dev": ([vp, vp, i64, vp, i32, vp, vp, ctypes.POINTER(i64), vp], i32),
+        "ps_set_schedule_budget": ([vp, i64], i32),
         "ps_read_state": ([vp, vp, vp, vp, vp, vp], i32),
         "ps_table_info": ([vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i32)], i32),
         "ps_last_error": ([vp], ctypes.c_char_p),
@@ -216,6 +219,30 @@ def ps_probe_hits_dev(ctx, d_pool: torch.Tensor, pool_len: int, d_reqs: torch.Te
         _stream_handle(stream)))
 
 
+def ps_schedule_window_dev(ctx, d_pool: torch.Tensor, pool_len: int, d_reqs: torch.Tensor,
+                           n_req: int, d_out: torch.Tensor,
+                           d_sizes: Optional[torch.Tensor] = None, stream=None) -> int:
+    """Algorithm 1 per arrival over a device-resident window; returns the
+    number of blocks refused at the table cap."""
+    dropped = ctypes.c_int64()
+    _check(ctx, load_library().ps_schedule_window_dev(
+        ctx, _dev_ptr(d_pool), int(pool_len), _dev_ptr(d_reqs), int(n_req), _dev_ptr(d_out),
+        _dev_ptr(d_sizes), ctypes.byref(dropped), _stream_handle(stream)))
+    return int(dropped.value)
+
+
+def ps_replay_window_dev(ctx, d_pool: torch.Tensor, pool_len: int, d_reqs: torch.Tensor,
+                         n_req: int, d_inst: torch.Tensor, d_out: torch.Tensor,
+                         stream=None) -> int:
+    """Latencies of given placements at their arrival, committing each;
+    returns the number of blocks refused at the table cap."""
+    dropped = ctypes.c_int64()
+    _check(ctx, load_library().ps_replay_window_dev(
+        ctx, _dev_ptr(d_pool), int(pool_len), _dev_ptr(d_reqs), int(n_req), _dev_ptr(d_inst),
+        _dev_ptr(d_out), ctypes.byref(dropped), _stream_handle(stream)))
+    return int(dropped.value)
+
+
 def ps_commit(ctx, pool: np.ndarray, reqs: np.ndarray, inst: np.ndarray) -> int:
     pool, pp = _ptr(pool, np.uint64)
     reqs = np.ascontiguousarray(reqs, dtype=PS_REQ_DTYPE)
@@ -319,6 +346,16 @@ class Scorer:
 
     def commit(self, pool, reqs, inst) -> int:
         return ps_commit(self.ctx, pool, reqs, inst)
+
+    def schedule_dev(self, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes=None, stream=None) -> int:
+        return ps_schedule_window_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes,
+                                      stream)
+
+    def set_schedule_budget(self, n_bytes: int) -> None:
+        _check(self.ctx, load_library().ps_set_schedule_budget(self.ctx, int(n_bytes)))
+
+    def replay_dev(self, d_pool, pool_len, d_reqs, n_req, d_inst, d_out, stream=None) -> int:
+        return ps_replay_window_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_inst, d_out, stream)
 
     def state(self) -> dict:
         return ps_read_state(self.ctx, self.n_inst)

@@ -57,6 +57,10 @@ struct ps_ctx {
   // staging for the host-memory entry points
   void* d_stage[3] = {nullptr, nullptr, nullptr};
   size_t stage_cap[3] = {0, 0, 0};
+  // per-arrival scheduler: hits of one launch's requests on every instance
+  uint32_t* d_seq_hits = nullptr;
+  size_t seq_hits_cap = 0;  // elements
+  size_t seq_budget = (size_t)256 << 20;  // bytes of hits per scheduler launch
 };
 
 namespace {
@@ -305,6 +309,7 @@ ps_status ps_destroy(ps_ctx* c) {
   dfree(c->d_counter);
   for (int k = 0; k < 3; ++k)
     if (c->d_stage[k]) (void)hipFree(c->d_stage[k]);
+  dfree(c->d_seq_hits);
   if (c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
   return PS_OK;
@@ -585,6 +590,29 @@ ps_status ps_score_window(ps_ctx* c, const uint64_t* pool, int64_t pool_len, con
   return PS_OK;
 }
 
+// After placements were committed on the device (work queued on `s`, the
+// dropped-block count in d_counter): read the counters back and rebuild the
+// derived data the window kernel reads (sorted rooms, key order, prefix
+// index).  Synchronous.
+static ps_status after_commit(ps_ctx* c, hipStream_t s, int64_t* n_dropped) {
+  unsigned long long dropped = 0;
+  HIP_TRY(c, hipMemcpyAsync(&dropped, c->d_counter, sizeof dropped, hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(c->h_state.data(), c->d_inst, c->h_state.size() * sizeof(InstState),
+                            hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(c->h_count.data(), c->t.count, c->h_count.size() * sizeof(uint32_t),
+                            hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  std::vector<int64_t> rs = rooms_of(c->h_state, c->h_model);
+  std::sort(rs.begin(), rs.end());
+  HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+  const std::vector<uint32_t> o0 = key_order(c->h_state);
+  HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+  HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  if (n_dropped) *n_dropped = (int64_t)dropped;
+  return PS_OK;
+}
+
 ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_req* reqs,
                     const int32_t* inst, int32_t n, int64_t* n_dropped) {
   if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
@@ -652,21 +680,126 @@ ps_status ps_commit(ps_ctx* c, const uint64_t* pool, int64_t pool_len, const ps_
   CommitArgs ca{c->t, c->d_inst, c->d_room, c->d_model, (const uint64_t*)dp, (const ps_req*)dr,
                 d_order, d_grp_off, d_grp_inst, (int32_t)n_grp, (uint32_t)c->cap, c->d_counter};
   HIP_TRY(c, ps_launch_commit(ca, s));
-  unsigned long long dropped = 0;
-  HIP_TRY(c, hipMemcpyAsync(&dropped, c->d_counter, sizeof dropped, hipMemcpyDeviceToHost, s));
-  HIP_TRY(c, hipMemcpyAsync(c->h_state.data(), c->d_inst, c->h_state.size() * sizeof(InstState),
-                            hipMemcpyDeviceToHost, s));
-  HIP_TRY(c, hipMemcpyAsync(c->h_count.data(), c->t.count, c->h_count.size() * sizeof(uint32_t),
-                            hipMemcpyDeviceToHost, s));
-  HIP_TRY(c, hipStreamSynchronize(s));
-  std::vector<int64_t> rs = rooms_of(c->h_state, c->h_model);
-  std::sort(rs.begin(), rs.end());
-  HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
-  const std::vector<uint32_t> o0 = key_order(c->h_state);
-  HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
-  HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
-  if (n_dropped) *n_dropped = (int64_t)dropped;
+  return after_commit(c, s, n_dropped);
+}
+
+static bool req_ok_host(const ps_req& q, int64_t pool_len) {
+  return q.pre_len >= 0 && q.tail_len >= 0 && q.pre_off >= 0 && q.tail_off >= 0 &&
+         q.pre_off <= pool_len && q.tail_off <= pool_len && q.pre_len <= pool_len - q.pre_off &&
+         q.tail_len <= pool_len - q.tail_off && (int64_t)q.pre_len + q.tail_len <= PS_MAX_CHAIN;
+}
+
+// Shared body of the per-arrival scheduler and the replay: launches of the
+// hits pass and the single-workgroup scheduler over chunks of requests,
+// then the refresh of the derived data.
+static ps_status run_sequential(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                                const ps_req* d_reqs, int32_t n_req, const int32_t* d_forced,
+                                ps_result* d_out, uint32_t* d_sizes, int64_t* n_dropped,
+                                hipStream_t s) {
+  const int32_t ni = c->n_inst;
+  const size_t per_req = (size_t)ni * sizeof(uint32_t);
+  const int32_t chunk = (int32_t)std::max<size_t>(1, std::min<size_t>((size_t)n_req, c->seq_budget / per_req));
+  const size_t need = (size_t)chunk * (size_t)ni;
+  if (need > c->seq_hits_cap) {
+    dfree(c->d_seq_hits);
+    c->seq_hits_cap = 0;
+    HIP_TRY(c, hipMalloc(&c->d_seq_hits, need * sizeof(uint32_t)));
+    c->seq_hits_cap = need;
+  }
+  HIP_TRY(c, hipMemsetAsync(c->d_counter, 0, sizeof(unsigned long long), s));
+  const int threads = (int)std::min<int64_t>(kSeqMaxThreads, ((int64_t)ni + 63) / 64 * 64);
+  for (int32_t r0 = 0; r0 < n_req; r0 += chunk) {
+    const int32_t r1 = std::min(n_req, r0 + chunk);
+    ScoreArgs pa{};
+    pa.t = c->t;
+    pa.x = c->x;
+    pa.inst = c->d_inst;
+    pa.room = c->d_room;
+    pa.model = c->d_model;
+    pa.pool = d_pool;
+    pa.pool_len = pool_len;
+    pa.reqs = d_reqs + r0;
+    pa.n_req = r1 - r0;
+    pa.n_inst = ni;
+    pa.hits_out = c->d_seq_hits;
+    const int grid = std::min(r1 - r0, std::max(1, c->num_cus) * 32);
+    HIP_TRY(c, ps_launch_score(pa, c->hits_in_lds, grid, true, s));
+    SeqArgs q{c->t, c->d_inst, c->d_room, c->d_model, d_pool, pool_len, d_reqs, r0, r1, ni,
+              c->d_seq_hits, d_forced, d_out, d_sizes, (uint32_t)c->cap, c->d_counter};
+    HIP_TRY(c, ps_launch_seq(q, threads, s));
+  }
+  return after_commit(c, s, n_dropped);
+}
+
+ps_status ps_set_schedule_budget(ps_ctx* c, int64_t bytes) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (bytes < 0) return fail(c, PS_E_INVAL, "negative budget");
+  c->seq_budget = bytes == 0 ? ((size_t)256 << 20) : (size_t)bytes;
   return PS_OK;
+}
+
+ps_status ps_schedule_window_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                                 const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                                 uint32_t* d_sizes, int64_t* n_dropped, void* hip_stream) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n_req < 0 || pool_len < 0) return fail(c, PS_E_INVAL, "negative n_req or pool_len");
+  if (n_dropped) *n_dropped = 0;
+  if (n_req == 0) return PS_OK;
+  if (!d_reqs || !d_out || (pool_len > 0 && !d_pool))
+    return fail(c, PS_E_INVAL, "device buffer is NULL");
+  // Every placement needs A + 1 <= B_max and S + L <= M_KV, which bounds the
+  // counters an instance can reach; they must stay inside their limits.
+  const DevModel& m = c->h_model;
+  for (int32_t i = 0; i < c->n_inst; ++i) {
+    const InstState& st = c->h_state[(size_t)i];
+    if ((int64_t)m.b_max - 1 - st.D > PS_MAX_DQ)
+      return fail(c, PS_E_RANGE, "instance %d: B_max - 1 - D exceeds the queued limit %d", i, PS_MAX_DQ);
+    const int64_t grow = std::max<int64_t>(0, m.kv_cap - st.S);
+    if (st.P + grow > PS_MAX_PENDING || st.S + grow > PS_MAX_CONTEXT)
+      return fail(c, PS_E_RANGE, "instance %d: M_KV allows token counters beyond their limits", i);
+  }
+  DeviceScope ds(c->device);
+  return run_sequential(c, d_pool, pool_len, d_reqs, n_req, nullptr, d_out, d_sizes, n_dropped,
+                        (hipStream_t)hip_stream);
+}
+
+ps_status ps_replay_window_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                               const ps_req* d_reqs, int32_t n_req, const int32_t* d_inst,
+                               ps_result* d_out, int64_t* n_dropped, void* hip_stream) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n_req < 0 || pool_len < 0) return fail(c, PS_E_INVAL, "negative n_req or pool_len");
+  if (n_dropped) *n_dropped = 0;
+  if (n_req == 0) return PS_OK;
+  if (!d_reqs || !d_out || !d_inst || (pool_len > 0 && !d_pool))
+    return fail(c, PS_E_INVAL, "device buffer is NULL");
+  DeviceScope ds(c->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  std::vector<int32_t> inst((size_t)n_req);
+  std::vector<ps_req> reqs((size_t)n_req);
+  HIP_TRY(c, hipMemcpyAsync(inst.data(), d_inst, inst.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(reqs.data(), d_reqs, reqs.size() * sizeof(ps_req), hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  const int32_t ni = c->n_inst;
+  const int64_t bs = c->h_model.bs;
+  std::vector<int32_t> cnt((size_t)ni, 0);
+  std::vector<int64_t> add((size_t)ni, 0);
+  for (int32_t k = 0; k < n_req; ++k) {
+    const int32_t i = inst[(size_t)k];
+    if (i < -1 || i >= ni) return fail(c, PS_E_RANGE, "entry %d: instance %d outside [-1, %d)", k, i, ni);
+    if (i < 0 || !req_ok_host(reqs[(size_t)k], pool_len)) continue;
+    cnt[(size_t)i] += 1;
+    add[(size_t)i] += ((int64_t)reqs[(size_t)k].pre_len + reqs[(size_t)k].tail_len) * bs;
+  }
+  for (int32_t i = 0; i < ni; ++i) {
+    const InstState& st = c->h_state[(size_t)i];
+    if (st.Q + cnt[(size_t)i] > PS_MAX_DQ)
+      return fail(c, PS_E_RANGE, "instance %d: queued would exceed %d", i, PS_MAX_DQ);
+    if (st.P + add[(size_t)i] > PS_MAX_PENDING || st.S + add[(size_t)i] > PS_MAX_CONTEXT)
+      return fail(c, PS_E_RANGE, "instance %d: token counters would exceed their limits", i);
+  }
+  return run_sequential(c, d_pool, pool_len, d_reqs, n_req, d_inst, d_out, nullptr, n_dropped, s);
 }
 
 ps_status ps_apply_events(ps_ctx* c, const ps_event* ev, int32_t n) {

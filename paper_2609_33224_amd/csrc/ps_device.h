@@ -133,6 +133,33 @@ struct CommitArgs {
   unsigned long long* dropped;
 };
 
+// One launch of the per-arrival scheduler: requests [r0, r1) of the window,
+// taken in order by a single workgroup.  `hits` holds every request's hit on
+// every instance at the launch's starting state, (r1 - r0) x n_inst; the
+// kernel extends them in place where a block committed by an earlier
+// request of the launch continues the prefix.
+constexpr int kSeqMaxThreads = 512;  // workgroup of the per-arrival scheduler
+constexpr int kSeqWaves = kSeqMaxThreads / 64;
+constexpr uint32_t kExtMax = 128;    // hit extensions walked by whole waves per request
+
+struct SeqArgs {
+  Tables t;
+  InstState* inst;
+  int64_t* room;
+  const DevModel* model;
+  const uint64_t* pool;
+  int64_t pool_len;
+  const ps_req* reqs;      // the whole window (r indexes it)
+  int32_t r0, r1;
+  int32_t n_inst;
+  uint32_t* hits;
+  const int32_t* forced;   // replay: placement of every request (-1 none); null: Algorithm 1
+  ps_result* out;          // whole window
+  uint32_t* sizes;         // optional |A|,|C|,|T| (Algorithm 1 only)
+  uint32_t cap;            // distinct keys allowed per instance
+  unsigned long long* dropped;
+};
+
 struct BuildArgs {
   Tables t;
   const int64_t* blk_off;
@@ -160,4 +187,8 @@ hipError_t ps_build_index(const ps::Tables& t, int32_t n_inst, const uint32_t* c
                           ps::GIndex* x, hipStream_t s);
 void ps_free_index(ps::GIndex* x);
 hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
+// Per-arrival scheduler: one workgroup of `threads` (a multiple of 64, at
+// most kSeqMaxThreads) over requests [a.r0, a.r1).
+hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);
+size_t ps_seq_lds_bytes(int32_t n_inst);
 size_t ps_score_lds_bytes(int32_t n_inst);

@@ -1076,6 +1076,308 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
   }
 }
 
+// ----------------------------------------------------- per-arrival scheduler
+// One wave's share of a workgroup-wide reduction.
+struct SeqPart {
+  uint64_t keyT, keyF;
+  uint32_t hroom, nC, nT, wmin, nA, cnt;
+};
+
+// Algorithm 1 per arrival (each placement changes the state the next
+// request is scored against).  One workgroup takes the launch's requests in
+// order; thread t owns the instances t, t + blockDim.x, ...  Per request:
+//  (1) live hits: the hit at the launch's start, extended where an instance
+//      that took a request earlier in the launch now holds the next block
+//      (one probe per such instance; the extensions are walked by whole
+//      waves along the instance's row);
+//  (2) W_min and |A| over the capacity-eligible instances, then C, T and the
+//      selector's key exactly as the window kernel evaluates them, each
+//      reduced over the workgroup (every thread combines the waves'
+//      partials, so all of them hold the decision);
+//  (3) the owner of the chosen instance writes the result and moves the
+//      instance's counters; wave 0 inserts the request's new blocks into
+//      the instance's table and row, in chain order, up to the cap.
+// The next request starts after a barrier and a device-scope fence, so its
+// probes and walks see those inserts.  Replay (a.forced): (2) is skipped and
+// the given instance is measured and committed.
+__global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int32_t n_inst = a.n_inst;
+  const int32_t nw = (n_inst + 63) >> 6;
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
+  uint64_t* dirty = stage + kStage;  // instances that took a request in this launch
+  SeqPart* part = reinterpret_cast<SeqPart*>(dirty + nw);             // 2 x kSeqWaves
+  uint32_t* ext = reinterpret_cast<uint32_t*>(part + 2 * kSeqWaves);  // kExtMax x (id, from)
+  uint32_t* shv = ext + 2 * kExtMax;  // [0] extensions, [1] chosen hit, [2] random pick
+  const int tid = threadIdx.x;
+  const int NT = blockDim.x;
+  const int lane = tid & 63, wv = tid >> 6, nwv = NT >> 6;
+  const int g = lane >> 3, s = lane & 7;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  const DevModel& m = *a.model;
+  const bool replay = a.forced != nullptr;
+  ScoreArgs sa{};
+  sa.inst = a.inst;
+  for (int32_t w = tid; w < nw; w += NT) dirty[w] = 0ull;
+  unsigned long long drop = 0;
+  int pb = 0;  // partial buffer of the next reduction (alternates)
+
+  for (int32_t r = a.r0; r < a.r1; ++r) {
+    __syncthreads();
+    __threadfence();  // acquire: the previous request's inserts, rows and counters
+    const ps_req q = a.reqs[r];
+    if (!req_valid(q, a.pool_len)) {
+      if (tid == 0) {
+        a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
+        if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+      }
+      continue;
+    }
+    const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
+    const int32_t ell = c.len;
+    const int64_t L = (int64_t)ell * m.bs;
+    const float Lf = (float)L;
+    const int32_t nst = ell < kStage ? ell : kStage;
+    uint32_t* H = a.hits + (size_t)(r - a.r0) * (size_t)n_inst;
+    for (int32_t j = tid; j < nst; j += NT) stage[j] = chain_global(c, j);
+    if (tid == 0) {
+      shv[0] = 0u;
+      shv[2] = ~0u;
+    }
+    __syncthreads();
+
+    // (1) live hits
+    for (int32_t i = tid; i < n_inst; i += NT) {
+      if (!test_bit(dirty, (uint32_t)i)) continue;
+      const uint32_t v = H[i];
+      if ((int32_t)v >= ell) continue;
+      const uint64_t key = v < (uint32_t)kStage ? stage[v] : chain_global(c, (int32_t)v);
+      if (!probe(a.t, (uint32_t)i, key)) continue;
+      const uint32_t e = atomicAdd(&shv[0], 1u);
+      if (e < kExtMax) {
+        ext[2 * e] = (uint32_t)i;
+        ext[2 * e + 1] = v + 1u;
+      } else {  // beyond the list: walk it alone
+        uint32_t h = v + 1u;
+        while ((int32_t)h < ell &&
+               probe(a.t, (uint32_t)i, h < (uint32_t)kStage ? stage[h] : chain_global(c, (int32_t)h)))
+          ++h;
+        H[i] = h;
+      }
+    }
+    __syncthreads();
+    const uint32_t n_ext = shv[0] < kExtMax ? shv[0] : kExtMax;
+    for (uint32_t e = (uint32_t)wv; e < n_ext; e += (uint32_t)nwv) {
+      const uint32_t i = ext[2 * e];
+      const uint32_t h = run_walk<true>(a.t, i, c, stage, (int32_t)ext[2 * e + 1], g, s);
+      if (lane == 0) H[i] = h;
+    }
+    __syncthreads();
+
+    const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
+    const float tpf_cold = t_prefill(m, Lf, 0.0f);
+    const float slo = fmaxf(m.ttft_floor, tpf_cold);
+    const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+    int32_t best = -1;
+    uint32_t fl = PS_R_REJECT;
+    uint32_t nA = 0, nC = 0, nT = 0;
+    if (replay) {
+      best = a.forced[r];
+      fl = 0;
+    } else {
+      // (2a) minimum recomputation penalty over A, and |A|
+      uint32_t wl = 0x7F800000u, al = 0;
+      for (int32_t i = tid; i < n_inst; i += NT) {
+        const InstState st = a.inst[i];
+        if (!eligible(m, st.A1, st.S, L)) continue;
+        ++al;
+        const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)H[i] * m.bs), Lf));
+        const uint32_t wb = __float_as_uint(W);
+        wl = wb < wl ? wb : wl;
+      }
+      wl = (uint32_t)wave_min_u64((uint64_t)wl);
+      al = wave_sum_u32(al);
+      if (lane == 0) {
+        part[pb * kSeqWaves + wv].wmin = wl;
+        part[pb * kSeqWaves + wv].nA = al;
+      }
+      __syncthreads();
+      uint32_t wmin_bits = 0x7F800000u;
+      for (int k = 0; k < nwv; ++k) {
+        const SeqPart& p = part[pb * kSeqWaves + k];
+        wmin_bits = p.wmin < wmin_bits ? p.wmin : wmin_bits;
+        nA += p.nA;
+      }
+      pb ^= 1;
+      const float wmin = __uint_as_float(wmin_bits);
+
+      // (2b) filters and keys
+      Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
+      if (nA > 0) {
+        for (int32_t i = tid; i < n_inst; i += NT) {
+          const InstState st = a.inst[i];
+          if (eligible(m, st.A1, st.S, L))
+            evaluate(sa, m, acc, (uint32_t)i, H[i], L, Lf, wmin, Z, kvc, slo);
+        }
+      }
+      uint64_t kT;
+      uint32_t hr = ~0u;
+      if (m.sel == PS_SEL_HCQ) {
+        const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
+        kT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
+        hr = (uint32_t)hmin;
+      } else {
+        kT = wave_min_u64(acc.keyT);
+      }
+      const uint64_t kF = wave_min_u64(acc.keyF);
+      const uint32_t cC = wave_sum_u32(acc.nC);
+      const uint32_t cT = wave_sum_u32(acc.nT);
+      if (lane == 0) {
+        SeqPart& p = part[pb * kSeqWaves + wv];
+        p.keyT = kT;
+        p.keyF = kF;
+        p.hroom = hr;
+        p.nC = cC;
+        p.nT = cT;
+      }
+      __syncthreads();
+      uint64_t keyT = ~0ull, keyF = ~0ull;
+      uint32_t hroom = ~0u;
+      for (int k = 0; k < nwv; ++k) {
+        const SeqPart& p = part[pb * kSeqWaves + k];
+        if (m.sel == PS_SEL_HCQ) {
+          if (p.hroom < hroom || (p.hroom == hroom && p.keyT < keyT)) {
+            hroom = p.hroom;
+            keyT = p.keyT;
+          }
+        } else {
+          keyT = p.keyT < keyT ? p.keyT : keyT;
+        }
+        keyF = p.keyF < keyF ? p.keyF : keyF;
+        nC += p.nC;
+        nT += p.nT;
+      }
+      pb ^= 1;
+
+      if (m.sel == PS_SEL_RANDOM && nT > 0) {
+        // the k-th member of T in id order
+        const uint64_t z = splitmix64_at(m.rand_seed, r);
+        const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
+        const float wmin2 = wmin;
+        uint32_t seen = 0;
+        for (int32_t base = 0; base < n_inst; base += NT) {
+          const int32_t i = base + tid;
+          bool inT = false;
+          if (i < n_inst) {
+            const InstState st = a.inst[i];
+            if (eligible(m, st.A1, st.S, L))
+              inT = member(sa, m, (uint32_t)i, H[i], L, Lf, wmin2, Z, kvc, slo).inT;
+          }
+          const uint64_t mm = __ballot(inT);
+          if (lane == 0) part[pb * kSeqWaves + wv].cnt = (uint32_t)__popcll(mm);
+          __syncthreads();
+          uint32_t before = seen, tot = 0;
+          for (int k = 0; k < nwv; ++k) {
+            const uint32_t cn = part[pb * kSeqWaves + k].cnt;
+            if (k < wv) before += cn;
+            tot += cn;
+          }
+          pb ^= 1;
+          if (seen + tot > kth) {
+            if (inT && before + (uint32_t)__popcll(mm & lt_mask) == kth) shv[2] = (uint32_t)i;
+            __syncthreads();
+            keyT = shv[2] < (uint32_t)n_inst ? (uint64_t)shv[2] : ~0ull;
+            break;
+          }
+          seen += tot;
+        }
+      }
+
+      // Decision.  With finite arithmetic C holds the minimum-penalty
+      // candidate whenever A is non-empty; the key test only keeps a
+      // non-finite model from selecting an out-of-range id.
+      if (nA > 0 && (keyT != ~0ull || keyF != ~0ull)) {
+        fl = 0;
+        if (keyT != ~0ull) {
+          best = (int32_t)(keyT & 0xFFFFu);
+        } else {
+          best = (int32_t)(keyF & 0xFFFFu);
+          fl |= PS_R_FALLBACK;
+        }
+      }
+    }
+
+    // (3) result and commit
+    if (best >= 0 && best % NT == tid) {
+      const uint32_t v = H[best];
+      const int64_t c_tok = (int64_t)v * m.bs;
+      InstState st = a.inst[best];
+      const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
+      if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
+      a.out[r] = ps_result{best, (int32_t)v, lt.ttft, lt.tpot, fl};
+      if (a.sizes) {
+        a.sizes[3 * (size_t)r] = nA;
+        a.sizes[3 * (size_t)r + 1] = nC;
+        a.sizes[3 * (size_t)r + 2] = nT;
+      }
+      st.Q += 1;
+      st.A1 += 1;
+      st.P += L - c_tok;
+      st.S += L;
+      st.seg = segment_of(m, st.A1);
+      a.inst[best] = st;
+      a.room[best] = st.A1 <= m.b_max ? m.kv_cap - st.S : -1;
+      dirty[best >> 6] |= 1ull << (best & 63);
+      shv[1] = v;
+    } else if (best < 0 && tid == 0) {
+      a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+      if (a.sizes) {
+        a.sizes[3 * (size_t)r] = nA;
+        a.sizes[3 * (size_t)r + 1] = nC;
+        a.sizes[3 * (size_t)r + 2] = nT;
+      }
+    }
+    __syncthreads();
+    if (best >= 0 && wv == 0) {
+      const uint32_t inst = (uint32_t)best;
+      uint32_t count = a.t.count[inst];
+      for (int32_t base = (int32_t)shv[1]; base < ell; base += 64) {
+        const int32_t j = base + lane;
+        const bool in = j < ell;
+        const uint64_t key = in ? (j < kStage ? stage[j] : chain_global(c, j)) : 0ull;
+        const bool present = in && key != 0ull ? probe(a.t, inst, key) : true;
+        // repeated keys inside this chunk: only the first occurrence counts
+        int first = lane;
+        for (int sl = 63; sl >= 0; --sl) {
+          const uint64_t o = __shfl(key, sl);
+          if (sl < lane && o == key) first = sl;
+        }
+        const bool dup = first != lane;
+        const bool want = !present && !dup;
+        const uint64_t wm = __ballot(want);
+        const uint32_t rank = (uint32_t)__popcll(wm & lt_mask);
+        const uint32_t room = a.cap > count ? a.cap - count : 0u;
+        const bool ins = want && rank < room;
+        if (ins) {  // new blocks join the row in chain order
+          uint32_t slot = 0;
+          (void)insert_key(a.t, inst, key, &slot);
+          a.t.rows[(size_t)inst * a.t.row_cap + count + rank] = key;
+          a.t.rowpos[(size_t)inst * a.t.slots + slot] = count + rank;
+        }
+        const uint64_t im = __ballot(ins);
+        const uint64_t dup_drop = __ballot(!present && dup && !((im >> first) & 1ull));
+        const uint32_t nins = (uint32_t)__popcll(im);
+        count += nins;
+        drop += (unsigned long long)(__popcll(wm) - nins + __popcll(dup_drop));
+        __threadfence();  // later probes of this wave must see these inserts
+      }
+      if (lane == 0) a.t.count[inst] = count;
+    }
+    __threadfence();  // release: this request's inserts, rows and counters
+  }
+  if (tid == 0 && drop) atomicAdd(a.dropped, drop);
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
@@ -1125,5 +1427,19 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
 hipError_t ps_launch_commit(const CommitArgs& a, hipStream_t s) {
   if (a.n_grp == 0) return hipSuccess;
   hipLaunchKernelGGL(commit_kernel, dim3(a.n_grp), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+size_t ps_seq_lds_bytes(int32_t n_inst) {
+  const size_t nw = ((size_t)n_inst + 63) / 64;
+  return (size_t)kStage * sizeof(uint64_t) + nw * sizeof(uint64_t) +
+         2 * (size_t)kSeqWaves * sizeof(SeqPart) + 2 * (size_t)kExtMax * sizeof(uint32_t) +
+         4 * sizeof(uint32_t);
+}
+
+hipError_t ps_launch_seq(const SeqArgs& a, int threads, hipStream_t s) {
+  if (a.r1 <= a.r0) return hipSuccess;
+  if (threads < 64 || threads > kSeqMaxThreads || threads % 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(seq_kernel, dim3(1), dim3(threads), ps_seq_lds_bytes(a.n_inst), s, a);
   return hipGetLastError();
 }

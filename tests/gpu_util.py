@@ -26,6 +26,31 @@ def reqs_of(win):
     return ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
 
 
+# Edge-case windows: a smooth synthetic model (fp32 coefficients) and random
+# load, with explicit per-instance block lists and request chains.
+ALPHA = [0.02, 1e-4, 1.5e-9, 7.5e-10, 1e-7, 1e-14]
+SEG_UB, BETA, GAMMA = (8, 64, 512), ((0.01, 1e-4, 1e-8),) * 3, (1.0, 1.1, 1.2)
+
+
+def edge_window(sets, chains, **kw):
+    from tests.tinywin import make_window
+    n = len(sets)
+    rng = np.random.default_rng(len(sets) * 7 + len(chains))
+    D = kw.pop("D", rng.integers(0, 64, n))
+    Q = kw.pop("Q", rng.integers(0, 4, n))
+    P = kw.pop("P", rng.integers(0, 8192, n) * (np.asarray(Q) > 0))
+    S = kw.pop("S", rng.integers(0, 500_000, n))
+    cap = kw.pop("cap", max(max((len(s) for s in sets), default=1), 1))
+    kw.setdefault("tpot_slo", 0.05)
+    kw.setdefault("b_max", 512)
+    kw.setdefault("kv_cap_tokens", 4_194_304)
+    w = make_window(sets, chains, D, Q, P, S, ALPHA, SEG_UB, BETA, GAMMA, cap=cap, **kw)
+    w.alpha = np.asarray(w.alpha, np.float32)
+    w.beta = np.asarray(w.beta, np.float32)
+    w.gamma = np.asarray(w.gamma, np.float32)
+    return w
+
+
 class DeviceWindow:
     """The window's pool and descriptors resident on the GPU."""
 
@@ -53,6 +78,29 @@ class DeviceWindow:
             return res, None
         sizes = self.d_sizes.cpu().numpy().view(np.uint32).reshape(-1, 3)[:self.n_req]
         return res, sizes
+
+    def schedule(self, scorer, with_sizes=True):
+        """Algorithm 1 per arrival: (results, sizes or None, dropped)."""
+        import paper_2609_33224_amd as ps
+        import torch
+        dropped = scorer.schedule_dev(self.d_pool, self.pool_len, self.d_reqs, self.n_req,
+                                      self.d_out, self.d_sizes if with_sizes else None)
+        torch.cuda.synchronize()
+        res = ps.results_from_device(self.d_out)[:self.n_req]
+        sizes = None
+        if with_sizes:
+            sizes = self.d_sizes.cpu().numpy().view(np.uint32).reshape(-1, 3)[:self.n_req]
+        return res, sizes, dropped
+
+    def replay(self, scorer, inst):
+        """Given placements measured at arrival: (results, dropped)."""
+        import paper_2609_33224_amd as ps
+        import torch
+        d_inst = torch.from_numpy(np.ascontiguousarray(inst, np.int32)).to("cuda")
+        dropped = scorer.replay_dev(self.d_pool, self.pool_len, self.d_reqs, self.n_req, d_inst,
+                                    self.d_out)
+        torch.cuda.synchronize()
+        return ps.results_from_device(self.d_out)[:self.n_req], dropped
 
     def hits(self, scorer, n_inst):
         import torch
@@ -89,3 +137,27 @@ def compare_decisions(res, sizes, od, idx=None, tol=NB_TOL, label=""):
         rel = np.abs(g - r) / np.maximum(np.abs(r), 1e-30)
         assert (rel <= tol).all(), f"{label}: {name} rel err {rel.max():.3g} > {tol}"
     return int(nb_dec.sum())
+
+
+def compare_sequential(res, sizes, od, tol=NB_TOL, label=""):
+    """Per-arrival results against the oracle's, in arrival order, up to the
+    first request whose decision differs; that request must carry a
+    near-boundary flag (from there on the two states differ and nothing
+    later is comparable).  Returns the number of requests compared."""
+    n = len(od.inst)
+    diff = (res["instance"] != od.inst) | (res["hit_blocks"] != od.hit)
+    bad = np.nonzero(diff)[0]
+    upto = n
+    if len(bad):
+        k = int(bad[0])
+        assert od.nb[k] & oracle.NB_DECISION, (
+            f"{label}: request {k} differs without a near-boundary flag: gpu {res[k]} "
+            f"oracle inst={od.inst[k]} hit={od.hit[k]} flags={od.flags[k]} sizes={od.sizes[k]}")
+        upto = k
+    head = oracle.Decisions(inst=od.inst[:upto], hit=od.hit[:upto], ttft=od.ttft[:upto],
+                            tpot=od.tpot[:upto], flags=od.flags[:upto], sizes=od.sizes[:upto],
+                            nb=od.nb[:upto])
+    if upto:
+        sz = sizes[:upto] if sizes is not None else od.sizes[:upto]
+        compare_decisions(res[:upto], sz, head, tol=tol, label=label)
+    return upto

@@ -20,7 +20,8 @@ def test_header_declares_the_entry_points():
     names = _declared()
     for n in ("ps_create", "ps_destroy", "ps_load_instances", "ps_score_window",
               "ps_score_window_dev", "ps_probe_hits_dev", "ps_commit", "ps_read_state",
-              "ps_table_info", "ps_last_error"):
+              "ps_table_info", "ps_last_error", "ps_schedule_window_dev",
+              "ps_replay_window_dev"):
         assert n in names
 
 
@@ -49,6 +50,8 @@ def test_errors_without_a_context():
     assert lib.ps_load_instances(None, None, None) == ps.binding.PS_E_INVAL
     assert lib.ps_score_window(None, None, 0, None, 0, None) == ps.binding.PS_E_INVAL
     assert lib.ps_commit(None, None, 0, None, None, 0, None) == ps.binding.PS_E_INVAL
+    assert lib.ps_schedule_window_dev(None, None, 0, None, 0, None, None, None, None) == ps.binding.PS_E_INVAL
+    assert lib.ps_replay_window_dev(None, None, 0, None, 0, None, None, None, None) == ps.binding.PS_E_INVAL
     assert b"ctx is NULL" in lib.ps_last_error(None)
 
 

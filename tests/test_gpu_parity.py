@@ -13,6 +13,7 @@ import pytest
 import oracle
 import synth
 from tests.gpu_util import DeviceWindow, compare_decisions, gpu_model, load_window, reqs_of
+from tests.gpu_util import edge_window as _edge
 from tests.tinywin import chain_hashes, make_window
 
 pytestmark = pytest.mark.gpu
@@ -106,28 +107,8 @@ def test_policy_variants(ps, scorer, policy):
 
 
 # ------------------------------------------------------------- edge windows
-ALPHA = [0.02, 1e-4, 1.5e-9, 7.5e-10, 1e-7, 1e-14]
-SEG_UB, BETA, GAMMA = (8, 64, 512), ((0.01, 1e-4, 1e-8),) * 3, (1.0, 1.1, 1.2)
-
-
-def _edge(sets, chains, n=None, **kw):
-    n = len(sets)
-    rng = np.random.default_rng(len(sets) * 7 + len(chains))
-    D = kw.pop("D", rng.integers(0, 64, n))
-    Q = kw.pop("Q", rng.integers(0, 4, n))
-    P = kw.pop("P", rng.integers(0, 8192, n) * (np.asarray(Q) > 0))
-    S = kw.pop("S", rng.integers(0, 500_000, n))
-    cap = kw.pop("cap", max(max((len(s) for s in sets), default=1), 1))
-    kw.setdefault("tpot_slo", 0.05)
-    kw.setdefault("b_max", 512)
-    kw.setdefault("kv_cap_tokens", 4_194_304)
-    return make_window(sets, chains, D, Q, P, S, ALPHA, SEG_UB, BETA, GAMMA, cap=cap, **kw)
-
-
 def _check_edge(ps, scorer, w, label, **policy):
     w.alpha = np.asarray(w.alpha, np.float32)
-    w.beta = np.asarray(w.beta, np.float32)
-    w.gamma = np.asarray(w.gamma, np.float32)
     load_window(scorer, w, **policy)
     dw = DeviceWindow(w)
     got = dw.hits(scorer, w.n_inst)
