@@ -227,6 +227,83 @@ def cpu_baseline(win, budget_s: float):
                        f"{reps} repetitions")
 
 
+def cpu_sequential_baseline(win, budget_s: float):
+    """The oracle's Algorithm 1 per arrival (one thread: each request waits
+    for the one before it) over the window or its leading slice."""
+    import oracle
+    o = oracle.Oracle.from_window(win)
+    n = win.n_req
+    t0 = time.perf_counter()
+    o.window_schedule(win.subset(range(min(n, 256))))
+    one = (time.perf_counter() - t0) / min(n, 256)
+    if one * n > budget_s:
+        n = max(256, int(budget_s / max(one, 1e-9)))
+    o = oracle.Oracle.from_window(win)
+    t0 = time.perf_counter()
+    o.window_schedule(win.subset(range(n)) if n < win.n_req else win)
+    dt = time.perf_counter() - t0
+    return dict(value=n / dt, unit="decisions/s", cores=1, kind="oracle",
+                sample=(f"first {n} of {win.n_req} requests, per arrival, once" if n < win.n_req
+                        else f"whole window ({win.n_req} requests), per arrival, once"))
+
+
+def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
+    """Algorithm 1 per arrival (ps_schedule_window_dev) on the same window and
+    starting state, and the herding of the snapshot placements: the same
+    placements replayed in arrival order (ps_replay_window_dev)."""
+    import numpy as np
+    import torch
+    import paper_2609_33224_amd as ps
+
+    def reload():
+        sc.load(win.n_inst, win.cap, win.blk_off, win.blk, win.D, win.Q, win.P, win.S, model)
+        torch.cuda.synchronize()
+
+    n = win.n_req
+    d_out = torch.empty(n * 20, dtype=torch.uint8, device="cuda")
+    times = []
+    for k in range(reps + 1):  # the first call is a warm-up
+        reload()
+        t0 = time.perf_counter()
+        sc.schedule_dev(d_pool, len(win.pool), d_reqs, n, d_out, None, stream)
+        dt = time.perf_counter() - t0
+        if k:
+            times.append(dt)
+    seq = ps.results_from_device(d_out)
+    reload()
+    d_inst = torch.from_numpy(np.ascontiguousarray(snap["instance"], np.int32)).to("cuda")
+    t0 = time.perf_counter()
+    sc.replay_dev(d_pool, len(win.pool), d_reqs, n, d_inst, d_out, stream)
+    replay_s = time.perf_counter() - t0
+    rep = ps.results_from_device(d_out)
+    tau = float(np.float32(win.policy["tpot_slo"]))
+    fb = ps.PS_R_FALLBACK
+    ok_snap = (snap["instance"] >= 0) & ((snap["flags"] & fb) == 0)
+    ok_seq = (seq["instance"] >= 0) & ((seq["flags"] & fb) == 0)
+    per_snap = np.bincount(snap["instance"][snap["instance"] >= 0], minlength=win.n_inst)
+    per_seq = np.bincount(seq["instance"][seq["instance"] >= 0], minlength=win.n_inst)
+    ms = float(np.mean(times)) * 1e3
+    return {
+        "entry": "ps_schedule_window_dev: Algorithm 1 per arrival (hits pass, one-workgroup "
+                 "scheduler, rebuild of the derived data)",
+        "ms_per_window": ms, "decisions_per_s": n / (ms * 1e-3),
+        "us_per_decision": ms * 1e3 / n, "reps": reps,
+        "bound": "latency (each decision waits for the commit before it)",
+        "placed": int((seq["instance"] >= 0).sum()),
+        "fallback": int(((seq["flags"] & fb) != 0).sum()),
+        "tpot_at_or_above_target_non_fallback": int((seq["tpot"][ok_seq] >= tau).sum()),
+        "herding": {
+            "snapshot_choice_differs_frac": float(np.mean(seq["instance"] != snap["instance"])),
+            "snapshot_non_fallback_placed": int(ok_snap.sum()),
+            "snapshot_tpot_at_or_above_target_at_arrival": int((rep["tpot"][ok_snap] >= tau).sum()),
+            "snapshot_ttft_miss_at_arrival": int(((rep["flags"] & ps.PS_R_TTFT_MISS) != 0).sum()),
+            "max_requests_per_instance": {"snapshot": int(per_snap.max()),
+                                          "per_arrival": int(per_seq.max())},
+            "replay_ms": replay_s * 1e3,
+        },
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -236,6 +313,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--sequential-reps", type=int, default=3,
+                    help="timed calls of the per-arrival scheduler (0: skip that block)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (a plain copy "
                          "kernel of known size, to scale the HBM byte counters)")
@@ -353,10 +432,16 @@ def main():
         "placed": int((res["instance"] >= 0).sum()),
         "fallback": int(((res["flags"] & ps.PS_R_FALLBACK) != 0).sum()),
     }
+    if args.sequential_reps > 0:
+        print("bench: per-arrival scheduling", file=sys.stderr, flush=True)
+        out["sequential"] = sequential_block(sc, win, m, d_pool, d_reqs, res,
+                                             args.sequential_reps, stream)
     sc.close()
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(win, args.cpu_budget)
+        if args.sequential_reps > 0:
+            out["cpu_baseline"]["sequential"] = cpu_sequential_baseline(win, args.cpu_budget)
     print(json.dumps(out), flush=True)
 
 

@@ -707,7 +707,7 @@ static ps_status run_sequential(ps_ctx* c, const uint64_t* d_pool, int64_t pool_
     c->seq_hits_cap = need;
   }
   HIP_TRY(c, hipMemsetAsync(c->d_counter, 0, sizeof(unsigned long long), s));
-  const int threads = (int)std::min<int64_t>(kSeqMaxThreads, ((int64_t)ni + 63) / 64 * 64);
+  const int threads = kSeqMaxThreads;  // every step of a request uses the whole workgroup
   for (int32_t r0 = 0; r0 < n_req; r0 += chunk) {
     const int32_t r1 = std::min(n_req, r0 + chunk);
     ScoreArgs pa{};

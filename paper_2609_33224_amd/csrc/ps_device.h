@@ -138,9 +138,11 @@ struct CommitArgs {
 // every instance at the launch's starting state, (r1 - r0) x n_inst; the
 // kernel extends them in place where a block committed by an earlier
 // request of the launch continues the prefix.
-constexpr int kSeqMaxThreads = 512;  // workgroup of the per-arrival scheduler
+constexpr int kSeqMaxThreads = 256;  // workgroup of the per-arrival scheduler (one wave per SIMD)
 constexpr int kSeqWaves = kSeqMaxThreads / 64;
-constexpr uint32_t kExtMax = 128;    // hit extensions walked by whole waves per request
+constexpr int kSeqStage = 4096;      // chain blocks staged in LDS per request (32 KiB)
+constexpr int kSeqU = 6;             // positions per thread in one sweep or insert step
+constexpr uint32_t kExtMax = 128;    // hit extensions swept by the workgroup per request
 
 struct SeqArgs {
   Tables t;

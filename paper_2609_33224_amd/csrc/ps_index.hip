@@ -15,18 +15,35 @@ using namespace ps;
 
 namespace {
 
-// Pairs of instance i go to [base[i], base[i] + count[i]) in slot order.
+// Pairs of instance i go to [base[i], base[i] + count[i]) (any order inside
+// the range).  A wave whose slots all belong to one instance claims its
+// positions with one atomic.
 __global__ void extract_kernel(Tables t, int32_t n_inst, const int64_t* base, uint64_t* pk,
                                uint16_t* pv, unsigned int* cursor) {
   const int64_t total = (int64_t)n_inst * t.slots;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int lane = threadIdx.x & 63;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += stride) {
     const uint64_t key = t.keys[k];
-    if (key == 0) continue;
     const int32_t i = (int32_t)(k / t.slots);
-    const int64_t at = base[i] + atomicAdd(&cursor[i], 1u);
-    pk[at] = key;
-    pv[at] = (uint16_t)i;
+    const uint64_t act = __ballot(1);
+    const int leader = __builtin_ctzll(act);
+    const int32_t i0 = __shfl(i, leader);
+    int64_t at = -1;
+    if (__ballot(i == i0) == act) {
+      const uint64_t wm = __ballot(key != 0);
+      uint32_t b0 = 0;
+      if (lane == leader && wm) b0 = atomicAdd(&cursor[i0], (unsigned int)__popcll(wm));
+      b0 = (uint32_t)__shfl((int)b0, leader);
+      if (key != 0) at = base[i0] + b0 + __popcll(wm & lt_mask);
+    } else if (key != 0) {
+      at = base[i] + atomicAdd(&cursor[i], 1u);
+    }
+    if (at >= 0) {
+      pk[at] = key;
+      pv[at] = (uint16_t)i;
+    }
   }
 }
 
