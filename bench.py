@@ -31,7 +31,6 @@ METRIC = ("request×instance candidate evals/sec + decisions/sec; "
 HBM_PEAK_GBS = 8000.0
 BUCKET_BYTES = 64
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_33224_amd", "csrc", "ps_kernels.hip")
 
 WORKLOAD_NAMES = {
     "c1": "16 instances x 1,024 requests, TPOT 50 ms",
@@ -44,10 +43,12 @@ WORKLOAD_NAMES = {
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        h = hashlib.sha256(f.read())
-    with open(os.path.join(ROOT, "paper_2609_33224_amd", "csrc", "ps_device.h"), "rb") as f:
-        h.update(f.read())
+    """Hash of the window kernel's sources (kernels, shared device helpers,
+    device layout); the committed counter summary applies only to it."""
+    h = hashlib.sha256()
+    for name in ("ps_kernels.hip", "ps_common.h", "ps_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_33224_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
@@ -260,6 +261,7 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
         torch.cuda.synchronize()
 
     n = win.n_req
+    snap_all = snap
     d_out = torch.empty(n * 20, dtype=torch.uint8, device="cuda")
     times = []
     for k in range(reps + 1):  # the first call is a warm-up
@@ -270,17 +272,28 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
         if k:
             times.append(dt)
     seq = ps.results_from_device(d_out)
+    # The replay stops before the first placement that would take an
+    # instance's queue past its 12-bit limit (snapshot herding can).
+    n_rep, q = n, win.Q.astype(np.int64).copy()
+    for k, i in enumerate(snap["instance"]):
+        if i >= 0:
+            q[i] += 1
+            if q[i] > 4095:
+                n_rep = k
+                break
     reload()
-    d_inst = torch.from_numpy(np.ascontiguousarray(snap["instance"], np.int32)).to("cuda")
+    d_inst = torch.from_numpy(np.ascontiguousarray(snap["instance"][:n_rep], np.int32)).to("cuda")
     t0 = time.perf_counter()
-    sc.replay_dev(d_pool, len(win.pool), d_reqs, n, d_inst, d_out, stream)
+    if n_rep:
+        sc.replay_dev(d_pool, len(win.pool), d_reqs, n_rep, d_inst, d_out, stream)
     replay_s = time.perf_counter() - t0
-    rep = ps.results_from_device(d_out)
+    rep = ps.results_from_device(d_out)[:n_rep]
+    snap = snap[:n_rep]
     tau = float(np.float32(win.policy["tpot_slo"]))
     fb = ps.PS_R_FALLBACK
     ok_snap = (snap["instance"] >= 0) & ((snap["flags"] & fb) == 0)
     ok_seq = (seq["instance"] >= 0) & ((seq["flags"] & fb) == 0)
-    per_snap = np.bincount(snap["instance"][snap["instance"] >= 0], minlength=win.n_inst)
+    per_snap = np.bincount(snap_all["instance"][snap_all["instance"] >= 0], minlength=win.n_inst)
     per_seq = np.bincount(seq["instance"][seq["instance"] >= 0], minlength=win.n_inst)
     ms = float(np.mean(times)) * 1e3
     return {
@@ -293,7 +306,8 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
         "fallback": int(((seq["flags"] & fb) != 0).sum()),
         "tpot_at_or_above_target_non_fallback": int((seq["tpot"][ok_seq] >= tau).sum()),
         "herding": {
-            "snapshot_choice_differs_frac": float(np.mean(seq["instance"] != snap["instance"])),
+            "snapshot_choice_differs_frac": float(np.mean(seq["instance"] != snap_all["instance"])),
+            "replayed_requests": int(n_rep),
             "snapshot_non_fallback_placed": int(ok_snap.sum()),
             "snapshot_tpot_at_or_above_target_at_arrival": int((rep["tpot"][ok_snap] >= tau).sum()),
             "snapshot_ttft_miss_at_arrival": int(((rep["flags"] & ps.PS_R_TTFT_MISS) != 0).sum()),

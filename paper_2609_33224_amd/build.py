@@ -17,7 +17,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libpackserve.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("ps_kernels.hip", "ps_index.hip", "ps_api.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("ps_kernels.hip", "ps_sequential.hip", "ps_index.hip",
+                                                   "ps_api.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

@@ -141,8 +141,9 @@ struct CommitArgs {
 constexpr int kSeqMaxThreads = 256;  // workgroup of the per-arrival scheduler (one wave per SIMD)
 constexpr int kSeqWaves = kSeqMaxThreads / 64;
 constexpr int kSeqStage = 4096;      // chain blocks staged in LDS per request (32 KiB)
-constexpr int kSeqU = 6;             // positions per thread in one sweep or insert step
+constexpr int kSeqU = 4;             // positions per thread in one sweep or insert step
 constexpr uint32_t kExtMax = 128;    // hit extensions swept by the workgroup per request
+constexpr int kSeqB = 2;             // instances per thread whose loads are issued together
 
 struct SeqArgs {
   Tables t;
