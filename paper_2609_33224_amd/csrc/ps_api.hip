@@ -40,6 +40,7 @@ struct ps_ctx {
   int64_t* d_room = nullptr;
   int64_t* d_room_sorted = nullptr;
   uint32_t* d_order0 = nullptr;
+  InstState* d_inst_key = nullptr;  // states in d_order0's order
   GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
@@ -212,6 +213,7 @@ void free_snapshot(ps_ctx* c) {
   dfree(c->d_room);
   dfree(c->d_room_sorted);
   dfree(c->d_order0);
+  dfree(c->d_inst_key);
   dfree(c->d_scratch);
   ps_free_index(&c->x);
   c->loaded = false;
@@ -234,6 +236,13 @@ int32_t segment_of_dev(const DevModel& m, int32_t B) {
 
 // Instance ids in the order of the packing key of a candidate with no cached
 // prefix: most decoding first, then fewest queued, then lowest id.
+std::vector<InstState> states_in_order(const std::vector<InstState>& hs,
+                                       const std::vector<uint32_t>& order) {
+  std::vector<InstState> v(order.size());
+  for (size_t k = 0; k < order.size(); ++k) v[k] = hs[order[k]];
+  return v;
+}
+
 std::vector<uint32_t> key_order(const std::vector<InstState>& hs) {
   std::vector<uint32_t> o(hs.size());
   for (size_t i = 0; i < o.size(); ++i) o[i] = (uint32_t)i;
@@ -261,6 +270,8 @@ ps_status refresh_derived(ps_ctx* c) {
   HIP_TRY(c, hipMemcpy(c->d_room, room.data(), room.size() * sizeof(int64_t), hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+  const std::vector<InstState> ik = states_in_order(c->h_state, o0);
+  HIP_TRY(c, hipMemcpy(c->d_inst_key, ik.data(), ik.size() * sizeof(InstState), hipMemcpyHostToDevice));
   return PS_OK;
 }
 
@@ -387,6 +398,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     dfree(fresh.d_room);
     dfree(fresh.d_room_sorted);
     dfree(fresh.d_order0);
+    dfree(fresh.d_inst_key);
     dfree(fresh.d_scratch);
     ps_free_index(&fresh.x);
     dfree(d_off);
@@ -405,6 +417,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room_sorted, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_order0, (size_t)n * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst_key, (size_t)n * sizeof(InstState));
   if (e == hipSuccess && rows)
     e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint16_t));
   if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
@@ -429,6 +442,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   std::vector<int64_t> hroom_sorted = hroom;
   std::sort(hroom_sorted.begin(), hroom_sorted.end());
   const std::vector<uint32_t> horder0 = key_order(hs);
+  const std::vector<InstState> hinst_key = states_in_order(hs, horder0);
   hipStream_t sm = c->stream;
   e = hipMemsetAsync(fresh.t.keys, 0, tab_bytes, sm);
   if (e == hipSuccess) e = hipMemsetAsync(fresh.t.count, 0, (size_t)n * sizeof(uint32_t), sm);
@@ -446,6 +460,9 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
                        hipMemcpyHostToDevice, sm);
   if (e == hipSuccess)
     e = hipMemcpyAsync(fresh.d_order0, horder0.data(), horder0.size() * sizeof(uint32_t),
+                       hipMemcpyHostToDevice, sm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(fresh.d_inst_key, hinst_key.data(), hinst_key.size() * sizeof(InstState),
                        hipMemcpyHostToDevice, sm);
   BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter, d_won, d_slot, d_rank};
   if (e == hipSuccess) e = ps_launch_build(ba, sm);
@@ -483,6 +500,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->d_room = fresh.d_room;
   c->d_room_sorted = fresh.d_room_sorted;
   c->d_order0 = fresh.d_order0;
+  c->d_inst_key = fresh.d_inst_key;
   c->x = fresh.x;
   c->d_scratch = fresh.d_scratch;
   c->scratch_rows = rows;
@@ -506,6 +524,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.d_room = nullptr;
   fresh.d_room_sorted = nullptr;
   fresh.d_order0 = nullptr;
+  fresh.d_inst_key = nullptr;
   fresh.x = GIndex{nullptr, nullptr, nullptr, 0, 0, 64};
   fresh.d_scratch = nullptr;
   return PS_OK;
@@ -519,6 +538,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.x = c->x;
   a.room_sorted = c->d_room_sorted;
   a.order0 = c->d_order0;
+  a.inst_key = c->d_inst_key;
   a.inst = c->d_inst;
   a.room = c->d_room;
   a.model = c->d_model;
@@ -607,6 +627,8 @@ static ps_status after_commit(ps_ctx* c, hipStream_t s, int64_t* n_dropped) {
   HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
   const std::vector<uint32_t> o0 = key_order(c->h_state);
   HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+  const std::vector<InstState> ik = states_in_order(c->h_state, o0);
+  HIP_TRY(c, hipMemcpy(c->d_inst_key, ik.data(), ik.size() * sizeof(InstState), hipMemcpyHostToDevice));
   HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
   HIP_TRY(c, hipStreamSynchronize(s));
   if (n_dropped) *n_dropped = (int64_t)dropped;

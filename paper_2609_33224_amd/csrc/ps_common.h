@@ -292,6 +292,35 @@ __device__ uint32_t deep_walk(const Tables& t, uint32_t inst, const ChainRef& c,
   return (uint32_t)ell;
 }
 
+// One compare step of a row walk: chain positions q.. against row entries
+// k.., U x 64 of them (U per lane, coalesced).  Returns the first position
+// whose block differs from the row entry (or lies past the row's end), or
+// -1 when all of them match.
+template <bool STAGED, int U>
+__device__ __forceinline__ int32_t run_compare(const ChainRef& c, const uint64_t* stage,
+                                               const uint64_t* row, int64_t rlen, int32_t q,
+                                               int64_t k, int lane) {
+  const int32_t ell = c.len;
+  bool mism[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int32_t j = q + 64 * u + lane;
+    const int64_t kk = k + 64 * u + lane;
+    const bool valid = j < ell;
+    uint64_t cj = 0ull, rk = 0ull;
+    if (valid) cj = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+    if (valid && kk < rlen) rk = row[kk];
+    mism[u] = valid && (kk >= rlen || cj != rk);
+  }
+  int32_t next = -1;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint64_t mm = __ballot(mism[u]);
+    if (next < 0 && mm) next = q + 64 * u + __builtin_ctzll(mm);
+  }
+  return next;
+}
+
 // Walk of one instance along its row: one octet probe finds the block at
 // `pos` and its row position; the chain blocks after it are compared with
 // the row entries after it, 256 per step (4 per lane, coalesced), and the
@@ -313,11 +342,14 @@ __device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, con
     int64_t rp = -1;
     bool decided = false;
     for (uint32_t step = 0; step <= t.bmask && !decided; ++step) {
+      // each slot's row position is read with the slot (no second trip)
       const uint64_t val = g == 0 ? tab[(size_t)b * kSlotsPerBucket + s] : 0ull;
+      const uint32_t rpv =
+          g == 0 ? t.rowpos[(size_t)inst * t.slots + (size_t)b * kSlotsPerBucket + s] : 0u;
       const uint64_t fm = __ballot(g == 0 && val == key) & 0xFFull;
       const uint64_t em = __ballot(g == 0 && val == 0ull) & 0xFFull;
       if (fm) {
-        rp = t.rowpos[(size_t)inst * t.slots + (size_t)b * kSlotsPerBucket + __builtin_ctzll(fm)];
+        rp = (uint32_t)__shfl((int)rpv, __builtin_ctzll(fm));
         decided = true;
       } else if (em) {
         decided = true;
@@ -329,29 +361,16 @@ __device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, con
     const int32_t start = pos + 1;
     int32_t q = start;
     int64_t k = rp + 1;
-    int32_t next = -1;
+    // The first step compares 4 positions per lane; a run that goes on is
+    // likely long (a session prefix), so later steps compare kWalkU per lane.
+    int32_t next = run_compare<STAGED, 4>(c, stage, row, rlen, q, k, lane);
+    q += 256;
+    k += 256;
     while (next < 0) {
-      bool mism[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int32_t j = q + 64 * u + lane;
-        const int64_t kk = k + 64 * u + lane;
-        const bool valid = j < ell;
-        uint64_t cj = 0ull, rk = 0ull;
-        if (valid) cj = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
-        if (valid && kk < rlen) rk = row[kk];
-        mism[u] = valid && (kk >= rlen || cj != rk);
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint64_t mm = __ballot(mism[u]);
-        if (next < 0 && mm) next = q + 64 * u + __builtin_ctzll(mm);
-      }
-      if (next < 0) {
-        q += 256;
-        k += 256;
-        if (q >= ell) return (uint32_t)ell;
-      }
+      if (q >= ell) return (uint32_t)ell;
+      next = run_compare<STAGED, kWalkU>(c, stage, row, rlen, q, k, lane);
+      q += 64 * kWalkU;
+      k += 64 * kWalkU;
     }
     if (next - start < 8) return deep_walk<STAGED>(t, inst, c, stage, next, g, s);
     pos = next;

@@ -13,7 +13,8 @@ namespace ps {
 constexpr int kStage = 256;            // chain blocks staged in LDS per request (2 KiB)
 constexpr int kSlotsPerBucket = 8;     // 8 x 64-bit keys = one 64-byte bucket
 constexpr int kBreadthRounds = 8;      // octet loads per lane in flight: 64 instances per step
-constexpr int kDeepRounds = 8;         // octet loads per lane in flight: 64 positions per step
+constexpr int kDeepRounds = 2;         // octet loads per lane in flight: 16 positions per step
+constexpr int kWalkU = 4;             // row-walk positions per lane after the first step
 // Per-candidate hit slots (u16 in LDS): exact hits up to kHitMax, then two
 // markers.
 constexpr uint32_t kHitMax = 0xFFFDu;
@@ -104,6 +105,7 @@ struct ScoreArgs {
   GIndex x;
   const int64_t* room_sorted;  // rooms ascending (eligible count = n - lower_bound(L))
   const uint32_t* order0;      // instance ids by (decoding desc, queued asc, id asc)
+  const InstState* inst_key;   // the instances' states in that order
   const InstState* inst;
   const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
   const DevModel* model;

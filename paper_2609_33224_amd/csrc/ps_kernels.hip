@@ -83,6 +83,7 @@ __global__ void row_kernel(BuildArgs a) {
 // on all instances (octets of lanes over instances, 64 per step), then a
 // deep walk of each instance that holds it.
 __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
+  static_assert(kBreadthRounds * 8 == 64, "one breadth step covers the 64 instances of a lane mask");
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
   const int lane = threadIdx.x;
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
 // candidate bitmap (instances holding the first block) | 64 candidate ids |
 // u16 hit slots (or device scratch for large pools).
 template <bool HITS_IN_LDS>
-__global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
   const int32_t nw = (n_inst + 63) >> 6;
@@ -170,12 +171,22 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
     const int64_t L = (int64_t)ell * m.bs;
     const float Lf = (float)L;
     const int32_t nst = ell < kStage ? ell : kStage;
-    __syncthreads();
-    for (int32_t j = lane; j < nst; j += 64) stage[j] = chain_global(c, j);
-    __syncthreads();
-
+    // The chain head's loads and the room search's are in flight together.
+    uint64_t sv[kStage / 64];
+#pragma unroll
+    for (int u = 0; u < kStage / 64; ++u) {
+      const int32_t j = lane + 64 * u;
+      sv[u] = j < nst ? chain_global(c, j) : 0ull;
+    }
     // |A|: capacity-eligible instances are those with room >= L.
     const uint32_t nA = (uint32_t)(n_inst - wave_lower_bound(a.room_sorted, n_inst, L, lane));
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kStage / 64; ++u) {
+      const int32_t j = lane + 64 * u;
+      if (j < nst) stage[j] = sv[u];
+    }
+    __syncthreads();
 
     // (1) Holders of the first block among the eligible instances.
     uint32_t nCand = 0;
@@ -404,10 +415,11 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
             const int32_t k = base + lane;
             bool ok = false;
             uint32_t i = 0;
+            InstState st{};
             if (k < n_inst) {
               i = a.order0[k];
-              if (a.room[i] >= L && !test_bit(bmC, i)) {
-                const InstState st = a.inst[i];
+              st = a.inst_key[k];  // contiguous, loaded with the id
+              if (eligible(m, st.A1, st.S, L) && !test_bit(bmC, i)) {
                 const Lat lt = latency(m, st, Lf, 0.0f, L);
                 ok = ((m.flags & PS_F_NO_TPOT_FILTER) || lt.tpot < m.tau) &&
                      (!(m.flags & PS_F_TTFT_ADMIT) || lt.ttft <= slo);
@@ -416,7 +428,6 @@ __global__ __launch_bounds__(64) void score_kernel(ScoreArgs a) {
             const uint64_t okm = __ballot(ok);
             if (okm) {
               if (lane == __builtin_ctzll(okm)) {
-                const InstState st = a.inst[i];
                 const uint64_t kt = select_key(m.sel, st, 0u, i, 0ull);
                 acc.keyT = kt < acc.keyT ? kt : acc.keyT;
               }
