@@ -78,7 +78,73 @@ def probe_bytes(win, hits):
     return n_probes * BUCKET_BYTES + int(np.minimum(ell, 256).sum()) * 8, n_probes
 
 
-def score_bytes(win, r0, hits):
+GROUP_MIN, GROUP_HOLD = 8, 16  # shortest grouped segment; holders a group record keeps
+
+
+def group_info(win):
+    """Prefix groups as the kernels form them: requests with a shared
+    segment of at least GROUP_MIN blocks and equal pre_off; per group the
+    longest member segment and the first request holding it."""
+    import numpy as np
+    R = win.n_req
+    grouped = win.pre_len >= GROUP_MIN
+    idx = np.nonzero(grouped)[0]
+    order = idx[np.lexsort((idx, -win.pre_len[idx].astype(np.int64), win.pre_off[idx]))]
+    first = np.ones(len(order), bool)
+    first[1:] = win.pre_off[order[1:]] != win.pre_off[order[:-1]]
+    gid_sorted = np.cumsum(first) - 1
+    gid = np.full(R, -1, np.int64)
+    gid[order] = gid_sorted
+    rep = order[first]
+    return gid, rep, win.pre_len[rep].astype(np.int64)
+
+
+def group_segment_hits(sc, win, d_pool, rep, plen, chunk_pairs=1 << 25):
+    """Hit of each group's longest segment on every instance (the walk the
+    group pass makes), from the exhaustive hits of the representatives."""
+    import numpy as np
+    import torch
+    import paper_2609_33224_amd as ps
+    G, N = len(rep), win.n_inst
+    H = np.zeros((G, N), np.int64)
+    if G == 0:
+        return H
+    reqs = ps.pack_reqs(win.pre_off[rep], win.pre_len[rep], win.tail_off[rep], win.tail_len[rep])
+    chunk = max(1, min(G, chunk_pairs // N))
+    d_hits = torch.empty(chunk * N, dtype=torch.int32, device="cuda")
+    for g0 in range(0, G, chunk):
+        n = min(chunk, G - g0)
+        sc.hits_dev(d_pool, len(win.pool), ps.to_device_bytes(reqs[g0:g0 + n]), n, d_hits)
+        torch.cuda.synchronize()
+        h = d_hits[: n * N].cpu().numpy().view(np.uint32).reshape(n, N).astype(np.int64)
+        H[g0:g0 + n] = np.minimum(h, plen[g0:g0 + n, None])
+    return H
+
+
+def group_pass_bytes(win, gid, rep, plen, H):
+    """Algorithmic bytes of the prefix-group pass.  Claim: descriptor, slot
+    read, the claiming compare-and-swap, the length maximum and the slot
+    entry per request.  Walk: slot entry per request; per group its
+    segment head staged (<= 256 hashes), one index bucket, the holder ids,
+    per holder (when at most GROUP_HOLD) a probe of the first block with its
+    row position, 16 bytes per compared position, a final probe where the
+    segment leaves the cache, and the record."""
+    import numpy as np
+    R = win.n_req
+    g = gid >= 0
+    by = 28 * R + int(g.sum()) * (8 + 16) + len(rep) * 16
+    by += 4 * R
+    cnt0 = (H >= 1).sum(1)
+    by += int((16 + 8 * np.minimum(plen, 256) + 128 + 2 * cnt0).sum())
+    ok = cnt0 <= GROUP_HOLD
+    hc = np.minimum(H, (plen - 1)[:, None])
+    walk = np.where(H >= 1, 68 + 16 * hc + 64 * (H < plen[:, None]), 0)
+    walk = np.where((plen > 1)[:, None], walk, np.where(H >= 1, 68, 0))
+    by += int(walk[ok].sum()) + int((8 + 8 * cnt0[ok]).sum()) + int((~ok).sum()) * 8
+    return by
+
+
+def score_bytes(win, r0, hits, grp=None):
     """Algorithmic bytes the scoring kernel moves for requests r0 .. r0 +
     len(hits) (the path without set sizes), from its data movement per
     request: descriptor, result and staged chain head; the 64-way search of
@@ -90,7 +156,12 @@ def score_bytes(win, r0, hits):
     index bucket plus the holder data per walked position; 32 bytes of state
     per member of C; the key-ordered scan of the hit-0 class (4-byte order
     entry + 8-byte room per scanned instance, 32 bytes of state per eligible
-    one)."""
+    one).  With prefix groups (`grp`: per request its group's segment hits
+    Hg, whether the group record holds a result, and whether the request is
+    grouped at all), a request with a group result reads the record (meta +
+    16 holders) and the holders' rooms instead of staging, index and walks,
+    and walks only where the group's segment is cached up to its own
+    segment length (from there, on its tail)."""
     import numpy as np
     R, N = hits.shape
     pol = win.policy
@@ -123,7 +194,19 @@ def score_bytes(win, r0, hits):
     hc = np.minimum(h, (ell - 1)[:, None])
     walk = np.where(cand, 68 + 16 * hc + 64 * (h < ell[:, None]), 0).sum(1)
     by += np.where(act & few & (ell > 1), walk, 0)
-    for r in np.nonzero(act & ~few & (ell > 1))[0]:
+    has = np.zeros(R, bool)
+    if grp is not None:
+        has = grp["has"]
+        p = win.pre_len[sl].astype(np.int64)
+        Hg = grp["Hg"]
+        gby = 48 + 136 + 512 * levels + np.where(act, 8 * cnt0, 0)
+        resume = cand & (Hg >= p[:, None]) & (p < ell)[:, None]
+        rb = np.where(h > p[:, None],
+                      68 + 16 * (np.minimum(h, (ell - 1)[:, None]) - p[:, None]) +
+                      64 * (h < ell[:, None]), 68)
+        gby += np.where(resume, rb, 0).sum(1)
+        by = np.where(has, gby, by + 4 + np.where(grp["grouped"], 136, 0))
+    for r in np.nonzero(act & ~few & (ell > 1) & ~has)[0]:
         hr = np.sort(h[r][cand[r]])[::-1]
         P = int(min(ell[r] - 1, hr[1]))
         cnts = (h[r][None, :] > np.arange(1, P + 1)[:, None]).sum(1)
@@ -163,12 +246,17 @@ def score_bytes(win, r0, hits):
     return int(by.sum())
 
 
-def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 27):
-    """Both byte counts over the whole window, from the exhaustive per-pair
-    hits exported chunk by chunk (untimed)."""
+def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 25):
+    """The byte counts of the scoring kernel, the prefix-group pass and the
+    exhaustive probe kernel over the whole window, from the exhaustive
+    per-pair hits exported chunk by chunk (untimed)."""
     import numpy as np
     import torch
     import paper_2609_33224_amd as ps
+    gid, rep, plen = group_info(win)
+    H = group_segment_hits(sc, win, d_pool, rep, plen)
+    g_has = (H >= 1).sum(1) <= GROUP_HOLD if len(rep) else np.zeros(0, bool)
+    gb = group_pass_bytes(win, gid, rep, plen, H)
     chunk = max(1, min(win.n_req, chunk_pairs // win.n_inst))
     reqs = ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
     d_hits = torch.empty(chunk * win.n_inst, dtype=torch.int32, device="cuda")
@@ -182,9 +270,12 @@ def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 27):
         b, p_ = probe_bytes(win.subset(range(r0, r0 + n)), hits)
         pb += b
         npr += p_
-        sb += score_bytes(win, r0, hits)
-    sb += win.n_inst * 0
-    return sb, pb, npr
+        gc = gid[r0:r0 + n]
+        grouped = gc >= 0
+        has = grouped & g_has[np.maximum(gc, 0)] if len(rep) else grouped
+        Hg = H[np.maximum(gc, 0)] if len(rep) else np.zeros(hits.shape, np.int64)
+        sb += score_bytes(win, r0, hits, dict(has=has, grouped=grouped, Hg=Hg))
+    return sb, gb, pb, npr
 
 
 def traffic_for(workload: str, src_hash: str):
@@ -370,7 +461,7 @@ def main():
 
     # untimed: byte counts from the per-pair hits, and the end-to-end host call
     print("bench: counting algorithmic bytes", file=sys.stderr, flush=True)
-    alg_bytes, probe_alg_bytes, n_probes = algorithmic_bytes(sc, win, d_pool, d_reqs)
+    alg_bytes, group_bytes, probe_alg_bytes, n_probes = algorithmic_bytes(sc, win, d_pool, d_reqs)
     t0 = time.perf_counter()
     sc.score(win.pool, reqs)
     host_call_s = time.perf_counter() - t0
@@ -403,10 +494,17 @@ def main():
         b.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    step_ms = [a.elapsed_time(b) for a, b in ev]
     ms_per_step = wall * 1e3 / args.steps
-    kern_avg = float(np.mean(kern_ms))
+    step_avg = float(np.mean(step_ms))
     res = ps.results_from_device(d_out)
+    # The same steps again with the library's events around its launches:
+    # the prefix-group pass and the scoring kernel, each on the launch stream.
+    sc.set_timing(True)
+    for _ in range(args.steps):
+        sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
+    n_timed, group_ms, kern_avg = sc.read_timing()
+    sc.set_timing(False)
 
     evals = win.n_req * win.n_inst
     src_hash = kernel_source_hash()
@@ -428,12 +526,19 @@ def main():
         "config": {"workload": f"{args.workload}: {WORKLOAD_NAMES[args.workload]}",
                    "n_inst": win.n_inst, "n_req": win.n_req, "seed": args.seed},
         "decisions_per_s": win.n_req / (ms_per_step * 1e-3),
+        "step_ms_events": step_avg,
+        "kernel": "score_kernel (prefix hits from the group records, latency model, filters, keys)",
         "kernel_ms_avg": kern_avg,
-        "kernel_ms_min": float(np.min(kern_ms)),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
         "algorithmic_bytes_per_launch": alg_bytes,
+        "group_pass": {"kernels": "group_claim_kernel + group_kernel (walk of each shared "
+                                  "segment once per window)",
+                       "ms_avg": group_ms, "algorithmic_bytes": group_bytes,
+                       "achieved_GBs": group_bytes / (group_ms * 1e-3) / 1e9 if group_ms > 0 else None,
+                       "groups": int(len(np.unique(win.pre_off[win.pre_len >= GROUP_MIN]))),
+                       "timed_calls": n_timed},
         "probe_kernel": {"kernel": "ps_probe_hits_dev (every request x instance probed)",
                          "ms_per_window": probe_ms, "probes": n_probes,
                          "algorithmic_bytes": probe_alg_bytes,

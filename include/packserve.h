@@ -194,11 +194,28 @@ ps_status ps_score_window(ps_ctx* ctx, const uint64_t* pool, int64_t pool_len,
  * NULL, |A|, |C|, |T| per request into d_sizes[3 * n_req]), asynchronously
  * on `hip_stream`.  Descriptors are checked by the kernel: a malformed one
  * yields instance -1 with PS_R_INVALID.  A zero hash in a chain never
- * matches (it ends the prefix walk).
+ * matches (it ends the prefix walk).  Requests with the same pre_off share
+ * one walk of that segment per window (identical results); the context
+ * keeps a group table for that, grown (hipMalloc) when a window has more
+ * requests than any before it: under 620 bytes per request, none for
+ * windows above 4,194,304 requests, which are scored without it.  Calls
+ * that overlap on one context (two streams) race on that table.
  */
 ps_status ps_score_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_len,
                               const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
                               uint32_t* d_sizes, void* hip_stream);
+
+/*
+ * Measurement: with on != 0, the next ps_score_window(_dev) calls (up to
+ * 4,096 of them) record HIP events on their stream around their two parts:
+ * the prefix-group pass (two launches) and the scoring kernel.
+ * ps_read_timing waits for those calls and returns their number and the
+ * mean duration of each part in milliseconds, then starts a new count.
+ * PS_E_STATE if no call was recorded.  Switching it on or off resets the
+ * count.  The events are kept until ps_destroy.
+ */
+ps_status ps_set_timing(ps_ctx* ctx, int32_t on);
+ps_status ps_read_timing(ps_ctx* ctx, int32_t* n_calls, float* ms_group, float* ms_score);
 
 /*
  * Diagnostic: the longest cached prefix (blocks) of every request on every

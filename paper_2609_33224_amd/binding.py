@@ -110,6 +110,9 @@ def load_library() -> ctypes.CDLL:
         "ps_feedback_decode": ([vp, vp, vp, vp, i32], i32),
         "ps_feedback_output": ([vp, vp, i32], i32),
         "ps_read_model": ([vp, vp, vp, vp], i32),
+        "ps_set_timing": ([vp, i32], i32),
+        "ps_read_timing": ([vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_float),
+                            ctypes.POINTER(ctypes.c_float)], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -340,6 +343,17 @@ class Scorer:
 
     def score_dev(self, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes=None, stream=None):
         ps_score_window_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, stream)
+
+    def set_timing(self, on: bool) -> None:
+        _check(self.ctx, load_library().ps_set_timing(self.ctx, 1 if on else 0))
+
+    def read_timing(self) -> tuple:
+        """(calls, mean ms of the prefix-group pass, mean ms of the scoring
+        kernel) over the scoring calls timed since the last read."""
+        n, g, k = ctypes.c_int32(), ctypes.c_float(), ctypes.c_float()
+        _check(self.ctx, load_library().ps_read_timing(self.ctx, ctypes.byref(n), ctypes.byref(g),
+                                                       ctypes.byref(k)))
+        return int(n.value), float(g.value), float(k.value)
 
     def hits_dev(self, d_pool, pool_len, d_reqs, n_req, d_hits, stream=None):
         ps_probe_hits_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_hits, stream)

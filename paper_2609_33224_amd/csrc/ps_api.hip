@@ -24,6 +24,9 @@ thread_local std::string g_create_error;
 // device scratch instead of LDS.
 constexpr int kScratchRowsPerCU = 16;
 
+// Scoring calls whose launches are timed between two reads of the timing.
+constexpr int32_t kTimingCalls = 4096;
+
 }  // namespace
 
 struct ps_ctx {
@@ -62,6 +65,21 @@ struct ps_ctx {
   uint32_t* d_seq_hits = nullptr;
   size_t seq_hits_cap = 0;  // elements
   size_t seq_budget = (size_t)256 << 20;  // bytes of hits per scheduler launch
+  // prefix groups of the scored windows: slot keys (tagged with a window
+  // generation, so a new window needs no clearing), slot records, and each
+  // request's slot
+  unsigned long long* d_gkeys = nullptr;  // keys, then the tagged segment lengths
+  uint2* d_grec = nullptr;
+  uint32_t* d_gslot = nullptr;
+  uint32_t gslots = 0;   // power of two
+  int32_t greq_cap = 0;  // entries of d_gslot
+  uint64_t ggen = 0;
+  // optional per-launch timing of the scoring path: events recorded on the
+  // call's stream before the group pass, between it and the scoring kernel,
+  // and after it, for up to kTimingCalls calls
+  bool timing = false;
+  int32_t n_timed = 0;
+  std::vector<hipEvent_t> ev;  // 3 per call
 };
 
 namespace {
@@ -321,6 +339,10 @@ ps_status ps_destroy(ps_ctx* c) {
   for (int k = 0; k < 3; ++k)
     if (c->d_stage[k]) (void)hipFree(c->d_stage[k]);
   dfree(c->d_seq_hits);
+  dfree(c->d_gkeys);
+  dfree(c->d_grec);
+  dfree(c->d_gslot);
+  for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
   if (c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
   return PS_OK;
@@ -530,6 +552,37 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   return PS_OK;
 }
 
+// Group table for a window of n_req requests (at least two slots per
+// request) and the next window generation.  Grows (and clears) only when a
+// larger window arrives; a wrapped generation clears the keys once.
+static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
+  uint32_t want = 64;
+  while (want < 2u * (uint32_t)n_req) want <<= 1;
+  bool clear = false;
+  if (want > c->gslots) {
+    dfree(c->d_gkeys);
+    dfree(c->d_grec);
+    c->gslots = 0;
+    HIP_TRY(c, hipMalloc((void**)&c->d_gkeys, 2 * (size_t)want * sizeof(unsigned long long)));
+    HIP_TRY(c, hipMalloc((void**)&c->d_grec, (size_t)want * kGroupRec * sizeof(uint2)));
+    c->gslots = want;
+    clear = true;
+  }
+  if (n_req > c->greq_cap) {
+    dfree(c->d_gslot);
+    c->greq_cap = 0;
+    HIP_TRY(c, hipMalloc((void**)&c->d_gslot, (size_t)n_req * sizeof(uint32_t)));
+    c->greq_cap = n_req;
+  }
+  if (++c->ggen > kGroupGenMax) {
+    c->ggen = 1;
+    clear = true;
+  }
+  if (clear)
+    HIP_TRY(c, hipMemsetAsync(c->d_gkeys, 0, 2 * (size_t)c->gslots * sizeof(unsigned long long), s));
+  return PS_OK;
+}
+
 static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
                               const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
                               uint32_t* d_sizes, uint32_t* d_hits, hipStream_t s) {
@@ -551,8 +604,34 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.sizes = d_sizes;
   a.hits_out = d_hits;
   a.scratch = c->d_scratch;
+  a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, 0u, 0ull};
+  const bool probe_all = d_hits != nullptr;
+  if (!probe_all && n_req <= kGroupMaxReq && pool_len < ((int64_t)1 << kGroupGenShift) - 1) {
+    ps_status st = group_buffers(c, n_req, s);
+    if (st != PS_OK) return st;
+    a.grp = GroupTab{c->d_gkeys, c->d_gkeys + c->gslots, c->d_grec, c->d_gslot, c->gslots - 1u,
+                     c->ggen};
+  }
   const int grid = c->hits_in_lds ? n_req : std::min(n_req, c->scratch_rows);
-  HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, grid, d_hits != nullptr, s));
+  hipEvent_t* ev = nullptr;
+  if (c->timing && !probe_all && c->n_timed < kTimingCalls) {
+    if (c->ev.size() < 3 * (size_t)(c->n_timed + 1)) {
+      for (int k = 0; k < 3; ++k) {
+        hipEvent_t e = nullptr;
+        HIP_TRY(c, hipEventCreate(&e));
+        c->ev.push_back(e);
+      }
+    }
+    ev = &c->ev[3 * (size_t)c->n_timed];
+  }
+  if (ev) HIP_TRY(c, hipEventRecord(ev[0], s));
+  if (a.grp.keys) HIP_TRY(c, ps_launch_group(a, s));
+  if (ev) HIP_TRY(c, hipEventRecord(ev[1], s));
+  HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, grid, probe_all, s));
+  if (ev) {
+    HIP_TRY(c, hipEventRecord(ev[2], s));
+    ++c->n_timed;
+  }
   return PS_OK;
 }
 
@@ -568,6 +647,35 @@ ps_status ps_score_window_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   DeviceScope ds(c->device);
   return launch_score(c, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, nullptr,
                       (hipStream_t)hip_stream);
+}
+
+ps_status ps_set_timing(ps_ctx* c, int32_t on) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  c->timing = on != 0;
+  c->n_timed = 0;
+  return PS_OK;
+}
+
+ps_status ps_read_timing(ps_ctx* c, int32_t* n_calls, float* ms_group, float* ms_score) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!n_calls || !ms_group || !ms_score) return fail(c, PS_E_INVAL, "output is NULL");
+  if (c->n_timed == 0) return fail(c, PS_E_STATE, "no timed scoring call to read");
+  DeviceScope ds(c->device);
+  double g = 0.0, k = 0.0;
+  for (int32_t n = 0; n < c->n_timed; ++n) {
+    hipEvent_t* ev = &c->ev[3 * (size_t)n];
+    float a = 0.0f, b = 0.0f;
+    HIP_TRY(c, hipEventSynchronize(ev[2]));
+    HIP_TRY(c, hipEventElapsedTime(&a, ev[0], ev[1]));
+    HIP_TRY(c, hipEventElapsedTime(&b, ev[1], ev[2]));
+    g += a;
+    k += b;
+  }
+  *n_calls = c->n_timed;
+  *ms_group = (float)(g / c->n_timed);
+  *ms_score = (float)(k / c->n_timed);
+  c->n_timed = 0;
+  return PS_OK;
 }
 
 ps_status ps_probe_hits_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,

@@ -100,9 +100,45 @@ struct GIndex {
   uint32_t shift;
 };
 
+// Prefix groups of one window.  Requests whose chains begin with the same
+// pool segment (equal pre_off) share it: the longest cached prefix of that
+// segment, up to the longest member's segment length p_max, is computed
+// once per window on every holder of its first block (by the request that
+// claimed the group, its leader), and every member derives its own hit: a
+// member with segment length p has hit H on an instance whose walk of the
+// shared segment stopped at H < p; otherwise its first p blocks are all
+// cached there and its own walk resumes at its tail.
+constexpr int32_t kGroupMin = 8;             // shortest shared segment walked as a group
+constexpr uint32_t kGroupHold = 16;          // holders of the first block per group record
+constexpr uint32_t kGroupNone = 0xFFFFFFFFu; // record without a result (more holders)
+constexpr int kGroupGenShift = 40;           // key = gen << 40 | (pre_off + 1)
+constexpr uint64_t kGroupGenMax = (1ull << 24) - 1;
+constexpr int32_t kGroupMaxReq = 1 << 22;    // larger windows are scored without groups
+
+// Record of one group slot: GroupMeta, then up to kGroupHold holders in
+// ascending id order as {instance id, hit of the leader's segment there}.
+struct alignas(8) GroupMeta {
+  int32_t plen;  // length of the segment the leader walked
+  uint32_t cnt;  // holders of its first block, or kGroupNone
+};
+constexpr int kGroupRec = 1 + (int)kGroupHold;  // 8-byte words per slot record
+
+constexpr uint32_t kGroupLead = 0x80000000u;  // slot_of flag of the group's leader
+constexpr uint32_t kGroupNoSlot = 0xFFFFFFFFu;
+
+struct GroupTab {
+  unsigned long long* keys;  // slots; a key of another generation is an empty slot
+  unsigned long long* plen;  // slots: gen << 40 | p_max (an older generation compares lower)
+  uint2* rec;                // slots * kGroupRec words
+  uint32_t* slot_of;         // per request: slot (| kGroupLead), or kGroupNoSlot
+  uint32_t mask;             // slots - 1
+  uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
+};
+
 struct ScoreArgs {
   Tables t;
   GIndex x;
+  GroupTab grp;  // keys == nullptr: no prefix groups in this launch
   const int64_t* room_sorted;  // rooms ascending (eligible count = n - lower_bound(L))
   const uint32_t* order0;      // instance ids by (decoding desc, queued asc, id asc)
   const InstState* inst_key;   // the instances' states in that order
@@ -192,6 +228,9 @@ hipError_t ps_build_index(const ps::Tables& t, int32_t n_inst, const uint32_t* c
                           ps::GIndex* x, hipStream_t s);
 void ps_free_index(ps::GIndex* x);
 hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
+// Prefix groups of a window: slot of every request and the longest member
+// segment per group, then the walks of the leaders.
+hipError_t ps_launch_group(const ps::ScoreArgs& a, hipStream_t s);
 // Per-arrival scheduler: one workgroup of `threads` (a multiple of 64, at
 // most kSeqMaxThreads) over requests [a.r0, a.r1).
 hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);

@@ -136,6 +136,97 @@ __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
   }
 }
 
+// Slot of a request's prefix group.  Linear probing over the window's
+// group table; a slot whose key belongs to an older window is empty and is
+// claimed with a 64-bit compare-and-swap.  Keys of the current window never
+// change once written, so a plain read that shows one is exact, and a stale
+// read only makes the compare-and-swap fail, whose result then decides.
+// *leader = 1 for the request whose swap claimed the slot.
+__device__ int32_t group_claim(const GroupTab& G, int64_t pre_off, int* leader) {
+  const unsigned long long key =
+      ((unsigned long long)G.gen << kGroupGenShift) | (unsigned long long)(pre_off + 1);
+  uint32_t b = (uint32_t)(((uint64_t)(pre_off + 1) * 0x9E3779B97F4A7C15ull) >> 32) & G.mask;
+  *leader = 0;
+  for (uint32_t step = 0; step <= G.mask; ++step, b = (b + 1) & G.mask) {
+    const unsigned long long v = G.keys[b];
+    if (v == key) return (int32_t)b;
+    if ((v >> kGroupGenShift) == G.gen) continue;  // another group of this window
+    const unsigned long long old = atomicCAS(&G.keys[b], v, key);
+    if (old == v) {
+      *leader = 1;
+      return (int32_t)b;
+    }
+    if (old == key) return (int32_t)b;
+    // otherwise claimed for another group of this window meanwhile
+  }
+  return -1;  // table full (not reached: it holds at least twice the requests)
+}
+
+// Prefix groups, pass 1 (one thread per request): the slot of every
+// request's group and the group's longest segment (a 64-bit maximum over
+// generation-tagged lengths, so no slot needs clearing between windows).
+__global__ void group_claim_kernel(ScoreArgs a) {
+  const GroupTab& G = a.grp;
+  for (int32_t r = blockIdx.x * blockDim.x + threadIdx.x; r < a.n_req;
+       r += gridDim.x * blockDim.x) {
+    const ps_req q = a.reqs[r];
+    uint32_t out = kGroupNoSlot;
+    if (req_valid(q, a.pool_len) && q.pre_len >= kGroupMin) {
+      int leader = 0;
+      const int32_t slot = group_claim(G, q.pre_off, &leader);
+      if (slot >= 0) {
+        atomicMax(&G.plen[slot], ((unsigned long long)G.gen << kGroupGenShift) |
+                                     (unsigned long long)q.pre_len);
+        out = (uint32_t)slot | (leader ? kGroupLead : 0u);
+      }
+    }
+    G.slot_of[r] = out;
+  }
+}
+
+// Prefix groups, pass 2 (one wave per request; only leaders work): the walk
+// of the group's longest segment on every holder of its first block, into
+// the slot's record.
+__global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
+  const int lane = threadIdx.x;
+  const int g = lane >> 3, s = lane & 7;
+  const GroupTab& G = a.grp;
+  for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
+    const uint32_t so = G.slot_of[r];
+    if (so == kGroupNoSlot || !(so & kGroupLead)) continue;
+    const uint32_t slot = so & ~kGroupLead;
+    const int64_t pre_off = a.reqs[r].pre_off;
+    const int32_t plen =
+        (int32_t)(G.plen[slot] & ((1ull << kGroupGenShift) - 1ull));  // every member lies in the pool
+    const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
+    const int32_t nst = plen < kStage ? plen : kStage;
+    __syncthreads();
+    for (int32_t j = lane; j < nst; j += 64) stage[j] = c.pre[j];
+    __syncthreads();
+    const IdxHit h0 = index_lookup(a.x, stage[0], g == 0, g, s);
+    const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
+    const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
+    uint2* rec = G.rec + (size_t)slot * kGroupRec;
+    uint32_t cnt = 0u;
+    if (found0 && cnt0 > kGroupHold) {
+      cnt = kGroupNone;
+    } else if (found0) {
+      const uint32_t id = (uint32_t)lane < cnt0 ? a.x.holders[off0 + lane] : 0u;
+      uint32_t myhit = 0;
+      for (uint32_t k = 0; k < cnt0; ++k) {
+        const uint32_t idk = (uint32_t)__shfl((int)id, (int)k);
+        const uint32_t hk = run_walk<true>(a.t, idk, c, stage, 0, g, s);
+        if ((uint32_t)lane == k) myhit = hk;
+      }
+      if ((uint32_t)lane < cnt0) rec[1 + lane] = make_uint2(id, myhit);
+      cnt = cnt0;
+    }
+    if (lane == 0) rec[0] = make_uint2((uint32_t)plen, cnt);
+  }
+}
+
 // LDS of one scoring wave: chain stage | live bitmap | next bitmap |
 // candidate bitmap (instances holding the first block) | 64 candidate ids |
 // u16 hit slots (or device scratch for large pools).
@@ -148,7 +239,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   uint64_t* bmA = stage + kStage;
   uint64_t* bmN = bmA + nw;
   uint64_t* bmC = bmN + nw;
-  uint16_t* cl = reinterpret_cast<uint16_t*>(bmC + nw);
+  uint32_t* ch = reinterpret_cast<uint32_t*>(bmC + nw);  // group hits of the candidates
+  uint16_t* cl = reinterpret_cast<uint16_t*>(ch + 64);
   uint16_t* hits = HITS_IN_LDS ? cl + 64 : a.scratch + (size_t)blockIdx.x * (size_t)n_inst;
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
@@ -158,6 +250,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   for (int32_t w = lane; w < 3 * nw; w += 64) bmA[w] = 0ull;
 
   for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
+    const uint32_t gso = a.grp.keys ? a.grp.slot_of[r] : kGroupNoSlot;
     const ps_req q = a.reqs[r];
     if (!req_valid(q, a.pool_len)) {
       if (lane == 0) {
@@ -170,7 +263,19 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
     const int32_t ell = c.len;
     const int64_t L = (int64_t)ell * m.bs;
     const float Lf = (float)L;
-    const int32_t nst = ell < kStage ? ell : kStage;
+    // The group record (meta and the first 16 holders) is read with the
+    // room search's first loads; a request with a group result needs no
+    // staged chain.
+    GroupMeta gm{0, kGroupNone};
+    uint2 hd = make_uint2(0u, 0u);
+    if (gso != kGroupNoSlot) {
+      const uint2* grec = a.grp.rec + (size_t)(gso & ~kGroupLead) * kGroupRec;
+      const uint2 m0 = grec[0];
+      if ((uint32_t)lane < kGroupHold) hd = grec[1 + lane];
+      gm = GroupMeta{(int32_t)m0.x, m0.y};
+    }
+    const bool grp = gm.cnt != kGroupNone;
+    const int32_t nst = grp ? 0 : (ell < kStage ? ell : kStage);
     // The chain head's loads and the room search's are in flight together.
     uint64_t sv[kStage / 64];
 #pragma unroll
@@ -180,17 +285,29 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
     }
     // |A|: capacity-eligible instances are those with room >= L.
     const uint32_t nA = (uint32_t)(n_inst - wave_lower_bound(a.room_sorted, n_inst, L, lane));
-    __syncthreads();
+    if (!grp) {
+      __syncthreads();
 #pragma unroll
-    for (int u = 0; u < kStage / 64; ++u) {
-      const int32_t j = lane + 64 * u;
-      if (j < nst) stage[j] = sv[u];
+      for (int u = 0; u < kStage / 64; ++u) {
+        const int32_t j = lane + 64 * u;
+        if (j < nst) stage[j] = sv[u];
+      }
+      __syncthreads();
     }
-    __syncthreads();
 
     // (1) Holders of the first block among the eligible instances.
     uint32_t nCand = 0;
-    if (nA > 0 && ell > 0) {
+    if (grp) {  // from the group record: ids and hits of the shared segment
+      const bool el = nA > 0 && (uint32_t)lane < gm.cnt && a.room[hd.x] >= L;
+      const uint64_t em = __ballot(el);
+      const uint32_t rank = (uint32_t)__popcll(em & lt_mask);
+      if (el) {
+        cl[rank] = (uint16_t)hd.x;
+        ch[rank] = hd.y;
+        atomicOr(reinterpret_cast<unsigned long long*>(&bmC[hd.x >> 6]), 1ull << (hd.x & 63));
+      }
+      nCand = (uint32_t)__popcll(em);
+    } else if (nA > 0 && ell > 0) {
       const IdxHit h0 = index_lookup(a.x, stage[0], g == 0, g, s);
       const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
       const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
@@ -236,7 +353,24 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
     // Walks.  few: each holder on its own table; else: all live holders
     // through the index, one position at a time.
     uint32_t myid = 0, myhit = 0;
-    if (few) {
+    if (few && grp) {
+      // Hit H of the shared segment: exact below the request's segment
+      // length p; otherwise the walk resumes on its own chain at p.
+      const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
+      if ((uint32_t)lane < nCand) {
+        myid = cl[lane];
+        myhit = ch[lane];
+      }
+      uint64_t need = __ballot((uint32_t)lane < nCand && (int32_t)myhit >= p0);
+      while (need) {
+        const int k = __builtin_ctzll(need);
+        need &= need - 1;
+        const uint32_t id = (uint32_t)__shfl((int)myid, k);
+        const uint32_t hk = run_walk<false>(a.t, id, c, nullptr, p0, g, s);
+        if (lane == k) myhit = hk;
+      }
+      if ((uint32_t)lane < nCand) hits[myid] = encode_hit(myhit);
+    } else if (few) {
       if ((uint32_t)lane < nCand) myid = cl[lane];
       for (uint32_t k = 0; k < nCand; ++k) {
         const uint32_t id = (uint32_t)__shfl((int)myid, (int)k);
@@ -468,7 +602,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         while (ovf) {
           const int k = __builtin_ctzll(ovf);
           ovf &= ovf - 1;
-          const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+          const uint32_t hk = grp ? run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, 0, g, s)
+                                  : run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
           if (lane == k) v = hk;
         }
         bool inT = false;
@@ -598,8 +733,8 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
 size_t ps_score_lds_bytes(int32_t n_inst) {
   const size_t nw = ((size_t)n_inst + 63) / 64;
   const size_t hits = ps_hits_fit_lds(n_inst) ? (size_t)n_inst * sizeof(uint16_t) : 0;
-  return (size_t)kStage * sizeof(uint64_t) + 3 * nw * sizeof(uint64_t) + 64 * sizeof(uint16_t) +
-         (hits + 15) / 16 * 16;
+  return (size_t)kStage * sizeof(uint64_t) + 3 * nw * sizeof(uint64_t) + 64 * sizeof(uint32_t) +
+         64 * sizeof(uint16_t) + (hits + 15) / 16 * 16;
 }
 
 bool ps_hits_fit_lds(int32_t n_inst) {
@@ -635,6 +770,15 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
     else
       hipLaunchKernelGGL(score_kernel<false>, dim3(grid), dim3(64), lds, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t ps_launch_group(const ScoreArgs& a, hipStream_t s) {
+  if (a.n_req == 0) return hipSuccess;
+  hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + 255) / 256), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_kernel, dim3(a.n_req), dim3(64), (size_t)kStage * sizeof(uint64_t), s, a);
   return hipGetLastError();
 }
 

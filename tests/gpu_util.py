@@ -32,10 +32,13 @@ ALPHA = [0.02, 1e-4, 1.5e-9, 7.5e-10, 1e-7, 1e-14]
 SEG_UB, BETA, GAMMA = (8, 64, 512), ((0.01, 1e-4, 1e-8),) * 3, (1.0, 1.1, 1.2)
 
 
-def edge_window(sets, chains, **kw):
-    from tests.tinywin import make_window
+def edge_window(sets, chains, pool=None, reqs=None, **kw):
+    """Edge-case window from explicit block sets and chains, or (chains None)
+    from an explicit pool and descriptors (pre_off, pre_len, tail_off,
+    tail_len) that may share pool segments."""
+    from tests.tinywin import make_window, make_window_pool
     n = len(sets)
-    rng = np.random.default_rng(len(sets) * 7 + len(chains))
+    rng = np.random.default_rng(len(sets) * 7 + (len(chains) if chains is not None else len(reqs)))
     D = kw.pop("D", rng.integers(0, 64, n))
     Q = kw.pop("Q", rng.integers(0, 4, n))
     P = kw.pop("P", rng.integers(0, 8192, n) * (np.asarray(Q) > 0))
@@ -44,7 +47,10 @@ def edge_window(sets, chains, **kw):
     kw.setdefault("tpot_slo", 0.05)
     kw.setdefault("b_max", 512)
     kw.setdefault("kv_cap_tokens", 4_194_304)
-    w = make_window(sets, chains, D, Q, P, S, ALPHA, SEG_UB, BETA, GAMMA, cap=cap, **kw)
+    if chains is None:
+        w = make_window_pool(sets, pool, reqs, D, Q, P, S, ALPHA, SEG_UB, BETA, GAMMA, cap=cap, **kw)
+    else:
+        w = make_window(sets, chains, D, Q, P, S, ALPHA, SEG_UB, BETA, GAMMA, cap=cap, **kw)
     w.alpha = np.asarray(w.alpha, np.float32)
     w.beta = np.asarray(w.beta, np.float32)
     w.gamma = np.asarray(w.gamma, np.float32)

@@ -180,6 +180,88 @@ def test_edge_large_instance_count_uses_scratch(ps, scorer):
     assert not scorer.table_info()["hits_in_lds"]
 
 
+# ------------------------------------------------------------- prefix groups
+def _shared_pool_window(base=101, order_seed=0, **kw):
+    """Requests sharing pool segments with different prefix lengths and
+    their own tails (some cached after the segment), so that whichever
+    request leads a group, members lie on both sides of its segment length.
+    Segment S1's first block has more holders than a group record keeps,
+    S2's has none, S3 has a zero hash inside."""
+    rng = np.random.default_rng(base)
+    S0 = chain_hashes(400, base=base)
+    S1 = chain_hashes(120, base=base + 5 * 10**6)
+    S2 = chain_hashes(40, base=base + 9 * 10**6)
+    S3 = chain_hashes(30, base=base + 13 * 10**6)
+    S3[5] = 0
+    tails = [chain_hashes(int(rng.integers(1, 6)), base=base + 10**8 + 10**4 * k) for k in range(12)]
+    pool = []
+
+    def put(seq):
+        off = len(pool)
+        pool.extend(seq)
+        return off
+
+    o0, o1, o2, o3 = put(S0), put(S1), put(S2), put(S3)
+    t_off = [put(t) for t in tails]
+    n_inst = 26
+    sets = [[] for _ in range(n_inst)]
+    sets[0] = S0 + tails[0] + tails[1]      # all of S0, then tails 0 and 1
+    sets[1] = S0[:120] + tails[2][:2]        # a shorter prefix, then tail 2's head
+    sets[2] = S0[:50] + S0[60:100]           # a hole at block 50
+    sets[3] = S0[:10] + tails[3]             # tail 3, reachable only after S0[:10]
+    sets[4] = S0[:300]
+    sets[5] = S0[1:200]                      # lacks the first block
+    for i in range(6, 24):                   # 18 holders of S1's first block
+        sets[i] = S1[:int(rng.integers(1, 121))]
+    sets[6] += S0[:8]
+    sets[7] += S3[:5] + S3[6:]
+    sets[24] = S3[:5]
+    sets[25] = S0[:399]
+    reqs = []
+    for k, p in enumerate([8, 9, 10, 11, 49, 50, 51, 100, 119, 120, 121, 200, 299, 300, 301,
+                           398, 399, 400]):
+        t = k % 4
+        reqs.append((o0, p, t_off[t], len(tails[t])))
+    reqs += [(o0, 10, t_off[3], len(tails[3])), (o0, 120, t_off[2], len(tails[2])),
+             (o0, 400, t_off[0], len(tails[0])), (o0, 400, t_off[1], 0),
+             (o0, 400, t_off[1], len(tails[1])), (o0, 300, t_off[0], 0)]
+    reqs += [(o1, p, t_off[5], len(tails[5])) for p in (8, 60, 120)]
+    reqs += [(o2, p, t_off[6], 1) for p in (8, 40)]
+    reqs += [(o3, p, t_off[7], len(tails[7])) for p in (8, 30)]
+    # no group: a short shared segment, a tail-only chain, an offset segment
+    reqs += [(o0, 3, t_off[8], 2), (o0, 0, o0, 50), (o0 + 10, 30, t_off[9], 1), (o0 + 10, 30, t_off[9], 0)]
+    perm = np.random.default_rng(order_seed).permutation(len(reqs))
+    reqs = [reqs[k] for k in perm]
+    return _edge(sets, None, pool=pool, reqs=reqs, cap=420, **kw)
+
+
+def test_prefix_groups_shared_segments(ps, scorer):
+    """Members of one group with segment lengths on both sides of the
+    leader's, cached tails, holes, records without a result, zero hashes;
+    several request orders (different leaders), policies and repeated calls."""
+    for order_seed in range(4):
+        w = _shared_pool_window(order_seed=order_seed)
+        _check_edge(ps, scorer, w, f"groups order={order_seed}")
+        _check_edge(ps, scorer, w, f"groups order={order_seed} b_max=40", b_max=40)
+        _check_edge(ps, scorer, w, f"groups order={order_seed} eta=1", eta=1.0)
+    # the same offsets with other contents: nothing of an earlier window's
+    # groups may be used
+    for base in (7, 555, 7):
+        _check_edge(ps, scorer, _shared_pool_window(base=base), f"groups base={base}")
+
+
+def test_prefix_groups_window_sizes(ps, scorer):
+    """Windows of growing and shrinking request counts on one context (the
+    group table grows; later smaller windows reuse it)."""
+    w = synth.generate("c2", n_req=4096)
+    load_window(scorer, w)
+    o = oracle.Oracle.from_window(w)
+    for n in (1, 7, 4096, 300, 2048, 1):
+        sub = w.subset(range(n))
+        res, sizes = DeviceWindow(sub).score(scorer)
+        compare_decisions(res, sizes, o.window_score(sub), label=f"c2 first {n}")
+
+
 def test_invalid_descriptor_flagged_on_device(ps, scorer):
     import torch
     w = synth.generate("c1", n_req=8)

@@ -53,3 +53,16 @@ def make_window(sets, chains, D, Q, P, S, alpha, seg_ub, beta, gamma, cap=None, 
 def chain_hashes(n, base=1000):
     """n distinct nonzero block hashes."""
     return [base + 7 * j + 1 for j in range(n)]
+
+
+def make_window_pool(sets, pool, reqs, D, Q, P, S, alpha, seg_ub, beta, gamma, cap=None,
+                     **policy):
+    """Like make_window, with an explicit hash pool and descriptors
+    (pre_off, pre_len, tail_off, tail_len), so that several requests can
+    share one pool segment."""
+    w = make_window(sets, [], D, Q, P, S, alpha, seg_ub, beta, gamma, cap=cap, **policy)
+    w.pool = np.asarray(pool, dtype=np.uint64)
+    d = np.asarray(reqs, dtype=np.int64).reshape(-1, 4)
+    w.pre_off, w.pre_len = d[:, 0].copy(), d[:, 1].astype(np.int32)
+    w.tail_off, w.tail_len = d[:, 2].copy(), d[:, 3].astype(np.int32)
+    return w
