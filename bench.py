@@ -154,12 +154,11 @@ def score_bytes(win, r0, hits, grp=None):
     position and 16 bytes (chain + row) per compared position, and a final
     64-byte probe at the first absent block; with more than 64 holders, one
     index bucket plus the holder data per walked position; 32 bytes of state
-    per member of C; the key-ordered scan of the hit-0 class (4-byte order
-    entry + 8-byte room per scanned instance, 32 bytes of state per eligible
-    one).  With prefix groups (`grp`: per request its group's segment hits
-    Hg, whether the group record holds a result, and whether the request is
-    grouped at all), a request with a group result reads the record (meta +
-    16 holders) and the holders' rooms instead of staging, index and walks,
+    per member of C; the threshold search of the hit-0 class (below).  With
+    prefix groups (`grp`: per request its group's segment hits Hg, whether
+    the group record holds a result, and whether the request is grouped at
+    all), a request with a group result reads the record (meta + 16
+    holders) and the holders' rooms instead of staging, index and walks,
     and walks only where the group's segment is cached up to its own
     segment length (from there, on its tail)."""
     import numpy as np
@@ -232,17 +231,31 @@ def score_bytes(win, r0, hits, grp=None):
     seg = np.searchsorted(ub, A1, side="left")
     seg = np.minimum(seg, len(ub) - 1)
     order0 = np.lexsort((np.arange(N), win.Q, -win.D.astype(np.int64)))
+    n1 = (N + 63) // 64
     for r in np.nonzero(act & admit0)[0]:
+        # The threshold search of the hit-0 class (the benchmark's policy:
+        # a monotone model, no TTFT admission, the D-C-Q key): 64 chunk
+        # maxima per read (4 B each), 64 threshold entries per visited chunk
+        # (16 B each) up to the first admitted non-holder.
         t_iter = gam[seg] * (beta[seg, 0] + beta[seg, 1] * A1 + beta[seg, 2] * (win.S + L[r]))
         tpot0 = t_iter + np.where(A1 > 1, _tpf(a, float(L[r]), 0.0) / lout1, 0.0)
         zero = elig[r] & ~hold0[r]
+        feas = np.zeros(n1 * 64, bool)
+        feas[:N] = (elig[r] & (tpot0 < tau))[order0]
         ok = (zero & (tpot0 < tau))[order0]
-        if ok.any():
-            k = int(np.argmax(ok))
-            scanned = (k // 64 + 1) * 64
-            by[r] += min(scanned, N) * 12 + 32 * int(zero[order0[:scanned]].sum())
-        else:
-            by[r] += N * 12 + 32 * int(zero.sum())
+        found = bool(ok.any())
+        cs = int(np.argmax(ok)) // 64 if found else n1 - 1
+        by[r] += 256 * (cs // 64 + 1) + 1024 * int(feas.reshape(n1, 64)[:cs + 1].any(1).sum())
+        if found:
+            continue
+        # No member of the class is in T: it is evaluated in full (room and
+        # state of each eligible non-holder) only when no candidate is in T.
+        cr = cand[r] & inC[r]
+        if cr.any():
+            tp = t_iter[cr] + np.where(A1[cr] > 1, _tpf(a, n[r][cr], c[r][cr]) / lout1, 0.0)
+            if (tp < tau).any():
+                continue
+        by[r] += 8 * N + 32 * int(zero.sum())
     return int(by.sum())
 
 

@@ -44,6 +44,8 @@ struct ps_ctx {
   int64_t* d_room_sorted = nullptr;
   uint32_t* d_order0 = nullptr;
   InstState* d_inst_key = nullptr;  // states in d_order0's order
+  int4* d_lm = nullptr;              // zero-hit admission thresholds in that order
+  int32_t* d_lm1 = nullptr;          // their maxima per 64 positions
   GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
@@ -177,6 +179,23 @@ ps_status check_model(ps_ctx* c, const ps_model* m) {
   return PS_OK;
 }
 
+// Whether the zero-hit TPOT test of every instance is one threshold on the
+// request length L: T_pf(L, 0) = a0 + L (a1 + a3 L) and the decode term
+// gamma (b0 + b1 B + b2 (S + L)) are then non-decreasing in L in fp32 too
+// (each rounded step is a monotone function of non-negative operands).
+uint32_t monotone(const DevModel& d) {
+  for (int k = 0; k < 6; ++k)
+    if (!std::isfinite(d.a[k])) return 0u;
+  if (!(d.a[1] >= 0.0f) || !(d.a[3] >= 0.0f)) return 0u;
+  if (!std::isfinite(d.lout1) || !(d.lout1 > 0.0f) || !std::isfinite(d.tau)) return 0u;
+  for (int s = 0; s < d.n_seg; ++s) {
+    for (int k = 0; k < 4; ++k)
+      if (!std::isfinite(d.seg[s][k])) return 0u;
+    if (!(d.seg[s][2] >= 0.0f) || !(d.seg[s][3] >= 0.0f)) return 0u;
+  }
+  return 1u;
+}
+
 DevModel device_model(const ps_model& m) {
   DevModel d{};
   for (int k = 0; k < 6; ++k) d.a[k] = m.alpha[k];
@@ -200,6 +219,7 @@ DevModel device_model(const ps_model& m) {
     for (int k = 0; k < 3; ++k) d.seg[s][k] = s < m.n_seg ? m.beta[s][k] : 0.0f;
     d.seg[s][3] = s < m.n_seg ? m.gamma[s] : 1.0f;
   }
+  d.mono = monotone(d);
   return d;
 }
 
@@ -232,9 +252,20 @@ void free_snapshot(ps_ctx* c) {
   dfree(c->d_room_sorted);
   dfree(c->d_order0);
   dfree(c->d_inst_key);
+  dfree(c->d_lm);
+  dfree(c->d_lm1);
   dfree(c->d_scratch);
   ps_free_index(&c->x);
   c->loaded = false;
+}
+
+// Zero-hit admission thresholds for the current state and model, complete
+// before the entry point returns.
+ps_status refresh_lmax(ps_ctx* c) {
+  HIP_TRY(c, ps_launch_lmax(c->d_inst_key, c->d_order0, c->d_model, c->n_inst, c->d_lm, c->d_lm1,
+                            c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return PS_OK;
 }
 
 // Per-instance room (kv_cap - S when A + 1 <= B_max, else -1; an instance
@@ -290,12 +321,13 @@ ps_status refresh_derived(ps_ctx* c) {
   HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
   const std::vector<InstState> ik = states_in_order(c->h_state, o0);
   HIP_TRY(c, hipMemcpy(c->d_inst_key, ik.data(), ik.size() * sizeof(InstState), hipMemcpyHostToDevice));
-  return PS_OK;
+  return refresh_lmax(c);
 }
 
 ps_status upload_model(ps_ctx* c) {
+  c->h_model.mono = monotone(c->h_model);
   HIP_TRY(c, hipMemcpy(c->d_model, &c->h_model, sizeof c->h_model, hipMemcpyHostToDevice));
-  return PS_OK;
+  return refresh_lmax(c);
 }
 
 }  // namespace
@@ -421,6 +453,8 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     dfree(fresh.d_room_sorted);
     dfree(fresh.d_order0);
     dfree(fresh.d_inst_key);
+    dfree(fresh.d_lm);
+    dfree(fresh.d_lm1);
     dfree(fresh.d_scratch);
     ps_free_index(&fresh.x);
     dfree(d_off);
@@ -440,6 +474,8 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room_sorted, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_order0, (size_t)n * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst_key, (size_t)n * sizeof(InstState));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_lm, (size_t)n * sizeof(int4));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_lm1, (size_t)((n + 63) / 64) * sizeof(int32_t));
   if (e == hipSuccess && rows)
     e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint16_t));
   if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
@@ -523,6 +559,8 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->d_room_sorted = fresh.d_room_sorted;
   c->d_order0 = fresh.d_order0;
   c->d_inst_key = fresh.d_inst_key;
+  c->d_lm = fresh.d_lm;
+  c->d_lm1 = fresh.d_lm1;
   c->x = fresh.x;
   c->d_scratch = fresh.d_scratch;
   c->scratch_rows = rows;
@@ -547,8 +585,15 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.d_room_sorted = nullptr;
   fresh.d_order0 = nullptr;
   fresh.d_inst_key = nullptr;
+  fresh.d_lm = nullptr;
+  fresh.d_lm1 = nullptr;
   fresh.x = GIndex{nullptr, nullptr, nullptr, 0, 0, 64};
   fresh.d_scratch = nullptr;
+  const ps_status lst = refresh_lmax(c);
+  if (lst != PS_OK) {
+    free_snapshot(c);
+    return lst;
+  }
   return PS_OK;
 }
 
@@ -592,6 +637,8 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.room_sorted = c->d_room_sorted;
   a.order0 = c->d_order0;
   a.inst_key = c->d_inst_key;
+  a.lm = c->d_lm;
+  a.lm1 = c->d_lm1;
   a.inst = c->d_inst;
   a.room = c->d_room;
   a.model = c->d_model;
@@ -739,6 +786,8 @@ static ps_status after_commit(ps_ctx* c, hipStream_t s, int64_t* n_dropped) {
   HIP_TRY(c, hipMemcpy(c->d_inst_key, ik.data(), ik.size() * sizeof(InstState), hipMemcpyHostToDevice));
   HIP_TRY(c, ps_build_index(c->t, c->n_inst, c->h_count.data(), &c->x, s));
   HIP_TRY(c, hipStreamSynchronize(s));
+  const ps_status lst = refresh_lmax(c);
+  if (lst != PS_OK) return lst;
   if (n_dropped) *n_dropped = (int64_t)dropped;
   return PS_OK;
 }

@@ -45,6 +45,10 @@ struct DevModel {
   uint32_t sel;       // PS_SEL_*
   uint64_t rand_seed;
   int32_t n_seg;
+  // 1 when the zero-hit TPOT test can only turn from pass to fail as L
+  // grows (finite coefficients, alpha1, alpha3, every beta2 and gamma >= 0):
+  // then an instance's zero-hit admission is one threshold on L.
+  uint32_t mono;
   int32_t seg_ub[PS_MAX_SEG];
   float seg[PS_MAX_SEG][4];  // beta0, beta1, beta2, gamma
 };
@@ -142,6 +146,8 @@ struct ScoreArgs {
   const int64_t* room_sorted;  // rooms ascending (eligible count = n - lower_bound(L))
   const uint32_t* order0;      // instance ids by (decoding desc, queued asc, id asc)
   const InstState* inst_key;   // the instances' states in that order
+  const int4* lm;              // key order: {longest zero-hit admitted chain (blocks, -1 none), id, D, Q}
+  const int32_t* lm1;          // maxima of lm[].x over 64-entry chunks
   const InstState* inst;
   const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
   const DevModel* model;
@@ -228,6 +234,9 @@ hipError_t ps_build_index(const ps::Tables& t, int32_t n_inst, const uint32_t* c
                           ps::GIndex* x, hipStream_t s);
 void ps_free_index(ps::GIndex* x);
 hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
+// Zero-hit admission thresholds in key order and their chunk maxima.
+hipError_t ps_launch_lmax(const ps::InstState* inst_key, const uint32_t* order0,
+                          const ps::DevModel* m, int32_t n, int4* lm, int32_t* lm1, hipStream_t s);
 // Prefix groups of a window: slot of every request and the longest member
 // segment per group, then the walks of the leaders.
 hipError_t ps_launch_group(const ps::ScoreArgs& a, hipStream_t s);

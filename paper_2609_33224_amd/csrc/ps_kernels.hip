@@ -136,6 +136,42 @@ __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
   }
 }
 
+// Zero-hit admission threshold of the instance at key position k: the
+// longest chain (blocks) it admits with no cached prefix, i.e. capacity-
+// eligible and, unless the TPOT test is off, predicted TPOT below the
+// target.  With a monotone model both tests hold for every shorter chain
+// too, so a binary search over the length finds the boundary with the same
+// fp32 evaluation the scoring kernel makes; -1 when not even an empty
+// chain is admitted.  lm1 = the maximum over each 64-entry chunk.
+__global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, const uint32_t* order0,
+                                                  const DevModel* mp, int32_t n, int4* lm,
+                                                  int32_t* lm1) {
+  const DevModel& m = *mp;
+  const int32_t k = blockIdx.x * 64 + threadIdx.x;
+  int32_t best = -1;
+  if (k < n) {
+    const InstState st = inst_key[k];
+    auto admits = [&](int32_t ell) {
+      const int64_t L = (int64_t)ell * m.bs;
+      if (!eligible(m, st.A1, st.S, L)) return false;
+      if (m.flags & PS_F_NO_TPOT_FILTER) return true;
+      return latency(m, st, (float)L, 0.0f, L).tpot < m.tau;
+    };
+    if (admits(0)) {
+      int32_t lo = 0, hi = PS_MAX_CHAIN + 1;  // admits(lo); hi fails or lies past the range
+      while (hi - lo > 1) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (admits(mid)) lo = mid;
+        else hi = mid;
+      }
+      best = lo;
+    }
+    lm[k] = make_int4(best, (int)order0[k], st.D, st.Q);
+  }
+  const uint64_t mx = ~wave_min_u64(~(uint64_t)(uint32_t)(best + 1));
+  if (threadIdx.x == 0) lm1[blockIdx.x] = (int32_t)mx - 1;
+}
+
 // Slot of a request's prefix group.  Linear probing over the window's
 // group table; a slot whose key belongs to an older window is empty and is
 // claimed with a 64-bit compare-and-swap.  Keys of the current window never
@@ -544,7 +580,33 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         // when no member is in T (then the fallback key may come from it).
         bool done0 = false;
         const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
-        if (!a.sizes && keyed) {
+        if (!a.sizes && keyed && m.mono && !(m.flags & PS_F_TTFT_ADMIT)) {
+          // The first member of T in key order: the first key position whose
+          // threshold admits this length and whose instance does not hold
+          // the first block.  Chunk maxima skip 64 positions per entry.
+          const int32_t n1 = (n_inst + 63) >> 6;
+          for (int32_t c0 = 0; c0 < n1 && !done0; c0 += 64) {
+            const int32_t cc = c0 + lane;
+            uint64_t cm = __ballot(cc < n1 && a.lm1[cc] >= ell);
+            while (cm && !done0) {
+              const int32_t k0 = (c0 + __builtin_ctzll(cm)) * 64;
+              cm &= cm - 1;
+              const int32_t k = k0 + lane;
+              const int4 e = k < n_inst ? a.lm[k] : make_int4(-1, 0, 0, 0);
+              const uint64_t om = __ballot(e.x >= ell && !test_bit(bmC, (uint32_t)e.y));
+              if (om) {
+                if (lane == __builtin_ctzll(om)) {
+                  InstState st{};
+                  st.D = e.z;
+                  st.Q = e.w;
+                  const uint64_t kt = select_key(m.sel, st, 0u, (uint32_t)e.y, 0ull);
+                  acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                }
+                done0 = true;
+              }
+            }
+          }
+        } else if (!a.sizes && keyed) {
           for (int32_t base = 0; base < n_inst && !done0; base += 64) {
             const int32_t k = base + lane;
             bool ok = false;
@@ -569,6 +631,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
             }
           }
         }
+        // No member of the class is in T: its keys matter only for the
+        // fallback, i.e. when no candidate is in T either.
+        if (!done0 && !a.sizes && keyed) done0 = wave_min_u64(acc.keyT) != ~0ull;
         if (!done0) {
           for (int32_t base = 0; base < n_inst; base += 64) {
             const int32_t i = base + lane;
@@ -770,6 +835,14 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
     else
       hipLaunchKernelGGL(score_kernel<false>, dim3(grid), dim3(64), lds, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, const DevModel* m,
+                          int32_t n, int4* lm, int32_t* lm1, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(lmax_kernel, dim3((n + 63) / 64), dim3(64), 0, s, inst_key, order0, m, n, lm,
+                     lm1);
   return hipGetLastError();
 }
 

@@ -106,6 +106,25 @@ def test_policy_variants(ps, scorer, policy):
         assert ((res["flags"] & ps.PS_R_FALLBACK) != 0).all()
 
 
+def test_non_monotone_model(ps, scorer):
+    """Coefficients under which the zero-hit TPOT test is not one threshold
+    on the request length (a negative context or quadratic term): the
+    kernel scans the class in key order instead of using the thresholds."""
+    for name, gen in (("c1", {}), ("c2", dict(n_req=2048))):
+        w = synth.generate(name, **gen)
+        w.beta = np.asarray(w.beta, np.float32).copy()
+        w.beta[:, 2] = -2e-10
+        w.alpha = np.asarray(w.alpha, np.float32).copy()
+        w.alpha[3] = -1e-12
+        load_window(scorer, w)
+        dw = DeviceWindow(w)
+        res, sizes = dw.score(scorer)
+        od = oracle.Oracle.from_window(w).window_score(w)
+        compare_decisions(res, sizes, od, label=f"{name} non-monotone")
+        res2, _ = dw.score(scorer, with_sizes=False)
+        assert res2.tobytes() == res.tobytes()
+
+
 # ------------------------------------------------------------- edge windows
 def _check_edge(ps, scorer, w, label, **policy):
     w.alpha = np.asarray(w.alpha, np.float32)
