@@ -73,6 +73,7 @@ struct ps_ctx {
   unsigned long long* d_gkeys = nullptr;  // keys, then the tagged segment lengths
   uint2* d_grec = nullptr;
   uint32_t* d_gslot = nullptr;
+  uint32_t* d_gpop = nullptr;  // counter word, then the popular rows
   uint32_t gslots = 0;   // power of two
   int32_t greq_cap = 0;  // entries of d_gslot
   uint64_t ggen = 0;
@@ -374,6 +375,7 @@ ps_status ps_destroy(ps_ctx* c) {
   dfree(c->d_gkeys);
   dfree(c->d_grec);
   dfree(c->d_gslot);
+  dfree(c->d_gpop);
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
   if (c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
@@ -613,6 +615,7 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     c->gslots = want;
     clear = true;
   }
+  if (!c->d_gpop) HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + 256));
   if (n_req > c->greq_cap) {
     dfree(c->d_gslot);
     c->greq_cap = 0;
@@ -651,15 +654,31 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.sizes = d_sizes;
   a.hits_out = d_hits;
   a.scratch = c->d_scratch;
-  a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, 0u, 0ull};
+  a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0u, 0u, 0ull};
   const bool probe_all = d_hits != nullptr;
   if (!probe_all && n_req <= kGroupMaxReq && pool_len < ((int64_t)1 << kGroupGenShift) - 1) {
     ps_status st = group_buffers(c, n_req, s);
     if (st != PS_OK) return st;
-    a.grp = GroupTab{c->d_gkeys, c->d_gkeys + c->gslots, c->d_grec, c->d_gslot, c->gslots - 1u,
+    a.grp = GroupTab{c->d_gkeys,
+                     c->d_gkeys + c->gslots,
+                     c->d_grec,
+                     c->d_gslot,
+                     c->d_gpop + 64,
+                     c->d_gpop,
+                     (uint32_t)(kGroupPopBytes / ((size_t)c->n_inst * sizeof(uint32_t))),
+                     c->gslots - 1u,
                      c->ggen};
   }
-  const int grid = c->hits_in_lds ? n_req : std::min(n_req, c->scratch_rows);
+  // The scoring kernel takes batches of a.batch requests per wave; a small
+  // pool's waves copy the pool's state into LDS once and take batches in
+  // turn (16 waves per CU: 4 per SIMD).  The exhaustive probe takes one
+  // request per wave.
+  a.batch = ps_score_batch(n_req, c->num_cus * 16);
+  const int batches = (n_req + a.batch - 1) / a.batch;
+  const int grid = probe_all                       ? (c->hits_in_lds ? n_req : std::min(n_req, c->scratch_rows))
+                   : ps_score_small(c->n_inst) ? std::min(batches, c->num_cus * 16)
+                   : c->hits_in_lds            ? batches
+                                               : std::min(batches, c->scratch_rows);
   hipEvent_t* ev = nullptr;
   if (c->timing && !probe_all && c->n_timed < kTimingCalls) {
     if (c->ev.size() < 3 * (size_t)(c->n_timed + 1)) {

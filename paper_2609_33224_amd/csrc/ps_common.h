@@ -45,6 +45,22 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+template <int CTRL, int RM>
+__device__ __forceinline__ void min32_step(uint32_t& v) {
+  const uint32_t t = dpp_src<CTRL, RM>(0xFFFFFFFFu, v);
+  v = t < v ? t : v;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  min32_step<0x111, 0xF>(v);
+  min32_step<0x112, 0xF>(v);
+  min32_step<0x114, 0xF>(v);
+  min32_step<0x118, 0xF>(v);
+  min32_step<0x142, 0xA>(v);
+  min32_step<0x143, 0xC>(v);
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
   add_step<0x111, 0xF>(v);
   add_step<0x112, 0xF>(v);
@@ -323,11 +339,13 @@ __device__ __forceinline__ int32_t run_compare(const ChainRef& c, const uint64_t
 
 // Walk of one instance along its row: one octet probe finds the block at
 // `pos` and its row position; the chain blocks after it are compared with
-// the row entries after it, 256 per step (4 per lane, coalesced), and the
-// first mismatch is probed again (it may begin another run of the row, e.g.
-// after a shared system prompt).  A run shorter than 8 blocks hands the rest
-// of the walk to the octet walk.  Wave-uniform arguments; returns the hit.
-template <bool STAGED>
+// the row entries after it, 256 per step (4 per lane, coalesced; W per lane
+// after the first step), and the first mismatch is probed again (it may
+// begin another run of the row, e.g. after a shared system prompt).  A run
+// shorter than 8 blocks hands the rest of the walk to the octet walk.
+// Wave-uniform arguments; returns the hit.  U0 = positions per lane in the
+// first step.
+template <bool STAGED, int W = kWalkU, int U0 = 4>
 __device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, const ChainRef& c,
                              const uint64_t* stage, int32_t pos, int g, int s) {
   const int lane = g * 8 + s;
@@ -361,16 +379,16 @@ __device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, con
     const int32_t start = pos + 1;
     int32_t q = start;
     int64_t k = rp + 1;
-    // The first step compares 4 positions per lane; a run that goes on is
-    // likely long (a session prefix), so later steps compare kWalkU per lane.
-    int32_t next = run_compare<STAGED, 4>(c, stage, row, rlen, q, k, lane);
-    q += 256;
-    k += 256;
+    // The first step compares U0 positions per lane; a run that goes on is
+    // likely long (a session prefix), so later steps compare W per lane.
+    int32_t next = run_compare<STAGED, U0>(c, stage, row, rlen, q, k, lane);
+    q += 64 * U0;
+    k += 64 * U0;
     while (next < 0) {
       if (q >= ell) return (uint32_t)ell;
-      next = run_compare<STAGED, kWalkU>(c, stage, row, rlen, q, k, lane);
-      q += 64 * kWalkU;
-      k += 64 * kWalkU;
+      next = run_compare<STAGED, W>(c, stage, row, rlen, q, k, lane);
+      q += 64 * W;
+      k += 64 * W;
     }
     if (next - start < 8) return deep_walk<STAGED>(t, inst, c, stage, next, g, s);
     pos = next;

@@ -129,12 +129,20 @@ constexpr int kGroupRec = 1 + (int)kGroupHold;  // 8-byte words per slot record
 
 constexpr uint32_t kGroupLead = 0x80000000u;  // slot_of flag of the group's leader
 constexpr uint32_t kGroupNoSlot = 0xFFFFFFFFu;
+// GroupMeta.cnt with this bit (and not kGroupNone): the group's first block
+// has more holders than a record keeps; the hits of all of them are in the
+// popular area, row (cnt & ~kGroupPop).
+constexpr uint32_t kGroupPop = 0x80000000u;
+constexpr size_t kGroupPopBytes = (size_t)64 << 20;  // popular area: hits of n_inst u32 per row
 
 struct GroupTab {
   unsigned long long* keys;  // slots; a key of another generation is an empty slot
   unsigned long long* plen;  // slots: gen << 40 | p_max (an older generation compares lower)
   uint2* rec;                // slots * kGroupRec words
   uint32_t* slot_of;         // per request: slot (| kGroupLead), or kGroupNoSlot
+  uint32_t* pop;             // popular rows: pop_cap * n_inst hits (holders' entries only)
+  uint32_t* pop_ctr;         // rows taken in this window (reset by the claim pass)
+  uint32_t pop_cap;
   uint32_t mask;             // slots - 1
   uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
 };
@@ -160,6 +168,7 @@ struct ScoreArgs {
   uint32_t* sizes;       // optional |A|,|C|,|T| per request
   uint32_t* hits_out;    // probe-all diagnostic: n_req * n_inst
   uint16_t* scratch;     // per-wave hit rows when they do not fit LDS
+  int32_t batch;         // requests per batch of the scoring kernel
 };
 
 struct CommitArgs {
@@ -245,3 +254,9 @@ hipError_t ps_launch_group(const ps::ScoreArgs& a, hipStream_t s);
 hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);
 size_t ps_seq_lds_bytes(int32_t n_inst);
 size_t ps_score_lds_bytes(int32_t n_inst);
+// Pools small enough for the scoring kernel to keep rooms, states and
+// zero-hit thresholds in LDS (it then runs a persistent grid).
+bool ps_score_small(int32_t n_inst);
+// Requests per batch of the scoring kernel (one wave loads a batch's
+// inputs together): about one batch per resident wave, at most 4.
+int32_t ps_score_batch(int32_t n_req, int32_t resident_waves);

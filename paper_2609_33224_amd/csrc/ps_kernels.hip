@@ -172,6 +172,115 @@ __global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, con
   if (threadIdx.x == 0) lm1[blockIdx.x] = (int32_t)mx - 1;
 }
 
+// Hits of the live holders (the bits of bmA, nalive of them, all holding
+// the chain's first p blocks), walked together through the prefix index:
+// eight positions per batched lookup; each position's holders (a list, or
+// a bitmap for popular hashes) intersect the live set, and an instance that
+// drops out at position pos gets put(id, pos); a single survivor continues
+// on its own row, and survivors of the whole chain get put(id, ell).  bmN
+// must be clear; both bitmaps are clear on return.  Wave-uniform arguments.
+template <bool STAGED, class Put>
+__device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c,
+                                           const uint64_t* stage, uint64_t* bmA, uint64_t* bmN,
+                                           int32_t nw, uint32_t nalive, int32_t p, Put put,
+                                           int lane, int g, int s) {
+  const int32_t ell = c.len;
+  while (p < ell && nalive > 0) {
+    if (nalive == 1) {  // a single live holder: walk its own table
+      uint32_t who = 0;
+      for (int32_t w0 = 0; w0 < nw; w0 += 64) {
+        const int32_t w = w0 + lane;
+        const uint64_t word = w < nw ? bmA[w] : 0ull;
+        const uint64_t any = __ballot(word != 0ull);
+        if (any) {
+          const int ln = __builtin_ctzll(any);
+          const uint64_t wd = __shfl(word, ln);
+          who = (uint32_t)((w0 + ln) * 64 + __builtin_ctzll(wd));
+          break;
+        }
+      }
+      const uint32_t hk = run_walk<STAGED>(a.t, who, c, stage, p, g, s);
+      if (lane == 0) {
+        put(who, hk);
+        bmA[who >> 6] = 0ull;
+      }
+      nalive = 0;
+      __syncthreads();
+      break;
+    }
+    const int32_t jq = p + g;
+    const uint64_t kq =
+      jq < ell ? ((STAGED && jq < kStage) ? stage[jq] : chain_global(c, jq)) : 0ull;
+    const IdxHit hq = index_lookup(a.x, kq, jq < ell, g, s);
+    int32_t used = 0;
+    for (int t = 0; t < 8; ++t) {
+      const int32_t pos = p + t;
+      if (pos >= ell || nalive <= 1) break;
+      const bool f = __shfl(hq.found ? 1 : 0, 8 * t) != 0;
+      const uint32_t off = __shfl(hq.off, 8 * t), cnt = __shfl(hq.cnt, 8 * t);
+      if (f && cnt > kPopular) {  // live &= holder bitmap, lane-owned words
+        const uint64_t* bm = a.x.bitmaps + (size_t)off * a.x.nw;
+        uint32_t live = 0;
+        for (int32_t w = lane; w < nw; w += 64) {
+          const uint64_t aw = bmA[w];
+          const uint64_t nwd = aw & bm[w];
+          uint64_t d = aw & ~nwd;
+          while (d) {
+            const int b = __builtin_ctzll(d);
+            d &= d - 1;
+            put((uint32_t)(w * 64 + b), (uint32_t)pos);
+          }
+          bmA[w] = nwd;
+          live += (uint32_t)__popcll(nwd);
+        }
+        nalive = wave_sum_u32(live);
+        used = t + 1;
+        continue;
+      }
+      if (f) {
+        for (uint32_t t0 = 0; t0 < cnt; t0 += 64) {
+          const uint32_t tt = t0 + lane;
+          if (tt < cnt) {
+            const uint32_t id = a.x.holders[off + tt];
+            if (test_bit(bmA, id))
+              atomicOr(reinterpret_cast<unsigned long long*>(&bmN[id >> 6]), 1ull << (id & 63));
+          }
+        }
+      }
+      __syncthreads();
+      uint32_t live = 0;
+      for (int32_t w = lane; w < nw; w += 64) {
+        const uint64_t aw = bmA[w], nwd = bmN[w];
+        uint64_t d = aw & ~nwd;
+        while (d) {
+          const int b = __builtin_ctzll(d);
+          d &= d - 1;
+          put((uint32_t)(w * 64 + b), (uint32_t)pos);
+        }
+        bmA[w] = nwd;
+        bmN[w] = 0ull;
+        live += (uint32_t)__popcll(nwd);
+      }
+      __syncthreads();
+      nalive = wave_sum_u32(live);
+      used = t + 1;
+    }
+    p += used;
+  }
+  if (nalive > 0) {  // survived to the end of the chain
+    for (int32_t w = lane; w < nw; w += 64) {
+      uint64_t d = bmA[w];
+      while (d) {
+        const int b = __builtin_ctzll(d);
+        d &= d - 1;
+        put((uint32_t)(w * 64 + b), (uint32_t)ell);
+      }
+      bmA[w] = 0ull;
+    }
+  }
+  __syncthreads();
+}
+
 // Slot of a request's prefix group.  Linear probing over the window's
 // group table; a slot whose key belongs to an older window is empty and is
 // claimed with a 64-bit compare-and-swap.  Keys of the current window never
@@ -203,6 +312,7 @@ __device__ int32_t group_claim(const GroupTab& G, int64_t pre_off, int* leader) 
 // generation-tagged lengths, so no slot needs clearing between windows).
 __global__ void group_claim_kernel(ScoreArgs a) {
   const GroupTab& G = a.grp;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *G.pop_ctr = 0u;  // read only by the walk pass
   for (int32_t r = blockIdx.x * blockDim.x + threadIdx.x; r < a.n_req;
        r += gridDim.x * blockDim.x) {
     const ps_req q = a.reqs[r];
@@ -222,10 +332,16 @@ __global__ void group_claim_kernel(ScoreArgs a) {
 
 // Prefix groups, pass 2 (one wave per request; only leaders work): the walk
 // of the group's longest segment on every holder of its first block, into
-// the slot's record.
+// the slot's record (up to kGroupHold holders, each walked on its row) or a
+// row of the popular area (more holders, walked together through the
+// prefix index).
 __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
+  const int32_t nw = (a.n_inst + 63) >> 6;
+  uint64_t* bmA = stage + kStage;
+  uint64_t* bmN = bmA + nw;
+  for (int32_t w = threadIdx.x; w < 2 * nw; w += 64) bmA[w] = 0ull;
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
   const GroupTab& G = a.grp;
@@ -247,13 +363,34 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
     uint2* rec = G.rec + (size_t)slot * kGroupRec;
     uint32_t cnt = 0u;
     if (found0 && cnt0 > kGroupHold) {
+      uint32_t row = 0;
+      if (lane == 0) row = atomicAdd(G.pop_ctr, 1u);
+      row = (uint32_t)__shfl((int)row, 0);
       cnt = kGroupNone;
+      if (row < G.pop_cap) {
+        // the live set: every holder of the first block
+        if (cnt0 > kPopular) {
+          const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
+          for (int32_t w = lane; w < nw; w += 64) bmA[w] = bm[w];
+        } else {
+          for (uint32_t t = lane; t < cnt0; t += 64) {
+            const uint32_t id = a.x.holders[off0 + t];
+            atomicOr(reinterpret_cast<unsigned long long*>(&bmA[id >> 6]), 1ull << (id & 63));
+          }
+        }
+        __syncthreads();
+        uint32_t* hp = G.pop + (size_t)row * (size_t)a.n_inst;
+        index_walk<true>(a, c, stage, bmA, bmN, nw, cnt0, 1,
+                         [&](uint32_t id, uint32_t h) { hp[id] = h; }, lane, g, s);
+        cnt = kGroupPop | row;
+      }
     } else if (found0) {
       const uint32_t id = (uint32_t)lane < cnt0 ? a.x.holders[off0 + lane] : 0u;
       uint32_t myhit = 0;
       for (uint32_t k = 0; k < cnt0; ++k) {
         const uint32_t idk = (uint32_t)__shfl((int)id, (int)k);
-        const uint32_t hk = run_walk<true>(a.t, idk, c, stage, 0, g, s);
+        // a group's segment is typically a long run: 512 positions per step
+        const uint32_t hk = run_walk<true, 8, 8>(a.t, idk, c, stage, 0, g, s);
         if ((uint32_t)lane == k) myhit = hk;
       }
       if ((uint32_t)lane < cnt0) rec[1 + lane] = make_uint2(id, myhit);
@@ -264,9 +401,32 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
 }
 
 // LDS of one scoring wave: chain stage | live bitmap | next bitmap |
-// candidate bitmap (instances holding the first block) | 64 candidate ids |
-// u16 hit slots (or device scratch for large pools).
-template <bool HITS_IN_LDS>
+// candidate bitmap (instances holding the first block) | group hits and ids
+// of up to 64 candidates | u16 hit slots (or device scratch for large
+// pools) | for pools of at most 64 instances (SMALL) the rooms, states and
+// zero-hit thresholds, copied once per launch.
+constexpr int32_t kSmallPool = 64;
+
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+constexpr int32_t kBatch = 4;  // most requests whose inputs one wave loads together
+// Bytes of the batch buffers: group records, descriptors, group slots (a
+// multiple of 16).
+constexpr size_t kBatchLds = (size_t)kBatch * (kGroupRec * 8 + 3 * 8 + 4);
+static_assert(kBatchLds % 16 == 0, "batch buffers keep the LDS layout 16-byte aligned");
+
+__host__ __device__ inline size_t score_lds_base(int32_t n_inst, bool hits_in_lds) {
+  const size_t nw = ((size_t)n_inst + 63) / 64;
+  const size_t hits = hits_in_lds ? (size_t)n_inst * sizeof(uint16_t) : 0;
+  const size_t b = (size_t)kStage * sizeof(uint64_t) + 3 * nw * sizeof(uint64_t) +
+                   64 * sizeof(uint32_t) + 64 * sizeof(uint16_t) + hits;
+  return (b + 15) / 16 * 16;
+}
+
+template <bool HITS_IN_LDS, bool SMALL>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
@@ -278,455 +438,438 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   uint32_t* ch = reinterpret_cast<uint32_t*>(bmC + nw);  // group hits of the candidates
   uint16_t* cl = reinterpret_cast<uint16_t*>(ch + 64);
   uint16_t* hits = HITS_IN_LDS ? cl + 64 : a.scratch + (size_t)blockIdx.x * (size_t)n_inst;
+  uint2* lrec = reinterpret_cast<uint2*>(smem + score_lds_base(n_inst, HITS_IN_LDS));
+  int64_t* lq64 = reinterpret_cast<int64_t*>(lrec + kBatch * kGroupRec);
+  uint32_t* lgso = reinterpret_cast<uint32_t*>(lq64 + 3 * kBatch);
+  int64_t* lroom = reinterpret_cast<int64_t*>(lgso + kBatch);
+  InstState* linst = reinterpret_cast<InstState*>(lroom + kSmallPool);
+  int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
   const DevModel& m = *a.model;
+  auto room_of = [&](uint32_t i) -> int64_t { return SMALL ? lroom[i] : a.room[i]; };
+  auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
 
   for (int32_t w = lane; w < 3 * nw; w += 64) bmA[w] = 0ull;
-
-  for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
-    const uint32_t gso = a.grp.keys ? a.grp.slot_of[r] : kGroupNoSlot;
-    const ps_req q = a.reqs[r];
-    if (!req_valid(q, a.pool_len)) {
-      if (lane == 0) {
-        a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
-        if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
-      }
-      continue;
-    }
-    const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
-    const int32_t ell = c.len;
-    const int64_t L = (int64_t)ell * m.bs;
-    const float Lf = (float)L;
-    // The group record (meta and the first 16 holders) is read with the
-    // room search's first loads; a request with a group result needs no
-    // staged chain.
-    GroupMeta gm{0, kGroupNone};
-    uint2 hd = make_uint2(0u, 0u);
-    if (gso != kGroupNoSlot) {
-      const uint2* grec = a.grp.rec + (size_t)(gso & ~kGroupLead) * kGroupRec;
-      const uint2 m0 = grec[0];
-      if ((uint32_t)lane < kGroupHold) hd = grec[1 + lane];
-      gm = GroupMeta{(int32_t)m0.x, m0.y};
-    }
-    const bool grp = gm.cnt != kGroupNone;
-    const int32_t nst = grp ? 0 : (ell < kStage ? ell : kStage);
-    // The chain head's loads and the room search's are in flight together.
-    uint64_t sv[kStage / 64];
-#pragma unroll
-    for (int u = 0; u < kStage / 64; ++u) {
-      const int32_t j = lane + 64 * u;
-      sv[u] = j < nst ? chain_global(c, j) : 0ull;
-    }
-    // |A|: capacity-eligible instances are those with room >= L.
-    const uint32_t nA = (uint32_t)(n_inst - wave_lower_bound(a.room_sorted, n_inst, L, lane));
-    if (!grp) {
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < kStage / 64; ++u) {
-        const int32_t j = lane + 64 * u;
-        if (j < nst) stage[j] = sv[u];
-      }
-      __syncthreads();
-    }
-
-    // (1) Holders of the first block among the eligible instances.
-    uint32_t nCand = 0;
-    if (grp) {  // from the group record: ids and hits of the shared segment
-      const bool el = nA > 0 && (uint32_t)lane < gm.cnt && a.room[hd.x] >= L;
-      const uint64_t em = __ballot(el);
-      const uint32_t rank = (uint32_t)__popcll(em & lt_mask);
-      if (el) {
-        cl[rank] = (uint16_t)hd.x;
-        ch[rank] = hd.y;
-        atomicOr(reinterpret_cast<unsigned long long*>(&bmC[hd.x >> 6]), 1ull << (hd.x & 63));
-      }
-      nCand = (uint32_t)__popcll(em);
-    } else if (nA > 0 && ell > 0) {
-      const IdxHit h0 = index_lookup(a.x, stage[0], g == 0, g, s);
-      const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
-      const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
-      if (found0 && cnt0 > kPopular) {  // holders as a bitmap: lanes over its words
-        const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
-        for (int32_t w0 = 0; w0 < nw; w0 += 64) {
-          const int32_t w = w0 + lane;
-          uint64_t d = w < nw ? bm[w] : 0ull, el_bits = 0ull;
-          while (d) {
-            const int b = __builtin_ctzll(d);
-            d &= d - 1;
-            if (a.room[w * 64 + b] >= L) el_bits |= 1ull << b;
-          }
-          const uint32_t cntl = (uint32_t)__popcll(el_bits);
-          uint32_t rank = nCand + wave_exclusive_sum(cntl, lane);
-          if (w < nw) bmC[w] = el_bits;
-          uint64_t e2 = el_bits;
-          while (e2 && rank < 64) {
-            const int b = __builtin_ctzll(e2);
-            e2 &= e2 - 1;
-            cl[rank++] = (uint16_t)(w * 64 + b);
-          }
-          nCand += wave_sum_u32(cntl);
-        }
-      } else if (found0) {
-        for (uint32_t t0 = 0; t0 < cnt0; t0 += 64) {
-          const uint32_t t = t0 + lane;
-          const uint32_t id = t < cnt0 ? a.x.holders[off0 + t] : 0u;
-          const bool el = t < cnt0 && a.room[id] >= L;
-          const uint64_t em = __ballot(el);
-          const uint32_t rank = nCand + (uint32_t)__popcll(em & lt_mask);
-          if (el) {
-            if (rank < 64) cl[rank] = (uint16_t)id;
-            atomicOr(reinterpret_cast<unsigned long long*>(&bmC[id >> 6]), 1ull << (id & 63));
-          }
-          nCand += (uint32_t)__popcll(em);
-        }
-      }
+  if (SMALL) {
+    if (lane < n_inst) {
+      lroom[lane] = a.room[lane];
+      linst[lane] = a.inst[lane];
+      llm[lane] = a.lm[lane];
     }
     __syncthreads();
-    const bool few = nCand <= 64;
+  }
 
-    // Walks.  few: each holder on its own table; else: all live holders
-    // through the index, one position at a time.
-    uint32_t myid = 0, myhit = 0;
-    if (few && grp) {
-      // Hit H of the shared segment: exact below the request's segment
-      // length p; otherwise the walk resumes on its own chain at p.
-      const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
-      if ((uint32_t)lane < nCand) {
-        myid = cl[lane];
-        myhit = ch[lane];
+  // Requests are taken in batches of a.batch (<= kBatch) consecutive ones: their
+  // descriptors and group slots arrive with one round trip, their group
+  // records with a second, into LDS; then each is scored from there.
+  const int32_t B = a.batch;
+  for (int32_t rb = blockIdx.x * B; rb < a.n_req; rb += gridDim.x * B) {
+    const int32_t nb = a.n_req - rb < B ? a.n_req - rb : B;
+    __syncthreads();  // the previous batch is done with the batch buffers
+    if (lane < nb) lgso[lane] = a.grp.keys ? a.grp.slot_of[rb + lane] : kGroupNoSlot;
+    if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rb)[lane];
+    __syncthreads();
+    for (int32_t w = lane; w < nb * kGroupRec; w += 64) {
+      const uint32_t so = lgso[w / kGroupRec];
+      if (so != kGroupNoSlot)
+        lrec[w] = a.grp.rec[(size_t)(so & ~kGroupLead) * kGroupRec + (uint32_t)(w % kGroupRec)];
+    }
+    __syncthreads();
+    for (int32_t b = 0; b < nb; ++b) {
+      const int32_t r = rb + b;
+      // wave-uniform values read from LDS are moved to scalar registers
+      const uint32_t gso = (uint32_t)__builtin_amdgcn_readfirstlane((int)lgso[b]);
+      const ps_req ql = reinterpret_cast<const ps_req*>(lq64)[b];
+      const ps_req q{uniform64(ql.pre_off), uniform64(ql.tail_off),
+                     __builtin_amdgcn_readfirstlane(ql.pre_len),
+                     __builtin_amdgcn_readfirstlane(ql.tail_len)};
+      if (!req_valid(q, a.pool_len)) {
+        if (lane == 0) {
+          a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
+          if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+        }
+        continue;
       }
-      uint64_t need = __ballot((uint32_t)lane < nCand && (int32_t)myhit >= p0);
-      while (need) {
-        const int k = __builtin_ctzll(need);
-        need &= need - 1;
-        const uint32_t id = (uint32_t)__shfl((int)myid, k);
-        const uint32_t hk = run_walk<false>(a.t, id, c, nullptr, p0, g, s);
-        if (lane == k) myhit = hk;
+      const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
+      const int32_t ell = c.len;
+      const int64_t L = (int64_t)ell * m.bs;
+      const float Lf = (float)L;
+      // The group record (meta and up to 16 holders); a request with a
+      // group result needs no staged chain.
+      GroupMeta gm{0, kGroupNone};
+      uint2 hd = make_uint2(0u, 0u);
+      if (gso != kGroupNoSlot) {
+        const uint2* grec = lrec + b * kGroupRec;
+        const uint2 m0 = grec[0];
+        if ((uint32_t)lane < kGroupHold) hd = grec[1 + lane];
+        gm = GroupMeta{__builtin_amdgcn_readfirstlane((int)m0.x),
+                       (uint32_t)__builtin_amdgcn_readfirstlane((int)m0.y)};
       }
-      if ((uint32_t)lane < nCand) hits[myid] = encode_hit(myhit);
-    } else if (few) {
-      if ((uint32_t)lane < nCand) myid = cl[lane];
-      for (uint32_t k = 0; k < nCand; ++k) {
-        const uint32_t id = (uint32_t)__shfl((int)myid, (int)k);
-        const uint32_t hk = ell > 1 ? run_walk<true>(a.t, id, c, stage, 0, g, s) : 1u;
-        if ((uint32_t)lane == k) myhit = hk;
+      const bool grp = gm.cnt != kGroupNone;
+      const bool gpop = grp && (gm.cnt & kGroupPop) != 0u;  // holders from the index
+      const int32_t nst = grp ? 0 : (ell < kStage ? ell : kStage);
+      // The chain head's loads and the room search's are in flight together.
+      uint64_t sv[kStage / 64];
+  #pragma unroll
+      for (int u = 0; u < kStage / 64; ++u) {
+        const int32_t j = lane + 64 * u;
+        sv[u] = j < nst ? chain_global(c, j) : 0ull;
       }
-      if ((uint32_t)lane < nCand) hits[myid] = encode_hit(myhit);
-    } else {
-      for (int32_t w = lane; w < nw; w += 64) bmA[w] = bmC[w];
-      __syncthreads();
-      uint32_t nalive = nCand;
-      int32_t p = 1;
-      while (p < ell && nalive > 0) {
-        if (nalive == 1) {  // a single live holder: walk its own table
-          uint32_t who = 0;
+      // |A|: capacity-eligible instances are those with room >= L.
+      const uint32_t nA =
+          SMALL ? (uint32_t)__popcll(__ballot(lane < n_inst && lroom[lane] >= L))
+                : (uint32_t)(n_inst - wave_lower_bound(a.room_sorted, n_inst, L, lane));
+      if (!grp) {
+        __syncthreads();
+  #pragma unroll
+        for (int u = 0; u < kStage / 64; ++u) {
+          const int32_t j = lane + 64 * u;
+          if (j < nst) stage[j] = sv[u];
+        }
+        __syncthreads();
+      }
+
+      // (1) Holders of the first block among the eligible instances.
+      uint32_t nCand = 0;
+      if (grp && !gpop) {  // from the group record: ids and hits of the shared segment
+        const bool el = nA > 0 && (uint32_t)lane < gm.cnt && room_of(hd.x) >= L;
+        const uint64_t em = __ballot(el);
+        const uint32_t rank = (uint32_t)__popcll(em & lt_mask);
+        if (el) {
+          cl[rank] = (uint16_t)hd.x;
+          ch[rank] = hd.y;
+          atomicOr(reinterpret_cast<unsigned long long*>(&bmC[hd.x >> 6]), 1ull << (hd.x & 63));
+        }
+        nCand = (uint32_t)__popcll(em);
+      } else if (nA > 0 && ell > 0) {
+        const IdxHit h0 = index_lookup(a.x, grp ? c.pre[0] : stage[0], g == 0, g, s);
+        const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
+        const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
+        if (found0 && cnt0 > kPopular) {  // holders as a bitmap: lanes over its words
+          const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
           for (int32_t w0 = 0; w0 < nw; w0 += 64) {
             const int32_t w = w0 + lane;
-            const uint64_t word = w < nw ? bmA[w] : 0ull;
-            const uint64_t any = __ballot(word != 0ull);
-            if (any) {
-              const int ln = __builtin_ctzll(any);
-              const uint64_t wd = __shfl(word, ln);
-              who = (uint32_t)((w0 + ln) * 64 + __builtin_ctzll(wd));
-              break;
-            }
-          }
-          const uint32_t hk = run_walk<true>(a.t, who, c, stage, p, g, s);
-          if (lane == 0) {
-            hits[who] = encode_hit(hk);
-            bmA[who >> 6] = 0ull;
-          }
-          nalive = 0;
-          __syncthreads();
-          break;
-        }
-        const int32_t jq = p + g;
-        const uint64_t kq = jq < ell ? ((jq < kStage) ? stage[jq] : chain_global(c, jq)) : 0ull;
-        const IdxHit hq = index_lookup(a.x, kq, jq < ell, g, s);
-        int32_t used = 0;
-        for (int t = 0; t < 8; ++t) {
-          const int32_t pos = p + t;
-          if (pos >= ell || nalive <= 1) break;
-          const bool f = __shfl(hq.found ? 1 : 0, 8 * t) != 0;
-          const uint32_t off = __shfl(hq.off, 8 * t), cnt = __shfl(hq.cnt, 8 * t);
-          if (f && cnt > kPopular) {  // live &= holder bitmap, lane-owned words
-            const uint64_t* bm = a.x.bitmaps + (size_t)off * a.x.nw;
-            uint32_t live = 0;
-            for (int32_t w = lane; w < nw; w += 64) {
-              const uint64_t aw = bmA[w];
-              const uint64_t nwd = aw & bm[w];
-              uint64_t d = aw & ~nwd;
-              while (d) {
-                const int b = __builtin_ctzll(d);
-                d &= d - 1;
-                hits[w * 64 + b] = encode_hit((uint32_t)pos);
-              }
-              bmA[w] = nwd;
-              live += (uint32_t)__popcll(nwd);
-            }
-            nalive = wave_sum_u32(live);
-            used = t + 1;
-            continue;
-          }
-          if (f) {
-            for (uint32_t t0 = 0; t0 < cnt; t0 += 64) {
-              const uint32_t tt = t0 + lane;
-              if (tt < cnt) {
-                const uint32_t id = a.x.holders[off + tt];
-                if (test_bit(bmA, id))
-                  atomicOr(reinterpret_cast<unsigned long long*>(&bmN[id >> 6]), 1ull << (id & 63));
-              }
-            }
-          }
-          __syncthreads();
-          uint32_t live = 0;
-          for (int32_t w = lane; w < nw; w += 64) {
-            const uint64_t aw = bmA[w], nwd = bmN[w];
-            uint64_t d = aw & ~nwd;
+            uint64_t d = w < nw ? bm[w] : 0ull, el_bits = 0ull;
             while (d) {
               const int b = __builtin_ctzll(d);
               d &= d - 1;
-              hits[w * 64 + b] = encode_hit((uint32_t)pos);
+              if (room_of((uint32_t)(w * 64 + b)) >= L) el_bits |= 1ull << b;
             }
-            bmA[w] = nwd;
-            bmN[w] = 0ull;
-            live += (uint32_t)__popcll(nwd);
+            const uint32_t cntl = (uint32_t)__popcll(el_bits);
+            uint32_t rank = nCand + wave_exclusive_sum(cntl, lane);
+            if (w < nw) bmC[w] = el_bits;
+            uint64_t e2 = el_bits;
+            while (e2 && rank < 64) {
+              const int b = __builtin_ctzll(e2);
+              e2 &= e2 - 1;
+              cl[rank++] = (uint16_t)(w * 64 + b);
+            }
+            nCand += wave_sum_u32(cntl);
           }
-          __syncthreads();
-          nalive = wave_sum_u32(live);
-          used = t + 1;
-        }
-        p += used;
-      }
-      if (nalive > 0) {  // survived to the end of the chain
-        for (int32_t w = lane; w < nw; w += 64) {
-          uint64_t d = bmA[w];
-          while (d) {
-            const int b = __builtin_ctzll(d);
-            d &= d - 1;
-            hits[w * 64 + b] = encode_hit((uint32_t)ell);
+        } else if (found0) {
+          for (uint32_t t0 = 0; t0 < cnt0; t0 += 64) {
+            const uint32_t t = t0 + lane;
+            const uint32_t id = t < cnt0 ? a.x.holders[off0 + t] : 0u;
+            const bool el = t < cnt0 && room_of(id) >= L;
+            const uint64_t em = __ballot(el);
+            const uint32_t rank = nCand + (uint32_t)__popcll(em & lt_mask);
+            if (el) {
+              if (rank < 64) cl[rank] = (uint16_t)id;
+              atomicOr(reinterpret_cast<unsigned long long*>(&bmC[id >> 6]), 1ull << (id & 63));
+            }
+            nCand += (uint32_t)__popcll(em);
           }
-          bmA[w] = 0ull;
         }
       }
       __syncthreads();
-    }
+      const bool few = nCand <= 64;
 
-    // (2)-(3) Minimum recomputation penalty over A.  Every eligible
-    // non-holder has hit 0 and the penalty W(n = L).
-    const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
-    const float W0 = fmaxf(0.0f, Z);
-    const uint32_t n0 = nA - nCand;
-    uint32_t wmin_bits = n0 > 0 ? __float_as_uint(W0) : 0x7F800000u;
-    if (few) {
-      if ((uint32_t)lane < nCand) {
-        const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)myhit * m.bs), Lf));
-        const uint32_t wb = __float_as_uint(W);
-        wmin_bits = wb < wmin_bits ? wb : wmin_bits;
-      }
-    } else {
-      for (int32_t base = 0; base < n_inst; base += 64) {
-        const int32_t i = base + lane;
-        const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
-        uint32_t v = cand ? hits[i] : 0u;
-        uint64_t ovf = __ballot(cand && v == kHitOverflow);
-        while (ovf) {  // hits beyond the u16 slot: walk again
-          const int k = __builtin_ctzll(ovf);
-          ovf &= ovf - 1;
-          const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
-          if (lane == k) v = hk;
+      // Walks.  few: each holder on its own table; else: all live holders
+      // through the index, one position at a time.
+      uint32_t myid = 0, myhit = 0;
+      if (few && grp) {
+        // Hit H of the shared segment: exact below the request's segment
+        // length p; otherwise the walk resumes on its own chain at p.
+        const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
+        if ((uint32_t)lane < nCand) {
+          myid = cl[lane];
+          myhit = gpop ? a.grp.pop[(size_t)(gm.cnt & ~kGroupPop) * (size_t)n_inst + myid] : ch[lane];
         }
-        if (cand) {
-          const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)v * m.bs), Lf));
+        uint64_t need = __ballot((uint32_t)lane < nCand && (int32_t)myhit >= p0);
+        while (need) {
+          const int k = __builtin_ctzll(need);
+          need &= need - 1;
+          const uint32_t id = (uint32_t)__shfl((int)myid, k);
+          const uint32_t hk = run_walk<false>(a.t, id, c, nullptr, p0, g, s);
+          if (lane == k) myhit = hk;
+        }
+        if ((uint32_t)lane < nCand) hits[myid] = encode_hit(myhit);
+      } else if (few) {
+        if ((uint32_t)lane < nCand) myid = cl[lane];
+        for (uint32_t k = 0; k < nCand; ++k) {
+          const uint32_t id = (uint32_t)__shfl((int)myid, (int)k);
+          const uint32_t hk = ell > 1 ? run_walk<true>(a.t, id, c, stage, 0, g, s) : 1u;
+          if ((uint32_t)lane == k) myhit = hk;
+        }
+        if ((uint32_t)lane < nCand) hits[myid] = encode_hit(myhit);
+      } else if (!grp) {
+        for (int32_t w = lane; w < nw; w += 64) bmA[w] = bmC[w];
+        __syncthreads();
+        index_walk<true>(a, c, stage, bmA, bmN, nw, nCand, 1,
+                         [&](uint32_t id, uint32_t h) { hits[id] = encode_hit(h); }, lane, g, s);
+      } else {
+        // many candidates with a popular group's result: lanes over the
+        // pool, resumes walked one at a time
+        const uint32_t* hp = a.grp.pop + (size_t)(gm.cnt & ~kGroupPop) * (size_t)n_inst;
+        const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
+        for (int32_t base = 0; base < n_inst; base += 64) {
+          const int32_t i = base + lane;
+          const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
+          uint32_t v = cand ? hp[i] : 0u;
+          uint64_t need = __ballot(cand && (int32_t)v >= p0);
+          while (need) {
+            const int k = __builtin_ctzll(need);
+            need &= need - 1;
+            const uint32_t hk = run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, p0, g, s);
+            if (lane == k) v = hk;
+          }
+          if (cand) hits[i] = encode_hit(v);
+        }
+        __syncthreads();
+      }
+
+      // (2)-(3) Minimum recomputation penalty over A.  Every eligible
+      // non-holder has hit 0 and the penalty W(n = L).
+      const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
+      const float W0 = fmaxf(0.0f, Z);
+      const uint32_t n0 = nA - nCand;
+      uint32_t wmin_bits = n0 > 0 ? __float_as_uint(W0) : 0x7F800000u;
+      if (few) {
+        if ((uint32_t)lane < nCand) {
+          const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)myhit * m.bs), Lf));
           const uint32_t wb = __float_as_uint(W);
           wmin_bits = wb < wmin_bits ? wb : wmin_bits;
         }
-      }
-    }
-    const float wmin = __uint_as_float((uint32_t)wave_min_u64((uint64_t)wmin_bits));
-
-    // (3)-(4) Filters and keys.  The hit-0 class is visited only if its
-    // common penalty passes Eq. 9.
-    const float tpf_cold = t_prefill(m, Lf, 0.0f);
-    const float slo = fmaxf(m.ttft_floor, tpf_cold);
-    const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
-    const bool admit0 = n0 > 0 && (!kvc || (W0 - wmin) / Z <= m.eta);
-    Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
-    if (nA > 0) {
-      if (few) {
-        if ((uint32_t)lane < nCand) evaluate(a, m, acc, myid, myhit, L, Lf, wmin, Z, kvc, slo);
       } else {
         for (int32_t base = 0; base < n_inst; base += 64) {
           const int32_t i = base + lane;
           const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
           uint32_t v = cand ? hits[i] : 0u;
           uint64_t ovf = __ballot(cand && v == kHitOverflow);
-          while (ovf) {
+          while (ovf) {  // hits beyond the u16 slot: walk again
             const int k = __builtin_ctzll(ovf);
             ovf &= ovf - 1;
-            const uint32_t hk = run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+            const uint32_t hk =
+                grp ? run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, 0, g, s)
+                    : run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
             if (lane == k) v = hk;
           }
-          if (cand) evaluate(a, m, acc, (uint32_t)i, v, L, Lf, wmin, Z, kvc, slo);
+          if (cand) {
+            const float W = fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)v * m.bs), Lf));
+            const uint32_t wb = __float_as_uint(W);
+            wmin_bits = wb < wmin_bits ? wb : wmin_bits;
+          }
         }
       }
-      if (admit0) {
-        // The eligible non-holders (hit 0) share n = L.  Without set sizes
-        // to report, only the best packing key of that class matters: the
-        // first member of T in key order (decoding desc, queued asc, id
-        // asc).  The whole class is evaluated when sizes are requested or
-        // when no member is in T (then the fallback key may come from it).
-        bool done0 = false;
-        const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
-        if (!a.sizes && keyed && m.mono && !(m.flags & PS_F_TTFT_ADMIT)) {
-          // The first member of T in key order: the first key position whose
-          // threshold admits this length and whose instance does not hold
-          // the first block.  Chunk maxima skip 64 positions per entry.
-          const int32_t n1 = (n_inst + 63) >> 6;
-          for (int32_t c0 = 0; c0 < n1 && !done0; c0 += 64) {
-            const int32_t cc = c0 + lane;
-            uint64_t cm = __ballot(cc < n1 && a.lm1[cc] >= ell);
-            while (cm && !done0) {
-              const int32_t k0 = (c0 + __builtin_ctzll(cm)) * 64;
-              cm &= cm - 1;
-              const int32_t k = k0 + lane;
-              const int4 e = k < n_inst ? a.lm[k] : make_int4(-1, 0, 0, 0);
-              const uint64_t om = __ballot(e.x >= ell && !test_bit(bmC, (uint32_t)e.y));
-              if (om) {
-                if (lane == __builtin_ctzll(om)) {
-                  InstState st{};
-                  st.D = e.z;
-                  st.Q = e.w;
-                  const uint64_t kt = select_key(m.sel, st, 0u, (uint32_t)e.y, 0ull);
+      const float wmin = __uint_as_float(wave_min_u32(wmin_bits));
+
+      // (3)-(4) Filters and keys.  The hit-0 class is visited only if its
+      // common penalty passes Eq. 9.
+      const float tpf_cold = t_prefill(m, Lf, 0.0f);
+      const float slo = fmaxf(m.ttft_floor, tpf_cold);
+      const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+      const bool admit0 = n0 > 0 && (!kvc || (W0 - wmin) / Z <= m.eta);
+      Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
+      if (nA > 0) {
+        if (few) {
+          if ((uint32_t)lane < nCand)
+            evaluate_with(m, acc, myid, myhit, [&]() { return state_of(myid); }, L, Lf, wmin, Z, kvc,
+                          slo);
+        } else {
+          for (int32_t base = 0; base < n_inst; base += 64) {
+            const int32_t i = base + lane;
+            const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
+            uint32_t v = cand ? hits[i] : 0u;
+            uint64_t ovf = __ballot(cand && v == kHitOverflow);
+            while (ovf) {
+              const int k = __builtin_ctzll(ovf);
+              ovf &= ovf - 1;
+              const uint32_t hk =
+                  grp ? run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, 0, g, s)
+                      : run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+              if (lane == k) v = hk;
+            }
+            if (cand)
+              evaluate_with(m, acc, (uint32_t)i, v, [&]() { return state_of((uint32_t)i); }, L, Lf,
+                            wmin, Z, kvc, slo);
+          }
+        }
+        if (admit0) {
+          // The eligible non-holders (hit 0) share n = L.  Without set sizes
+          // to report, only the best packing key of that class matters: the
+          // first member of T in key order (decoding desc, queued asc, id
+          // asc).  The whole class is evaluated when sizes are requested or
+          // when no member is in T (then the fallback key may come from it).
+          bool done0 = false;
+          const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
+          if (!a.sizes && keyed && m.mono && !(m.flags & PS_F_TTFT_ADMIT)) {
+            // The first member of T in key order: the first key position whose
+            // threshold admits this length and whose instance does not hold
+            // the first block.  Chunk maxima skip 64 positions per entry.
+            const int32_t n1 = (n_inst + 63) >> 6;
+            for (int32_t c0 = 0; c0 < n1 && !done0; c0 += 64) {
+              const int32_t cc = c0 + lane;
+              uint64_t cm = __ballot(cc < n1 && (SMALL || a.lm1[cc] >= ell));
+              while (cm && !done0) {
+                const int32_t k0 = (c0 + __builtin_ctzll(cm)) * 64;
+                cm &= cm - 1;
+                const int32_t k = k0 + lane;
+                const int4 e = k < n_inst ? (SMALL ? llm[k] : a.lm[k]) : make_int4(-1, 0, 0, 0);
+                const uint64_t om = __ballot(e.x >= ell && !test_bit(bmC, (uint32_t)e.y));
+                if (om) {
+                  if (lane == __builtin_ctzll(om)) {
+                    InstState st{};
+                    st.D = e.z;
+                    st.Q = e.w;
+                    const uint64_t kt = select_key(m.sel, st, 0u, (uint32_t)e.y, 0ull);
+                    acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                  }
+                  done0 = true;
+                }
+              }
+            }
+          } else if (!a.sizes && keyed) {
+            for (int32_t base = 0; base < n_inst && !done0; base += 64) {
+              const int32_t k = base + lane;
+              bool ok = false;
+              uint32_t i = 0;
+              InstState st{};
+              if (k < n_inst) {
+                i = a.order0[k];
+                st = a.inst_key[k];  // contiguous, loaded with the id
+                if (eligible(m, st.A1, st.S, L) && !test_bit(bmC, i)) {
+                  const Lat lt = latency(m, st, Lf, 0.0f, L);
+                  ok = ((m.flags & PS_F_NO_TPOT_FILTER) || lt.tpot < m.tau) &&
+                       (!(m.flags & PS_F_TTFT_ADMIT) || lt.ttft <= slo);
+                }
+              }
+              const uint64_t okm = __ballot(ok);
+              if (okm) {
+                if (lane == __builtin_ctzll(okm)) {
+                  const uint64_t kt = select_key(m.sel, st, 0u, i, 0ull);
                   acc.keyT = kt < acc.keyT ? kt : acc.keyT;
                 }
                 done0 = true;
               }
             }
           }
-        } else if (!a.sizes && keyed) {
-          for (int32_t base = 0; base < n_inst && !done0; base += 64) {
-            const int32_t k = base + lane;
-            bool ok = false;
-            uint32_t i = 0;
-            InstState st{};
-            if (k < n_inst) {
-              i = a.order0[k];
-              st = a.inst_key[k];  // contiguous, loaded with the id
-              if (eligible(m, st.A1, st.S, L) && !test_bit(bmC, i)) {
-                const Lat lt = latency(m, st, Lf, 0.0f, L);
-                ok = ((m.flags & PS_F_NO_TPOT_FILTER) || lt.tpot < m.tau) &&
-                     (!(m.flags & PS_F_TTFT_ADMIT) || lt.ttft <= slo);
-              }
-            }
-            const uint64_t okm = __ballot(ok);
-            if (okm) {
-              if (lane == __builtin_ctzll(okm)) {
-                const uint64_t kt = select_key(m.sel, st, 0u, i, 0ull);
-                acc.keyT = kt < acc.keyT ? kt : acc.keyT;
-              }
-              done0 = true;
+          // No member of the class is in T: its keys matter only for the
+          // fallback, i.e. when no candidate is in T either.
+          if (!done0 && !a.sizes && keyed) done0 = wave_min_u64(acc.keyT) != ~0ull;
+          if (!done0) {
+            for (int32_t base = 0; base < n_inst; base += 64) {
+              const int32_t i = base + lane;
+              if (i < n_inst && !test_bit(bmC, (uint32_t)i) && room_of((uint32_t)i) >= L)
+                evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return state_of((uint32_t)i); }, L, Lf,
+                              wmin, Z, kvc, slo);
             }
           }
         }
-        // No member of the class is in T: its keys matter only for the
-        // fallback, i.e. when no candidate is in T either.
-        if (!done0 && !a.sizes && keyed) done0 = wave_min_u64(acc.keyT) != ~0ull;
-        if (!done0) {
-          for (int32_t base = 0; base < n_inst; base += 64) {
-            const int32_t i = base + lane;
-            if (i < n_inst && !test_bit(bmC, (uint32_t)i) && a.room[i] >= L)
-              evaluate(a, m, acc, (uint32_t)i, 0u, L, Lf, wmin, Z, kvc, slo);
-          }
-        }
       }
-    }
-    uint64_t keyT;
-    if (m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
-      const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
-      keyT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
-    } else {
-      keyT = wave_min_u64(acc.keyT);
-    }
-    const uint64_t keyF = wave_min_u64(acc.keyF);
-    const uint32_t nC = wave_sum_u32(acc.nC);
-    const uint32_t nT = wave_sum_u32(acc.nT);
-    if (m.sel == PS_SEL_RANDOM && nT > 0) {
-      // the k-th member of T in id order
-      const uint64_t z = splitmix64_at(m.rand_seed, r);
-      const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
-      uint32_t seen = 0;
-      for (int32_t base = 0; base < n_inst; base += 64) {
-        const int32_t i = base + lane;
-        const bool el = i < n_inst && a.room[i] >= L;
-        const bool cand = el && test_bit(bmC, (uint32_t)i);
-        uint32_t v = cand ? hits[i] : 0u;
-        uint64_t ovf = __ballot(cand && v == kHitOverflow);
-        while (ovf) {
-          const int k = __builtin_ctzll(ovf);
-          ovf &= ovf - 1;
-          const uint32_t hk = grp ? run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, 0, g, s)
-                                  : run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
-          if (lane == k) v = hk;
-        }
-        bool inT = false;
-        if (el && (cand || admit0)) inT = member(a, m, (uint32_t)i, v, L, Lf, wmin, Z, kvc, slo).inT;
-        uint64_t mm = __ballot(inT);
-        const uint32_t cnt = (uint32_t)__popcll(mm);
-        if (seen + cnt > kth) {
-          for (uint32_t j = seen; j < kth; ++j) mm &= mm - 1;
-          keyT = (uint64_t)(base + __builtin_ctzll(mm));
-          break;
-        }
-        seen += cnt;
-      }
-    }
-
-    // Decision.  With finite arithmetic C holds at least the minimum-penalty
-    // candidate whenever A is non-empty; the key test only keeps a
-    // non-finite model from selecting an out-of-range id.
-    ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
-    if (nA > 0 && (keyT != ~0ull || keyF != ~0ull)) {
-      uint32_t fl = 0;
-      uint32_t best;
-      if (keyT != ~0ull) {
-        best = (uint32_t)(keyT & 0xFFFFu);
+      uint64_t keyT;
+      if (m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
+        const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
+        keyT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
       } else {
-        best = (uint32_t)(keyF & 0xFFFFu);
-        fl |= PS_R_FALLBACK;
+        keyT = wave_min_u64(acc.keyT);
       }
-      uint32_t v = 0;
-      if (test_bit(bmC, best)) {
-        if (few) {
-          const uint64_t mk = __ballot((uint32_t)lane < nCand && myid == best);
-          v = (uint32_t)__shfl((int)myhit, __builtin_ctzll(mk));
-        } else {
-          v = hits[best];
-          if (v == kHitOverflow) v = run_walk<true>(a.t, best, c, stage, 0, g, s);
+      // the fallback key matters only when T is empty; the set sizes only
+      // when reported or for the random selector
+      const uint64_t keyF = keyT == ~0ull ? wave_min_u64(acc.keyF) : ~0ull;
+      const bool counts = a.sizes || m.sel == PS_SEL_RANDOM;
+      const uint32_t nC = counts ? wave_sum_u32(acc.nC) : 0u;
+      const uint32_t nT = counts ? wave_sum_u32(acc.nT) : 0u;
+      if (m.sel == PS_SEL_RANDOM && nT > 0) {
+        // the k-th member of T in id order
+        const uint64_t z = splitmix64_at(m.rand_seed, r);
+        const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
+        uint32_t seen = 0;
+        for (int32_t base = 0; base < n_inst; base += 64) {
+          const int32_t i = base + lane;
+          const bool el = i < n_inst && room_of((uint32_t)i) >= L;
+          const bool cand = el && test_bit(bmC, (uint32_t)i);
+          uint32_t v = cand ? hits[i] : 0u;
+          uint64_t ovf = __ballot(cand && v == kHitOverflow);
+          while (ovf) {
+            const int k = __builtin_ctzll(ovf);
+            ovf &= ovf - 1;
+            const uint32_t hk = grp ? run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, 0, g, s)
+                                    : run_walk<true>(a.t, (uint32_t)(base + k), c, stage, 0, g, s);
+            if (lane == k) v = hk;
+          }
+          bool inT = false;
+          if (el && (cand || admit0))
+            inT = member_with(m, [&]() { return state_of((uint32_t)i); }, v, L, Lf, wmin, Z, kvc, slo)
+                      .inT;
+          uint64_t mm = __ballot(inT);
+          const uint32_t cnt = (uint32_t)__popcll(mm);
+          if (seen + cnt > kth) {
+            for (uint32_t j = seen; j < kth; ++j) mm &= mm - 1;
+            keyT = (uint64_t)(base + __builtin_ctzll(mm));
+            break;
+          }
+          seen += cnt;
         }
       }
-      const int64_t c_tok = (int64_t)v * m.bs;
-      const InstState st = a.inst[best];
-      const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
-      if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
-      res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot, fl};
-    }
-    if (lane == 0) {
-      a.out[r] = res;
-      if (a.sizes) {
-        a.sizes[3 * (size_t)r] = nA;
-        a.sizes[3 * (size_t)r + 1] = nC;
-        a.sizes[3 * (size_t)r + 2] = nT;
+
+      // Decision.  With finite arithmetic C holds at least the minimum-penalty
+      // candidate whenever A is non-empty; the key test only keeps a
+      // non-finite model from selecting an out-of-range id.
+      ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+      if (nA > 0 && (keyT != ~0ull || keyF != ~0ull)) {
+        uint32_t fl = 0;
+        uint32_t best;
+        if (keyT != ~0ull) {
+          best = (uint32_t)(keyT & 0xFFFFu);
+        } else {
+          best = (uint32_t)(keyF & 0xFFFFu);
+          fl |= PS_R_FALLBACK;
+        }
+        uint32_t v = 0;
+        if (test_bit(bmC, best)) {
+          if (few) {
+            const uint64_t mk = __ballot((uint32_t)lane < nCand && myid == best);
+            v = (uint32_t)__shfl((int)myhit, __builtin_ctzll(mk));
+          } else {
+            v = hits[best];
+            if (v == kHitOverflow)
+              v = grp ? run_walk<false>(a.t, best, c, nullptr, 0, g, s)
+                      : run_walk<true>(a.t, best, c, stage, 0, g, s);
+          }
+        }
+        const int64_t c_tok = (int64_t)v * m.bs;
+        const InstState st = state_of(best);
+        const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
+        if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
+        res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot, fl};
       }
-    }
-    // leave the candidate bitmap clear for the next request
-    __syncthreads();
-    if (few) {
-      if ((uint32_t)lane < nCand) bmC[myid >> 6] = 0ull;
-    } else {
-      for (int32_t w = lane; w < nw; w += 64) bmC[w] = 0ull;
+      if (lane == 0) {
+        a.out[r] = res;
+        if (a.sizes) {
+          a.sizes[3 * (size_t)r] = nA;
+          a.sizes[3 * (size_t)r + 1] = nC;
+          a.sizes[3 * (size_t)r + 2] = nT;
+        }
+      }
+      // leave the candidate bitmap clear for the next request
+      __syncthreads();
+      if (few) {
+        if ((uint32_t)lane < nCand) bmC[myid >> 6] = 0ull;
+      } else {
+        for (int32_t w = lane; w < nw; w += 64) bmC[w] = 0ull;
+      }
     }
   }
 }
@@ -795,11 +938,18 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
+bool ps_score_small(int32_t n_inst) { return n_inst <= kSmallPool; }
+
+int32_t ps_score_batch(int32_t n_req, int32_t resident_waves) {
+  const int32_t b = resident_waves > 0 ? n_req / resident_waves : 1;
+  return b < 1 ? 1 : (b > kBatch ? kBatch : b);
+}
+
 size_t ps_score_lds_bytes(int32_t n_inst) {
-  const size_t nw = ((size_t)n_inst + 63) / 64;
-  const size_t hits = ps_hits_fit_lds(n_inst) ? (size_t)n_inst * sizeof(uint16_t) : 0;
-  return (size_t)kStage * sizeof(uint64_t) + 3 * nw * sizeof(uint64_t) + 64 * sizeof(uint32_t) +
-         64 * sizeof(uint16_t) + (hits + 15) / 16 * 16;
+  return score_lds_base(n_inst, ps_hits_fit_lds(n_inst)) + kBatchLds +
+         (ps_score_small(n_inst)
+              ? (size_t)kSmallPool * (sizeof(int64_t) + sizeof(InstState) + sizeof(int4))
+              : 0);
 }
 
 bool ps_hits_fit_lds(int32_t n_inst) {
@@ -830,10 +980,12 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
                        a);
   } else {
     const size_t lds = ps_score_lds_bytes(a.n_inst);
-    if (hits_in_lds)
-      hipLaunchKernelGGL(score_kernel<true>, dim3(grid), dim3(64), lds, s, a);
+    if (ps_score_small(a.n_inst))
+      hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(64), lds, s, a);
+    else if (hits_in_lds)
+      hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
     else
-      hipLaunchKernelGGL(score_kernel<false>, dim3(grid), dim3(64), lds, s, a);
+      hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
   }
   return hipGetLastError();
 }
@@ -851,7 +1003,9 @@ hipError_t ps_launch_group(const ScoreArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + 255) / 256), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(group_kernel, dim3(a.n_req), dim3(64), (size_t)kStage * sizeof(uint64_t), s, a);
+  const size_t nw = ((size_t)a.n_inst + 63) / 64;
+  const size_t lds = (size_t)kStage * sizeof(uint64_t) + 2 * nw * sizeof(uint64_t);
+  hipLaunchKernelGGL(group_kernel, dim3(a.n_req), dim3(64), lds, s, a);
   return hipGetLastError();
 }
 

@@ -126,20 +126,41 @@ def test_non_monotone_model(ps, scorer):
 
 
 # ------------------------------------------------------------- edge windows
+def _tail_only(w):
+    """The same chains as tail segments only (no shared segment, so no
+    prefix group): every request takes the scorer's per-request path.
+    Needs each request's tail to follow its prefix in the pool."""
+    assert (w.tail_off == w.pre_off + w.pre_len).all() or (w.tail_len == 0).all()
+    t = w.subset(range(w.n_req))
+    t.tail_off = w.pre_off.copy()
+    t.tail_len = (w.pre_len + w.tail_len).astype(np.int32)
+    t.pre_len = np.zeros_like(w.pre_len)
+    return t
+
+
 def _check_edge(ps, scorer, w, label, **policy):
     w.alpha = np.asarray(w.alpha, np.float32)
     load_window(scorer, w, **policy)
-    dw = DeviceWindow(w)
-    got = dw.hits(scorer, w.n_inst)
     o = oracle.Oracle.from_window(w)
-    want = o.window_hits(w)
-    assert (got == want).all(), f"{label}: hits differ at {np.argwhere(got != want)[:3]}"
-    res, sizes = dw.score(scorer)
-    od = o.window_score(w, **policy)
-    compare_decisions(res, sizes, od, label=label)
-    res2, _ = dw.score(scorer, with_sizes=False)
-    assert res2.tobytes() == res.tobytes(), f"{label}: path without sizes differs"
-    return res
+    variants = [(w, label)]
+    if (w.tail_off == w.pre_off + w.pre_len).all() and (w.pre_len > 0).any():
+        variants.append((_tail_only(w), label + " tail-only"))
+    first = None
+    for v, lab in variants:
+        dw = DeviceWindow(v)
+        got = dw.hits(scorer, v.n_inst)
+        want = o.window_hits(v)
+        assert (got == want).all(), f"{lab}: hits differ at {np.argwhere(got != want)[:3]}"
+        res, sizes = dw.score(scorer)
+        od = o.window_score(v, **policy)
+        compare_decisions(res, sizes, od, label=lab)
+        res2, _ = dw.score(scorer, with_sizes=False)
+        assert res2.tobytes() == res.tobytes(), f"{lab}: path without sizes differs"
+        if first is None:
+            first = res
+        else:
+            assert res.tobytes() == first.tobytes(), f"{lab}: differs from the grouped path"
+    return first
 
 
 def test_edge_single_instance_and_ragged_counts(ps, scorer):
