@@ -121,26 +121,55 @@ def group_segment_hits(sc, win, d_pool, rep, plen, chunk_pairs=1 << 25):
     return H
 
 
+def index_walk_bytes(h, ell, nw, h_all=None):
+    """Bytes of walking the live holders (h >= 1) of a chain of ell blocks
+    together through the prefix index: per position up to the second
+    longest hit one 128-byte index bucket plus that position's holders in
+    the pool (hits h_all, default h; a 2-byte id each, or the bitmap's
+    8-byte words for more than 64 holders), then the longest holder alone
+    along its row."""
+    import numpy as np
+    if h_all is None:
+        h_all = h
+    hr = np.sort(h[h >= 1])[::-1]
+    if len(hr) == 0 or ell <= 1:
+        return 0
+    P = int(min(ell - 1, hr[1] if len(hr) > 1 else 0))
+    by = 0
+    if P > 0:
+        cnts = (h_all[None, :] > np.arange(1, P + 1)[:, None]).sum(1)
+        by += 128 * P + int(np.where(cnts > 64, 8 * nw, 2 * cnts).sum())
+    if hr[0] > P:
+        by += 68 + 16 * max(0, min(int(hr[0]), ell - 1) - (P + 1)) + (64 if hr[0] < ell else 0)
+    return by
+
+
 def group_pass_bytes(win, gid, rep, plen, H):
     """Algorithmic bytes of the prefix-group pass.  Claim: descriptor, slot
     read, the claiming compare-and-swap, the length maximum and the slot
     entry per request.  Walk: slot entry per request; per group its
-    segment head staged (<= 256 hashes), one index bucket, the holder ids,
-    per holder (when at most GROUP_HOLD) a probe of the first block with its
-    row position, 16 bytes per compared position, a final probe where the
-    segment leaves the cache, and the record."""
+    segment head staged (<= 256 hashes), one index bucket, the holder ids
+    (or bitmap), then with at most GROUP_HOLD holders per holder a probe of
+    the first block with its row position, 16 bytes per compared position,
+    a final probe where the segment leaves the cache, and the record; with
+    more, the holders walked together through the index and one 4-byte hit
+    per holder in the popular row."""
     import numpy as np
-    R = win.n_req
+    R, N = win.n_req, win.n_inst
+    nw = (N + 63) // 64
     g = gid >= 0
     by = 28 * R + int(g.sum()) * (8 + 16) + len(rep) * 16
     by += 4 * R
     cnt0 = (H >= 1).sum(1)
-    by += int((16 + 8 * np.minimum(plen, 256) + 128 + 2 * cnt0).sum())
+    by += int((16 + 8 * np.minimum(plen, 256) + 128 +
+               np.where(cnt0 > 64, 8 * nw, 2 * cnt0)).sum())
     ok = cnt0 <= GROUP_HOLD
     hc = np.minimum(H, (plen - 1)[:, None])
     walk = np.where(H >= 1, 68 + 16 * hc + 64 * (H < plen[:, None]), 0)
     walk = np.where((plen > 1)[:, None], walk, np.where(H >= 1, 68, 0))
-    by += int(walk[ok].sum()) + int((8 + 8 * cnt0[ok]).sum()) + int((~ok).sum()) * 8
+    by += int(walk[ok].sum()) + int((8 + 8 * cnt0[ok]).sum())
+    for k in np.nonzero(~ok)[0]:
+        by += 8 + index_walk_bytes(H[k], int(plen[k]), nw) + 4 * int(cnt0[k])
     return by
 
 
@@ -198,7 +227,13 @@ def score_bytes(win, r0, hits, grp=None):
         has = grp["has"]
         p = win.pre_len[sl].astype(np.int64)
         Hg = grp["Hg"]
-        gby = 48 + 136 + 512 * levels + np.where(act, 8 * cnt0, 0)
+        # record path: the holders' rooms; popular rows: the index bucket
+        # and holders of the first block, then one 4-byte hit per candidate
+        gby = 48 + 136 + 512 * levels + np.where(
+            grp["pop"],
+            np.where(act & (ell > 0), 128 + np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0)
+                     + 4 * ncand, 0),
+            np.where(act, 8 * cnt0, 0))
         resume = cand & (Hg >= p[:, None]) & (p < ell)[:, None]
         rb = np.where(h > p[:, None],
                       68 + 16 * (np.minimum(h, (ell - 1)[:, None]) - p[:, None]) +
@@ -206,12 +241,7 @@ def score_bytes(win, r0, hits, grp=None):
         gby += np.where(resume, rb, 0).sum(1)
         by = np.where(has, gby, by + 4 + np.where(grp["grouped"], 136, 0))
     for r in np.nonzero(act & ~few & (ell > 1) & ~has)[0]:
-        hr = np.sort(h[r][cand[r]])[::-1]
-        P = int(min(ell[r] - 1, hr[1]))
-        cnts = (h[r][None, :] > np.arange(1, P + 1)[:, None]).sum(1)
-        by[r] += 128 * P + int(np.where(cnts > 64, 8 * nw, 2 * cnts).sum())
-        if hr[0] > P:
-            by[r] += 68 + 16 * (min(hr[0], ell[r] - 1) - (P + 1)) + (64 if hr[0] < ell[r] else 0)
+        by[r] += index_walk_bytes(np.where(cand[r], h[r], 0), int(ell[r]), nw, h[r])
     # the recomputation filter and the hit-0 class
     n = (L[:, None] - h * bs).astype(np.float64)
     c = (h * bs).astype(np.float64)
@@ -268,7 +298,11 @@ def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 25):
     import paper_2609_33224_amd as ps
     gid, rep, plen = group_info(win)
     H = group_segment_hits(sc, win, d_pool, rep, plen)
-    g_has = (H >= 1).sum(1) <= GROUP_HOLD if len(rep) else np.zeros(0, bool)
+    # every group gets a result: a record, or a popular row (the area holds
+    # 64 MiB / (4 n_inst) rows, more than any benchmark window needs)
+    g_has = np.ones(len(rep), bool)
+    g_pop = (H >= 1).sum(1) > GROUP_HOLD if len(rep) else np.zeros(0, bool)
+    assert int(g_pop.sum()) <= (64 << 20) // (4 * win.n_inst)
     gb = group_pass_bytes(win, gid, rep, plen, H)
     chunk = max(1, min(win.n_req, chunk_pairs // win.n_inst))
     reqs = ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
@@ -286,8 +320,9 @@ def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 25):
         gc = gid[r0:r0 + n]
         grouped = gc >= 0
         has = grouped & g_has[np.maximum(gc, 0)] if len(rep) else grouped
+        pop = grouped & g_pop[np.maximum(gc, 0)] if len(rep) else grouped
         Hg = H[np.maximum(gc, 0)] if len(rep) else np.zeros(hits.shape, np.int64)
-        sb += score_bytes(win, r0, hits, dict(has=has, grouped=grouped, Hg=Hg))
+        sb += score_bytes(win, r0, hits, dict(has=has, pop=pop, grouped=grouped, Hg=Hg))
     return sb, gb, pb, npr
 
 
@@ -433,6 +468,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--sequential-reps", type=int, default=3,
                     help="timed calls of the per-arrival scheduler (0: skip that block)")
+    ap.add_argument("--skip-bytes", action="store_true",
+                    help="skip the algorithmic byte counts (roofline fields null; for counter runs)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (a plain copy "
                          "kernel of known size, to scale the HBM byte counters)")
@@ -473,8 +510,11 @@ def main():
     stream = torch.cuda.current_stream()
 
     # untimed: byte counts from the per-pair hits, and the end-to-end host call
-    print("bench: counting algorithmic bytes", file=sys.stderr, flush=True)
-    alg_bytes, group_bytes, probe_alg_bytes, n_probes = algorithmic_bytes(sc, win, d_pool, d_reqs)
+    if args.skip_bytes:
+        alg_bytes = group_bytes = probe_alg_bytes = n_probes = None
+    else:
+        print("bench: counting algorithmic bytes", file=sys.stderr, flush=True)
+        alg_bytes, group_bytes, probe_alg_bytes, n_probes = algorithmic_bytes(sc, win, d_pool, d_reqs)
     t0 = time.perf_counter()
     sc.score(win.pool, reqs)
     host_call_s = time.perf_counter() - t0
@@ -522,7 +562,11 @@ def main():
     evals = win.n_req * win.n_inst
     src_hash = kernel_source_hash()
     traffic = traffic_for(args.workload, src_hash)
-    achieved = alg_bytes / (kern_avg * 1e-3) / 1e9
+    def rate(nbytes, ms):
+        return nbytes / (ms * 1e-3) / 1e9 if nbytes is not None and ms > 0 else None
+
+    achieved = rate(alg_bytes, kern_avg)
+    probe_gbs = rate(probe_alg_bytes, probe_ms)
     out = {
         "metric": METRIC,
         "value": evals / (ms_per_step * 1e-3),
@@ -543,20 +587,20 @@ def main():
         "kernel": "score_kernel (prefix hits from the group records, latency model, filters, keys)",
         "kernel_ms_avg": kern_avg,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
+                     "frac": achieved / HBM_PEAK_GBS if achieved is not None else None,
                      "traffic": traffic},
         "algorithmic_bytes_per_launch": alg_bytes,
         "group_pass": {"kernels": "group_claim_kernel + group_kernel (walk of each shared "
                                   "segment once per window)",
                        "ms_avg": group_ms, "algorithmic_bytes": group_bytes,
-                       "achieved_GBs": group_bytes / (group_ms * 1e-3) / 1e9 if group_ms > 0 else None,
+                       "achieved_GBs": rate(group_bytes, group_ms),
                        "groups": int(len(np.unique(win.pre_off[win.pre_len >= GROUP_MIN]))),
                        "timed_calls": n_timed},
         "probe_kernel": {"kernel": "ps_probe_hits_dev (every request x instance probed)",
                          "ms_per_window": probe_ms, "probes": n_probes,
                          "algorithmic_bytes": probe_alg_bytes,
-                         "achieved_GBs": probe_alg_bytes / (probe_ms * 1e-3) / 1e9,
-                         "frac_of_hbm_peak": probe_alg_bytes / (probe_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                         "achieved_GBs": probe_gbs,
+                         "frac_of_hbm_peak": probe_gbs / HBM_PEAK_GBS if probe_gbs is not None else None,
                          "evals_per_s": win.n_req * win.n_inst / (probe_ms * 1e-3)},
         "kernel_source_sha": src_hash,
         "load_instances_s": load_s,

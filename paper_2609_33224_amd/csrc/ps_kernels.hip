@@ -307,27 +307,52 @@ __device__ int32_t group_claim(const GroupTab& G, int64_t pre_off, int* leader) 
   return -1;  // table full (not reached: it holds at least twice the requests)
 }
 
-// Prefix groups, pass 1 (one thread per request): the slot of every
-// request's group and the group's longest segment (a 64-bit maximum over
-// generation-tagged lengths, so no slot needs clearing between windows).
+// Prefix groups, pass 1 (one thread per request; the grid covers every
+// request once): the slot of every request's group and the group's longest
+// segment (a 64-bit maximum over generation-tagged lengths, so no slot
+// needs clearing between windows).  Requests of one wave with the same
+// segment claim once: the lowest such lane claims and takes the maximum
+// over all of them, so a popular session does not serialise on one slot's
+// atomics.
 __global__ void group_claim_kernel(ScoreArgs a) {
   const GroupTab& G = a.grp;
   if (blockIdx.x == 0 && threadIdx.x == 0) *G.pop_ctr = 0u;  // read only by the walk pass
-  for (int32_t r = blockIdx.x * blockDim.x + threadIdx.x; r < a.n_req;
-       r += gridDim.x * blockDim.x) {
+  const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  bool want = false;
+  int64_t off = -1;
+  int32_t plen = 0;
+  if (r < a.n_req) {
     const ps_req q = a.reqs[r];
-    uint32_t out = kGroupNoSlot;
-    if (req_valid(q, a.pool_len) && q.pre_len >= kGroupMin) {
-      int leader = 0;
-      const int32_t slot = group_claim(G, q.pre_off, &leader);
-      if (slot >= 0) {
-        atomicMax(&G.plen[slot], ((unsigned long long)G.gen << kGroupGenShift) |
-                                     (unsigned long long)q.pre_len);
-        out = (uint32_t)slot | (leader ? kGroupLead : 0u);
-      }
+    want = req_valid(q, a.pool_len) && q.pre_len >= kGroupMin;
+    if (want) {
+      off = q.pre_off;
+      plen = q.pre_len;
     }
-    G.slot_of[r] = out;
   }
+  int first = lane;
+  int32_t mx = plen;
+  for (int l = 63; l >= 0; --l) {
+    const int64_t o = __shfl(off, l);
+    const int32_t pl = __shfl(plen, l);
+    if (want && o == off) {
+      first = l;
+      mx = pl > mx ? pl : mx;
+    }
+  }
+  int32_t slot = -1;
+  int leader = 0;
+  if (want && first == lane) {
+    slot = group_claim(G, off, &leader);
+    if (slot >= 0)
+      atomicMax(&G.plen[slot],
+                ((unsigned long long)G.gen << kGroupGenShift) | (unsigned long long)mx);
+  }
+  slot = __shfl(slot, first);
+  if (r < a.n_req)
+    G.slot_of[r] = want && slot >= 0
+                       ? (uint32_t)slot | (first == lane && leader ? kGroupLead : 0u)
+                       : kGroupNoSlot;
 }
 
 // Prefix groups, pass 2 (one wave per request; only leaders work): the walk
