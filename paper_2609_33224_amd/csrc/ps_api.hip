@@ -655,6 +655,9 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.hits_out = d_hits;
   a.scratch = c->d_scratch;
   a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0u, 0u, 0ull};
+  a.sel = c->h_model.sel;
+  a.defer_any = nullptr;
+  a.defer_only = 0;
   const bool probe_all = d_hits != nullptr;
   if (!probe_all && n_req <= kGroupMaxReq && pool_len < ((int64_t)1 << kGroupGenShift) - 1) {
     ps_status st = group_buffers(c, n_req, s);
@@ -668,6 +671,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                      (uint32_t)(kGroupPopBytes / ((size_t)c->n_inst * sizeof(uint32_t))),
                      c->gslots - 1u,
                      c->ggen};
+    a.defer_any = c->d_gpop + 1;
   }
   // The scoring kernel takes batches of a.batch requests per wave; a small
   // pool's waves copy the pool's state into LDS once and take batches in

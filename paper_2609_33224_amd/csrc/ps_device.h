@@ -141,7 +141,8 @@ struct GroupTab {
   uint2* rec;                // slots * kGroupRec words
   uint32_t* slot_of;         // per request: slot (| kGroupLead), or kGroupNoSlot
   uint32_t* pop;             // popular rows: pop_cap * n_inst hits (holders' entries only)
-  uint32_t* pop_ctr;         // rows taken in this window (reset by the claim pass)
+  uint32_t* pop_ctr;         // rows taken in this window, then the deferral word (both
+                             // reset by the claim pass)
   uint32_t pop_cap;
   uint32_t mask;             // slots - 1
   uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
@@ -169,6 +170,9 @@ struct ScoreArgs {
   uint32_t* hits_out;    // probe-all diagnostic: n_req * n_inst
   uint16_t* scratch;     // per-wave hit rows when they do not fit LDS
   int32_t batch;         // requests per batch of the scoring kernel
+  uint32_t sel;          // the model's selector (host copy, picks the kernels)
+  uint32_t* defer_any;   // set when the lean kernel left requests to the general one
+  int32_t defer_only;    // general kernel: score only requests marked as left to it
 };
 
 struct CommitArgs {

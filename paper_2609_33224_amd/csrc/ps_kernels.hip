@@ -316,7 +316,10 @@ __device__ int32_t group_claim(const GroupTab& G, int64_t pre_off, int* leader) 
 // atomics.
 __global__ void group_claim_kernel(ScoreArgs a) {
   const GroupTab& G = a.grp;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *G.pop_ctr = 0u;  // read only by the walk pass
+  if (blockIdx.x == 0 && threadIdx.x == 0) {  // read only by the later kernels of this window
+    G.pop_ctr[0] = 0u;
+    G.pop_ctr[1] = 0u;
+  }
   const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   bool want = false;
@@ -438,9 +441,12 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 constexpr int32_t kBatch = 4;  // most requests whose inputs one wave loads together
-// Bytes of the batch buffers: group records, descriptors, group slots (a
-// multiple of 16).
-constexpr size_t kBatchLds = (size_t)kBatch * (kGroupRec * 8 + 3 * 8 + 4);
+// Bytes of the batch buffers: group records, descriptors, group slots,
+// deferral marks (a multiple of 16).
+constexpr size_t kBatchLds = (size_t)kBatch * (kGroupRec * 8 + 3 * 8 + 4 + 4);
+// Result flag of a request the lean scoring kernel left to the general one
+// (never returned: the general kernel overwrites the result).
+constexpr uint32_t kDeferred = 0x80000000u;
 static_assert(kBatchLds % 16 == 0, "batch buffers keep the LDS layout 16-byte aligned");
 
 __host__ __device__ inline size_t score_lds_base(int32_t n_inst, bool hits_in_lds) {
@@ -451,7 +457,13 @@ __host__ __device__ inline size_t score_lds_base(int32_t n_inst, bool hits_in_ld
   return (b + 15) / 16 * 16;
 }
 
-template <bool HITS_IN_LDS, bool SMALL>
+// LEAN: only requests whose group record holds their hits (at most
+// kGroupHold holders of the first block), and no random or H-C-Q selector;
+// every other valid request is marked kDeferred (and *a.defer_any set) for
+// the general kernel that follows it, which then scores only those
+// (a.defer_only).  Leaving the index walks, staging and those selectors out
+// keeps the lean kernel's registers and instructions down.
+template <bool HITS_IN_LDS, bool SMALL, bool LEAN>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
@@ -466,7 +478,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   uint2* lrec = reinterpret_cast<uint2*>(smem + score_lds_base(n_inst, HITS_IN_LDS));
   int64_t* lq64 = reinterpret_cast<int64_t*>(lrec + kBatch * kGroupRec);
   uint32_t* lgso = reinterpret_cast<uint32_t*>(lq64 + 3 * kBatch);
-  int64_t* lroom = reinterpret_cast<int64_t*>(lgso + kBatch);
+  uint32_t* ldef = lgso + kBatch;
+  int64_t* lroom = reinterpret_cast<int64_t*>(ldef + kBatch);
   InstState* linst = reinterpret_cast<InstState*>(lroom + kSmallPool);
   int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);
   const int lane = threadIdx.x;
@@ -476,6 +489,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   auto room_of = [&](uint32_t i) -> int64_t { return SMALL ? lroom[i] : a.room[i]; };
   auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
 
+  if (!LEAN && a.defer_only && *a.defer_any == 0u) return;  // nothing was left to this kernel
+  bool deferred_any = false;
   for (int32_t w = lane; w < 3 * nw; w += 64) bmA[w] = 0ull;
   if (SMALL) {
     if (lane < n_inst) {
@@ -493,7 +508,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   for (int32_t rb = blockIdx.x * B; rb < a.n_req; rb += gridDim.x * B) {
     const int32_t nb = a.n_req - rb < B ? a.n_req - rb : B;
     __syncthreads();  // the previous batch is done with the batch buffers
-    if (lane < nb) lgso[lane] = a.grp.keys ? a.grp.slot_of[rb + lane] : kGroupNoSlot;
+    if (lane < nb) {
+      lgso[lane] = a.grp.keys ? a.grp.slot_of[rb + lane] : kGroupNoSlot;
+      if (!LEAN && a.defer_only) ldef[lane] = a.out[rb + lane].flags & kDeferred;
+    }
     if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rb)[lane];
     __syncthreads();
     for (int32_t w = lane; w < nb * kGroupRec; w += 64) {
@@ -504,6 +522,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
     __syncthreads();
     for (int32_t b = 0; b < nb; ++b) {
       const int32_t r = rb + b;
+      if (!LEAN && a.defer_only && __builtin_amdgcn_readfirstlane((int)ldef[b]) == 0) continue;
       // wave-uniform values read from LDS are moved to scalar registers
       const uint32_t gso = (uint32_t)__builtin_amdgcn_readfirstlane((int)lgso[b]);
       const ps_req ql = reinterpret_cast<const ps_req*>(lq64)[b];
@@ -532,8 +551,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         gm = GroupMeta{__builtin_amdgcn_readfirstlane((int)m0.x),
                        (uint32_t)__builtin_amdgcn_readfirstlane((int)m0.y)};
       }
-      const bool grp = gm.cnt != kGroupNone;
-      const bool gpop = grp && (gm.cnt & kGroupPop) != 0u;  // holders from the index
+      bool grp = gm.cnt != kGroupNone;
+      bool gpop = grp && (gm.cnt & kGroupPop) != 0u;  // holders from the index
+      if (LEAN) {
+        if (!grp || gpop) {
+          if (lane == 0) a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, kDeferred};
+          deferred_any = true;
+          continue;
+        }
+        grp = true;
+        gpop = false;
+      }
       const int32_t nst = grp ? 0 : (ell < kStage ? ell : kStage);
       // The chain head's loads and the room search's are in flight together.
       uint64_t sv[kStage / 64];
@@ -572,26 +600,26 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         const IdxHit h0 = index_lookup(a.x, grp ? c.pre[0] : stage[0], g == 0, g, s);
         const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
         const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
-        if (found0 && cnt0 > kPopular) {  // holders as a bitmap: lanes over its words
+        if (found0 && cnt0 > kPopular) {  // holders as a bitmap: lanes over the pool
+          // 64 instances per step, rooms read coalesced, four steps in flight
           const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
-          for (int32_t w0 = 0; w0 < nw; w0 += 64) {
-            const int32_t w = w0 + lane;
-            uint64_t d = w < nw ? bm[w] : 0ull, el_bits = 0ull;
-            while (d) {
-              const int b = __builtin_ctzll(d);
-              d &= d - 1;
-              if (room_of((uint32_t)(w * 64 + b)) >= L) el_bits |= 1ull << b;
+          for (int32_t w0 = 0; w0 < nw; w0 += 4) {
+            bool el[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int32_t w = w0 + u;
+              const int32_t i = w * 64 + lane;
+              el[u] = w < nw && i < n_inst && ((bm[w] >> lane) & 1ull) && room_of((uint32_t)i) >= L;
             }
-            const uint32_t cntl = (uint32_t)__popcll(el_bits);
-            uint32_t rank = nCand + wave_exclusive_sum(cntl, lane);
-            if (w < nw) bmC[w] = el_bits;
-            uint64_t e2 = el_bits;
-            while (e2 && rank < 64) {
-              const int b = __builtin_ctzll(e2);
-              e2 &= e2 - 1;
-              cl[rank++] = (uint16_t)(w * 64 + b);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int32_t w = w0 + u;
+              const uint64_t em = __ballot(el[u]);
+              if (w < nw && lane == 0) bmC[w] = em;
+              const uint32_t rank = nCand + (uint32_t)__popcll(em & lt_mask);
+              if (el[u] && rank < 64) cl[rank] = (uint16_t)(w * 64 + lane);
+              nCand += (uint32_t)__popcll(em);
             }
-            nCand += wave_sum_u32(cntl);
           }
         } else if (found0) {
           for (uint32_t t0 = 0; t0 < cnt0; t0 += 64) {
@@ -737,9 +765,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
           // first member of T in key order (decoding desc, queued asc, id
           // asc).  The whole class is evaluated when sizes are requested or
           // when no member is in T (then the fallback key may come from it).
-          bool done0 = false;
+          bool done0 = false, searched = false;
           const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
           if (!a.sizes && keyed && m.mono && !(m.flags & PS_F_TTFT_ADMIT)) {
+            searched = true;
             // The first member of T in key order: the first key position whose
             // threshold admits this length and whose instance does not hold
             // the first block.  Chunk maxima skip 64 positions per entry.
@@ -765,7 +794,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
                 }
               }
             }
-          } else if (!a.sizes && keyed) {
+          } else if (!LEAN && !a.sizes && keyed) {
+            searched = true;
             for (int32_t base = 0; base < n_inst && !done0; base += 64) {
               const int32_t k = base + lane;
               bool ok = false;
@@ -790,9 +820,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
               }
             }
           }
-          // No member of the class is in T: its keys matter only for the
-          // fallback, i.e. when no candidate is in T either.
-          if (!done0 && !a.sizes && keyed) done0 = wave_min_u64(acc.keyT) != ~0ull;
+          // A search found no member of the class in T: its keys matter only
+          // for the fallback, i.e. when no candidate is in T either.
+          if (!done0 && searched) done0 = wave_min_u64(acc.keyT) != ~0ull;
           if (!done0) {
             for (int32_t base = 0; base < n_inst; base += 64) {
               const int32_t i = base + lane;
@@ -804,7 +834,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         }
       }
       uint64_t keyT;
-      if (m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
+      if (!LEAN && m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
         const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
         keyT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
       } else {
@@ -816,7 +846,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       const bool counts = a.sizes || m.sel == PS_SEL_RANDOM;
       const uint32_t nC = counts ? wave_sum_u32(acc.nC) : 0u;
       const uint32_t nT = counts ? wave_sum_u32(acc.nT) : 0u;
-      if (m.sel == PS_SEL_RANDOM && nT > 0) {
+      if (!LEAN && m.sel == PS_SEL_RANDOM && nT > 0) {
         // the k-th member of T in id order
         const uint64_t z = splitmix64_at(m.rand_seed, r);
         const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
@@ -897,6 +927,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       }
     }
   }
+  if (LEAN && deferred_any && lane == 0) atomicOr(a.defer_any, 1u);
 }
 
 // One wave per instance that receives placements; its entries are applied
@@ -997,21 +1028,38 @@ hipError_t ps_launch_rows(const BuildArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <bool LEAN>
+static void launch_score_variant(const ScoreArgs& a, bool hits_in_lds, int grid, size_t lds,
+                                 hipStream_t s) {
+  if (ps_score_small(a.n_inst))
+    hipLaunchKernelGGL((score_kernel<true, true, LEAN>), dim3(grid), dim3(64), lds, s, a);
+  else if (hits_in_lds)
+    hipLaunchKernelGGL((score_kernel<true, false, LEAN>), dim3(grid), dim3(64), lds, s, a);
+  else
+    hipLaunchKernelGGL((score_kernel<false, false, LEAN>), dim3(grid), dim3(64), lds, s, a);
+}
+
 hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s) {
   if (a.n_req == 0) return hipSuccess;
   if (probe_all) {
     hipLaunchKernelGGL(probe_all_kernel, dim3(grid), dim3(64), (size_t)kStage * sizeof(uint64_t), s,
                        a);
-  } else {
-    const size_t lds = ps_score_lds_bytes(a.n_inst);
-    if (ps_score_small(a.n_inst))
-      hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(64), lds, s, a);
-    else if (hits_in_lds)
-      hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
-    else
-      hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
+    return hipGetLastError();
   }
+  // The lean kernel first when the groups give requests their hits and the
+  // selector is neither random nor H-C-Q; the general kernel then finishes
+  // whatever it left (or scores every request).
+  const bool lean = a.grp.keys && a.defer_any && a.sel != PS_SEL_RANDOM && a.sel != PS_SEL_HCQ;
+  const size_t lds = ps_score_lds_bytes(a.n_inst);
+  ScoreArgs g = a;
+  g.defer_only = lean ? 1 : 0;
+  if (lean) {
+    launch_score_variant<true>(a, hits_in_lds, grid, lds, s);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  launch_score_variant<false>(g, hits_in_lds, grid, lds, s);
   return hipGetLastError();
 }
 
