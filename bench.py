@@ -584,7 +584,7 @@ def main():
                    "n_inst": win.n_inst, "n_req": win.n_req, "seed": args.seed},
         "decisions_per_s": win.n_req / (ms_per_step * 1e-3),
         "step_ms_events": step_avg,
-        "kernel": "score_kernel (prefix hits from the group records, latency model, filters, keys)",
+        "kernel": "score_kernel, lean pass + general pass (prefix hits from the group records, latency model, filters, keys)",
         "kernel_ms_avg": kern_avg,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS if achieved is not None else None,
