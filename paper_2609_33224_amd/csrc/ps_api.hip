@@ -44,6 +44,8 @@ struct ps_ctx {
   int64_t* d_room_sorted = nullptr;
   uint32_t* d_order0 = nullptr;
   InstState* d_inst_key = nullptr;  // states in d_order0's order
+  TopRoom* d_rtop = nullptr;         // the kTopRooms largest rooms with their ids
+  int32_t lean_wpc = 0;              // resident lean-scorer waves per CU (0: not asked yet)
   int4* d_lm = nullptr;              // zero-hit admission thresholds in that order
   int32_t* d_lm1 = nullptr;          // their maxima per 64 positions
   GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
@@ -253,6 +255,7 @@ void free_snapshot(ps_ctx* c) {
   dfree(c->d_room_sorted);
   dfree(c->d_order0);
   dfree(c->d_inst_key);
+  dfree(c->d_rtop);
   dfree(c->d_lm);
   dfree(c->d_lm1);
   dfree(c->d_scratch);
@@ -267,6 +270,17 @@ ps_status refresh_lmax(ps_ctx* c) {
                             c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return PS_OK;
+}
+
+// The kTopRooms largest rooms with their ids, descending (pads: room -1).
+std::vector<TopRoom> top_rooms(const std::vector<int64_t>& room) {
+  std::vector<TopRoom> t(room.size());
+  for (size_t i = 0; i < room.size(); ++i) t[i] = TopRoom{room[i], (int32_t)i, 0};
+  const size_t k = std::min(room.size(), (size_t)kTopRooms);
+  std::partial_sort(t.begin(), t.begin() + (long)k, t.end(),
+                    [](const TopRoom& x, const TopRoom& y) { return x.room > y.room; });
+  t.resize(kTopRooms, TopRoom{-1, 0, 0});
+  return t;
 }
 
 // Per-instance room (kv_cap - S when A + 1 <= B_max, else -1; an instance
@@ -319,6 +333,8 @@ ps_status refresh_derived(ps_ctx* c) {
                        hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemcpy(c->d_room, room.data(), room.size() * sizeof(int64_t), hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+  const std::vector<TopRoom> tr = top_rooms(room);
+  HIP_TRY(c, hipMemcpy(c->d_rtop, tr.data(), tr.size() * sizeof(TopRoom), hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemcpy(c->d_order0, o0.data(), o0.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
   const std::vector<InstState> ik = states_in_order(c->h_state, o0);
   HIP_TRY(c, hipMemcpy(c->d_inst_key, ik.data(), ik.size() * sizeof(InstState), hipMemcpyHostToDevice));
@@ -455,6 +471,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     dfree(fresh.d_room_sorted);
     dfree(fresh.d_order0);
     dfree(fresh.d_inst_key);
+    dfree(fresh.d_rtop);
     dfree(fresh.d_lm);
     dfree(fresh.d_lm1);
     dfree(fresh.d_scratch);
@@ -476,6 +493,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_room_sorted, (size_t)n * sizeof(int64_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_order0, (size_t)n * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_inst_key, (size_t)n * sizeof(InstState));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_rtop, (size_t)kTopRooms * sizeof(TopRoom));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_lm, (size_t)n * sizeof(int4));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_lm1, (size_t)((n + 63) / 64) * sizeof(int32_t));
   if (e == hipSuccess && rows)
@@ -524,6 +542,10 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   if (e == hipSuccess)
     e = hipMemcpyAsync(fresh.d_inst_key, hinst_key.data(), hinst_key.size() * sizeof(InstState),
                        hipMemcpyHostToDevice, sm);
+  const std::vector<TopRoom> htop = top_rooms(hroom);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(fresh.d_rtop, htop.data(), htop.size() * sizeof(TopRoom), hipMemcpyHostToDevice,
+                       sm);
   BuildArgs ba{fresh.t, d_off, d_blk, n, n_blk, c->d_counter, d_won, d_slot, d_rank};
   if (e == hipSuccess) e = ps_launch_build(ba, sm);
   if (e == hipSuccess) e = ps_exclusive_scan_u32(d_won, d_rank, n_blk, sm);
@@ -561,6 +583,8 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->d_room_sorted = fresh.d_room_sorted;
   c->d_order0 = fresh.d_order0;
   c->d_inst_key = fresh.d_inst_key;
+  c->d_rtop = fresh.d_rtop;
+  c->lean_wpc = 0;
   c->d_lm = fresh.d_lm;
   c->d_lm1 = fresh.d_lm1;
   c->x = fresh.x;
@@ -587,6 +611,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.d_room_sorted = nullptr;
   fresh.d_order0 = nullptr;
   fresh.d_inst_key = nullptr;
+  fresh.d_rtop = nullptr;
   fresh.d_lm = nullptr;
   fresh.d_lm1 = nullptr;
   fresh.x = GIndex{nullptr, nullptr, nullptr, 0, 0, 64};
@@ -640,6 +665,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.room_sorted = c->d_room_sorted;
   a.order0 = c->d_order0;
   a.inst_key = c->d_inst_key;
+  a.rtop = c->d_rtop;
   a.lm = c->d_lm;
   a.lm1 = c->d_lm1;
   a.inst = c->d_inst;
@@ -697,6 +723,19 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   if (ev) HIP_TRY(c, hipEventRecord(ev[0], s));
   if (a.grp.keys) HIP_TRY(c, ps_launch_group(a, s));
   if (ev) HIP_TRY(c, hipEventRecord(ev[1], s));
+  // The lean scorer first when the groups give the requests their hits and
+  // the selector is neither Random nor H-C-Q (persistent grid at its own
+  // occupancy); the general scorer then finishes what it left.
+  const bool lean = !probe_all && a.grp.keys && a.sel != PS_SEL_RANDOM && a.sel != PS_SEL_HCQ;
+  if (lean) {
+    if (!c->lean_wpc) c->lean_wpc = ps_lean_waves_per_cu(c->n_inst);
+    const int resident = c->num_cus * c->lean_wpc;
+    ScoreArgs la = a;
+    la.batch = ps_score_batch(n_req, resident);
+    const int lgrid = std::min((n_req + la.batch - 1) / la.batch, resident);
+    HIP_TRY(c, ps_launch_lean(la, lgrid, s));
+    a.defer_only = 1;
+  }
   HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, grid, probe_all, s));
   if (ev) {
     HIP_TRY(c, hipEventRecord(ev[2], s));
@@ -801,6 +840,8 @@ static ps_status after_commit(ps_ctx* c, hipStream_t s, int64_t* n_dropped) {
                             hipMemcpyDeviceToHost, s));
   HIP_TRY(c, hipStreamSynchronize(s));
   std::vector<int64_t> rs = rooms_of(c->h_state, c->h_model);
+  const std::vector<TopRoom> tr = top_rooms(rs);
+  HIP_TRY(c, hipMemcpy(c->d_rtop, tr.data(), tr.size() * sizeof(TopRoom), hipMemcpyHostToDevice));
   std::sort(rs.begin(), rs.end());
   HIP_TRY(c, hipMemcpy(c->d_room_sorted, rs.data(), rs.size() * sizeof(int64_t), hipMemcpyHostToDevice));
   const std::vector<uint32_t> o0 = key_order(c->h_state);

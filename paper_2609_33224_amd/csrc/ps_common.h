@@ -428,6 +428,18 @@ __device__ __forceinline__ Lat latency(const DevModel& m, const InstState& st, f
   return r;
 }
 
+// Another lane's state (every lane must call it).
+__device__ __forceinline__ InstState shfl_state(const InstState& st, int src) {
+  InstState r;
+  r.D = __shfl(st.D, src);
+  r.Q = __shfl(st.Q, src);
+  r.A1 = __shfl(st.A1, src);
+  r.seg = __shfl(st.seg, src);
+  r.P = __shfl(st.P, src);
+  r.S = __shfl(st.S, src);
+  return r;
+}
+
 __device__ __forceinline__ bool eligible(const DevModel& m, int32_t A1, int64_t S, int64_t L) {
   return A1 <= m.b_max && S + L <= m.kv_cap;
 }

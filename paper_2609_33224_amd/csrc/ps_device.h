@@ -148,6 +148,14 @@ struct GroupTab {
   uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
 };
 
+// One of the pool's 64 largest rooms (descending; pads: room -1).
+struct alignas(16) TopRoom {
+  int64_t room;
+  int32_t id;
+  int32_t pad;
+};
+constexpr int kTopRooms = 64;
+
 struct ScoreArgs {
   Tables t;
   GIndex x;
@@ -159,6 +167,7 @@ struct ScoreArgs {
   const int32_t* lm1;          // maxima of lm[].x over 64-entry chunks
   const InstState* inst;
   const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
+  const TopRoom* rtop;   // the kTopRooms largest rooms
   const DevModel* model;
   const uint64_t* pool;
   int64_t pool_len;
@@ -240,6 +249,10 @@ hipError_t ps_launch_rows(const ps::BuildArgs& a, hipStream_t s);   // rows, row
 hipError_t ps_exclusive_scan_u32(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t s);
 hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s);
+// Lean scorer (requests with group records); its LDS and resident waves per CU.
+hipError_t ps_launch_lean(const ps::ScoreArgs& a, int grid, hipStream_t s);
+size_t ps_lean_lds_bytes(int32_t n_inst);
+int32_t ps_lean_waves_per_cu(int32_t n_inst);
 bool ps_hits_fit_lds(int32_t n_inst);
 // Prefix index build (ps_index.hip): from the per-instance tables.  Frees and
 // replaces *x.  count_host: distinct keys per instance.

@@ -457,13 +457,9 @@ __host__ __device__ inline size_t score_lds_base(int32_t n_inst, bool hits_in_ld
   return (b + 15) / 16 * 16;
 }
 
-// LEAN: only requests whose group record holds their hits (at most
-// kGroupHold holders of the first block), and no random or H-C-Q selector;
-// every other valid request is marked kDeferred (and *a.defer_any set) for
-// the general kernel that follows it, which then scores only those
-// (a.defer_only).  Leaving the index walks, staging and those selectors out
-// keeps the lean kernel's registers and instructions down.
-template <bool HITS_IN_LDS, bool SMALL, bool LEAN>
+// The general scorer: every request (groups or not, every selector), or
+// with a.defer_only only the requests the lean scorer marked kDeferred.
+template <bool HITS_IN_LDS, bool SMALL>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
@@ -489,8 +485,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   auto room_of = [&](uint32_t i) -> int64_t { return SMALL ? lroom[i] : a.room[i]; };
   auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
 
-  if (!LEAN && a.defer_only && *a.defer_any == 0u) return;  // nothing was left to this kernel
-  bool deferred_any = false;
+  if (a.defer_only && *a.defer_any == 0u) return;  // nothing was left to this kernel
   for (int32_t w = lane; w < 3 * nw; w += 64) bmA[w] = 0ull;
   if (SMALL) {
     if (lane < n_inst) {
@@ -510,7 +505,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
     __syncthreads();  // the previous batch is done with the batch buffers
     if (lane < nb) {
       lgso[lane] = a.grp.keys ? a.grp.slot_of[rb + lane] : kGroupNoSlot;
-      if (!LEAN && a.defer_only) ldef[lane] = a.out[rb + lane].flags & kDeferred;
+      if (a.defer_only) ldef[lane] = a.out[rb + lane].flags & kDeferred;
     }
     if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rb)[lane];
     __syncthreads();
@@ -522,7 +517,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
     __syncthreads();
     for (int32_t b = 0; b < nb; ++b) {
       const int32_t r = rb + b;
-      if (!LEAN && a.defer_only && __builtin_amdgcn_readfirstlane((int)ldef[b]) == 0) continue;
+      if (a.defer_only && __builtin_amdgcn_readfirstlane((int)ldef[b]) == 0) continue;
       // wave-uniform values read from LDS are moved to scalar registers
       const uint32_t gso = (uint32_t)__builtin_amdgcn_readfirstlane((int)lgso[b]);
       const ps_req ql = reinterpret_cast<const ps_req*>(lq64)[b];
@@ -551,17 +546,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         gm = GroupMeta{__builtin_amdgcn_readfirstlane((int)m0.x),
                        (uint32_t)__builtin_amdgcn_readfirstlane((int)m0.y)};
       }
-      bool grp = gm.cnt != kGroupNone;
-      bool gpop = grp && (gm.cnt & kGroupPop) != 0u;  // holders from the index
-      if (LEAN) {
-        if (!grp || gpop) {
-          if (lane == 0) a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, kDeferred};
-          deferred_any = true;
-          continue;
-        }
-        grp = true;
-        gpop = false;
-      }
+      const bool grp = gm.cnt != kGroupNone;
+      const bool gpop = grp && (gm.cnt & kGroupPop) != 0u;  // holders from the index
       const int32_t nst = grp ? 0 : (ell < kStage ? ell : kStage);
       // The chain head's loads and the room search's are in flight together.
       uint64_t sv[kStage / 64];
@@ -794,7 +780,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
                 }
               }
             }
-          } else if (!LEAN && !a.sizes && keyed) {
+          } else if (!a.sizes && keyed) {
             searched = true;
             for (int32_t base = 0; base < n_inst && !done0; base += 64) {
               const int32_t k = base + lane;
@@ -834,7 +820,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         }
       }
       uint64_t keyT;
-      if (!LEAN && m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
+      if (m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
         const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
         keyT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
       } else {
@@ -846,7 +832,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       const bool counts = a.sizes || m.sel == PS_SEL_RANDOM;
       const uint32_t nC = counts ? wave_sum_u32(acc.nC) : 0u;
       const uint32_t nT = counts ? wave_sum_u32(acc.nT) : 0u;
-      if (!LEAN && m.sel == PS_SEL_RANDOM && nT > 0) {
+      if (m.sel == PS_SEL_RANDOM && nT > 0) {
         // the k-th member of T in id order
         const uint64_t z = splitmix64_at(m.rand_seed, r);
         const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
@@ -927,7 +913,252 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       }
     }
   }
-  if (LEAN && deferred_any && lane == 0) atomicOr(a.defer_any, 1u);
+}
+
+// ------------------------------------------------------------ lean scorer
+// Scoring of the requests whose group record holds their hits (at most
+// kGroupHold holders of the first block), for every selector except Random
+// and H-C-Q.  Its read schedule is built for a chain of dependent reads
+// per request: a wave's batch of descriptors, slots and records arrive in
+// two round trips; the pool's 64 largest rooms and the zero-hit threshold
+// maxima (window constants) sit in registers for the whole launch; per
+// request the holders' states (which also decide their eligibility) and
+// the first passing chunk of zero-hit thresholds, with the key-ordered
+// states, are read together, so a decision usually needs one more round
+// trip after the record.  Every other valid request is marked kDeferred
+// (and *a.defer_any set) for the general kernel that follows.
+template <bool SMALL>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void lean_kernel(ScoreArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int32_t n_inst = a.n_inst;
+  const int32_t nw = (n_inst + 63) >> 6;
+  uint64_t* bmH = reinterpret_cast<uint64_t*>(smem);  // holders of the request's first block
+  uint2* lrec = reinterpret_cast<uint2*>(bmH + ((nw + 1) & ~1));
+  int64_t* lq64 = reinterpret_cast<int64_t*>(lrec + kBatch * kGroupRec);
+  uint32_t* lgso = reinterpret_cast<uint32_t*>(lq64 + 3 * kBatch);
+  InstState* linst = reinterpret_cast<InstState*>(lgso + kBatch);  // SMALL: states by id
+  int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);          // SMALL: thresholds
+  const int lane = threadIdx.x;
+  const int g = lane >> 3, s = lane & 7;
+  const DevModel& m = *a.model;
+  for (int32_t w = lane; w < nw; w += 64) bmH[w] = 0ull;
+  const TopRoom trm = a.rtop[lane];
+  const int32_t n1 = (n_inst + 63) >> 6;
+  const int32_t lm1r = lane < n1 ? a.lm1[lane] : -1;
+  if (SMALL && lane < n_inst) {
+    linst[lane] = a.inst[lane];
+    llm[lane] = a.lm[lane];
+  }
+  __syncthreads();
+  auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
+  const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
+  const bool fast0 = !a.sizes && keyed && m.mono && !(m.flags & PS_F_TTFT_ADMIT);
+  bool deferred_any = false;
+
+  const int32_t B = a.batch;
+  for (int32_t rb = blockIdx.x * B; rb < a.n_req; rb += gridDim.x * B) {
+    const int32_t nb = a.n_req - rb < B ? a.n_req - rb : B;
+    __syncthreads();  // the previous batch is done with the batch buffers
+    if (lane < nb) lgso[lane] = a.grp.slot_of[rb + lane];
+    if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rb)[lane];
+    __syncthreads();
+    for (int32_t w = lane; w < nb * kGroupRec; w += 64) {
+      const uint32_t so = lgso[w / kGroupRec];
+      if (so != kGroupNoSlot)
+        lrec[w] = a.grp.rec[(size_t)(so & ~kGroupLead) * kGroupRec + (uint32_t)(w % kGroupRec)];
+    }
+    __syncthreads();
+    for (int32_t b = 0; b < nb; ++b) {
+      const int32_t r = rb + b;
+      const uint32_t gso = (uint32_t)__builtin_amdgcn_readfirstlane((int)lgso[b]);
+      const ps_req ql = reinterpret_cast<const ps_req*>(lq64)[b];
+      const ps_req q{uniform64(ql.pre_off), uniform64(ql.tail_off),
+                     __builtin_amdgcn_readfirstlane(ql.pre_len),
+                     __builtin_amdgcn_readfirstlane(ql.tail_len)};
+      if (!req_valid(q, a.pool_len)) {
+        if (lane == 0) {
+          a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
+          if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+        }
+        continue;
+      }
+      uint32_t cnt = kGroupNone;
+      uint2 hd = make_uint2(0u, 0u);
+      if (gso != kGroupNoSlot) {
+        const uint2* grec = lrec + b * kGroupRec;
+        cnt = (uint32_t)__builtin_amdgcn_readfirstlane((int)grec[0].y);
+        if ((uint32_t)lane < kGroupHold) hd = grec[1 + lane];
+      }
+      if (cnt == kGroupNone || (cnt & kGroupPop)) {  // no record with the hits: the general kernel
+        if (lane == 0) a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, kDeferred};
+        deferred_any = true;
+        continue;
+      }
+      const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
+      const int32_t ell = c.len;
+      const int64_t L = (int64_t)ell * m.bs;
+      const float Lf = (float)L;
+      const int32_t p = q.pre_len;
+      uint32_t nA_exact = 0;
+      if (a.sizes) nA_exact = (uint32_t)(n_inst - wave_lower_bound(a.room_sorted, n_inst, L, lane));
+      if (!(__shfl(trm.room, 0) >= L)) {  // A is empty: Reject
+        if (lane == 0) {
+          a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+          if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+        }
+        continue;
+      }
+      // The first chunk of zero-hit thresholds that admits this length, with
+      // the key-ordered states, read together with the holders' states.
+      uint64_t cmask = fast0 ? __ballot(lane < n1 && lm1r >= ell) : 0ull;
+      int32_t c0 = 0;
+      int4 e = make_int4(-1, 0, 0, 0);
+      InstState est{};
+      bool have = false;
+      if (cmask) {
+        const int32_t k = (int32_t)__builtin_ctzll(cmask) * 64 + lane;
+        if (k < n_inst) {
+          e = SMALL ? llm[k] : a.lm[k];
+          if (!SMALL) est = a.inst_key[k];
+        }
+        have = true;
+      }
+      // Holders: state (and with it eligibility) and hit; the holder bitmap.
+      InstState hst{};
+      bool el = false;
+      uint32_t id = 0, hit = 0;
+      if ((uint32_t)lane < cnt) {
+        id = hd.x;
+        hit = hd.y;
+        hst = state_of(id);
+        el = eligible(m, hst.A1, hst.S, L);
+        atomicOr(reinterpret_cast<unsigned long long*>(&bmH[id >> 6]), 1ull << (id & 63));
+      }
+      if (SMALL && have && e.x >= 0) est = linst[e.y];
+      __syncthreads();
+      // Hits that reach the request's segment end continue on its tail.
+      uint64_t need = __ballot(el && (int32_t)hit >= p);
+      while (need) {
+        const int k = __builtin_ctzll(need);
+        need &= need - 1;
+        const uint32_t idk = (uint32_t)__shfl((int)id, k);
+        const uint32_t hk = run_walk<false>(a.t, idk, c, nullptr, p, g, s);
+        if (lane == k) hit = hk;
+      }
+      // Some eligible instance holds nothing (exact from the 64 largest
+      // rooms: 64 eligible ones cannot all be among at most 16 holders).
+      const bool topel = trm.room >= L;
+      const bool any0 = __ballot(topel && !test_bit(bmH, (uint32_t)trm.id)) != 0ull ||
+                        __shfl(topel ? 1 : 0, 63) != 0;
+      // Minimum recomputation penalty over A.
+      const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
+      const float W0 = fmaxf(0.0f, Z);
+      uint32_t wb = 0x7F800000u;
+      if (el) wb = __float_as_uint(fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)hit * m.bs), Lf)));
+      if (any0 && lane == 0) wb = wb < __float_as_uint(W0) ? wb : __float_as_uint(W0);
+      const float wmin = __uint_as_float(wave_min_u32(wb));
+      const float tpf_cold = t_prefill(m, Lf, 0.0f);
+      const float slo = fmaxf(m.ttft_floor, tpf_cold);
+      const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+      const bool admit0 = any0 && (!kvc || (W0 - wmin) / Z <= m.eta);
+      Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
+      if (el) evaluate_with(m, acc, id, hit, [&]() { return hst; }, L, Lf, wmin, Z, kvc, slo);
+      // The hit-0 class: eligible non-holders, one penalty W(L).
+      int32_t win0 = -1;  // lane of the class member found by the search
+      if (admit0) {
+        bool done0 = false;
+        if (fast0) {
+          while (have) {
+            const uint64_t om = __ballot(e.x >= ell && !test_bit(bmH, (uint32_t)e.y));
+            if (om) {
+              win0 = __builtin_ctzll(om);
+              if (lane == win0) {
+                InstState kst{};
+                kst.D = e.z;
+                kst.Q = e.w;
+                const uint64_t kt = select_key(m.sel, kst, 0u, (uint32_t)e.y, 0ull);
+                acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+              }
+              done0 = true;
+              break;
+            }
+            // the next chunk whose maximum admits this length
+            cmask &= cmask - 1;
+            while (!cmask) {
+              c0 += 64;
+              if (c0 >= n1) break;
+              const int32_t cc = c0 + lane;
+              cmask = __ballot(cc < n1 && a.lm1[cc] >= ell);
+            }
+            have = cmask != 0ull;
+            if (have) {
+              const int32_t k = (c0 + (int32_t)__builtin_ctzll(cmask)) * 64 + lane;
+              e = make_int4(-1, 0, 0, 0);
+              if (k < n_inst) {
+                e = SMALL ? llm[k] : a.lm[k];
+                est = SMALL ? linst[e.y] : a.inst_key[k];
+              }
+            }
+          }
+          // No member of the class is in T: its keys matter only for the
+          // fallback, i.e. when no candidate is in T either.
+          if (!done0) done0 = wave_min_u64(acc.keyT) != ~0ull;
+        }
+        if (!done0) {  // the whole class, lanes over the pool
+          for (int32_t base = 0; base < n_inst; base += 64) {
+            const int32_t i = base + lane;
+            if (i < n_inst && !test_bit(bmH, (uint32_t)i)) {
+              const InstState st = state_of((uint32_t)i);
+              if (eligible(m, st.A1, st.S, L))
+                evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return st; }, L, Lf, wmin, Z, kvc,
+                              slo);
+            }
+          }
+        }
+      }
+      const uint64_t keyT = wave_min_u64(acc.keyT);
+      const uint64_t keyF = keyT == ~0ull ? wave_min_u64(acc.keyF) : ~0ull;
+      uint32_t nC = 0, nT = 0;
+      if (a.sizes) {
+        nC = wave_sum_u32(acc.nC);
+        nT = wave_sum_u32(acc.nT);
+      }
+      // Decision: the chosen instance's state from the lane that read it.
+      ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+      if (keyT != ~0ull || keyF != ~0ull) {
+        const bool t = keyT != ~0ull;
+        const uint32_t best = (uint32_t)((t ? keyT : keyF) & 0xFFFFu);
+        const uint64_t hb = __ballot(el && id == best);
+        InstState bs{};
+        uint32_t v = 0;
+        if (hb) {
+          const int src = __builtin_ctzll(hb);
+          bs = shfl_state(hst, src);
+          v = (uint32_t)__shfl((int)hit, src);
+        } else if (win0 >= 0 && (uint32_t)__shfl(e.y, win0) == best) {
+          bs = shfl_state(est, win0);
+        } else {
+          bs = state_of(best);
+        }
+        const int64_t c_tok = (int64_t)v * m.bs;
+        const Lat lt = latency(m, bs, (float)(L - c_tok), (float)c_tok, L);
+        res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot,
+                        (t ? 0u : PS_R_FALLBACK) | (lt.ttft > slo ? PS_R_TTFT_MISS : 0u)};
+      }
+      if (lane == 0) {
+        a.out[r] = res;
+        if (a.sizes) {
+          a.sizes[3 * (size_t)r] = nA_exact;
+          a.sizes[3 * (size_t)r + 1] = nC;
+          a.sizes[3 * (size_t)r + 2] = nT;
+        }
+      }
+      __syncthreads();
+      if ((uint32_t)lane < cnt) bmH[id >> 6] = 0ull;
+      __syncthreads();
+    }
+  }
+  if (deferred_any && lane == 0) atomicOr(a.defer_any, 1u);
 }
 
 // One wave per instance that receives placements; its entries are applied
@@ -1028,15 +1259,21 @@ hipError_t ps_launch_rows(const BuildArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <bool LEAN>
-static void launch_score_variant(const ScoreArgs& a, bool hits_in_lds, int grid, size_t lds,
-                                 hipStream_t s) {
-  if (ps_score_small(a.n_inst))
-    hipLaunchKernelGGL((score_kernel<true, true, LEAN>), dim3(grid), dim3(64), lds, s, a);
-  else if (hits_in_lds)
-    hipLaunchKernelGGL((score_kernel<true, false, LEAN>), dim3(grid), dim3(64), lds, s, a);
-  else
-    hipLaunchKernelGGL((score_kernel<false, false, LEAN>), dim3(grid), dim3(64), lds, s, a);
+size_t ps_lean_lds_bytes(int32_t n_inst) {
+  const size_t nw = ((size_t)n_inst + 63) / 64;
+  return ((nw + 1) & ~(size_t)1) * sizeof(uint64_t) + (size_t)kBatch * kGroupRec * sizeof(uint2) +
+         3 * (size_t)kBatch * sizeof(int64_t) + (size_t)kBatch * sizeof(uint32_t) +
+         (ps_score_small(n_inst) ? (size_t)kSmallPool * (sizeof(InstState) + sizeof(int4)) : 0);
+}
+
+int32_t ps_lean_waves_per_cu(int32_t n_inst) {
+  int blocks = 0;
+  const size_t lds = ps_lean_lds_bytes(n_inst);
+  const hipError_t e =
+      ps_score_small(n_inst)
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, lean_kernel<true>, 64, lds)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, lean_kernel<false>, 64, lds);
+  return e == hipSuccess && blocks > 0 ? blocks : 16;
 }
 
 hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
@@ -1047,19 +1284,23 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
                        a);
     return hipGetLastError();
   }
-  // The lean kernel first when the groups give requests their hits and the
-  // selector is neither random nor H-C-Q; the general kernel then finishes
-  // whatever it left (or scores every request).
-  const bool lean = a.grp.keys && a.defer_any && a.sel != PS_SEL_RANDOM && a.sel != PS_SEL_HCQ;
   const size_t lds = ps_score_lds_bytes(a.n_inst);
-  ScoreArgs g = a;
-  g.defer_only = lean ? 1 : 0;
-  if (lean) {
-    launch_score_variant<true>(a, hits_in_lds, grid, lds, s);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  launch_score_variant<false>(g, hits_in_lds, grid, lds, s);
+  if (ps_score_small(a.n_inst))
+    hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(64), lds, s, a);
+  else if (hits_in_lds)
+    hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
+  else
+    hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t ps_launch_lean(const ScoreArgs& a, int grid, hipStream_t s) {
+  if (a.n_req == 0) return hipSuccess;
+  const size_t lds = ps_lean_lds_bytes(a.n_inst);
+  if (ps_score_small(a.n_inst))
+    hipLaunchKernelGGL(lean_kernel<true>, dim3(grid), dim3(64), lds, s, a);
+  else
+    hipLaunchKernelGGL(lean_kernel<false>, dim3(grid), dim3(64), lds, s, a);
   return hipGetLastError();
 }
 
