@@ -7,12 +7,13 @@ request window with a 30 ms TPOT target (c2).  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload c2] [--no-cpu-baseline]
 
-The roofline block counts the algorithmic bytes of a launch: one 64-byte
-bucket per probe, min(hit + 1, chain length) probes per capacity-eligible
-(request, instance) pair, plus the request chain read up to the deepest
-probe, 24 bytes of descriptor and 24 of instance state per request /
-instance, and 20 bytes of result per request.  `traffic` comes from the
-committed rocprofv3 counter summary of the same kernel source, or is null.
+The roofline block is the scoring pass's (lean + general kernels):
+algorithmic bytes from `score_bytes` over the library's HIP-event time on
+the launch stream.  The probe_kernel block is the exhaustive probe kernel's
+(ps_probe_hits_dev): one 64-byte bucket per probe, min(hit + 1, chain
+length) probes per (request, instance) pair, plus the staged chain head.
+`traffic` comes from the committed rocprofv3 counter summary of the same
+kernel sources, or is null.
 """
 from __future__ import annotations
 
@@ -29,7 +30,8 @@ sys.path.insert(0, ROOT)
 METRIC = ("request×instance candidate evals/sec + decisions/sec; "
           "probe-kernel % of HBM peak")
 HBM_PEAK_GBS = 8000.0
-BUCKET_BYTES = 64
+BUCKET_BYTES = 64  # one 8-slot bucket of a per-instance table
+PROBE_ROWPOS = BUCKET_BYTES + 4  # a probe that also reads the found slot's row position
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 WORKLOAD_NAMES = {
@@ -140,7 +142,7 @@ def index_walk_bytes(h, ell, nw, h_all=None):
         cnts = (h_all[None, :] > np.arange(1, P + 1)[:, None]).sum(1)
         by += 128 * P + int(np.where(cnts > 64, 8 * nw, 2 * cnts).sum())
     if hr[0] > P:
-        by += 68 + 16 * max(0, min(int(hr[0]), ell - 1) - (P + 1)) + (64 if hr[0] < ell else 0)
+        by += PROBE_ROWPOS + 16 * max(0, min(int(hr[0]), ell - 1) - (P + 1)) + (BUCKET_BYTES if hr[0] < ell else 0)
     return by
 
 
@@ -165,8 +167,8 @@ def group_pass_bytes(win, gid, rep, plen, H):
                np.where(cnt0 > 64, 8 * nw, 2 * cnt0)).sum())
     ok = cnt0 <= GROUP_HOLD
     hc = np.minimum(H, (plen - 1)[:, None])
-    walk = np.where(H >= 1, 68 + 16 * hc + 64 * (H < plen[:, None]), 0)
-    walk = np.where((plen > 1)[:, None], walk, np.where(H >= 1, 68, 0))
+    walk = np.where(H >= 1, PROBE_ROWPOS + 16 * hc + BUCKET_BYTES * (H < plen[:, None]), 0)
+    walk = np.where((plen > 1)[:, None], walk, np.where(H >= 1, PROBE_ROWPOS, 0))
     by += int(walk[ok].sum()) + int((8 + 8 * cnt0[ok]).sum())
     for k in np.nonzero(~ok)[0]:
         by += 8 + index_walk_bytes(H[k], int(plen[k]), nw) + 4 * int(cnt0[k])
@@ -174,22 +176,34 @@ def group_pass_bytes(win, gid, rep, plen, H):
 
 
 def score_bytes(win, r0, hits, grp=None):
-    """Algorithmic bytes the scoring kernel moves for requests r0 .. r0 +
-    len(hits) (the path without set sizes), from its data movement per
-    request: descriptor, result and staged chain head; the 64-way search of
-    the sorted rooms; one 128-byte index bucket for the first block; the
-    holders of the first block (2-byte ids + 8-byte rooms, or a bitmap when
-    more than 64 hold it); per walked holder one 64-byte probe, a 4-byte row
-    position and 16 bytes (chain + row) per compared position, and a final
-    64-byte probe at the first absent block; with more than 64 holders, one
-    index bucket plus the holder data per walked position; 32 bytes of state
-    per member of C; the threshold search of the hit-0 class (below).  With
-    prefix groups (`grp`: per request its group's segment hits Hg, whether
-    the group record holds a result, and whether the request is grouped at
-    all), a request with a group result reads the record (meta + 16
-    holders) and the holders' rooms instead of staging, index and walks,
-    and walks only where the group's segment is cached up to its own
-    segment length (from there, on its tail)."""
+    """Algorithmic bytes the scoring pass moves for requests r0 .. r0 +
+    len(hits) (the benchmark's policy: D-C-Q, monotone model, no set sizes).
+
+    Requests whose group record holds their hits go through the lean kernel:
+    24 B descriptor + 4 B group slot + 136 B record + 20 B result; for pools
+    above 64 instances 32 B of state per holder of the first block (that
+    read also decides eligibility) and 64 x (16 B threshold + 32 B key-
+    ordered state) per chunk of zero-hit thresholds read (the first chunk
+    that admits the request's length is read in any case, later ones until
+    an admitted non-holder is found); a resume walk on each candidate whose
+    shared segment is cached to the request's segment end (a probe with its
+    row position, 16 B per compared position, a final probe); when no
+    member of the hit-0 class and no candidate is in T, the states of all
+    non-holders.  Pools of at most 64 instances keep states and thresholds
+    in LDS (no bytes).  The rooms and threshold maxima are read once per
+    wave (not counted).
+
+    Other requests go through the general kernel: descriptor, slot, result;
+    the 64-way search of the sorted rooms; with a popular group row the
+    record, one 128-byte index bucket, the first block's holders (2-byte ids
+    + 8-byte rooms, or the bitmap's words + rooms) and a 4-byte hit per
+    candidate; without a group the staged chain head and the per-request
+    walks (per walked holder a probe with its row position, 16 B per
+    compared position and a final probe; with more than 64 holders the
+    index walk); 32 B of state per member of C; the zero-hit threshold
+    search (4 B per chunk maximum, 16 B per threshold of each visited chunk)
+    or, when the class must be evaluated, 8 B room + 32 B state per eligible
+    non-holder."""
     import numpy as np
     R, N = hits.shape
     pol = win.policy
@@ -199,10 +213,13 @@ def score_bytes(win, r0, hits, grp=None):
     a, ub, beta, gam = _fp64_model(win)
     sl = slice(r0, r0 + R)
     ell = win.pre_len[sl].astype(np.int64) + win.tail_len[sl]
+    p = win.pre_len[sl].astype(np.int64)
     L = ell * bs
     A1 = win.D.astype(np.int64) + win.Q + 1
     room = np.where(A1 <= bmax, kv - win.S, -1)
+    small = N <= 64
     nw = (N + 63) // 64
+    n1 = nw
     levels, span = 1, N
     while span > 64:
         span = (span + 63) // 64
@@ -214,34 +231,36 @@ def score_bytes(win, r0, hits, grp=None):
     ncand = cand.sum(1)
     nA = elig.sum(1)
     cnt0 = hold0.sum(1)
-    by = 44 + 8 * np.minimum(ell, 256) + 512 * levels
     act = nA > 0
-    by += np.where(act & (ell > 0), 128, 0)
-    by += np.where(act & (ell > 0), np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0), 0)
+    if grp is None:
+        grp = dict(has=np.zeros(R, bool), pop=np.zeros(R, bool), grouped=np.zeros(R, bool),
+                   Hg=np.zeros_like(h))
+    lean = grp["has"] & ~grp["pop"]
+    pop = grp["has"] & grp["pop"]
+    # resume walks of grouped requests
+    Hg = grp["Hg"]
+    resume = cand & (Hg >= p[:, None]) & (p < ell)[:, None]
+    rb = np.where(h > p[:, None],
+                  PROBE_ROWPOS + 16 * (np.minimum(h, (ell - 1)[:, None]) - p[:, None]) +
+                  BUCKET_BYTES * (h < ell[:, None]), PROBE_ROWPOS)
+    resume_by = np.where(resume, rb, 0).sum(1)
+    # general kernel: per-request parts
+    gen = 48 + 512 * levels + np.zeros(R, np.int64)
+    gen += np.where(pop, 136 + np.where(act & (ell > 0), 128 + np.where(
+        cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0) + 4 * ncand, 0) + resume_by, 0)
+    nogrp = ~grp["has"]
+    gen += np.where(nogrp, 8 * np.minimum(ell, 256) + np.where(grp["grouped"], 136, 0), 0)
+    gen += np.where(nogrp & act & (ell > 0), 128 + np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0), 0)
     few = ncand <= 64
     hc = np.minimum(h, (ell - 1)[:, None])
-    walk = np.where(cand, 68 + 16 * hc + 64 * (h < ell[:, None]), 0).sum(1)
-    by += np.where(act & few & (ell > 1), walk, 0)
-    has = np.zeros(R, bool)
-    if grp is not None:
-        has = grp["has"]
-        p = win.pre_len[sl].astype(np.int64)
-        Hg = grp["Hg"]
-        # record path: the holders' rooms; popular rows: the index bucket
-        # and holders of the first block, then one 4-byte hit per candidate
-        gby = 48 + 136 + 512 * levels + np.where(
-            grp["pop"],
-            np.where(act & (ell > 0), 128 + np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0)
-                     + 4 * ncand, 0),
-            np.where(act, 8 * cnt0, 0))
-        resume = cand & (Hg >= p[:, None]) & (p < ell)[:, None]
-        rb = np.where(h > p[:, None],
-                      68 + 16 * (np.minimum(h, (ell - 1)[:, None]) - p[:, None]) +
-                      64 * (h < ell[:, None]), 68)
-        gby += np.where(resume, rb, 0).sum(1)
-        by = np.where(has, gby, by + 4 + np.where(grp["grouped"], 136, 0))
-    for r in np.nonzero(act & ~few & (ell > 1) & ~has)[0]:
-        by[r] += index_walk_bytes(np.where(cand[r], h[r], 0), int(ell[r]), nw, h[r])
+    walk = np.where(cand, PROBE_ROWPOS + 16 * hc + BUCKET_BYTES * (h < ell[:, None]), 0).sum(1)
+    gen += np.where(nogrp & act & few & (ell > 1), walk, 0)
+    for r in np.nonzero(nogrp & act & ~few & (ell > 1))[0]:
+        gen[r] += index_walk_bytes(np.where(cand[r], h[r], 0), int(ell[r]), nw, h[r])
+    # lean kernel: per-request parts
+    lby = 184 + (0 if small else 32) * cnt0 + resume_by
+    lby = np.where(act, lby, 184)
+    by = np.where(lean, lby, gen)
     # the recomputation filter and the hit-0 class
     n = (L[:, None] - h * bs).astype(np.float64)
     c = (h * bs).astype(np.float64)
@@ -253,7 +272,7 @@ def score_bytes(win, r0, hits, grp=None):
     with np.errstate(divide="ignore", invalid="ignore"):
         rho = (W - Wmin[:, None]) / Z[:, None]
     inC = elig & (~kvc[:, None] | (rho <= eta))
-    by += 32 * (cand & inC).sum(1)
+    by += np.where(lean, 0, 32 * (cand & inC).sum(1))
     n0 = nA - ncand
     W0 = np.maximum(0.0, Z)
     with np.errstate(divide="ignore", invalid="ignore"):
@@ -261,31 +280,37 @@ def score_bytes(win, r0, hits, grp=None):
     seg = np.searchsorted(ub, A1, side="left")
     seg = np.minimum(seg, len(ub) - 1)
     order0 = np.lexsort((np.arange(N), win.Q, -win.D.astype(np.int64)))
-    n1 = (N + 63) // 64
-    for r in np.nonzero(act & admit0)[0]:
-        # The threshold search of the hit-0 class (the benchmark's policy:
-        # a monotone model, no TTFT admission, the D-C-Q key): 64 chunk
-        # maxima per read (4 B each), 64 threshold entries per visited chunk
-        # (16 B each) up to the first admitted non-holder.
+    chunk_lean = 0 if small else 64 * (16 + 32)
+    for r in np.nonzero(act & (admit0 | lean))[0]:
         t_iter = gam[seg] * (beta[seg, 0] + beta[seg, 1] * A1 + beta[seg, 2] * (win.S + L[r]))
         tpot0 = t_iter + np.where(A1 > 1, _tpf(a, float(L[r]), 0.0) / lout1, 0.0)
         zero = elig[r] & ~hold0[r]
         feas = np.zeros(n1 * 64, bool)
         feas[:N] = (elig[r] & (tpot0 < tau))[order0]
+        passing = feas.reshape(n1, 64).any(1)
         ok = (zero & (tpot0 < tau))[order0]
         found = bool(ok.any())
         cs = int(np.argmax(ok)) // 64 if found else n1 - 1
-        by[r] += 256 * (cs // 64 + 1) + 1024 * int(feas.reshape(n1, 64)[:cs + 1].any(1).sum())
+        if lean[r]:
+            if not admit0[r]:  # only the speculative first chunk
+                by[r] += chunk_lean if passing.any() else 0
+                continue
+            by[r] += chunk_lean * int(passing[:cs + 1].sum())
+        else:
+            by[r] += 256 * (cs // 64 + 1) + 1024 * int(passing[:cs + 1].sum())
         if found:
             continue
-        # No member of the class is in T: it is evaluated in full (room and
-        # state of each eligible non-holder) only when no candidate is in T.
+        # No member of the class is in T: it is evaluated in full only when
+        # no candidate is in T either.
         cr = cand[r] & inC[r]
         if cr.any():
             tp = t_iter[cr] + np.where(A1[cr] > 1, _tpf(a, n[r][cr], c[r][cr]) / lout1, 0.0)
             if (tp < tau).any():
                 continue
-        by[r] += 8 * N + 32 * int(zero.sum())
+        if lean[r]:
+            by[r] += 0 if small else 32 * (N - int(cnt0[r])) + 32
+        else:
+            by[r] += 8 * N + 32 * int(zero.sum())
     return int(by.sum())
 
 
