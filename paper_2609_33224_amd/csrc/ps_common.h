@@ -260,42 +260,42 @@ __device__ __forceinline__ bool req_valid(const ps_req& q, int64_t pool_len) {
 }
 
 // Deep walk of one instance: octets over chain positions.  A step issues
-// the bucket reads of kDeepRounds x 8 positions, then prefetches the next
-// step's chain hashes, then evaluates in chain order and stops at the first
-// absent position.  Positions below kStage read the LDS copy of the chain.
+// the bucket reads of DR x 8 positions (DR loads per lane in flight), then
+// prefetches the next step's chain hashes, then evaluates in chain order
+// and stops at the first absent position.  Positions below kStage read the LDS copy of the chain.
 // Wave-uniform arguments; returns the hit.
-template <bool STAGED>
+template <bool STAGED, int DR = kDeepRounds>
 __device__ uint32_t deep_walk(const Tables& t, uint32_t inst, const ChainRef& c,
                               const uint64_t* stage, int32_t pos, int g, int s) {
   const int32_t ell = c.len;
   const uint64_t* tab = table_of(t, inst);
-  uint64_t nk[kDeepRounds];
+  uint64_t nk[DR];
 #pragma unroll
-  for (int r = 0; r < kDeepRounds; ++r) {
+  for (int r = 0; r < DR; ++r) {
     const int32_t j = pos + r * 8 + g;
     nk[r] = 0ull;
     if (j < ell) nk[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
   }
   while (pos < ell) {
-    uint64_t key[kDeepRounds], val[kDeepRounds];
-    uint32_t b[kDeepRounds];
+    uint64_t key[DR], val[DR];
+    uint32_t b[DR];
 #pragma unroll
-    for (int r = 0; r < kDeepRounds; ++r) {
+    for (int r = 0; r < DR; ++r) {
       const int32_t j = pos + r * 8 + g;
       key[r] = nk[r];
       b[r] = bucket_of(key[r], inst, t.shift);
       val[r] = 0ull;
       if (j < ell && key[r] != 0ull) val[r] = tab[(size_t)b[r] * kSlotsPerBucket + s];
     }
-    const int32_t next = pos + kDeepRounds * 8;
+    const int32_t next = pos + DR * 8;
 #pragma unroll
-    for (int r = 0; r < kDeepRounds; ++r) {
+    for (int r = 0; r < DR; ++r) {
       const int32_t j = next + r * 8 + g;
       nk[r] = 0ull;
       if (j < ell) nk[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
     }
 #pragma unroll
-    for (int r = 0; r < kDeepRounds; ++r) {
+    for (int r = 0; r < DR; ++r) {
       const int32_t j = pos + r * 8 + g;
       const bool act = j < ell;
       uint32_t st = octet_status(val[r], key[r], act, g);

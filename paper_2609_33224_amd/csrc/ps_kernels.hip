@@ -128,7 +128,8 @@ __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
       while (deep) {
         const int k = __builtin_ctzll(deep);
         deep &= deep - 1;
-        const uint32_t hk = deep_walk<true>(a.t, (uint32_t)(base + k), c, stage, 1, g, s);
+        // 64 positions per step: deep walks dominate the walk-heavy windows
+        const uint32_t hk = deep_walk<true, 8>(a.t, (uint32_t)(base + k), c, stage, 1, g, s);
         if (lane == k) h = hk;
       }
       if (base + lane < n_inst) a.hits_out[(size_t)r * n_inst + base + lane] = h;
