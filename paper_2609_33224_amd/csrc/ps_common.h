@@ -308,6 +308,82 @@ __device__ uint32_t deep_walk(const Tables& t, uint32_t inst, const ChainRef& c,
   return (uint32_t)ell;
 }
 
+// Lane probing: one lane reads the whole 64-byte bucket of its own key
+// (four 16-byte loads).  1 found, 0 absent (an empty slot ends the probe
+// sequence, and the zero hash is never stored), 2 full bucket without the
+// key (the next bucket decides).
+__device__ __forceinline__ uint32_t lane_status(const Bucket& bk, uint64_t key) {
+  bool f = false, e = false;
+#pragma unroll
+  for (int s = 0; s < kSlotsPerBucket; ++s) {
+    f |= bk.k[s] == key;
+    e |= bk.k[s] == 0ull;
+  }
+  if (key == 0ull) return 0u;
+  return f ? 1u : (e ? 0u : 2u);
+}
+
+// Linear probing past full buckets for one lane (rare at load factor <= 0.5);
+// true when the key is found.
+__device__ __noinline__ bool lane_resolve(const Tables& t, const uint64_t* tab, uint32_t b,
+                                          uint64_t key) {
+  for (uint32_t step = 1; step <= t.bmask; ++step) {
+    b = (b + 1) & t.bmask;
+    const uint32_t st = lane_status(load_bucket(tab + (size_t)b * kSlotsPerBucket), key);
+    if (st != 2u) return st == 1u;
+  }
+  return false;
+}
+
+// Deep walk with lane probing: positions pos.. of the chain on one
+// instance, DR x 64 per step (lane l takes pos + 64 r + l), the next step's
+// keys read while the buckets are in flight.  Wave-uniform arguments;
+// returns the first position whose block the instance does not hold.
+template <bool STAGED, int DR>
+__device__ uint32_t lane_walk(const Tables& t, uint32_t inst, const ChainRef& c,
+                              const uint64_t* stage, int32_t pos, int lane) {
+  const int32_t ell = c.len;
+  const uint64_t* tab = table_of(t, inst);
+  uint64_t nk[DR];
+#pragma unroll
+  for (int r = 0; r < DR; ++r) {
+    const int32_t j = pos + r * 64 + lane;
+    nk[r] = 0ull;
+    if (j < ell) nk[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+  }
+  while (pos < ell) {
+    uint64_t key[DR];
+    uint32_t b[DR];
+    Bucket v[DR];
+#pragma unroll
+    for (int r = 0; r < DR; ++r) {
+      const int32_t j = pos + r * 64 + lane;
+      key[r] = nk[r];
+      b[r] = bucket_of(key[r], inst, t.shift);
+      v[r] = Bucket{};
+      if (j < ell && key[r] != 0ull) v[r] = load_bucket(tab + (size_t)b[r] * kSlotsPerBucket);
+    }
+    const int32_t next = pos + DR * 64;
+#pragma unroll
+    for (int r = 0; r < DR; ++r) {
+      const int32_t j = next + r * 64 + lane;
+      nk[r] = 0ull;
+      if (j < ell) nk[r] = (STAGED && j < kStage) ? stage[j] : chain_global(c, j);
+    }
+#pragma unroll
+    for (int r = 0; r < DR; ++r) {
+      const int32_t j = pos + r * 64 + lane;
+      const bool act = j < ell;
+      uint32_t st = act ? lane_status(v[r], key[r]) : 1u;
+      if (st == 2u) st = lane_resolve(t, tab, b[r], key[r]) ? 1u : 0u;
+      const uint64_t miss = __ballot(st != 1u);
+      if (miss) return (uint32_t)(pos + r * 64 + __builtin_ctzll(miss));
+    }
+    pos = next;
+  }
+  return (uint32_t)ell;
+}
+
 // One compare step of a row walk: chain positions q.. against row entries
 // k.., U x 64 of them (U per lane, coalesced).  Returns the first position
 // whose block differs from the row entry (or lies past the row's end), or

@@ -12,7 +12,6 @@ namespace ps {
 
 constexpr int kStage = 256;            // chain blocks staged in LDS per request (2 KiB)
 constexpr int kSlotsPerBucket = 8;     // 8 x 64-bit keys = one 64-byte bucket
-constexpr int kBreadthRounds = 8;      // octet loads per lane in flight: 64 instances per step
 constexpr int kDeepRounds = 2;         // octet loads per lane in flight: 16 positions per step
 constexpr int kWalkU = 4;             // row-walk positions per lane after the first step
 // Per-candidate hit slots (u16 in LDS): exact hits up to kHitMax, then two

@@ -22,7 +22,8 @@
 //                             DPP wave minima.
 //   probe_all_kernel  - diagnostic: the hit of every request on every
 //                       instance by direct probing of the per-instance tables
-//                       (breadth probe of the first block, then deep walks).
+//                       (breadth probe of the first block, then deep walks;
+//                       one lane per probe, a whole bucket per lane).
 //   commit_kernel     - ordered placement of decisions, one wave per instance.
 //
 // The path does no dense contraction, so it uses no MFMA.
@@ -79,15 +80,15 @@ __global__ void row_kernel(BuildArgs a) {
   }
 }
 
-// Hit of every request on every instance by direct probing: the first block
-// on all instances (octets of lanes over instances, 64 per step), then a
-// deep walk of each instance that holds it.
-__global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
-  static_assert(kBreadthRounds * 8 == 64, "one breadth step covers the 64 instances of a lane mask");
+// Hit of every request on every instance by direct probing, one wave per
+// request.  Lane l probes the first block on instance base + 64 r + l (BR x
+// 64 instances per step, a whole 64-byte bucket per lane), then each
+// instance that holds it is walked with DR x 64 positions per step.
+template <int BR, int DR>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void probe_all_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
   const int lane = threadIdx.x;
-  const int g = lane >> 3, s = lane & 7;
   const int32_t n_inst = a.n_inst;
   for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
     const ps_req q = a.reqs[r];
@@ -102,37 +103,34 @@ __global__ __launch_bounds__(64) void probe_all_kernel(ScoreArgs a) {
     for (int32_t j = lane; j < nst; j += 64) stage[j] = chain_global(c, j);
     __syncthreads();
     const uint64_t k0 = ell > 0 ? stage[0] : 0ull;
-    for (int32_t base = 0; base < n_inst; base += 64) {
-      const uint64_t E = __ballot(base + lane < n_inst);
-      uint64_t val[kBreadthRounds];
-      uint32_t bkt[kBreadthRounds];
+    for (int32_t base = 0; base < n_inst; base += 64 * BR) {
+      Bucket v[BR];
+      uint32_t bkt[BR];
 #pragma unroll
-      for (int rr = 0; rr < kBreadthRounds; ++rr) {
-        const int k = rr * 8 + g;
-        bkt[rr] = bucket_of(k0, (uint32_t)(base + k), a.t.shift);
-        val[rr] = 0ull;
-        if (((E >> k) & 1ull) && k0 != 0ull)
-          val[rr] = table_of(a.t, (uint32_t)(base + k))[(size_t)bkt[rr] * kSlotsPerBucket + s];
+      for (int rr = 0; rr < BR; ++rr) {
+        const uint32_t i = (uint32_t)(base + rr * 64 + lane);
+        bkt[rr] = bucket_of(k0, i, a.t.shift);
+        v[rr] = Bucket{};
+        if ((int32_t)i < n_inst && k0 != 0ull)
+          v[rr] = load_bucket(table_of(a.t, i) + (size_t)bkt[rr] * kSlotsPerBucket);
       }
-      uint64_t F = 0ull;  // bit k: instance base + k holds the first block
 #pragma unroll
-      for (int rr = 0; rr < kBreadthRounds; ++rr) {
-        const int k = rr * 8 + g;
-        const bool act = ((E >> k) & 1ull) != 0ull;
-        uint32_t st = octet_status(val[rr], k0, act, g);
-        st = octet_resolve(a.t, table_of(a.t, (uint32_t)(base + k)), bkt[rr], k0, st, s, g);
-        F |= (uint64_t)gather_octet_bits(__ballot(st == 1u && s == 0)) << (8 * rr);
+      for (int rr = 0; rr < BR; ++rr) {
+        const int32_t b0 = base + rr * 64;
+        if (b0 >= n_inst) break;
+        const uint32_t i = (uint32_t)(b0 + lane);
+        uint32_t st = (int32_t)i < n_inst ? lane_status(v[rr], k0) : 0u;
+        if (st == 2u) st = lane_resolve(a.t, table_of(a.t, i), bkt[rr], k0) ? 1u : 0u;
+        uint32_t h = st == 1u ? 1u : 0u;
+        uint64_t deep = ell > 1 ? __ballot(st == 1u) : 0ull;
+        while (deep) {
+          const int k = __builtin_ctzll(deep);
+          deep &= deep - 1;
+          const uint32_t hk = lane_walk<true, DR>(a.t, (uint32_t)(b0 + k), c, stage, 1, lane);
+          if (lane == k) h = hk;
+        }
+        if ((int32_t)i < n_inst) a.hits_out[(size_t)r * n_inst + i] = h;
       }
-      uint32_t h = (uint32_t)((F >> lane) & 1ull);
-      uint64_t deep = ell > 1 ? F : 0ull;
-      while (deep) {
-        const int k = __builtin_ctzll(deep);
-        deep &= deep - 1;
-        // 64 positions per step: deep walks dominate the walk-heavy windows
-        const uint32_t hk = deep_walk<true, 8>(a.t, (uint32_t)(base + k), c, stage, 1, g, s);
-        if (lane == k) h = hk;
-      }
-      if (base + lane < n_inst) a.hits_out[(size_t)r * n_inst + base + lane] = h;
     }
   }
 }
@@ -1281,8 +1279,10 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
                            hipStream_t s) {
   if (a.n_req == 0) return hipSuccess;
   if (probe_all) {
-    hipLaunchKernelGGL(probe_all_kernel, dim3(grid), dim3(64), (size_t)kStage * sizeof(uint64_t), s,
-                       a);
+    // two 64-instance steps of first-block probes and 128 walk positions
+    // in flight per wave (4 waves per SIMD)
+    hipLaunchKernelGGL((probe_all_kernel<2, 2>), dim3(grid), dim3(64), (size_t)kStage * sizeof(uint64_t),
+                       s, a);
     return hipGetLastError();
   }
   const size_t lds = ps_score_lds_bytes(a.n_inst);
