@@ -79,6 +79,10 @@ struct ps_ctx {
   uint32_t gslots = 0;   // power of two
   int32_t greq_cap = 0;  // entries of d_gslot
   uint64_t ggen = 0;
+  // order of the exhaustive probe's requests (counting-sort bins, order)
+  uint32_t* d_obins = nullptr;
+  int32_t* d_order = nullptr;
+  int32_t order_cap = 0;
   // optional per-launch timing of the scoring path: events recorded on the
   // call's stream before the group pass, between it and the scoring kernel,
   // and after it, for up to kTimingCalls calls
@@ -392,6 +396,8 @@ ps_status ps_destroy(ps_ctx* c) {
   dfree(c->d_grec);
   dfree(c->d_gslot);
   dfree(c->d_gpop);
+  dfree(c->d_obins);
+  dfree(c->d_order);
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
   if (c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
@@ -684,7 +690,20 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.sel = c->h_model.sel;
   a.defer_any = nullptr;
   a.defer_only = 0;
+  a.req_order = nullptr;
   const bool probe_all = d_hits != nullptr;
+  if (probe_all) {  // longest chains first
+    if (!c->d_obins)
+      HIP_TRY(c, hipMalloc((void**)&c->d_obins, kOrderAll * sizeof(uint32_t)));
+    if (n_req > c->order_cap) {
+      dfree(c->d_order);
+      c->order_cap = 0;
+      HIP_TRY(c, hipMalloc((void**)&c->d_order, (size_t)n_req * sizeof(int32_t)));
+      c->order_cap = n_req;
+    }
+    HIP_TRY(c, ps_launch_order(d_reqs, n_req, pool_len, c->d_obins, c->d_order, s));
+    a.req_order = c->d_order;
+  }
   if (!probe_all && n_req <= kGroupMaxReq && pool_len < ((int64_t)1 << kGroupGenShift) - 1) {
     ps_status st = group_buffers(c, n_req, s);
     if (st != PS_OK) return st;
@@ -705,7 +724,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   // request per wave.
   a.batch = ps_score_batch(n_req, c->num_cus * 16);
   const int batches = (n_req + a.batch - 1) / a.batch;
-  const int grid = probe_all                       ? (c->hits_in_lds ? n_req : std::min(n_req, c->scratch_rows))
+  const int grid = probe_all                       ? (n_req + kXcds * kOrderChunk - 1) / (kXcds * kOrderChunk) * (kXcds * kOrderChunk)
                    : ps_score_small(c->n_inst) ? std::min(batches, c->num_cus * 16)
                    : c->hits_in_lds            ? batches
                                                : std::min(batches, c->scratch_rows);

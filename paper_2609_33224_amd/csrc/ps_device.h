@@ -176,12 +176,25 @@ struct ScoreArgs {
   ps_result* out;
   uint32_t* sizes;       // optional |A|,|C|,|T| per request
   uint32_t* hits_out;    // probe-all diagnostic: n_req * n_inst
+  const int32_t* req_order;  // probe-all: requests taken in this order (nullptr: array order)
   uint16_t* scratch;     // per-wave hit rows when they do not fit LDS
   int32_t batch;         // requests per batch of the scoring kernel
   uint32_t sel;          // the model's selector (host copy, picks the kernels)
   uint32_t* defer_any;   // set when the lean kernel left requests to the general one
   int32_t defer_only;    // general kernel: score only requests marked as left to it
 };
+
+// Order of the exhaustive probe: requests by descending chain length in
+// bins of 256 blocks (chains of 16,128 blocks or more share the first bin),
+// then by a hash of the shared segment (256 values); invalid descriptors
+// last.  Chunks of 64 consecutive requests of the order go to the XCDs in
+// turn.
+constexpr int32_t kOrderLenBins = 64;
+constexpr int kOrderShift = 8;
+constexpr int32_t kOrderHashBins = 256;
+constexpr int32_t kOrderAll = kOrderLenBins * kOrderHashBins;
+constexpr int32_t kOrderChunk = 64;
+constexpr int32_t kXcds = 8;  // workgroups go to the XCDs in turn
 
 struct CommitArgs {
   Tables t;
@@ -249,6 +262,8 @@ hipError_t ps_exclusive_scan_u32(const uint32_t* in, uint32_t* out, int64_t n, h
 hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s);
 // Lean scorer (requests with group records); its LDS and resident waves per CU.
+hipError_t ps_launch_order(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins,
+                           int32_t* order, hipStream_t s);
 hipError_t ps_launch_lean(const ps::ScoreArgs& a, int grid, hipStream_t s);
 size_t ps_lean_lds_bytes(int32_t n_inst);
 int32_t ps_lean_waves_per_cu(int32_t n_inst);

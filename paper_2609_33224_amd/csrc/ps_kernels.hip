@@ -90,10 +90,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void pr
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
   const int lane = threadIdx.x;
   const int32_t n_inst = a.n_inst;
-  for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
+  // With an order: the order's chunks of kOrderChunk requests are dealt to
+  // the XCDs in turn (workgroup b runs on XCD b % kXcds), and each XCD takes
+  // its chunks in order.  Otherwise array order.
+  const int32_t x = (int32_t)(blockIdx.x % kXcds);
+  const int32_t gx = (int32_t)(gridDim.x / kXcds);
+  for (int32_t i = (int32_t)(blockIdx.x / kXcds), w0 = (int32_t)blockIdx.x;; i += gx, w0 += gridDim.x) {
+    const int64_t w = a.req_order ? ((int64_t)x + (int64_t)kXcds * (i / kOrderChunk)) * kOrderChunk +
+                                        i % kOrderChunk
+                                  : (int64_t)w0;
+    if (w >= a.n_req) break;
+    const int32_t r = a.req_order ? a.req_order[w] : w;
     const ps_req q = a.reqs[r];
     if (!req_valid(q, a.pool_len)) {
-      for (int32_t i = lane; i < n_inst; i += 64) a.hits_out[(size_t)r * n_inst + i] = 0xFFFFFFFFu;
+      for (int32_t k = lane; k < n_inst; k += 64) a.hits_out[(size_t)r * n_inst + k] = 0xFFFFFFFFu;
       continue;
     }
     const ChainRef c{a.pool + q.pre_off, a.pool + q.tail_off, q.pre_len, q.pre_len + q.tail_len};
@@ -133,6 +143,65 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void pr
       }
     }
   }
+}
+
+// Counting sort of the requests for the exhaustive probe: by descending
+// chain length in bins of 256 blocks, so that the longest walks start first
+// and the launch does not end on a few long walks begun late, and within a
+// length bin by a hash of the shared segment, so that requests of one
+// session sit together and share the L2 of one XCD.  Within a bin the
+// order is arbitrary: every request's hits go to its own row.
+__device__ __forceinline__ uint32_t order_bin(const ps_req& q, int64_t pool_len) {
+  if (!req_valid(q, pool_len)) return kOrderAll - 1;
+  const int64_t b = ((int64_t)q.pre_len + q.tail_len) >> kOrderShift;
+  const uint32_t lb = (uint32_t)(kOrderLenBins - 1) - (uint32_t)(b < kOrderLenBins - 1 ? b : kOrderLenBins - 1);
+  const uint32_t hb = (uint32_t)(((uint64_t)q.pre_off * 0x9E3779B97F4A7C15ull) >> 56);
+  return lb * kOrderHashBins + hb;
+}
+
+__global__ void order_clear_kernel(uint32_t* bins) {
+  for (int32_t i = threadIdx.x; i < kOrderAll; i += blockDim.x) bins[i] = 0u;
+}
+
+__global__ void order_count_kernel(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) atomicAdd(&bins[order_bin(reqs[i], pool_len)], 1u);
+}
+
+// Exclusive prefix sum of the bin counts in place (one workgroup of
+// 1,024 threads): each bin's first position in the order.
+__global__ __launch_bounds__(1024) void order_scan_kernel(uint32_t* bins) {
+  constexpr int E = kOrderAll / 1024;  // bins per thread
+  __shared__ uint32_t wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  uint32_t v[E], tot = 0u;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    v[e] = bins[tid * E + e];
+    tot += v[e];
+  }
+  const uint32_t ex = wave_exclusive_sum(tot, lane);
+  if (lane == 63) wsum[wv] = ex + tot;
+  __syncthreads();
+  if (wv == 0) {
+    const uint32_t t = lane < 16 ? wsum[lane] : 0u;
+    const uint32_t te = wave_exclusive_sum(t, lane);
+    if (lane < 16) wsum[lane] = te;
+  }
+  __syncthreads();
+  uint32_t run = wsum[wv] + ex;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int32_t k = tid * E + e;
+    bins[k] = run;
+    run += v[e];
+  }
+}
+
+__global__ void order_place_kernel(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins,
+                                   int32_t* order) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) order[atomicAdd(&bins[order_bin(reqs[i], pool_len)], 1u)] = i;
 }
 
 // Zero-hit admission threshold of the instance at key position k: the
@@ -1292,6 +1361,18 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
     hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
   else
     hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t ps_launch_order(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins,
+                           int32_t* order, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(order_clear_kernel, dim3(1), dim3(1024), 0, s, bins);
+  hipLaunchKernelGGL(order_count_kernel, dim3(blocks), dim3(256), 0, s, reqs, n, pool_len, bins);
+  hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, s, bins);
+  hipLaunchKernelGGL(order_place_kernel, dim3(blocks), dim3(256), 0, s, reqs, n, pool_len, bins,
+                     order);
   return hipGetLastError();
 }
 
