@@ -11,9 +11,12 @@ The roofline block is the scoring pass's (lean + general kernels):
 algorithmic bytes from `score_bytes` over the library's HIP-event time on
 the launch stream.  The probe_kernel block is the exhaustive probe kernel's
 (ps_probe_hits_dev): one 64-byte bucket per probe, min(hit + 1, chain
-length) probes per (request, instance) pair, plus the staged chain head.
-`traffic` comes from the committed rocprofv3 counter summary of the same
-kernel sources, or is null.
+length) probes per (request, instance) pair, plus the staged chain head;
+its measured_bytes are the HBM-side bytes of its dispatches per window
+(rocprofv3 FETCH_SIZE and WRITE_SIZE, scaled as for `traffic`), below the
+algorithmic bytes where requests that share a segment hit in the caches.
+`traffic` and measured_bytes come from the committed rocprofv3 counter
+summary of the same kernel sources, or are null.
 """
 from __future__ import annotations
 
@@ -360,7 +363,7 @@ def traffic_for(workload: str, src_hash: str):
     ent = t.get(workload)
     if not ent or ent.get("kernel_source_sha") != src_hash:
         return None
-    return ent.get("bytes_per_launch")
+    return ent
 
 
 def cpu_baseline(win, budget_s: float):
@@ -586,7 +589,9 @@ def main():
 
     evals = win.n_req * win.n_inst
     src_hash = kernel_source_hash()
-    traffic = traffic_for(args.workload, src_hash)
+    tent = traffic_for(args.workload, src_hash) or {}
+    traffic = tent.get("bytes_per_launch")
+    probe_meas = tent.get("probe_bytes_per_window")
     def rate(nbytes, ms):
         return nbytes / (ms * 1e-3) / 1e9 if nbytes is not None and ms > 0 else None
 
@@ -626,6 +631,10 @@ def main():
                          "algorithmic_bytes": probe_alg_bytes,
                          "achieved_GBs": probe_gbs,
                          "frac_of_hbm_peak": probe_gbs / HBM_PEAK_GBS if probe_gbs is not None else None,
+                         "measured_bytes": probe_meas,
+                         "measured_GBs": rate(probe_meas, probe_ms),
+                         "measured_frac_of_hbm_peak": (rate(probe_meas, probe_ms) / HBM_PEAK_GBS
+                                                       if probe_meas is not None else None),
                          "evals_per_s": win.n_req * win.n_inst / (probe_ms * 1e-3)},
         "kernel_source_sha": src_hash,
         "load_instances_s": load_s,

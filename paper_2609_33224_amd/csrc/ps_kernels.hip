@@ -163,9 +163,38 @@ __global__ void order_clear_kernel(uint32_t* bins) {
   for (int32_t i = threadIdx.x; i < kOrderAll; i += blockDim.x) bins[i] = 0u;
 }
 
+// Lanes of a wave with the same bin add to it once (one lane, the count of
+// them): a popular session would otherwise serialise thousands of atomics on
+// one bin.  Returns, in every active lane, the bin's old value plus the
+// lane's rank among those lanes.
+__device__ __forceinline__ uint32_t wave_bin_add(uint32_t* bins, uint32_t bin, bool act) {
+  const int lane = threadIdx.x & 63;
+  // each lane's leader (the lowest lane with its bin), rank and, in the
+  // leader, the count: ballots only
+  uint64_t todo = __ballot(act);
+  int leader = lane;
+  uint32_t rank = 0u, cnt = 0u;
+  while (todo) {
+    const int src = __builtin_ctzll(todo);
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)bin, src);
+    const uint64_t same = __ballot(act && bin == b);
+    todo &= ~same;
+    if (act && bin == b) {
+      leader = src;
+      rank = (uint32_t)__popcll(same & ((1ull << lane) - 1ull));
+      cnt = (uint32_t)__popcll(same);
+    }
+  }
+  // then all leaders' atomics at once
+  uint32_t base = 0u;
+  if (act && leader == lane) base = atomicAdd(&bins[bin], cnt);
+  return (uint32_t)__shfl((int)base, leader) + rank;
+}
+
 __global__ void order_count_kernel(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) atomicAdd(&bins[order_bin(reqs[i], pool_len)], 1u);
+  const bool act = i < n;
+  (void)wave_bin_add(bins, act ? order_bin(reqs[i], pool_len) : 0u, act);
 }
 
 // Exclusive prefix sum of the bin counts in place (one workgroup of
@@ -201,7 +230,9 @@ __global__ __launch_bounds__(1024) void order_scan_kernel(uint32_t* bins) {
 __global__ void order_place_kernel(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins,
                                    int32_t* order) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) order[atomicAdd(&bins[order_bin(reqs[i], pool_len)], 1u)] = i;
+  const bool act = i < n;
+  const uint32_t pos = wave_bin_add(bins, act ? order_bin(reqs[i], pool_len) : 0u, act);
+  if (act) order[pos] = i;
 }
 
 // Zero-hit admission threshold of the instance at key position k: the
