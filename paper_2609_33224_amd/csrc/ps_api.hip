@@ -46,6 +46,7 @@ struct ps_ctx {
   InstState* d_inst_key = nullptr;  // states in d_order0's order
   TopRoom* d_rtop = nullptr;         // the kTopRooms largest rooms with their ids
   int32_t lean_wpc = 0;              // resident lean-scorer waves per CU (0: not asked yet)
+  int32_t rows_wpc = 0;              // the same for the four-requests-per-wave scorer
   int4* d_lm = nullptr;              // zero-hit admission thresholds in that order
   int32_t* d_lm1 = nullptr;          // their maxima per 64 positions
   GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
@@ -591,6 +592,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->d_inst_key = fresh.d_inst_key;
   c->d_rtop = fresh.d_rtop;
   c->lean_wpc = 0;
+  c->rows_wpc = 0;
   c->d_lm = fresh.d_lm;
   c->d_lm1 = fresh.d_lm1;
   c->x = fresh.x;
@@ -746,7 +748,16 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   // the selector is neither Random nor H-C-Q (persistent grid at its own
   // occupancy); the general scorer then finishes what it left.
   const bool lean = !probe_all && a.grp.keys && a.sel != PS_SEL_RANDOM && a.sel != PS_SEL_HCQ;
-  if (lean) {
+  const DevModel& hm = c->h_model;
+  const bool rows = lean && !d_sizes && hm.mono && !(hm.flags & PS_F_TTFT_ADMIT) &&
+                    (a.sel == PS_SEL_DCQ || a.sel == PS_SEL_DQ || a.sel == PS_SEL_DQC) &&
+                    c->n_inst <= kRowsMaxInst;
+  if (rows) {  // four requests per wave
+    if (!c->rows_wpc) c->rows_wpc = ps_lean_rows_waves_per_cu(c->n_inst);
+    const int resident = c->num_cus * c->rows_wpc;
+    HIP_TRY(c, ps_launch_lean_rows(a, std::min((n_req + 3) / 4, resident), s));
+    a.defer_only = 1;
+  } else if (lean) {
     if (!c->lean_wpc) c->lean_wpc = ps_lean_waves_per_cu(c->n_inst);
     const int resident = c->num_cus * c->lean_wpc;
     ScoreArgs la = a;

@@ -261,9 +261,17 @@ hipError_t ps_launch_rows(const ps::BuildArgs& a, hipStream_t s);   // rows, row
 hipError_t ps_exclusive_scan_u32(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t s);
 hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
                            hipStream_t s);
-// Lean scorer (requests with group records); its LDS and resident waves per CU.
+// Order of the exhaustive probe's requests (bins: kOrderAll words).
 hipError_t ps_launch_order(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins,
                            int32_t* order, hipStream_t s);
+// The lean scorer with four requests per wave (rows of 16 lanes), for the
+// keyed selectors with a monotone model, no TTFT admission, no candidate-set
+// sizes and at most kRowsMaxInst instances; its LDS and resident waves per CU.
+constexpr int32_t kRowsMaxInst = 4096;
+hipError_t ps_launch_lean_rows(const ps::ScoreArgs& a, int grid, hipStream_t s);
+size_t ps_lean_rows_lds_bytes(int32_t n_inst);
+int32_t ps_lean_rows_waves_per_cu(int32_t n_inst);
+// Lean scorer (requests with group records); its LDS and resident waves per CU.
 hipError_t ps_launch_lean(const ps::ScoreArgs& a, int grid, hipStream_t s);
 size_t ps_lean_lds_bytes(int32_t n_inst);
 int32_t ps_lean_waves_per_cu(int32_t n_inst);

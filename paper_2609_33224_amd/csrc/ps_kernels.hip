@@ -1260,6 +1260,258 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   if (deferred_any && lane == 0) atomicOr(a.defer_any, 1u);
 }
 
+// ------------------------------------------------------- lean scorer, rows
+// The lean scorer with four requests per wave, one per row of 16 lanes:
+// lane t of a row takes holder t of its request's record (at most
+// kGroupHold = 16) and entries t, t + 16, t + 32, t + 48 of a chunk of
+// zero-hit thresholds, so one wave-wide instruction serves four requests.
+// Row reductions are DPP shifts inside the row.  It serves the common case
+// of the keyed selectors (D-C-Q, D-Q, D-Q-C) with a monotone model, no TTFT
+// admission and no candidate-set sizes, on pools of at most 4,096
+// instances.  When no candidate is in T while the zero-hit class is in C,
+// the row scans the whole class for its fallback keys.
+
+// Minimum over the 16 lanes of each row, in every lane of the row.
+__device__ __forceinline__ uint32_t row_min_u32(uint32_t v) {
+  min32_step<0x111, 0xF>(v);  // row_shr:1
+  min32_step<0x112, 0xF>(v);  // row_shr:2
+  min32_step<0x114, 0xF>(v);  // row_shr:4
+  min32_step<0x118, 0xF>(v);  // row_shr:8
+  return (uint32_t)__shfl((int)v, (int)((threadIdx.x & 48u) | 15u));
+}
+
+__device__ __forceinline__ uint64_t row_min_u64(uint64_t v) {
+  min_step<0x111, 0xF>(v);
+  min_step<0x112, 0xF>(v);
+  min_step<0x114, 0xF>(v);
+  min_step<0x118, 0xF>(v);
+  const int src = (int)((threadIdx.x & 48u) | 15u);
+  const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src);
+  const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// This lane's row's 16 bits of a ballot.
+__device__ __forceinline__ uint32_t row_bits(uint64_t b) {
+  return (uint32_t)(b >> (threadIdx.x & 48u)) & 0xFFFFu;
+}
+
+__device__ __forceinline__ int64_t lane_value64(int64_t v, int src) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), src);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+template <bool SMALL>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void lean_rows_kernel(ScoreArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int32_t n_inst = a.n_inst;
+  const int32_t nw = (n_inst + 63) >> 6;
+  const int32_t nwp = (nw + 1) & ~1;
+  uint64_t* bmall = reinterpret_cast<uint64_t*>(smem);                      // 4 holder bitmaps
+  InstState* linst = reinterpret_cast<InstState*>(bmall + 4 * (size_t)nwp);  // SMALL: states by id
+  int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);                    // SMALL: thresholds
+  const int lane = threadIdx.x;
+  const int q = lane >> 4, t = lane & 15;
+  const int g = lane >> 3, s = lane & 7;
+  const DevModel& m = *a.model;
+  uint64_t* bmH = bmall + (size_t)q * nwp;  // this row's request's holders
+  for (int32_t w = lane; w < 4 * nwp; w += 64) bmall[w] = 0ull;
+  const TopRoom trm = a.rtop[lane];
+  const int64_t room0 = lane_value64(trm.room, 0);   // the largest room
+  const int64_t room63 = lane_value64(trm.room, 63);  // the 64th largest
+  const int32_t n1 = (n_inst + 63) >> 6;  // <= 64
+  const int32_t lm1r = lane < n1 ? a.lm1[lane] : -1;
+  if (SMALL && lane < n_inst) {
+    linst[lane] = a.inst[lane];
+    llm[lane] = a.lm[lane];
+  }
+  __syncthreads();
+  auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
+  bool deferred_any = false;
+
+  for (int32_t rb = blockIdx.x * 4; rb < a.n_req; rb += gridDim.x * 4) {
+    const int32_t r = rb + q;
+    const bool inr = r < a.n_req;
+    // descriptor and slot (every lane of a row reads its row's), then the record
+    ps_req qd{0, 0, 0, 0};
+    uint32_t gso = kGroupNoSlot;
+    if (inr) {
+      qd = a.reqs[r];
+      gso = a.grp.slot_of[r];
+    }
+    const bool valid = inr && req_valid(qd, a.pool_len);
+    uint32_t cnt = kGroupNone;
+    uint2 hd = make_uint2(0u, 0u);
+    if (valid && gso != kGroupNoSlot) {
+      const uint2* grec = a.grp.rec + (size_t)(gso & ~kGroupLead) * kGroupRec;
+      cnt = grec[0].y;
+      hd = grec[1 + t];
+    }
+    const ChainRef c{a.pool + qd.pre_off, a.pool + qd.tail_off, qd.pre_len, qd.pre_len + qd.tail_len};
+    const int32_t ell = c.len;
+    const int64_t L = (int64_t)ell * m.bs;
+    const float Lf = (float)L;
+    const int32_t p = qd.pre_len;
+    // 0 scored here, 1 invalid, 2 left to the general kernel, 3 rejected
+    uint32_t fate = !inr ? 4u : !valid ? 1u : (cnt == kGroupNone || (cnt & kGroupPop)) ? 2u
+                                   : !(room0 >= L) ? 3u : 0u;
+    const bool live = fate == 0u;
+    // the first chunk of zero-hit thresholds that admits this length
+    uint64_t cm = 0ull;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t ek = __builtin_amdgcn_readlane(ell, 16 * k);
+      const uint64_t b = __ballot(lane < n1 && lm1r >= ek);
+      if (q == k) cm = b;
+    }
+    if (!live) cm = 0ull;
+    int4 e[4];
+    auto load_chunk = [&](uint64_t cmask) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        e[u] = make_int4(-1, 0, 0, 0);
+        if (cmask) {
+          const int32_t k = (int32_t)__builtin_ctzll(cmask) * 64 + 16 * u + t;
+          if (k < n_inst) e[u] = SMALL ? llm[k] : a.lm[k];
+        }
+      }
+    };
+    load_chunk(cm);
+    // holders: state (and with it eligibility) and hit; the row's bitmap
+    InstState hst{};
+    bool el = false;
+    uint32_t id = 0, hit = 0;
+    if (live && (uint32_t)t < cnt) {
+      id = hd.x;
+      hit = hd.y;
+      hst = state_of(id);
+      el = eligible(m, hst.A1, hst.S, L);
+      atomicOr(reinterpret_cast<unsigned long long*>(&bmH[id >> 6]), 1ull << (id & 63));
+    }
+    __syncthreads();
+    // hits that reach the request's segment end continue on its tail
+    uint64_t need = __ballot(el && (int32_t)hit >= p);
+    while (need) {
+      const int k = __builtin_ctzll(need);
+      need &= need - 1;
+      const int kr = k & 48;
+      const ps_req qk{lane_value64(qd.pre_off, kr), lane_value64(qd.tail_off, kr),
+                      __builtin_amdgcn_readlane(qd.pre_len, kr), __builtin_amdgcn_readlane(qd.tail_len, kr)};
+      const ChainRef ck{a.pool + qk.pre_off, a.pool + qk.tail_off, qk.pre_len, qk.pre_len + qk.tail_len};
+      const uint32_t idk = (uint32_t)__builtin_amdgcn_readlane((int)id, k);
+      const uint32_t hk = run_walk<false>(a.t, idk, ck, nullptr, qk.pre_len, g, s);
+      if (lane == k) hit = hk;
+    }
+    // some eligible instance holds nothing (exact from the 64 largest rooms:
+    // 64 eligible ones cannot all be among at most 16 holders)
+    bool any0 = false;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t Lk = lane_value64(L, 16 * k);
+      const uint64_t* bmk = bmall + (size_t)k * nwp;
+      const bool ok = __ballot(trm.room >= Lk && !test_bit(bmk, (uint32_t)trm.id)) != 0ull || room63 >= Lk;
+      if (q == k) any0 = ok;
+    }
+    // minimum recomputation penalty over A
+    const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
+    const float W0 = fmaxf(0.0f, Z);
+    uint32_t wb = 0x7F800000u;
+    if (el) wb = __float_as_uint(fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)hit * m.bs), Lf)));
+    if (any0 && t == 0) wb = wb < __float_as_uint(W0) ? wb : __float_as_uint(W0);
+    const float wmin = __uint_as_float(row_min_u32(wb));
+    const float tpf_cold = t_prefill(m, Lf, 0.0f);
+    const float slo = fmaxf(m.ttft_floor, tpf_cold);
+    const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+    const bool admit0 = live && any0 && (!kvc || (W0 - wmin) / Z <= m.eta);
+    Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
+    if (el) evaluate_with(m, acc, id, hit, [&]() { return hst; }, L, Lf, wmin, Z, kvc, slo);
+    // the hit-0 class: eligible non-holders, one penalty W(L); its first
+    // admitted member in key order
+    bool searching = admit0 && cm != 0ull;
+    bool found0 = false;
+    while (__ballot(searching) != 0ull) {
+      uint32_t jmin = 64u;
+#pragma unroll
+      for (int u = 3; u >= 0; --u) {
+        const uint32_t f = row_bits(__ballot(searching && e[u].x >= ell && !test_bit(bmH, (uint32_t)e[u].y)));
+        if (f) jmin = 16u * u + (uint32_t)__builtin_ctz(f);
+      }
+      if (searching && jmin < 64u) {
+        searching = false;
+        found0 = true;
+        if ((uint32_t)t == (jmin & 15u)) {
+          const uint32_t uw = jmin >> 4;
+          const int4 ew = uw == 0 ? e[0] : uw == 1 ? e[1] : uw == 2 ? e[2] : e[3];
+          InstState kst{};
+          kst.D = ew.z;
+          kst.Q = ew.w;
+          const uint64_t kt = select_key(m.sel, kst, 0u, (uint32_t)ew.y, 0ull);
+          acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+        }
+      } else if (searching) {  // the next chunk whose maximum admits this length
+        cm &= cm - 1;
+        searching = cm != 0ull;
+      }
+      load_chunk(searching ? cm : 0ull);
+    }
+    uint64_t keyT = row_min_u64(acc.keyT);
+    // no candidate in T while the class is in C: its fallback keys need the
+    // whole class (16 lanes over the pool, two states in flight per lane)
+    const bool scan = live && keyT == ~0ull && admit0 && !found0;
+    if (__ballot(scan) != 0ull) {
+      for (int32_t base = 0; base < n_inst; base += 32) {
+        InstState st[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int32_t i = base + 16 * u + t;
+          if (scan && i < n_inst) st[u] = state_of((uint32_t)i);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int32_t i = base + 16 * u + t;
+          if (scan && i < n_inst && !test_bit(bmH, (uint32_t)i) && eligible(m, st[u].A1, st[u].S, L))
+            evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return st[u]; }, L, Lf, wmin, Z, kvc, slo);
+        }
+      }
+      keyT = row_min_u64(acc.keyT);
+    }
+    const uint64_t kF = row_min_u64(acc.keyF);
+    const uint64_t keyF = keyT == ~0ull ? kF : ~0ull;
+    ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+    if (fate == 0u && (keyT != ~0ull || keyF != ~0ull)) {
+      const bool tt = keyT != ~0ull;
+      const uint32_t best = (uint32_t)((tt ? keyT : keyF) & 0xFFFFu);
+      const uint32_t hb = row_bits(__ballot(el && id == best));
+      const int src = (lane & 48) + (hb ? __builtin_ctz(hb) : 0);
+      const InstState sst = shfl_state(hst, src);
+      const uint32_t sv = (uint32_t)__shfl((int)hit, src);
+      InstState bs{};
+      uint32_t v = 0;
+      if (hb) {
+        bs = sst;
+        v = sv;
+      } else {
+        bs = state_of(best);
+      }
+      const int64_t c_tok = (int64_t)v * m.bs;
+      const Lat lt = latency(m, bs, (float)(L - c_tok), (float)c_tok, L);
+      res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot,
+                      (tt ? 0u : PS_R_FALLBACK) | (lt.ttft > slo ? PS_R_TTFT_MISS : 0u)};
+    }
+    if (t == 0 && fate != 4u) {
+      if (fate == 1u) a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
+      else if (fate == 2u) a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, kDeferred};
+      else a.out[r] = res;
+    }
+    if (fate == 2u) deferred_any = true;
+    __syncthreads();
+    if (live && (uint32_t)t < cnt) bmH[id >> 6] = 0ull;
+    __syncthreads();
+  }
+  if (__ballot(deferred_any) != 0ull && lane == 0) atomicOr(a.defer_any, 1u);
+}
+
 // One wave per instance that receives placements; its entries are applied
 // in array order, each measured against the table as the earlier entries
 // left it.
@@ -1414,6 +1666,32 @@ hipError_t ps_launch_lean(const ScoreArgs& a, int grid, hipStream_t s) {
     hipLaunchKernelGGL(lean_kernel<true>, dim3(grid), dim3(64), lds, s, a);
   else
     hipLaunchKernelGGL(lean_kernel<false>, dim3(grid), dim3(64), lds, s, a);
+  return hipGetLastError();
+}
+
+size_t ps_lean_rows_lds_bytes(int32_t n_inst) {
+  const size_t nw = ((size_t)n_inst + 63) / 64;
+  return 4 * ((nw + 1) & ~(size_t)1) * sizeof(uint64_t) +
+         (ps_score_small(n_inst) ? (size_t)kSmallPool * (sizeof(InstState) + sizeof(int4)) : 0);
+}
+
+int32_t ps_lean_rows_waves_per_cu(int32_t n_inst) {
+  int blocks = 0;
+  const size_t lds = ps_lean_rows_lds_bytes(n_inst);
+  const hipError_t e =
+      ps_score_small(n_inst)
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, lean_rows_kernel<true>, 64, lds)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, lean_rows_kernel<false>, 64, lds);
+  return e == hipSuccess && blocks > 0 ? blocks : 16;
+}
+
+hipError_t ps_launch_lean_rows(const ScoreArgs& a, int grid, hipStream_t s) {
+  if (a.n_req == 0) return hipSuccess;
+  const size_t lds = ps_lean_rows_lds_bytes(a.n_inst);
+  if (ps_score_small(a.n_inst))
+    hipLaunchKernelGGL(lean_rows_kernel<true>, dim3(grid), dim3(64), lds, s, a);
+  else
+    hipLaunchKernelGGL(lean_rows_kernel<false>, dim3(grid), dim3(64), lds, s, a);
   return hipGetLastError();
 }
 
