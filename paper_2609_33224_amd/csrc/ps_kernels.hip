@@ -762,18 +762,26 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         // pool, resumes walked one at a time
         const uint32_t* hp = a.grp.pop + (size_t)(gm.cnt & ~kGroupPop) * (size_t)n_inst;
         const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
-        for (int32_t base = 0; base < n_inst; base += 64) {
-          const int32_t i = base + lane;
-          const bool cand = i < n_inst && test_bit(bmC, (uint32_t)i);
-          uint32_t v = cand ? hp[i] : 0u;
-          uint64_t need = __ballot(cand && (int32_t)v >= p0);
-          while (need) {
-            const int k = __builtin_ctzll(need);
-            need &= need - 1;
-            const uint32_t hk = run_walk<false>(a.t, (uint32_t)(base + k), c, nullptr, p0, g, s);
-            if (lane == k) v = hk;
+        for (int32_t base = 0; base < n_inst; base += 256) {  // four steps in flight
+          bool cand[4];
+          uint32_t v[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int32_t i = base + 64 * u + lane;
+            cand[u] = i < n_inst && test_bit(bmC, (uint32_t)i);
+            v[u] = cand[u] ? hp[i] : 0u;
           }
-          if (cand) hits[i] = encode_hit(v);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            uint64_t need = __ballot(cand[u] && (int32_t)v[u] >= p0);
+            while (need) {
+              const int k = __builtin_ctzll(need);
+              need &= need - 1;
+              const uint32_t hk = run_walk<false>(a.t, (uint32_t)(base + 64 * u + k), c, nullptr, p0, g, s);
+              if (lane == k) v[u] = hk;
+            }
+            if (cand[u]) hits[base + 64 * u + lane] = encode_hit(v[u]);
+          }
         }
         __syncthreads();
       }
