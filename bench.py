@@ -182,19 +182,20 @@ def score_bytes(win, r0, hits, grp=None):
     """Algorithmic bytes the scoring pass moves for requests r0 .. r0 +
     len(hits) (the benchmark's policy: D-C-Q, monotone model, no set sizes).
 
-    Requests whose group record holds their hits go through the lean kernel:
-    24 B descriptor + 4 B group slot + 136 B record + 20 B result; for pools
-    above 64 instances 32 B of state per holder of the first block (that
-    read also decides eligibility) and 64 x (16 B threshold + 32 B key-
-    ordered state) per chunk of zero-hit thresholds read (the first chunk
-    that admits the request's length is read in any case, later ones until
-    an admitted non-holder is found); a resume walk on each candidate whose
-    shared segment is cached to the request's segment end (a probe with its
-    row position, 16 B per compared position, a final probe); when no
-    member of the hit-0 class and no candidate is in T, the states of all
-    non-holders.  Pools of at most 64 instances keep states and thresholds
-    in LDS (no bytes).  The rooms and threshold maxima are read once per
-    wave (not counted).
+    Requests whose group record holds their hits go through the lean kernel
+    (four requests per wave): 24 B descriptor + 4 B group slot + 136 B
+    record + 20 B result; for pools above 64 instances 32 B of state per
+    holder of the first block (that read also decides eligibility), 64 x
+    16 B per chunk of zero-hit thresholds read (the first chunk that admits
+    the request's length is read in any case, later ones until an admitted
+    non-holder is found) and 32 B for the chosen instance's state when an
+    admitted non-holder is found (an upper bound: it is read only when that
+    instance wins); a resume walk on each candidate whose shared segment is
+    cached to the request's segment end (a probe with its row position, 16
+    B per compared position, a final probe); when no member of the hit-0
+    class and no candidate is in T, the states of all instances.  Pools of
+    at most 64 instances keep states and thresholds in LDS (no bytes).  The
+    rooms and threshold maxima are read once per wave (not counted).
 
     Other requests go through the general kernel: descriptor, slot, result;
     the 64-way search of the sorted rooms; with a popular group row the
@@ -283,7 +284,7 @@ def score_bytes(win, r0, hits, grp=None):
     seg = np.searchsorted(ub, A1, side="left")
     seg = np.minimum(seg, len(ub) - 1)
     order0 = np.lexsort((np.arange(N), win.Q, -win.D.astype(np.int64)))
-    chunk_lean = 0 if small else 64 * (16 + 32)
+    chunk_lean = 0 if small else 64 * 16
     for r in np.nonzero(act & (admit0 | lean))[0]:
         t_iter = gam[seg] * (beta[seg, 0] + beta[seg, 1] * A1 + beta[seg, 2] * (win.S + L[r]))
         tpot0 = t_iter + np.where(A1 > 1, _tpf(a, float(L[r]), 0.0) / lout1, 0.0)
@@ -298,7 +299,7 @@ def score_bytes(win, r0, hits, grp=None):
             if not admit0[r]:  # only the speculative first chunk
                 by[r] += chunk_lean if passing.any() else 0
                 continue
-            by[r] += chunk_lean * int(passing[:cs + 1].sum())
+            by[r] += chunk_lean * int(passing[:cs + 1].sum()) + (0 if small or not found else 32)
         else:
             by[r] += 256 * (cs // 64 + 1) + 1024 * int(passing[:cs + 1].sum())
         if found:
@@ -311,7 +312,7 @@ def score_bytes(win, r0, hits, grp=None):
             if (tp < tau).any():
                 continue
         if lean[r]:
-            by[r] += 0 if small else 32 * (N - int(cnt0[r])) + 32
+            by[r] += 0 if small else 32 * N + 32
         else:
             by[r] += 8 * N + 32 * int(zero.sum())
     return int(by.sum())
@@ -614,7 +615,7 @@ def main():
                    "n_inst": win.n_inst, "n_req": win.n_req, "seed": args.seed},
         "decisions_per_s": win.n_req / (ms_per_step * 1e-3),
         "step_ms_events": step_avg,
-        "kernel": "score_kernel, lean pass + general pass (prefix hits from the group records, latency model, filters, keys)",
+        "kernel": "scoring pass: lean_rows_kernel (four requests per wave) + general score_kernel (prefix hits from the group records, latency model, filters, keys)",
         "kernel_ms_avg": kern_avg,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS if achieved is not None else None,

@@ -1317,7 +1317,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   const int32_t nw = (n_inst + 63) >> 6;
   const int32_t nwp = (nw + 1) & ~1;
   uint64_t* bmall = reinterpret_cast<uint64_t*>(smem);                      // 4 holder bitmaps
-  InstState* linst = reinterpret_cast<InstState*>(bmall + 4 * (size_t)nwp);  // SMALL: states by id
+  TopRoom* ltop = reinterpret_cast<TopRoom*>(bmall + 4 * (size_t)nwp);        // the 64 largest rooms
+  int32_t* llm1 = reinterpret_cast<int32_t*>(ltop + kTopRooms);              // threshold chunk maxima
+  InstState* linst = reinterpret_cast<InstState*>(llm1 + 64);                // SMALL: states by id
   int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);                    // SMALL: thresholds
   const int lane = threadIdx.x;
   const int q = lane >> 4, t = lane & 15;
@@ -1325,16 +1327,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   const DevModel& m = *a.model;
   uint64_t* bmH = bmall + (size_t)q * nwp;  // this row's request's holders
   for (int32_t w = lane; w < 4 * nwp; w += 64) bmall[w] = 0ull;
-  const TopRoom trm = a.rtop[lane];
-  const int64_t room0 = lane_value64(trm.room, 0);   // the largest room
-  const int64_t room63 = lane_value64(trm.room, 63);  // the 64th largest
+  // window constants in LDS (read again per request: registers are scarce)
+  {
+    const TopRoom tr = a.rtop[lane];
+    ltop[lane] = tr;
+  }
   const int32_t n1 = (n_inst + 63) >> 6;  // <= 64
-  const int32_t lm1r = lane < n1 ? a.lm1[lane] : -1;
+  llm1[lane] = lane < n1 ? a.lm1[lane] : -1;
   if (SMALL && lane < n_inst) {
     linst[lane] = a.inst[lane];
     llm[lane] = a.lm[lane];
   }
   __syncthreads();
+  const int64_t room0 = ltop[0].room;    // the largest room
+  const int64_t room63 = ltop[63].room;  // the 64th largest
   auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
   bool deferred_any = false;
 
@@ -1370,22 +1376,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int32_t ek = __builtin_amdgcn_readlane(ell, 16 * k);
-      const uint64_t b = __ballot(lane < n1 && lm1r >= ek);
+      const uint64_t b = __ballot(lane < n1 && llm1[lane] >= ek);
       if (q == k) cm = b;
     }
     if (!live) cm = 0ull;
-    int4 e[4];
-    auto load_chunk = [&](uint64_t cmask) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        e[u] = make_int4(-1, 0, 0, 0);
-        if (cmask) {
-          const int32_t k = (int32_t)__builtin_ctzll(cmask) * 64 + 16 * u + t;
-          if (k < n_inst) e[u] = SMALL ? llm[k] : a.lm[k];
-        }
-      }
-    };
-    load_chunk(cm);
+    // entries t + 16 u of the chunk (kept in registers: no array escapes)
+    int4 e0, e1, e2, e3;
+#define PS_ROWS_LOAD_CHUNK(cmask)                                                  \
+    do {                                                                           \
+      const uint64_t cmk = (cmask);                                                \
+      const int32_t k0 = cmk ? (int32_t)__builtin_ctzll(cmk) * 64 + t : n_inst;   \
+      e0 = k0 < n_inst ? (SMALL ? llm[k0] : a.lm[k0]) : make_int4(-1, 0, 0, 0);   \
+      e1 = k0 + 16 < n_inst ? (SMALL ? llm[k0 + 16] : a.lm[k0 + 16]) : make_int4(-1, 0, 0, 0); \
+      e2 = k0 + 32 < n_inst ? (SMALL ? llm[k0 + 32] : a.lm[k0 + 32]) : make_int4(-1, 0, 0, 0); \
+      e3 = k0 + 48 < n_inst ? (SMALL ? llm[k0 + 48] : a.lm[k0 + 48]) : make_int4(-1, 0, 0, 0); \
+    } while (0)
+    PS_ROWS_LOAD_CHUNK(cm);
     // holders: state (and with it eligibility) and hit; the row's bitmap
     InstState hst{};
     bool el = false;
@@ -1408,18 +1414,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
                       __builtin_amdgcn_readlane(qd.pre_len, kr), __builtin_amdgcn_readlane(qd.tail_len, kr)};
       const ChainRef ck{a.pool + qk.pre_off, a.pool + qk.tail_off, qk.pre_len, qk.pre_len + qk.tail_len};
       const uint32_t idk = (uint32_t)__builtin_amdgcn_readlane((int)id, k);
-      const uint32_t hk = run_walk<false>(a.t, idk, ck, nullptr, qk.pre_len, g, s);
+      const uint32_t hk = run_walk<false, 2, 2>(a.t, idk, ck, nullptr, qk.pre_len, g, s);
       if (lane == k) hit = hk;
     }
     // some eligible instance holds nothing (exact from the 64 largest rooms:
     // 64 eligible ones cannot all be among at most 16 holders)
     bool any0 = false;
+    {
+      const TopRoom trm = ltop[lane];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int64_t Lk = lane_value64(L, 16 * k);
-      const uint64_t* bmk = bmall + (size_t)k * nwp;
-      const bool ok = __ballot(trm.room >= Lk && !test_bit(bmk, (uint32_t)trm.id)) != 0ull || room63 >= Lk;
-      if (q == k) any0 = ok;
+      for (int k = 0; k < 4; ++k) {
+        const int64_t Lk = lane_value64(L, 16 * k);
+        const uint64_t* bmk = bmall + (size_t)k * nwp;
+        const bool ok = __ballot(trm.room >= Lk && !test_bit(bmk, (uint32_t)trm.id)) != 0ull || room63 >= Lk;
+        if (q == k) any0 = ok;
+      }
     }
     // minimum recomputation penalty over A
     const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
@@ -1440,17 +1449,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
     bool found0 = false;
     while (__ballot(searching) != 0ull) {
       uint32_t jmin = 64u;
-#pragma unroll
-      for (int u = 3; u >= 0; --u) {
-        const uint32_t f = row_bits(__ballot(searching && e[u].x >= ell && !test_bit(bmH, (uint32_t)e[u].y)));
-        if (f) jmin = 16u * u + (uint32_t)__builtin_ctz(f);
+      {
+        const uint32_t f3 = row_bits(__ballot(searching && e3.x >= ell && !test_bit(bmH, (uint32_t)e3.y)));
+        const uint32_t f2 = row_bits(__ballot(searching && e2.x >= ell && !test_bit(bmH, (uint32_t)e2.y)));
+        const uint32_t f1 = row_bits(__ballot(searching && e1.x >= ell && !test_bit(bmH, (uint32_t)e1.y)));
+        const uint32_t f0 = row_bits(__ballot(searching && e0.x >= ell && !test_bit(bmH, (uint32_t)e0.y)));
+        if (f3) jmin = 48u + (uint32_t)__builtin_ctz(f3);
+        if (f2) jmin = 32u + (uint32_t)__builtin_ctz(f2);
+        if (f1) jmin = 16u + (uint32_t)__builtin_ctz(f1);
+        if (f0) jmin = (uint32_t)__builtin_ctz(f0);
       }
       if (searching && jmin < 64u) {
         searching = false;
         found0 = true;
         if ((uint32_t)t == (jmin & 15u)) {
           const uint32_t uw = jmin >> 4;
-          const int4 ew = uw == 0 ? e[0] : uw == 1 ? e[1] : uw == 2 ? e[2] : e[3];
+          const int4 ew = uw == 0 ? e0 : uw == 1 ? e1 : uw == 2 ? e2 : e3;
           InstState kst{};
           kst.D = ew.z;
           kst.Q = ew.w;
@@ -1461,25 +1475,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
         cm &= cm - 1;
         searching = cm != 0ull;
       }
-      load_chunk(searching ? cm : 0ull);
+      PS_ROWS_LOAD_CHUNK(searching ? cm : 0ull);
     }
+#undef PS_ROWS_LOAD_CHUNK
     uint64_t keyT = row_min_u64(acc.keyT);
     // no candidate in T while the class is in C: its fallback keys need the
-    // whole class (16 lanes over the pool, two states in flight per lane)
+    // whole class (16 lanes over the pool)
     const bool scan = live && keyT == ~0ull && admit0 && !found0;
     if (__ballot(scan) != 0ull) {
-      for (int32_t base = 0; base < n_inst; base += 32) {
-        InstState st[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int32_t i = base + 16 * u + t;
-          if (scan && i < n_inst) st[u] = state_of((uint32_t)i);
-        }
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int32_t i = base + 16 * u + t;
-          if (scan && i < n_inst && !test_bit(bmH, (uint32_t)i) && eligible(m, st[u].A1, st[u].S, L))
-            evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return st[u]; }, L, Lf, wmin, Z, kvc, slo);
+      for (int32_t base = 0; base < n_inst; base += 16) {
+        const int32_t i = base + t;
+        if (scan && i < n_inst && !test_bit(bmH, (uint32_t)i)) {
+          const InstState st = state_of((uint32_t)i);
+          if (eligible(m, st.A1, st.S, L))
+            evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return st; }, L, Lf, wmin, Z, kvc, slo);
         }
       }
       keyT = row_min_u64(acc.keyT);
@@ -1490,18 +1499,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
     if (fate == 0u && (keyT != ~0ull || keyF != ~0ull)) {
       const bool tt = keyT != ~0ull;
       const uint32_t best = (uint32_t)((tt ? keyT : keyF) & 0xFFFFu);
+      // the chosen instance's state is read again (keeping the holders'
+      // states live to here would spill); its hit from the holder's lane
       const uint32_t hb = row_bits(__ballot(el && id == best));
       const int src = (lane & 48) + (hb ? __builtin_ctz(hb) : 0);
-      const InstState sst = shfl_state(hst, src);
       const uint32_t sv = (uint32_t)__shfl((int)hit, src);
-      InstState bs{};
-      uint32_t v = 0;
-      if (hb) {
-        bs = sst;
-        v = sv;
-      } else {
-        bs = state_of(best);
-      }
+      const InstState bs = state_of(best);
+      const uint32_t v = hb ? sv : 0u;
       const int64_t c_tok = (int64_t)v * m.bs;
       const Lat lt = latency(m, bs, (float)(L - c_tok), (float)c_tok, L);
       res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot,
@@ -1679,7 +1683,8 @@ hipError_t ps_launch_lean(const ScoreArgs& a, int grid, hipStream_t s) {
 
 size_t ps_lean_rows_lds_bytes(int32_t n_inst) {
   const size_t nw = ((size_t)n_inst + 63) / 64;
-  return 4 * ((nw + 1) & ~(size_t)1) * sizeof(uint64_t) +
+  return 4 * ((nw + 1) & ~(size_t)1) * sizeof(uint64_t) + kTopRooms * sizeof(TopRoom) +
+         64 * sizeof(int32_t) +
          (ps_score_small(n_inst) ? (size_t)kSmallPool * (sizeof(InstState) + sizeof(int4)) : 0);
 }
 
