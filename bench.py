@@ -565,21 +565,27 @@ def main():
     for _ in range(args.warmup):
         sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    # The timed region: exactly K steps back to back, bracketed by device
+    # synchronisation (no events inside it: a marker between steps costs the
+    # stream a few microseconds of its own).
     print(f"bench: timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     w0 = time.perf_counter()
+    for _ in range(args.steps):
+        sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_per_step = wall * 1e3 / args.steps
+    res = ps.results_from_device(d_out)
+    # The same steps again, each between two events (per-step device time).
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     for a, b in ev:
         a.record(stream)
         sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
         b.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    step_ms = [a.elapsed_time(b) for a, b in ev]
-    ms_per_step = wall * 1e3 / args.steps
-    step_avg = float(np.mean(step_ms))
-    res = ps.results_from_device(d_out)
+    step_avg = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     # The same steps again with the library's events around its launches:
     # the prefix-group pass and the scoring kernel, each on the launch stream.
     sc.set_timing(True)
