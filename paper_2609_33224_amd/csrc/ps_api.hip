@@ -770,7 +770,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   // four waves per resident slot: enough waves to balance uneven work (the
   // popular groups), few enough that an empty pass costs little.
   HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, lean ? std::min(grid, c->num_cus * 64) : grid,
-                             probe_all, s));
+                             probe_all, s, rows));
   if (ev) {
     HIP_TRY(c, hipEventRecord(ev[2], s));
     ++c->n_timed;

@@ -583,7 +583,9 @@ struct Member {
 
 // `state()` supplies the instance's load state; it is called only for
 // members of C.
-template <class State>
+// KEYED: the caller guarantees a keyed selector (D-C-Q, D-Q, D-Q-C) and no
+// TTFT admission, so those branches compile away.
+template <bool KEYED = false, class State>
 __device__ __forceinline__ Member member_with(const DevModel& m, State state, uint32_t v,
                                               int64_t L, float Lf, float wmin, float Z, bool kvc,
                                               float slo) {
@@ -599,7 +601,7 @@ __device__ __forceinline__ Member member_with(const DevModel& m, State state, ui
   r.st = state();
   r.lt = latency(m, r.st, n, (float)c_tok, L);
   const bool tpot_ok = (m.flags & PS_F_NO_TPOT_FILTER) || r.lt.tpot < m.tau;
-  const bool ttft_ok = !(m.flags & PS_F_TTFT_ADMIT) || r.lt.ttft <= slo;
+  const bool ttft_ok = KEYED || !(m.flags & PS_F_TTFT_ADMIT) || r.lt.ttft <= slo;
   r.inT = tpot_ok && ttft_ok;
   return r;
 }
@@ -610,11 +612,11 @@ __device__ __forceinline__ Member member(const ScoreArgs& a, const DevModel& m, 
   return member_with(m, [&]() { return a.inst[i]; }, v, L, Lf, wmin, Z, kvc, slo);
 }
 
-template <class State>
+template <bool KEYED = false, class State>
 __device__ __forceinline__ void evaluate_with(const DevModel& m, Acc& acc, uint32_t i, uint32_t v,
                                               State state, int64_t L, float Lf, float wmin,
                                               float Z, bool kvc, float slo) {
-  const Member mb = member_with(m, state, v, L, Lf, wmin, Z, kvc, slo);
+  const Member mb = member_with<KEYED>(m, state, v, L, Lf, wmin, Z, kvc, slo);
   if (!mb.inC) return;
   ++acc.nC;
   const uint64_t lm = (uint64_t)(mb.st.P + mb.n_tok) * (uint64_t)mb.st.A1;
@@ -622,9 +624,9 @@ __device__ __forceinline__ void evaluate_with(const DevModel& m, Acc& acc, uint3
   acc.keyF = kf < acc.keyF ? kf : acc.keyF;
   if (!mb.inT) return;
   ++acc.nT;
-  if (m.sel == PS_SEL_RANDOM) return;
+  if (!KEYED && m.sel == PS_SEL_RANDOM) return;
   const uint64_t kt = select_key(m.sel, mb.st, v, i, lm);
-  if (m.sel == PS_SEL_HCQ) {
+  if (!KEYED && m.sel == PS_SEL_HCQ) {
     const uint32_t h = sortable_bits(m.tau - mb.lt.tpot);
     if (h < acc.hroom || (h == acc.hroom && kt < acc.keyT)) {
       acc.hroom = h;

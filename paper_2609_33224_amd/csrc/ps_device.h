@@ -259,8 +259,11 @@ struct BuildArgs {
 hipError_t ps_launch_build(const ps::BuildArgs& a, hipStream_t s);  // slots, won, slot_of
 hipError_t ps_launch_rows(const ps::BuildArgs& a, hipStream_t s);   // rows, rowpos (needs rank)
 hipError_t ps_exclusive_scan_u32(const uint32_t* in, uint32_t* out, int64_t n, hipStream_t s);
+// fast: the policy of the four-requests-per-wave scorer (keyed selector,
+// monotone model, no TTFT admission, no set sizes) selects a kernel built
+// for it alone.
 hipError_t ps_launch_score(const ps::ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
-                           hipStream_t s);
+                           hipStream_t s, bool fast = false);
 // Order of the exhaustive probe's requests (bins: kOrderAll words).
 hipError_t ps_launch_order(const ps_req* reqs, int32_t n, int64_t pool_len, uint32_t* bins,
                            int32_t* order, hipStream_t s);

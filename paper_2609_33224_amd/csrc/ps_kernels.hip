@@ -558,7 +558,10 @@ __host__ __device__ inline size_t score_lds_base(int32_t n_inst, bool hits_in_ld
 
 // The general scorer: every request (groups or not, every selector), or
 // with a.defer_only only the requests the lean scorer marked kDeferred.
-template <bool HITS_IN_LDS, bool SMALL>
+// FAST: the policy the four-requests-per-wave scorer serves (keyed
+// selector, monotone model, no TTFT admission, no set sizes), so the
+// other policies' paths compile away.
+template <bool HITS_IN_LDS, bool SMALL, bool FAST>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
@@ -581,6 +584,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   const int g = lane >> 3, s = lane & 7;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
   const DevModel& m = *a.model;
+  uint32_t* const sizes = FAST ? nullptr : a.sizes;
+  const bool sel_hcq = !FAST && m.sel == PS_SEL_HCQ;
+  const bool sel_random = !FAST && m.sel == PS_SEL_RANDOM;
   auto room_of = [&](uint32_t i) -> int64_t { return SMALL ? lroom[i] : a.room[i]; };
   auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
 
@@ -626,7 +632,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       if (!req_valid(q, a.pool_len)) {
         if (lane == 0) {
           a.out[r] = ps_result{-1, 0, 0.0f, 0.0f, PS_R_INVALID};
-          if (a.sizes) a.sizes[3 * (size_t)r] = a.sizes[3 * (size_t)r + 1] = a.sizes[3 * (size_t)r + 2] = 0;
+          if (sizes) sizes[3 * (size_t)r] = sizes[3 * (size_t)r + 1] = sizes[3 * (size_t)r + 2] = 0;
         }
         continue;
       }
@@ -831,7 +837,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       if (nA > 0) {
         if (few) {
           if ((uint32_t)lane < nCand)
-            evaluate_with(m, acc, myid, myhit, [&]() { return state_of(myid); }, L, Lf, wmin, Z, kvc,
+            evaluate_with<FAST>(m, acc, myid, myhit, [&]() { return state_of(myid); }, L, Lf, wmin, Z, kvc,
                           slo);
         } else {
           for (int32_t base = 0; base < n_inst; base += 64) {
@@ -848,7 +854,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
               if (lane == k) v = hk;
             }
             if (cand)
-              evaluate_with(m, acc, (uint32_t)i, v, [&]() { return state_of((uint32_t)i); }, L, Lf,
+              evaluate_with<FAST>(m, acc, (uint32_t)i, v, [&]() { return state_of((uint32_t)i); }, L, Lf,
                             wmin, Z, kvc, slo);
           }
         }
@@ -859,8 +865,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
           // asc).  The whole class is evaluated when sizes are requested or
           // when no member is in T (then the fallback key may come from it).
           bool done0 = false, searched = false;
-          const bool keyed = m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
-          if (!a.sizes && keyed && m.mono && !(m.flags & PS_F_TTFT_ADMIT)) {
+          const bool keyed = FAST || m.sel == PS_SEL_DCQ || m.sel == PS_SEL_DQ || m.sel == PS_SEL_DQC;
+          if (!sizes && keyed && (FAST || (m.mono && !(m.flags & PS_F_TTFT_ADMIT)))) {
             searched = true;
             // The first member of T in key order: the first key position whose
             // threshold admits this length and whose instance does not hold
@@ -887,7 +893,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
                 }
               }
             }
-          } else if (!a.sizes && keyed) {
+          } else if (!sizes && keyed) {
             searched = true;
             for (int32_t base = 0; base < n_inst && !done0; base += 64) {
               const int32_t k = base + lane;
@@ -920,14 +926,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
             for (int32_t base = 0; base < n_inst; base += 64) {
               const int32_t i = base + lane;
               if (i < n_inst && !test_bit(bmC, (uint32_t)i) && room_of((uint32_t)i) >= L)
-                evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return state_of((uint32_t)i); }, L, Lf,
+                evaluate_with<FAST>(m, acc, (uint32_t)i, 0u, [&]() { return state_of((uint32_t)i); }, L, Lf,
                               wmin, Z, kvc, slo);
             }
           }
         }
       }
       uint64_t keyT;
-      if (m.sel == PS_SEL_HCQ) {  // smallest headroom first, then the rest of the key
+      if (sel_hcq) {  // smallest headroom first, then the rest of the key
         const uint64_t hmin = wave_min_u64((uint64_t)acc.hroom);
         keyT = wave_min_u64((uint64_t)acc.hroom == hmin ? acc.keyT : ~0ull);
       } else {
@@ -936,10 +942,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       // the fallback key matters only when T is empty; the set sizes only
       // when reported or for the random selector
       const uint64_t keyF = keyT == ~0ull ? wave_min_u64(acc.keyF) : ~0ull;
-      const bool counts = a.sizes || m.sel == PS_SEL_RANDOM;
+      const bool counts = sizes || sel_random;
       const uint32_t nC = counts ? wave_sum_u32(acc.nC) : 0u;
       const uint32_t nT = counts ? wave_sum_u32(acc.nT) : 0u;
-      if (m.sel == PS_SEL_RANDOM && nT > 0) {
+      if (sel_random && nT > 0) {
         // the k-th member of T in id order
         const uint64_t z = splitmix64_at(m.rand_seed, r);
         const uint32_t kth = (uint32_t)(((z >> 32) * (uint64_t)nT) >> 32);
@@ -959,7 +965,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
           }
           bool inT = false;
           if (el && (cand || admit0))
-            inT = member_with(m, [&]() { return state_of((uint32_t)i); }, v, L, Lf, wmin, Z, kvc, slo)
+            inT = member_with<FAST>(m, [&]() { return state_of((uint32_t)i); }, v, L, Lf, wmin, Z, kvc, slo)
                       .inT;
           uint64_t mm = __ballot(inT);
           const uint32_t cnt = (uint32_t)__popcll(mm);
@@ -1005,10 +1011,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       }
       if (lane == 0) {
         a.out[r] = res;
-        if (a.sizes) {
-          a.sizes[3 * (size_t)r] = nA;
-          a.sizes[3 * (size_t)r + 1] = nC;
-          a.sizes[3 * (size_t)r + 2] = nT;
+        if (sizes) {
+          sizes[3 * (size_t)r] = nA;
+          sizes[3 * (size_t)r + 1] = nC;
+          sizes[3 * (size_t)r + 2] = nT;
         }
       }
       // leave the candidate bitmap clear for the next request
@@ -1442,7 +1448,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
     const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
     const bool admit0 = live && any0 && (!kvc || (W0 - wmin) / Z <= m.eta);
     Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
-    if (el) evaluate_with(m, acc, id, hit, [&]() { return hst; }, L, Lf, wmin, Z, kvc, slo);
+    if (el) evaluate_with<true>(m, acc, id, hit, [&]() { return hst; }, L, Lf, wmin, Z, kvc, slo);
     // the hit-0 class: eligible non-holders, one penalty W(L); its first
     // admitted member in key order
     bool searching = admit0 && cm != 0ull;
@@ -1488,7 +1494,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
         if (scan && i < n_inst && !test_bit(bmH, (uint32_t)i)) {
           const InstState st = state_of((uint32_t)i);
           if (eligible(m, st.A1, st.S, L))
-            evaluate_with(m, acc, (uint32_t)i, 0u, [&]() { return st; }, L, Lf, wmin, Z, kvc, slo);
+            evaluate_with<true>(m, acc, (uint32_t)i, 0u, [&]() { return st; }, L, Lf, wmin, Z, kvc, slo);
         }
       }
       keyT = row_min_u64(acc.keyT);
@@ -1640,7 +1646,7 @@ int32_t ps_lean_waves_per_cu(int32_t n_inst) {
 }
 
 hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool probe_all,
-                           hipStream_t s) {
+                           hipStream_t s, bool fast) {
   if (a.n_req == 0) return hipSuccess;
   if (probe_all) {
     // two 64-instance steps of first-block probes and 128 walk positions
@@ -1650,12 +1656,20 @@ hipError_t ps_launch_score(const ScoreArgs& a, bool hits_in_lds, int grid, bool 
     return hipGetLastError();
   }
   const size_t lds = ps_score_lds_bytes(a.n_inst);
-  if (ps_score_small(a.n_inst))
-    hipLaunchKernelGGL((score_kernel<true, true>), dim3(grid), dim3(64), lds, s, a);
-  else if (hits_in_lds)
-    hipLaunchKernelGGL((score_kernel<true, false>), dim3(grid), dim3(64), lds, s, a);
-  else
-    hipLaunchKernelGGL((score_kernel<false, false>), dim3(grid), dim3(64), lds, s, a);
+  if (fast) {
+    if (ps_score_small(a.n_inst))
+      hipLaunchKernelGGL((score_kernel<true, true, true>), dim3(grid), dim3(64), lds, s, a);
+    else if (hits_in_lds)
+      hipLaunchKernelGGL((score_kernel<true, false, true>), dim3(grid), dim3(64), lds, s, a);
+    else
+      hipLaunchKernelGGL((score_kernel<false, false, true>), dim3(grid), dim3(64), lds, s, a);
+  } else if (ps_score_small(a.n_inst)) {
+    hipLaunchKernelGGL((score_kernel<true, true, false>), dim3(grid), dim3(64), lds, s, a);
+  } else if (hits_in_lds) {
+    hipLaunchKernelGGL((score_kernel<true, false, false>), dim3(grid), dim3(64), lds, s, a);
+  } else {
+    hipLaunchKernelGGL((score_kernel<false, false, false>), dim3(grid), dim3(64), lds, s, a);
+  }
   return hipGetLastError();
 }
 
