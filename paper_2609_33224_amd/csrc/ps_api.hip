@@ -76,7 +76,10 @@ struct ps_ctx {
   unsigned long long* d_gkeys = nullptr;  // keys, then the tagged segment lengths
   uint2* d_grec = nullptr;
   uint32_t* d_gslot = nullptr;
-  uint32_t* d_gpop = nullptr;  // counter word, then the popular rows
+  uint32_t* d_gpop = nullptr;  // counter words (rows taken, deferral, two sets of leader list
+                               // lengths at 16 and 24), then the popular rows
+  unsigned long long* d_glist = nullptr;  // the leaders' lists (kXcds * glcap)
+  uint32_t glcap = 0;           // entries per list
   uint32_t gslots = 0;   // power of two
   int32_t greq_cap = 0;  // entries of d_gslot
   uint64_t ggen = 0;
@@ -397,6 +400,7 @@ ps_status ps_destroy(ps_ctx* c) {
   dfree(c->d_grec);
   dfree(c->d_gslot);
   dfree(c->d_gpop);
+  dfree(c->d_glist);
   dfree(c->d_obins);
   dfree(c->d_order);
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
@@ -648,7 +652,20 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     c->gslots = want;
     clear = true;
   }
-  if (!c->d_gpop) HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + 256));
+  if (!c->d_gpop) {
+    HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + 256));
+    HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, 256, s));  // counter words
+  }
+  // leader lists: the claim pass's waves take the kXcds lists in turn, at
+  // most 64 leaders per wave
+  const uint32_t waves = (uint32_t)((n_req + 255) / 256) * 4u;
+  const uint32_t lcap = (waves + kXcds - 1) / kXcds * 64u;
+  if (lcap > c->glcap) {
+    dfree(c->d_glist);
+    c->glcap = 0;
+    HIP_TRY(c, hipMalloc((void**)&c->d_glist, (size_t)kXcds * lcap * sizeof(unsigned long long)));
+    c->glcap = lcap;
+  }
   if (n_req > c->greq_cap) {
     dfree(c->d_gslot);
     c->greq_cap = 0;
@@ -659,8 +676,10 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     c->ggen = 1;
     clear = true;
   }
-  if (clear)
+  if (clear) {
     HIP_TRY(c, hipMemsetAsync(c->d_gkeys, 0, 2 * (size_t)c->gslots * sizeof(unsigned long long), s));
+    HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, 256, s));  // both sets of list lengths
+  }
   return PS_OK;
 }
 
@@ -688,7 +707,8 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.sizes = d_sizes;
   a.hits_out = d_hits;
   a.scratch = c->d_scratch;
-  a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0u, 0u, 0ull};
+  a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0u, 0u, 0ull,
+                   nullptr, nullptr, nullptr, 0u};
   a.sel = c->h_model.sel;
   a.defer_any = nullptr;
   a.defer_only = 0;
@@ -717,7 +737,11 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                      c->d_gpop,
                      (uint32_t)(kGroupPopBytes / ((size_t)c->n_inst * sizeof(uint32_t))),
                      c->gslots - 1u,
-                     c->ggen};
+                     c->ggen,
+                     c->d_glist,
+                     c->d_gpop + 16 + 8 * (c->ggen & 1u),
+                     c->d_gpop + 16 + 8 * ((c->ggen + 1u) & 1u),
+                     c->glcap};
     a.defer_any = c->d_gpop + 1;
   }
   // The scoring kernel takes batches of a.batch requests per wave; a small
@@ -742,7 +766,11 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
     ev = &c->ev[3 * (size_t)c->n_timed];
   }
   if (ev) HIP_TRY(c, hipEventRecord(ev[0], s));
-  if (a.grp.keys) HIP_TRY(c, ps_launch_group(a, s));
+  // the walk pass over the leaders' lists: a wave per four requests (about
+  // two waves per group at the usual group sizes), so the dispatcher
+  // balances long walks (popular groups) against short ones
+  if (a.grp.keys)
+    HIP_TRY(c, ps_launch_group(a, std::max(64, (n_req / 4 + 63) / 64 * 64), s));
   if (ev) HIP_TRY(c, hipEventRecord(ev[1], s));
   // The lean scorer first when the groups give the requests their hits and
   // the selector is neither Random nor H-C-Q (persistent grid at its own

@@ -145,6 +145,13 @@ struct GroupTab {
   uint32_t pop_cap;
   uint32_t mask;             // slots - 1
   uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
+  // this window's leaders in kXcds lists (list x at x * lcap), each entry
+  // (pre_off + 1) << 24 | slot, with their lengths in lctr; lctr_next: the
+  // other window parity's lengths, cleared here for the next window
+  unsigned long long* lists;
+  uint32_t* lctr;
+  uint32_t* lctr_next;
+  uint32_t lcap;
 };
 
 // One of the pool's 64 largest rooms (descending; pads: room -1).
@@ -290,7 +297,7 @@ hipError_t ps_launch_lmax(const ps::InstState* inst_key, const uint32_t* order0,
                           const ps::DevModel* m, int32_t n, int4* lm, int32_t* lm1, hipStream_t s);
 // Prefix groups of a window: slot of every request and the longest member
 // segment per group, then the walks of the leaders.
-hipError_t ps_launch_group(const ps::ScoreArgs& a, hipStream_t s);
+hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s);  // grid: a multiple of 64
 // Per-arrival scheduler: one workgroup of `threads` (a multiple of 64, at
 // most kSeqMaxThreads) over requests [a.r0, a.r1).
 hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);

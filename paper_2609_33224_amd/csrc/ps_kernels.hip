@@ -419,6 +419,7 @@ __global__ void group_claim_kernel(ScoreArgs a) {
     G.pop_ctr[0] = 0u;
     G.pop_ctr[1] = 0u;
   }
+  if (blockIdx.x == 0 && threadIdx.x < kXcds) G.lctr_next[threadIdx.x] = 0u;  // the next window's
   const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   bool want = false;
@@ -450,6 +451,22 @@ __global__ void group_claim_kernel(ScoreArgs a) {
       atomicMax(&G.plen[slot],
                 ((unsigned long long)G.gen << kGroupGenShift) | (unsigned long long)mx);
   }
+  static_assert(2 * kGroupMaxReq <= (1 << 24) && kGroupGenShift + 24 <= 64,
+                "a list entry packs a slot (24 bits) and a segment offset (40 bits)");
+  // the leaders' slots into this wave's list: one atomic per wave, lists
+  // dealt to waves in turn (a list holds at most lcap entries: 64 per wave
+  // that writes it)
+  const bool lead = want && first == lane && slot >= 0 && leader;
+  const uint64_t lm = __ballot(lead);
+  if (lm) {
+    const uint32_t x = ((uint32_t)(blockIdx.x * blockDim.x + threadIdx.x) >> 6) % (uint32_t)kXcds;
+    uint32_t base = 0u;
+    if (lane == 0) base = atomicAdd(&G.lctr[x], (uint32_t)__popcll(lm));
+    base = (uint32_t)__shfl((int)base, 0);
+    if (lead)
+      G.lists[(size_t)x * G.lcap + base + (uint32_t)__popcll(lm & ((1ull << lane) - 1ull))] =
+          ((unsigned long long)(off + 1) << 24) | (unsigned long long)slot;
+  }
   slot = __shfl(slot, first);
   if (r < a.n_req)
     G.slot_of[r] = want && slot >= 0
@@ -457,11 +474,11 @@ __global__ void group_claim_kernel(ScoreArgs a) {
                        : kGroupNoSlot;
 }
 
-// Prefix groups, pass 2 (one wave per request; only leaders work): the walk
-// of the group's longest segment on every holder of its first block, into
-// the slot's record (up to kGroupHold holders, each walked on its row) or a
-// row of the popular area (more holders, walked together through the
-// prefix index).
+// Prefix groups, pass 2 (a persistent grid over the leaders' lists, which
+// the claim pass wrote): the walk of the group's longest segment on every
+// holder of its first block, into the slot's record (up to kGroupHold
+// holders, each walked on its row) or a row of the popular area (more
+// holders, walked together through the prefix index).
 __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
@@ -472,11 +489,16 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
   const GroupTab& G = a.grp;
-  for (int32_t r = blockIdx.x; r < a.n_req; r += gridDim.x) {
-    const uint32_t so = G.slot_of[r];
-    if (so == kGroupNoSlot || !(so & kGroupLead)) continue;
-    const uint32_t slot = so & ~kGroupLead;
-    const int64_t pre_off = a.reqs[r].pre_off;
+  // workgroup b takes entry (b / 64) * 8 + b % 8 of list (b / 8) % 8, then
+  // every (grid / 8)-th after it: each list is spread over all XCDs (b runs
+  // on XCD b % 8), so an XCD does not inherit one list's share of long walks
+  static_assert(kXcds == 8, "the list walk maps workgroups to 8 lists");
+  const uint32_t x = (blockIdx.x >> 3) & 7u;
+  const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x]);
+  for (uint32_t idx = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u); idx < nx; idx += gridDim.x >> 3) {
+    const unsigned long long ent = G.lists[(size_t)x * G.lcap + idx];
+    const uint32_t slot = (uint32_t)(ent & 0xFFFFFFull);
+    const int64_t pre_off = (int64_t)(ent >> 24) - 1;
     const int32_t plen =
         (int32_t)(G.plen[slot] & ((1ull << kGroupGenShift) - 1ull));  // every member lies in the pool
     const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
@@ -1730,14 +1752,14 @@ hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, con
   return hipGetLastError();
 }
 
-hipError_t ps_launch_group(const ScoreArgs& a, hipStream_t s) {
+hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s) {
   if (a.n_req == 0) return hipSuccess;
   hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + 255) / 256), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t nw = ((size_t)a.n_inst + 63) / 64;
   const size_t lds = (size_t)kStage * sizeof(uint64_t) + 2 * nw * sizeof(uint64_t);
-  hipLaunchKernelGGL(group_kernel, dim3(a.n_req), dim3(64), lds, s, a);
+  hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, s, a);
   return hipGetLastError();
 }
 
