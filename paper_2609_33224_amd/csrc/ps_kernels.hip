@@ -409,11 +409,12 @@ __device__ int32_t group_claim(const GroupTab& G, int64_t pre_off, int* leader) 
 // Prefix groups, pass 1 (one thread per request; the grid covers every
 // request once): the slot of every request's group and the group's longest
 // segment (a 64-bit maximum over generation-tagged lengths, so no slot
-// needs clearing between windows).  Requests of one wave with the same
-// segment claim once: the lowest such lane claims and takes the maximum
-// over all of them, so a popular session does not serialise on one slot's
-// atomics.
-__global__ void group_claim_kernel(ScoreArgs a) {
+// needs clearing between windows).  Requests of one workgroup with the
+// same segment claim once (see below); each new leader goes into a list for
+// the walk pass.
+constexpr int kClaimBlock = 256;  // threads (requests) per workgroup of the claim pass
+
+__global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
   const GroupTab& G = a.grp;
   if (blockIdx.x == 0 && threadIdx.x == 0) {  // read only by the later kernels of this window
     G.pop_ctr[0] = 0u;
@@ -433,30 +434,51 @@ __global__ void group_claim_kernel(ScoreArgs a) {
       plen = q.pre_len;
     }
   }
-  int first = lane;
-  int32_t mx = plen;
-  for (int l = 63; l >= 0; --l) {
-    const int64_t o = __shfl(off, l);
-    const int32_t pl = __shfl(plen, l);
-    if (want && o == off) {
-      first = l;
-      mx = pl > mx ? pl : mx;
-    }
+  // Requests of this workgroup with the same segment meet in an LDS hash
+  // table: the lowest thread claims for all of them, with their longest
+  // length (a popular session would otherwise serialise its atomics on one
+  // slot).
+  __shared__ unsigned long long lkey[2 * kClaimBlock];
+  __shared__ int32_t llen[2 * kClaimBlock], lfirst[2 * kClaimBlock], lslot[2 * kClaimBlock];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < 2 * kClaimBlock; i += kClaimBlock) {
+    lkey[i] = 0ull;
+    llen[i] = 0;
+    lfirst[i] = kClaimBlock;
+    lslot[i] = -1;
   }
+  __syncthreads();
+  int h = 0;
+  if (want) {
+    const unsigned long long k = (unsigned long long)(off + 1);
+    uint32_t b = (uint32_t)((k * 0x9E3779B97F4A7C15ull) >> 40) & (2 * kClaimBlock - 1);
+    for (int step = 0; step < 2 * kClaimBlock; ++step) {  // at most kClaimBlock keys: a free entry exists
+      const unsigned long long old = atomicCAS(&lkey[b], 0ull, k);
+      if (old == 0ull || old == k) break;
+      b = (b + 1) & (2 * kClaimBlock - 1);
+    }
+    h = (int)b;
+    atomicMax(&llen[h], plen);
+    atomicMin(&lfirst[h], tid);
+  }
+  __syncthreads();
+  const bool first = want && lfirst[h] == tid;
   int32_t slot = -1;
   int leader = 0;
-  if (want && first == lane) {
+  if (first) {
     slot = group_claim(G, off, &leader);
     if (slot >= 0)
       atomicMax(&G.plen[slot],
-                ((unsigned long long)G.gen << kGroupGenShift) | (unsigned long long)mx);
+                ((unsigned long long)G.gen << kGroupGenShift) | (unsigned long long)llen[h]);
+    lslot[h] = slot;
   }
+  __syncthreads();
   static_assert(2 * kGroupMaxReq <= (1 << 24) && kGroupGenShift + 24 <= 64,
                 "a list entry packs a slot (24 bits) and a segment offset (40 bits)");
   // the leaders' slots into this wave's list: one atomic per wave, lists
   // dealt to waves in turn (a list holds at most lcap entries: 64 per wave
   // that writes it)
-  const bool lead = want && first == lane && slot >= 0 && leader;
+  const bool lead = first && slot >= 0 && leader;
   const uint64_t lm = __ballot(lead);
   if (lm) {
     const uint32_t x = ((uint32_t)(blockIdx.x * blockDim.x + threadIdx.x) >> 6) % (uint32_t)kXcds;
@@ -467,11 +489,9 @@ __global__ void group_claim_kernel(ScoreArgs a) {
       G.lists[(size_t)x * G.lcap + base + (uint32_t)__popcll(lm & ((1ull << lane) - 1ull))] =
           ((unsigned long long)(off + 1) << 24) | (unsigned long long)slot;
   }
-  slot = __shfl(slot, first);
+  if (want) slot = lslot[h];
   if (r < a.n_req)
-    G.slot_of[r] = want && slot >= 0
-                       ? (uint32_t)slot | (first == lane && leader ? kGroupLead : 0u)
-                       : kGroupNoSlot;
+    G.slot_of[r] = want && slot >= 0 ? (uint32_t)slot | (lead ? kGroupLead : 0u) : kGroupNoSlot;
 }
 
 // Prefix groups, pass 2 (a persistent grid over the leaders' lists, which
@@ -1754,7 +1774,8 @@ hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, con
 
 hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s) {
   if (a.n_req == 0) return hipSuccess;
-  hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + 255) / 256), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + kClaimBlock - 1) / kClaimBlock),
+                     dim3(kClaimBlock), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t nw = ((size_t)a.n_inst + 63) / 64;
