@@ -71,6 +71,13 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// A 64-bit value of lane src (a wave-uniform result).
+__device__ __forceinline__ int64_t lane_value64(int64_t v, int src) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), src);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // Exclusive prefix sum of v over the lanes of the wave.
 __device__ __forceinline__ uint32_t wave_exclusive_sum(uint32_t v, int lane) {
   uint32_t x = v;

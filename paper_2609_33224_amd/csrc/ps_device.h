@@ -119,12 +119,18 @@ constexpr uint64_t kGroupGenMax = (1ull << 24) - 1;
 constexpr int32_t kGroupMaxReq = 1 << 22;    // larger windows are scored without groups
 
 // Record of one group slot: GroupMeta, then up to kGroupHold holders in
-// ascending id order as {instance id, hit of the leader's segment there}.
+// ascending id order as {instance id, hit of the leader's segment there},
+// then one word {class, bitmap} for popular groups (below).
 struct alignas(8) GroupMeta {
   int32_t plen;  // length of the segment the leader walked
   uint32_t cnt;  // holders of its first block, or kGroupNone
 };
-constexpr int kGroupRec = 1 + (int)kGroupHold;  // 8-byte words per slot record
+constexpr int kGroupRec = 2 + (int)kGroupHold;  // 8-byte words per slot record
+// Popular groups (kGroupPop) whose holders all have one hit H* but for at
+// most kGroupHold exceptions: the record keeps the exceptions in place of
+// the holders and, in its last word, {n_exc << 24 | H*, the first block's
+// holder bitmap number}; otherwise that word's first half is kGroupNone.
+constexpr int kGroupClsWord = 1 + (int)kGroupHold;
 
 constexpr uint32_t kGroupLead = 0x80000000u;  // slot_of flag of the group's leader
 constexpr uint32_t kGroupNoSlot = 0xFFFFFFFFu;

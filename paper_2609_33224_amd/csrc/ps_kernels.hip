@@ -552,6 +552,56 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
         index_walk<true>(a, c, stage, bmA, bmN, nw, cnt0, 1,
                          [&](uint32_t id, uint32_t h) { hp[id] = h; }, lane, g, s);
         cnt = kGroupPop | row;
+        // The shared-hit class: H* = the most frequent hit among the holders
+        // of the first 64-instance word that has any; when at most
+        // kGroupHold holders differ from it, the record keeps them.
+        uint32_t clsw = kGroupNone;
+        if (cnt0 > kPopular) {
+          // this wave's hit writes, then its reads of them (a workgroup-scope
+          // fence: a device-scope one writes back the XCD's whole L2)
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+          const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
+          uint32_t hs = 0u;
+          for (int32_t w = 0; w < nw; ++w) {
+            const uint64_t word = bm[w];
+            if (!word) continue;
+            const bool hold = ((word >> lane) & 1ull) != 0ull;
+            const uint32_t v = hold ? hp[w * 64 + lane] : 0u;
+            uint64_t rem = word;
+            uint32_t bestc = 0u;
+            while (rem) {
+              const uint32_t val = (uint32_t)__builtin_amdgcn_readlane((int)v, __builtin_ctzll(rem));
+              const uint64_t same = __ballot(hold && v == val);
+              rem &= ~same;
+              if ((uint32_t)__popcll(same) > bestc) {
+                bestc = (uint32_t)__popcll(same);
+                hs = val;
+              }
+            }
+            break;
+          }
+          uint32_t nexc = 0u;
+          for (int32_t w0 = 0; w0 < nw && nexc <= kGroupHold; w0 += 4) {  // four words in flight
+            bool hold[4];
+            uint32_t v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int32_t w = w0 + u;
+              hold[u] = w < nw && ((bm[w] >> lane) & 1ull) != 0ull;
+              v[u] = hold[u] ? hp[w * 64 + lane] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const bool ex = hold[u] && v[u] != hs;
+              const uint64_t em = __ballot(ex);
+              const uint32_t k = nexc + (uint32_t)__popcll(em & ((1ull << lane) - 1ull));
+              if (ex && k < kGroupHold) rec[1 + k] = make_uint2((uint32_t)((w0 + u) * 64 + lane), v[u]);
+              nexc += (uint32_t)__popcll(em);
+            }
+          }
+          if (nexc <= kGroupHold && hs > 0u && hs < (1u << 24)) clsw = (nexc << 24) | hs;
+        }
+        if (lane == 0) rec[kGroupClsWord] = make_uint2(clsw, off0);
       }
     } else if (found0) {
       const uint32_t id = (uint32_t)lane < cnt0 ? a.x.holders[off0 + lane] : 0u;
@@ -695,6 +745,137 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       }
       const bool grp = gm.cnt != kGroupNone;
       const bool gpop = grp && (gm.cnt & kGroupPop) != 0u;  // holders from the index
+      // A popular group whose holders share one hit H* (but for at most
+      // kGroupHold exceptions): the exceptions are candidates of their own,
+      // the other holders one class (hit H*, one penalty, the first member of
+      // T in key order found by a scan of the key-ordered states), the
+      // non-holders the zero-hit class.  When a class's eligibility cannot be
+      // told from the 64 largest rooms, or no candidate is in T, the request
+      // takes the general path below.
+      if (FAST && gpop) {
+        const uint2 cwd = lrec[b * kGroupRec + kGroupClsWord];
+        const uint32_t clsw = (uint32_t)__builtin_amdgcn_readfirstlane((int)cwd.x);
+        const uint32_t hs = clsw & 0xFFFFFFu, nexc = clsw >> 24;
+        const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
+        if (clsw != kGroupNone && (int32_t)hs < p0) {
+          const uint64_t* hb = a.x.bitmaps + (size_t)__builtin_amdgcn_readfirstlane((int)cwd.y) * a.x.nw;
+          const TopRoom trm = a.rtop[lane];
+          // exceptions: state, eligibility, hit (resumed where it reaches p0)
+          const bool eact = (uint32_t)lane < nexc;
+          const uint32_t eid = eact ? hd.x : 0u;
+          uint32_t ehit = eact ? hd.y : 0u;
+          InstState est{};
+          if (eact) {
+            est = state_of(eid);
+            atomicOr(reinterpret_cast<unsigned long long*>(&bmC[eid >> 6]), 1ull << (eid & 63));
+          }
+          const bool eel = eact && eligible(m, est.A1, est.S, L);
+          __syncthreads();
+          uint64_t need = __ballot(eel && (int32_t)ehit >= p0);
+          while (need) {
+            const int k = __builtin_ctzll(need);
+            need &= need - 1;
+            const uint32_t hk = run_walk<false>(a.t, (uint32_t)__shfl((int)eid, k), c, nullptr, p0, g, s);
+            if (lane == k) ehit = hk;
+          }
+          const int64_t room0 = lane_value64(trm.room, 0), room63 = lane_value64(trm.room, 63);
+          const bool topel = trm.room >= L;
+          const bool thold = test_bit(hb, (uint32_t)trm.id);
+          const bool texc = test_bit(bmC, (uint32_t)trm.id);
+          const bool anyK = __ballot(topel && thold && !texc) != 0ull;
+          const bool any0 = __ballot(topel && !thold) != 0ull;
+          // with the 64th room eligible, a class absent from the top rooms may
+          // still have eligible members
+          bool decided = false;
+          ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
+          if (!(room0 >= L)) {
+            decided = true;  // A is empty
+          } else if (!(room63 >= L) || (anyK && any0)) {
+            const float Z = recompute_raw(m, Lf, Lf);
+            const float W0 = fmaxf(0.0f, Z);
+            const int64_t cK = (int64_t)hs * m.bs;
+            const float WK = fmaxf(0.0f, recompute_raw(m, (float)(L - cK), Lf));
+            uint32_t wb = 0x7F800000u;
+            if (eel) wb = __float_as_uint(fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)ehit * m.bs), Lf)));
+            if (lane == 0 && any0) wb = wb < __float_as_uint(W0) ? wb : __float_as_uint(W0);
+            if (lane == 1 && anyK) wb = wb < __float_as_uint(WK) ? wb : __float_as_uint(WK);
+            const float wmin = __uint_as_float(wave_min_u32(wb));
+            const float slo = fmaxf(m.ttft_floor, t_prefill(m, Lf, 0.0f));
+            const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+            const bool admitK = anyK && (!kvc || (WK - wmin) / Z <= m.eta);
+            const bool admit0 = any0 && (!kvc || (W0 - wmin) / Z <= m.eta);
+            Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
+            if (eel) evaluate_with<true>(m, acc, eid, ehit, [&]() { return est; }, L, Lf, wmin, Z, kvc, slo);
+            if (admitK) {  // the class's first member of T in key order
+              const float nK = (float)(L - cK), cKf = (float)cK;
+              bool found = false;
+              for (int32_t base = 0; base < n_inst && !found; base += 64) {
+                const int32_t k = base + lane;
+                bool ok = false;
+                uint32_t i = 0;
+                InstState st{};
+                if (k < n_inst) {
+                  i = a.order0[k];
+                  st = a.inst_key[k];
+                  ok = test_bit(hb, i) && !test_bit(bmC, i) && eligible(m, st.A1, st.S, L) &&
+                       ((m.flags & PS_F_NO_TPOT_FILTER) || latency(m, st, nK, cKf, L).tpot < m.tau);
+                }
+                const uint64_t om = __ballot(ok);
+                if (om) {
+                  if (lane == __builtin_ctzll(om)) {
+                    const uint64_t kt = select_key(m.sel, st, hs, i, 0ull);
+                    acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                  }
+                  found = true;
+                }
+              }
+            }
+            if (admit0) {  // the zero-hit class's first member of T: thresholds
+              const int32_t n1 = (n_inst + 63) >> 6;
+              bool found = false;
+              for (int32_t c0 = 0; c0 < n1 && !found; c0 += 64) {
+                const int32_t cc = c0 + lane;
+                uint64_t cm = __ballot(cc < n1 && (SMALL || a.lm1[cc] >= ell));
+                while (cm && !found) {
+                  const int32_t k = (c0 + __builtin_ctzll(cm)) * 64 + lane;
+                  cm &= cm - 1;
+                  const int4 e = k < n_inst ? (SMALL ? llm[k] : a.lm[k]) : make_int4(-1, 0, 0, 0);
+                  const uint64_t om = __ballot(e.x >= ell && !test_bit(hb, (uint32_t)e.y));
+                  if (om) {
+                    if (lane == __builtin_ctzll(om)) {
+                      InstState st{};
+                      st.D = e.z;
+                      st.Q = e.w;
+                      const uint64_t kt = select_key(m.sel, st, 0u, (uint32_t)e.y, 0ull);
+                      acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                    }
+                    found = true;
+                  }
+                }
+              }
+            }
+            const uint64_t keyT = wave_min_u64(acc.keyT);
+            if (keyT != ~0ull) {  // (no candidate in T: the fallback needs the general path)
+              const uint32_t best = (uint32_t)(keyT & 0xFFFFu);
+              const uint64_t em = __ballot(eact && eid == best);
+              const uint32_t ev = (uint32_t)__shfl((int)ehit, em ? __builtin_ctzll(em) : 0);
+              const uint32_t v = em ? ev : test_bit(hb, best) ? hs : 0u;
+              const int64_t c_tok = (int64_t)v * m.bs;
+              const Lat lt = latency(m, state_of(best), (float)(L - c_tok), (float)c_tok, L);
+              res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot,
+                              lt.ttft > slo ? PS_R_TTFT_MISS : 0u};
+              decided = true;
+            }
+          }
+          __syncthreads();
+          if (eact) bmC[eid >> 6] = 0ull;
+          __syncthreads();
+          if (decided) {
+            if (lane == 0) a.out[r] = res;
+            continue;
+          }
+        }
+      }
       const int32_t nst = grp ? 0 : (ell < kStage ? ell : kStage);
       // The chain head's loads and the room search's are in flight together.
       uint64_t sv[kStage / 64];
@@ -1352,12 +1533,6 @@ __device__ __forceinline__ uint32_t row_bits(uint64_t b) {
   return (uint32_t)(b >> (threadIdx.x & 48u)) & 0xFFFFu;
 }
 
-__device__ __forceinline__ int64_t lane_value64(int64_t v, int src) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), src);
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
 template <bool SMALL>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void lean_rows_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -1621,7 +1796,9 @@ __global__ __launch_bounds__(64) void commit_kernel(CommitArgs a) {
       const uint32_t nins = (uint32_t)__popcll(im);
       count += nins;
       dropped += (unsigned long long)(__popcll(wm) - nins + __popcll(dup_drop));
-      __threadfence();  // later probes of this wave must see these inserts
+      // later probes of this wave must see these inserts (workgroup scope: a
+      // device-scope fence would write back the XCD's whole L2)
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
     }
   }
   st.seg = segment_of(m, st.A1);
