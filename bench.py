@@ -149,6 +149,41 @@ def index_walk_bytes(h, ell, nw, h_all=None):
     return by
 
 
+def group_classes(H):
+    """The shared-hit class of each group as the group kernel forms it (for
+    popular groups with more than 64 holders of the first block): H* = the
+    most frequent hit among the holders in the first 64-instance word that
+    has any (the lowest-lane value among equally frequent ones), the
+    exceptions = the holders whose hit differs; class-able with at most
+    GROUP_HOLD exceptions.  Returns (classable, H*, exception mask)."""
+    import numpy as np
+    G, N = H.shape
+    ok = np.zeros(G, bool)
+    hs = np.zeros(G, np.int64)
+    exc = np.zeros((G, N), bool)
+    hold = H >= 1
+    for k in np.nonzero(hold.sum(1) > 64)[0]:
+        w = int(np.argmax(hold[k].reshape(-1, 64).any(1))) if N % 64 == 0 else None
+        if w is None:
+            words = [hold[k][i:i + 64] for i in range(0, N, 64)]
+            w = next(i for i, x in enumerate(words) if x.any())
+        lanes = np.nonzero(hold[k][w * 64:(w + 1) * 64])[0]
+        vals = H[k][w * 64 + lanes]
+        best, bestc = 0, 0
+        seen = set()
+        for v in vals:  # distinct values in lane order; a strictly larger count wins
+            if v in seen:
+                continue
+            seen.add(v)
+            c = int((vals == v).sum())
+            if c > bestc:
+                best, bestc = int(v), c
+        hs[k] = best
+        exc[k] = hold[k] & (H[k] != best)
+        ok[k] = exc[k].sum() <= GROUP_HOLD and 0 < best < (1 << 24)
+    return ok, hs, exc
+
+
 def group_pass_bytes(win, gid, rep, plen, H):
     """Algorithmic bytes of the prefix-group pass.  Claim: descriptor, slot
     read, the claiming compare-and-swap, the length maximum and the slot
@@ -158,7 +193,8 @@ def group_pass_bytes(win, gid, rep, plen, H):
     the first block with its row position, 16 bytes per compared position,
     a final probe where the segment leaves the cache, and the record; with
     more, the holders walked together through the index and one 4-byte hit
-    per holder in the popular row."""
+    per holder in the popular row, and for more than 64 holders the bitmap
+    and the hits read back for the shared-hit class, and its word."""
     import numpy as np
     R, N = win.n_req, win.n_inst
     nw = (N + 63) // 64
@@ -175,6 +211,8 @@ def group_pass_bytes(win, gid, rep, plen, H):
     by += int(walk[ok].sum()) + int((8 + 8 * cnt0[ok]).sum())
     for k in np.nonzero(~ok)[0]:
         by += 8 + index_walk_bytes(H[k], int(plen[k]), nw) + 4 * int(cnt0[k])
+        if cnt0[k] > 64:  # the shared-hit class: bitmap and hits read back, the class word
+            by += 8 * nw + 4 * int(cnt0[k]) + 8
     return by
 
 
@@ -196,6 +234,14 @@ def score_bytes(win, r0, hits, grp=None):
     class and no candidate is in T, the states of all instances.  Pools of
     at most 64 instances keep states and thresholds in LDS (no bytes).  The
     rooms and threshold maxima are read once per wave (not counted).
+
+    Requests of a popular group with a shared-hit class below their
+    segment end take the general kernel's class path: descriptor, slot,
+    144 B record, result, the 64 largest rooms (1 KB), the holder bitmap,
+    32 B per exception's state and its resume walk, one chunk of 64 key-
+    ordered states with their ids, one chunk of thresholds with the chunk
+    maxima, and the chosen state (a lower bound: later chunks are not
+    counted).
 
     Other requests go through the general kernel: descriptor, slot, result;
     the 64-way search of the sorted rooms; with a popular group row the
@@ -241,6 +287,14 @@ def score_bytes(win, r0, hits, grp=None):
                    Hg=np.zeros_like(h))
     lean = grp["has"] & ~grp["pop"]
     pop = grp["has"] & grp["pop"]
+    # popular groups with a shared-hit class, where H* lies below the
+    # request's segment end (p0): the class path of the general kernel
+    if "cls" in grp:
+        p0 = np.minimum(win.pre_len[r0:r0 + R].astype(np.int64), grp["gplen"])
+        clsp = grp["cls"] & (grp["hs"] < p0)
+    else:
+        clsp = np.zeros(R, bool)
+    pop = pop & ~clsp
     # resume walks of grouped requests
     Hg = grp["Hg"]
     resume = cand & (Hg >= p[:, None]) & (p < ell)[:, None]
@@ -250,10 +304,10 @@ def score_bytes(win, r0, hits, grp=None):
     resume_by = np.where(resume, rb, 0).sum(1)
     # general kernel: per-request parts
     gen = 48 + 512 * levels + np.zeros(R, np.int64)
-    gen += np.where(pop, 136 + np.where(act & (ell > 0), 128 + np.where(
+    gen += np.where(pop, 144 + np.where(act & (ell > 0), 128 + np.where(
         cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0) + 4 * ncand, 0) + resume_by, 0)
     nogrp = ~grp["has"]
-    gen += np.where(nogrp, 8 * np.minimum(ell, 256) + np.where(grp["grouped"], 136, 0), 0)
+    gen += np.where(nogrp, 8 * np.minimum(ell, 256) + np.where(grp["grouped"], 144, 0), 0)
     gen += np.where(nogrp & act & (ell > 0), 128 + np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0), 0)
     few = ncand <= 64
     hc = np.minimum(h, (ell - 1)[:, None])
@@ -265,6 +319,12 @@ def score_bytes(win, r0, hits, grp=None):
     lby = 184 + (0 if small else 32) * cnt0 + resume_by
     lby = np.where(act, lby, 184)
     by = np.where(lean, lby, gen)
+    if clsp.any():
+        exc = grp["exc"]
+        ex_res = np.where(resume & exc, rb, 0).sum(1)
+        cby = (24 + 4 + 8 * 18 + 20 + 64 * 16 + 8 * nw + 32 * exc.sum(1) + ex_res +
+               64 * (4 + 32) + 4 * n1 + 64 * 16 + 32)
+        by = np.where(clsp, cby, by)
     # the recomputation filter and the hit-0 class
     n = (L[:, None] - h * bs).astype(np.float64)
     c = (h * bs).astype(np.float64)
@@ -276,7 +336,7 @@ def score_bytes(win, r0, hits, grp=None):
     with np.errstate(divide="ignore", invalid="ignore"):
         rho = (W - Wmin[:, None]) / Z[:, None]
     inC = elig & (~kvc[:, None] | (rho <= eta))
-    by += np.where(lean, 0, 32 * (cand & inC).sum(1))
+    by += np.where(lean | clsp, 0, 32 * (cand & inC).sum(1))
     n0 = nA - ncand
     W0 = np.maximum(0.0, Z)
     with np.errstate(divide="ignore", invalid="ignore"):
@@ -285,7 +345,7 @@ def score_bytes(win, r0, hits, grp=None):
     seg = np.minimum(seg, len(ub) - 1)
     order0 = np.lexsort((np.arange(N), win.Q, -win.D.astype(np.int64)))
     chunk_lean = 0 if small else 64 * 16
-    for r in np.nonzero(act & (admit0 | lean))[0]:
+    for r in np.nonzero(act & (admit0 | lean) & ~clsp)[0]:
         t_iter = gam[seg] * (beta[seg, 0] + beta[seg, 1] * A1 + beta[seg, 2] * (win.S + L[r]))
         tpot0 = t_iter + np.where(A1 > 1, _tpf(a, float(L[r]), 0.0) / lout1, 0.0)
         zero = elig[r] & ~hold0[r]
@@ -333,6 +393,8 @@ def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 25):
     g_pop = (H >= 1).sum(1) > GROUP_HOLD if len(rep) else np.zeros(0, bool)
     assert int(g_pop.sum()) <= (64 << 20) // (4 * win.n_inst)
     gb = group_pass_bytes(win, gid, rep, plen, H)
+    g_cls, g_hs, g_exc = group_classes(H) if len(rep) else (np.zeros(0, bool), np.zeros(0, np.int64),
+                                                            np.zeros((0, win.n_inst), bool))
     chunk = max(1, min(win.n_req, chunk_pairs // win.n_inst))
     reqs = ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
     d_hits = torch.empty(chunk * win.n_inst, dtype=torch.int32, device="cuda")
@@ -351,7 +413,13 @@ def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 25):
         has = grouped & g_has[np.maximum(gc, 0)] if len(rep) else grouped
         pop = grouped & g_pop[np.maximum(gc, 0)] if len(rep) else grouped
         Hg = H[np.maximum(gc, 0)] if len(rep) else np.zeros(hits.shape, np.int64)
-        sb += score_bytes(win, r0, hits, dict(has=has, pop=pop, grouped=grouped, Hg=Hg))
+        gi = np.maximum(gc, 0)
+        cls = pop & g_cls[gi] if len(rep) else np.zeros(n, bool)
+        hs = g_hs[gi] if len(rep) else np.zeros(n, np.int64)
+        exc = g_exc[gi] if len(rep) else np.zeros(hits.shape, bool)
+        gpl = plen[gi] if len(rep) else np.zeros(n, np.int64)
+        sb += score_bytes(win, r0, hits, dict(has=has, pop=pop, grouped=grouped, Hg=Hg, cls=cls,
+                                              hs=hs, exc=exc, gplen=gpl))
     return sb, gb, pb, npr
 
 
