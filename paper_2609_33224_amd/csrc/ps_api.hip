@@ -76,8 +76,9 @@ struct ps_ctx {
   unsigned long long* d_gkeys = nullptr;  // keys, then the tagged segment lengths
   uint2* d_grec = nullptr;
   uint32_t* d_gslot = nullptr;
-  uint32_t* d_gpop = nullptr;  // counter words (rows taken, deferral, two sets of leader list
-                               // lengths at 16 and 24), then the popular rows
+  uint32_t* d_gpop = nullptr;  // kGroupHeadWords counter words (rows taken, deferral; two sets
+                               // of leader list lengths, one 128-byte line per list), then
+                               // the popular rows
   unsigned long long* d_glist = nullptr;  // the leaders' lists (kXcds * glcap)
   uint32_t glcap = 0;           // entries per list
   uint32_t gslots = 0;   // power of two
@@ -653,8 +654,8 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     clear = true;
   }
   if (!c->d_gpop) {
-    HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + 256));
-    HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, 256, s));  // counter words
+    HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + kGroupHeadWords * sizeof(uint32_t)));
+    HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, kGroupHeadWords * sizeof(uint32_t), s));  // counter words
   }
   // leader lists: the claim pass's waves take the kXcds lists in turn, at
   // most 64 leaders per wave
@@ -678,7 +679,7 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
   }
   if (clear) {
     HIP_TRY(c, hipMemsetAsync(c->d_gkeys, 0, 2 * (size_t)c->gslots * sizeof(unsigned long long), s));
-    HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, 256, s));  // both sets of list lengths
+    HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, kGroupHeadWords * sizeof(uint32_t), s));  // list lengths
   }
   return PS_OK;
 }
@@ -733,14 +734,14 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                      c->d_gkeys + c->gslots,
                      c->d_grec,
                      c->d_gslot,
-                     c->d_gpop + 64,
+                     c->d_gpop + kGroupHeadWords,
                      c->d_gpop,
                      (uint32_t)(kGroupPopBytes / ((size_t)c->n_inst * sizeof(uint32_t))),
                      c->gslots - 1u,
                      c->ggen,
                      c->d_glist,
-                     c->d_gpop + 16 + 8 * (c->ggen & 1u),
-                     c->d_gpop + 16 + 8 * ((c->ggen + 1u) & 1u),
+                     c->d_gpop + kListCtrWords * (1u + kXcds * (uint32_t)(c->ggen & 1u)),
+                     c->d_gpop + kListCtrWords * (1u + kXcds * (uint32_t)((c->ggen + 1u) & 1u)),
                      c->glcap};
     a.defer_any = c->d_gpop + 1;
   }

@@ -139,6 +139,11 @@ constexpr uint32_t kGroupNoSlot = 0xFFFFFFFFu;
 // popular area, row (cnt & ~kGroupPop).
 constexpr uint32_t kGroupPop = 0x80000000u;
 constexpr size_t kGroupPopBytes = (size_t)64 << 20;  // popular area: hits of n_inst u32 per row
+// Header of the popular area: the first line holds the rows-taken and
+// deferral words, then two sets (window parities) of kXcds leader list
+// lengths, each length on a 128-byte line of its own (a wave's atomic on
+// one list does not queue behind the others' on a shared line).
+constexpr uint32_t kListCtrWords = 32;  // 128 bytes
 
 struct GroupTab {
   unsigned long long* keys;  // slots; a key of another generation is an empty slot
@@ -152,8 +157,9 @@ struct GroupTab {
   uint32_t mask;             // slots - 1
   uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
   // this window's leaders in kXcds lists (list x at x * lcap), each entry
-  // (pre_off + 1) << 24 | slot, with their lengths in lctr; lctr_next: the
-  // other window parity's lengths, cleared here for the next window
+  // (pre_off + 1) << 24 | slot, with their lengths in lctr[x * kListCtrWords];
+  // lctr_next: the other window parity's lengths, cleared here for the next
+  // window
   unsigned long long* lists;
   uint32_t* lctr;
   uint32_t* lctr_next;
@@ -208,6 +214,7 @@ constexpr int32_t kOrderHashBins = 256;
 constexpr int32_t kOrderAll = kOrderLenBins * kOrderHashBins;
 constexpr int32_t kOrderChunk = 64;
 constexpr int32_t kXcds = 8;  // workgroups go to the XCDs in turn
+constexpr uint32_t kGroupHeadWords = kListCtrWords * (1 + 2 * kXcds);
 
 struct CommitArgs {
   Tables t;

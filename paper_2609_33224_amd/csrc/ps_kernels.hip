@@ -420,7 +420,7 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
     G.pop_ctr[0] = 0u;
     G.pop_ctr[1] = 0u;
   }
-  if (blockIdx.x == 0 && threadIdx.x < kXcds) G.lctr_next[threadIdx.x] = 0u;  // the next window's
+  if (blockIdx.x == 0 && threadIdx.x < kXcds) G.lctr_next[threadIdx.x * kListCtrWords] = 0u;  // the next window's
   const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   bool want = false;
@@ -483,7 +483,7 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
   if (lm) {
     const uint32_t x = ((uint32_t)(blockIdx.x * blockDim.x + threadIdx.x) >> 6) % (uint32_t)kXcds;
     uint32_t base = 0u;
-    if (lane == 0) base = atomicAdd(&G.lctr[x], (uint32_t)__popcll(lm));
+    if (lane == 0) base = atomicAdd(&G.lctr[x * kListCtrWords], (uint32_t)__popcll(lm));
     base = (uint32_t)__shfl((int)base, 0);
     if (lead)
       G.lists[(size_t)x * G.lcap + base + (uint32_t)__popcll(lm & ((1ull << lane) - 1ull))] =
@@ -514,7 +514,7 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   // on XCD b % 8), so an XCD does not inherit one list's share of long walks
   static_assert(kXcds == 8, "the list walk maps workgroups to 8 lists");
   const uint32_t x = (blockIdx.x >> 3) & 7u;
-  const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x]);
+  const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x * kListCtrWords]);
   for (uint32_t idx = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u); idx < nx; idx += gridDim.x >> 3) {
     const unsigned long long ent = G.lists[(size_t)x * G.lcap + idx];
     const uint32_t slot = (uint32_t)(ent & 0xFFFFFFull);
