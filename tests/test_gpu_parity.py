@@ -290,6 +290,64 @@ def test_prefix_groups_shared_segments(ps, scorer):
         _check_edge(ps, scorer, _shared_pool_window(base=base), f"groups base={base}")
 
 
+def _shared_hit_window(base=301, crowded_non_holders=False, **kw):
+    """A popular first block (a 12-block shared prompt held by 86 of 96
+    instances, so its holders are a bitmap) under two sessions' segments:
+    most holders hit exactly the prompt (the shared-hit class, H* = 12),
+    six are exceptions (longer hits from a session's own blocks, one to
+    the segment's end with a cached tail after it, two with half the
+    prompt), ten instances hold none of it.  Members' segment lengths lie
+    on both sides of H*.  With crowded_non_holders the non-holders are
+    nearly full, so the 64 largest rooms all belong to holders."""
+    rng = np.random.default_rng(base)
+    SP = chain_hashes(12, base=base)
+    X = SP + chain_hashes(40, base=base + 10**6)
+    Y = SP + chain_hashes(30, base=base + 2 * 10**6)
+    tails = [chain_hashes(int(rng.integers(1, 4)), base=base + 10**8 + 10**4 * k) for k in range(6)]
+    pool = []
+
+    def put(seq):
+        off = len(pool)
+        pool.extend(seq)
+        return off
+
+    ox, oy = put(X), put(Y)
+    t_off = [put(t) for t in tails]
+    n_inst = 96
+    filler = chain_hashes(400, base=base + 5 * 10**7)
+    sets = [SP + filler[4 * i:4 * i + 3] for i in range(80)]    # the class: hit 12
+    sets += [X[:22], X[:32], X + tails[0], X[:17]]              # exceptions of X
+    sets += [SP[:6], SP[:6] + filler[350:352]]                   # exceptions: half the prompt
+    sets += [filler[300 + 4 * i:302 + 4 * i] for i in range(10)]  # non-holders
+    sets[5] = sets[5] + Y[12:20]                                  # an exception of Y only
+    reqs = []
+    for k, p in enumerate([8, 11, 12, 13, 17, 20, 22, 30, 40, 51, 52]):
+        reqs.append((ox, p, t_off[k % 3], len(tails[k % 3])))
+    reqs += [(ox, 52, t_off[0], len(tails[0])), (ox, 52, t_off[1], 0)]
+    reqs += [(oy, p, t_off[3 + k % 3], len(tails[3 + k % 3])) for k, p in enumerate([9, 12, 15, 20, 42])]
+    order = np.random.default_rng(base + 1).permutation(len(reqs))
+    reqs = [reqs[i] for i in order]
+    S = rng.integers(0, 500_000, n_inst)
+    if crowded_non_holders:
+        S[86:] = 4_194_304 - 64
+    return _edge(sets, None, pool=pool, reqs=reqs, S=S, cap=64, **kw)
+
+
+def test_popular_shared_hit_class(ps, scorer):
+    """The shared-hit class of popular groups (the fast path's class scan
+    and its fallbacks: H* at or past a member's segment end, no candidate
+    in T, a class not visible among the 64 largest rooms) against the
+    oracle and the path with set sizes."""
+    for base in (301, 302):
+        w = _shared_hit_window(base=base)
+        _check_edge(ps, scorer, w, f"shared hit {base}")
+        _check_edge(ps, scorer, w, f"shared hit {base} eta=0", eta=0.0)
+        _check_edge(ps, scorer, w, f"shared hit {base} tpot=1e-6", tpot_slo=1e-6)
+        _check_edge(ps, scorer, w, f"shared hit {base} b_max=40", b_max=40)
+    w = _shared_hit_window(base=303, crowded_non_holders=True)
+    _check_edge(ps, scorer, w, "shared hit crowded")
+
+
 def test_prefix_groups_window_sizes(ps, scorer):
     """Windows of growing and shrinking request counts on one context (the
     group table grows; later smaller windows reuse it)."""
