@@ -709,7 +709,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.hits_out = d_hits;
   a.scratch = c->d_scratch;
   a.grp = GroupTab{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0u, 0u, 0ull,
-                   nullptr, nullptr, nullptr, 0u};
+                   nullptr, nullptr, nullptr, 0u, 1u};
   a.sel = c->h_model.sel;
   a.defer_any = nullptr;
   a.defer_only = 0;
@@ -742,7 +742,9 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                      c->d_glist,
                      c->d_gpop + kListCtrWords * (1u + kXcds * (uint32_t)(c->ggen & 1u)),
                      c->d_gpop + kListCtrWords * (1u + kXcds * (uint32_t)((c->ggen + 1u) & 1u)),
-                     c->glcap};
+                     c->glcap,
+                     // walkers: half the resident waves (8 per CU)
+                     (uint32_t)(8 * c->num_cus)};
     a.defer_any = c->d_gpop + 1;
   }
   // The scoring kernel takes batches of a.batch requests per wave; a small

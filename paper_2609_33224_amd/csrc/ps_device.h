@@ -164,7 +164,14 @@ struct GroupTab {
   uint32_t* lctr;
   uint32_t* lctr_next;
   uint32_t lcap;
+  // walkers the walk pass aims for: with fewer groups than that, each group
+  // gets up to kGroupSplitMax waves, wave k walking the k-th part of the
+  // segment on each holder, and the record's hits are the minima of the
+  // parts' first misses (every new leader sets them to ~0 in the claim pass)
+  uint32_t walkers;
 };
+constexpr uint32_t kGroupSplitMax = 4;
+constexpr int32_t kGroupPartMin = 1024;  // positions per part at least
 
 // One of the pool's 64 largest rooms (descending; pads: room -1).
 struct alignas(16) TopRoom {

@@ -485,9 +485,12 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
     uint32_t base = 0u;
     if (lane == 0) base = atomicAdd(&G.lctr[x * kListCtrWords], (uint32_t)__popcll(lm));
     base = (uint32_t)__shfl((int)base, 0);
-    if (lead)
+    if (lead) {
       G.lists[(size_t)x * G.lcap + base + (uint32_t)__popcll(lm & ((1ull << lane) - 1ull))] =
           ((unsigned long long)(off + 1) << 24) | (unsigned long long)slot;
+      uint2* rec = G.rec + (size_t)slot * kGroupRec;  // hits: minima of the walk's parts
+      for (uint32_t t = 0; t < kGroupHold; ++t) rec[1 + t] = make_uint2(0u, 0xFFFFFFFFu);
+    }
   }
   if (want) slot = lslot[h];
   if (r < a.n_req)
@@ -513,14 +516,30 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   // every (grid / 8)-th after it: each list is spread over all XCDs (b runs
   // on XCD b % 8), so an XCD does not inherit one list's share of long walks
   static_assert(kXcds == 8, "the list walk maps workgroups to 8 lists");
+  // (with Q waves per group, entry v of the list is part v % Q of group
+  // v / Q)
   const uint32_t x = (blockIdx.x >> 3) & 7u;
-  const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x * kListCtrWords]);
-  for (uint32_t idx = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u); idx < nx; idx += gridDim.x >> 3) {
+  uint32_t groups = 0u;  // every list's length (the same in every wave)
+  for (int l = 0; l < kXcds; ++l) groups += G.lctr[l * kListCtrWords];
+  groups = (uint32_t)__builtin_amdgcn_readfirstlane((int)groups);
+  const uint32_t q0 = groups ? G.walkers / groups : 1u;
+  const uint32_t Q = q0 < 1u ? 1u : (q0 > kGroupSplitMax ? kGroupSplitMax : q0);
+  const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x * kListCtrWords]) * Q;
+  for (uint32_t v = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u); v < nx; v += gridDim.x >> 3) {
+    const uint32_t idx = v / Q, part = v % Q;
     const unsigned long long ent = G.lists[(size_t)x * G.lcap + idx];
     const uint32_t slot = (uint32_t)(ent & 0xFFFFFFull);
     const int64_t pre_off = (int64_t)(ent >> 24) - 1;
     const int32_t plen =
         (int32_t)(G.plen[slot] & ((1ull << kGroupGenShift) - 1ull));  // every member lies in the pool
+    // this wave's part of the segment: [s0, s1), at least kGroupPartMin
+    // positions and whole 512-position compare steps (a part costs its own
+    // preamble of dependent reads)
+    const int32_t step0 = (((plen + (int32_t)Q - 1) / (int32_t)Q) + 511) / 512 * 512;
+    const int32_t step = step0 > kGroupPartMin ? step0 : kGroupPartMin;
+    const int32_t s0 = (int32_t)part * step;
+    const int32_t s1 = s0 + step < plen ? s0 + step : plen;
+    if (part != 0u && s0 >= plen) continue;  // (uniform: no workgroup barrier skipped)
     const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
     const int32_t nst = plen < kStage ? plen : kStage;
     __syncthreads();
@@ -532,6 +551,7 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
     uint2* rec = G.rec + (size_t)slot * kGroupRec;
     uint32_t cnt = 0u;
     if (found0 && cnt0 > kGroupHold) {
+      if (part != 0u) continue;  // a popular group: one wave walks all holders
       uint32_t row = 0;
       if (lane == 0) row = atomicAdd(G.pop_ctr, 1u);
       row = (uint32_t)__shfl((int)row, 0);
@@ -604,18 +624,28 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
         if (lane == 0) rec[kGroupClsWord] = make_uint2(clsw, off0);
       }
     } else if (found0) {
+      // the walk from s0 on the chain cut at s1: the first position there
+      // whose block the holder lacks
+      const ChainRef cp{c.pre, c.tail, s1, s1};
       const uint32_t id = (uint32_t)lane < cnt0 ? a.x.holders[off0 + lane] : 0u;
       uint32_t myhit = 0;
       for (uint32_t k = 0; k < cnt0; ++k) {
         const uint32_t idk = (uint32_t)__shfl((int)id, (int)k);
         // a group's segment is typically a long run: 512 positions per step
-        const uint32_t hk = run_walk<true, 8, 8>(a.t, idk, c, stage, 0, g, s);
-        if ((uint32_t)lane == k) myhit = hk;
+        const uint32_t hk = s0 < s1 ? run_walk<true, 8, 8>(a.t, idk, cp, stage, s0, g, s) : (uint32_t)s1;
+        if ((uint32_t)lane == k) myhit = (int32_t)hk < s1 ? hk : (uint32_t)plen;  // no miss here: plen
       }
-      if ((uint32_t)lane < cnt0) rec[1 + lane] = make_uint2(id, myhit);
+      if ((uint32_t)lane < cnt0) {
+        if (Q == 1u) {
+          rec[1 + lane] = make_uint2(id, myhit);
+        } else {
+          if (part == 0u) rec[1 + lane].x = id;
+          atomicMin(&rec[1 + lane].y, myhit);
+        }
+      }
       cnt = cnt0;
     }
-    if (lane == 0) rec[0] = make_uint2((uint32_t)plen, cnt);
+    if (lane == 0 && part == 0u) rec[0] = make_uint2((uint32_t)plen, cnt);
   }
 }
 
