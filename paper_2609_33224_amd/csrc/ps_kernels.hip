@@ -278,12 +278,16 @@ __global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, con
 // drops out at position pos gets put(id, pos); a single survivor continues
 // on its own row, and survivors of the whole chain get put(id, ell).  bmN
 // must be clear; both bitmaps are clear on return.  Wave-uniform arguments.
-template <bool STAGED, class Put>
+// PF: on pools of at most 4,096 instances (one bitmap word per lane) the
+// holder bitmaps of a batch's popular positions are loaded together, before
+// the batch is applied in order.
+template <bool STAGED, bool PF, class Put>
 __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c,
                                            const uint64_t* stage, uint64_t* bmA, uint64_t* bmN,
                                            int32_t nw, uint32_t nalive, int32_t p, Put put,
                                            int lane, int g, int s) {
   const int32_t ell = c.len;
+  const bool pf = PF && nw <= 64;
   while (p < ell && nalive > 0) {
     if (nalive == 1) {  // a single live holder: walk its own table
       uint32_t who = 0;
@@ -311,7 +315,18 @@ __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c
     const uint64_t kq =
       jq < ell ? ((STAGED && jq < kStage) ? stage[jq] : chain_global(c, jq)) : 0ull;
     const IdxHit hq = index_lookup(a.x, kq, jq < ell, g, s);
+    uint64_t pw[8];
+    if (PF) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const bool f = __shfl(hq.found ? 1 : 0, 8 * t) != 0;
+        const uint32_t off = __shfl(hq.off, 8 * t), cnt = __shfl(hq.cnt, 8 * t);
+        pw[t] = pf && f && cnt > kPopular && lane < nw ? a.x.bitmaps[(size_t)off * a.x.nw + lane] : 0ull;
+      }
+    }
     int32_t used = 0;
+    constexpr int kUnroll = PF ? 8 : 1;  // (pw stays in registers)
+#pragma unroll kUnroll
     for (int t = 0; t < 8; ++t) {
       const int32_t pos = p + t;
       if (pos >= ell || nalive <= 1) break;
@@ -322,7 +337,7 @@ __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c
         uint32_t live = 0;
         for (int32_t w = lane; w < nw; w += 64) {
           const uint64_t aw = bmA[w];
-          const uint64_t nwd = aw & bm[w];
+          const uint64_t nwd = aw & (pf ? pw[t] : bm[w]);
           uint64_t d = aw & ~nwd;
           while (d) {
             const int b = __builtin_ctzll(d);
@@ -569,8 +584,8 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
         }
         __syncthreads();
         uint32_t* hp = G.pop + (size_t)row * (size_t)a.n_inst;
-        index_walk<true>(a, c, stage, bmA, bmN, nw, cnt0, 1,
-                         [&](uint32_t id, uint32_t h) { hp[id] = h; }, lane, g, s);
+        index_walk<true, true>(a, c, stage, bmA, bmN, nw, cnt0, 1,
+                               [&](uint32_t id, uint32_t h) { hp[id] = h; }, lane, g, s);
         cnt = kGroupPop | row;
         // The shared-hit class: H* = the most frequent hit among the holders
         // of the first 64-instance word that has any; when at most
@@ -1014,8 +1029,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       } else if (!grp) {
         for (int32_t w = lane; w < nw; w += 64) bmA[w] = bmC[w];
         __syncthreads();
-        index_walk<true>(a, c, stage, bmA, bmN, nw, nCand, 1,
-                         [&](uint32_t id, uint32_t h) { hits[id] = encode_hit(h); }, lane, g, s);
+        index_walk<true, false>(a, c, stage, bmA, bmN, nw, nCand, 1,
+                                [&](uint32_t id, uint32_t h) { hits[id] = encode_hit(h); }, lane, g, s);
       } else {
         // many candidates with a popular group's result: lanes over the
         // pool, resumes walked one at a time
