@@ -664,7 +664,13 @@ def main():
 
     evals = win.n_req * win.n_inst
     src_hash = kernel_source_hash()
-    tent = traffic_for(args.workload, src_hash) or {}
+    from paper_2609_33224_amd import build as ps_build
+    lib_id = ps.ps_build_id()
+    lib_fresh = lib_id == ps_build.source_hash()
+    if not lib_fresh:
+        print(f"bench: libpackserve.so was built from other sources ({lib_id}); "
+              "rebuild it (__graft_entry__.build()); counter bytes are not applied", file=sys.stderr)
+    tent = (traffic_for(args.workload, src_hash) or {}) if lib_fresh else {}
     traffic = tent.get("bytes_per_launch")
     probe_meas = tent.get("probe_bytes_per_window")
     def rate(nbytes, ms):
@@ -712,6 +718,8 @@ def main():
                                                        if probe_meas is not None else None),
                          "evals_per_s": win.n_req * win.n_inst / (probe_ms * 1e-3)},
         "kernel_source_sha": src_hash,
+        "library_build_id": lib_id,
+        "library_matches_sources": lib_fresh,
         "load_instances_s": load_s,
         "host_call_s_incl_pcie": host_call_s,
         "placed": int((res["instance"] >= 0).sum()),

@@ -355,6 +355,13 @@ ps_status ps_read_model(ps_ctx* ctx, float* gamma, float* lout, int32_t* n_seg);
 /* Message of the last failed call on ctx (or of ps_create when ctx is NULL). */
 const char* ps_last_error(const ps_ctx* ctx);
 
+/* Identity of this build: the first 16 hex digits of the SHA-256 of the
+ * library's sources (the csrc files in name order, then this header), as
+ * the build computed it, so a caller can tell a library built from other
+ * sources; "unknown" for a build that did not pass one.  A static string,
+ * never freed; no error case. */
+const char* ps_build_id(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -106,6 +106,7 @@ def load_library() -> ctypes.CDLL:
         "ps_read_state": ([vp, vp, vp, vp, vp, vp], i32),
         "ps_table_info": ([vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i32)], i32),
         "ps_last_error": ([vp], ctypes.c_char_p),
+        "ps_build_id": ([], ctypes.c_char_p),
         "ps_apply_events": ([vp, vp, i32], i32),
         "ps_feedback_decode": ([vp, vp, vp, vp, i32], i32),
         "ps_feedback_output": ([vp, vp, i32], i32),
@@ -188,6 +189,11 @@ def ps_destroy(ctx) -> None:
 def ps_last_error(ctx) -> str:
     msg = load_library().ps_last_error(ctx)
     return msg.decode() if msg else ""
+
+
+def ps_build_id() -> str:
+    """Source hash the library was built from (build.source_hash() of a fresh build)."""
+    return load_library().ps_build_id().decode()
 
 
 def ps_load_instances(ctx, n_inst, table_cap_blocks, blk_off, blk, decoding, queued,

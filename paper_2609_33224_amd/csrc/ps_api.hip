@@ -414,6 +414,11 @@ const char* ps_last_error(const ps_ctx* c) {
   return c ? c->err.c_str() : g_create_error.c_str();
 }
 
+#ifndef PS_SOURCE_HASH
+#define PS_SOURCE_HASH "unknown"
+#endif
+const char* ps_build_id(void) { return PS_SOURCE_HASH; }
+
 ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m) {
   if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
   if (!in) return fail(c, PS_E_INVAL, "instances is NULL");

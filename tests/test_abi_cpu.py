@@ -32,6 +32,14 @@ def test_library_exports_every_declared_symbol():
     assert not missing, missing
 
 
+def test_library_is_built_from_these_sources():
+    """ps_build_id() names the sources the library was compiled from: a
+    stale libpackserve.so (sources changed, no rebuild) fails here."""
+    import paper_2609_33224_amd as ps
+    from paper_2609_33224_amd import build
+    assert ps.ps_build_id() == build.source_hash()
+
+
 def test_struct_layouts_match_header():
     import paper_2609_33224_amd as ps
     assert ps.PS_REQ_DTYPE.itemsize == 24
