@@ -140,9 +140,10 @@ constexpr uint32_t kGroupNoSlot = 0xFFFFFFFFu;
 constexpr uint32_t kGroupPop = 0x80000000u;
 constexpr size_t kGroupPopBytes = (size_t)64 << 20;  // popular area: hits of n_inst u32 per row
 // Header of the popular area: the first line holds the rows-taken and
-// deferral words, then two sets (window parities) of kXcds leader list
-// lengths, each length on a 128-byte line of its own (a wave's atomic on
-// one list does not queue behind the others' on a shared line).
+// deferral words, then two sets (window parities) of kXcds leader lists'
+// {length, longest leader segment}, each pair on a 128-byte line of its own
+// (a wave's atomics on one list do not queue behind the others' on a shared
+// line).
 constexpr uint32_t kListCtrWords = 32;  // 128 bytes
 
 struct GroupTab {
@@ -157,9 +158,9 @@ struct GroupTab {
   uint32_t mask;             // slots - 1
   uint64_t gen;              // this window's generation, 1 .. kGroupGenMax
   // this window's leaders in kXcds lists (list x at x * lcap), each entry
-  // (pre_off + 1) << 24 | slot, with their lengths in lctr[x * kListCtrWords];
-  // lctr_next: the other window parity's lengths, cleared here for the next
-  // window
+  // (pre_off + 1) << 24 | slot, with their lengths in lctr[x * kListCtrWords]
+  // and their longest segments in the next word; lctr_next: the other window
+  // parity's words, cleared here for the next window
   unsigned long long* lists;
   uint32_t* lctr;
   uint32_t* lctr_next;

@@ -435,7 +435,8 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
     G.pop_ctr[0] = 0u;
     G.pop_ctr[1] = 0u;
   }
-  if (blockIdx.x == 0 && threadIdx.x < kXcds) G.lctr_next[threadIdx.x * kListCtrWords] = 0u;  // the next window's
+  if (blockIdx.x == 0 && threadIdx.x < 2 * kXcds)  // the next window's list lengths and longest segments
+    G.lctr_next[(threadIdx.x >> 1) * kListCtrWords + (threadIdx.x & 1u)] = 0u;
   const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   bool want = false;
@@ -495,8 +496,12 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
   // that writes it)
   const bool lead = first && slot >= 0 && leader;
   const uint64_t lm = __ballot(lead);
+  const uint32_t x = ((uint32_t)(blockIdx.x * blockDim.x + threadIdx.x) >> 6) % (uint32_t)kXcds;
+  // a bound on every group's segment length (its claims' lengths; only
+  // lengths above one part's minimum matter to the walk pass)
+  const uint32_t cmax = (uint32_t)(~wave_min_u64(~(uint64_t)(uint32_t)(first && slot >= 0 ? llen[h] : 0)));
+  if (lane == 0 && cmax > (uint32_t)kGroupPartMin) atomicMax(&G.lctr[x * kListCtrWords + 1], cmax);
   if (lm) {
-    const uint32_t x = ((uint32_t)(blockIdx.x * blockDim.x + threadIdx.x) >> 6) % (uint32_t)kXcds;
     uint32_t base = 0u;
     if (lane == 0) base = atomicAdd(&G.lctr[x * kListCtrWords], (uint32_t)__popcll(lm));
     base = (uint32_t)__shfl((int)base, 0);
@@ -534,10 +539,18 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   // (with Q waves per group, entry v of the list is part v % Q of group
   // v / Q)
   const uint32_t x = (blockIdx.x >> 3) & 7u;
-  uint32_t groups = 0u;  // every list's length (the same in every wave)
-  for (int l = 0; l < kXcds; ++l) groups += G.lctr[l * kListCtrWords];
+  uint32_t groups = 0u, pmax = 0u;  // every list's length and longest segment (the same in every wave)
+  for (int l = 0; l < kXcds; ++l) {
+    const uint2 lw = *reinterpret_cast<const uint2*>(G.lctr + l * kListCtrWords);
+    groups += lw.x;
+    pmax = lw.y > pmax ? lw.y : pmax;
+  }
   groups = (uint32_t)__builtin_amdgcn_readfirstlane((int)groups);
-  const uint32_t q0 = groups ? G.walkers / groups : 1u;
+  pmax = (uint32_t)__builtin_amdgcn_readfirstlane((int)pmax);
+  // no more parts than the longest segment fills (kGroupPartMin positions each)
+  const uint32_t qp = (pmax + kGroupPartMin - 1u) / kGroupPartMin;
+  uint32_t q0 = groups ? G.walkers / groups : 1u;
+  q0 = q0 < qp ? q0 : qp;
   const uint32_t Q = q0 < 1u ? 1u : (q0 > kGroupSplitMax ? kGroupSplitMax : q0);
   const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x * kListCtrWords]) * Q;
   for (uint32_t v = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u); v < nx; v += gridDim.x >> 3) {
