@@ -816,7 +816,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
         const uint32_t hs = clsw & 0xFFFFFFu, nexc = clsw >> 24;
         const int32_t p0 = q.pre_len < gm.plen ? q.pre_len : gm.plen;
         if (clsw != kGroupNone && (int32_t)hs < p0) {
-          const uint64_t* hb = a.x.bitmaps + (size_t)__builtin_amdgcn_readfirstlane((int)cwd.y) * a.x.nw;
+          // the holder bitmap, copied to LDS (bmA: free outside the index
+          // walk, which sets it first): the class scan tests one bit per
+          // instance
+          const uint64_t* hg = a.x.bitmaps + (size_t)__builtin_amdgcn_readfirstlane((int)cwd.y) * a.x.nw;
+          for (int32_t w = lane; w < nw; w += 64) bmA[w] = hg[w];
+          const uint64_t* hb = bmA;
           const TopRoom trm = a.rtop[lane];
           // exceptions: state, eligibility, hit (resumed where it reaches p0)
           const bool eact = (uint32_t)lane < nexc;
@@ -864,27 +869,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
             const bool admit0 = any0 && (!kvc || (W0 - wmin) / Z <= m.eta);
             Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
             if (eel) evaluate_with<true>(m, acc, eid, ehit, [&]() { return est; }, L, Lf, wmin, Z, kvc, slo);
-            if (admitK) {  // the class's first member of T in key order
+            if (admitK) {  // the class's first member of T in key order (two chunks of 64 in flight)
               const float nK = (float)(L - cK), cKf = (float)cK;
               bool found = false;
-              for (int32_t base = 0; base < n_inst && !found; base += 64) {
-                const int32_t k = base + lane;
-                bool ok = false;
-                uint32_t i = 0;
-                InstState st{};
-                if (k < n_inst) {
-                  i = a.order0[k];
-                  st = a.inst_key[k];
-                  ok = test_bit(hb, i) && !test_bit(bmC, i) && eligible(m, st.A1, st.S, L) &&
-                       ((m.flags & PS_F_NO_TPOT_FILTER) || latency(m, st, nK, cKf, L).tpot < m.tau);
-                }
-                const uint64_t om = __ballot(ok);
-                if (om) {
-                  if (lane == __builtin_ctzll(om)) {
-                    const uint64_t kt = select_key(m.sel, st, hs, i, 0ull);
-                    acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+              for (int32_t base = 0; base < n_inst && !found; base += 128) {
+                uint32_t i[2];
+                InstState st[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                  const int32_t k = base + 64 * u + lane;
+                  i[u] = 0u;
+                  st[u] = InstState{};
+                  if (k < n_inst) {
+                    i[u] = a.order0[k];
+                    st[u] = a.inst_key[k];
                   }
-                  found = true;
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                  const int32_t k = base + 64 * u + lane;
+                  const bool ok = k < n_inst && test_bit(hb, i[u]) && !test_bit(bmC, i[u]) &&
+                                  eligible(m, st[u].A1, st[u].S, L) &&
+                                  ((m.flags & PS_F_NO_TPOT_FILTER) || latency(m, st[u], nK, cKf, L).tpot < m.tau);
+                  const uint64_t om = __ballot(ok);
+                  if (!found && om) {
+                    if (lane == __builtin_ctzll(om)) {
+                      const uint64_t kt = select_key(m.sel, st[u], hs, i[u], 0ull);
+                      acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                    }
+                    found = true;
+                  }
                 }
               }
             }
