@@ -807,9 +807,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
       // kGroupHold exceptions): the exceptions are candidates of their own,
       // the other holders one class (hit H*, one penalty, the first member of
       // T in key order found by a scan of the key-ordered states), the
-      // non-holders the zero-hit class.  When a class's eligibility cannot be
-      // told from the 64 largest rooms, or no candidate is in T, the request
-      // takes the general path below.
+      // non-holders the zero-hit class.  When no candidate is in T, the
+      // fallback key is the minimum over C: the exceptions in it and the
+      // eligible members of the admitted classes, scanned in id order.  When
+      // a class's eligibility cannot be told from the 64 largest rooms, the
+      // request takes the general path below.
       if (FAST && gpop) {
         const uint2 cwd = lrec[b * kGroupRec + kGroupClsWord];
         const uint32_t clsw = (uint32_t)__builtin_amdgcn_readfirstlane((int)cwd.x);
@@ -927,15 +929,46 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
               }
             }
             const uint64_t keyT = wave_min_u64(acc.keyT);
-            if (keyT != ~0ull) {  // (no candidate in T: the fallback needs the general path)
-              const uint32_t best = (uint32_t)(keyT & 0xFFFFu);
+            uint64_t keyF = ~0ull;
+            if (keyT == ~0ull) {
+              // T is empty: the fallback key over C, whose members outside
+              // the exceptions are the eligible members of the admitted
+              // classes (the exceptions' keys are in acc.keyF); instances in
+              // id order, two chunks of 64 states in flight
+              const int64_t nKt = L - cK;
+              for (int32_t base = 0; base < n_inst; base += 128) {
+                InstState st[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                  const int32_t i = base + 64 * u + lane;
+                  st[u] = i < n_inst ? state_of((uint32_t)i) : InstState{};
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                  const uint32_t i = (uint32_t)(base + 64 * u + lane);
+                  if ((int32_t)i < n_inst && !test_bit(bmC, i) && eligible(m, st[u].A1, st[u].S, L)) {
+                    const bool hold = test_bit(hb, i);
+                    if (hold ? admitK : admit0) {
+                      const uint32_t v = hold ? hs : 0u;
+                      const uint64_t lm = (uint64_t)(st[u].P + (hold ? nKt : L)) * (uint64_t)st[u].A1;
+                      const uint64_t kf = (m.flags & PS_F_FALLBACK_DCQ) ? dcq_key(st[u], v, i) : ((lm << 16) | i);
+                      acc.keyF = kf < acc.keyF ? kf : acc.keyF;
+                    }
+                  }
+                }
+              }
+              keyF = wave_min_u64(acc.keyF);
+            }
+            if (keyT != ~0ull || keyF != ~0ull) {  // (neither: a non-finite model; the general path decides)
+              const bool t = keyT != ~0ull;
+              const uint32_t best = (uint32_t)((t ? keyT : keyF) & 0xFFFFu);
               const uint64_t em = __ballot(eact && eid == best);
               const uint32_t ev = (uint32_t)__shfl((int)ehit, em ? __builtin_ctzll(em) : 0);
               const uint32_t v = em ? ev : test_bit(hb, best) ? hs : 0u;
               const int64_t c_tok = (int64_t)v * m.bs;
               const Lat lt = latency(m, state_of(best), (float)(L - c_tok), (float)c_tok, L);
               res = ps_result{(int32_t)best, (int32_t)v, lt.ttft, lt.tpot,
-                              lt.ttft > slo ? PS_R_TTFT_MISS : 0u};
+                              (t ? 0u : PS_R_FALLBACK) | (lt.ttft > slo ? PS_R_TTFT_MISS : 0u)};
               decided = true;
             }
           }

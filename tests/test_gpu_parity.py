@@ -336,13 +336,17 @@ def _shared_hit_window(base=301, crowded_non_holders=False, **kw):
 def test_popular_shared_hit_class(ps, scorer):
     """The shared-hit class of popular groups (the fast path's class scan
     and its fallbacks: H* at or past a member's segment end, no candidate
-    in T, a class not visible among the 64 largest rooms) against the
-    oracle and the path with set sizes."""
+    in T (the fallback key by LMetric and by D-C-Q, with and without the
+    recomputation budget admitting every class), a class not visible among
+    the 64 largest rooms) against the oracle and the path with set sizes."""
     for base in (301, 302):
         w = _shared_hit_window(base=base)
         _check_edge(ps, scorer, w, f"shared hit {base}")
         _check_edge(ps, scorer, w, f"shared hit {base} eta=0", eta=0.0)
         _check_edge(ps, scorer, w, f"shared hit {base} tpot=1e-6", tpot_slo=1e-6)
+        _check_edge(ps, scorer, w, f"shared hit {base} tpot=1e-6 dcq fallback", tpot_slo=1e-6,
+                    flags=ps.PS_F_FALLBACK_DCQ)
+        _check_edge(ps, scorer, w, f"shared hit {base} tpot=1e-6 eta=0", tpot_slo=1e-6, eta=0.0)
         _check_edge(ps, scorer, w, f"shared hit {base} b_max=40", b_max=40)
     w = _shared_hit_window(base=303, crowded_non_holders=True)
     _check_edge(ps, scorer, w, "shared hit crowded")
