@@ -49,6 +49,7 @@ struct ps_ctx {
   int32_t rows_wpc = 0;              // the same for the four-requests-per-wave scorer
   int4* d_lm = nullptr;              // zero-hit admission thresholds in that order
   int32_t* d_lm1 = nullptr;          // their maxima per 64 positions
+  uint4* d_csum = nullptr;           // per 64 positions: least t_iter (A1 > 1, A1 <= 1), largest room
   GIndex x{nullptr, nullptr, nullptr, 0, 0, 64};
   DevModel* d_model = nullptr;
   unsigned long long* d_counter = nullptr;
@@ -267,6 +268,7 @@ void free_snapshot(ps_ctx* c) {
   dfree(c->d_rtop);
   dfree(c->d_lm);
   dfree(c->d_lm1);
+  dfree(c->d_csum);
   dfree(c->d_scratch);
   ps_free_index(&c->x);
   c->loaded = false;
@@ -276,7 +278,7 @@ void free_snapshot(ps_ctx* c) {
 // before the entry point returns.
 ps_status refresh_lmax(ps_ctx* c) {
   HIP_TRY(c, ps_launch_lmax(c->d_inst_key, c->d_order0, c->d_model, c->n_inst, c->d_lm, c->d_lm1,
-                            c->stream));
+                            c->d_csum, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return PS_OK;
 }
@@ -491,6 +493,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
     dfree(fresh.d_rtop);
     dfree(fresh.d_lm);
     dfree(fresh.d_lm1);
+    dfree(fresh.d_csum);
     dfree(fresh.d_scratch);
     ps_free_index(&fresh.x);
     dfree(d_off);
@@ -513,6 +516,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_rtop, (size_t)kTopRooms * sizeof(TopRoom));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_lm, (size_t)n * sizeof(int4));
   if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_lm1, (size_t)((n + 63) / 64) * sizeof(int32_t));
+  if (e == hipSuccess) e = hipMalloc((void**)&fresh.d_csum, (size_t)((n + 63) / 64) * sizeof(uint4));
   if (e == hipSuccess && rows)
     e = hipMalloc((void**)&fresh.d_scratch, (size_t)rows * (size_t)n * sizeof(uint16_t));
   if (e == hipSuccess) e = hipMalloc((void**)&d_off, (size_t)(n + 1) * sizeof(int64_t));
@@ -605,6 +609,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->rows_wpc = 0;
   c->d_lm = fresh.d_lm;
   c->d_lm1 = fresh.d_lm1;
+  c->d_csum = fresh.d_csum;
   c->x = fresh.x;
   c->d_scratch = fresh.d_scratch;
   c->scratch_rows = rows;
@@ -632,6 +637,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   fresh.d_rtop = nullptr;
   fresh.d_lm = nullptr;
   fresh.d_lm1 = nullptr;
+  fresh.d_csum = nullptr;
   fresh.x = GIndex{nullptr, nullptr, nullptr, 0, 0, 64};
   fresh.d_scratch = nullptr;
   const ps_status lst = refresh_lmax(c);
@@ -701,6 +707,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.rtop = c->d_rtop;
   a.lm = c->d_lm;
   a.lm1 = c->d_lm1;
+  a.csum = c->d_csum;
   a.inst = c->d_inst;
   a.room = c->d_room;
   a.model = c->d_model;

@@ -499,11 +499,16 @@ struct Lat {
 // by the segment's EMA factor; prefill interference amortised over the
 // median output length, only on a busy instance) and Eq. 4's TTFT with the
 // queue estimate a0 Q + a1 P.
+// Eq. 8's decode-iteration time with the request's L tokens added to S.
+__device__ __forceinline__ float t_iter_of(const DevModel& m, const InstState& st, int64_t L) {
+  const float* sg = m.seg[st.seg];
+  return sg[3] * (sg[0] + sg[1] * (float)st.A1 + sg[2] * (float)(st.S + L));
+}
+
 __device__ __forceinline__ Lat latency(const DevModel& m, const InstState& st, float n, float c,
                                        int64_t L) {
   const float tp = t_prefill(m, n, c);
-  const float* sg = m.seg[st.seg];
-  const float t_iter = sg[3] * (sg[0] + sg[1] * (float)st.A1 + sg[2] * (float)(st.S + L));
+  const float t_iter = t_iter_of(m, st, L);
   const float interf = st.A1 > 1 ? tp / m.lout1 : 0.0f;
   Lat r;
   r.tpot = t_iter + interf;

@@ -191,6 +191,10 @@ struct ScoreArgs {
   const InstState* inst_key;   // the instances' states in that order
   const int4* lm;              // key order: {longest zero-hit admitted chain (blocks, -1 none), id, D, Q}
   const int32_t* lm1;          // maxima of lm[].x over 64-entry chunks
+  // key order, per 64-entry chunk: {least t_iter at L = 0 over the
+  // instances with A1 > 1, the same over A1 <= 1 (fp32 bits; +inf for
+  // none), largest room (int64; -1 for none)}
+  const uint4* csum;
   const InstState* inst;
   const int64_t* room;   // per instance: kv_cap - S if A1 <= b_max, else -1 (eligible iff L <= room)
   const TopRoom* rtop;   // the kTopRooms largest rooms
@@ -315,7 +319,8 @@ void ps_free_index(ps::GIndex* x);
 hipError_t ps_launch_commit(const ps::CommitArgs& a, hipStream_t s);
 // Zero-hit admission thresholds in key order and their chunk maxima.
 hipError_t ps_launch_lmax(const ps::InstState* inst_key, const uint32_t* order0,
-                          const ps::DevModel* m, int32_t n, int4* lm, int32_t* lm1, hipStream_t s);
+                          const ps::DevModel* m, int32_t n, int4* lm, int32_t* lm1, uint4* csum,
+                          hipStream_t s);
 // Prefix groups of a window: slot of every request and the longest member
 // segment per group, then the walks of the leaders.
 hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s);  // grid: a multiple of 64

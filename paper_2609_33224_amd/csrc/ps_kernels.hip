@@ -244,12 +244,22 @@ __global__ void order_place_kernel(const ps_req* reqs, int32_t n, int64_t pool_l
 // chain is admitted.  lm1 = the maximum over each 64-entry chunk.
 __global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, const uint32_t* order0,
                                                   const DevModel* mp, int32_t n, int4* lm,
-                                                  int32_t* lm1) {
+                                                  int32_t* lm1, uint4* csum) {
   const DevModel& m = *mp;
   const int32_t k = blockIdx.x * 64 + threadIdx.x;
   int32_t best = -1;
+  uint32_t tb = 0xFFFFFFFFu, ti = 0xFFFFFFFFu;  // order-preserving bits (sortable_bits)
+  uint64_t rm1 = 0ull;                           // room + 1
   if (k < n) {
     const InstState st = inst_key[k];
+    // the chunk summary for scans of a class with c > 0 (every member's
+    // TPOT is at least its t_iter at L = 0 plus the class's interference
+    // when A1 > 1, under a monotone model)
+    const uint32_t t0 = sortable_bits(t_iter_of(m, st, 0));
+    if (st.A1 > 1) tb = t0;
+    else ti = t0;
+    const int64_t room = st.A1 <= m.b_max ? m.kv_cap - st.S : -1;
+    rm1 = room >= 0 ? (uint64_t)(room + 1) : 0ull;
     auto admits = [&](int32_t ell) {
       const int64_t L = (int64_t)ell * m.bs;
       if (!eligible(m, st.A1, st.S, L)) return false;
@@ -268,7 +278,15 @@ __global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, con
     lm[k] = make_int4(best, (int)order0[k], st.D, st.Q);
   }
   const uint64_t mx = ~wave_min_u64(~(uint64_t)(uint32_t)(best + 1));
-  if (threadIdx.x == 0) lm1[blockIdx.x] = (int32_t)mx - 1;
+  const uint32_t tbm = wave_min_u32(tb), tim = wave_min_u32(ti);
+  const uint64_t rmx = ~wave_min_u64(~rm1) - 1ull;
+  auto unsort = [](uint32_t b) {  // inverse of sortable_bits (all ones: +inf, no member)
+    return b == 0xFFFFFFFFu ? 0x7F800000u : ((b & 0x80000000u) ? (b & 0x7FFFFFFFu) : ~b);
+  };
+  if (threadIdx.x == 0) {
+    lm1[blockIdx.x] = (int32_t)mx - 1;
+    csum[blockIdx.x] = make_uint4(unsort(tbm), unsort(tim), (uint32_t)rmx, (uint32_t)(rmx >> 32));
+  }
 }
 
 // Hits of the live holders (the bits of bmA, nalive of them, all holding
@@ -871,35 +889,58 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
             const bool admit0 = any0 && (!kvc || (W0 - wmin) / Z <= m.eta);
             Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
             if (eel) evaluate_with<true>(m, acc, eid, ehit, [&]() { return est; }, L, Lf, wmin, Z, kvc, slo);
-            if (admitK) {  // the class's first member of T in key order (two chunks of 64 in flight)
+            if (admitK) {  // the class's first member of T in key order
               const float nK = (float)(L - cK), cKf = (float)cK;
+              // chunks of 64 key-ordered instances that may hold one: some
+              // room holds L, and (monotone model: TPOT is at least t_iter
+              // at L = 0, plus the class's interference when A1 > 1) some
+              // lower bound passes the TPOT test; two chunks in flight
+              const bool notpot = (m.flags & PS_F_NO_TPOT_FILTER) != 0u;
+              const float xK = t_prefill(m, nK, cKf) / m.lout1;
+              const int32_t n1 = (n_inst + 63) >> 6;
               bool found = false;
-              for (int32_t base = 0; base < n_inst && !found; base += 128) {
-                uint32_t i[2];
-                InstState st[2];
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                  const int32_t k = base + 64 * u + lane;
-                  i[u] = 0u;
-                  st[u] = InstState{};
-                  if (k < n_inst) {
-                    i[u] = a.order0[k];
-                    st[u] = a.inst_key[k];
-                  }
+              for (int32_t c0 = 0; c0 < n1 && !found; c0 += 64) {
+                const int32_t cc = c0 + lane;
+                bool may = false;
+                if (cc < n1) {
+                  const uint4 cs = a.csum[cc];
+                  const int64_t rmx = (int64_t)(((uint64_t)cs.w << 32) | cs.z);
+                  may = rmx >= L && (notpot || __uint_as_float(cs.x) + xK < m.tau ||
+                                     __uint_as_float(cs.y) < m.tau);
                 }
+                uint64_t cm = __ballot(may);
+                while (cm && !found) {
+                  int32_t kc[2];
+                  kc[0] = c0 + __builtin_ctzll(cm);
+                  cm &= cm - 1;
+                  kc[1] = cm ? c0 + __builtin_ctzll(cm) : -1;
+                  if (cm) cm &= cm - 1;
+                  uint32_t i[2];
+                  InstState st[2];
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                  const int32_t k = base + 64 * u + lane;
-                  const bool ok = k < n_inst && test_bit(hb, i[u]) && !test_bit(bmC, i[u]) &&
-                                  eligible(m, st[u].A1, st[u].S, L) &&
-                                  ((m.flags & PS_F_NO_TPOT_FILTER) || latency(m, st[u], nK, cKf, L).tpot < m.tau);
-                  const uint64_t om = __ballot(ok);
-                  if (!found && om) {
-                    if (lane == __builtin_ctzll(om)) {
-                      const uint64_t kt = select_key(m.sel, st[u], hs, i[u], 0ull);
-                      acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                  for (int u = 0; u < 2; ++u) {
+                    const int32_t k = kc[u] * 64 + lane;
+                    i[u] = 0u;
+                    st[u] = InstState{};
+                    if (kc[u] >= 0 && k < n_inst) {
+                      i[u] = a.order0[k];
+                      st[u] = a.inst_key[k];
                     }
-                    found = true;
+                  }
+#pragma unroll
+                  for (int u = 0; u < 2; ++u) {
+                    const int32_t k = kc[u] * 64 + lane;
+                    const bool ok = kc[u] >= 0 && k < n_inst && test_bit(hb, i[u]) && !test_bit(bmC, i[u]) &&
+                                    eligible(m, st[u].A1, st[u].S, L) &&
+                                    (notpot || latency(m, st[u], nK, cKf, L).tpot < m.tau);
+                    const uint64_t om = __ballot(ok);
+                    if (!found && om) {
+                      if (lane == __builtin_ctzll(om)) {
+                        const uint64_t kt = select_key(m.sel, st[u], hs, i[u], 0ull);
+                        acc.keyT = kt < acc.keyT ? kt : acc.keyT;
+                      }
+                      found = true;
+                    }
                   }
                 }
               }
@@ -2047,10 +2088,10 @@ hipError_t ps_launch_lean_rows(const ScoreArgs& a, int grid, hipStream_t s) {
 }
 
 hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, const DevModel* m,
-                          int32_t n, int4* lm, int32_t* lm1, hipStream_t s) {
+                          int32_t n, int4* lm, int32_t* lm1, uint4* csum, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(lmax_kernel, dim3((n + 63) / 64), dim3(64), 0, s, inst_key, order0, m, n, lm,
-                     lm1);
+                     lm1, csum);
   return hipGetLastError();
 }
 

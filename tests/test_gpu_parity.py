@@ -330,6 +330,7 @@ def _shared_hit_window(base=301, crowded_non_holders=False, **kw):
     S = rng.integers(0, 500_000, n_inst)
     if crowded_non_holders:
         S[86:] = 4_194_304 - 64
+    S = kw.pop("S", S)
     return _edge(sets, None, pool=pool, reqs=reqs, S=S, cap=64, **kw)
 
 
@@ -350,6 +351,37 @@ def test_popular_shared_hit_class(ps, scorer):
         _check_edge(ps, scorer, w, f"shared hit {base} b_max=40", b_max=40)
     w = _shared_hit_window(base=303, crowded_non_holders=True)
     _check_edge(ps, scorer, w, "shared hit crowded")
+
+
+def test_shared_hit_class_scan_bounds(ps, scorer):
+    """The class scan skips 64-instance chunks by their least decode-
+    iteration time at L = 0 (instances with and without running requests
+    apart) and their largest room: idle instances among busy ones, a
+    prefill interference that rules out every busy instance, negative
+    decode-iteration times (beta0, beta1 < 0, still a monotone model) and a
+    first chunk whose rooms cannot hold any request."""
+    n = 96
+    rng = np.random.default_rng(7)
+    D = rng.integers(0, 64, n)
+    Q = rng.integers(0, 4, n)
+    D[::5] = 0
+    Q[::5] = 0                      # A1 = 1: no prefill interference
+    w = _shared_hit_window(base=311, D=D, Q=Q)
+    w.alpha = np.asarray(w.alpha, np.float32).copy()
+    w.alpha[1] *= 100.0             # interference of several ms per busy instance
+    _check_edge(ps, scorer, w, "class bounds: interference")
+    _check_edge(ps, scorer, w, "class bounds: tight tpot", tpot_slo=0.02)
+    _check_edge(ps, scorer, w, "class bounds: loose tpot", tpot_slo=0.2)
+    wn = _shared_hit_window(base=312, D=D, Q=Q)
+    wn.beta = np.asarray(wn.beta, np.float32).copy()
+    wn.beta[..., 0] = -0.02         # t_iter below zero on lightly loaded instances
+    wn.beta[..., 1] = -1e-5
+    _check_edge(ps, scorer, wn, "class bounds: negative t_iter")
+    _check_edge(ps, scorer, wn, "class bounds: negative t_iter, tpot 1e-3", tpot_slo=1e-3)
+    S = np.random.default_rng(8).integers(0, 500_000, n)
+    S[:64] = 4_194_304 - 16         # no room in the first chunk
+    wc = _shared_hit_window(base=313, D=D, Q=Q, S=S)
+    _check_edge(ps, scorer, wc, "class bounds: full first chunk")
 
 
 def test_prefix_groups_window_sizes(ps, scorer):
