@@ -238,10 +238,11 @@ def score_bytes(win, r0, hits, grp=None):
     Requests of a popular group with a shared-hit class below their
     segment end take the general kernel's class path: descriptor, slot,
     144 B record, result, the 64 largest rooms (1 KB), the holder bitmap,
-    32 B per exception's state and its resume walk, one chunk of 64 key-
-    ordered states with their ids, one chunk of thresholds with the chunk
-    maxima, and the chosen state (a lower bound: later chunks are not
-    counted).
+    32 B per exception's state and its resume walk, the 16-byte summaries
+    of the key-ordered chunks, one chunk of 64 key-ordered states with
+    their ids, one chunk of thresholds with the chunk maxima, and the
+    chosen state (a lower bound: later chunks and the fallback scan are
+    not counted).
 
     Other requests go through the general kernel: descriptor, slot, result;
     the 64-way search of the sorted rooms; with a popular group row the
@@ -323,7 +324,7 @@ def score_bytes(win, r0, hits, grp=None):
         exc = grp["exc"]
         ex_res = np.where(resume & exc, rb, 0).sum(1)
         cby = (24 + 4 + 8 * 18 + 20 + 64 * 16 + 8 * nw + 32 * exc.sum(1) + ex_res +
-               64 * (4 + 32) + 4 * n1 + 64 * 16 + 32)
+               16 * n1 + 64 * (4 + 32) + 4 * n1 + 64 * 16 + 32)
         by = np.where(clsp, cby, by)
     # the recomputation filter and the hit-0 class
     n = (L[:, None] - h * bs).astype(np.float64)
