@@ -34,8 +34,12 @@ SEL_DCQ, SEL_D, SEL_DQ, SEL_DC, SEL_DQC, SEL_HCQ, SEL_RANDOM, SEL_LMETRIC = rang
 def selector_flags(sel: int) -> int:
     return (int(sel) & 0xF) << 8
 R_REJECT, R_FALLBACK, R_TTFT_MISS = 1, 2, 4
-NB_RHO, NB_TPOT, NB_TTFT, NB_Z, NB_MISSFLAG, NB_HEADROOM = 1, 2, 4, 8, 16, 32
+# Near-boundary bits (see oracle.cpp): the decision, the TTFT_MISS flag, or
+# only |C| / |T| may be decided by rounding.
+NB_RHO, NB_TPOT, NB_TTFT, NB_Z, NB_MISSFLAG, NB_HEADROOM, NB_SIZES = 1, 2, 4, 8, 16, 32, 64
 NB_DECISION = NB_RHO | NB_TPOT | NB_TTFT | NB_Z | NB_HEADROOM
+NB_SET_C = NB_RHO | NB_Z            # |C| (and so |T|) may be decided by rounding
+NB_UNSURE_SHIFT = 16                # nb >> 16: candidates whose T membership is unsure
 
 
 def build(verbose: bool = False) -> str:
@@ -119,7 +123,7 @@ def _load():
     lib.orc_commit.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, ctypes.POINTER(i64)]
     lib.orc_commit.restype = ctypes.c_int
     lib.orc_schedule.argtypes = [vp, ctypes.POINTER(Model), vp, vp, vp, vp, vp, i32,
-                                 vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i64)]
+                                 vp, vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i64)]
     lib.orc_schedule.restype = ctypes.c_int
     lib.orc_replay.argtypes = [vp, ctypes.POINTER(Model), vp, vp, vp, vp, vp, vp, i32,
                                vp, vp, vp, ctypes.POINTER(i64)]
@@ -212,20 +216,29 @@ class Oracle:
                           int(nthreads))
         return d
 
-    def schedule(self, model: Model, pool, pre_off, pre_len, tail_off, tail_len):
+    def schedule(self, model: Model, pool, pre_off, pre_len, tail_off, tail_len, follow=None):
         """Algorithm 1 per arrival (the snapshot moves to the final state).
-        Returns (Decisions, dropped)."""
+        ``follow``: another implementation's placements, committed instead of
+        the oracle's own where its decision is near a boundary and they differ
+        (they must be capacity-eligible).  Returns (Decisions, dropped)."""
         keep, ptrs = self._reqs(pool, pre_off, pre_len, tail_off, tail_len)
         n = len(keep[1][0])
+        fp = None
+        if follow is not None:
+            fa, fp = _c(follow, np.int32)
+            assert len(fa) == n
+            keep.append((fa, fp))
         d = Decisions(inst=np.zeros(n, np.int32), hit=np.zeros(n, np.int32),
                       ttft=np.zeros(n, np.float64), tpot=np.zeros(n, np.float64),
                       flags=np.zeros(n, np.uint32), sizes=np.zeros((n, 3), np.uint32),
                       nb=np.zeros(n, np.uint32))
         dropped = ctypes.c_int64()
-        _load().orc_schedule(self._h, ctypes.byref(model), *ptrs, n, d.inst.ctypes.data,
-                             d.hit.ctypes.data, d.ttft.ctypes.data, d.tpot.ctypes.data,
-                             d.flags.ctypes.data, d.sizes.ctypes.data, d.nb.ctypes.data,
-                             ctypes.byref(dropped))
+        rc = _load().orc_schedule(self._h, ctypes.byref(model), *ptrs, n, d.inst.ctypes.data,
+                                  d.hit.ctypes.data, d.ttft.ctypes.data, d.tpot.ctypes.data,
+                                  d.flags.ctypes.data, d.sizes.ctypes.data, d.nb.ctypes.data,
+                                  fp, ctypes.byref(dropped))
+        if rc != 0:
+            raise ValueError("a followed placement is not capacity-eligible")
         return d, int(dropped.value)
 
     def replay(self, model: Model, pool, pre_off, pre_len, tail_off, tail_len, inst):
@@ -288,9 +301,9 @@ class Oracle:
         return self.score(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,
                           win.tail_off, win.tail_len, nthreads)
 
-    def window_schedule(self, win, **policy):
+    def window_schedule(self, win, follow=None, **policy):
         return self.schedule(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,
-                             win.tail_off, win.tail_len)
+                             win.tail_off, win.tail_len, follow=follow)
 
     def window_replay(self, win, inst, **policy):
         return self.replay(model_of(win, **policy), win.pool, win.pre_off, win.pre_len,

@@ -84,8 +84,13 @@ constexpr uint32_t F_TTFT_ADMIT = 1u, F_NO_KVC = 2u, F_NO_TPOT = 4u, F_FALLBACK_
 // Selection orders within T (Table 4 of the paper, plus LMetric alone).
 enum Selector : uint32_t { SEL_DCQ = 0, SEL_D, SEL_DQ, SEL_DC, SEL_DQC, SEL_HCQ, SEL_RANDOM, SEL_LMETRIC };
 constexpr uint32_t R_REJECT = 1u, R_FALLBACK = 2u, R_TTFT_MISS = 4u;
+// Near-boundary bits.  NB_RHO, NB_TPOT, NB_TTFT, NB_Z and NB_HEADROOM mark a
+// decision (instance, hit, flags) that rounding may change; NB_MISSFLAG marks
+// a TTFT_MISS flag that rounding may change; NB_SIZES marks a |T| that
+// rounding may change while the decision cannot.  Bits 16..31 count the
+// candidates behind NB_SIZES.
 constexpr uint32_t NB_RHO = 1u, NB_TPOT = 2u, NB_TTFT = 4u, NB_Z = 8u, NB_MISSFLAG = 16u,
-                   NB_HEADROOM = 32u;
+                   NB_HEADROOM = 32u, NB_SIZES = 64u;
 constexpr double NB_REL = 1e-5;
 
 struct Snapshot {
@@ -154,6 +159,7 @@ struct Cand {
   double rho;
   double tpot, ttft;
   bool inC, inT;
+  bool unsure;  // member of C whose T membership rounding may change
 };
 
 struct Decision {
@@ -232,18 +238,35 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
 
   // SLO-aware admission (Eq. 10) and the TTFT estimate (Eq. 4).
   const double slo = std::max(m.ttft_floor, tpf_cold);
+  // A candidate with nothing cached and nothing queued has TTFT = T_pf(L, 0),
+  // the very quantity the budget is (when it exceeds the floor): the two are
+  // equal in any precision, so that comparison is never near a boundary.
+  auto ttft_is_budget = [&](const Cand& c) {
+    return c.c == 0 && sn.Q[c.i] == 0 && sn.P[c.i] == 0 && tpf_cold >= m.ttft_floor;
+  };
   for (Cand& c : A) {
     candidate_latency(sn, m, c.i, c.n, c.c, L, c.tpot, c.ttft);
     const bool tpot_ok = (m.flags & F_NO_TPOT) || c.tpot < m.tau;
     const bool ttft_ok = !(m.flags & F_TTFT_ADMIT) || c.ttft <= slo;
     c.inT = c.inC && tpot_ok && ttft_ok;
-    if (!(m.flags & F_NO_TPOT) && std::fabs(c.tpot - m.tau) <= NB_REL * m.tau) d.nb |= NB_TPOT;
-    if ((m.flags & F_TTFT_ADMIT) && std::fabs(c.ttft - slo) <= NB_REL * slo) d.nb |= NB_TTFT;
+    // T membership is decided by rounding when a test it needs lies within
+    // the relative window of its bound and the other test passes or is
+    // itself that close.
+    const bool tpot_near = !(m.flags & F_NO_TPOT) && std::fabs(c.tpot - m.tau) <= NB_REL * m.tau;
+    const bool ttft_near = (m.flags & F_TTFT_ADMIT) && !ttft_is_budget(c) &&
+                           std::fabs(c.ttft - slo) <= NB_REL * slo;
+    c.unsure = c.inC && ((tpot_near && (ttft_ok || ttft_near)) || (ttft_near && (tpot_ok || tpot_near)));
+    if (c.unsure) d.nb |= NB_SIZES;
   }
+  uint32_t n_unsure = 0;
   for (const Cand& c : A) {
     d.nC += c.inC;
     d.nT += c.inT;
+    n_unsure += c.unsure;
   }
+  // bits 16..31: how many candidates' T membership rounding may change
+  // (|T| can differ by at most that many), saturated
+  d.nb |= std::min<uint32_t>(n_unsure, 0xFFFFu) << 16;
 
   // Packing within T by the selector; D-C-Q by default (most decoding
   // requests, then most cached blocks, then fewest queued, then lowest id).
@@ -318,6 +341,17 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
         if (c.inT && &c != best && std::fabs((m.tau - c.tpot) - hb) <= NB_REL * m.tau) d.nb |= NB_HEADROOM;
     }
   }
+  // A candidate whose T membership rounding may change can change the
+  // decision only if it is the choice, or if it is outside T and would come
+  // first (or T is empty).  With a total order on T, flipping any set of
+  // other unsure candidates leaves the choice where it is.  The random and
+  // H-C-Q selectors depend on all of T.
+  for (const Cand& c : A) {
+    if (!c.unsure) continue;
+    const bool decides = sel == SEL_RANDOM || sel == SEL_HCQ || &c == best ||
+                         (!c.inT && (!best || before(sel, c, *best)));
+    if (decides) d.nb |= (std::fabs(c.tpot - m.tau) <= NB_REL * m.tau) ? NB_TPOT : NB_TTFT;
+  }
   d.flags = 0;
   if (!best) {
     if (m.flags & F_FALLBACK_DCQ) {
@@ -345,7 +379,7 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
   d.ttft = best->ttft;
   d.tpot = best->tpot;
   if (best->ttft > slo) d.flags |= R_TTFT_MISS;
-  if (std::fabs(best->ttft - slo) <= NB_REL * slo) d.nb |= NB_MISSFLAG;
+  if (!ttft_is_budget(*best) && std::fabs(best->ttft - slo) <= NB_REL * slo) d.nb |= NB_MISSFLAG;
   return d;
 }
 
@@ -509,16 +543,31 @@ int orc_commit(void* h, const uint64_t* pool, const int64_t* pre_off, const int3
 // committed (as orc_commit) before the next one is scored.  Outputs as
 // orc_score, plus the blocks refused at the cap in *dropped.  The snapshot
 // is left in the final state.
+//
+// follow (optional): placements made by another implementation of the same
+// schedule.  Where the oracle's own decision is near a boundary (rounding may
+// decide it) and follow[r] differs, follow[r] is committed instead, so that
+// both continue from the same state; it must be a capacity-eligible instance
+// (else -1 is returned).  The outputs still hold the oracle's own decision.
 int orc_schedule(void* h, const orc_model* m, const uint64_t* pool, const int64_t* pre_off,
                  const int32_t* pre_len, const int64_t* tail_off, const int32_t* tail_len,
                  int32_t n_req, int32_t* inst, int32_t* hit, double* ttft, double* tpot,
-                 uint32_t* flags, uint32_t* sizes, uint32_t* nb, int64_t* dropped) {
+                 uint32_t* flags, uint32_t* sizes, uint32_t* nb, const int32_t* follow,
+                 int64_t* dropped) {
   Snapshot& sn = *static_cast<Snapshot*>(h);
   int64_t drop = 0;
   std::vector<Cand> A;
+  constexpr uint32_t NB_CHOICE = NB_RHO | NB_TPOT | NB_TTFT | NB_Z | NB_HEADROOM;
   for (int32_t r = 0; r < n_req; ++r) {
     Chain ch = chain_of(pool, pre_off, pre_len, tail_off, tail_len, r);
     const Decision d = score_one(sn, *m, ch, A, r);
+    int32_t place = d.inst;
+    if (follow && (d.nb & NB_CHOICE) && follow[r] != d.inst) {
+      bool eligible = false;
+      for (const Cand& c : A) eligible |= c.i == follow[r];
+      if (!eligible) return -1;
+      place = follow[r];
+    }
     inst[r] = d.inst;
     hit[r] = d.hit;
     ttft[r] = d.ttft;
@@ -530,7 +579,7 @@ int orc_schedule(void* h, const orc_model* m, const uint64_t* pool, const int64_
       sizes[3 * (size_t)r + 2] = d.nT;
     }
     if (nb) nb[r] = d.nb;
-    if (d.inst >= 0) (void)commit_one(sn, ch, d.inst, m->block_tokens, drop);
+    if (place >= 0) (void)commit_one(sn, ch, place, m->block_tokens, drop);
   }
   *dropped = drop;
   return 0;

@@ -116,54 +116,71 @@ class DeviceWindow:
         return d_hits.cpu().numpy().view(np.uint32).reshape(-1, n_inst)[:self.n_req]
 
 
-def compare_decisions(res, sizes, od, idx=None, tol=NB_TOL, label=""):
+def nb_cap(n_req):
+    """Most near-boundary decisions a window of n_req requests may exclude
+    from the exact check: 0.1% of its requests, at least 8.  (The oracle's
+    synthetic windows have 0.00-0.06%.)"""
+    return max(8, n_req // 1000)
+
+
+def compare_decisions(res, sizes, od, idx=None, tol=NB_TOL, label="", max_nb=None):
     """GPU results vs oracle decisions (optionally the oracle holds only the
-    requests `idx` of the GPU window).  Returns the near-boundary count.
-    Bit-exact on chosen instance, hit, flags and set sizes except where the
-    oracle flags a near-boundary comparison; latencies within `tol`."""
+    requests `idx` of the GPU window).  Returns the near-boundary count,
+    which must not exceed `max_nb` (default nb_cap(n)).
+
+    * chosen instance, hit and flags: bit-exact except on requests whose
+      decision the oracle marks near a boundary (NB_DECISION); the TTFT_MISS
+      flag is skipped where the oracle marks that flag near its boundary;
+    * |A|: exact on every request (integer capacity tests);
+    * |C|: exact except where a recomputation-filter comparison is near its
+      boundary (NB_SET_C);
+    * |T|: within the number of candidates whose T membership the oracle
+      marks as decided by rounding (nb >> 16), exact where that is 0;
+    * TTFT / TPOT of the choice within `tol` relative (non-NB requests)."""
     if idx is not None:
-        res, sizes = res[idx], sizes[idx]
+        res = res[idx]
+        sizes = sizes[idx] if sizes is not None else None
+    n = len(od.inst)
     nb_dec = (od.nb & oracle.NB_DECISION) != 0
     nb_flag = (od.nb & oracle.NB_MISSFLAG) != 0
+    n_dec = int(nb_dec.sum())
+    cap = nb_cap(n) if max_nb is None else max_nb
+    assert n_dec <= cap, f"{label}: {n_dec} near-boundary decisions excluded, more than {cap}"
     ok = ~nb_dec
     bad = np.nonzero(ok & ((res["instance"] != od.inst) | (res["hit_blocks"] != od.hit)))[0]
     assert len(bad) == 0, (
         f"{label}: {len(bad)} decisions differ, first r={bad[0]}: gpu "
         f"{res[bad[0]]} oracle inst={od.inst[bad[0]]} hit={od.hit[bad[0]]} "
-        f"flags={od.flags[bad[0]]} sizes={od.sizes[bad[0]]} gpu sizes={sizes[bad[0]]}")
+        f"flags={od.flags[bad[0]]} sizes={od.sizes[bad[0]]} nb={od.nb[bad[0]]:#x}"
+        + (f" gpu sizes={sizes[bad[0]]}" if sizes is not None else ""))
     fl_mask = np.where(nb_flag, ~np.uint32(oracle.R_TTFT_MISS), np.uint32(0xFFFFFFFF))
     fbad = np.nonzero(ok & ((res["flags"] & fl_mask) != (od.flags & fl_mask)))[0]
     assert len(fbad) == 0, f"{label}: flags differ at r={fbad[:5]}"
-    sbad = np.nonzero(ok & (sizes != od.sizes).any(axis=1))[0]
-    assert len(sbad) == 0, f"{label}: set sizes differ at r={sbad[:5]}: {sizes[sbad[0]]} vs {od.sizes[sbad[0]]}"
+    if sizes is not None:
+        sizes = np.asarray(sizes, np.int64)
+        want = od.sizes.astype(np.int64)
+        abad = np.nonzero(sizes[:, 0] != want[:, 0])[0]
+        assert len(abad) == 0, f"{label}: |A| differs at r={abad[:5]}: {sizes[abad[0]]} vs {want[abad[0]]}"
+        c_ok = (od.nb & oracle.NB_SET_C) == 0
+        cbad = np.nonzero(c_ok & (sizes[:, 1] != want[:, 1]))[0]
+        assert len(cbad) == 0, f"{label}: |C| differs at r={cbad[:5]}: {sizes[cbad[0]]} vs {want[cbad[0]]}"
+        unsure = (od.nb >> oracle.NB_UNSURE_SHIFT).astype(np.int64)
+        tbad = np.nonzero(c_ok & (np.abs(sizes[:, 2] - want[:, 2]) > unsure))[0]
+        assert len(tbad) == 0, (f"{label}: |T| differs at r={tbad[:5]}: {sizes[tbad[0]]} vs "
+                                f"{want[tbad[0]]} ({unsure[tbad[0]]} unsure)")
     chosen = ok & (od.inst >= 0)
     for name, ref in (("ttft", od.ttft), ("tpot", od.tpot)):
         g = res[name][chosen].astype(np.float64)
         r = ref[chosen]
         rel = np.abs(g - r) / np.maximum(np.abs(r), 1e-30)
         assert (rel <= tol).all(), f"{label}: {name} rel err {rel.max():.3g} > {tol}"
-    return int(nb_dec.sum())
+    return n_dec
 
 
-def compare_sequential(res, sizes, od, tol=NB_TOL, label=""):
-    """Per-arrival results against the oracle's, in arrival order, up to the
-    first request whose decision differs; that request must carry a
-    near-boundary flag (from there on the two states differ and nothing
-    later is comparable).  Returns the number of requests compared."""
-    n = len(od.inst)
-    diff = (res["instance"] != od.inst) | (res["hit_blocks"] != od.hit)
-    bad = np.nonzero(diff)[0]
-    upto = n
-    if len(bad):
-        k = int(bad[0])
-        assert od.nb[k] & oracle.NB_DECISION, (
-            f"{label}: request {k} differs without a near-boundary flag: gpu {res[k]} "
-            f"oracle inst={od.inst[k]} hit={od.hit[k]} flags={od.flags[k]} sizes={od.sizes[k]}")
-        upto = k
-    head = oracle.Decisions(inst=od.inst[:upto], hit=od.hit[:upto], ttft=od.ttft[:upto],
-                            tpot=od.tpot[:upto], flags=od.flags[:upto], sizes=od.sizes[:upto],
-                            nb=od.nb[:upto])
-    if upto:
-        sz = sizes[:upto] if sizes is not None else od.sizes[:upto]
-        compare_decisions(res[:upto], sz, head, tol=tol, label=label)
-    return upto
+def compare_sequential(res, sizes, od, tol=NB_TOL, label="", max_nb=None):
+    """Per-arrival results against the oracle's schedule run with
+    follow=res["instance"] (so the oracle committed the GPU's placement
+    wherever its own decision was near a boundary and they differ, and both
+    went on from the same state).  Every request is compared as by
+    compare_decisions; returns the number of near-boundary requests."""
+    return compare_decisions(res, sizes, od, tol=tol, label=label, max_nb=max_nb)

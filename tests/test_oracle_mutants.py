@@ -60,12 +60,34 @@ MUTANTS = [
     ("upper median", "m->lout = (double)recent[(cnt - 1) / 2];", "m->lout = (double)recent[cnt / 2];"),
     ("first token keeps pending", "P[i] -= tokens[k];", "P[i] -= 0;"),
     ("commit ignores cap", "if ((int64_t)set.size() < sn.cap) set.insert(key);", "if (true) set.insert(key);"),
-    ("schedule without commit", "if (d.inst >= 0) (void)commit_one(sn, ch, d.inst, m->block_tokens, drop);", "(void)0;"),
+    ("schedule without commit", "if (place >= 0) (void)commit_one(sn, ch, place, m->block_tokens, drop);", "(void)0;"),
     ("commit keeps the queue", "sn.Q[i] += 1;", "sn.Q[i] += 0;"),
     ("replay measures after commit",
      "    candidate_latency(sn, *m, i, L - c, c, L, tpot[k], ttft[k]);\n    hit[k] = (int32_t)hb;\n    (void)commit_one(sn, ch, i, m->block_tokens, drop);",
      "    (void)commit_one(sn, ch, i, m->block_tokens, drop);\n    candidate_latency(sn, *m, i, L - c, c, L, tpot[k], ttft[k]);\n    hit[k] = (int32_t)hb;"),
     ("replay hit after commit", "const int64_t hb = prefix_hit(sn.sets[(size_t)i], ch);", "const int64_t hb = ch.len();"),
+    # the near-boundary rule (what the GPU parity check may skip)
+    ("NB_TPOT window widened", "std::fabs(c.tpot - m.tau) <= NB_REL * m.tau;", "std::fabs(c.tpot - m.tau) <= 10 * NB_REL * m.tau;"),
+    ("NB_TPOT never raised", "std::fabs(c.tpot - m.tau) <= NB_REL * m.tau;", "std::fabs(c.tpot - m.tau) < 0.0;"),
+    ("NB_TPOT always raised", "const bool tpot_near = !(m.flags & F_NO_TPOT) &&", "const bool tpot_near = true ||"),
+    ("NB_TPOT over all of A", "c.unsure = c.inC && (", "c.unsure = ("),
+    ("every unsure candidate decides", "const bool decides = sel == SEL_RANDOM", "const bool decides = true || sel == SEL_RANDOM"),
+    ("only the choice decides", "&c == best ||\n                         (!c.inT && (!best || before(sel, c, *best)));", "&c == best;"),
+    ("unsure count not reported", "d.nb |= std::min<uint32_t>(n_unsure, 0xFFFFu) << 16;", "(void)n_unsure;"),
+    ("NB_TTFT window widened", "std::fabs(c.ttft - slo) <= NB_REL * slo;", "std::fabs(c.ttft - slo) <= 10 * NB_REL * slo;"),
+    ("NB_TTFT never raised", "std::fabs(c.ttft - slo) <= NB_REL * slo;", "std::fabs(c.ttft - slo) < 0.0;"),
+    ("NB_TTFT on TTFT equal to the budget", "(m.flags & F_TTFT_ADMIT) && !ttft_is_budget(c) &&", "(m.flags & F_TTFT_ADMIT) &&"),
+    ("NB_MISSFLAG window widened", "std::fabs(best->ttft - slo) <= NB_REL * slo) d.nb |= NB_MISSFLAG;", "std::fabs(best->ttft - slo) <= 10 * NB_REL * slo) d.nb |= NB_MISSFLAG;"),
+    ("NB_MISSFLAG never raised", "std::fabs(best->ttft - slo) <= NB_REL * slo) d.nb |= NB_MISSFLAG;", "std::fabs(best->ttft - slo) < 0.0) d.nb |= NB_MISSFLAG;"),
+    ("NB_MISSFLAG on TTFT equal to the budget", "if (!ttft_is_budget(*best) && std::fabs", "if (std::fabs"),
+    ("NB_RHO window widened", "std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0)", "std::fabs(c.rho - m.eta) <= 10 * NB_REL * std::max(m.eta, 1.0)"),
+    ("NB_RHO never raised", "std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0)", "std::fabs(c.rho - m.eta) < 0.0"),
+    ("NB_Z window widened", "std::fabs(Z) <= NB_REL * std::fabs(tpf_cold)", "std::fabs(Z) <= 10 * NB_REL * std::fabs(tpf_cold)"),
+    ("NB_Z never raised", "std::fabs(Z) <= NB_REL * std::fabs(tpf_cold)", "std::fabs(Z) < 0.0"),
+    # following another implementation's near-boundary placements
+    ("follow ignored", "      place = follow[r];", "      place = d.inst;"),
+    ("follow at every request", "if (follow && (d.nb & NB_CHOICE) && follow[r] != d.inst)", "if (follow && follow[r] != d.inst)"),
+    ("follow unchecked", "if (!eligible) return -1;", "(void)eligible;"),
 ]
 
 

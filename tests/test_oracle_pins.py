@@ -601,6 +601,157 @@ def test_headroom_near_tie_is_flagged():
     assert d.inst[0] == 1 and d.nb[0] & oracle.NB_HEADROOM
 
 
+# -- near-boundary rule: which comparisons rounding may decide ---------------
+# The parity tests exclude a decision from the exact check only where the
+# oracle marks it; these pins fix each mark's window (1e-5 relative: inside
+# at 0.5e-5, outside at 2e-5) and where it applies.
+
+NB_ALL_DEC = oracle.NB_DECISION
+
+
+def _nb_tpot_window(S, tau, D=None, hits=None, eta=0.5):
+    """Instances with nothing queued and A = 0 unless D is given, a 128-token
+    request, decode time t_iter = 0.5 + 1e-6 (S + 128) (no interference on an
+    idle instance), so TPOT is set by S; alpha of the simple model."""
+    n = len(S)
+    ch = chain_hashes(8)
+    hits = hits if hits is not None else [0] * n
+    return make_window([ch[:h] for h in hits], [ch], D if D is not None else [0] * n, [0] * n,
+                       [0] * n, S, SIMPLE_ALPHA, (10_000,), ((0.5, 0.0, 1e-6),), (1.0,), cap=8,
+                       tpot_slo=tau, eta=eta, b_max=10_000, kv_cap_tokens=10**9, lout=556.0)
+
+
+def test_nb_tpot_window():
+    """One idle instance, TPOT = 0.500128: tau 0.5e-5 above or below it marks
+    the decision (the choice itself, or an empty T whose fallback it would
+    replace), 2e-5 away marks nothing."""
+    tp = 0.5 + 1e-6 * 128
+    for rel, marked in ((0.5e-5, True), (-0.5e-5, True), (2e-5, False), (-2e-5, False)):
+        d = _decide(_nb_tpot_window([0], tp * (1 + rel)))
+        assert bool(d.nb[0] & oracle.NB_TPOT) == marked, rel
+        assert bool(d.nb[0] & oracle.NB_SIZES) == marked, rel
+        assert d.nb[0] >> oracle.NB_UNSURE_SHIFT == (1 if marked else 0), rel
+        assert d.nb[0] & (NB_ALL_DEC & ~oracle.NB_TPOT) == 0, rel
+        assert bool(d.flags[0] & oracle.R_FALLBACK) == (rel < 0), rel
+
+
+def test_nb_tpot_only_where_it_can_change_the_decision():
+    """tau = 1.  Instance 0 (TPOT 0.500128) is the choice; a second instance
+    with TPOT within 1e-5 of tau (S = 499,872: TPOT = 1.0) that comes after it
+    in key order moves only |T| (NB_SIZES, one unsure candidate); placed
+    first in key order it could be the choice (NB_TPOT); outside C (eta = 0,
+    hit 0 against a full hit) it is not counted at all."""
+    d = _decide(_nb_tpot_window([0, 499_872], 1.0))
+    assert d.inst[0] == 0 and d.nb[0] & NB_ALL_DEC == 0
+    assert d.nb[0] & oracle.NB_SIZES and d.nb[0] >> oracle.NB_UNSURE_SHIFT == 1
+    d = _decide(_nb_tpot_window([0, 499_872 - 2], 1.0))     # inside T, not the choice
+    assert d.inst[0] == 0 and d.nb[0] & NB_ALL_DEC == 0 and d.nb[0] & oracle.NB_SIZES
+    d = _decide(_nb_tpot_window([499_872, 0], 1.0))         # first in key order
+    assert d.inst[0] == 1 and d.nb[0] & oracle.NB_TPOT
+    d = _decide(_nb_tpot_window([0, 499_872], 1.0, hits=[8, 0], eta=0.0))   # not in C
+    assert d.inst[0] == 0 and list(d.sizes[0]) == [2, 1, 1] and d.nb[0] == 0
+
+
+def _nb_ttft_window(floor, Q=1, flags=0):
+    """One instance, alpha = (0.5, 1e-3, 0, ...), a 128-token request with
+    nothing cached: T_pf(128, 0) = 0.628, Z = 0.128, TTFT = 0.628 + 0.5 Q.
+    The budget is the floor (above 0.628) unless the floor is lower."""
+    ch = chain_hashes(8)
+    return make_window([[]], [ch], [0], [Q], [0], [0], [0.5, 1e-3, 0, 0, 0, 0], (10_000,),
+                       ((0.01, 0.0, 0.0),), (1.0,), cap=8, tpot_slo=10.0, ttft_floor=floor,
+                       b_max=100, kv_cap_tokens=10**9, flags=flags)
+
+
+def test_nb_ttft_admission_window():
+    """TTFT admission on, TTFT = 1.128: a budget within 0.5e-5 of it marks
+    the decision (NB_TTFT), 2e-5 away marks nothing."""
+    tt = 0.628 + 0.5
+    for rel, marked in ((0.5e-5, True), (-0.5e-5, True), (2e-5, False), (-2e-5, False)):
+        d = _decide(_nb_ttft_window(tt * (1 + rel), flags=oracle.F_TTFT_ADMIT))
+        assert bool(d.nb[0] & oracle.NB_TTFT) == marked, rel
+        assert d.nb[0] & (NB_ALL_DEC & ~oracle.NB_TTFT) == 0, rel
+        assert bool(d.flags[0] & oracle.R_FALLBACK) == (rel < 0), rel
+        # without admission TTFT decides nothing
+        d = _decide(_nb_ttft_window(tt * (1 + rel)))
+        assert d.nb[0] & NB_ALL_DEC == 0 and not d.flags[0] & oracle.R_FALLBACK, rel
+
+
+def test_nb_ttft_miss_flag_window():
+    """The chosen instance's TTFT_MISS flag (TTFT above the budget): within
+    0.5e-5 of the budget it is marked (NB_MISSFLAG), 2e-5 away it is not,
+    and in neither case is the decision marked."""
+    tt = 0.628 + 0.5
+    for rel, marked in ((0.5e-5, True), (-0.5e-5, True), (2e-5, False), (-2e-5, False)):
+        d = _decide(_nb_ttft_window(tt * (1 + rel)))
+        assert bool(d.nb[0] & oracle.NB_MISSFLAG) == marked, rel
+        assert d.nb[0] & NB_ALL_DEC == 0, rel
+        assert bool(d.flags[0] & oracle.R_TTFT_MISS) == (rel < 0), rel
+
+
+def test_nb_ttft_equal_to_budget_by_construction():
+    """Nothing cached, nothing queued and the budget T_pf(L, 0) above the
+    floor: TTFT is the budget itself, so the comparison is exact in any
+    precision and marks nothing (no TTFT_MISS, admitted under admission)."""
+    for flags in (0, oracle.F_TTFT_ADMIT):
+        d = _decide(_nb_ttft_window(0.1, Q=0, flags=flags))
+        assert d.ttft[0] == pytest.approx(0.628, rel=1e-12)
+        assert d.nb[0] == 0 and d.flags[0] == 0, flags
+
+
+def test_nb_rho_window():
+    """T_pf = N makes rho = 1/2 exactly for hits 8 and 4 of 8 blocks: eta
+    within 0.5e-5 of it marks the decision, 3e-5 away does not."""
+    alpha = [0, 1.0, 0, 0, 0, 0]
+    for off, marked in ((0.5e-5, True), (-0.5e-5, True), (3e-5, False), (-3e-5, False)):
+        d = _decide(_multi([8, 4], alpha=alpha, eta=0.5 + off, D=[0, 5]))
+        assert bool(d.nb[0] & oracle.NB_RHO) == marked, off
+        assert d.inst[0] == (1 if off > 0 else 0), off
+
+
+def test_nb_zero_benefit_window():
+    """Z = a1 L with T_pf(L, 0) = 0.02 + a1 L: Z within 1e-5 of T_pf(L, 0)
+    marks the decision, 3e-5 does not."""
+    for z_rel, marked in ((0.5e-5, True), (3e-5, False)):
+        a1 = 0.02 * z_rel / (1 - z_rel) / 128
+        d = _decide(_multi([0, 3, 5, 8], alpha=[0.02, a1, 0, 0, 0, 0], eta=0.0))
+        assert bool(d.nb[0] & oracle.NB_Z) == marked, z_rel
+
+
+def _follow_window():
+    """Two idle instances and one at its batch limit, no cache, two requests
+    with the same 8-block chain; tau within 1e-5 above instance 0's TPOT, so
+    the first decision (instance 0) is near its boundary; instance 1 is
+    far above tau."""
+    ch = chain_hashes(8)
+    tp0 = 0.5 + 1e-6 * 128
+    return make_window([[], [], []], [ch, ch], [0, 0, 10], [0, 0, 0], [0, 0, 0], [0, 50_000, 0],
+                       SIMPLE_ALPHA, (10_000,), ((0.5, 0.0, 1e-6),), (1.0,), cap=64,
+                       tpot_slo=tp0 * (1 + 0.5e-5), eta=0.0, b_max=10, kv_cap_tokens=10**9)
+
+
+def test_schedule_follows_only_near_boundary_decisions():
+    """Per arrival with another implementation's placements: at the first
+    request (near the TPOT boundary) the oracle commits the followed
+    instance 1, so the second request finds its blocks there (hit 8, the
+    only member of C at eta = 0, TPOT above tau: fallback); at the second
+    request (not near a boundary) a different followed placement is
+    ignored.  Without placements to follow both go to instance 0; a
+    followed instance outside A is refused."""
+    w = _follow_window()
+    o = oracle.Oracle.from_window(w)
+    d, _ = o.window_schedule(w)
+    assert list(d.inst) == [0, 0] and list(d.hit) == [0, 8]
+    assert d.nb[0] & oracle.NB_TPOT and d.nb[1] & NB_ALL_DEC == 0
+    o = oracle.Oracle.from_window(w)
+    d, _ = o.window_schedule(w, follow=[1, 0])
+    assert list(d.inst) == [0, 1] and list(d.hit) == [0, 8]
+    assert d.flags[1] & oracle.R_FALLBACK and d.nb[1] & NB_ALL_DEC == 0
+    assert list(o.state()["Q"]) == [0, 2, 0]
+    o = oracle.Oracle.from_window(w)
+    with pytest.raises(ValueError):
+        o.window_schedule(w, follow=[2, 0])
+
+
 # -- feedback path: EMA calibration (Sec. 5.3), median output, transitions ----
 
 def _fb_model(gamma=(1.0, 1.0)):
