@@ -220,6 +220,11 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
   }
   const double Z = tpf_cold - tpf_cached;
   const bool kvc_on = !(m.flags & F_NO_KVC);
+  // A fully cached candidate has W = 0 exactly, so W_min = 0 exactly; a
+  // candidate with nothing cached has W = Z (the same expression), so its
+  // rho is then exactly 1 under any rounding.
+  bool some_full = false;
+  for (const Cand& c : A) some_full |= c.n == 0;
   if (kvc_on && std::fabs(Z) <= NB_REL * std::fabs(tpf_cold)) d.nb |= NB_Z;
   for (Cand& c : A) {
     if (!kvc_on || Z <= 0.0) {
@@ -229,10 +234,13 @@ Decision score_one(const Snapshot& sn, const orc_model& m, const Chain& ch, std:
       c.rho = (c.W - Wmin) / Z;
       c.inC = c.rho <= m.eta;
       // A candidate with the minimiser's own hit has rho = 0 exactly under
-      // any rounding; every other rho within the relative window of eta is
-      // decided by rounding.
+      // any rounding, and so has one with nothing cached rho = 1 when the
+      // minimiser is fully cached; every other rho within the relative
+      // window of eta is decided by rounding.
       const bool exact_zero = c.W == Wmin && c.hit == hit_at_min;
-      if (!exact_zero && std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0)) d.nb |= NB_RHO;
+      const bool exact_one = some_full && c.c == 0;
+      if (!exact_zero && !exact_one && std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0))
+        d.nb |= NB_RHO;
     }
   }
 

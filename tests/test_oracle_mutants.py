@@ -81,6 +81,8 @@ MUTANTS = [
     ("NB_MISSFLAG never raised", "std::fabs(best->ttft - slo) <= NB_REL * slo) d.nb |= NB_MISSFLAG;", "std::fabs(best->ttft - slo) < 0.0) d.nb |= NB_MISSFLAG;"),
     ("NB_MISSFLAG on TTFT equal to the budget", "if (!ttft_is_budget(*best) && std::fabs", "if (std::fabs"),
     ("NB_RHO window widened", "std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0)", "std::fabs(c.rho - m.eta) <= 10 * NB_REL * std::max(m.eta, 1.0)"),
+    ("NB_RHO on rho = 1 by construction", "const bool exact_one = some_full && c.c == 0;", "const bool exact_one = false;"),
+    ("rho = 1 exemption without a full hit", "const bool exact_one = some_full && c.c == 0;", "const bool exact_one = c.c == 0;"),
     ("NB_RHO never raised", "std::fabs(c.rho - m.eta) <= NB_REL * std::max(m.eta, 1.0)", "std::fabs(c.rho - m.eta) < 0.0"),
     ("NB_Z window widened", "std::fabs(Z) <= NB_REL * std::fabs(tpf_cold)", "std::fabs(Z) <= 10 * NB_REL * std::fabs(tpf_cold)"),
     ("NB_Z never raised", "std::fabs(Z) <= NB_REL * std::fabs(tpf_cold)", "std::fabs(Z) < 0.0"),

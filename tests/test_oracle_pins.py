@@ -708,6 +708,21 @@ def test_nb_rho_window():
         assert d.inst[0] == (1 if off > 0 else 0), off
 
 
+def test_nb_rho_one_by_construction():
+    """A fully cached candidate makes W_min = 0 exactly, and a candidate with
+    nothing cached has W = Z: its rho is exactly 1 in any precision, so eta
+    = 1 keeps it unmarked (and in C); eta = 1 + 0.5e-5 still marks nothing,
+    while a partly cached minimiser leaves the zero-hit rho = 1 - W_min / Z
+    to rounding only near eta."""
+    for eta in (1.0, 1.0 + 0.5e-5):
+        d = _decide(_multi([8, 0, 0], D=[0, 5, 0], eta=eta))
+        assert d.nb[0] == 0 and list(d.sizes[0][:2]) == [3, 3] and d.inst[0] == 1, eta
+    d = _decide(_multi([8, 0], alpha=[0, 1.0, 0, 0, 0, 0], eta=1.0 + 0.5e-5, D=[0, 5]))
+    assert d.nb[0] == 0 and d.inst[0] == 1
+    d = _decide(_multi([4, 0], alpha=[0, 1.0, 0, 0, 0, 0], eta=0.5 + 0.5e-5, D=[0, 5]))
+    assert d.nb[0] & oracle.NB_RHO
+
+
 def test_nb_zero_benefit_window():
     """Z = a1 L with T_pf(L, 0) = 0.02 + a1 L: Z within 1e-5 of T_pf(L, 0)
     marks the decision, 3e-5 does not."""
