@@ -207,8 +207,9 @@ ps_status ps_score_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_
 
 /*
  * Measurement: with on != 0, the next ps_score_window(_dev) calls (up to
- * 4,096 of them) record HIP events on their stream around their two parts:
- * the prefix-group pass (two launches) and the scoring kernel.
+ * 4,096 of them) record HIP events on their stream around their launches:
+ * the prefix-group pass (claim, walk) and the scoring pass (lean scorer,
+ * general scorer).
  * ps_read_timing waits for those calls and returns their number and the
  * mean duration of each part in milliseconds, then starts a new count.
  * PS_E_STATE if no call was recorded.  Switching it on or off resets the
@@ -216,6 +217,15 @@ ps_status ps_score_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_
  */
 ps_status ps_set_timing(ps_ctx* ctx, int32_t on);
 ps_status ps_read_timing(ps_ctx* ctx, int32_t* n_calls, float* ms_group, float* ms_score);
+
+/*
+ * Measurement, per kernel: like ps_read_timing (same recorded calls; it
+ * starts a new count too), but ms[0..3] receive the mean milliseconds of the
+ * four launches of a scoring call: the group claim pass, the group walk, the
+ * lean scorer and the general scorer (0 for a launch the call did not make).
+ * ms points to 4 host floats.
+ */
+ps_status ps_read_kernel_timing(ps_ctx* ctx, int32_t* n_calls, float* ms);
 
 /*
  * Diagnostic: the longest cached prefix (blocks) of every request on every

@@ -112,6 +112,7 @@ def load_library() -> ctypes.CDLL:
         "ps_feedback_output": ([vp, vp, i32], i32),
         "ps_read_model": ([vp, vp, vp, vp], i32),
         "ps_set_timing": ([vp, i32], i32),
+        "ps_read_kernel_timing": ([vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_float)], i32),
         "ps_read_timing": ([vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_float),
                             ctypes.POINTER(ctypes.c_float)], i32),
     }
@@ -360,6 +361,14 @@ class Scorer:
         _check(self.ctx, load_library().ps_read_timing(self.ctx, ctypes.byref(n), ctypes.byref(g),
                                                        ctypes.byref(k)))
         return int(n.value), float(g.value), float(k.value)
+
+    def read_kernel_timing(self) -> tuple:
+        """(calls, [mean ms of the claim pass, group walk, lean scorer,
+        general scorer]) over the scoring calls timed since the last read."""
+        n = ctypes.c_int32()
+        ms = (ctypes.c_float * 4)()
+        _check(self.ctx, load_library().ps_read_kernel_timing(self.ctx, ctypes.byref(n), ms))
+        return int(n.value), [float(x) for x in ms]
 
     def hits_dev(self, d_pool, pool_len, d_reqs, n_req, d_hits, stream=None):
         ps_probe_hits_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_hits, stream)

@@ -26,6 +26,9 @@ constexpr int kScratchRowsPerCU = 16;
 
 // Scoring calls whose launches are timed between two reads of the timing.
 constexpr int32_t kTimingCalls = 4096;
+// Events per timed call: around the claim pass, the group walk, the lean
+// scorer and the general scorer.
+constexpr int kTimingEvents = 5;
 
 }  // namespace
 
@@ -769,24 +772,29 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                    : ps_score_small(c->n_inst) ? std::min(batches, c->num_cus * 16)
                    : c->hits_in_lds            ? batches
                                                : std::min(batches, c->scratch_rows);
+  // Timed calls record kTimingEvents events: before the claim pass, between
+  // it and the group walk, after the walk, after the lean scorer, after the
+  // general scorer (a part that is not launched spans no time).
   hipEvent_t* ev = nullptr;
   if (c->timing && !probe_all && c->n_timed < kTimingCalls) {
-    if (c->ev.size() < 3 * (size_t)(c->n_timed + 1)) {
-      for (int k = 0; k < 3; ++k) {
+    if (c->ev.size() < kTimingEvents * (size_t)(c->n_timed + 1)) {
+      for (int k = 0; k < kTimingEvents; ++k) {
         hipEvent_t e = nullptr;
         HIP_TRY(c, hipEventCreate(&e));
         c->ev.push_back(e);
       }
     }
-    ev = &c->ev[3 * (size_t)c->n_timed];
+    ev = &c->ev[kTimingEvents * (size_t)c->n_timed];
   }
   if (ev) HIP_TRY(c, hipEventRecord(ev[0], s));
   // the walk pass over the leaders' lists: a wave per four requests (about
   // two waves per group at the usual group sizes), so the dispatcher
   // balances long walks (popular groups) against short ones
   if (a.grp.keys)
-    HIP_TRY(c, ps_launch_group(a, std::max(64, (n_req / 4 + 63) / 64 * 64), s));
-  if (ev) HIP_TRY(c, hipEventRecord(ev[1], s));
+    HIP_TRY(c, ps_launch_group(a, std::max(64, (n_req / 4 + 63) / 64 * 64), s, ev ? ev[1] : nullptr));
+  else if (ev)
+    HIP_TRY(c, hipEventRecord(ev[1], s));
+  if (ev) HIP_TRY(c, hipEventRecord(ev[2], s));
   // The lean scorer first when the groups give the requests their hits and
   // the selector is neither Random nor H-C-Q (persistent grid at its own
   // occupancy); the general scorer then finishes what it left.
@@ -809,13 +817,14 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
     HIP_TRY(c, ps_launch_lean(la, lgrid, s));
     a.defer_only = 1;
   }
+  if (ev) HIP_TRY(c, hipEventRecord(ev[3], s));
   // Finishing what the lean kernel left, the general kernel runs on at most
   // four waves per resident slot: enough waves to balance uneven work (the
   // popular groups), few enough that an empty pass costs little.
   HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, lean ? std::min(grid, c->num_cus * 64) : grid,
                              probe_all, s, rows));
   if (ev) {
-    HIP_TRY(c, hipEventRecord(ev[2], s));
+    HIP_TRY(c, hipEventRecord(ev[4], s));
     ++c->n_timed;
   }
   return PS_OK;
@@ -842,25 +851,45 @@ ps_status ps_set_timing(ps_ctx* c, int32_t on) {
   return PS_OK;
 }
 
+// Mean milliseconds between consecutive timing events of the timed calls:
+// part k spans events k .. k + 1.  Starts a new count.
+static ps_status read_parts(ps_ctx* c, int32_t* n_calls, double* ms) {
+  if (c->n_timed == 0) return fail(c, PS_E_STATE, "no timed scoring call to read");
+  DeviceScope ds(c->device);
+  for (int k = 0; k + 1 < kTimingEvents; ++k) ms[k] = 0.0;
+  for (int32_t n = 0; n < c->n_timed; ++n) {
+    hipEvent_t* ev = &c->ev[kTimingEvents * (size_t)n];
+    HIP_TRY(c, hipEventSynchronize(ev[kTimingEvents - 1]));
+    for (int k = 0; k + 1 < kTimingEvents; ++k) {
+      float t = 0.0f;
+      HIP_TRY(c, hipEventElapsedTime(&t, ev[k], ev[k + 1]));
+      ms[k] += t;
+    }
+  }
+  for (int k = 0; k + 1 < kTimingEvents; ++k) ms[k] /= c->n_timed;
+  *n_calls = c->n_timed;
+  c->n_timed = 0;
+  return PS_OK;
+}
+
 ps_status ps_read_timing(ps_ctx* c, int32_t* n_calls, float* ms_group, float* ms_score) {
   if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
   if (!n_calls || !ms_group || !ms_score) return fail(c, PS_E_INVAL, "output is NULL");
-  if (c->n_timed == 0) return fail(c, PS_E_STATE, "no timed scoring call to read");
-  DeviceScope ds(c->device);
-  double g = 0.0, k = 0.0;
-  for (int32_t n = 0; n < c->n_timed; ++n) {
-    hipEvent_t* ev = &c->ev[3 * (size_t)n];
-    float a = 0.0f, b = 0.0f;
-    HIP_TRY(c, hipEventSynchronize(ev[2]));
-    HIP_TRY(c, hipEventElapsedTime(&a, ev[0], ev[1]));
-    HIP_TRY(c, hipEventElapsedTime(&b, ev[1], ev[2]));
-    g += a;
-    k += b;
-  }
-  *n_calls = c->n_timed;
-  *ms_group = (float)(g / c->n_timed);
-  *ms_score = (float)(k / c->n_timed);
-  c->n_timed = 0;
+  double ms[kTimingEvents - 1];
+  ps_status st = read_parts(c, n_calls, ms);
+  if (st != PS_OK) return st;
+  *ms_group = (float)(ms[0] + ms[1]);
+  *ms_score = (float)(ms[2] + ms[3]);
+  return PS_OK;
+}
+
+ps_status ps_read_kernel_timing(ps_ctx* c, int32_t* n_calls, float* ms) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!n_calls || !ms) return fail(c, PS_E_INVAL, "output is NULL");
+  double t[kTimingEvents - 1];
+  ps_status st = read_parts(c, n_calls, t);
+  if (st != PS_OK) return st;
+  for (int k = 0; k + 1 < kTimingEvents; ++k) ms[k] = (float)t[k];
   return PS_OK;
 }
 

@@ -323,7 +323,9 @@ hipError_t ps_launch_lmax(const ps::InstState* inst_key, const uint32_t* order0,
                           hipStream_t s);
 // Prefix groups of a window: slot of every request and the longest member
 // segment per group, then the walks of the leaders.
-hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s);  // grid: a multiple of 64
+// grid: a multiple of 64; mid (optional) is recorded between the claim and
+// walk launches
+hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid);
 // Per-arrival scheduler: one workgroup of `threads` (a multiple of 64, at
 // most kSeqMaxThreads) over requests [a.r0, a.r1).
 hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);

@@ -2095,12 +2095,16 @@ hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, con
   return hipGetLastError();
 }
 
-hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s) {
+hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid) {
   if (a.n_req == 0) return hipSuccess;
   hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + kClaimBlock - 1) / kClaimBlock),
                      dim3(kClaimBlock), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (mid) {
+    e = hipEventRecord(mid, s);
+    if (e != hipSuccess) return e;
+  }
   const size_t nw = ((size_t)a.n_inst + 63) / 64;
   const size_t lds = (size_t)kStage * sizeof(uint64_t) + 2 * nw * sizeof(uint64_t);
   hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, s, a);

@@ -395,6 +395,26 @@ def test_prefix_groups_window_sizes(ps, scorer):
         compare_decisions(res, sizes, o.window_score(sub), label=f"c2 first {n}")
 
 
+def test_kernel_timing(ps, scorer):
+    """Per-launch timing of scoring calls: the claim pass, group walk and
+    lean scorer of a grouped window take time, every part is non-negative,
+    and a read starts a new count."""
+    w = synth.generate("c2", n_req=4096)
+    load_window(scorer, w)
+    dw = DeviceWindow(w)
+    scorer.set_timing(True)
+    for _ in range(3):
+        dw.score(scorer, with_sizes=False)
+    n, ms = scorer.read_kernel_timing()
+    assert n == 3 and len(ms) == 4 and min(ms) >= 0.0 and ms[0] > 0 and ms[1] > 0 and ms[2] > 0
+    with pytest.raises(ps.PackServeError):
+        scorer.read_timing()
+    dw.score(scorer, with_sizes=False)
+    n, g, k = scorer.read_timing()
+    assert n == 1 and g > 0 and k > 0
+    scorer.set_timing(False)
+
+
 def test_invalid_descriptor_flagged_on_device(ps, scorer):
     import torch
     w = synth.generate("c1", n_req=8)
