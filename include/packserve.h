@@ -206,6 +206,26 @@ ps_status ps_score_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_
                               uint32_t* d_sizes, void* hip_stream);
 
 /*
+ * ps_score_window_dev without any device allocation, for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, results and asynchrony as
+ * ps_score_window_dev (byte-identical results); the window's prefix-group
+ * table lives in a fixed device array of about 37 MiB per GPU instead of
+ * memory the context grows, set up by the first ps_create on the device and
+ * held until the process ends.  No hipMalloc, hipFree, memset node or event
+ * is issued (timing is not recorded).  Limit: n_req <= 65,536 per call
+ * (PS_E_RANGE above; split larger windows); at most 16 MiB of popular-group
+ * hit rows (a group beyond them takes the per-request path, same results).
+ * Every call on one GPU, from any context, shares that array and leaves its
+ * contents to the next: calls that overlap on one GPU (two streams, two
+ * threads, two contexts) race.  PS_E_STATE if the context has no snapshot
+ * or the array was not set up on its device.
+ */
+ps_status ps_score_window_dev_fixed(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool_len,
+                                    const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                                    uint32_t* d_sizes, void* hip_stream);
+
+/*
  * Measurement: with on != 0, the next ps_score_window(_dev) calls (up to
  * 4,096 of them) record HIP events on their stream around their launches:
  * the prefix-group pass (claim, walk) and the scoring pass (lean scorer,

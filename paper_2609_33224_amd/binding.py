@@ -98,6 +98,7 @@ def load_library() -> ctypes.CDLL:
         "ps_load_instances": ([vp, ctypes.POINTER(PsInstances), ctypes.POINTER(PsModel)], i32),
         "ps_score_window": ([vp, vp, i64, vp, i32, vp], i32),
         "ps_score_window_dev": ([vp, vp, i64, vp, i32, vp, vp, vp], i32),
+        "ps_score_window_dev_fixed": ([vp, vp, i64, vp, i32, vp, vp, vp], i32),
         "ps_probe_hits_dev": ([vp, vp, i64, vp, i32, vp, vp], i32),
         "ps_commit": ([vp, vp, i64, vp, vp, i32, ctypes.POINTER(i64)], i32),
         "ps_schedule_window_dev": ([vp, vp, i64, vp, i32, vp, vp, ctypes.POINTER(i64), vp], i32),
@@ -218,6 +219,16 @@ def ps_score_window_dev(ctx, d_pool: torch.Tensor, pool_len: int, d_reqs: torch.
                         n_req: int, d_out: torch.Tensor, d_sizes: Optional[torch.Tensor] = None,
                         stream=None) -> None:
     _check(ctx, load_library().ps_score_window_dev(
+        ctx, _dev_ptr(d_pool), int(pool_len), _dev_ptr(d_reqs), int(n_req), _dev_ptr(d_out),
+        _dev_ptr(d_sizes), _stream_handle(stream)))
+
+
+def ps_score_window_dev_fixed(ctx, d_pool: torch.Tensor, pool_len: int, d_reqs: torch.Tensor,
+                              n_req: int, d_out: torch.Tensor,
+                              d_sizes: Optional[torch.Tensor] = None, stream=None) -> None:
+    """ps_score_window_dev with the group table in the library's fixed device
+    array (no allocation; at most 65,536 requests per call)."""
+    _check(ctx, load_library().ps_score_window_dev_fixed(
         ctx, _dev_ptr(d_pool), int(pool_len), _dev_ptr(d_reqs), int(n_req), _dev_ptr(d_out),
         _dev_ptr(d_sizes), _stream_handle(stream)))
 
@@ -350,6 +361,9 @@ class Scorer:
 
     def score_dev(self, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes=None, stream=None):
         ps_score_window_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, stream)
+
+    def score_dev_fixed(self, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes=None, stream=None):
+        ps_score_window_dev_fixed(self.ctx, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, stream)
 
     def set_timing(self, on: bool) -> None:
         _check(self.ctx, load_library().ps_set_timing(self.ctx, 1 if on else 0))

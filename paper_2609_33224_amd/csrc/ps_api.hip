@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -29,6 +30,71 @@ constexpr int32_t kTimingCalls = 4096;
 // Events per timed call: around the claim pass, the group walk, the lean
 // scorer and the general scorer.
 constexpr int kTimingEvents = 5;
+
+// Entries per leader list for a window of n_req requests: the claim pass's
+// waves (4 per 256 requests) take the kXcds lists in turn, at most 64
+// leaders per wave.
+constexpr uint32_t leader_list_cap(int32_t n_req) {
+  return ((uint32_t)((n_req + 255) / 256) * 4u + kXcds - 1) / kXcds * 64u;
+}
+
+// The fixed scratch of the allocation-free scoring entry point: one window's
+// prefix-group table for up to kFixedMaxReq requests, laid out as the
+// context's own (slot keys and tagged lengths, slot records, per-request
+// slots, leader lists, counter words, popular rows).
+constexpr int32_t kFixedMaxReq = 65536;
+constexpr uint32_t kFixedSlots = 131072;  // a power of two >= 2 * kFixedMaxReq
+constexpr uint32_t kFixedListCap = leader_list_cap(kFixedMaxReq);
+constexpr size_t kFixedPopBytes = (size_t)16 << 20;
+constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr size_t kFixedOffKeys = 0;
+constexpr size_t kFixedOffRec = align256(kFixedOffKeys + 2 * (size_t)kFixedSlots * sizeof(unsigned long long));
+constexpr size_t kFixedOffSlot = align256(kFixedOffRec + (size_t)kFixedSlots * kGroupRec * sizeof(uint2));
+constexpr size_t kFixedOffList = align256(kFixedOffSlot + (size_t)kFixedMaxReq * sizeof(uint32_t));
+constexpr size_t kFixedOffHead = align256(kFixedOffList + (size_t)kXcds * kFixedListCap * sizeof(unsigned long long));
+constexpr size_t kFixedOffPop = align256(kFixedOffHead + (size_t)kGroupHeadWords * sizeof(uint32_t));
+constexpr size_t kFixedBytes = align256(kFixedOffPop + kFixedPopBytes);  // about 37 MiB
+static_assert(kFixedSlots >= 2u * (uint32_t)kFixedMaxReq, "fixed group table too small");
+
+}  // namespace
+
+// The allocation-free entry point's device scratch: one copy per GPU, held
+// until the process ends.  Host code never passes this name to a kernel or a
+// copy: it uses the address hipGetSymbolAddress returned for the device.
+static __device__ __align__(256) unsigned char scratch[kFixedBytes];
+
+namespace {
+
+// Per device: the address of `scratch` on that device (set once, at the
+// first ps_create on it) and the window generation of its group table.
+struct FixedScratch {
+  unsigned char* ptr = nullptr;
+  uint64_t gen = 0;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_fixed_mu;
+FixedScratch g_fixed[kMaxDevices];
+
+__global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// Zeroes n 32-bit words with a kernel (not a memset node, so a caller may
+// capture it in a graph).
+hipError_t fill_zero(void* p, size_t words, hipStream_t s) {
+  const int grid = (int)std::min<size_t>((words + 255) / 256, 4096);
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(grid), dim3(256), 0, s, (uint32_t*)p, words, 0u);
+  return hipGetLastError();
+}
+
+// What must start at zero in the fixed group table: the slot keys and
+// tagged lengths (a zero key is an empty slot) and the counter words.
+hipError_t clear_fixed(unsigned char* base, hipStream_t s) {
+  hipError_t e = fill_zero(base + kFixedOffKeys, 2 * (size_t)kFixedSlots * 2, s);
+  if (e == hipSuccess) e = fill_zero(base + kFixedOffHead, kGroupHeadWords, s);
+  return e;
+}
 
 }  // namespace
 
@@ -388,6 +454,22 @@ ps_status ps_create(int device, ps_ctx** out) {
     return fail(nullptr, PS_E_DEVICE, "device set-up failed: %s", hipGetErrorString(e));
   }
   c->num_cus = prop.multiProcessorCount;
+  // Once per device, with the device current: the address of the fixed
+  // scratch on this device, cleared where it must start at zero.
+  if (device < kMaxDevices) {
+    std::lock_guard<std::mutex> lk(g_fixed_mu);
+    if (!g_fixed[device].ptr) {
+      void* p = nullptr;
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e == hipSuccess) e = clear_fixed((unsigned char*)p, c->stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+      if (e != hipSuccess) {
+        ps_destroy(c);
+        return fail(nullptr, PS_E_DEVICE, "fixed scratch set-up failed: %s", hipGetErrorString(e));
+      }
+      g_fixed[device].ptr = (unsigned char*)p;
+    }
+  }
   *out = c;
   return PS_OK;
 }
@@ -671,10 +753,7 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + kGroupHeadWords * sizeof(uint32_t)));
     HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, kGroupHeadWords * sizeof(uint32_t), s));  // counter words
   }
-  // leader lists: the claim pass's waves take the kXcds lists in turn, at
-  // most 64 leaders per wave
-  const uint32_t waves = (uint32_t)((n_req + 255) / 256) * 4u;
-  const uint32_t lcap = (waves + kXcds - 1) / kXcds * 64u;
+  const uint32_t lcap = leader_list_cap(n_req);
   if (lcap > c->glcap) {
     dfree(c->d_glist);
     c->glcap = 0;
@@ -698,9 +777,12 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
   return PS_OK;
 }
 
+// fixed (optional): the window's prefix-group table in the fixed scratch
+// instead of the context's (the allocation-free entry point; no timing).
 static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
                               const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
-                              uint32_t* d_sizes, uint32_t* d_hits, hipStream_t s) {
+                              uint32_t* d_sizes, uint32_t* d_hits, hipStream_t s,
+                              const GroupTab* fixed = nullptr) {
   ScoreArgs a{};
   a.t = c->t;
   a.x = c->x;
@@ -742,7 +824,10 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
     HIP_TRY(c, ps_launch_order(d_reqs, n_req, pool_len, c->d_obins, c->d_order, s));
     a.req_order = c->d_order;
   }
-  if (!probe_all && n_req <= kGroupMaxReq && pool_len < ((int64_t)1 << kGroupGenShift) - 1) {
+  if (!probe_all && fixed) {
+    a.grp = *fixed;
+    a.defer_any = fixed->pop_ctr + 1;
+  } else if (!probe_all && n_req <= kGroupMaxReq && pool_len < ((int64_t)1 << kGroupGenShift) - 1) {
     ps_status st = group_buffers(c, n_req, s);
     if (st != PS_OK) return st;
     a.grp = GroupTab{c->d_gkeys,
@@ -776,7 +861,7 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   // it and the group walk, after the walk, after the lean scorer, after the
   // general scorer (a part that is not launched spans no time).
   hipEvent_t* ev = nullptr;
-  if (c->timing && !probe_all && c->n_timed < kTimingCalls) {
+  if (c->timing && !probe_all && !fixed && c->n_timed < kTimingCalls) {
     if (c->ev.size() < kTimingEvents * (size_t)(c->n_timed + 1)) {
       for (int k = 0; k < kTimingEvents; ++k) {
         hipEvent_t e = nullptr;
@@ -842,6 +927,57 @@ ps_status ps_score_window_dev(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   DeviceScope ds(c->device);
   return launch_score(c, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, nullptr,
                       (hipStream_t)hip_stream);
+}
+
+ps_status ps_score_window_dev_fixed(ps_ctx* c, const uint64_t* d_pool, int64_t pool_len,
+                                    const ps_req* d_reqs, int32_t n_req, ps_result* d_out,
+                                    uint32_t* d_sizes, void* hip_stream) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (!c->loaded) return fail(c, PS_E_STATE, "ps_load_instances has not succeeded yet");
+  if (n_req < 0 || pool_len < 0) return fail(c, PS_E_INVAL, "negative n_req or pool_len");
+  if (n_req > kFixedMaxReq)
+    return fail(c, PS_E_RANGE, "n_req %d exceeds the fixed scratch's %d requests per call", n_req,
+                kFixedMaxReq);
+  if (n_req == 0) return PS_OK;
+  if (!d_reqs || !d_out || (pool_len > 0 && !d_pool))
+    return fail(c, PS_E_INVAL, "device buffer is NULL");
+  if (c->device >= kMaxDevices) return fail(c, PS_E_STATE, "no fixed scratch on device %d", c->device);
+  DeviceScope ds(c->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  unsigned char* base = nullptr;
+  uint64_t gen = 0;
+  bool wrap = false;
+  {
+    std::lock_guard<std::mutex> lk(g_fixed_mu);
+    FixedScratch& f = g_fixed[c->device];
+    base = f.ptr;
+    if (++f.gen > kGroupGenMax) {
+      f.gen = 1;
+      wrap = true;
+    }
+    gen = f.gen;
+  }
+  if (!base) return fail(c, PS_E_STATE, "fixed scratch was not set up on device %d", c->device);
+  if (wrap) HIP_TRY(c, clear_fixed(base, s));
+  if (pool_len >= ((int64_t)1 << kGroupGenShift) - 1)  // too long for tagged keys: no groups
+    return launch_score(c, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, nullptr, s);
+  unsigned long long* keys = (unsigned long long*)(base + kFixedOffKeys);
+  uint32_t* head = (uint32_t*)(base + kFixedOffHead);
+  const GroupTab g{keys,
+                   keys + kFixedSlots,
+                   (uint2*)(base + kFixedOffRec),
+                   (uint32_t*)(base + kFixedOffSlot),
+                   (uint32_t*)(base + kFixedOffPop),
+                   head,
+                   (uint32_t)(kFixedPopBytes / ((size_t)c->n_inst * sizeof(uint32_t))),
+                   kFixedSlots - 1u,
+                   gen,
+                   (unsigned long long*)(base + kFixedOffList),
+                   head + kListCtrWords * (1u + kXcds * (uint32_t)(gen & 1u)),
+                   head + kListCtrWords * (1u + kXcds * (uint32_t)((gen + 1u) & 1u)),
+                   kFixedListCap,
+                   (uint32_t)(8 * c->num_cus)};
+  return launch_score(c, d_pool, pool_len, d_reqs, n_req, d_out, d_sizes, nullptr, s, &g);
 }
 
 ps_status ps_set_timing(ps_ctx* c, int32_t on) {

@@ -71,13 +71,15 @@ class DeviceWindow:
         self.d_out = torch.zeros(max(self.n_req, 1) * 20, dtype=torch.uint8, device="cuda")
         self.d_sizes = torch.zeros(max(self.n_req, 1) * 3, dtype=torch.int32, device="cuda")
 
-    def score(self, scorer, with_sizes=True):
+    def score(self, scorer, with_sizes=True, fixed=False):
         """Results (and |A|, |C|, |T| unless with_sizes is False, which takes
-        the kernel's path that does not count the sets)."""
+        the kernel's path that does not count the sets); fixed: through the
+        allocation-free entry point."""
         import paper_2609_33224_amd as ps
         import torch
-        scorer.score_dev(self.d_pool, self.pool_len, self.d_reqs, self.n_req, self.d_out,
-                         self.d_sizes if with_sizes else None)
+        call = scorer.score_dev_fixed if fixed else scorer.score_dev
+        call(self.d_pool, self.pool_len, self.d_reqs, self.n_req, self.d_out,
+             self.d_sizes if with_sizes else None)
         torch.cuda.synchronize()
         res = ps.results_from_device(self.d_out)[:self.n_req]
         if not with_sizes:
