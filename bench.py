@@ -2,21 +2,23 @@
 
 A step is one call of ps_score_window_dev over the whole window (prefix
 match, latency model, filters and selection for every request x instance
-pair), inputs resident in HBM.  Default workload: the 64-instance x 16,384-
-request window with a 30 ms TPOT target (c2).  Prints one JSON line.
+pair), inputs resident in HBM.  Default workload: the largest window, 4,096
+instances x 262,144 requests with a 30 ms TPOT target (c5).  Prints one JSON
+line.
 
-  python bench.py [--steps K] [--warmup W] [--workload c2] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--workload c5] [--no-cpu-baseline]
 
-The roofline block is the scoring pass's (lean + general kernels):
-algorithmic bytes from `score_bytes` over the library's HIP-event time on
-the launch stream.  The probe_kernel block is the exhaustive probe kernel's
+The roofline block is the dominant kernel's (the longest of the call's four
+launches): its algorithmic bytes (the byte model below, per launch) over
+its mean duration from the library's HIP events on the launch stream;
+`traffic` is the rocprofv3 FETCH_SIZE + WRITE_SIZE bytes of the same kernel
+per dispatch, scaled by what the counters read for a plain copy, from the
+committed counter summary of these kernel sources (else null).  `kernels`
+gives the same for every launch of the call; `call` the whole call's bytes
+over the step time; `per_pair_walk` what walking every eligible pair would
+move.  The probe_kernel block is the exhaustive probe kernel's
 (ps_probe_hits_dev): one 64-byte bucket per probe, min(hit + 1, chain
-length) probes per (request, instance) pair, plus the staged chain head;
-its measured_bytes are the HBM-side bytes of its dispatches per window
-(rocprofv3 FETCH_SIZE and WRITE_SIZE, scaled as for `traffic`), below the
-algorithmic bytes where requests that share a segment hit in the caches.
-`traffic` and measured_bytes come from the committed rocprofv3 counter
-summary of the same kernel sources, or are null.
+length) probes per (request, instance) pair, plus the staged chain head.
 """
 from __future__ import annotations
 
@@ -71,17 +73,18 @@ def _tpf(a, n, c):
     return a[0] + a[1] * n + a[2] * n * c + a[3] * n * n + a[4] * c + a[5] * c * c
 
 
-def probe_bytes(win, hits):
-    """Algorithmic bytes of the exhaustive probe kernel (ps_probe_hits_dev):
-    one 64-byte bucket per probe, min(hit + 1, chain length) probes on every
-    (request, instance) pair, plus the chain head it stages."""
+def probe_bytes(win, r0, pr, ph, n_rows, N):
+    """Algorithmic bytes of the exhaustive probe kernel (ps_probe_hits_dev)
+    for requests r0 .. r0 + n_rows given their holder pairs (rows pr, hits
+    ph >= 1): one 64-byte bucket per probe, min(hit + 1, chain length)
+    probes on every (request, instance) pair (one on a pair with hit 0 and a
+    non-empty chain), plus the chain head it stages.  Returns (bytes,
+    probes)."""
     import numpy as np
-    ell = (win.pre_len.astype(np.int64) + win.tail_len)[: hits.shape[0]]
-    probes = np.minimum(hits.astype(np.int64) + 1, ell[:, None])
-    probes = np.where(ell[:, None] == 0, 0, probes)
-    n_probes = int(probes.sum())
+    ell = (win.pre_len.astype(np.int64) + win.tail_len)[r0:r0 + n_rows]
+    cnt = np.bincount(pr, minlength=n_rows)
+    n_probes = int(((N - cnt) * (ell > 0)).sum() + np.minimum(ph + 1, ell[pr]).sum())
     return n_probes * BUCKET_BYTES + int(np.minimum(ell, 256).sum()) * 8, n_probes
-
 
 GROUP_MIN, GROUP_HOLD = 8, 16  # shortest grouped segment; holders a group record keeps
 
@@ -106,14 +109,15 @@ def group_info(win):
 
 def group_segment_hits(sc, win, d_pool, rep, plen, chunk_pairs=1 << 25):
     """Hit of each group's longest segment on every instance (the walk the
-    group pass makes), from the exhaustive hits of the representatives."""
+    group pass makes), from the exhaustive hits of the representatives, as
+    sorted sparse pairs: keys g * n_inst + i and hits >= 1."""
     import numpy as np
     import torch
     import paper_2609_33224_amd as ps
     G, N = len(rep), win.n_inst
-    H = np.zeros((G, N), np.int64)
+    keys, vals = [np.zeros(0, np.int64)], [np.zeros(0, np.int64)]
     if G == 0:
-        return H
+        return keys[0], vals[0]
     reqs = ps.pack_reqs(win.pre_off[rep], win.pre_len[rep], win.tail_off[rep], win.tail_len[rep])
     chunk = max(1, min(G, chunk_pairs // N))
     d_hits = torch.empty(chunk * N, dtype=torch.int32, device="cuda")
@@ -121,10 +125,20 @@ def group_segment_hits(sc, win, d_pool, rep, plen, chunk_pairs=1 << 25):
         n = min(chunk, G - g0)
         sc.hits_dev(d_pool, len(win.pool), ps.to_device_bytes(reqs[g0:g0 + n]), n, d_hits)
         torch.cuda.synchronize()
-        h = d_hits[: n * N].cpu().numpy().view(np.uint32).reshape(n, N).astype(np.int64)
-        H[g0:g0 + n] = np.minimum(h, plen[g0:g0 + n, None])
-    return H
+        h = d_hits[: n * N].cpu().numpy().view(np.uint32).reshape(n, N)
+        gr, gi = np.nonzero(h)
+        keys.append((gr.astype(np.int64) + g0) * N + gi)
+        vals.append(np.minimum(h[gr, gi].astype(np.int64), plen[g0 + gr]))
+    return np.concatenate(keys), np.concatenate(vals)
 
+
+def _lookup(keys, vals, q):
+    """vals at the sorted keys q (0 where absent)."""
+    import numpy as np
+    if len(keys) == 0:
+        return np.zeros(len(q), np.int64)
+    k = np.minimum(np.searchsorted(keys, q), len(keys) - 1)
+    return np.where(keys[k] == q, vals[k], 0)
 
 def index_walk_bytes(h, ell, nw, h_all=None):
     """Bytes of walking the live holders (h >= 1) of a chain of ell blocks
@@ -149,26 +163,25 @@ def index_walk_bytes(h, ell, nw, h_all=None):
     return by
 
 
-def group_classes(H):
+def group_classes(Hk, Hv, G, N):
     """The shared-hit class of each group as the group kernel forms it (for
     popular groups with more than 64 holders of the first block): H* = the
     most frequent hit among the holders in the first 64-instance word that
     has any (the lowest-lane value among equally frequent ones), the
     exceptions = the holders whose hit differs; class-able with at most
-    GROUP_HOLD exceptions.  Returns (classable, H*, exception mask)."""
+    GROUP_HOLD exceptions.  Hk, Hv: the sparse group hits.  Returns
+    (classable, H*)."""
     import numpy as np
-    G, N = H.shape
     ok = np.zeros(G, bool)
     hs = np.zeros(G, np.int64)
-    exc = np.zeros((G, N), bool)
-    hold = H >= 1
-    for k in np.nonzero(hold.sum(1) > 64)[0]:
-        w = int(np.argmax(hold[k].reshape(-1, 64).any(1))) if N % 64 == 0 else None
-        if w is None:
-            words = [hold[k][i:i + 64] for i in range(0, N, 64)]
-            w = next(i for i, x in enumerate(words) if x.any())
-        lanes = np.nonzero(hold[k][w * 64:(w + 1) * 64])[0]
-        vals = H[k][w * 64 + lanes]
+    gk = Hk // N
+    cnt = np.bincount(gk, minlength=G)
+    start = np.concatenate([[0], np.cumsum(cnt)])
+    for k in np.nonzero(cnt > 64)[0]:
+        ids = Hk[start[k]:start[k + 1]] % N          # ascending
+        hv = Hv[start[k]:start[k + 1]]
+        w = ids[0] // 64
+        vals = hv[ids // 64 == w]                    # lane order
         best, bestc = 0, 0
         seen = set()
         for v in vals:  # distinct values in lane order; a strictly larger count wins
@@ -179,46 +192,50 @@ def group_classes(H):
             if c > bestc:
                 best, bestc = int(v), c
         hs[k] = best
-        exc[k] = hold[k] & (H[k] != best)
-        ok[k] = exc[k].sum() <= GROUP_HOLD and 0 < best < (1 << 24)
-    return ok, hs, exc
+        ok[k] = int((hv != best).sum()) <= GROUP_HOLD and 0 < best < (1 << 24)
+    return ok, hs
 
-
-def group_pass_bytes(win, gid, rep, plen, H):
-    """Algorithmic bytes of the prefix-group pass.  Claim: descriptor, slot
-    read, the claiming compare-and-swap, the length maximum and the slot
-    entry per request.  Walk: slot entry per request; per group its
-    segment head staged (<= 256 hashes), one index bucket, the holder ids
-    (or bitmap), then with at most GROUP_HOLD holders per holder a probe of
-    the first block with its row position, 16 bytes per compared position,
-    a final probe where the segment leaves the cache, and the record; with
-    more, the holders walked together through the index and one 4-byte hit
-    per holder in the popular row, and for more than 64 holders the bitmap
-    and the hits read back for the shared-hit class, and its word."""
+def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
+    """Algorithmic bytes of the prefix-group pass, as (claim pass, walk).
+    Claim: descriptor, slot read, the claiming compare-and-swap, the length
+    maximum and the slot entry per request, a leader-list entry per group.
+    Walk: slot entry per request; per group its segment head staged (<= 256
+    hashes), one index bucket, the holder ids (or bitmap), then with at most
+    GROUP_HOLD holders per holder a probe of the first block with its row
+    position, 16 bytes per compared position, a final probe where the
+    segment leaves the cache, and the record; with more, the holders walked
+    together through the index and one 4-byte hit per holder in the popular
+    row, and for more than 64 holders the bitmap and the hits read back for
+    the shared-hit class, and its word.  Hk, Hv: the sparse group hits."""
     import numpy as np
     R, N = win.n_req, win.n_inst
+    G = len(rep)
     nw = (N + 63) // 64
     g = gid >= 0
-    by = 28 * R + int(g.sum()) * (8 + 16) + len(rep) * 16
-    by += 4 * R
-    cnt0 = (H >= 1).sum(1)
-    by += int((16 + 8 * np.minimum(plen, 256) + 128 +
-               np.where(cnt0 > 64, 8 * nw, 2 * cnt0)).sum())
+    claim = 28 * R + int(g.sum()) * (8 + 16) + G * 16
+    walk = 4 * R
+    gk = Hk // N
+    cnt0 = np.bincount(gk, minlength=G)
+    walk += int((16 + 8 * np.minimum(plen, 256) + 128 +
+                 np.where(cnt0 > 64, 8 * nw, 2 * cnt0)).sum())
     ok = cnt0 <= GROUP_HOLD
-    hc = np.minimum(H, (plen - 1)[:, None])
-    walk = np.where(H >= 1, PROBE_ROWPOS + 16 * hc + BUCKET_BYTES * (H < plen[:, None]), 0)
-    walk = np.where((plen > 1)[:, None], walk, np.where(H >= 1, PROBE_ROWPOS, 0))
-    by += int(walk[ok].sum()) + int((8 + 8 * cnt0[ok]).sum())
+    pl = plen[gk]
+    w = np.where(pl > 1, PROBE_ROWPOS + 16 * np.minimum(Hv, pl - 1) + BUCKET_BYTES * (Hv < pl),
+                 PROBE_ROWPOS)
+    walk += int(w[ok[gk]].sum()) + int((8 + 8 * cnt0[ok]).sum())
+    start = np.concatenate([[0], np.cumsum(cnt0)])
     for k in np.nonzero(~ok)[0]:
-        by += 8 + index_walk_bytes(H[k], int(plen[k]), nw) + 4 * int(cnt0[k])
+        h = np.zeros(N, np.int64)
+        h[Hk[start[k]:start[k + 1]] % N] = Hv[start[k]:start[k + 1]]
+        walk += 8 + index_walk_bytes(h, int(plen[k]), nw) + 4 * int(cnt0[k])
         if cnt0[k] > 64:  # the shared-hit class: bitmap and hits read back, the class word
-            by += 8 * nw + 4 * int(cnt0[k]) + 8
-    return by
-
+            walk += 8 * nw + 4 * int(cnt0[k]) + 8
+    return claim, walk
 
 def score_bytes(win, r0, hits, grp=None):
     """Algorithmic bytes the scoring pass moves for requests r0 .. r0 +
-    len(hits) (the benchmark's policy: D-C-Q, monotone model, no set sizes).
+    len(hits) (the benchmark's policy: D-C-Q, monotone model, no set sizes),
+    as (lean scorer's, general scorer's).
 
     Requests whose group record holds their hits go through the lean kernel
     (four requests per wave): 24 B descriptor + 4 B group slot + 136 B
@@ -234,6 +251,11 @@ def score_bytes(win, r0, hits, grp=None):
     class and no candidate is in T, the states of all instances.  Pools of
     at most 64 instances keep states and thresholds in LDS (no bytes).  The
     rooms and threshold maxima are read once per wave (not counted).
+
+    grp: per request its group's id ("gid", -1 none), whether the group has a
+    record ("has"), a popular row ("pop"), a shared-hit class ("cls", with
+    H* "hs" and the group's segment length "gplen"); "grouped"; the group
+    hits as sparse pairs ("Hk", "Hv").
 
     Requests of a popular group with a shared-hit class below their
     segment end take the general kernel's class path: descriptor, slot,
@@ -275,34 +297,41 @@ def score_bytes(win, r0, hits, grp=None):
     while span > 64:
         span = (span + 63) // 64
         levels += 1
-    h = hits.astype(np.int64)
-    elig = room[None, :] >= L[:, None]
-    hold0 = h >= 1
-    cand = elig & hold0
-    ncand = cand.sum(1)
-    nA = elig.sum(1)
-    cnt0 = hold0.sum(1)
-    act = nA > 0
     if grp is None:
         grp = dict(has=np.zeros(R, bool), pop=np.zeros(R, bool), grouped=np.zeros(R, bool),
-                   Hg=np.zeros_like(h))
+                   gid=np.full(R, -1, np.int64), Hk=np.zeros(0, np.int64),
+                   Hv=np.zeros(0, np.int64))
+    # Holder pairs (hit >= 1), in row order; every per-pair term below is
+    # zero on the other pairs.
+    pr, pi = np.nonzero(hits)
+    ph = hits[pr, pi].astype(np.int64)
+    p_elig = room[pi] >= L[pr]
+
+    def per_row(v):
+        return np.bincount(pr, weights=v, minlength=R).astype(np.int64)
+
+    room_sorted = np.sort(room)
+    nA = N - np.searchsorted(room_sorted, L, side="left")   # eligible instances
+    cnt0 = np.bincount(pr, minlength=R)                      # holders of the first block
+    ncand = np.bincount(pr, weights=p_elig, minlength=R).astype(np.int64)
+    act = nA > 0
     lean = grp["has"] & ~grp["pop"]
     pop = grp["has"] & grp["pop"]
     # popular groups with a shared-hit class, where H* lies below the
     # request's segment end (p0): the class path of the general kernel
     if "cls" in grp:
-        p0 = np.minimum(win.pre_len[r0:r0 + R].astype(np.int64), grp["gplen"])
+        p0 = np.minimum(p, grp["gplen"])
         clsp = grp["cls"] & (grp["hs"] < p0)
     else:
         clsp = np.zeros(R, bool)
     pop = pop & ~clsp
-    # resume walks of grouped requests
-    Hg = grp["Hg"]
-    resume = cand & (Hg >= p[:, None]) & (p < ell)[:, None]
-    rb = np.where(h > p[:, None],
-                  PROBE_ROWPOS + 16 * (np.minimum(h, (ell - 1)[:, None]) - p[:, None]) +
-                  BUCKET_BYTES * (h < ell[:, None]), PROBE_ROWPOS)
-    resume_by = np.where(resume, rb, 0).sum(1)
+    # resume walks of grouped requests: the group's segment hit on the pair
+    p_Hg = np.where(grp["gid"][pr] >= 0,
+                    _lookup(grp["Hk"], grp["Hv"], np.maximum(grp["gid"][pr], 0) * N + pi), 0)
+    p_resume = p_elig & (p_Hg >= p[pr]) & (p[pr] < ell[pr])
+    p_rb = np.where(ph > p[pr], PROBE_ROWPOS + 16 * (np.minimum(ph, ell[pr] - 1) - p[pr]) +
+                    BUCKET_BYTES * (ph < ell[pr]), PROBE_ROWPOS)
+    resume_by = per_row(np.where(p_resume, p_rb, 0))
     # general kernel: per-request parts
     gen = 48 + 512 * levels + np.zeros(R, np.int64)
     gen += np.where(pop, 144 + np.where(act & (ell > 0), 128 + np.where(
@@ -311,120 +340,233 @@ def score_bytes(win, r0, hits, grp=None):
     gen += np.where(nogrp, 8 * np.minimum(ell, 256) + np.where(grp["grouped"], 144, 0), 0)
     gen += np.where(nogrp & act & (ell > 0), 128 + np.where(cnt0 <= 64, 10 * cnt0, 8 * nw + 8 * cnt0), 0)
     few = ncand <= 64
-    hc = np.minimum(h, (ell - 1)[:, None])
-    walk = np.where(cand, PROBE_ROWPOS + 16 * hc + BUCKET_BYTES * (h < ell[:, None]), 0).sum(1)
+    walk = per_row(np.where(p_elig, PROBE_ROWPOS + 16 * np.minimum(ph, ell[pr] - 1) +
+                            BUCKET_BYTES * (ph < ell[pr]), 0))
     gen += np.where(nogrp & act & few & (ell > 1), walk, 0)
     for r in np.nonzero(nogrp & act & ~few & (ell > 1))[0]:
-        gen[r] += index_walk_bytes(np.where(cand[r], h[r], 0), int(ell[r]), nw, h[r])
+        h_r = hits[r].astype(np.int64)
+        gen[r] += index_walk_bytes(np.where(room >= L[r], h_r, 0), int(ell[r]), nw, h_r)
     # lean kernel: per-request parts
     lby = 184 + (0 if small else 32) * cnt0 + resume_by
     lby = np.where(act, lby, 184)
     by = np.where(lean, lby, gen)
     if clsp.any():
-        exc = grp["exc"]
-        ex_res = np.where(resume & exc, rb, 0).sum(1)
-        cby = (24 + 4 + 8 * 18 + 20 + 64 * 16 + 8 * nw + 32 * exc.sum(1) + ex_res +
+        p_exc = (p_Hg >= 1) & (p_Hg != grp["hs"][pr])    # holders off the class hit
+        ex_res = per_row(np.where(p_resume & p_exc, p_rb, 0))
+        cby = (24 + 4 + 8 * 18 + 20 + 64 * 16 + 8 * nw + 32 * per_row(p_exc) + ex_res +
                16 * n1 + 64 * (4 + 32) + 4 * n1 + 64 * 16 + 32)
         by = np.where(clsp, cby, by)
-    # the recomputation filter and the hit-0 class
-    n = (L[:, None] - h * bs).astype(np.float64)
-    c = (h * bs).astype(np.float64)
-    Lf = L.astype(np.float64)[:, None]
-    W = np.maximum(0.0, _tpf(a, n, c) - _tpf(a, 0.0, Lf))
-    Z = (_tpf(a, Lf, 0.0) - _tpf(a, 0.0, Lf))[:, 0]
-    Wmin = np.where(elig, W, np.inf).min(1)
+    # The recomputation filter: W = max(0, T_pf(n, c) - T_pf(0, L)); a
+    # non-holder (n = L) has W = max(0, Z).
+    Lf = L.astype(np.float64)
+    Z = _tpf(a, Lf, 0.0) - _tpf(a, 0.0, Lf)
+    W0 = np.maximum(0.0, Z)
+    p_n = (L[pr] - ph * bs).astype(np.float64)
+    p_c = (ph * bs).astype(np.float64)
+    p_W = np.maximum(0.0, _tpf(a, p_n, p_c) - _tpf(a, 0.0, Lf[pr]))
+    n0 = nA - ncand
+    Wmin = np.where(n0 > 0, W0, np.inf)
+    np.minimum.at(Wmin, pr[p_elig], p_W[p_elig])
     kvc = Z > 0
     with np.errstate(divide="ignore", invalid="ignore"):
-        rho = (W - Wmin[:, None]) / Z[:, None]
-    inC = elig & (~kvc[:, None] | (rho <= eta))
-    by += np.where(lean | clsp, 0, 32 * (cand & inC).sum(1))
-    n0 = nA - ncand
-    W0 = np.maximum(0.0, Z)
-    with np.errstate(divide="ignore", invalid="ignore"):
+        p_rho = (p_W - Wmin[pr]) / Z[pr]
         admit0 = (n0 > 0) & (~kvc | ((W0 - Wmin) / Z <= eta))
+    p_inC = p_elig & (~kvc[pr] | (p_rho <= eta))
+    by += np.where(lean | clsp, 0, 32 * per_row(p_inC))
     seg = np.searchsorted(ub, A1, side="left")
     seg = np.minimum(seg, len(ub) - 1)
     order0 = np.lexsort((np.arange(N), win.Q, -win.D.astype(np.int64)))
     chunk_lean = 0 if small else 64 * 16
-    for r in np.nonzero(act & (admit0 | lean) & ~clsp)[0]:
-        t_iter = gam[seg] * (beta[seg, 0] + beta[seg, 1] * A1 + beta[seg, 2] * (win.S + L[r]))
-        tpot0 = t_iter + np.where(A1 > 1, _tpf(a, float(L[r]), 0.0) / lout1, 0.0)
-        zero = elig[r] & ~hold0[r]
-        feas = np.zeros(n1 * 64, bool)
-        feas[:N] = (elig[r] & (tpot0 < tau))[order0]
-        passing = feas.reshape(n1, 64).any(1)
-        ok = (zero & (tpot0 < tau))[order0]
-        found = bool(ok.any())
-        cs = int(np.argmax(ok)) // 64 if found else n1 - 1
-        if lean[r]:
-            if not admit0[r]:  # only the speculative first chunk
-                by[r] += chunk_lean if passing.any() else 0
-                continue
-            by[r] += chunk_lean * int(passing[:cs + 1].sum()) + (0 if small or not found else 32)
-        else:
-            by[r] += 256 * (cs // 64 + 1) + 1024 * int(passing[:cs + 1].sum())
-        if found:
-            continue
+
+    def dense_rows(rr):
+        """Eligibility, holders, new / cached tokens and C membership of the
+        candidates of the requests rr, on every instance."""
+        h = hits[rr].astype(np.int64)
+        el = room[None, :] >= L[rr][:, None]
+        hold = h >= 1
+        n_ = (L[rr][:, None] - h * bs).astype(np.float64)
+        c_ = (h * bs).astype(np.float64)
+        W = np.maximum(0.0, _tpf(a, n_, c_) - _tpf(a, 0.0, Lf[rr][:, None]))
+        with np.errstate(divide="ignore", invalid="ignore"):
+            rho = (W - Wmin[rr][:, None]) / Z[rr][:, None]
+        inC_ = el & (~kvc[rr][:, None] | (rho <= eta))
+        return el, hold, n_, c_, inC_
+
+    # The zero-hit class per request: which 64-instance chunks of the key
+    # order hold a member of T, the first that holds an admitted non-holder,
+    # and whether the class is evaluated in full (no member of the class and
+    # no candidate in T).
+    rows = np.nonzero(act & (admit0 | lean) & ~clsp)[0]
+    mono = (beta[:, 2] >= 0).all() and (gam >= 0).all() and a[1] >= 0 and a[3] >= 0
+
+    def tpot0_of(Lt, idx=slice(None)):
+        """TPOT of a zero-hit request of Lt tokens on the instances idx."""
+        sg = seg[idx]
+        t_it = gam[sg] * (beta[sg, 0] + beta[sg, 1] * A1[idx] + beta[sg, 2] * (win.S[idx] + Lt))
+        return t_it, t_it + np.where(A1[idx] > 1, _tpf(a, Lt, 0.0) / lout1, 0.0)
+
+    def dense(rr):
+        """Every instance of every request of rr (any model)."""
+        k = len(rr)
+        el, hold, _, _, _ = dense_rows(rr)
+        t_iter, tpot0 = tpot0_of(L[rr].astype(np.float64)[:, None])
+        below = tpot0 < tau
+        zero = el & ~hold
+        feas = np.zeros((k, n1 * 64), bool)
+        feas[:, :N] = (el & below)[:, order0]
+        passing = feas.reshape(k, n1, 64).any(2)
+        okm = (zero & below)[:, order0]
+        found = okm.any(1)
+        cs = np.where(found, np.argmax(okm, 1) // 64, n1 - 1)
+        return found, cs, passing
+
+    def finish(rr, found, cs, passing):
+        k = len(rr)
+        npass = np.cumsum(passing, 1)[np.arange(k), cs]
+        lean_r, adm = lean[rr], admit0[rr]
+        spec = lean_r & ~adm          # only the speculative first chunk
+        add = np.zeros(k, np.int64)
+        add[spec] = np.where(passing[spec].any(1), chunk_lean, 0)
+        m = lean_r & adm
+        add[m] = chunk_lean * npass[m] + (0 if small else 32 * found[m])
+        m = ~lean_r
+        add[m] = 256 * (cs[m] // 64 + 1) + 1024 * npass[m]
         # No member of the class is in T: it is evaluated in full only when
         # no candidate is in T either.
-        cr = cand[r] & inC[r]
-        if cr.any():
-            tp = t_iter[cr] + np.where(A1[cr] > 1, _tpf(a, n[r][cr], c[r][cr]) / lout1, 0.0)
-            if (tp < tau).any():
-                continue
-        if lean[r]:
-            by[r] += 0 if small else 32 * N + 32
-        else:
-            by[r] += 8 * N + 32 * int(zero.sum())
-    return int(by.sum())
+        need = ~found & ~spec
+        if need.any():
+            rn = rr[need]
+            el, hold, n_, c_, inC_ = dense_rows(rn)
+            t_iter = tpot0_of(L[rn].astype(np.float64)[:, None])[0]
+            tp = t_iter + np.where(A1[None, :] > 1, _tpf(a, n_, c_) / lout1, 0.0)
+            none_t = ~(el & hold & inC_ & (tp < tau)).any(1)
+            full = np.zeros(k, bool)
+            full[need] = none_t
+            nz = np.zeros(k, np.int64)
+            nz[need] = (el & ~hold).sum(1)
+            add += np.where(full & lean_r, 0 if small else 32 * N + 32, 0)
+            add += np.where(full & ~lean_r, 8 * N + 32 * nz, 0)
+        by[rr] += add
+
+    if mono and len(rows):
+        # Monotone model: "eligible and TPOT below tau" for a zero-hit request
+        # of L tokens is L <= thr_i = min(room_i, the longest admitted L), so
+        # the first admitted instance in key order comes from a prefix
+        # maximum; rows whose first admitted instance holds the first block
+        # take the dense path.
+        ell_hi = int(max(1, (win.pre_len.astype(np.int64) + win.tail_len).max()))
+        lo = np.full(N, -1, np.int64)           # admitted at lo blocks (-1: none)
+        hi = np.full(N, ell_hi + 1, np.int64)   # refused at hi blocks
+        ok_hi = tpot0_of(float(ell_hi * bs))[1] < tau
+        lo[ok_hi] = ell_hi
+        while (hi > lo + 1).any():
+            open_ = hi > lo + 1
+            mid = np.where(open_, (lo + hi) // 2, lo)
+            okm = tpot0_of((np.maximum(mid, 0) * bs).astype(np.float64))[1] < tau
+            lo = np.where(open_ & okm, mid, lo)
+            hi = np.where(open_ & ~okm, mid, hi)
+        lmax = np.where(lo >= 0, lo * bs, -1)
+        thr = np.minimum(room, lmax)
+        thr_o = np.full(n1 * 64, -2, np.int64)
+        thr_o[:N] = thr[order0]
+        cmax = thr_o.reshape(n1, 64).max(1)
+        pmax = np.maximum.accumulate(thr_o)
+        p0 = np.searchsorted(pmax, L[rows], side="left")   # first position admitting L
+        anyadm = p0 < N
+        first = order0[np.minimum(p0, N - 1)]
+        holder_first = anyadm & (hits[rows, first] >= 1)
+        rf = rows[~holder_first]
+        found = anyadm[~holder_first]
+        cs = np.where(found, p0[~holder_first] // 64, n1 - 1)
+        finish(rf, found, cs, cmax[None, :] >= L[rf][:, None])
+        rows = rows[holder_first]
+    for b0 in range(0, len(rows), 512):
+        rr = rows[b0:b0 + 512]
+        found, cs, passing = dense(rr)
+        finish(rr, found, cs, passing)
+    return int(by[lean].sum()), int(by[~lean].sum())
 
 
-def algorithmic_bytes(sc, win, d_pool, d_reqs, chunk_pairs=1 << 25):
-    """The byte counts of the scoring kernel, the prefix-group pass and the
-    exhaustive probe kernel over the whole window, from the exhaustive
+def survey_pair_bytes(win, r0, pr, pi, ph, n_rows, N):
+    """The per-window algorithmic bytes of a walk of every capacity-eligible
+    (request, instance) pair, for requests r0 .. r0 + n_rows: 64 B per probe,
+    min(hit + 1, chain length) probes per eligible pair, plus 8 B per
+    request-chain block read (min(longest eligible hit + 1, chain length)),
+    plus 20 B of result per request.  (The instances' 24 B of state are
+    added once per window by the caller.)"""
+    import numpy as np
+    pol = win.policy
+    bs, bmax, kv = int(pol["block_tokens"]), int(pol["b_max"]), int(pol["kv_cap_tokens"])
+    A1 = win.D.astype(np.int64) + win.Q + 1
+    room = np.where(A1 <= bmax, kv - win.S, -1)
+    ell = (win.pre_len.astype(np.int64) + win.tail_len)[r0:r0 + n_rows]
+    L = ell * bs
+    nA = N - np.searchsorted(np.sort(room), L, side="left")
+    el = room[pi] >= L[pr]
+    ncand = np.bincount(pr, weights=el, minlength=n_rows).astype(np.int64)
+    probes = (nA - ncand) * (ell > 0) + np.bincount(
+        pr, weights=np.where(el, np.minimum(ph + 1, ell[pr]), 0), minlength=n_rows).astype(np.int64)
+    hmax = np.zeros(n_rows, np.int64)
+    np.maximum.at(hmax, pr[el], ph[el])
+    chain = np.where(nA > 0, np.minimum(hmax + 1, ell), 0)
+    return int(64 * probes.sum() + 8 * chain.sum() + 20 * n_rows)
+
+
+def algorithmic_bytes(sc, win, d_pool, chunk_pairs=1 << 25):
+    """Algorithmic bytes of every kernel of one scoring call (claim pass,
+    group walk, lean scorer, general scorer), of the exhaustive probe
+    kernel over the window, and the per-pair figure, from the exhaustive
     per-pair hits exported chunk by chunk (untimed)."""
     import numpy as np
     import torch
     import paper_2609_33224_amd as ps
+    N = win.n_inst
     gid, rep, plen = group_info(win)
-    H = group_segment_hits(sc, win, d_pool, rep, plen)
+    Hk, Hv = group_segment_hits(sc, win, d_pool, rep, plen)
+    G = len(rep)
+    cnt = np.bincount(Hk // N, minlength=G) if G else np.zeros(0, np.int64)
     # every group gets a result: a record, or a popular row (the area holds
     # 64 MiB / (4 n_inst) rows, more than any benchmark window needs)
-    g_has = np.ones(len(rep), bool)
-    g_pop = (H >= 1).sum(1) > GROUP_HOLD if len(rep) else np.zeros(0, bool)
-    assert int(g_pop.sum()) <= (64 << 20) // (4 * win.n_inst)
-    gb = group_pass_bytes(win, gid, rep, plen, H)
-    g_cls, g_hs, g_exc = group_classes(H) if len(rep) else (np.zeros(0, bool), np.zeros(0, np.int64),
-                                                            np.zeros((0, win.n_inst), bool))
-    chunk = max(1, min(win.n_req, chunk_pairs // win.n_inst))
+    g_pop = cnt > GROUP_HOLD
+    assert int(g_pop.sum()) <= (64 << 20) // (4 * N)
+    claim_b, walk_b = group_pass_bytes(win, gid, rep, plen, Hk, Hv)
+    g_cls, g_hs = group_classes(Hk, Hv, G, N)
+    chunk = max(1, min(win.n_req, chunk_pairs // N))
     reqs = ps.pack_reqs(win.pre_off, win.pre_len, win.tail_off, win.tail_len)
-    d_hits = torch.empty(chunk * win.n_inst, dtype=torch.int32, device="cuda")
-    sb = pb = npr = 0
+    d_hits = torch.empty(chunk * N, dtype=torch.int32, device="cuda")
+    lean_b = gen_b = probe_b = n_probes = pair_b = 0
     for r0 in range(0, win.n_req, chunk):
         n = min(chunk, win.n_req - r0)
         d_r = ps.to_device_bytes(reqs[r0:r0 + n])
         sc.hits_dev(d_pool, len(win.pool), d_r, n, d_hits)
         torch.cuda.synchronize()
-        hits = d_hits[: n * win.n_inst].cpu().numpy().view(np.uint32).reshape(n, win.n_inst)
-        b, p_ = probe_bytes(win.subset(range(r0, r0 + n)), hits)
-        pb += b
-        npr += p_
+        hits = d_hits[: n * N].cpu().numpy().view(np.uint32).reshape(n, N)
+        pr, pi = np.nonzero(hits)
+        ph = hits[pr, pi].astype(np.int64)
+        b, p_ = probe_bytes(win, r0, pr, ph, n, N)
+        probe_b += b
+        n_probes += p_
+        pair_b += survey_pair_bytes(win, r0, pr, pi, ph, n, N)
         gc = gid[r0:r0 + n]
         grouped = gc >= 0
-        has = grouped & g_has[np.maximum(gc, 0)] if len(rep) else grouped
-        pop = grouped & g_pop[np.maximum(gc, 0)] if len(rep) else grouped
-        Hg = H[np.maximum(gc, 0)] if len(rep) else np.zeros(hits.shape, np.int64)
         gi = np.maximum(gc, 0)
-        cls = pop & g_cls[gi] if len(rep) else np.zeros(n, bool)
-        hs = g_hs[gi] if len(rep) else np.zeros(n, np.int64)
-        exc = g_exc[gi] if len(rep) else np.zeros(hits.shape, bool)
-        gpl = plen[gi] if len(rep) else np.zeros(n, np.int64)
-        sb += score_bytes(win, r0, hits, dict(has=has, pop=pop, grouped=grouped, Hg=Hg, cls=cls,
-                                              hs=hs, exc=exc, gplen=gpl))
-    return sb, gb, pb, npr
+        if G:
+            pop = grouped & g_pop[gi]
+            grp = dict(has=grouped, pop=pop, grouped=grouped, gid=gc, Hk=Hk, Hv=Hv,
+                       cls=pop & g_cls[gi], hs=g_hs[gi], gplen=plen[gi])
+        else:
+            grp = None
+        lb, gb = score_bytes(win, r0, hits, grp)
+        lean_b += lb
+        gen_b += gb
+    pair_b += 24 * N
+    return dict(claim=claim_b, walk=walk_b, lean=lean_b, general=gen_b, probe=probe_b,
+                probes=n_probes, pairs=pair_b, groups=G, popular_groups=int(g_pop.sum()))
 
 
 def traffic_for(workload: str, src_hash: str):
+    """The committed counter summary for this workload, if it was taken on
+    these kernel sources."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -437,32 +579,35 @@ def traffic_for(workload: str, src_hash: str):
 
 
 def cpu_baseline(win, budget_s: float):
-    """The oracle on the host cores, over the same window, repeated (or on a
-    leading slice) to fill roughly `budget_s` seconds."""
+    """The oracle on the host cores over a leading slice of the window sized
+    from a short timed slice to fill about `budget_s` seconds (the whole
+    window, repeated, when it takes less)."""
     import oracle
     o = oracle.Oracle.from_window(win)
     threads = oracle.max_threads()
+    n0 = min(win.n_req, 2048)
     t0 = time.perf_counter()
-    o.window_score(win)
-    one = time.perf_counter() - t0
-    if one > budget_s:
-        n = max(64, int(win.n_req * budget_s / one))
+    o.window_score(win.subset(range(n0)))
+    per_req = (time.perf_counter() - t0) / n0
+    if per_req * win.n_req < budget_s:
+        reps = max(1, int(budget_s / max(per_req * win.n_req, 1e-3)))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            o.window_score(win)
+        dt = (time.perf_counter() - t0) / reps
+        n, sample = win.n_req, (f"whole window ({win.n_req} requests x {win.n_inst} instances), "
+                                f"{reps} repetitions")
+    else:
+        n = max(n0, min(win.n_req, int(budget_s / per_req)))
         sub = win.subset(range(n))
         t0 = time.perf_counter()
         o.window_score(sub)
         dt = time.perf_counter() - t0
-        return dict(value=n * win.n_inst / dt, unit="candidate evals/s", cores=threads,
-                    kind="oracle", decisions_per_s=n / dt,
-                    sample=f"first {n} of {win.n_req} requests of the window, once")
-    reps = max(1, int(budget_s / max(one, 1e-3)))
-    t0 = time.perf_counter()
-    for _ in range(reps):
-        o.window_score(win)
-    dt = (time.perf_counter() - t0) / reps
-    return dict(value=win.n_req * win.n_inst / dt, unit="candidate evals/s", cores=threads,
-                kind="oracle", decisions_per_s=win.n_req / dt,
-                sample=f"whole window ({win.n_req} requests x {win.n_inst} instances), "
-                       f"{reps} repetitions")
+        sample = (f"first {n} of {win.n_req} requests x {win.n_inst} instances, once "
+                  f"(sized from a timed slice of {n0})")
+    o.close()
+    return dict(value=n * win.n_inst / dt, unit="candidate evals/s", cores=threads,
+                kind="oracle", decisions_per_s=n / dt, seconds=dt, sample=sample)
 
 
 def cpu_sequential_baseline(win, budget_s: float):
@@ -476,19 +621,22 @@ def cpu_sequential_baseline(win, budget_s: float):
     one = (time.perf_counter() - t0) / min(n, 256)
     if one * n > budget_s:
         n = max(256, int(budget_s / max(one, 1e-9)))
+    o.close()
     o = oracle.Oracle.from_window(win)
     t0 = time.perf_counter()
     o.window_schedule(win.subset(range(n)) if n < win.n_req else win)
     dt = time.perf_counter() - t0
+    o.close()
     return dict(value=n / dt, unit="decisions/s", cores=1, kind="oracle",
                 sample=(f"first {n} of {win.n_req} requests, per arrival, once" if n < win.n_req
                         else f"whole window ({win.n_req} requests), per arrival, once"))
 
 
-def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
-    """Algorithm 1 per arrival (ps_schedule_window_dev) on the same window and
-    starting state, and the herding of the snapshot placements: the same
-    placements replayed in arrival order (ps_replay_window_dev)."""
+def sequential_block(sc, win, model, d_pool, d_reqs, n, snap, reps, stream):
+    """Algorithm 1 per arrival (ps_schedule_window_dev) on the window's first
+    n requests from the loaded state, and the herding of the snapshot
+    placements of the same requests: those placements replayed in arrival
+    order (ps_replay_window_dev)."""
     import numpy as np
     import torch
     import paper_2609_33224_amd as ps
@@ -497,8 +645,7 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
         sc.load(win.n_inst, win.cap, win.blk_off, win.blk, win.D, win.Q, win.P, win.S, model)
         torch.cuda.synchronize()
 
-    n = win.n_req
-    snap_all = snap
+    snap_all = snap[:n]
     d_out = torch.empty(n * 20, dtype=torch.uint8, device="cuda")
     times = []
     for k in range(reps + 1):  # the first call is a warm-up
@@ -512,23 +659,23 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
     # The replay stops before the first placement that would take an
     # instance's queue past its 12-bit limit (snapshot herding can).
     n_rep, q = n, win.Q.astype(np.int64).copy()
-    for k, i in enumerate(snap["instance"]):
+    for k, i in enumerate(snap_all["instance"]):
         if i >= 0:
             q[i] += 1
             if q[i] > 4095:
                 n_rep = k
                 break
     reload()
-    d_inst = torch.from_numpy(np.ascontiguousarray(snap["instance"][:n_rep], np.int32)).to("cuda")
+    d_inst = torch.from_numpy(np.ascontiguousarray(snap_all["instance"][:n_rep], np.int32)).to("cuda")
     t0 = time.perf_counter()
     if n_rep:
         sc.replay_dev(d_pool, len(win.pool), d_reqs, n_rep, d_inst, d_out, stream)
     replay_s = time.perf_counter() - t0
     rep = ps.results_from_device(d_out)[:n_rep]
-    snap = snap[:n_rep]
+    snap_r = snap_all[:n_rep]
     tau = float(np.float32(win.policy["tpot_slo"]))
     fb = ps.PS_R_FALLBACK
-    ok_snap = (snap["instance"] >= 0) & ((snap["flags"] & fb) == 0)
+    ok_snap = (snap_r["instance"] >= 0) & ((snap_r["flags"] & fb) == 0)
     ok_seq = (seq["instance"] >= 0) & ((seq["flags"] & fb) == 0)
     per_snap = np.bincount(snap_all["instance"][snap_all["instance"] >= 0], minlength=win.n_inst)
     per_seq = np.bincount(seq["instance"][seq["instance"] >= 0], minlength=win.n_inst)
@@ -536,7 +683,8 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
     return {
         "entry": "ps_schedule_window_dev: Algorithm 1 per arrival (hits pass, one-workgroup "
                  "scheduler, rebuild of the derived data)",
-        "ms_per_window": ms, "decisions_per_s": n / (ms * 1e-3),
+        "requests": n, "of_window": win.n_req,
+        "ms_per_call": ms, "decisions_per_s": n / (ms * 1e-3),
         "us_per_decision": ms * 1e3 / n, "reps": reps,
         "bound": "latency (each decision waits for the commit before it)",
         "placed": int((seq["instance"] >= 0).sum()),
@@ -555,17 +703,30 @@ def sequential_block(sc, win, model, d_pool, d_reqs, snap, reps, stream):
     }
 
 
+KERNELS = ("group_claim_kernel", "group_kernel", "lean_rows_kernel", "score_kernel")
+KERNEL_ROLE = {
+    "group_claim_kernel": "prefix-group claim pass (each request's group slot, leader lists)",
+    "group_kernel": "prefix-group walk (each shared segment walked once on every holder of its "
+                    "first block)",
+    "lean_rows_kernel": "scorer, four requests per wave (hits from the group records, latency "
+                        "model, filters, packing key, argmin)",
+    "score_kernel": "general scorer (requests the lean scorer left: popular groups)",
+}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--workload", default="c5", choices=sorted(WORKLOAD_NAMES))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=10.0)
-    ap.add_argument("--sequential-reps", type=int, default=3,
-                    help="timed calls of the per-arrival scheduler (0: skip that block)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the CPU baseline (sized from a timed slice)")
+    ap.add_argument("--sequential-requests", type=int, default=16384,
+                    help="leading requests of the window scheduled per arrival (0: skip)")
+    ap.add_argument("--sequential-reps", type=int, default=2)
     ap.add_argument("--skip-bytes", action="store_true",
                     help="skip the algorithmic byte counts (roofline fields null; for counter runs)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -591,13 +752,17 @@ def main():
     import synth
     import paper_2609_33224_amd as ps
 
-    print(f"bench: generating {args.workload}", file=sys.stderr, flush=True)
+    def say(msg):
+        print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+    say(f"generating {args.workload}")
     win = synth.generate(args.workload, seed=args.seed)
     sc = ps.Scorer(0)
     m = ps.make_model(win.alpha, win.seg_ub, win.beta, win.gamma, win.policy["eta"],
                       win.policy["tpot_slo"], win.policy["ttft_floor"], win.policy["lout"],
                       win.policy["block_tokens"], win.policy["b_max"],
                       win.policy["kv_cap_tokens"], win.policy["flags"], win.policy["rand_seed"])
+    say("loading the instances")
     t0 = time.perf_counter()
     sc.load(win.n_inst, win.cap, win.blk_off, win.blk, win.D, win.Q, win.P, win.S, m)
     load_s = time.perf_counter() - t0
@@ -609,15 +774,16 @@ def main():
 
     # untimed: byte counts from the per-pair hits, and the end-to-end host call
     if args.skip_bytes:
-        alg_bytes = group_bytes = probe_alg_bytes = n_probes = None
+        nb = None
     else:
-        print("bench: counting algorithmic bytes", file=sys.stderr, flush=True)
-        alg_bytes, group_bytes, probe_alg_bytes, n_probes = algorithmic_bytes(sc, win, d_pool, d_reqs)
+        say("counting algorithmic bytes")
+        nb = algorithmic_bytes(sc, win, d_pool)
     t0 = time.perf_counter()
     sc.score(win.pool, reqs)
     host_call_s = time.perf_counter() - t0
 
     # the exhaustive per-instance probe kernel (ps_probe_hits_dev), timed alone
+    say("timing the exhaustive probe kernel")
     pk_chunk = max(1, min(win.n_req, (1 << 28) // win.n_inst))
     d_ph = torch.empty(pk_chunk * win.n_inst, dtype=torch.int32, device="cuda")
     d_pr = ps.to_device_bytes(reqs[:pk_chunk])
@@ -637,7 +803,7 @@ def main():
     # The timed region: exactly K steps back to back, bracketed by device
     # synchronisation (no events inside it: a marker between steps costs the
     # stream a few microseconds of its own).
-    print(f"bench: timing {args.steps} steps", file=sys.stderr, flush=True)
+    say(f"timing {args.steps} steps")
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     for _ in range(args.steps):
@@ -655,12 +821,12 @@ def main():
         b.record(stream)
     torch.cuda.synchronize()
     step_avg = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    # The same steps again with the library's events around its launches:
-    # the prefix-group pass and the scoring kernel, each on the launch stream.
+    # The same steps again with the library's events around each of its
+    # launches, recorded on the launch stream.
     sc.set_timing(True)
     for _ in range(args.steps):
         sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
-    n_timed, group_ms, kern_avg = sc.read_timing()
+    n_timed, kern_ms = sc.read_kernel_timing()
     sc.set_timing(False)
 
     evals = win.n_req * win.n_inst
@@ -669,16 +835,29 @@ def main():
     lib_id = ps.ps_build_id()
     lib_fresh = lib_id == ps_build.source_hash()
     if not lib_fresh:
-        print(f"bench: libpackserve.so was built from other sources ({lib_id}); "
-              "rebuild it (__graft_entry__.build()); counter bytes are not applied", file=sys.stderr)
+        say(f"libpackserve.so was built from other sources ({lib_id}); rebuild it "
+            "(__graft_entry__.build()); counter bytes are not applied")
     tent = (traffic_for(args.workload, src_hash) or {}) if lib_fresh else {}
-    traffic = tent.get("bytes_per_launch")
-    probe_meas = tent.get("probe_bytes_per_window")
-    def rate(nbytes, ms):
-        return nbytes / (ms * 1e-3) / 1e9 if nbytes is not None and ms > 0 else None
+    tk = tent.get("kernels", {})
 
-    achieved = rate(alg_bytes, kern_avg)
-    probe_gbs = rate(probe_alg_bytes, probe_ms)
+    def rate(nbytes, ms):
+        return nbytes / (ms * 1e-3) / 1e9 if nbytes is not None and ms and ms > 0 else None
+
+    kb = dict(zip(KERNELS, (nb["claim"], nb["walk"], nb["lean"], nb["general"]) if nb else (None,) * 4))
+    kernels = {}
+    for name, ms in zip(KERNELS, kern_ms):
+        ach = rate(kb[name], ms)
+        kernels[name] = {"role": KERNEL_ROLE[name], "ms_avg": ms, "algorithmic_bytes": kb[name],
+                         "achieved_GBs": ach,
+                         "frac_of_hbm_peak": ach / HBM_PEAK_GBS if ach is not None else None,
+                         "counter_bytes": (tk.get(name) or {}).get("bytes_per_launch")}
+    dom = max(KERNELS, key=lambda k: kernels[k]["ms_avg"])
+    dk = kernels[dom]
+    call_bytes = sum(kb.values()) if nb else None
+    call_gbs = rate(call_bytes, ms_per_step)
+    probe_gbs = rate(nb["probe"] if nb else None, probe_ms)
+    probe_meas = tent.get("probe_bytes_per_window")
+    pair_gbs = rate(nb["pairs"] if nb else None, ms_per_step)
     out = {
         "metric": METRIC,
         "value": evals / (ms_per_step * 1e-3),
@@ -696,21 +875,24 @@ def main():
                    "n_inst": win.n_inst, "n_req": win.n_req, "seed": args.seed},
         "decisions_per_s": win.n_req / (ms_per_step * 1e-3),
         "step_ms_events": step_avg,
-        "kernel": "scoring pass: lean_rows_kernel (four requests per wave) + general score_kernel (prefix hits from the group records, latency model, filters, keys)",
-        "kernel_ms_avg": kern_avg,
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS if achieved is not None else None,
-                     "traffic": traffic},
-        "algorithmic_bytes_per_launch": alg_bytes,
-        "group_pass": {"kernels": "group_claim_kernel + group_kernel (walk of each shared "
-                                  "segment once per window)",
-                       "ms_avg": group_ms, "algorithmic_bytes": group_bytes,
-                       "achieved_GBs": rate(group_bytes, group_ms),
-                       "groups": int(len(np.unique(win.pre_off[win.pre_len >= GROUP_MIN]))),
-                       "timed_calls": n_timed},
+        "roofline": {"bound": "hbm", "achieved": dk["achieved_GBs"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": dk["frac_of_hbm_peak"], "traffic": dk["counter_bytes"],
+                     "kernel": dom},
+        "kernels": kernels,
+        "kernel_timed_calls": n_timed,
+        "call": {"algorithmic_bytes": call_bytes, "achieved_GBs": call_gbs,
+                 "frac_of_hbm_peak": call_gbs / HBM_PEAK_GBS if call_gbs is not None else None},
+        "per_pair_walk": {
+            "about": "bytes of walking every capacity-eligible request x instance pair with 64 B "
+                     "bucket probes (the scoring call does not: the prefix index and the group "
+                     "pass skip them), over the step's time",
+            "bytes": nb["pairs"] if nb else None, "GBs_over_step": pair_gbs,
+            "frac_of_hbm_peak": pair_gbs / HBM_PEAK_GBS if pair_gbs is not None else None},
+        "groups": {"groups": nb["groups"] if nb else None,
+                   "popular_groups": nb["popular_groups"] if nb else None},
         "probe_kernel": {"kernel": "ps_probe_hits_dev (every request x instance probed)",
-                         "ms_per_window": probe_ms, "probes": n_probes,
-                         "algorithmic_bytes": probe_alg_bytes,
+                         "ms_per_window": probe_ms, "probes": nb["probes"] if nb else None,
+                         "algorithmic_bytes": nb["probe"] if nb else None,
                          "achieved_GBs": probe_gbs,
                          "frac_of_hbm_peak": probe_gbs / HBM_PEAK_GBS if probe_gbs is not None else None,
                          "measured_bytes": probe_meas,
@@ -726,16 +908,18 @@ def main():
         "placed": int((res["instance"] >= 0).sum()),
         "fallback": int(((res["flags"] & ps.PS_R_FALLBACK) != 0).sum()),
     }
-    if args.sequential_reps > 0:
-        print("bench: per-arrival scheduling", file=sys.stderr, flush=True)
-        out["sequential"] = sequential_block(sc, win, m, d_pool, d_reqs, res,
+    n_seq = min(args.sequential_requests, win.n_req)
+    if n_seq > 0:
+        say(f"per-arrival scheduling of the first {n_seq} requests")
+        out["sequential"] = sequential_block(sc, win, m, d_pool, d_reqs, n_seq, res,
                                              args.sequential_reps, stream)
     sc.close()
     if not args.no_cpu_baseline:
-        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        say("timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(win, args.cpu_budget)
-        if args.sequential_reps > 0:
-            out["cpu_baseline"]["sequential"] = cpu_sequential_baseline(win, args.cpu_budget)
+        if n_seq > 0:
+            out["cpu_baseline"]["sequential"] = cpu_sequential_baseline(
+                win.subset(range(n_seq)), args.cpu_budget / 3)
     print(json.dumps(out), flush=True)
 
 
