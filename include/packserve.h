@@ -171,7 +171,13 @@ ps_status ps_create(int device, ps_ctx** out);
 ps_status ps_destroy(ps_ctx* ctx);
 
 /*
- * Replace the snapshot: build one open-addressing table per instance from the
+ * Replace the snapshot: what Algorithm 1 reads about the instance pool.  The
+ * cached block sets stand for each instance's local prefix tree (Sec. 7: the
+ * scheduler keeps a prefix tree per instance and asks it for the longest
+ * cached prefix); the counters D_i, Q_i, P_i, S_i are the scheduler-
+ * observable instance state and the model the configuration profile that
+ * Sec. 5.1 names as the latency model's inputs (Eqs. 4, 7, 8, 10).
+ * Builds one open-addressing table per instance from the
  * CSR block lists (buckets of 8 x 64-bit slots, at least 2 * table_cap_blocks
  * slots, a per-instance salted bucket index) and upload the load counters
  * and the model.  Synchronous.  PS_E_INVAL on a null pointer, a zero hash, a
@@ -180,6 +186,10 @@ ps_status ps_destroy(ps_ctx* ctx);
 ps_status ps_load_instances(ps_ctx* ctx, const ps_instances* inst, const ps_model* model);
 
 /*
+ * Algorithm 1 (Sec. 6) for every request of a window: its input is the
+ * request, the instance pool with its state, eta and tau; its output the
+ * chosen instance or Reject; here each request's result also carries the
+ * prefix hit and the predicted TTFT (Eq. 4) and TPOT (Eq. 10) of the choice.
  * Score a window held in host memory: copies pool[0, pool_len) and reqs to
  * the device, runs ps_score_window_dev on the context stream and copies the
  * n_req results back.  Synchronous.  Descriptors must lie inside the pool,
@@ -190,6 +200,12 @@ ps_status ps_score_window(ps_ctx* ctx, const uint64_t* pool, int64_t pool_len,
                           const ps_req* reqs, int32_t n_req, ps_result* out);
 
 /*
+ * Algorithm 1 (Sec. 6) for every request of a device-resident window, as
+ * ps_score_window.  d_sizes is an addition to the boundary Algorithm 1
+ * implies: the sizes of its candidate sets (capacity-eligible, after the
+ * recomputation filter of Eq. 9, after the TPOT filter) are what the
+ * parity tests check beside the decision, and a caller can read how many
+ * instances each filter kept.  Pass NULL to skip them (the faster path).
  * Score a device-resident window into d_out[n_req] (and, if d_sizes is not
  * NULL, |A|, |C|, |T| per request into d_sizes[3 * n_req]), asynchronously
  * on `hip_stream`.  Descriptors are checked by the kernel: a malformed one
@@ -302,6 +318,12 @@ ps_status ps_replay_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t pool
                                ps_result* d_out, int64_t* n_dropped, void* hip_stream);
 
 /*
+ * The request-path update of the instance state (Sec. 7: the scheduler's
+ * view of each instance, its counters and its prefix tree, is updated as
+ * requests are routed, with no round trip to the engine).  pool_len is an
+ * addition to the placements Algorithm 1 outputs: the chains are named by
+ * offsets into the caller's hash pool, and its length lets every
+ * descriptor be checked before any change.
  * Apply placements (host memory) in array order: entry k places request
  * reqs[k] on instance inst[k] (-1 = skip).  For each placed request, against
  * the table as left by the earlier entries: Q_i += 1, P_i += uncached tokens
