@@ -177,10 +177,10 @@ ps_status ps_destroy(ps_ctx* ctx);
  * cached prefix); the counters D_i, Q_i, P_i, S_i are the scheduler-
  * observable instance state and the model the configuration profile that
  * Sec. 5.1 names as the latency model's inputs (Eqs. 4, 7, 8, 10).
- * Builds one open-addressing table per instance from the
- * CSR block lists (buckets of 8 x 64-bit slots, at least 2 * table_cap_blocks
- * slots, a per-instance salted bucket index) and upload the load counters
- * and the model.  Synchronous.  PS_E_INVAL on a null pointer, a zero hash, a
+ * Builds one open-addressing table per instance from the CSR block lists
+ * (buckets of 8 x 64-bit slots, at least 2 * table_cap_blocks slots, a
+ * per-instance salted bucket index) and uploads the load counters and the
+ * model.  Synchronous.  PS_E_INVAL on a null pointer, a zero hash, a
  * malformed CSR or model; PS_E_RANGE when a limit above is exceeded.
  */
 ps_status ps_load_instances(ps_ctx* ctx, const ps_instances* inst, const ps_model* model);
