@@ -479,6 +479,18 @@ __device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, con
   return (uint32_t)ell;
 }
 
+// The model in LDS for the launch of a persistent kernel.  Read through the
+// device pointer, every field is a global load that the compiler repeats,
+// and waits for, after each store of the kernel's loop (the pointer may
+// alias them); the LDS copy is read with LDS loads.  Every lane of the
+// workgroup calls it; the copy is visible after the next barrier.
+__device__ __forceinline__ void stage_model(DevModel& dst, const DevModel* src, int tid,
+                                            int nthreads) {
+  static_assert(sizeof(DevModel) % 4 == 0, "the model is copied in 4-byte words");
+  for (int k = tid; k < (int)(sizeof(DevModel) / 4); k += nthreads)
+    reinterpret_cast<uint32_t*>(&dst)[k] = reinterpret_cast<const uint32_t*>(src)[k];
+}
+
 // ------------------------------------------------------------- latency model
 // Eq. 7 with the empirical C and C^2 terms: n new, c cached tokens.
 __device__ __forceinline__ float t_prefill(const DevModel& m, float n, float c) {

@@ -730,7 +730,7 @@ __host__ __device__ inline size_t score_lds_base(int32_t n_inst, bool hits_in_ld
 // selector, monotone model, no TTFT admission, no set sizes), so the
 // other policies' paths compile away.
 template <bool HITS_IN_LDS, bool SMALL, bool FAST>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void score_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void score_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
   const int32_t nw = (n_inst + 63) >> 6;
@@ -751,14 +751,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
-  const DevModel& m = *a.model;
+  if (a.defer_only && *a.defer_any == 0u) return;  // nothing was left to this kernel
+  __shared__ DevModel lmodel;
+  stage_model(lmodel, a.model, lane, 64);
+  __syncthreads();
+  const DevModel& m = lmodel;
   uint32_t* const sizes = FAST ? nullptr : a.sizes;
   const bool sel_hcq = !FAST && m.sel == PS_SEL_HCQ;
   const bool sel_random = !FAST && m.sel == PS_SEL_RANDOM;
   auto room_of = [&](uint32_t i) -> int64_t { return SMALL ? lroom[i] : a.room[i]; };
   auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
 
-  if (a.defer_only && *a.defer_any == 0u) return;  // nothing was left to this kernel
   for (int32_t w = lane; w < 3 * nw; w += 64) bmA[w] = 0ull;
   if (SMALL) {
     if (lane < n_inst) {
@@ -1410,7 +1413,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void sc
 // trip after the record.  Every other valid request is marked kDeferred
 // (and *a.defer_any set) for the general kernel that follows.
 template <bool SMALL>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void lean_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void lean_kernel(ScoreArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int32_t n_inst = a.n_inst;
   const int32_t nw = (n_inst + 63) >> 6;
@@ -1422,7 +1425,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);          // SMALL: thresholds
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
-  const DevModel& m = *a.model;
+  __shared__ DevModel lmodel;  // visible after the barrier below
+  stage_model(lmodel, a.model, lane, 64);
+  const DevModel& m = lmodel;
   for (int32_t w = lane; w < nw; w += 64) bmH[w] = 0ull;
   const TopRoom trm = a.rtop[lane];
   const int32_t n1 = (n_inst + 63) >> 6;
@@ -1693,7 +1698,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   const int lane = threadIdx.x;
   const int q = lane >> 4, t = lane & 15;
   const int g = lane >> 3, s = lane & 7;
-  const DevModel& m = *a.model;
+  __shared__ DevModel lmodel;  // read by every batch (visible after the barrier below)
+  stage_model(lmodel, a.model, lane, 64);
+  const DevModel& m = lmodel;
   uint64_t* bmH = bmall + (size_t)q * nwp;  // this row's request's holders
   for (int32_t w = lane; w < 4 * nwp; w += 64) bmall[w] = 0ull;
   // window constants in LDS (read again per request: registers are scarce)

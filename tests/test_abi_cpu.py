@@ -71,3 +71,16 @@ def test_no_device_reports_an_error(monkeypatch):
     with pytest.raises(ps.PackServeError) as e:
         ps.ps_create(0)
     assert e.value.code in (ps.binding.PS_E_DEVICE, ps.binding.PS_E_INVAL)
+
+
+def test_build_spill_report_parser():
+    """The build refuses kernels that spill vector registers: the report
+    parser picks each kernel's spill count out of the compiler's remarks."""
+    from paper_2609_33224_amd import build
+    txt = ("k.hip:1:1: remark: Function Name: kern_a [-Rpass-analysis=kernel-resource-usage]\n"
+           "k.hip:1:1: remark:     VGPRs: 128 [-Rpass-analysis=kernel-resource-usage]\n"
+           "k.hip:1:1: remark:     VGPRs Spill: 3 [-Rpass-analysis=kernel-resource-usage]\n"
+           "    1 | __global__ void kern_a() {\n"
+           "k.hip:9:1: remark: Function Name: kern_b [-Rpass-analysis=kernel-resource-usage]\n"
+           "k.hip:9:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]\n")
+    assert build.vgpr_spills(txt) == {"kern_a": 3, "kern_b": 0}
