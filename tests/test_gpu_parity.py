@@ -182,6 +182,22 @@ def test_edge_chain_lengths_around_stage(ps, scorer):
     _check_edge(ps, scorer, _edge(sets, chains), "stage")
 
 
+def test_edge_hits_beyond_u16_slots(ps, scorer):
+    """Hits above 65,533 blocks do not fit the scorer's 16-bit hit slots: the
+    slot keeps an overflow mark and the hit is walked again where it is
+    needed.  Chains of up to 70,000 blocks on instances holding 70,000,
+    66,000, 65,534, 65,535 and 10 of them (grouped and tail-only)."""
+    ch = chain_hashes(70000, base=31)
+    sets = [ch[:70000], ch[:66000], ch[:65534], ch[:65535], ch[:10]]
+    chains = [ch[:70000], ch[:65535], ch[:66001], ch[:65534], (ch[:30000], ch[30000:70000]),
+              (ch[:8], ch[8:66500])]
+    for eta in (0.5, 0.0):
+        res = _check_edge(ps, scorer, _edge(sets, chains, cap=70000, D=[5, 9, 1, 2, 0],
+                                            kv_cap_tokens=10**8), f"u16 overflow eta={eta}",
+                          eta=eta)
+    assert res["hit_blocks"].max() > 65533
+
+
 def test_edge_fully_cached_and_empty_chain(ps, scorer):
     ch = chain_hashes(40, base=5)
     sets = [ch, ch[:20], []]
