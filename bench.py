@@ -656,6 +656,16 @@ def sequential_block(sc, win, model, d_pool, d_reqs, n, snap, reps, stream):
         if k:
             times.append(dt)
     seq = ps.results_from_device(d_out)
+    n_spec, n_full = sc.schedule_stats()
+    # the same leading requests with every request scored in full by the
+    # one scheduler workgroup (no speculative batches), for comparison
+    n_off = min(n, 4096)
+    sc.set_schedule_speculation(0)
+    reload()
+    t0 = time.perf_counter()
+    sc.schedule_dev(d_pool, len(win.pool), d_reqs, n_off, d_out, None, stream)
+    off_s = time.perf_counter() - t0
+    sc.set_schedule_speculation(256)
     # The replay stops before the first placement that would take an
     # instance's queue past its 12-bit limit (snapshot herding can).
     n_rep, q = n, win.Q.astype(np.int64).copy()
@@ -681,11 +691,16 @@ def sequential_block(sc, win, model, d_pool, d_reqs, n, snap, reps, stream):
     per_seq = np.bincount(seq["instance"][seq["instance"] >= 0], minlength=win.n_inst)
     ms = float(np.mean(times)) * 1e3
     return {
-        "entry": "ps_schedule_window_dev: Algorithm 1 per arrival (hits pass, one-workgroup "
-                 "scheduler, rebuild of the derived data)",
+        "entry": "ps_schedule_window_dev: Algorithm 1 per arrival (batches of 256: hits pass, "
+                 "every request scored in parallel against the batch's starting state, then "
+                 "one workgroup checks each result against the instances placed on since, "
+                 "decides and commits in arrival order; rebuild of the derived data)",
         "requests": n, "of_window": win.n_req,
         "ms_per_call": ms, "decisions_per_s": n / (ms * 1e-3),
         "us_per_decision": ms * 1e3 / n, "reps": reps,
+        "decided_from_speculation": n_spec, "scored_in_full": n_full,
+        "without_speculation": {"requests": n_off, "ms_per_call": off_s * 1e3,
+                                "us_per_decision": off_s * 1e6 / max(n_off, 1)},
         "bound": "latency (each decision waits for the commit before it)",
         "placed": int((seq["instance"] >= 0).sum()),
         "fallback": int(((seq["flags"] & fb) != 0).sum()),

@@ -303,6 +303,31 @@ ps_status ps_schedule_window_dev(ps_ctx* ctx, const uint64_t* d_pool, int64_t po
 ps_status ps_set_schedule_budget(ps_ctx* ctx, int64_t bytes);
 
 /*
+ * Speculative batches of ps_schedule_window_dev (Algorithm 1 per request,
+ * Sec. 6, with the state moving along the request path, Sec. 7, as above;
+ * the results do not depend on this setting).  The requests are taken in
+ * batches of `batch`: every request of a batch is first scored in parallel
+ * against the state at the batch's start, keeping |A|, |C|, |T|, W_min and
+ * the first members of T and of C in key order; then, in arrival order, the
+ * instances that earlier requests of the batch were placed on are scored
+ * again against the current state, and when they cannot change W_min and
+ * the speculative lists show the least key, the request is decided from
+ * them; otherwise it is scored in full.  batch in [1, 256]; 0 scores every
+ * request in full (one workgroup, no speculation).  Default 256.  The
+ * Random and H-C-Q selectors are always scored in full.  PS_E_INVAL for a
+ * batch outside [0, 256].
+ */
+ps_status ps_set_schedule_speculation(ps_ctx* ctx, int32_t batch);
+
+/*
+ * Of the requests the last ps_schedule_window_dev call scored (every valid
+ * descriptor), how many were decided from their speculative result
+ * (*n_spec) and how many were scored in full (*n_full; both 0 without
+ * speculation).  Host pointers, either may be NULL.  Synchronous.
+ */
+ps_status ps_read_schedule_stats(ps_ctx* ctx, int64_t* n_spec, int64_t* n_full);
+
+/*
  * Replay given placements (device array d_inst[n_req], -1 = none) in array
  * order: for each placed request, d_out gets the instance, the hit, TTFT
  * and TPOT that instance offers at the request's arrival (the state left by

@@ -104,6 +104,8 @@ def load_library() -> ctypes.CDLL:
         "ps_schedule_window_dev": ([vp, vp, i64, vp, i32, vp, vp, ctypes.POINTER(i64), vp], i32),
         "ps_replay_window_dev": ([vp, vp, i64, vp, i32, vp, vp, ctypes.POINTER(i64), vp], i32),
         "ps_set_schedule_budget": ([vp, i64], i32),
+        "ps_set_schedule_speculation": ([vp, i32], i32),
+        "ps_read_schedule_stats": ([vp, ctypes.POINTER(i64), ctypes.POINTER(i64)], i32),
         "ps_read_state": ([vp, vp, vp, vp, vp, vp], i32),
         "ps_table_info": ([vp, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i32)], i32),
         "ps_last_error": ([vp], ctypes.c_char_p),
@@ -396,6 +398,16 @@ class Scorer:
 
     def set_schedule_budget(self, n_bytes: int) -> None:
         _check(self.ctx, load_library().ps_set_schedule_budget(self.ctx, int(n_bytes)))
+
+    def set_schedule_speculation(self, batch: int) -> None:
+        _check(self.ctx, load_library().ps_set_schedule_speculation(self.ctx, int(batch)))
+
+    def schedule_stats(self) -> tuple:
+        """(decided from speculation, scored in full) of the last schedule call."""
+        a, b = ctypes.c_int64(), ctypes.c_int64()
+        _check(self.ctx, load_library().ps_read_schedule_stats(self.ctx, ctypes.byref(a),
+                                                                ctypes.byref(b)))
+        return int(a.value), int(b.value)
 
     def replay_dev(self, d_pool, pool_len, d_reqs, n_req, d_inst, d_out, stream=None) -> int:
         return ps_replay_window_dev(self.ctx, d_pool, pool_len, d_reqs, n_req, d_inst, d_out, stream)

@@ -140,6 +140,11 @@ struct ps_ctx {
   uint32_t* d_seq_hits = nullptr;
   size_t seq_hits_cap = 0;  // elements
   size_t seq_budget = (size_t)256 << 20;  // bytes of hits per scheduler launch
+  // speculative batches (requests per batch; 0: every request scored in full)
+  int32_t spec_batch = kSpecBatch;
+  SpecRec* d_spec = nullptr;
+  int32_t spec_cap = 0;                          // records
+  unsigned long long* d_seq_stats = nullptr;     // decisions from speculation, scored in full
   // prefix groups of the scored windows: slot keys (tagged with a window
   // generation, so a new window needs no clearing), slot records, and each
   // request's slot
@@ -484,6 +489,8 @@ ps_status ps_destroy(ps_ctx* c) {
   for (int k = 0; k < 3; ++k)
     if (c->d_stage[k]) (void)hipFree(c->d_stage[k]);
   dfree(c->d_seq_hits);
+  dfree(c->d_spec);
+  dfree(c->d_seq_stats);
   dfree(c->d_gkeys);
   dfree(c->d_grec);
   dfree(c->d_gslot);
@@ -1193,8 +1200,24 @@ static ps_status run_sequential(ps_ctx* c, const uint64_t* d_pool, int64_t pool_
   }
   HIP_TRY(c, hipMemsetAsync(c->d_counter, 0, sizeof(unsigned long long), s));
   const int threads = kSeqMaxThreads;  // every step of a request uses the whole workgroup
-  for (int32_t r0 = 0; r0 < n_req; r0 += chunk) {
-    const int32_t r1 = std::min(n_req, r0 + chunk);
+  // Speculative batches: Algorithm 1 with a keyed selector (the Random and
+  // H-C-Q choices are not a least key, so they are always scored in full)
+  const uint32_t sel = c->h_model.sel;
+  const bool spec = !d_forced && c->spec_batch > 0 && sel != PS_SEL_RANDOM && sel != PS_SEL_HCQ;
+  int32_t step = chunk;
+  if (spec) {
+    step = std::min(chunk, c->spec_batch);
+    if (c->spec_cap < step) {
+      dfree(c->d_spec);
+      c->spec_cap = 0;
+      HIP_TRY(c, hipMalloc(&c->d_spec, (size_t)step * sizeof(SpecRec)));
+      c->spec_cap = step;
+    }
+  }
+  if (!c->d_seq_stats) HIP_TRY(c, hipMalloc(&c->d_seq_stats, 2 * sizeof(unsigned long long)));
+  HIP_TRY(c, hipMemsetAsync(c->d_seq_stats, 0, 2 * sizeof(unsigned long long), s));
+  for (int32_t r0 = 0; r0 < n_req; r0 += step) {
+    const int32_t r1 = std::min(n_req, r0 + step);
     ScoreArgs pa{};
     pa.t = c->t;
     pa.x = c->x;
@@ -1210,7 +1233,12 @@ static ps_status run_sequential(ps_ctx* c, const uint64_t* d_pool, int64_t pool_
     const int grid = std::min(r1 - r0, std::max(1, c->num_cus) * 32);
     HIP_TRY(c, ps_launch_score(pa, c->hits_in_lds, grid, true, s));
     SeqArgs q{c->t, c->d_inst, c->d_room, c->d_model, d_pool, pool_len, d_reqs, r0, r1, ni,
-              c->d_seq_hits, d_forced, d_out, d_sizes, (uint32_t)c->cap, c->d_counter};
+              c->d_seq_hits, d_forced, d_out, d_sizes, (uint32_t)c->cap, c->d_counter,
+              nullptr, c->d_seq_stats};
+    if (spec) {
+      HIP_TRY(c, ps_launch_spec(q, c->d_spec, s));
+      q.spec = c->d_spec;
+    }
     HIP_TRY(c, ps_launch_seq(q, threads, s));
   }
   return after_commit(c, s, n_dropped);
@@ -1220,6 +1248,26 @@ ps_status ps_set_schedule_budget(ps_ctx* c, int64_t bytes) {
   if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
   if (bytes < 0) return fail(c, PS_E_INVAL, "negative budget");
   c->seq_budget = bytes == 0 ? ((size_t)256 << 20) : (size_t)bytes;
+  return PS_OK;
+}
+
+ps_status ps_set_schedule_speculation(ps_ctx* c, int32_t batch) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  if (batch < 0 || batch > kSpecBatch)
+    return fail(c, PS_E_INVAL, "speculative batch %d outside [0, %d]", batch, kSpecBatch);
+  c->spec_batch = batch;
+  return PS_OK;
+}
+
+ps_status ps_read_schedule_stats(ps_ctx* c, int64_t* n_spec, int64_t* n_full) {
+  if (!c) return fail(nullptr, PS_E_INVAL, "ctx is NULL");
+  unsigned long long v[2] = {0, 0};
+  if (c->d_seq_stats) {
+    DeviceScope ds(c->device);
+    HIP_TRY(c, hipMemcpy(v, c->d_seq_stats, sizeof v, hipMemcpyDeviceToHost));
+  }
+  if (n_spec) *n_spec = (int64_t)v[0];
+  if (n_full) *n_full = (int64_t)v[1];
   return PS_OK;
 }
 

@@ -255,6 +255,35 @@ constexpr int kSeqU = 4;             // positions per thread in one sweep or ins
 constexpr uint32_t kExtMax = 128;    // hit extensions swept by the workgroup per request
 constexpr int kSeqB = 2;             // instances per thread whose loads are issued together
 
+// Speculative batches of the per-arrival scheduler.  Every request of a
+// batch is first scored in parallel (one workgroup each) against the state
+// at the batch's start; the scheduler workgroup then takes the batch in
+// order and, for each request, re-evaluates only the instances that earlier
+// requests of the batch were placed on (at most one per request, so at most
+// kSpecBatch): when the speculative result settles the decision against the
+// current state, the request is decided from it; otherwise it is scored in
+// full.  A speculative result keeps |A|, |C|, |T|, W_min and the first
+// members of T and of C in the order of their keys.
+constexpr int kSpecBatch = kSeqMaxThreads;  // requests per batch at most (one thread per changed instance)
+constexpr int kSpecList = 64;               // members of T (and of C) kept per request
+constexpr int kSpecTop = 4;                 // per-thread candidates gathered before the merge
+
+struct alignas(16) SpecEntry {
+  uint64_t key;  // the selector's key (T) or the fallback key (C); the id in bits 0..15
+  uint32_t w;    // the candidate's recomputation penalty W (fp32 bits)
+  uint32_t pad;
+};
+
+struct alignas(16) SpecRec {
+  uint32_t nA, nC, nT;
+  uint32_t wmin;       // W_min over A (fp32 bits)
+  uint32_t nLT, nLF;   // entries of lt and lf: the first nLT members of T by key (all of T
+                       // when nLT == nT), the first nLF members of C by fallback key
+  uint32_t pad[2];
+  SpecEntry lt[kSpecList];
+  SpecEntry lf[kSpecList];
+};
+
 struct SeqArgs {
   Tables t;
   InstState* inst;
@@ -271,6 +300,8 @@ struct SeqArgs {
   uint32_t* sizes;         // optional |A|,|C|,|T| (Algorithm 1 only)
   uint32_t cap;            // distinct keys allowed per instance
   unsigned long long* dropped;
+  const SpecRec* spec;     // speculative results of requests [r0, r1) (null: none)
+  unsigned long long* stats;  // [0] += decisions taken from them, [1] += decisions scored in full
 };
 
 struct BuildArgs {
@@ -329,6 +360,9 @@ hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s, hipE
 // Per-arrival scheduler: one workgroup of `threads` (a multiple of 64, at
 // most kSeqMaxThreads) over requests [a.r0, a.r1).
 hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);
+// Speculative scoring of requests [a.r0, a.r1) (one workgroup each) into
+// out[r - a.r0]; a.hits holds their hits at the current state.
+hipError_t ps_launch_spec(const ps::SeqArgs& a, ps::SpecRec* out, hipStream_t s);
 size_t ps_seq_lds_bytes(int32_t n_inst);
 size_t ps_score_lds_bytes(int32_t n_inst);
 // Pools small enough for the scoring kernel to keep rooms, states and

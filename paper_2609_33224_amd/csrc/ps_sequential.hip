@@ -13,19 +13,68 @@ struct SeqPart {
   uint32_t hroom, nC, nT, wmin, nA, pad;
 };
 
+// One wave's share of the check of a speculative result (below).
+struct FastPart {
+  uint64_t keyT, keyF;  // least selector / fallback key over the changed instances in T / C
+  uint32_t conf;        // a changed instance now holds the block where the hit stopped
+  uint32_t wb, wc;      // least W over the changed instances eligible then / now
+  uint32_t eb, ec;      // changed instances eligible then / now
+  uint32_t cb, cc;      // ... in C then / now
+  uint32_t tb, tc;      // ... in T then / now
+  uint32_t pad;
+};
+
 // Workgroup LDS of the scheduler (a fixed layout, plus the dirty bitmap).
 struct SeqShared {
   uint64_t stage[kSeqStage];          // the request's chain head
   SeqPart part[2][kSeqWaves];         // reduction partials (alternating)
+  FastPart fp[kSeqWaves];
   uint32_t cnt[kSeqU][kSeqWaves];     // per-wave counts of one insert step
   uint32_t ext[kExtMax][2];           // hit extensions: instance, first unknown position
   uint32_t ring[3];                   // first-absent minima of the sweeps
   uint32_t n_ext, hit, pick, count;
   int64_t rp;                         // row position found by a run walk's probe
+  // instances placed on in this launch (the dirty ones), in order, with
+  // their state at the launch's start
+  uint32_t n_u;
+  uint32_t n_fast, n_full;            // decisions from speculation / scored in full
+  uint32_t u_id[kSpecBatch];
+  InstState u_old[kSpecBatch];
 };
 
 __device__ __forceinline__ uint64_t seq_key(const SeqShared& sh, const ChainRef& c, int32_t j) {
   return j < kSeqStage ? sh.stage[j] : chain_global(c, j);
+}
+
+// The request's chain head into LDS, eight loads in flight per thread.
+// Visible after the next barrier.
+__device__ __forceinline__ void stage_chain(SeqShared& sh, const ChainRef& c, int tid, int NT) {
+  const int32_t nst = c.len < kSeqStage ? c.len : kSeqStage;
+  for (int32_t j0 = 0; j0 < nst; j0 += 8 * NT) {
+    uint64_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int32_t j = j0 + u * NT + tid;
+      v[u] = j < nst ? chain_global(c, j) : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int32_t j = j0 + u * NT + tid;
+      if (j < nst) sh.stage[j] = v[u];
+    }
+  }
+}
+
+// Key of the first of the n listed entries whose instance is not marked in
+// `dirty`, or ~0 when there is none (every lane of the wave gets it).  Lane
+// l holds the key of entry l (the lists have at most 64 entries).
+__device__ __forceinline__ uint64_t spec_first_outside(uint64_t k, uint32_t n,
+                                                       const uint64_t* dirty, int lane) {
+  static_assert(kSpecList == 64, "one list entry per lane");
+  const bool out = (uint32_t)lane < n && !test_bit(dirty, (uint32_t)(k & 0xFFFFu));
+  const uint64_t bm = __ballot(out);
+  if (bm == 0ull) return ~0ull;
+  return (uint64_t)lane_value64((int64_t)k, __builtin_ctzll(bm));
 }
 
 // First position at or after `pos` whose block instance i does not hold,
@@ -190,6 +239,7 @@ __global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
   ScoreArgs sa{};
   sa.inst = a.inst;
   for (int32_t w = tid; w < nw; w += NT) dirty[w] = 0ull;
+  if (tid == 0) sh.n_u = sh.n_fast = sh.n_full = 0u;
   unsigned long long drop = 0;
   int pb = 0;  // partial buffer of the next reduction (alternates)
   ps_req qn = a.reqs[a.r0];
@@ -219,8 +269,142 @@ __global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
     uint32_t* H = a.hits + (size_t)(r - a.r0) * (size_t)n_inst;
     const int32_t forced = replay ? a.forced[r] : -1;
 
+    int32_t best = -1;
+    uint32_t fl = PS_R_REJECT, nA = 0, nC = 0, nT = 0;
+    const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
+    const float tpf_cold = t_prefill(m, Lf, 0.0f);
+    const float slo = fmaxf(m.ttft_floor, tpf_cold);
+    const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+    bool staged = false, fast = false;
+
+    // (0) the speculative result: scored against the launch's starting
+    // state, it still decides the request unless an instance placed on
+    // since then (the set U) changes W_min or the choice
+    if (a.spec != nullptr && !replay) {
+      const SpecRec& sp = a.spec[r - a.r0];
+      stage_chain(sh, c, tid, NT);  // the commit reads it
+      const uint64_t lt_key = sp.lt[lane].key;  // read before n is known
+      staged = true;
+      const uint32_t n_u = sh.n_u;
+      const uint32_t wmin_b = sp.wmin;
+      const float wmin = __uint_as_float(wmin_b);
+      FastPart f{~0ull, ~0ull, 0u, ~0u, ~0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+      for (uint32_t k = (uint32_t)tid; k < n_u; k += (uint32_t)NT) {
+        const uint32_t u = sh.u_id[k];
+        const InstState so = sh.u_old[k];  // as the speculative scoring saw it
+        const InstState sc = a.inst[u];    // now
+        const uint32_t h = H[u];           // its hit then
+        const bool eb = eligible(m, so.A1, so.S, L), ec = eligible(m, sc.A1, sc.S, L);
+        // the hit still stops at h unless u has taken the block at h since
+        if (ec && (int32_t)h < ell && probe(a.t, u, chain_global(c, (int32_t)h))) f.conf = 1u;
+        const uint32_t wb = __float_as_uint(fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)h * m.bs), Lf)));
+        const bool cpass = !kvc || (__uint_as_float(wb) - wmin) / Z <= m.eta;
+        if (eb) {
+          f.eb += 1u;
+          f.wb = wb < f.wb ? wb : f.wb;
+          if (cpass) {
+            f.cb += 1u;
+            if (a.sizes)
+              f.tb += member_with(m, [&]() { return so; }, h, L, Lf, wmin, Z, kvc, slo).inT ? 1u : 0u;
+          }
+        }
+        if (ec) {
+          f.ec += 1u;
+          f.wc = wb < f.wc ? wb : f.wc;
+          const Member mb = member_with(m, [&]() { return sc; }, h, L, Lf, wmin, Z, kvc, slo);
+          if (mb.inC) {
+            f.cc += 1u;
+            const uint64_t lm = (uint64_t)(mb.st.P + mb.n_tok) * (uint64_t)mb.st.A1;
+            const uint64_t kf = (m.flags & PS_F_FALLBACK_DCQ) ? dcq_key(mb.st, h, u) : ((lm << 16) | u);
+            f.keyF = kf < f.keyF ? kf : f.keyF;
+            if (mb.inT) {
+              f.tc += 1u;
+              const uint64_t kt = select_key(m.sel, mb.st, h, u, lm);
+              f.keyT = kt < f.keyT ? kt : f.keyT;
+            }
+          }
+        }
+      }
+      {
+        FastPart w;
+        w.keyT = wave_min_u64(f.keyT);
+        w.keyF = wave_min_u64(f.keyF);
+        w.conf = __ballot(f.conf != 0u) ? 1u : 0u;
+        w.wb = wave_min_u32(f.wb);
+        w.wc = wave_min_u32(f.wc);
+        w.eb = wave_sum_u32(f.eb);
+        w.ec = wave_sum_u32(f.ec);
+        w.cb = wave_sum_u32(f.cb);
+        w.cc = wave_sum_u32(f.cc);
+        w.tb = wave_sum_u32(f.tb);
+        w.tc = wave_sum_u32(f.tc);
+        w.pad = 0u;
+        if (lane == 0) sh.fp[wv] = w;
+      }
+      __syncthreads();
+      FastPart g = sh.fp[0];
+      for (int k = 1; k < nwv; ++k) {
+        const FastPart& p = sh.fp[k];
+        g.keyT = p.keyT < g.keyT ? p.keyT : g.keyT;
+        g.keyF = p.keyF < g.keyF ? p.keyF : g.keyF;
+        g.conf |= p.conf;
+        g.wb = p.wb < g.wb ? p.wb : g.wb;
+        g.wc = p.wc < g.wc ? p.wc : g.wc;
+        g.eb += p.eb;
+        g.ec += p.ec;
+        g.cb += p.cb;
+        g.cc += p.cc;
+        g.tb += p.tb;
+        g.tc += p.tc;
+      }
+      const uint32_t nA_now = sp.nA - g.eb + g.ec;
+      // W_min is unchanged unless a hit moved (conf) or the only changed
+      // instances at the minimum all left A: then it is not known here
+      bool ok = g.conf == 0u && !(g.wb == wmin_b && g.wc != wmin_b) && g.wc >= wmin_b;
+      if (ok && nA_now > 0u) {
+        // the other members of T and C are as speculated; the first listed
+        // one outside U is the least of them when the list shows it
+        const uint64_t t0 = spec_first_outside(lt_key, sp.nLT, dirty, lane);
+        if (t0 == ~0ull && sp.nLT < sp.nT) {
+          ok = false;
+        } else {
+          const uint64_t kT = t0 < g.keyT ? t0 : g.keyT;
+          if (kT != ~0ull) {
+            best = (int32_t)(kT & 0xFFFFu);
+            fl = 0;
+          } else {
+            const uint64_t f0 = spec_first_outside(sp.lf[lane].key, sp.nLF, dirty, lane);
+            if (f0 == ~0ull && sp.nLF < sp.nC) {
+              ok = false;
+            } else {
+              const uint64_t kF = f0 < g.keyF ? f0 : g.keyF;
+              if (kF != ~0ull) {
+                best = (int32_t)(kF & 0xFFFFu);
+                fl = PS_R_FALLBACK;
+              }
+            }
+          }
+        }
+      }
+      if (ok) {
+        fast = true;
+        nA = nA_now;
+        if (nA_now > 0u) {
+          nC = sp.nC - g.cb + g.cc;
+          nT = sp.nT - g.tb + g.tc;
+        }
+      } else {
+        best = -1;
+        fl = PS_R_REJECT;
+      }
+      if (tid == 0) {
+        if (fast) sh.n_fast += 1u;
+        else sh.n_full += 1u;
+      }
+    }
+
+    if (!fast) {
     // (1) capacity guard
-    uint32_t nA = 0;
     if (!replay && L <= room_ub) {
       uint32_t al = 0;
       uint64_t rl = ~0ull;  // ~(room + 1), minimised (room >= -1)
@@ -256,27 +440,9 @@ __global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
       room_ub = (int64_t)(~rmin - 1ull);
     }
     const bool work = replay ? forced >= 0 : nA > 0;
-    int32_t best = -1;
-    uint32_t fl = PS_R_REJECT, nC = 0, nT = 0;
-    const float Z = recompute_raw(m, Lf, Lf);  // T_pf(L, 0) - T_pf(0, L)
-    const float tpf_cold = t_prefill(m, Lf, 0.0f);
-    const float slo = fmaxf(m.ttft_floor, tpf_cold);
     if (work) {
       // (2) live hits
-      const int32_t nst = ell < kSeqStage ? ell : kSeqStage;
-      for (int32_t j0 = 0; j0 < nst; j0 += 8 * NT) {  // eight loads in flight per thread
-        uint64_t v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int32_t j = j0 + u * NT + tid;
-          v[u] = j < nst ? chain_global(c, j) : 0ull;
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int32_t j = j0 + u * NT + tid;
-          if (j < nst) sh.stage[j] = v[u];
-        }
-      }
+      if (!staged) stage_chain(sh, c, tid, NT);
       if (tid == 0) sh.n_ext = 0u;
       __syncthreads();
       for (int32_t base = 0; base < n_inst; base += kSeqB * NT) {
@@ -374,7 +540,6 @@ __global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
         }
         pb ^= 1;
         const float wmin = __uint_as_float(wmin_bits);
-        const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
 
         // (3b) filters and keys
         Acc acc{~0ull, ~0ull, ~0u, 0u, 0u};
@@ -485,12 +650,18 @@ __global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
         }
       }
     }
+    }  // !fast
 
     // (4) result and commit
     if (best >= 0 && best % NT == tid) {
       const uint32_t v = H[best];
       const int64_t c_tok = (int64_t)v * m.bs;
       InstState st = a.inst[best];
+      if (!test_bit(dirty, (uint32_t)best) && sh.n_u < (uint32_t)kSpecBatch) {
+        sh.u_id[sh.n_u] = (uint32_t)best;  // first placement on it in this launch
+        sh.u_old[sh.n_u] = st;
+        sh.n_u += 1u;
+      }
       const Lat lt = latency(m, st, (float)(L - c_tok), (float)c_tok, L);
       if (lt.ttft > slo) fl |= PS_R_TTFT_MISS;
       a.out[r] = ps_result{best, (int32_t)v, lt.ttft, lt.tpot, fl};
@@ -678,9 +849,239 @@ __global__ __launch_bounds__(kSeqMaxThreads) void seq_kernel(SeqArgs a) {
     }
   }
   if (tid == 0 && drop) atomicAdd(a.dropped, drop);
+  if (tid == 0 && a.stats && (sh.n_fast | sh.n_full)) {
+    atomicAdd(a.stats, (unsigned long long)sh.n_fast);
+    atomicAdd(a.stats + 1, (unsigned long long)sh.n_full);
+  }
+}
+
+// ------------------------------------------------ speculative batch scoring
+// The kSpecTop least keys a thread has seen, ascending (keys are distinct:
+// each ends in its instance id).
+struct SpecTop {
+  uint64_t k[kSpecTop];
+  uint32_t w[kSpecTop];
+};
+
+__device__ __forceinline__ void spec_push(SpecTop& t, uint64_t key, uint32_t w) {
+  if (!(key < t.k[kSpecTop - 1])) return;
+  t.k[kSpecTop - 1] = key;
+  t.w[kSpecTop - 1] = w;
+#pragma unroll
+  for (int j = kSpecTop - 1; j > 0; --j) {
+    if (t.k[j] < t.k[j - 1]) {
+      const uint64_t x = t.k[j];
+      t.k[j] = t.k[j - 1];
+      t.k[j - 1] = x;
+      const uint32_t y = t.w[j];
+      t.w[j] = t.w[j - 1];
+      t.w[j - 1] = y;
+    }
+  }
+}
+
+struct SpecShared {
+  uint64_t tk[kSpecTop][kSeqMaxThreads];  // each thread's candidates of T, then of C
+  uint64_t fk[kSpecTop][kSeqMaxThreads];
+  uint32_t tw[kSpecTop][kSeqMaxThreads];
+  uint32_t fw[kSpecTop][kSeqMaxThreads];
+  uint64_t red[2][2][kSeqWaves];          // per-wave minima of a merge round (alternating)
+  uint32_t cnt[4][kSeqWaves];             // |A|, W_min, |C|, |T| partials
+  uint32_t stop[2][2];                    // [round parity][list]: a thread that kept only part
+                                          // of its members ran out (read in the next round)
+};
+
+// One workgroup per request of a batch: Algorithm 1's sets against the
+// state at the batch's start (hits from the batch's hits pass), exactly as
+// the scheduler evaluates them (same device functions, same fp32 values),
+// without a decision: |A|, |C|, |T|, W_min and the first kSpecList members
+// of T by the selector's key and of C by the fallback key.  Each thread
+// keeps its kSpecTop least keys; the merge takes the least head over the
+// threads, one per round, and stops after taking the last kept key of a
+// thread that saw more members than it kept (its next member is unknown),
+// so every list is the exact start of the ordered set.  Keyed selectors
+// only (not Random, not H-C-Q).
+__global__ __launch_bounds__(kSeqMaxThreads) void spec_kernel(SeqArgs a, SpecRec* out) {
+  __shared__ SpecShared sh;
+  const int tid = threadIdx.x, NT = blockDim.x;
+  const int lane = tid & 63, wv = tid >> 6, nwv = NT >> 6;
+  const int32_t n_inst = a.n_inst;
+  const int32_t r = a.r0 + (int32_t)blockIdx.x;
+  const ps_req q = a.reqs[r];
+  if (!req_valid(q, a.pool_len)) return;  // the scheduler rejects it without a look here
+  const DevModel& m = *a.model;
+  const int64_t L = ((int64_t)q.pre_len + q.tail_len) * m.bs;
+  const float Lf = (float)L;
+  const float Z = recompute_raw(m, Lf, Lf);
+  const float slo = fmaxf(m.ttft_floor, t_prefill(m, Lf, 0.0f));
+  const bool kvc = !(m.flags & PS_F_NO_KVC_FILTER) && Z > 0.0f;
+  const uint32_t* H = a.hits + (size_t)blockIdx.x * (size_t)n_inst;
+  SpecRec* o = out + blockIdx.x;
+
+  // |A| and W_min
+  uint32_t al = 0, wl = 0x7F800000u;
+  for (int32_t base = 0; base < n_inst; base += kSeqB * NT) {
+    InstState st[kSeqB];
+    uint32_t hv[kSeqB];
+#pragma unroll
+    for (int u = 0; u < kSeqB; ++u) {
+      const int32_t i = base + u * NT + tid;
+      if (i < n_inst) {
+        st[u] = a.inst[i];
+        hv[u] = H[i];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kSeqB; ++u) {
+      if (base + u * NT + tid >= n_inst || !eligible(m, st[u].A1, st[u].S, L)) continue;
+      ++al;
+      const uint32_t wb =
+          __float_as_uint(fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)hv[u] * m.bs), Lf)));
+      wl = wb < wl ? wb : wl;
+    }
+  }
+  al = wave_sum_u32(al);
+  wl = wave_min_u32(wl);
+  if (lane == 0) {
+    sh.cnt[0][wv] = al;
+    sh.cnt[1][wv] = wl;
+  }
+  if (tid < 4) sh.stop[tid >> 1][tid & 1] = 0u;
+  __syncthreads();
+  uint32_t nA = 0, wmin_bits = 0x7F800000u;
+  for (int k = 0; k < nwv; ++k) {
+    nA += sh.cnt[0][k];
+    wmin_bits = sh.cnt[1][k] < wmin_bits ? sh.cnt[1][k] : wmin_bits;
+  }
+  const float wmin = __uint_as_float(wmin_bits);
+
+  // members of C and T with their keys
+  SpecTop tt, ff;
+#pragma unroll
+  for (int j = 0; j < kSpecTop; ++j) {
+    tt.k[j] = ff.k[j] = ~0ull;
+    tt.w[j] = ff.w[j] = 0u;
+  }
+  uint32_t cC = 0, cT = 0;
+  if (nA > 0) {
+    for (int32_t base = 0; base < n_inst; base += kSeqB * NT) {
+      InstState st[kSeqB];
+      uint32_t hv[kSeqB];
+#pragma unroll
+      for (int u = 0; u < kSeqB; ++u) {
+        const int32_t i = base + u * NT + tid;
+        if (i < n_inst) {
+          st[u] = a.inst[i];
+          hv[u] = H[i];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kSeqB; ++u) {
+        const int32_t i = base + u * NT + tid;
+        if (i >= n_inst || !eligible(m, st[u].A1, st[u].S, L)) continue;
+        const InstState su = st[u];
+        const Member mb = member_with(m, [&]() { return su; }, hv[u], L, Lf, wmin, Z, kvc, slo);
+        if (!mb.inC) continue;
+        const uint32_t wb =
+            __float_as_uint(fmaxf(0.0f, recompute_raw(m, (float)(L - (int64_t)hv[u] * m.bs), Lf)));
+        ++cC;
+        const uint64_t lm = (uint64_t)(mb.st.P + mb.n_tok) * (uint64_t)mb.st.A1;
+        const uint64_t kf =
+            (m.flags & PS_F_FALLBACK_DCQ) ? dcq_key(mb.st, hv[u], (uint32_t)i) : ((lm << 16) | (uint32_t)i);
+        spec_push(ff, kf, wb);
+        if (!mb.inT) continue;
+        ++cT;
+        spec_push(tt, select_key(m.sel, mb.st, hv[u], (uint32_t)i, lm), wb);
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kSpecTop; ++j) {
+    sh.tk[j][tid] = tt.k[j];
+    sh.tw[j][tid] = tt.w[j];
+    sh.fk[j][tid] = ff.k[j];
+    sh.fw[j][tid] = ff.w[j];
+  }
+  {
+    const uint32_t sc = wave_sum_u32(cC), st = wave_sum_u32(cT);
+    if (lane == 0) {
+      sh.cnt[2][wv] = sc;
+      sh.cnt[3][wv] = st;
+    }
+  }
+  __syncthreads();
+  uint32_t nC = 0, nT = 0;
+  for (int k = 0; k < nwv; ++k) {
+    nC += sh.cnt[2][k];
+    nT += sh.cnt[3][k];
+  }
+
+  // merge: the least heads, one per round
+  const int lenT = cT < (uint32_t)kSpecTop ? (int)cT : kSpecTop;
+  const int lenF = cC < (uint32_t)kSpecTop ? (int)cC : kSpecTop;
+  const bool cutT = cT > (uint32_t)kSpecTop, cutF = cC > (uint32_t)kSpecTop;
+  int pT = 0, pF = 0, pb = 0;
+  uint32_t nLT = 0, nLF = 0;
+  bool doneT = nT == 0u, doneF = nC == 0u;
+  for (int round = 0; round < kSpecList && !(doneT && doneF); ++round) {
+    const uint64_t hT = (!doneT && pT < lenT) ? sh.tk[pT][tid] : ~0ull;
+    const uint64_t hF = (!doneF && pF < lenF) ? sh.fk[pF][tid] : ~0ull;
+    const uint64_t mT = wave_min_u64(hT), mF = wave_min_u64(hF);
+    if (lane == 0) {
+      sh.red[pb][0][wv] = mT;
+      sh.red[pb][1][wv] = mF;
+    }
+    __syncthreads();
+    uint64_t gT = ~0ull, gF = ~0ull;
+    for (int k = 0; k < nwv; ++k) {
+      gT = sh.red[pb][0][k] < gT ? sh.red[pb][0][k] : gT;
+      gF = sh.red[pb][1][k] < gF ? sh.red[pb][1][k] : gF;
+    }
+    pb ^= 1;
+    // written in the previous round (each round writes the slot the next
+    // one reads, after a barrier that every reader of the slot has passed)
+    if (sh.stop[round & 1][0]) doneT = true;
+    if (sh.stop[round & 1][1]) doneF = true;
+    if (!doneT) {
+      if (gT == ~0ull) {
+        doneT = true;
+      } else {
+        if (hT == gT) {
+          o->lt[nLT] = SpecEntry{gT, sh.tw[pT][tid], 0u};
+          if (++pT == lenT && cutT) sh.stop[(round + 1) & 1][0] = 1u;
+        }
+        ++nLT;
+      }
+    }
+    if (!doneF) {
+      if (gF == ~0ull) {
+        doneF = true;
+      } else {
+        if (hF == gF) {
+          o->lf[nLF] = SpecEntry{gF, sh.fw[pF][tid], 0u};
+          if (++pF == lenF && cutF) sh.stop[(round + 1) & 1][1] = 1u;
+        }
+        ++nLF;
+      }
+    }
+  }
+  if (tid == 0) {
+    o->nA = nA;
+    o->nC = nC;
+    o->nT = nT;
+    o->wmin = wmin_bits;
+    o->nLT = nLT;
+    o->nLF = nLF;
+  }
 }
 
 }  // namespace
+
+hipError_t ps_launch_spec(const SeqArgs& a, SpecRec* out, hipStream_t s) {
+  if (a.r1 <= a.r0) return hipSuccess;
+  hipLaunchKernelGGL(spec_kernel, dim3(a.r1 - a.r0), dim3(kSeqMaxThreads), 0, s, a, out);
+  return hipGetLastError();
+}
 
 size_t ps_seq_lds_bytes(int32_t n_inst) {
   const size_t nw = ((size_t)n_inst + 63) / 64;

@@ -251,3 +251,117 @@ def test_schedule_invalid_descriptor_and_errors(ps, scorer):
     with pytest.raises(ps.PackServeError) as e:
         scorer.schedule_dev(d_pool, len(w.pool), d_reqs, 16, d_out)
     assert e.value.code == ps.binding.PS_E_RANGE
+
+
+# ------------------------------------------------------------ speculative batches
+def _schedule_spec_and_full(ps, scorer, w, batch, **policy):
+    """The window scheduled from the same loaded state with every request
+    scored in full, then with speculative batches of `batch`: both runs'
+    (results, sizes, dropped, final state, stats)."""
+    runs = []
+    for b in (0, batch):
+        load_window(scorer, w, **policy)
+        scorer.set_schedule_speculation(b)
+        res, sizes, dropped = DeviceWindow(w).schedule(scorer)
+        runs.append((res, sizes, dropped, scorer.state(), scorer.schedule_stats()))
+    scorer.set_schedule_speculation(256)
+    return runs
+
+
+def _assert_same_schedule(runs, n_valid, label):
+    (r0, s0, d0, st0, (f0, g0)), (r1, s1, d1, st1, (f1, g1)) = runs
+    bad = np.nonzero(r0 != r1)[0]
+    assert len(bad) == 0, f"{label}: {len(bad)} results differ, first request {bad[0]}"
+    assert (s0 == s1).all(), f"{label}: set sizes differ at {np.nonzero((s0 != s1).any(1))[0][:5]}"
+    assert d0 == d1, f"{label}: dropped {d0} vs {d1}"
+    for k in st0:
+        assert (st0[k] == st1[k]).all(), f"{label}: final {k} differs"
+    assert (f0, g0) == (0, 0), f"{label}: without speculation the counts are {f0}, {g0}"
+    assert f1 + g1 == n_valid, f"{label}: {f1} + {g1} decisions of {n_valid}"
+    _say(f"{label}: identical; {f1} of {n_valid} decided from speculation")
+    return f1
+
+
+SPEC_WINDOWS = [("c1", {}, {}), ("c1", {}, dict(tpot_slo=0.030, b_max=96)),
+                ("c2", dict(n_req=4096), {}), ("c2_50", dict(n_req=4096), {}),
+                ("c3", dict(n_req=65536), {}), ("c4", dict(n_req=32768), {}),
+                ("c5", dict(n_req=262144), {})]
+
+
+@pytest.mark.parametrize("name,gen,policy", SPEC_WINDOWS)
+def test_speculation_matches_full_scoring(ps, scorer, name, gen, policy):
+    """Speculative batches decide exactly as scoring every request in full:
+    results, set sizes, refused blocks and the final state byte for byte;
+    most requests are decided from their speculative result."""
+    w = synth.generate(name, **gen)
+    if w.n_req > 4096:
+        w = w.subset(range(2048))
+    runs = _schedule_spec_and_full(ps, scorer, w, 256, **policy)
+    n_spec = _assert_same_schedule(runs, w.n_req, f"{name} {policy}")
+    assert n_spec > w.n_req // 2
+
+
+@pytest.mark.parametrize("batch", [1, 2, 7, 64, 255])
+def test_speculation_batch_sizes(ps, scorer, batch):
+    w = synth.generate("c2", n_req=1500)
+    _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, batch), w.n_req, f"batch {batch}")
+
+
+def test_speculation_selectors_and_layers(ps, scorer):
+    """Every keyed selector (Random and H-C-Q are always scored in full)
+    with every admission layer, TTFT admission and the D-C-Q fallback."""
+    w = synth.generate("c3", n_inst=128, n_sess=256, n_req=512)
+    for k, sel in enumerate(SELECTORS):
+        for layer, fl in list(LAYERS.items()) + [("F+TTFT", 1), ("F+DCQfb", 8 | 1)]:
+            pol = dict(flags=fl | (k << 8), rand_seed=7654321 + k)
+            runs = _schedule_spec_and_full(ps, scorer, w, 256, **pol)
+            keyed = sel not in ("RANDOM", "HCQ")
+            _assert_same_schedule(runs, w.n_req if keyed else 0, f"{sel} {layer}")
+
+
+def test_speculation_edge_windows(ps, scorer):
+    """Hit extensions inside a batch (sessions that follow their blocks),
+    repeats and holes, Z = 0, the table cap, small and odd pool sizes."""
+    rng = np.random.default_rng(3)
+    sess = [chain_hashes(int(n), base=10**7 * (k + 1)) for k, n in
+            enumerate(rng.integers(50, 1500, 12))]
+    chains = []
+    for step in range(6):
+        for s in sess:
+            k = min(len(s), 40 + step * 250)
+            chains.append((s[:k // 2], s[k // 2:k]) if step % 2 else s[:k])
+    sets = [sess[k % 12][:int(rng.integers(0, 30))] for k in range(20)]
+    for batch in (256, 5):
+        w = edge_window(sets, chains, cap=4000, eta=0.2)
+        _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, batch, eta=0.2), w.n_req,
+                              f"sessions batch {batch}")
+    ch = chain_hashes(200, base=3)
+    other = chain_hashes(50, base=7 * 10**6)
+    sets = [ch[:50] + ch[:50] + other, ch[1:150], ch[:10] + ch[11:200], ch[:100][::-1]]
+    chains = [ch, ch[:120], other, [], ch[:1], ch + ch[:5], other + other] * 3
+    w = edge_window(sets, chains, cap=600)
+    _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, 256), w.n_req, "dups/holes")
+    w.alpha = np.float32([0.02, 0.0, 1e-6, 0.0, 0.0, 0.0])  # Z = 0: all of A is kept
+    for eta in (0.0, 0.3):
+        _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, 256, eta=eta), w.n_req,
+                              f"Z=0 eta={eta}")
+    w = synth.generate("c1", n_req=1024, cap=1100)
+    _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, 256), w.n_req, "cap 1100")
+    for n_inst in (1, 63, 65, 257, 2100):
+        ch = chain_hashes(300, base=17)
+        rng = np.random.default_rng(n_inst)
+        sets = [ch[:int(rng.integers(0, 300))] for _ in range(n_inst)]
+        chains = [ch[:k] for k in (1, 2, 65, 150, 300, 299, 40)] * 20
+        for b_max in (512, 40):
+            w = edge_window(sets, chains, b_max=b_max, cap=400)
+            _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, 256, b_max=b_max),
+                                  w.n_req, f"n_inst={n_inst} b_max={b_max}")
+
+
+def test_speculation_setting_errors(ps, scorer):
+    for bad in (-1, 257, 10**6):
+        with pytest.raises(ps.PackServeError) as e:
+            scorer.set_schedule_speculation(bad)
+        assert e.value.code == ps.binding.PS_E_INVAL
+    scorer.set_schedule_speculation(0)
+    scorer.set_schedule_speculation(256)
