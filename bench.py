@@ -36,6 +36,7 @@ METRIC = ("request×instance candidate evals/sec + decisions/sec; "
           "probe-kernel % of HBM peak")
 HBM_PEAK_GBS = 8000.0
 BUCKET_BYTES = 64  # one 8-slot bucket of a per-instance table
+POP_WORDS = 64  # the popular pass takes pools of at most 64 x 64 instances
 PROBE_ROWPOS = BUCKET_BYTES + 4  # a probe that also reads the found slot's row position
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -206,7 +207,16 @@ def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
     segment leaves the cache, and the record; with more, the holders walked
     together through the index and one 4-byte hit per holder in the popular
     row, and for more than 64 holders the bitmap and the hits read back for
-    the shared-hit class, and its word.  Hk, Hv: the sparse group hits."""
+    the shared-hit class, and its word.  On pools of at most 4,096
+    instances, groups whose first block has more than 64 holders go to the
+    popular pass instead: per group of the window its list entry, first
+    block and index bucket (counted when the window has such groups), per
+    first block one walk of its representative's segment through the index
+    in rounds of 128 positions until one holder is left, plus the prefix
+    row; per group its staged head, 16 bytes per position of the common
+    prefix with the representative's segment, the prefix row, the walk on
+    from there, the hits, the class and the record.  Hk, Hv: the sparse
+    group hits."""
     import numpy as np
     R, N = win.n_req, win.n_inst
     G = len(rep)
@@ -224,10 +234,42 @@ def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
                  PROBE_ROWPOS)
     walk += int(w[ok[gk]].sum()) + int((8 + 8 * cnt0[ok]).sum())
     start = np.concatenate([[0], np.cumsum(cnt0)])
-    for k in np.nonzero(~ok)[0]:
+    popular = np.nonzero(~ok)[0]
+    pop_pass = N <= 64 * POP_WORDS and bool((cnt0 > 64).any())
+    if pop_pass:
+        # the popular pass's list kernel: per group its list entry, first
+        # block and index bucket; per listed group its entry and a minimum
+        walk += G * (8 + 8 + 128) + 16 * int((cnt0 > 64).sum())
+    first_block = {}
+    for k in popular:
         h = np.zeros(N, np.int64)
         h[Hk[start[k]:start[k + 1]] % N] = Hv[start[k]:start[k + 1]]
-        walk += 8 + index_walk_bytes(h, int(plen[k]), nw) + 4 * int(cnt0[k])
+        L = int(plen[k])
+        seg = win.pool[win.pre_off[rep[k]]:win.pre_off[rep[k]] + L]
+        if pop_pass and cnt0[k] > 64:
+            # the popular pass: the prefix walk once per first block (its
+            # representative, the first such group here), then each group from
+            # the end of the common prefix, k0, with the live set read from the
+            # prefix row
+            key = int(seg[0])
+            if key not in first_block:
+                hr = np.sort(h[h >= 1])[::-1]
+                P = int(min(L - 1, hr[1] if len(hr) > 1 else 0))
+                q = min(L, 1 + 128 * (P // 128 + 1))  # rounds of 128 positions
+                cnts = (h[None, :] > np.arange(1, q)[:, None]).sum(1)
+                walk += 8 * min(L, 256) + 128 * (q - 1) + int(np.where(cnts > 64, 8 * nw, 2 * cnts).sum())
+                walk += 4 * int(cnt0[k])  # the prefix row
+                first_block[key] = (seg, q)
+            rseg, q = first_block[key]
+            lim = min(L, len(rseg), q)
+            diff = np.nonzero(seg[:lim] != rseg[:lim])[0]
+            k0 = int(diff[0]) if len(diff) else lim
+            # staged head, LCP compare, prefix row read, walk from k0, hits, class, record
+            hk = np.where(h >= k0, h, 0)
+            walk += 8 * min(L, 256) + 16 * k0 + 4 * int(cnt0[k]) + index_walk_bytes(hk, L, nw) \
+                + 4 * int(cnt0[k]) + 8 * nw + 4 * int(cnt0[k]) + 8 + 8
+            continue
+        walk += 8 + index_walk_bytes(h, L, nw) + 4 * int(cnt0[k])
         if cnt0[k] > 64:  # the shared-hit class: bitmap and hits read back, the class word
             walk += 8 * nw + 4 * int(cnt0[k]) + 8
     return claim, walk
@@ -722,7 +764,8 @@ KERNELS = ("group_claim_kernel", "group_kernel", "lean_rows_kernel", "score_kern
 KERNEL_ROLE = {
     "group_claim_kernel": "prefix-group claim pass (each request's group slot, leader lists)",
     "group_kernel": "prefix-group walk (each shared segment walked once on every holder of its "
-                    "first block)",
+                    "first block; groups whose first block has a holder bitmap in the popular "
+                    "pass on a second stream beside it)",
     "lean_rows_kernel": "scorer, four requests per wave (hits from the group records, latency "
                         "model, filters, packing key, argmin)",
     "score_kernel": "general scorer (requests the lean scorer left: popular groups)",

@@ -101,6 +101,10 @@ hipError_t clear_fixed(unsigned char* base, hipStream_t s) {
 struct ps_ctx {
   int device = 0;
   hipStream_t stream = nullptr;
+  // the scoring call's second stream (the popular pass beside the walk
+  // pass) and the events of its fork and join
+  hipStream_t aux = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   int num_cus = 0;
   std::string err;
   bool loaded = false;
@@ -159,6 +163,12 @@ struct ps_ctx {
   uint32_t gslots = 0;   // power of two
   int32_t greq_cap = 0;  // entries of d_gslot
   uint64_t ggen = 0;
+  uint2* d_gplist = nullptr;  // the popular pass's groups
+  uint32_t gplist_cap = 0;
+  unsigned long long* d_grep = nullptr;  // representatives, per holder bitmap
+  uint32_t grep_cap = 0;
+  uint32_t* d_gpre = nullptr;            // prefix rows (grep_cap x n_inst), then grep_cap ends
+  size_t gpre_cap = 0;                   // words
   // order of the exhaustive probe's requests (counting-sort bins, order)
   uint32_t* d_obins = nullptr;
   int32_t* d_order = nullptr;
@@ -452,6 +462,9 @@ ps_status ps_create(int device, ps_ctx** out) {
   hipDeviceProp_t prop;
   e = hipGetDeviceProperties(&prop, device);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->join_ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMalloc((void**)&c->d_model, sizeof(DevModel));
   if (e == hipSuccess) e = hipMalloc((void**)&c->d_counter, sizeof(unsigned long long));
   if (e != hipSuccess) {
@@ -483,6 +496,7 @@ ps_status ps_destroy(ps_ctx* c) {
   if (!c) return PS_OK;
   DeviceScope ds(c->device);
   if (c->stream) (void)hipStreamSynchronize(c->stream);
+  if (c->aux) (void)hipStreamSynchronize(c->aux);
   free_snapshot(c);
   dfree(c->d_model);
   dfree(c->d_counter);
@@ -496,10 +510,16 @@ ps_status ps_destroy(ps_ctx* c) {
   dfree(c->d_gslot);
   dfree(c->d_gpop);
   dfree(c->d_glist);
+  dfree(c->d_gplist);
+  dfree(c->d_grep);
+  dfree(c->d_gpre);
   dfree(c->d_obins);
   dfree(c->d_order);
   for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
   if (c->stream) (void)hipStreamDestroy(c->stream);
+  if (c->aux) (void)hipStreamDestroy(c->aux);
+  if (c->fork_ev) (void)hipEventDestroy(c->fork_ev);
+  if (c->join_ev) (void)hipEventDestroy(c->join_ev);
   delete c;
   return PS_OK;
 }
@@ -740,6 +760,14 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   return PS_OK;
 }
 
+// Groups whose first block has a holder bitmap are walked by the popular
+// pass, beside the walk pass, on pools of at most 64 x kPopWords instances
+// whose index has such blocks.
+static bool popular_pass_ok(const ps_ctx* c) {
+  return c->x.n_pop > 0 && c->n_inst <= 64 * kPopWords &&
+         (size_t)c->x.n_pop * ((size_t)c->n_inst + 1) * sizeof(uint32_t) <= ((size_t)256 << 20);
+}
+
 // Group table for a window of n_req requests (at least two slots per
 // request) and the next window generation.  Grows (and clears) only when a
 // larger window arrives; a wrapped generation clears the keys once.
@@ -757,7 +785,8 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     clear = true;
   }
   if (!c->d_gpop) {
-    HIP_TRY(c, hipMalloc((void**)&c->d_gpop, kGroupPopBytes + kGroupHeadWords * sizeof(uint32_t)));
+    // two halves of rows: the walk pass's, then the popular pass's
+    HIP_TRY(c, hipMalloc((void**)&c->d_gpop, 2 * kGroupPopBytes + kGroupHeadWords * sizeof(uint32_t)));
     HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, kGroupHeadWords * sizeof(uint32_t), s));  // counter words
   }
   const uint32_t lcap = leader_list_cap(n_req);
@@ -773,6 +802,33 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     HIP_TRY(c, hipMalloc((void**)&c->d_gslot, (size_t)n_req * sizeof(uint32_t)));
     c->greq_cap = n_req;
   }
+  // the popular pass lists at most one entry per group: no more than the
+  // window's requests, nor than the popular area's rows
+  const uint32_t pcap = (uint32_t)std::min<size_t>((size_t)n_req,
+                                                   kGroupPopBytes / ((size_t)c->n_inst * sizeof(uint32_t)));
+  bool clear_rep = false;
+  if (popular_pass_ok(c)) {
+    if (pcap > c->gplist_cap) {
+      dfree(c->d_gplist);
+      c->gplist_cap = 0;
+      HIP_TRY(c, hipMalloc((void**)&c->d_gplist, (size_t)pcap * sizeof(uint2)));
+      c->gplist_cap = pcap;
+    }
+    if (c->x.n_pop > c->grep_cap) {
+      dfree(c->d_grep);
+      c->grep_cap = 0;
+      HIP_TRY(c, hipMalloc((void**)&c->d_grep, (size_t)c->x.n_pop * sizeof(unsigned long long)));
+      c->grep_cap = c->x.n_pop;
+      clear_rep = true;
+    }
+    const size_t pre_words = (size_t)c->x.n_pop * ((size_t)c->n_inst + 1);
+    if (pre_words > c->gpre_cap) {
+      dfree(c->d_gpre);
+      c->gpre_cap = 0;
+      HIP_TRY(c, hipMalloc((void**)&c->d_gpre, pre_words * sizeof(uint32_t)));
+      c->gpre_cap = pre_words;
+    }
+  }
   if (++c->ggen > kGroupGenMax) {
     c->ggen = 1;
     clear = true;
@@ -781,6 +837,8 @@ static ps_status group_buffers(ps_ctx* c, int32_t n_req, hipStream_t s) {
     HIP_TRY(c, hipMemsetAsync(c->d_gkeys, 0, 2 * (size_t)c->gslots * sizeof(unsigned long long), s));
     HIP_TRY(c, hipMemsetAsync(c->d_gpop, 0, kGroupHeadWords * sizeof(uint32_t), s));  // list lengths
   }
+  if ((clear || clear_rep) && c->grep_cap)  // representatives: all ones is above every tag
+    HIP_TRY(c, hipMemsetAsync(c->d_grep, 0xFF, (size_t)c->grep_cap * sizeof(unsigned long long), s));
   return PS_OK;
 }
 
@@ -851,7 +909,14 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
                      c->d_gpop + kListCtrWords * (1u + kXcds * (uint32_t)((c->ggen + 1u) & 1u)),
                      c->glcap,
                      // walkers: half the resident waves (8 per CU)
-                     (uint32_t)(8 * c->num_cus)};
+                     (uint32_t)(8 * c->num_cus),
+                     popular_pass_ok(c) && c->gplist_cap ? 1u : 0u,
+                     c->d_gplist,
+                     c->gplist_cap,
+                     c->d_grep,
+                     c->x.n_pop,
+                     c->d_gpre,
+                     c->d_gpre + (size_t)c->x.n_pop * (size_t)c->n_inst};
     a.defer_any = c->d_gpop + 1;
   }
   // The scoring kernel takes batches of a.batch requests per wave; a small
@@ -883,7 +948,8 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   // two waves per group at the usual group sizes), so the dispatcher
   // balances long walks (popular groups) against short ones
   if (a.grp.keys)
-    HIP_TRY(c, ps_launch_group(a, std::max(64, (n_req / 4 + 63) / 64 * 64), s, ev ? ev[1] : nullptr));
+    HIP_TRY(c, ps_launch_group(a, std::max(64, (n_req / 4 + 63) / 64 * 64), s, ev ? ev[1] : nullptr,
+                               c->aux, c->fork_ev, c->join_ev));
   else if (ev)
     HIP_TRY(c, hipEventRecord(ev[1], s));
   if (ev) HIP_TRY(c, hipEventRecord(ev[2], s));

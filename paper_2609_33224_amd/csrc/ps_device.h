@@ -101,6 +101,7 @@ struct GIndex {
   uint32_t nw;        // words per bitmap = ceil(n_inst / 64)
   uint32_t bmask;
   uint32_t shift;
+  uint32_t n_pop;     // bitmaps (hashes with more than kPopular holders)
 };
 
 // Prefix groups of one window.  Requests whose chains begin with the same
@@ -170,7 +171,30 @@ struct GroupTab {
   // segment on each holder, and the record's hits are the minima of the
   // parts' first misses (every new leader sets them to ~0 in the claim pass)
   uint32_t walkers;
+  // 1: the popular pass runs beside the walk pass (on pools of at most 64 x
+  // kPopWords instances), which then skips every group whose first block
+  // has a holder bitmap.  Its list kernel lists those groups in `plist`
+  // ({slot, bitmap number}, plist_cap entries; count in
+  // lctr[kPopCountWord], cleared by the previous window's claim pass) and
+  // elects per bitmap the listed group with the least slot, its
+  // representative (`rep`: (kGroupGenMax - gen) << 32 | slot; an older
+  // window's word compares higher).  The prefix kernel walks each
+  // representative's segment through the index while more than one holder
+  // is live and keeps, per holder, the position where it dropped out (~0:
+  // live at the stop, `pre_q`) in row `pre` of the bitmap; the member kernel
+  // starts every listed group's walk from that row at the common prefix of
+  // its segment and its representative's.  Listed group v takes popular
+  // row pop_cap + v (the second half of the area).
+  uint32_t pop_pass;
+  uint2* plist;
+  uint32_t plist_cap;
+  unsigned long long* rep;
+  uint32_t rep_cap;  // holder bitmaps of the index
+  uint32_t* pre;     // rep_cap rows of n_inst entries
+  uint32_t* pre_q;   // rep_cap
 };
+constexpr int32_t kPopWords = 64;       // bitmap words of the largest pool the popular pass takes
+constexpr uint32_t kPopCountWord = 2;   // on list 0's line of lctr
 constexpr uint32_t kGroupSplitMax = 4;
 constexpr int32_t kGroupPartMin = 1024;  // positions per part at least
 
@@ -356,7 +380,11 @@ hipError_t ps_launch_lmax(const ps::InstState* inst_key, const uint32_t* order0,
 // segment per group, then the walks of the leaders.
 // grid: a multiple of 64; mid (optional) is recorded between the claim and
 // walk launches
-hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid);
+// aux, fork, join: with a.grp.pop_pass, the second stream the popular
+// pass runs on beside the walk pass, and the events of the fork and join.
+hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid,
+                           hipStream_t aux = nullptr, hipEvent_t fork = nullptr,
+                           hipEvent_t join = nullptr);
 // Per-arrival scheduler: one workgroup of `threads` (a multiple of 64, at
 // most kSeqMaxThreads) over requests [a.r0, a.r1).
 hipError_t ps_launch_seq(const ps::SeqArgs& a, int threads, hipStream_t s);

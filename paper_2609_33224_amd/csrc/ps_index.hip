@@ -220,6 +220,7 @@ hipError_t ps_build_index(const Tables& t, int32_t n_inst, const uint32_t* count
     goto done;
   }
   nx.holders = sv;
+  nx.n_pop = n_pop;
   sv = nullptr;
   ps_free_index(x);
   *x = nx;

@@ -298,8 +298,9 @@ __global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, con
 // must be clear; both bitmaps are clear on return.  Wave-uniform arguments.
 // PF: on pools of at most 4,096 instances (one bitmap word per lane) the
 // holder bitmaps of a batch's popular positions are loaded together, before
-// the batch is applied in order.
-template <bool STAGED, bool PF, class Put>
+// the batch is applied in order.  RW, RU0: positions per lane of the
+// single-holder row walk's steps (run_walk).
+template <bool STAGED, bool PF, int RW = kWalkU, int RU0 = 4, class Put>
 __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c,
                                            const uint64_t* stage, uint64_t* bmA, uint64_t* bmN,
                                            int32_t nw, uint32_t nalive, int32_t p, Put put,
@@ -320,7 +321,7 @@ __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c
           break;
         }
       }
-      const uint32_t hk = run_walk<STAGED>(a.t, who, c, stage, p, g, s);
+      const uint32_t hk = run_walk<STAGED, RW, RU0>(a.t, who, c, stage, p, g, s);
       if (lane == 0) {
         put(who, hk);
         bmA[who >> 6] = 0ull;
@@ -439,6 +440,40 @@ __device__ int32_t group_claim(const GroupTab& G, int64_t pre_off, int* leader) 
   return -1;  // table full (not reached: it holds at least twice the requests)
 }
 
+// Single-thread lookup in the prefix index: the 8 entries of the key's
+// first bucket are read together (IdxBucket, 8 x {key, off | cnt << 32}),
+// then searched (index_search, which goes on to the next buckets while a
+// bucket is full without the key).  {off, cnt} of the key's entry; cnt 0
+// when it is absent.
+struct IdxBucket {
+  ulonglong2 v0, v1, v2, v3, v4, v5, v6, v7;
+};
+
+__device__ __forceinline__ IdxBucket index_bucket(const GIndex& x, uint32_t b) {
+  static_assert(sizeof(IdxEntry) == 16 && kSlotsPerBucket == 8, "a bucket is 8 x 16 bytes");
+  const ulonglong2* e = reinterpret_cast<const ulonglong2*>(x.ent + (size_t)b * kSlotsPerBucket);
+  return IdxBucket{e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]};
+}
+
+__device__ __forceinline__ uint2 index_search(const GIndex& x, uint64_t key, uint32_t b,
+                                              const IdxBucket& bk) {
+  if (key == 0ull) return make_uint2(0u, 0u);
+  for (const ulonglong2 v : {bk.v0, bk.v1, bk.v2, bk.v3, bk.v4, bk.v5, bk.v6, bk.v7}) {
+    if (v.x == key) return make_uint2((uint32_t)v.y, (uint32_t)(v.y >> 32));
+    if (v.x == 0ull) return make_uint2(0u, 0u);
+  }
+  // a full bucket without the key: the next buckets, one entry at a time
+  for (uint32_t step = 1; step <= x.bmask; ++step) {
+    b = (b + 1) & x.bmask;
+    for (int t = 0; t < kSlotsPerBucket; ++t) {
+      const IdxEntry e = x.ent[(size_t)b * kSlotsPerBucket + t];
+      if (e.key == key) return make_uint2(e.off, e.cnt);
+      if (e.key == 0ull) return make_uint2(0u, 0u);
+    }
+  }
+  return make_uint2(0u, 0u);
+}
+
 // Prefix groups, pass 1 (one thread per request; the grid covers every
 // request once): the slot of every request's group and the group's longest
 // segment (a 64-bit maximum over generation-tagged lengths, so no slot
@@ -455,6 +490,7 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
   }
   if (blockIdx.x == 0 && threadIdx.x < 2 * kXcds)  // the next window's list lengths and longest segments
     G.lctr_next[(threadIdx.x >> 1) * kListCtrWords + (threadIdx.x & 1u)] = 0u;
+  if (blockIdx.x == 0 && threadIdx.x == 0) G.lctr_next[kPopCountWord] = 0u;  // and popular count
   const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   bool want = false;
@@ -535,6 +571,59 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
     G.slot_of[r] = want && slot >= 0 ? (uint32_t)slot | (lead ? kGroupLead : 0u) : kGroupNoSlot;
 }
 
+// The shared-hit class of a popular group (hits of its holders in hp, the
+// holders in bitmap off0): H* = the most frequent hit among the holders of
+// the first 64-instance word that has any; when at most kGroupHold holders
+// differ from it, the record keeps them (rec[1..]) and the result is the
+// class word {n_exc << 24 | H*}, else kGroupNone.  The wave's own hit writes
+// are read back under a workgroup-scope fence (a device-scope one writes
+// back the XCD's whole L2).
+__device__ __forceinline__ uint32_t popular_class(const ScoreArgs& a, uint2* rec,
+                                                  const uint32_t* hp, uint32_t off0, int32_t nw,
+                                                  int lane) {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
+  uint32_t hs = 0u;
+  for (int32_t w = 0; w < nw; ++w) {
+    const uint64_t word = bm[w];
+    if (!word) continue;
+    const bool hold = ((word >> lane) & 1ull) != 0ull;
+    const uint32_t v = hold ? hp[w * 64 + lane] : 0u;
+    uint64_t rem = word;
+    uint32_t bestc = 0u;
+    while (rem) {
+      const uint32_t val = (uint32_t)__builtin_amdgcn_readlane((int)v, __builtin_ctzll(rem));
+      const uint64_t same = __ballot(hold && v == val);
+      rem &= ~same;
+      if ((uint32_t)__popcll(same) > bestc) {
+        bestc = (uint32_t)__popcll(same);
+        hs = val;
+      }
+    }
+    break;
+  }
+  uint32_t nexc = 0u;
+  for (int32_t w0 = 0; w0 < nw && nexc <= kGroupHold; w0 += 4) {  // four words in flight
+    bool hold[4];
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int32_t w = w0 + u;
+      hold[u] = w < nw && ((bm[w] >> lane) & 1ull) != 0ull;
+      v[u] = hold[u] ? hp[w * 64 + lane] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const bool ex = hold[u] && v[u] != hs;
+      const uint64_t em = __ballot(ex);
+      const uint32_t k = nexc + (uint32_t)__popcll(em & ((1ull << lane) - 1ull));
+      if (ex && k < kGroupHold) rec[1 + k] = make_uint2((uint32_t)((w0 + u) * 64 + lane), v[u]);
+      nexc += (uint32_t)__popcll(em);
+    }
+  }
+  return (nexc <= kGroupHold && hs > 0u && hs < (1u << 24)) ? ((nexc << 24) | hs) : kGroupNone;
+}
+
 // Prefix groups, pass 2 (a persistent grid over the leaders' lists, which
 // the claim pass wrote): the walk of the group's longest segment on every
 // holder of its first block, into the slot's record (up to kGroupHold
@@ -598,6 +687,7 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
     uint32_t cnt = 0u;
     if (found0 && cnt0 > kGroupHold) {
       if (part != 0u) continue;  // a popular group: one wave walks all holders
+      if (cnt0 > kPopular && G.pop_pass) continue;  // the popular pass's (it writes the record)
       uint32_t row = 0;
       if (lane == 0) row = atomicAdd(G.pop_ctr, 1u);
       row = (uint32_t)__shfl((int)row, 0);
@@ -618,55 +708,7 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
         index_walk<true, true>(a, c, stage, bmA, bmN, nw, cnt0, 1,
                                [&](uint32_t id, uint32_t h) { hp[id] = h; }, lane, g, s);
         cnt = kGroupPop | row;
-        // The shared-hit class: H* = the most frequent hit among the holders
-        // of the first 64-instance word that has any; when at most
-        // kGroupHold holders differ from it, the record keeps them.
-        uint32_t clsw = kGroupNone;
-        if (cnt0 > kPopular) {
-          // this wave's hit writes, then its reads of them (a workgroup-scope
-          // fence: a device-scope one writes back the XCD's whole L2)
-          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-          const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
-          uint32_t hs = 0u;
-          for (int32_t w = 0; w < nw; ++w) {
-            const uint64_t word = bm[w];
-            if (!word) continue;
-            const bool hold = ((word >> lane) & 1ull) != 0ull;
-            const uint32_t v = hold ? hp[w * 64 + lane] : 0u;
-            uint64_t rem = word;
-            uint32_t bestc = 0u;
-            while (rem) {
-              const uint32_t val = (uint32_t)__builtin_amdgcn_readlane((int)v, __builtin_ctzll(rem));
-              const uint64_t same = __ballot(hold && v == val);
-              rem &= ~same;
-              if ((uint32_t)__popcll(same) > bestc) {
-                bestc = (uint32_t)__popcll(same);
-                hs = val;
-              }
-            }
-            break;
-          }
-          uint32_t nexc = 0u;
-          for (int32_t w0 = 0; w0 < nw && nexc <= kGroupHold; w0 += 4) {  // four words in flight
-            bool hold[4];
-            uint32_t v[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int32_t w = w0 + u;
-              hold[u] = w < nw && ((bm[w] >> lane) & 1ull) != 0ull;
-              v[u] = hold[u] ? hp[w * 64 + lane] : 0u;
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const bool ex = hold[u] && v[u] != hs;
-              const uint64_t em = __ballot(ex);
-              const uint32_t k = nexc + (uint32_t)__popcll(em & ((1ull << lane) - 1ull));
-              if (ex && k < kGroupHold) rec[1 + k] = make_uint2((uint32_t)((w0 + u) * 64 + lane), v[u]);
-              nexc += (uint32_t)__popcll(em);
-            }
-          }
-          if (nexc <= kGroupHold && hs > 0u && hs < (1u << 24)) clsw = (nexc << 24) | hs;
-        }
+        const uint32_t clsw = cnt0 > kPopular ? popular_class(a, rec, hp, off0, nw, lane) : kGroupNone;
         if (lane == 0) rec[kGroupClsWord] = make_uint2(clsw, off0);
       }
     } else if (found0) {
@@ -692,6 +734,339 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
       cnt = cnt0;
     }
     if (lane == 0 && part == 0u) rec[0] = make_uint2((uint32_t)plen, cnt);
+  }
+}
+
+// ------------------------------------------------------------ popular pass
+// Beside the walk pass, on a second stream: the groups whose first block
+// has a holder bitmap (more than kPopular holders; at c3, a 128-block system
+// prompt held by nearly every instance).  The walk pass would walk each of
+// them through the index, eight positions per pair of dependent reads, all
+// over the same shared prefix.  Here the prefix is walked once per first
+// block (by its representative, every position of a round at once), and
+// each group starts from that walk at the end of its common prefix with the
+// representative's segment.
+
+// Leaders' list entry v of the window's kXcds lists taken back to back
+// (len: the lists' lengths).
+__device__ __forceinline__ unsigned long long list_entry(const GroupTab& G, const uint32_t* len,
+                                                         uint32_t v) {
+  uint32_t rem = v, lsel = 0u, isel = 0u;
+  bool done = false;
+#pragma unroll
+  for (int l = 0; l < kXcds; ++l) {
+    if (!done) {
+      if (rem < len[l]) {
+        lsel = (uint32_t)l;
+        isel = rem;
+        done = true;
+      } else {
+        rem -= len[l];
+      }
+    }
+  }
+  return G.lists[(size_t)lsel * G.lcap + isel];
+}
+
+// Popular pass 1: 64 leaders per wave and step, one per lane: the first
+// block's index entry; the groups whose first block has a holder bitmap go
+// into plist (one atomic per wave) and the least slot of each bitmap into
+// its representative word (one minimum per bitmap and wave, skipped when
+// the word already holds a lesser slot of this window: atomics on one
+// address queue).
+__global__ __launch_bounds__(64) void popular_list_kernel(ScoreArgs a) {
+  const GroupTab& G = a.grp;
+  const int lane = threadIdx.x;
+  uint32_t len[kXcds], total = 0u;
+#pragma unroll
+  for (int l = 0; l < kXcds; ++l) {
+    len[l] = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[l * kListCtrWords]);
+    total += len[l];
+  }
+  const unsigned long long tag = (kGroupGenMax - G.gen) << 32;
+  for (uint32_t base = blockIdx.x * 64u; base < total; base += gridDim.x * 64u) {
+    const uint32_t v = base + (uint32_t)lane;
+    bool pop = false;
+    uint32_t slot = 0u, off0 = 0u;
+    if (v < total) {
+      const unsigned long long ent = list_entry(G, len, v);
+      slot = (uint32_t)(ent & 0xFFFFFFull);
+      const uint64_t key0 = a.pool[(int64_t)(ent >> 24) - 1];
+      const uint32_t b = bucket_of(key0, kIndexSalt, a.x.shift);
+      const uint2 f = index_search(a.x, key0, b, index_bucket(a.x, b));
+      off0 = f.x;
+      pop = f.y > kPopular && off0 < G.rep_cap;
+    }
+    const uint64_t pm = __ballot(pop);
+    if (!pm) continue;
+    uint32_t k0 = 0u;
+    if (lane == 0) k0 = atomicAdd(&G.lctr[kPopCountWord], (uint32_t)__popcll(pm));
+    k0 = (uint32_t)__shfl((int)k0, 0);
+    const uint32_t k = k0 + (uint32_t)__popcll(pm & ((1ull << lane) - 1ull));
+    const bool listed = pop && k < G.plist_cap;
+    if (listed) G.plist[k] = make_uint2(slot, off0);
+    if (pop && !listed)  // no room: a record without a result (its requests walk on their own)
+      G.rec[(size_t)slot * kGroupRec] =
+          make_uint2((uint32_t)(G.plen[slot] & ((1ull << kGroupGenShift) - 1ull)), kGroupNone);
+    uint64_t pend = __ballot(listed);
+    while (pend) {
+      const int src = __builtin_ctzll(pend);
+      const uint32_t o = (uint32_t)__shfl((int)off0, src);
+      const bool same = listed && off0 == o;
+      const uint64_t sm = __ballot(same);
+      const uint32_t least = wave_min_u32(same ? slot : 0xFFFFFFFFu);
+      if (lane == src) {
+        const unsigned long long want = tag | (unsigned long long)least;
+        if (G.rep[o] > want) atomicMin(G.rep + o, want);
+      }
+      pend &= ~sm;
+    }
+  }
+}
+
+// Word `lane` of the holder bitmap of an index entry's holder list (cnt <=
+// kPopular ascending ids).
+__device__ __forceinline__ uint64_t list_word(const GIndex& x, uint32_t off, uint32_t cnt, int lane) {
+  const uint32_t idv = (uint32_t)lane < cnt ? (uint32_t)x.holders[off + (uint32_t)lane] : 0xFFFFFFFFu;
+  uint64_t m = 0ull;
+  for (uint32_t k = 0; k < cnt; ++k) {
+    const uint32_t id = (uint32_t)__shfl((int)idv, (int)k);
+    if ((id >> 6) == (uint32_t)lane) m |= 1ull << (id & 63u);
+  }
+  return m;
+}
+
+// Popular pass 2: one workgroup of kPrefixWaves waves per representative
+// (found by scanning plist).  Rounds of kPrefixWaves x 32 positions of its
+// segment: wave w looks up its 32 positions (four lookups, then the 32
+// holder bitmaps, all in flight) and takes, for every holder of the first
+// block, the first of them it lacks; the least over the waves (an LDS
+// minimum) is the holder's first missing position.  Rounds go on while
+// more than one holder holds every position so far.  Row `pre` of the
+// bitmap: that position, or ~0 for the holders that have all of them; pre_q:
+// the round's end.  Pools of at most 64 x kPopWords instances (the live set
+// is one bitmap word per lane).
+constexpr int kPrefixWaves = 4;
+constexpr int kPrefixSpan = 32;  // positions per wave and round
+constexpr int32_t kPrefixMax = 1 << 14;
+
+__global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(ScoreArgs a) {
+  __shared__ uint64_t stage[kStage];
+  __shared__ uint32_t fmiss[64 * kPopWords];  // first missing position per instance (~0: none)
+  __shared__ uint32_t reps[64 * kPrefixWaves], n_reps, live_part[kPrefixWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int g = lane >> 3, s = lane & 7;
+  const GroupTab& G = a.grp;
+  const unsigned long long lmask = (1ull << kGroupGenShift) - 1ull;
+  const int32_t nw = (a.n_inst + 63) >> 6;
+  if (nw > kPopWords) return;
+  uint32_t n = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[kPopCountWord]);
+  n = n < G.plist_cap ? n : G.plist_cap;
+  const uint32_t chunk = 64u * kPrefixWaves;
+  for (uint32_t base = blockIdx.x * chunk; base < n; base += gridDim.x * chunk) {
+    // the representatives among these listed groups
+    if (tid == 0) n_reps = 0u;
+    __syncthreads();
+    const uint32_t vl = base + (uint32_t)tid;
+    if (vl < n) {
+      const uint2 el = G.plist[vl];
+      if ((uint32_t)G.rep[el.y] == el.x) reps[atomicAdd(&n_reps, 1u)] = vl;
+    }
+    __syncthreads();
+    const uint32_t nr = n_reps;
+    for (uint32_t r = 0; r < nr; ++r) {
+      const uint2 ent = G.plist[reps[r]];
+      const uint32_t slot = ent.x, off0 = ent.y;
+      const int64_t pre_off = (int64_t)(G.keys[slot] & lmask) - 1;
+      const int32_t plen = (int32_t)(G.plen[slot] & lmask);
+      const int32_t lim = plen < kPrefixMax ? plen : kPrefixMax;
+      const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
+      const int32_t nst = plen < kStage ? plen : kStage;
+      for (int32_t j = tid; j < nst; j += 64 * kPrefixWaves) stage[j] = c.pre[j];
+      for (int32_t i = tid; i < 64 * nw; i += 64 * kPrefixWaves) fmiss[i] = 0xFFFFFFFFu;
+      const uint64_t first = lane < nw ? a.x.bitmaps[(size_t)off0 * a.x.nw + lane] : 0ull;
+      __syncthreads();
+      int32_t p = 1;
+      uint32_t nalive = 2u;
+      while (p < lim && nalive > 1u) {
+        const int32_t p0 = p + wv * kPrefixSpan;  // this wave's positions [p0, p0 + 32)
+        constexpr int U = kPrefixSpan / 8;
+        IdxHit hq[U];
+        uint64_t kq[U];
+        IdxEntry e[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int32_t jq = p0 + 8 * u + g;
+          kq[u] = jq < lim ? (jq < kStage ? stage[jq] : chain_global(c, jq)) : 0ull;
+          e[u] = kq[u] ? a.x.ent[(size_t)bucket_of(kq[u], kIndexSalt, a.x.shift) * kSlotsPerBucket + s]
+                       : IdxEntry{0ull, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const uint64_t fm = __ballot(kq[u] != 0ull && e[u].key == kq[u]);
+          const uint64_t em = __ballot(kq[u] != 0ull && e[u].key == 0ull);
+          const uint32_t f = (uint32_t)(fm >> (8 * g)) & 0xFFu;
+          const uint32_t z = (uint32_t)(em >> (8 * g)) & 0xFFu;
+          const int src = 8 * g + (f ? __builtin_ctz(f) : 0);
+          hq[u].found = f != 0u;
+          hq[u].off = __shfl(e[u].off, src);
+          hq[u].cnt = __shfl(e[u].cnt, src);
+          if (__ballot(kq[u] != 0ull && !f && !z)) hq[u] = index_lookup(a.x, kq[u], kq[u] != 0ull, g, s);
+        }
+        uint64_t pw[kPrefixSpan];
+#pragma unroll
+        for (int t = 0; t < kPrefixSpan; ++t) {
+          const bool f = __shfl(hq[t / 8].found ? 1 : 0, 8 * (t % 8)) != 0;
+          const uint32_t off = __shfl(hq[t / 8].off, 8 * (t % 8)), cnt = __shfl(hq[t / 8].cnt, 8 * (t % 8));
+          pw[t] = f && cnt > kPopular && lane < nw ? a.x.bitmaps[(size_t)off * a.x.nw + lane] : 0ull;
+        }
+        // the first of this wave's positions each holder lacks
+        uint64_t have = first;
+#pragma unroll
+        for (int t = 0; t < kPrefixSpan; ++t) {
+          if (p0 + t < lim) {
+            const bool f = __shfl(hq[t / 8].found ? 1 : 0, 8 * (t % 8)) != 0;
+            const uint32_t off = __shfl(hq[t / 8].off, 8 * (t % 8)), cnt = __shfl(hq[t / 8].cnt, 8 * (t % 8));
+            const uint64_t keep = !f ? 0ull : (cnt > kPopular ? pw[t] : list_word(a.x, off, cnt, lane));
+            uint64_t d = have & ~keep;
+            while (d) {
+              const int b = __builtin_ctzll(d);
+              d &= d - 1ull;
+              atomicMin(&fmiss[lane * 64 + b], (uint32_t)(p0 + t));
+            }
+            have &= keep;
+          }
+        }
+        __syncthreads();
+        // holders with every position so far (the first wave's words)
+        const int32_t pe = p + kPrefixWaves * kPrefixSpan < lim ? p + kPrefixWaves * kPrefixSpan : lim;
+        uint64_t all = 0ull;
+        if (wv == 0 && lane < nw) {
+          uint64_t w = first;
+          while (w) {
+            const int b = __builtin_ctzll(w);
+            w &= w - 1ull;
+            if (fmiss[lane * 64 + b] == 0xFFFFFFFFu) all |= 1ull << b;
+          }
+        }
+        if (wv == 0) {
+          const uint32_t cnt = wave_sum_u32((uint32_t)__popcll(all));
+          if (lane == 0) live_part[0] = cnt;
+        }
+        __syncthreads();
+        nalive = live_part[0];
+        p = pe;
+        __syncthreads();
+      }
+      // row of the bitmap: the holders' first missing positions
+      uint32_t* row = G.pre + (size_t)off0 * (size_t)a.n_inst;
+      if (wv == 0 && lane < nw) {
+        uint64_t w = first;
+        while (w) {
+          const int b = __builtin_ctzll(w);
+          w &= w - 1ull;
+          row[lane * 64 + b] = fmiss[lane * 64 + b];
+        }
+      }
+      if (tid == 0) G.pre_q[off0] = (uint32_t)p;
+      __syncthreads();
+    }
+  }
+}
+
+// Popular pass 3 (a persistent grid over plist): listed group v.  Its
+// segment and its representative's agree on their first k blocks
+// (compared here; k at most the prefix walk's end), so a holder whose first
+// missing position there is h < k has hit h here too, and the others hold
+// the first k blocks: only they are walked on, from k, through the index
+// (one holder left: along its row, 512 positions per step).  Then the
+// record, as the walk pass writes it, with popular row pop_cap + v.
+constexpr int kMemberChunk = 16;  // bitmap words whose holders' hits are read together
+constexpr int kPopListGrid = 512;    // waves of the popular pass's list kernel
+constexpr int kPopPrefixGrid = 64;   // workgroups of its prefix kernel
+constexpr int kPopWalkGrid = 4096;   // waves of its member kernel
+
+__global__ __launch_bounds__(64) void popular_member_kernel(ScoreArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem);
+  const int32_t nw = (a.n_inst + 63) >> 6;
+  uint64_t* bmA = stage + kStage;
+  uint64_t* bmN = bmA + nw;
+  for (int32_t w = threadIdx.x; w < 2 * nw; w += 64) bmA[w] = 0ull;
+  const int lane = threadIdx.x;
+  const int g = lane >> 3, s = lane & 7;
+  const GroupTab& G = a.grp;
+  const unsigned long long lmask = (1ull << kGroupGenShift) - 1ull;
+  if (nw > kPopWords) return;
+  uint32_t n = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[kPopCountWord]);
+  n = n < G.plist_cap ? n : G.plist_cap;
+  for (uint32_t v = blockIdx.x; v < n; v += gridDim.x) {
+    const uint2 ent = G.plist[v];
+    const uint32_t slot = ent.x, off0 = ent.y;
+    const int64_t pre_off = (int64_t)(G.keys[slot] & lmask) - 1;
+    const int32_t plen = (int32_t)(G.plen[slot] & lmask);
+    const uint32_t rslot = (uint32_t)G.rep[off0];  // this window's: every listed group set its tag
+    const uint32_t q = G.pre_q[off0];
+    const uint64_t myw = lane < nw ? a.x.bitmaps[(size_t)off0 * a.x.nw + lane] : 0ull;  // word `lane`
+    const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
+    const int32_t nst = plen < kStage ? plen : kStage;
+    __syncthreads();
+    for (int32_t j = lane; j < nst; j += 64) stage[j] = c.pre[j];
+    const int64_t rpre = (int64_t)(G.keys[rslot] & lmask) - 1;
+    const int32_t rlen = (int32_t)(G.plen[rslot] & lmask);
+    uint2* rec = G.rec + (size_t)slot * kGroupRec;
+    const uint32_t row = G.pop_cap + v;
+    uint32_t* hp = G.pop + (size_t)row * (size_t)a.n_inst;
+    // k: the common prefix of the two segments, at most the prefix walk's end
+    int32_t lim = plen < rlen ? plen : rlen;
+    lim = lim < (int32_t)q ? lim : (int32_t)q;
+    int32_t k = lim;
+    if (rslot != slot) {
+      const uint64_t* rc = a.pool + rpre;
+      for (int32_t j0 = 0; j0 < lim; j0 += 64 * 8) {
+        uint32_t firstm = ~0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int32_t j = j0 + u * 64 + lane;
+          if (j < lim && c.pre[j] != rc[j] && (uint32_t)j < firstm) firstm = (uint32_t)j;
+        }
+        firstm = wave_min_u32(firstm);
+        if (firstm != ~0u) {
+          k = (int32_t)firstm;
+          break;
+        }
+      }
+    }
+    // the live set at k; the holders missing a position before k keep it
+    const uint32_t* prow = G.pre + (size_t)off0 * (size_t)a.n_inst;
+    uint32_t nalive = 0u;
+    for (int32_t w0 = 0; w0 < nw; w0 += kMemberChunk) {
+      uint32_t h[kMemberChunk];
+#pragma unroll
+      for (int u = 0; u < kMemberChunk; ++u) {
+        const uint64_t word = (uint64_t)lane_value64((int64_t)myw, (w0 + u) & 63);
+        const bool hold = w0 + u < nw && ((word >> lane) & 1ull) != 0ull;
+        h[u] = hold ? prow[(w0 + u) * 64 + lane] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kMemberChunk; ++u) {
+        const uint64_t word = (uint64_t)lane_value64((int64_t)myw, (w0 + u) & 63);
+        const bool hold = w0 + u < nw && ((word >> lane) & 1ull) != 0ull;
+        const bool live = hold && h[u] >= (uint32_t)k;
+        if (hold && !live) hp[(w0 + u) * 64 + lane] = h[u];
+        const uint64_t lw = __ballot(live);
+        if (lane == 0 && w0 + u < nw) bmA[w0 + u] = lw;
+        nalive += (uint32_t)__popcll(lw);
+      }
+    }
+    __syncthreads();
+    index_walk<true, true, 8, 4>(a, c, stage, bmA, bmN, nw, nalive, k,
+                                 [&](uint32_t id, uint32_t hh) { hp[id] = hh; }, lane, g, s);
+    const uint32_t clsw = popular_class(a, rec, hp, off0, nw, lane);
+    if (lane == 0) {
+      rec[kGroupClsWord] = make_uint2(clsw, off0);
+      rec[0] = make_uint2((uint32_t)plen, kGroupPop | row);
+    }
   }
 }
 
@@ -2102,7 +2477,8 @@ hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, con
   return hipGetLastError();
 }
 
-hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid) {
+hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid,
+                           hipStream_t aux, hipEvent_t fork, hipEvent_t join) {
   if (a.n_req == 0) return hipSuccess;
   hipLaunchKernelGGL(group_claim_kernel, dim3((a.n_req + kClaimBlock - 1) / kClaimBlock),
                      dim3(kClaimBlock), 0, s, a);
@@ -2114,8 +2490,25 @@ hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s, hipEvent
   }
   const size_t nw = ((size_t)a.n_inst + 63) / 64;
   const size_t lds = (size_t)kStage * sizeof(uint64_t) + 2 * nw * sizeof(uint64_t);
+  if (!a.grp.pop_pass) {
+    hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, s, a);
+    return hipGetLastError();
+  }
+  // the popular pass on the second stream, forked after the claim pass and
+  // joined after the walk pass
+  if (!aux || !fork || !join) return hipErrorInvalidValue;
+  if ((e = hipEventRecord(fork, s)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(aux, fork, 0)) != hipSuccess) return e;
+  hipLaunchKernelGGL(popular_list_kernel, dim3(kPopListGrid), dim3(64), 0, aux, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(popular_prefix_kernel, dim3(kPopPrefixGrid), dim3(64 * kPrefixWaves), 0, aux, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(popular_member_kernel, dim3(kPopWalkGrid), dim3(64), lds, aux, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = hipEventRecord(join, aux)) != hipSuccess) return e;
   hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, s, a);
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return hipStreamWaitEvent(s, join, 0);
 }
 
 hipError_t ps_launch_commit(const CommitArgs& a, hipStream_t s) {

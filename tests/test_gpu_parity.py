@@ -670,3 +670,68 @@ def test_feedback_path(ps, scorer):
     res, sizes = DeviceWindow(w).score(scorer)
     od = o.score(m, w.pool, w.pre_off, w.pre_len, w.tail_off, w.tail_len)
     compare_decisions(res, sizes, od, label="after feedback")
+
+
+def _long_shared_prefix_window(base=401):
+    """A 300-block shared prefix (longer than a staged chain head and than
+    one round of the popular pass's prefix walk) held by 150 of 160
+    instances, cut short on some of them at positions around the round and
+    stage boundaries, and dropping to 40 (a holder list) and then 9 holders
+    past position 130; four sessions leave it at different positions (300,
+    200, 40, 1), so groups with one popular first block share prefixes of
+    different lengths with its representative; each session's own blocks
+    on one to three owners, one with a hole."""
+    rng = np.random.default_rng(base)
+    SP = chain_hashes(300, base=base)
+    own = {k: chain_hashes(60, base=base + (k + 1) * 10**6) for k in range(4)}
+    segs = {0: SP + own[0], 1: SP[:200] + own[1], 2: SP[:40] + own[2], 3: SP[:1] + own[3]}
+    pool = []
+
+    def put(seq):
+        off = len(pool)
+        pool.extend(seq)
+        return off
+
+    seg_off = {k: put(v) for k, v in segs.items()}
+    tail = chain_hashes(3, base=base + 9 * 10**7)
+    t_off = put(tail)
+    n_inst = 160
+    filler = chain_hashes(2000, base=base + 5 * 10**7)
+    cut = np.full(n_inst, 300)
+    cut[:40] = [5, 64, 127, 128, 129, 200, 255, 256, 257, 299] * 4
+    cut[40:150] = np.where(rng.random(110) < 0.9, 131, 300)   # 40 or so left past 130
+    cut[150:] = 0                                            # hold none of it
+    sets = []
+    for i in range(n_inst):
+        s = list(SP[:cut[i]]) + list(filler[10 * i:10 * i + 3])
+        sets.append(s)
+    for k in range(4):  # owners of each session's own blocks
+        lead = len(segs[k]) - 60
+        for j, i in enumerate(rng.choice(150, 3, replace=False)):
+            if cut[i] >= lead:
+                extra = own[k][:10 + 20 * j]
+                if j == 2:
+                    extra = extra[:5] + extra[6:]  # a hole
+                sets[i] = sets[i] + list(extra)
+    reqs = []
+    for k in range(4):
+        L = len(segs[k])
+        for p in (L - 60, L - 55, L - 30, L, max(8, L - 70)):
+            reqs.append((seg_off[k], p, t_off, 3))
+    order = np.random.default_rng(base + 1).permutation(len(reqs))
+    reqs = [reqs[i] for i in order]
+    return _edge(sets, None, pool=pool, reqs=reqs, cap=1024)
+
+
+def test_popular_pass_shared_prefixes(ps, scorer):
+    """Groups whose first block has a holder bitmap are walked by the
+    popular pass beside the walk pass (a prefix walk per first block, then
+    each group from the end of its common prefix with the representative):
+    oracle parity, and byte for byte the results of the allocation-free
+    entry point, whose walk pass walks every group itself."""
+    for base in (401, 402):
+        w = _long_shared_prefix_window(base=base)
+        res = _check_edge(ps, scorer, w, f"long shared prefix {base}")
+        fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
+        assert fixed.tobytes() == res.tobytes(), f"{base}: the walk pass alone decides differently"
+        _check_edge(ps, scorer, w, f"long shared prefix {base} eta=1", eta=1.0)
