@@ -209,8 +209,9 @@ def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
     row, and for more than 64 holders the bitmap and the hits read back for
     the shared-hit class, and its word.  On pools of at most 4,096
     instances, groups whose first block has more than 64 holders go to the
-    popular pass instead: per group of the window its list entry, first
-    block and index bucket (counted when the window has such groups), per
+    popular pass instead, listed by the claim pass (per leader its first
+    block and index bucket, per listed group its entry, class word and
+    representative minimum; counted when the window has such groups), per
     first block one walk of its representative's segment through the index
     in rounds of 128 positions until one holder is left, plus the prefix
     row; per group its staged head, 16 bytes per position of the common
@@ -237,9 +238,10 @@ def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
     popular = np.nonzero(~ok)[0]
     pop_pass = N <= 64 * POP_WORDS and bool((cnt0 > 64).any())
     if pop_pass:
-        # the popular pass's list kernel: per group its list entry, first
-        # block and index bucket; per listed group its entry and a minimum
-        walk += G * (8 + 8 + 128) + 16 * int((cnt0 > 64).sum())
+        # the claim pass lists the popular pass's groups: per leader its
+        # first block and index bucket; per listed group its entry, class
+        # word and a minimum
+        claim += G * (8 + 128) + 24 * int((cnt0 > 64).sum())
     first_block = {}
     for k in popular:
         h = np.zeros(N, np.int64)
@@ -765,7 +767,8 @@ KERNEL_ROLE = {
     "group_claim_kernel": "prefix-group claim pass (each request's group slot, leader lists)",
     "group_kernel": "prefix-group walk (each shared segment walked once on every holder of its "
                     "first block; groups whose first block has a holder bitmap in the popular "
-                    "pass on a second stream beside it)",
+                    "pass beside it, the walk then on a second stream; timed from the claim "
+                    "pass's end to the join of both on the calling stream)",
     "lean_rows_kernel": "scorer, four requests per wave (hits from the group records, latency "
                         "model, filters, packing key, argmin)",
     "score_kernel": "general scorer (requests the lean scorer left: popular groups)",

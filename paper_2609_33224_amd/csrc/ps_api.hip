@@ -101,8 +101,8 @@ hipError_t clear_fixed(unsigned char* base, hipStream_t s) {
 struct ps_ctx {
   int device = 0;
   hipStream_t stream = nullptr;
-  // the scoring call's second stream (the popular pass beside the walk
-  // pass) and the events of its fork and join
+  // the scoring call's second stream (the walk pass, beside the popular
+  // pass on the calling stream) and the events of its fork and join
   hipStream_t aux = nullptr;
   hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   int num_cus = 0;

@@ -132,6 +132,9 @@ constexpr int kGroupRec = 2 + (int)kGroupHold;  // 8-byte words per slot record
 // the holders and, in its last word, {n_exc << 24 | H*, the first block's
 // holder bitmap number}; otherwise that word's first half is kGroupNone.
 constexpr int kGroupClsWord = 1 + (int)kGroupHold;
+// Class word .y of a popular group that the popular pass's list had no
+// room for (the walk pass takes it); a listed one holds its bitmap number.
+constexpr uint32_t kGroupUnlisted = 0xFFFFFFFFu;
 
 constexpr uint32_t kGroupLead = 0x80000000u;  // slot_of flag of the group's leader
 constexpr uint32_t kGroupNoSlot = 0xFFFFFFFFu;
@@ -172,8 +175,8 @@ struct GroupTab {
   // parts' first misses (every new leader sets them to ~0 in the claim pass)
   uint32_t walkers;
   // 1: the popular pass runs beside the walk pass (on pools of at most 64 x
-  // kPopWords instances), which then skips every group whose first block
-  // has a holder bitmap.  Its list kernel lists those groups in `plist`
+  // kPopWords instances), which then skips every listed group.  The claim
+  // pass lists the groups whose first block has a holder bitmap in `plist`
   // ({slot, bitmap number}, plist_cap entries; count in
   // lctr[kPopCountWord], cleared by the previous window's claim pass) and
   // elects per bitmap the listed group with the least slot, its
@@ -380,8 +383,9 @@ hipError_t ps_launch_lmax(const ps::InstState* inst_key, const uint32_t* order0,
 // segment per group, then the walks of the leaders.
 // grid: a multiple of 64; mid (optional) is recorded between the claim and
 // walk launches
-// aux, fork, join: with a.grp.pop_pass, the second stream the popular
-// pass runs on beside the walk pass, and the events of the fork and join.
+// aux, fork, join: with a.grp.pop_pass, the second stream the walk pass
+// runs on beside the popular pass (on s), and the events of the fork and
+// join.
 hipError_t ps_launch_group(const ps::ScoreArgs& a, int grid, hipStream_t s, hipEvent_t mid,
                            hipStream_t aux = nullptr, hipEvent_t fork = nullptr,
                            hipEvent_t join = nullptr);

@@ -566,6 +566,49 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
       for (uint32_t t = 0; t < kGroupHold; ++t) rec[1 + t] = make_uint2(0u, 0xFFFFFFFFu);
     }
   }
+  // A leader whose first block has a holder bitmap (a popular group) goes
+  // into the popular pass's list (one atomic per wave) and its slot into
+  // the bitmap's representative word (the least slot of the window: one
+  // minimum per bitmap and wave, skipped when the word already holds a
+  // lesser one, since atomics on one address queue).  Its class word says
+  // whether it was listed; the walk pass takes the others.
+  if (G.pop_pass) {
+    bool pop = false;
+    uint32_t off0 = 0u;
+    if (lead) {
+      const uint64_t key0 = a.pool[off];
+      const uint32_t b = bucket_of(key0, kIndexSalt, a.x.shift);
+      const uint2 f = index_search(a.x, key0, b, index_bucket(a.x, b));
+      off0 = f.x;
+      pop = f.y > kPopular && off0 < G.rep_cap;
+    }
+    const uint64_t pm = __ballot(pop);
+    if (pm) {
+      uint32_t k0 = 0u;
+      if (lane == 0) k0 = atomicAdd(&G.lctr[kPopCountWord], (uint32_t)__popcll(pm));
+      k0 = (uint32_t)__shfl((int)k0, 0);
+      const uint32_t k = k0 + (uint32_t)__popcll(pm & ((1ull << lane) - 1ull));
+      const bool listed = pop && k < G.plist_cap;
+      if (listed) G.plist[k] = make_uint2((uint32_t)slot, off0);
+      if (pop)
+        G.rec[(size_t)slot * kGroupRec + kGroupClsWord] =
+            make_uint2(kGroupNone, listed ? off0 : kGroupUnlisted);
+      const unsigned long long tag = (kGroupGenMax - G.gen) << 32;
+      uint64_t pend = __ballot(listed);
+      while (pend) {
+        const int src = __builtin_ctzll(pend);
+        const uint32_t o = (uint32_t)__shfl((int)off0, src);
+        const bool same = listed && off0 == o;
+        const uint64_t sm = __ballot(same);
+        const uint32_t least = wave_min_u32(same ? (uint32_t)slot : 0xFFFFFFFFu);
+        if (lane == src) {
+          const unsigned long long want_rep = tag | (unsigned long long)least;
+          if (G.rep[o] > want_rep) atomicMin(G.rep + o, want_rep);
+        }
+        pend &= ~sm;
+      }
+    }
+  }
   if (want) slot = lslot[h];
   if (r < a.n_req)
     G.slot_of[r] = want && slot >= 0 ? (uint32_t)slot | (lead ? kGroupLead : 0u) : kGroupNoSlot;
@@ -575,50 +618,66 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
 // holders in bitmap off0): H* = the most frequent hit among the holders of
 // the first 64-instance word that has any; when at most kGroupHold holders
 // differ from it, the record keeps them (rec[1..]) and the result is the
-// class word {n_exc << 24 | H*}, else kGroupNone.  The wave's own hit writes
-// are read back under a workgroup-scope fence (a device-scope one writes
-// back the XCD's whole L2).
+// class word {n_exc << 24 | H*}, else kGroupNone.  Bitmap words are read 64
+// at a time (one per lane) and hits kClassChunk words at a time, all in
+// flight.  The
+// wave's own hit writes are read back under a workgroup-scope fence (a
+// device-scope one writes back the XCD's whole L2).
+template <int kClassChunk = 8>
 __device__ __forceinline__ uint32_t popular_class(const ScoreArgs& a, uint2* rec,
                                                   const uint32_t* hp, uint32_t off0, int32_t nw,
                                                   int lane) {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
   const uint64_t* bm = a.x.bitmaps + (size_t)off0 * a.x.nw;
-  uint32_t hs = 0u;
-  for (int32_t w = 0; w < nw; ++w) {
-    const uint64_t word = bm[w];
-    if (!word) continue;
-    const bool hold = ((word >> lane) & 1ull) != 0ull;
-    const uint32_t v = hold ? hp[w * 64 + lane] : 0u;
-    uint64_t rem = word;
-    uint32_t bestc = 0u;
-    while (rem) {
-      const uint32_t val = (uint32_t)__builtin_amdgcn_readlane((int)v, __builtin_ctzll(rem));
-      const uint64_t same = __ballot(hold && v == val);
-      rem &= ~same;
-      if ((uint32_t)__popcll(same) > bestc) {
-        bestc = (uint32_t)__popcll(same);
-        hs = val;
+  uint32_t hs = 0u, nexc = 0u;
+  bool have_hs = false;
+  for (int32_t wb = 0; wb < nw && nexc <= kGroupHold; wb += 64) {
+    const int32_t wn = nw - wb < 64 ? nw - wb : 64;
+    const uint64_t bmw = lane < wn ? bm[wb + lane] : 0ull;
+    for (int32_t w0 = 0; w0 < wn && nexc <= kGroupHold; w0 += kClassChunk) {
+      bool hold[kClassChunk];
+      uint32_t v[kClassChunk];
+#pragma unroll
+      for (int u = 0; u < kClassChunk; ++u) {
+        const uint64_t word = (uint64_t)lane_value64((int64_t)bmw, (w0 + u) & 63);
+        hold[u] = w0 + u < wn && ((word >> lane) & 1ull) != 0ull;
+        v[u] = hold[u] ? hp[(wb + w0 + u) * 64 + lane] : 0u;
       }
-    }
-    break;
-  }
-  uint32_t nexc = 0u;
-  for (int32_t w0 = 0; w0 < nw && nexc <= kGroupHold; w0 += 4) {  // four words in flight
-    bool hold[4];
-    uint32_t v[4];
+      if (!have_hs) {  // the mode over the first word with holders
+        uint64_t wsel = 0ull;
+        uint32_t vsel = 0u;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int32_t w = w0 + u;
-      hold[u] = w < nw && ((bm[w] >> lane) & 1ull) != 0ull;
-      v[u] = hold[u] ? hp[w * 64 + lane] : 0u;
-    }
+        for (int u = 0; u < kClassChunk; ++u) {
+          const uint64_t word = (uint64_t)lane_value64((int64_t)bmw, (w0 + u) & 63);
+          if (!wsel && w0 + u < wn && word) {
+            wsel = word;
+            vsel = v[u];
+          }
+        }
+        if (wsel) {
+          const bool hold0 = ((wsel >> lane) & 1ull) != 0ull;
+          uint64_t rem = wsel;
+          uint32_t bestc = 0u;
+          while (rem) {
+            const uint32_t val = (uint32_t)__builtin_amdgcn_readlane((int)vsel, __builtin_ctzll(rem));
+            const uint64_t same = __ballot(hold0 && vsel == val);
+            rem &= ~same;
+            if ((uint32_t)__popcll(same) > bestc) {
+              bestc = (uint32_t)__popcll(same);
+              hs = val;
+            }
+          }
+          have_hs = true;
+        }
+      }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const bool ex = hold[u] && v[u] != hs;
-      const uint64_t em = __ballot(ex);
-      const uint32_t k = nexc + (uint32_t)__popcll(em & ((1ull << lane) - 1ull));
-      if (ex && k < kGroupHold) rec[1 + k] = make_uint2((uint32_t)((w0 + u) * 64 + lane), v[u]);
-      nexc += (uint32_t)__popcll(em);
+      for (int u = 0; u < kClassChunk; ++u) {
+        const bool ex = hold[u] && v[u] != hs;
+        const uint64_t em = __ballot(ex);
+        const uint32_t k = nexc + (uint32_t)__popcll(em & ((1ull << lane) - 1ull));
+        if (ex && k < kGroupHold) rec[1 + k] = make_uint2((uint32_t)((wb + w0 + u) * 64 + lane), v[u]);
+        nexc += (uint32_t)__popcll(em);
+      }
     }
   }
   return (nexc <= kGroupHold && hs > 0u && hs < (1u << 24)) ? ((nexc << 24) | hs) : kGroupNone;
@@ -687,7 +746,9 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
     uint32_t cnt = 0u;
     if (found0 && cnt0 > kGroupHold) {
       if (part != 0u) continue;  // a popular group: one wave walks all holders
-      if (cnt0 > kPopular && G.pop_pass) continue;  // the popular pass's (it writes the record)
+      if (cnt0 > kPopular && G.pop_pass &&
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)rec[kGroupClsWord].y) != kGroupUnlisted)
+        continue;  // listed by the claim pass: the popular pass's (it writes the record)
       uint32_t row = 0;
       if (lane == 0) row = atomicAdd(G.pop_ctr, 1u);
       row = (uint32_t)__shfl((int)row, 0);
@@ -738,91 +799,14 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
 }
 
 // ------------------------------------------------------------ popular pass
-// Beside the walk pass, on a second stream: the groups whose first block
-// has a holder bitmap (more than kPopular holders; at c3, a 128-block system
-// prompt held by nearly every instance).  The walk pass would walk each of
+// Beside the walk pass (which runs on a second stream): the groups whose
+// first block has a holder bitmap (more than kPopular holders; e.g. a
+// 128-block system prompt held by nearly every instance).  The walk pass would walk each of
 // them through the index, eight positions per pair of dependent reads, all
 // over the same shared prefix.  Here the prefix is walked once per first
 // block (by its representative, every position of a round at once), and
 // each group starts from that walk at the end of its common prefix with the
 // representative's segment.
-
-// Leaders' list entry v of the window's kXcds lists taken back to back
-// (len: the lists' lengths).
-__device__ __forceinline__ unsigned long long list_entry(const GroupTab& G, const uint32_t* len,
-                                                         uint32_t v) {
-  uint32_t rem = v, lsel = 0u, isel = 0u;
-  bool done = false;
-#pragma unroll
-  for (int l = 0; l < kXcds; ++l) {
-    if (!done) {
-      if (rem < len[l]) {
-        lsel = (uint32_t)l;
-        isel = rem;
-        done = true;
-      } else {
-        rem -= len[l];
-      }
-    }
-  }
-  return G.lists[(size_t)lsel * G.lcap + isel];
-}
-
-// Popular pass 1: 64 leaders per wave and step, one per lane: the first
-// block's index entry; the groups whose first block has a holder bitmap go
-// into plist (one atomic per wave) and the least slot of each bitmap into
-// its representative word (one minimum per bitmap and wave, skipped when
-// the word already holds a lesser slot of this window: atomics on one
-// address queue).
-__global__ __launch_bounds__(64) void popular_list_kernel(ScoreArgs a) {
-  const GroupTab& G = a.grp;
-  const int lane = threadIdx.x;
-  uint32_t len[kXcds], total = 0u;
-#pragma unroll
-  for (int l = 0; l < kXcds; ++l) {
-    len[l] = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[l * kListCtrWords]);
-    total += len[l];
-  }
-  const unsigned long long tag = (kGroupGenMax - G.gen) << 32;
-  for (uint32_t base = blockIdx.x * 64u; base < total; base += gridDim.x * 64u) {
-    const uint32_t v = base + (uint32_t)lane;
-    bool pop = false;
-    uint32_t slot = 0u, off0 = 0u;
-    if (v < total) {
-      const unsigned long long ent = list_entry(G, len, v);
-      slot = (uint32_t)(ent & 0xFFFFFFull);
-      const uint64_t key0 = a.pool[(int64_t)(ent >> 24) - 1];
-      const uint32_t b = bucket_of(key0, kIndexSalt, a.x.shift);
-      const uint2 f = index_search(a.x, key0, b, index_bucket(a.x, b));
-      off0 = f.x;
-      pop = f.y > kPopular && off0 < G.rep_cap;
-    }
-    const uint64_t pm = __ballot(pop);
-    if (!pm) continue;
-    uint32_t k0 = 0u;
-    if (lane == 0) k0 = atomicAdd(&G.lctr[kPopCountWord], (uint32_t)__popcll(pm));
-    k0 = (uint32_t)__shfl((int)k0, 0);
-    const uint32_t k = k0 + (uint32_t)__popcll(pm & ((1ull << lane) - 1ull));
-    const bool listed = pop && k < G.plist_cap;
-    if (listed) G.plist[k] = make_uint2(slot, off0);
-    if (pop && !listed)  // no room: a record without a result (its requests walk on their own)
-      G.rec[(size_t)slot * kGroupRec] =
-          make_uint2((uint32_t)(G.plen[slot] & ((1ull << kGroupGenShift) - 1ull)), kGroupNone);
-    uint64_t pend = __ballot(listed);
-    while (pend) {
-      const int src = __builtin_ctzll(pend);
-      const uint32_t o = (uint32_t)__shfl((int)off0, src);
-      const bool same = listed && off0 == o;
-      const uint64_t sm = __ballot(same);
-      const uint32_t least = wave_min_u32(same ? slot : 0xFFFFFFFFu);
-      if (lane == src) {
-        const unsigned long long want = tag | (unsigned long long)least;
-        if (G.rep[o] > want) atomicMin(G.rep + o, want);
-      }
-      pend &= ~sm;
-    }
-  }
-}
 
 // Word `lane` of the holder bitmap of an index entry's holder list (cnt <=
 // kPopular ascending ids).
@@ -836,7 +820,7 @@ __device__ __forceinline__ uint64_t list_word(const GIndex& x, uint32_t off, uin
   return m;
 }
 
-// Popular pass 2: one workgroup of kPrefixWaves waves per representative
+// Popular pass 1: one workgroup of kPrefixWaves waves per representative
 // (found by scanning plist).  Rounds of kPrefixWaves x 32 positions of its
 // segment: wave w looks up its 32 positions (four lookups, then the 32
 // holder bitmaps, all in flight) and takes, for every holder of the first
@@ -974,7 +958,7 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(Score
   }
 }
 
-// Popular pass 3 (a persistent grid over plist): listed group v.  Its
+// Popular pass 2 (a persistent grid over plist): listed group v.  Its
 // segment and its representative's agree on their first k blocks
 // (compared here; k at most the prefix walk's end), so a holder whose first
 // missing position there is h < k has hit h here too, and the others hold
@@ -982,7 +966,6 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(Score
 // (one holder left: along its row, 512 positions per step).  Then the
 // record, as the walk pass writes it, with popular row pop_cap + v.
 constexpr int kMemberChunk = 16;  // bitmap words whose holders' hits are read together
-constexpr int kPopListGrid = 512;    // waves of the popular pass's list kernel
 constexpr int kPopPrefixGrid = 64;   // workgroups of its prefix kernel
 constexpr int kPopWalkGrid = 4096;   // waves of its member kernel
 
@@ -2494,19 +2477,19 @@ hipError_t ps_launch_group(const ScoreArgs& a, int grid, hipStream_t s, hipEvent
     hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, s, a);
     return hipGetLastError();
   }
-  // the popular pass on the second stream, forked after the claim pass and
-  // joined after the walk pass
+  // the walk pass on the second stream, forked after the claim pass (which
+  // lists the popular groups); the popular pass, the longer chain of
+  // dependent launches, stays on the calling stream, which then waits for
+  // the walk pass (long done by then: no cross-queue wake-up on the path)
   if (!aux || !fork || !join) return hipErrorInvalidValue;
   if ((e = hipEventRecord(fork, s)) != hipSuccess) return e;
   if ((e = hipStreamWaitEvent(aux, fork, 0)) != hipSuccess) return e;
-  hipLaunchKernelGGL(popular_list_kernel, dim3(kPopListGrid), dim3(64), 0, aux, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(popular_prefix_kernel, dim3(kPopPrefixGrid), dim3(64 * kPrefixWaves), 0, aux, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(popular_member_kernel, dim3(kPopWalkGrid), dim3(64), lds, aux, a);
+  hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, aux, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = hipEventRecord(join, aux)) != hipSuccess) return e;
-  hipLaunchKernelGGL(group_kernel, dim3(grid), dim3(64), lds, s, a);
+  hipLaunchKernelGGL(popular_prefix_kernel, dim3(kPopPrefixGrid), dim3(64 * kPrefixWaves), 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(popular_member_kernel, dim3(kPopWalkGrid), dim3(64), lds, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return hipStreamWaitEvent(s, join, 0);
 }

@@ -735,3 +735,45 @@ def test_popular_pass_shared_prefixes(ps, scorer):
         fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
         assert fixed.tobytes() == res.tobytes(), f"{base}: the walk pass alone decides differently"
         _check_edge(ps, scorer, w, f"long shared prefix {base} eta=1", eta=1.0)
+
+
+def _dwindling_prefix_window(base=411, survivor_len=300):
+    """A shared prefix held by 100 instances for its first 40 blocks and
+    by one (or two) of them further, to survivor_len: the popular pass's
+    prefix walk stops at its first round's end with one holder live, before
+    the 290 blocks that sessions A and B still share, so that holder is
+    walked again from the stop."""
+    SP = chain_hashes(300, base=base)
+    own = {k: chain_hashes(20, base=base + (k + 1) * 10**6) for k in range(3)}
+    segs = {0: SP + own[0], 1: SP[:290] + own[1], 2: SP[:35] + own[2]}
+    pool = []
+
+    def put(seq):
+        off = len(pool)
+        pool.extend(seq)
+        return off
+
+    seg_off = {k: put(v) for k, v in segs.items()}
+    n_inst = 110
+    filler = chain_hashes(2000, base=base + 5 * 10**7)
+    sets = [list(SP[:40]) + list(filler[5 * i:5 * i + 2]) for i in range(100)]
+    sets[7] = list(SP[:survivor_len]) + list(own[0][:10]) + list(own[1][:5])
+    sets[50] = list(SP[:survivor_len // 2]) + list(own[1][:3])
+    sets += [list(filler[1000 + 5 * i:1002 + 5 * i]) for i in range(10)]
+    reqs = []
+    for k in range(3):
+        L = len(segs[k])
+        for p in (L, L - 10, L - 25):
+            reqs.append((seg_off[k], p, put(chain_hashes(2, base=base + 10**8 + len(pool))), 2))
+    return _edge(sets, None, pool=pool, reqs=reqs, cap=1024)
+
+
+def test_popular_pass_early_prefix_stop(ps, scorer):
+    """The prefix walk stops with one holder live before the common prefix
+    of two groups ends: that holder is walked from the stop (holding the
+    rest, or not)."""
+    for surv in (300, 200, 41):
+        w = _dwindling_prefix_window(survivor_len=surv)
+        res = _check_edge(ps, scorer, w, f"dwindling prefix {surv}")
+        fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
+        assert fixed.tobytes() == res.tobytes(), f"{surv}: the walk pass alone decides differently"
