@@ -821,15 +821,16 @@ __device__ __forceinline__ uint64_t list_word(const GIndex& x, uint32_t off, uin
 }
 
 // Popular pass 1: one workgroup of kPrefixWaves waves per representative
-// (found by scanning plist).  Rounds of kPrefixWaves x 32 positions of its
-// segment: wave w looks up its 32 positions (four lookups, then the 32
-// holder bitmaps, all in flight) and takes, for every holder of the first
-// block, the first of them it lacks; the least over the waves (an LDS
-// minimum) is the holder's first missing position.  Rounds go on while
-// more than one holder holds every position so far.  Row `pre` of the
-// bitmap: that position, or ~0 for the holders that have all of them; pre_q:
-// the round's end.  Pools of at most 64 x kPopWords instances (the live set
-// is one bitmap word per lane).
+// (the bitmaps whose representative word this window's claim pass set).
+// Rounds of kPrefixWaves x 32 positions of its segment: wave w looks up its
+// 32 positions (four lookups, then the 32 holder bitmaps, all in flight)
+// and takes, for every holder of the first block, the first of them it
+// lacks; the least over the waves (an LDS minimum) is the holder's first
+// missing position, and the AND of the waves' survivors (LDS words) the
+// holders with every position so far.  Rounds go on while more than one
+// holder is left.  Row `pre` of the bitmap: that position, or ~0 for the
+// holders that have all of them; pre_q: the round's end.  Pools of at most
+// 64 x kPopWords instances (the live set is one bitmap word per lane).
 constexpr int kPrefixWaves = 4;
 constexpr int kPrefixSpan = 32;  // positions per wave and round
 constexpr int32_t kPrefixMax = 1 << 14;
@@ -837,30 +838,31 @@ constexpr int32_t kPrefixMax = 1 << 14;
 __global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(ScoreArgs a) {
   __shared__ uint64_t stage[kStage];
   __shared__ uint32_t fmiss[64 * kPopWords];  // first missing position per instance (~0: none)
-  __shared__ uint32_t reps[64 * kPrefixWaves], n_reps, live_part[kPrefixWaves];
+  __shared__ uint64_t firstw[kPopWords], livew[kPopWords];
+  __shared__ uint2 reps[64 * kPrefixWaves];  // {bitmap, representative slot}
+  __shared__ uint32_t n_reps, n_live;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g = lane >> 3, s = lane & 7;
   const GroupTab& G = a.grp;
   const unsigned long long lmask = (1ull << kGroupGenShift) - 1ull;
   const int32_t nw = (a.n_inst + 63) >> 6;
   if (nw > kPopWords) return;
-  uint32_t n = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[kPopCountWord]);
-  n = n < G.plist_cap ? n : G.plist_cap;
+  const uint32_t tag = (uint32_t)(kGroupGenMax - G.gen);
   const uint32_t chunk = 64u * kPrefixWaves;
-  for (uint32_t base = blockIdx.x * chunk; base < n; base += gridDim.x * chunk) {
-    // the representatives among these listed groups
+  for (uint32_t base = blockIdx.x * chunk; base < G.rep_cap; base += gridDim.x * chunk) {
+    // the bitmaps of this chunk that first blocks of listed groups have
     if (tid == 0) n_reps = 0u;
     __syncthreads();
-    const uint32_t vl = base + (uint32_t)tid;
-    if (vl < n) {
-      const uint2 el = G.plist[vl];
-      if ((uint32_t)G.rep[el.y] == el.x) reps[atomicAdd(&n_reps, 1u)] = vl;
+    const uint32_t bn = base + (uint32_t)tid;
+    if (bn < G.rep_cap) {
+      const unsigned long long rw = G.rep[bn];
+      if ((uint32_t)(rw >> 32) == tag) reps[atomicAdd(&n_reps, 1u)] = make_uint2(bn, (uint32_t)rw);
     }
     __syncthreads();
     const uint32_t nr = n_reps;
     for (uint32_t r = 0; r < nr; ++r) {
-      const uint2 ent = G.plist[reps[r]];
-      const uint32_t slot = ent.x, off0 = ent.y;
+      const uint2 ent = reps[r];
+      const uint32_t off0 = ent.x, slot = ent.y;
       const int64_t pre_off = (int64_t)(G.keys[slot] & lmask) - 1;
       const int32_t plen = (int32_t)(G.plen[slot] & lmask);
       const int32_t lim = plen < kPrefixMax ? plen : kPrefixMax;
@@ -869,6 +871,10 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(Score
       for (int32_t j = tid; j < nst; j += 64 * kPrefixWaves) stage[j] = c.pre[j];
       for (int32_t i = tid; i < 64 * nw; i += 64 * kPrefixWaves) fmiss[i] = 0xFFFFFFFFu;
       const uint64_t first = lane < nw ? a.x.bitmaps[(size_t)off0 * a.x.nw + lane] : 0ull;
+      if (wv == 0 && lane < nw) {
+        firstw[lane] = first;
+        livew[lane] = first;
+      }
       __syncthreads();
       int32_t p = 1;
       uint32_t nalive = 2u;
@@ -921,37 +927,20 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(Score
             have &= keep;
           }
         }
+        if (lane < nw) atomicAnd(reinterpret_cast<unsigned long long*>(&livew[lane]), have);
         __syncthreads();
-        // holders with every position so far (the first wave's words)
-        const int32_t pe = p + kPrefixWaves * kPrefixSpan < lim ? p + kPrefixWaves * kPrefixSpan : lim;
-        uint64_t all = 0ull;
-        if (wv == 0 && lane < nw) {
-          uint64_t w = first;
-          while (w) {
-            const int b = __builtin_ctzll(w);
-            w &= w - 1ull;
-            if (fmiss[lane * 64 + b] == 0xFFFFFFFFu) all |= 1ull << b;
-          }
-        }
-        if (wv == 0) {
-          const uint32_t cnt = wave_sum_u32((uint32_t)__popcll(all));
-          if (lane == 0) live_part[0] = cnt;
+        if (wv == 0) {  // holders with every position so far
+          const uint32_t cnt = wave_sum_u32(lane < nw ? (uint32_t)__popcll(livew[lane]) : 0u);
+          if (lane == 0) n_live = cnt;
         }
         __syncthreads();
-        nalive = live_part[0];
-        p = pe;
-        __syncthreads();
+        nalive = n_live;
+        p = p + kPrefixWaves * kPrefixSpan < lim ? p + kPrefixWaves * kPrefixSpan : lim;
       }
       // row of the bitmap: the holders' first missing positions
       uint32_t* row = G.pre + (size_t)off0 * (size_t)a.n_inst;
-      if (wv == 0 && lane < nw) {
-        uint64_t w = first;
-        while (w) {
-          const int b = __builtin_ctzll(w);
-          w &= w - 1ull;
-          row[lane * 64 + b] = fmiss[lane * 64 + b];
-        }
-      }
+      for (int32_t i = tid; i < a.n_inst; i += 64 * kPrefixWaves)
+        if ((firstw[i >> 6] >> (i & 63)) & 1ull) row[i] = fmiss[i];
       if (tid == 0) G.pre_q[off0] = (uint32_t)p;
       __syncthreads();
     }
