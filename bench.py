@@ -200,16 +200,18 @@ def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
     """Algorithmic bytes of the prefix-group pass, as (claim pass, walk).
     Claim: descriptor, slot read, the claiming compare-and-swap, the length
     maximum and the slot entry per request, a leader-list entry per group.
-    Walk: slot entry per request; per group its segment head staged (<= 256
-    hashes), one index bucket, the holder ids (or bitmap), then with at most
-    GROUP_HOLD holders per holder a probe of the first block with its row
-    position, 16 bytes per compared position, a final probe where the
-    segment leaves the cache, and the record; with more, the holders walked
-    together through the index and one 4-byte hit per holder in the popular
-    row, and for more than 64 holders the bitmap and the hits read back for
-    the shared-hit class, and its word.  On pools of at most 4,096
+    Walk: slot entry per request; per group its list entry and length, its
+    first block and one index bucket, then with at most GROUP_HOLD holders
+    their ids and per holder a probe of the first block with its row
+    position, 16 bytes per compared position (chain and row), a final probe
+    where the segment leaves the cache, and the record; with more, the
+    segment head staged (<= 256 hashes), the holder ids (or bitmap), the
+    holders walked together through the index and one 4-byte hit per holder
+    in the popular row, and for more than 64 holders the bitmap and the hits
+    read back for the shared-hit class, and its word.  On pools of at most 4,096
     instances, groups whose first block has more than 64 holders go to the
-    popular pass instead, listed by the claim pass (per leader its first
+    popular pass instead (the walk pass reads their class word), listed by
+    the claim pass (per leader its first
     block and index bucket, per listed group its entry, class word and
     representative minimum; counted when the window has such groups), per
     first block one walk of its representative's segment through the index
@@ -227,16 +229,21 @@ def group_pass_bytes(win, gid, rep, plen, Hk, Hv):
     walk = 4 * R
     gk = Hk // N
     cnt0 = np.bincount(gk, minlength=G)
-    walk += int((16 + 8 * np.minimum(plen, 256) + 128 +
-                 np.where(cnt0 > 64, 8 * nw, 2 * cnt0)).sum())
     ok = cnt0 <= GROUP_HOLD
+    pop_pass = N <= 64 * POP_WORDS and bool((cnt0 > 64).any())
+    in_pop = (cnt0 > 64) & pop_pass
+    # per group: list entry and length, first block, index bucket; then the
+    # holder ids (few), the class word (popular pass), or the staged head and
+    # the holder ids or bitmap (the walk pass's index walk)
+    walk += int((16 + 8 + 128 + np.where(
+        ok, 2 * cnt0, np.where(in_pop, 8, 8 * np.minimum(plen, 256) +
+                               np.where(cnt0 > 64, 8 * nw, 2 * cnt0)))).sum())
     pl = plen[gk]
     w = np.where(pl > 1, PROBE_ROWPOS + 16 * np.minimum(Hv, pl - 1) + BUCKET_BYTES * (Hv < pl),
                  PROBE_ROWPOS)
     walk += int(w[ok[gk]].sum()) + int((8 + 8 * cnt0[ok]).sum())
     start = np.concatenate([[0], np.cumsum(cnt0)])
     popular = np.nonzero(~ok)[0]
-    pop_pass = N <= 64 * POP_WORDS and bool((cnt0 > 64).any())
     if pop_pass:
         # the claim pass lists the popular pass's groups: per leader its
         # first block and index bucket; per listed group its entry, class

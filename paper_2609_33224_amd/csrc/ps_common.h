@@ -427,17 +427,21 @@ __device__ __forceinline__ int32_t run_compare(const ChainRef& c, const uint64_t
 // begin another run of the row, e.g. after a shared system prompt).  A run
 // shorter than 8 blocks hands the rest of the walk to the octet walk.
 // Wave-uniform arguments; returns the hit.  U0 = positions per lane in the
-// first step.
+// first step; key_at: the chain's block at `pos` when the caller has it (0:
+// read it).
 template <bool STAGED, int W = kWalkU, int U0 = 4>
 __device__ __forceinline__ uint32_t run_walk(const Tables& t, uint32_t inst, const ChainRef& c,
-                             const uint64_t* stage, int32_t pos, int g, int s) {
+                             const uint64_t* stage, int32_t pos, int g, int s,
+                             uint64_t key_at = 0ull) {
   const int lane = g * 8 + s;
   const int32_t ell = c.len;
   const uint64_t* tab = table_of(t, inst);
   const uint64_t* row = t.rows + (size_t)inst * (size_t)t.row_cap;
   const int64_t rlen = t.count[inst];
   while (pos < ell) {
-    const uint64_t key = (STAGED && pos < kStage) ? stage[pos] : chain_global(c, pos);
+    const uint64_t key = key_at != 0ull ? key_at
+                         : (STAGED && pos < kStage) ? stage[pos] : chain_global(c, pos);
+    key_at = 0ull;
     if (key == 0ull) return (uint32_t)pos;
     uint32_t b = bucket_of(key, inst, t.shift);
     int64_t rp = -1;

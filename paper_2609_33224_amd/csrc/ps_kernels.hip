@@ -735,11 +735,10 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
     const int32_t s1 = s0 + step < plen ? s0 + step : plen;
     if (part != 0u && s0 >= plen) continue;  // (uniform: no workgroup barrier skipped)
     const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
-    const int32_t nst = plen < kStage ? plen : kStage;
-    __syncthreads();
-    for (int32_t j = lane; j < nst; j += 64) stage[j] = c.pre[j];
-    __syncthreads();
-    const IdxHit h0 = index_lookup(a.x, stage[0], g == 0, g, s);
+    // the segment's first block, read beside its length (the holders' row
+    // walks read the chain directly; only the index walk stages its head)
+    const uint64_t key0 = c.pre[0];
+    const IdxHit h0 = index_lookup(a.x, key0, g == 0, g, s);
     const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
     const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
     uint2* rec = G.rec + (size_t)slot * kGroupRec;
@@ -749,6 +748,10 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
       if (cnt0 > kPopular && G.pop_pass &&
           (uint32_t)__builtin_amdgcn_readfirstlane((int)rec[kGroupClsWord].y) != kGroupUnlisted)
         continue;  // listed by the claim pass: the popular pass's (it writes the record)
+      const int32_t nst = plen < kStage ? plen : kStage;
+      __syncthreads();  // (the previous index walk is done with the stage)
+      for (int32_t j = lane; j < nst; j += 64) stage[j] = c.pre[j];
+      __syncthreads();
       uint32_t row = 0;
       if (lane == 0) row = atomicAdd(G.pop_ctr, 1u);
       row = (uint32_t)__shfl((int)row, 0);
@@ -781,7 +784,8 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
       for (uint32_t k = 0; k < cnt0; ++k) {
         const uint32_t idk = (uint32_t)__shfl((int)id, (int)k);
         // a group's segment is typically a long run: 512 positions per step
-        const uint32_t hk = s0 < s1 ? run_walk<true, 8, 8>(a.t, idk, cp, stage, s0, g, s) : (uint32_t)s1;
+        const uint32_t hk =
+            s0 < s1 ? run_walk<false, 8, 8>(a.t, idk, cp, nullptr, s0, g, s, s0 == 0 ? key0 : 0ull) : (uint32_t)s1;
         if ((uint32_t)lane == k) myhit = (int32_t)hk < s1 ? hk : (uint32_t)plen;  // no miss here: plen
       }
       if ((uint32_t)lane < cnt0) {
