@@ -777,3 +777,44 @@ def test_popular_pass_early_prefix_stop(ps, scorer):
         res = _check_edge(ps, scorer, w, f"dwindling prefix {surv}")
         fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
         assert fixed.tobytes() == res.tobytes(), f"{surv}: the walk pass alone decides differently"
+
+
+def _many_popular_groups_window(n_groups, n_inst=4096, base=431):
+    """n_groups sessions whose segments all start with one block held by
+    every instance (a holder bitmap), each then on its own 9 blocks held in
+    part by one or two owners: more popular groups than the popular pass's
+    list has rows at 4,096 instances (4,096), and past that more than the
+    walk pass's own popular rows hold, so groups take all three paths."""
+    rng = np.random.default_rng(base)
+    B0 = chain_hashes(1, base=base)[0]
+    own = chain_hashes(9 * n_groups, base=base + 10**6)
+    pool, reqs = [], []
+    tail_off = 0
+    # a shared four-block tail (with two or three blocks one request length
+    # puts the recomputation ratio of the first block's holders within
+    # 1e-5 of eta against the owners' hits: 0.6% near-boundary decisions)
+    pool.extend(chain_hashes(4, base=base + 10**8))
+    sets = [[B0] for _ in range(n_inst)]
+    for k in range(n_groups):
+        off = len(pool)
+        blocks = own[9 * k:9 * k + 9]
+        pool.append(B0)
+        pool.extend(blocks)
+        for j, i in enumerate(rng.choice(n_inst, 1 + (k % 2), replace=False)):
+            keep = int(rng.integers(0, 10))
+            sets[i].extend(blocks[:keep])
+        reqs.append((off, 10 if k % 3 else 9, tail_off, 4))
+    order = rng.permutation(len(reqs))
+    reqs = [reqs[i] for i in order]
+    return _edge(sets, None, pool=pool, reqs=reqs, cap=64)
+
+
+def test_popular_list_overflow(ps, scorer):
+    """8,500 popular groups at 4,096 instances: 4,096 in the popular pass,
+    the rest in the walk pass until its popular rows run out, the last ones
+    without a record (their requests walk on their own): oracle parity on
+    every request, and byte for byte the allocation-free entry point."""
+    w = _many_popular_groups_window(8500)
+    res = _check_edge(ps, scorer, w, "8,500 popular groups")
+    fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
+    assert fixed.tobytes() == res.tobytes(), "the walk pass alone decides differently"
