@@ -2070,17 +2070,32 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   const int64_t room63 = ltop[63].room;  // the 64th largest
   auto state_of = [&](uint32_t i) -> InstState { return SMALL ? linst[i] : a.inst[i]; };
   bool deferred_any = false;
+  // Descriptor and slot of the row's request (every lane of a row reads its
+  // row's); the next batch's are read near the end of the batch before, as
+  // vectors (register tuples the loads fill in place) and unconditionally
+  // at a request clamped into the window (n_req >= 1 here): a branch around
+  // them would end in register copies that wait for the loads.
+  uint4 qa;
+  uint2 qb;
+  uint32_t gn;
+  auto read_desc = [&](int32_t rq) {
+    const int32_t rc = rq < a.n_req ? rq : a.n_req - 1;
+    const char* d = reinterpret_cast<const char*>(a.reqs + rc);
+    qa = *reinterpret_cast<const uint4*>(d);
+    qb = *reinterpret_cast<const uint2*>(d + 16);
+    gn = a.grp.slot_of[rc];
+  };
+  static_assert(sizeof(ps_req) == 24, "a descriptor is 16 + 8 bytes");
+  read_desc((int32_t)blockIdx.x * 4 + q);
 
   for (int32_t rb = blockIdx.x * 4; rb < a.n_req; rb += gridDim.x * 4) {
     const int32_t r = rb + q;
     const bool inr = r < a.n_req;
-    // descriptor and slot (every lane of a row reads its row's), then the record
-    ps_req qd{0, 0, 0, 0};
-    uint32_t gso = kGroupNoSlot;
-    if (inr) {
-      qd = a.reqs[r];
-      gso = a.grp.slot_of[r];
-    }
+    // descriptor and slot, then the record
+    const ps_req qd = inr ? ps_req{(int64_t)(((uint64_t)qa.y << 32) | qa.x),
+                                   (int64_t)(((uint64_t)qa.w << 32) | qa.z), (int32_t)qb.x, (int32_t)qb.y}
+                          : ps_req{0, 0, 0, 0};
+    const uint32_t gso = inr ? gn : kGroupNoSlot;
     const bool valid = inr && req_valid(qd, a.pool_len);
     uint32_t cnt = kGroupNone;
     uint2 hd = make_uint2(0u, 0u);
@@ -2223,15 +2238,28 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
     const uint64_t kF = row_min_u64(acc.keyF);
     const uint64_t keyF = keyT == ~0ull ? kF : ~0ull;
     ps_result res{-1, 0, 0.0f, 0.0f, PS_R_REJECT};
-    if (fate == 0u && (keyT != ~0ull || keyF != ~0ull)) {
-      const bool tt = keyT != ~0ull;
-      const uint32_t best = (uint32_t)((tt ? keyT : keyF) & 0xFFFFu);
-      // the chosen instance's state is read again (keeping the holders'
-      // states live to here would spill); its hit from the holder's lane
+    const bool chosen = fate == 0u && (keyT != ~0ull || keyF != ~0ull);
+    const bool tt = keyT != ~0ull;
+    const uint32_t best = (uint32_t)((tt ? keyT : keyF) & 0xFFFFu);
+    // the chosen instance's state is read again (keeping the holders'
+    // states live to here would spill)
+    InstState bs{};
+    if (chosen) bs = state_of(best);
+    // the next batch's descriptors and slots, issued after this batch's last
+    // read: vector loads return in order, so issued earlier these (usually
+    // HBM misses) would hold up this batch's waits for its own L2 hits (an
+    // earlier variant that read them at the start of the batch was 124 ->
+    // 131 us at 4,096 x 262,144; this one 107 -> 105 us)
+    __builtin_amdgcn_sched_barrier(0);
+    {
+      read_desc(rb + (int32_t)gridDim.x * 4 + q);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (chosen) {
+      // its hit from the holder's lane
       const uint32_t hb = row_bits(__ballot(el && id == best));
       const int src = (lane & 48) + (hb ? __builtin_ctz(hb) : 0);
       const uint32_t sv = (uint32_t)__shfl((int)hit, src);
-      const InstState bs = state_of(best);
       const uint32_t v = hb ? sv : 0u;
       const int64_t c_tok = (int64_t)v * m.bs;
       const Lat lt = latency(m, bs, (float)(L - c_tok), (float)c_tok, L);
