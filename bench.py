@@ -611,8 +611,11 @@ def algorithmic_bytes(sc, win, d_pool, chunk_pairs=1 << 25):
         lean_b += lb
         gen_b += gb
     pair_b += 24 * N
+    # the key-only variant: 8 bytes (the key) per probe instead of the bucket
+    probe_key = probe_b - n_probes * (BUCKET_BYTES - 8)
     return dict(claim=claim_b, walk=walk_b, lean=lean_b, general=gen_b, probe=probe_b,
-                probes=n_probes, pairs=pair_b, groups=G, popular_groups=int(g_pop.sum()))
+                probe_key_only=probe_key, probes=n_probes, pairs=pair_b, groups=G,
+                popular_groups=int(g_pop.sum()))
 
 
 def traffic_for(workload: str, src_hash: str):
@@ -638,13 +641,13 @@ def cpu_baseline(win, budget_s: float):
     threads = oracle.max_threads()
     n0 = min(win.n_req, 2048)
     t0 = time.perf_counter()
-    o.window_score(win.subset(range(n0)))
+    o.window_score(win.subset(range(n0)), nthreads=threads)
     per_req = (time.perf_counter() - t0) / n0
     if per_req * win.n_req < budget_s:
         reps = max(1, int(budget_s / max(per_req * win.n_req, 1e-3)))
         t0 = time.perf_counter()
         for _ in range(reps):
-            o.window_score(win)
+            o.window_score(win, nthreads=threads)
         dt = (time.perf_counter() - t0) / reps
         n, sample = win.n_req, (f"whole window ({win.n_req} requests x {win.n_inst} instances), "
                                 f"{reps} repetitions")
@@ -652,13 +655,22 @@ def cpu_baseline(win, budget_s: float):
         n = max(n0, min(win.n_req, int(budget_s / per_req)))
         sub = win.subset(range(n))
         t0 = time.perf_counter()
-        o.window_score(sub)
+        o.window_score(sub, nthreads=threads)
         dt = time.perf_counter() - t0
         sample = (f"first {n} of {win.n_req} requests x {win.n_inst} instances, once "
                   f"(sized from a timed slice of {n0})")
+    # one core, on a leading slice of about two seconds
+    n1 = max(1, min(win.n_req, int(2.0 / max(per_req * threads, 1e-9))))
+    t0 = time.perf_counter()
+    o.window_score(win.subset(range(n1)), nthreads=1)
+    dt1 = time.perf_counter() - t0
     o.close()
     return dict(value=n * win.n_inst / dt, unit="candidate evals/s", cores=threads,
-                kind="oracle", decisions_per_s=n / dt, seconds=dt, sample=sample)
+                kind="oracle", decisions_per_s=n / dt, seconds=dt, sample=sample,
+                one_core=dict(value=n1 * win.n_inst / dt1, unit="candidate evals/s", cores=1,
+                              decisions_per_s=n1 / dt1,
+                              sample=f"first {n1} of {win.n_req} requests x {win.n_inst} "
+                                     f"instances, once"))
 
 
 def cpu_sequential_baseline(win, budget_s: float):
@@ -888,7 +900,8 @@ def main():
         sc.score_dev(d_pool, len(win.pool), d_reqs, win.n_req, d_out, None, stream)
         b.record(stream)
     torch.cuda.synchronize()
-    step_avg = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    step_ev = [a.elapsed_time(b) for a, b in ev]
+    step_avg = float(np.mean(step_ev))
     # The same steps again with the library's events around each of its
     # launches, recorded on the launch stream.
     sc.set_timing(True)
@@ -943,6 +956,7 @@ def main():
                    "n_inst": win.n_inst, "n_req": win.n_req, "seed": args.seed},
         "decisions_per_s": win.n_req / (ms_per_step * 1e-3),
         "step_ms_events": step_avg,
+        "step_ms_events_median": float(np.median(step_ev)),
         "roofline": {"bound": "hbm", "achieved": dk["achieved_GBs"], "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": dk["frac_of_hbm_peak"], "traffic": dk["counter_bytes"],
                      "kernel": dom},
@@ -962,6 +976,8 @@ def main():
                          "ms_per_window": probe_ms, "probes": nb["probes"] if nb else None,
                          "algorithmic_bytes": nb["probe"] if nb else None,
                          "achieved_GBs": probe_gbs,
+                         "algorithmic_bytes_key_only": nb["probe_key_only"] if nb else None,
+                         "achieved_GBs_key_only": rate(nb["probe_key_only"] if nb else None, probe_ms),
                          "frac_of_hbm_peak": probe_gbs / HBM_PEAK_GBS if probe_gbs is not None else None,
                          "measured_bytes": probe_meas,
                          "measured_GBs": rate(probe_meas, probe_ms),
