@@ -814,8 +814,9 @@ def main():
                          "kernel of known size, to scale the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the request-sharded multi-GPU design is described in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: the scorer runs on one GPU; --gpus {args.gpus} is not supported "
+              "(more GPUs would each score a slice of the requests against replicated "
+              "instance tables)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
