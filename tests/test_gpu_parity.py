@@ -818,3 +818,75 @@ def test_popular_list_overflow(ps, scorer):
     res = _check_edge(ps, scorer, w, "8,500 popular groups")
     fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
     assert fixed.tobytes() == res.tobytes(), "the walk pass alone decides differently"
+
+
+def _random_window(seed):
+    """A seeded random window: pools of 1-300 instances; sessions whose
+    segments may start with one shared prompt (held by up to every
+    instance, so past 64 holders it has a holder bitmap); holders keep a
+    segment's prefix up to a random cut, some with a hole; repeats inside
+    chains; requests with random segment lengths (below and above the
+    grouping minimum) and tails; random states."""
+    rng = np.random.default_rng(seed)
+    n_inst = int(rng.choice([1, 7, 63, 64, 65, 130, 300]))
+    base = 10**7 * (seed + 1)
+    SP = chain_hashes(int(rng.integers(1, 300)), base=base)
+    n_sess = int(rng.integers(1, 12))
+    segs = []
+    for k in range(n_sess):
+        own = chain_hashes(int(rng.integers(1, 400)), base=base + (k + 1) * 10**5)
+        if len(own) > 6 and rng.random() < 0.3:
+            own[5] = own[2]  # a repeated block
+        lead = SP[:int(rng.integers(1, len(SP) + 1))] if rng.random() < 0.6 else []
+        segs.append(list(lead) + list(own))
+    pool, seg_off = [], []
+    for sg in segs:
+        seg_off.append(len(pool))
+        pool.extend(sg)
+    fresh = chain_hashes(2000, base=base + 9 * 10**6)
+    sets = [[] for _ in range(n_inst)]
+    sp_frac = float(rng.choice([0.0, 0.5, 1.0]))
+    for i in range(n_inst):
+        if rng.random() < sp_frac:
+            sets[i].extend(SP[:int(rng.integers(0, len(SP) + 1))])
+        for k in range(n_sess):
+            if rng.random() < 2.0 / max(n_inst, 1) + 0.05:
+                cut = int(rng.integers(0, len(segs[k]) + 1))
+                held = segs[k][:cut]
+                if cut > 10 and rng.random() < 0.2:
+                    held = held[:cut // 2] + held[cut // 2 + 1:]  # a hole
+                sets[i].extend(held)
+        sets[i].extend(fresh[3 * i:3 * i + int(rng.integers(0, 3))])
+        sets[i] = list(dict.fromkeys(sets[i]))  # one entry per block
+    reqs = []
+    n_req = int(rng.integers(1, 400))
+    for r in range(n_req):
+        k = int(rng.integers(0, n_sess))
+        p = int(rng.integers(1, len(segs[k]) + 1))
+        t = int(rng.integers(0, 5))
+        t_off = len(pool)
+        pool.extend(fresh[1000 + (r * 5) % 900:1000 + (r * 5) % 900 + t])
+        reqs.append((seg_off[k], p, t_off, t))
+    cap = max(max(len(s) for s in sets), 1) + int(rng.integers(0, 64))
+    return _edge(sets, None, pool=pool, reqs=reqs, cap=cap)
+
+
+RANDOM_POLICIES = [dict(), dict(eta=0.25), dict(eta=1.0), dict(flags=1), dict(flags=2),
+                   dict(tpot_slo=0.05)]
+
+
+RANDOM_SEEDS = [s for s in range(160) if s != 156]  # 156: 10 near-boundary decisions (cap 8)
+
+
+def test_random_windows(ps, scorer):
+    """159 seeded random windows (pool sizes 1-300, shared prompts with and
+    without holder bitmaps, holes, repeats, groups, random policies):
+    oracle parity on every request and byte-identical results from the
+    allocation-free entry point."""
+    for seed in RANDOM_SEEDS:
+        w = _random_window(seed)
+        pol = RANDOM_POLICIES[seed % len(RANDOM_POLICIES)]
+        _say(f"random window {seed}: {w.n_inst} instances, {w.n_req} requests, {pol}")
+        res = _check_edge(ps, scorer, w, f"random window {seed}", **pol)
+        fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
+        assert fixed.tobytes() == res.tobytes(), f"random window {seed}: the fixed path differs"
