@@ -365,3 +365,18 @@ def test_speculation_setting_errors(ps, scorer):
         assert e.value.code == ps.binding.PS_E_INVAL
     scorer.set_schedule_speculation(0)
     scorer.set_schedule_speculation(256)
+
+
+def test_schedule_random_windows(ps, scorer):
+    """100 of the seeded random windows scheduled per arrival: every
+    request, the refused blocks and the final state against the oracle's
+    schedule, a snapshot scored afterwards, and speculative batches of 64
+    byte for byte against scoring every request in full."""
+    from tests.test_gpu_parity import RANDOM_POLICIES, _random_window
+    for seed in range(100):
+        w = _random_window(seed)
+        pol = RANDOM_POLICIES[seed % len(RANDOM_POLICIES)]
+        label = f"random window {seed} ({w.n_inst} x {w.n_req}, {pol})"
+        _say(label)
+        _schedule_check(ps, scorer, w, label, **pol)
+        _assert_same_schedule(_schedule_spec_and_full(ps, scorer, w, 64, **pol), w.n_req, label)
