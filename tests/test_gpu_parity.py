@@ -890,3 +890,53 @@ def test_random_windows(ps, scorer):
         res = _check_edge(ps, scorer, w, f"random window {seed}", **pol)
         fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
         assert fixed.tobytes() == res.tobytes(), f"random window {seed}: the fixed path differs"
+
+
+def _random_window_large(seed):
+    """Larger seeded random windows: 1,000-4,096 instances (holder bitmaps
+    of up to 64 words), segments of up to 6,000 blocks (past every staged
+    chain head), a shared prompt held by most instances, 200-2,000
+    requests over few sessions (groups of many members)."""
+    rng = np.random.default_rng(10**6 + seed)
+    n_inst = int(rng.choice([1000, 2100, 4096]))
+    base = 10**8 * (seed + 1)
+    SP = chain_hashes(int(rng.integers(50, 400)), base=base)
+    n_sess = int(rng.integers(2, 20))
+    segs = []
+    for k in range(n_sess):
+        own = chain_hashes(int(rng.integers(10, 6000)), base=base + (k + 1) * 10**6)
+        lead = SP[:int(rng.integers(1, len(SP) + 1))] if rng.random() < 0.7 else []
+        segs.append(list(lead) + list(own))
+    pool, seg_off = [], []
+    for sg in segs:
+        seg_off.append(len(pool))
+        pool.extend(sg)
+    sets = [[] for _ in range(n_inst)]
+    for i in np.nonzero(rng.random(n_inst) < 0.8)[0]:
+        sets[i].extend(SP[:int(rng.integers(len(SP) // 2, len(SP) + 1))])
+    for k in range(n_sess):  # each session on one to three owners
+        for i in rng.choice(n_inst, int(rng.integers(1, 4)), replace=False):
+            sets[i].extend(segs[k][:int(rng.integers(0, len(segs[k]) + 1))])
+    sets = [list(dict.fromkeys(s)) for s in sets]
+    fresh = chain_hashes(20000, base=base + 9 * 10**7)
+    reqs = []
+    for r in range(int(rng.integers(200, 2000))):
+        k = int(rng.integers(0, n_sess))
+        t = int(rng.integers(0, 4))
+        t_off = len(pool)
+        pool.extend(fresh[(r * 4) % 19000:(r * 4) % 19000 + t])
+        reqs.append((seg_off[k], int(rng.integers(1, len(segs[k]) + 1)), t_off, t))
+    cap = max(max(len(s) for s in sets), 1) + 64
+    return _edge(sets, None, pool=pool, reqs=reqs, cap=cap)
+
+
+def test_random_windows_large(ps, scorer):
+    """Twelve larger seeded random windows (1,000-4,096 instances, chains
+    of up to 6,000 blocks, large groups): oracle parity and byte-identical
+    results from the allocation-free entry point."""
+    for seed in range(12):
+        w = _random_window_large(seed)
+        _say(f"large random window {seed}: {w.n_inst} instances, {w.n_req} requests")
+        res = _check_edge(ps, scorer, w, f"large random window {seed}")
+        fixed, _ = DeviceWindow(w).score(scorer, fixed=True)
+        assert fixed.tobytes() == res.tobytes(), f"large random window {seed}: the fixed path differs"
