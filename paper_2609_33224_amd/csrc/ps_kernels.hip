@@ -299,8 +299,11 @@ __global__ __launch_bounds__(64) void lmax_kernel(const InstState* inst_key, con
 // PF: on pools of at most 4,096 instances (one bitmap word per lane) the
 // holder bitmaps of a batch's popular positions are loaded together, before
 // the batch is applied in order.  RW, RU0: positions per lane of the
-// single-holder row walk's steps (run_walk).
-template <bool STAGED, bool PF, int RW = kWalkU, int RU0 = 4, class Put>
+// single-holder row walk's steps (run_walk).  BULK (pools of at most 4,096
+// instances): when a listed position drops many holders at once, their
+// put calls go word by word with the lanes over the word's bits (one
+// coalesced round of stores per word) rather than bit by bit per lane.
+template <bool STAGED, bool PF, int RW = kWalkU, int RU0 = 4, bool BULK = false, class Put>
 __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c,
                                            const uint64_t* stage, uint64_t* bmA, uint64_t* bmN,
                                            int32_t nw, uint32_t nalive, int32_t p, Put put,
@@ -382,17 +385,39 @@ __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c
       }
       __syncthreads();
       uint32_t live = 0;
-      for (int32_t w = lane; w < nw; w += 64) {
-        const uint64_t aw = bmA[w], nwd = bmN[w];
+      if (BULK && nw <= 64) {  // word `lane`; many leaving holders: lanes over each word's bits
+        const uint64_t aw = lane < nw ? bmA[lane] : 0ull, nwd = lane < nw ? bmN[lane] : 0ull;
         uint64_t d = aw & ~nwd;
-        while (d) {
-          const int b = __builtin_ctzll(d);
-          d &= d - 1;
-          put((uint32_t)(w * 64 + b), (uint32_t)pos);
+        if (__ballot(__popcll(d) > 4u)) {
+          for (int32_t w = 0; w < nw; ++w) {
+            const uint64_t dw = (uint64_t)lane_value64((int64_t)d, w);
+            if ((dw >> lane) & 1ull) put((uint32_t)(w * 64 + lane), (uint32_t)pos);
+          }
+        } else {
+          while (d) {
+            const int b = __builtin_ctzll(d);
+            d &= d - 1;
+            put((uint32_t)(lane * 64 + b), (uint32_t)pos);
+          }
         }
-        bmA[w] = nwd;
-        bmN[w] = 0ull;
-        live += (uint32_t)__popcll(nwd);
+        if (lane < nw) {
+          bmA[lane] = nwd;
+          bmN[lane] = 0ull;
+        }
+        live = (uint32_t)__popcll(nwd);
+      } else {
+        for (int32_t w = lane; w < nw; w += 64) {
+          const uint64_t aw = bmA[w], nwd = bmN[w];
+          uint64_t d = aw & ~nwd;
+          while (d) {
+            const int b = __builtin_ctzll(d);
+            d &= d - 1;
+            put((uint32_t)(w * 64 + b), (uint32_t)pos);
+          }
+          bmA[w] = nwd;
+          bmN[w] = 0ull;
+          live += (uint32_t)__popcll(nwd);
+        }
       }
       __syncthreads();
       nalive = wave_sum_u32(live);
@@ -1036,7 +1061,7 @@ __global__ __launch_bounds__(64) void popular_member_kernel(ScoreArgs a) {
       }
     }
     __syncthreads();
-    index_walk<true, true, 8, 4>(a, c, stage, bmA, bmN, nw, nalive, k,
+    index_walk<true, true, 8, 4, true>(a, c, stage, bmA, bmN, nw, nalive, k,
                                  [&](uint32_t id, uint32_t hh) { hp[id] = hh; }, lane, g, s);
     const uint32_t clsw = popular_class(a, rec, hp, off0, nw, lane);
     if (lane == 0) {
