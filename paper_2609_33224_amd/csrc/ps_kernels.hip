@@ -357,17 +357,38 @@ __device__ __forceinline__ void index_walk(const ScoreArgs& a, const ChainRef& c
       if (f && cnt > kPopular) {  // live &= holder bitmap, lane-owned words
         const uint64_t* bm = a.x.bitmaps + (size_t)off * a.x.nw;
         uint32_t live = 0;
-        for (int32_t w = lane; w < nw; w += 64) {
-          const uint64_t aw = bmA[w];
-          const uint64_t nwd = aw & (pf ? pw[t] : bm[w]);
-          uint64_t d = aw & ~nwd;
-          while (d) {
-            const int b = __builtin_ctzll(d);
-            d &= d - 1;
-            put((uint32_t)(w * 64 + b), (uint32_t)pos);
+        if (BULK && nw <= 64) {
+          const uint64_t aw = lane < nw ? bmA[lane] : 0ull;
+          const uint64_t nwd = aw & (lane < nw ? (pf ? pw[t] : bm[lane]) : 0ull);
+          const uint64_t d = aw & ~nwd;
+          if (__ballot(__popcll(d) > 4u)) {
+            for (int32_t w = 0; w < nw; ++w) {
+              const uint64_t dw = (uint64_t)lane_value64((int64_t)d, w);
+              if ((dw >> lane) & 1ull) put((uint32_t)(w * 64 + lane), (uint32_t)pos);
+            }
+          } else {
+            uint64_t dd = d;
+            while (dd) {
+              const int b = __builtin_ctzll(dd);
+              dd &= dd - 1;
+              put((uint32_t)(lane * 64 + b), (uint32_t)pos);
+            }
           }
-          bmA[w] = nwd;
-          live += (uint32_t)__popcll(nwd);
+          if (lane < nw) bmA[lane] = nwd;
+          live = (uint32_t)__popcll(nwd);
+        } else {
+          for (int32_t w = lane; w < nw; w += 64) {
+            const uint64_t aw = bmA[w];
+            const uint64_t nwd = aw & (pf ? pw[t] : bm[w]);
+            uint64_t d = aw & ~nwd;
+            while (d) {
+              const int b = __builtin_ctzll(d);
+              d &= d - 1;
+              put((uint32_t)(w * 64 + b), (uint32_t)pos);
+            }
+            bmA[w] = nwd;
+            live += (uint32_t)__popcll(nwd);
+          }
         }
         nalive = wave_sum_u32(live);
         used = t + 1;
@@ -948,10 +969,17 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void popular_prefix_kernel(Score
             const uint32_t off = __shfl(hq[t / 8].off, 8 * (t % 8)), cnt = __shfl(hq[t / 8].cnt, 8 * (t % 8));
             const uint64_t keep = !f ? 0ull : (cnt > kPopular ? pw[t] : list_word(a.x, off, cnt, lane));
             uint64_t d = have & ~keep;
-            while (d) {
-              const int b = __builtin_ctzll(d);
-              d &= d - 1ull;
-              atomicMin(&fmiss[lane * 64 + b], (uint32_t)(p0 + t));
+            if (__ballot(__popcll(d) > 4u)) {  // many leave here: lanes over each word's bits
+              for (int32_t w = 0; w < nw; ++w) {
+                const uint64_t dw = (uint64_t)lane_value64((int64_t)d, w);
+                if ((dw >> lane) & 1ull) atomicMin(&fmiss[w * 64 + lane], (uint32_t)(p0 + t));
+              }
+            } else {
+              while (d) {
+                const int b = __builtin_ctzll(d);
+                d &= d - 1ull;
+                atomicMin(&fmiss[lane * 64 + b], (uint32_t)(p0 + t));
+              }
             }
             have &= keep;
           }
