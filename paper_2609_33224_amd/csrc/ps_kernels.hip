@@ -599,8 +599,16 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
   const uint32_t x = ((uint32_t)(blockIdx.x * blockDim.x + threadIdx.x) >> 6) % (uint32_t)kXcds;
   // a bound on every group's segment length (its claims' lengths; only
   // lengths above one part's minimum matter to the walk pass)
+  // (the walk pass reads the maximum over all lists, so one atomic per
+  // workgroup, on its first wave's list, with the workgroup's maximum:
+  // atomics on these eight lines queue at the memory side)
   const uint32_t cmax = (uint32_t)(~wave_min_u64(~(uint64_t)(uint32_t)(first && slot >= 0 ? llen[h] : 0)));
-  if (lane == 0 && cmax > (uint32_t)kGroupPartMin) atomicMax(&G.lctr[x * kListCtrWords + 1], cmax);
+  __shared__ uint32_t wg_cmax;
+  if (tid == 0) wg_cmax = 0u;
+  __syncthreads();
+  if (lane == 0 && cmax > (uint32_t)kGroupPartMin) atomicMax(&wg_cmax, cmax);
+  __syncthreads();
+  if (tid == 0 && wg_cmax) atomicMax(&G.lctr[x * kListCtrWords + 1], wg_cmax);
   if (lm) {
     uint32_t base = 0u;
     if (lane == 0) base = atomicAdd(&G.lctr[x * kListCtrWords], (uint32_t)__popcll(lm));
