@@ -637,10 +637,21 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
       pop = f.y > kPopular && off0 < G.rep_cap;
     }
     const uint64_t pm = __ballot(pop);
+    // one count atomic per workgroup (it shares list 0's line, whose
+    // atomics queue at the memory side): waves' counts in LDS
+    __shared__ uint32_t pcnt[kClaimBlock / 64], pbase;
+    const int wv = tid >> 6;
+    if (lane == 0) pcnt[wv] = (uint32_t)__popcll(pm);
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t tot = 0u;
+      for (int k = 0; k < kClaimBlock / 64; ++k) tot += pcnt[k];
+      pbase = tot ? atomicAdd(&G.lctr[kPopCountWord], tot) : 0u;
+    }
+    __syncthreads();
     if (pm) {
-      uint32_t k0 = 0u;
-      if (lane == 0) k0 = atomicAdd(&G.lctr[kPopCountWord], (uint32_t)__popcll(pm));
-      k0 = (uint32_t)__shfl((int)k0, 0);
+      uint32_t k0 = pbase;
+      for (int k = 0; k < wv; ++k) k0 += pcnt[k];
       const uint32_t k = k0 + (uint32_t)__popcll(pm & ((1ull << lane) - 1ull));
       const bool listed = pop && k < G.plist_cap;
       if (listed) G.plist[k] = make_uint2((uint32_t)slot, off0);
