@@ -179,9 +179,9 @@ struct GroupTab {
   // pass lists the groups whose first block has a holder bitmap in `plist`
   // ({slot, bitmap number}, plist_cap entries; count in
   // lctr[kPopCountWord], cleared by the previous window's claim pass) and
-  // elects per bitmap the listed group with the least slot, its
-  // representative (`rep`: (kGroupGenMax - gen) << 32 | slot; an older
-  // window's word compares higher).  The prefix kernel walks each
+  // stores per bitmap one of its listed groups, its representative (`rep`:
+  // (kGroupGenMax - gen) << 32 | slot; a word with another window's tag is
+  // stale; any listed group gives the same outputs).  The prefix kernel walks each
   // representative's segment through the index while more than one holder
   // is live and keeps, per holder, the position where it dropped out (~0:
   // live at the stop, `pre_q`) in row `pre` of the bitmap; the member kernel

@@ -621,11 +621,10 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
     }
   }
   // A leader whose first block has a holder bitmap (a popular group) goes
-  // into the popular pass's list (one atomic per wave) and its slot into
-  // the bitmap's representative word (the least slot of the window: one
-  // minimum per bitmap and wave, skipped when the word already holds a
-  // lesser one, since atomics on one address queue).  Its class word says
-  // whether it was listed; the walk pass takes the others.
+  // into the popular pass's list (one count atomic per workgroup) and its
+  // slot into the bitmap's representative word (one plain store per bitmap
+  // and wave; whichever lands last represents the bitmap).  Its class word
+  // says whether it was listed; the walk pass takes the others.
   if (G.pop_pass) {
     bool pop = false;
     uint32_t off0 = 0u;
@@ -658,19 +657,16 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
       if (pop)
         G.rec[(size_t)slot * kGroupRec + kGroupClsWord] =
             make_uint2(kGroupNone, listed ? off0 : kGroupUnlisted);
+      // any listed group of a bitmap can represent it (the popular pass is
+      // exact for every choice), so a plain store: an atomic per wave on
+      // one word would queue at the memory side
       const unsigned long long tag = (kGroupGenMax - G.gen) << 32;
       uint64_t pend = __ballot(listed);
       while (pend) {
         const int src = __builtin_ctzll(pend);
         const uint32_t o = (uint32_t)__shfl((int)off0, src);
-        const bool same = listed && off0 == o;
-        const uint64_t sm = __ballot(same);
-        const uint32_t least = wave_min_u32(same ? (uint32_t)slot : 0xFFFFFFFFu);
-        if (lane == src) {
-          const unsigned long long want_rep = tag | (unsigned long long)least;
-          if (G.rep[o] > want_rep) atomicMin(G.rep + o, want_rep);
-        }
-        pend &= ~sm;
+        pend &= ~__ballot(listed && off0 == o);
+        if (lane == src) G.rep[o] = tag | (unsigned long long)(uint32_t)slot;
       }
     }
   }
@@ -2068,7 +2064,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void le
       __syncthreads();
     }
   }
-  if (deferred_any && lane == 0) atomicOr(a.defer_any, 1u);
+  if (deferred_any && lane == 0) *a.defer_any = 1u;  // (a plain store: every writer writes 1)
 }
 
 // ------------------------------------------------------- lean scorer, rows
@@ -2348,7 +2344,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
     if (live && (uint32_t)t < cnt) bmH[id >> 6] = 0ull;
     __syncthreads();
   }
-  if (__ballot(deferred_any) != 0ull && lane == 0) atomicOr(a.defer_any, 1u);
+  if (__ballot(deferred_any) != 0ull && lane == 0) *a.defer_any = 1u;  // (a plain store: every writer writes 1)
 }
 
 // One wave per instance that receives placements; its entries are applied
