@@ -120,6 +120,7 @@ struct ps_ctx {
   TopRoom* d_rtop = nullptr;         // the kTopRooms largest rooms with their ids
   int32_t lean_wpc = 0;              // resident lean-scorer waves per CU (0: not asked yet)
   int32_t rows_wpc = 0;              // the same for the four-requests-per-wave scorer
+  int32_t score_wpc = 0;             // the same for the general scorer (fast policy)
   int4* d_lm = nullptr;              // zero-hit admission thresholds in that order
   int32_t* d_lm1 = nullptr;          // their maxima per 64 positions
   uint4* d_csum = nullptr;           // per 64 positions: least t_iter (A1 > 1, A1 <= 1), largest room
@@ -162,6 +163,11 @@ struct ps_ctx {
   uint32_t glcap = 0;           // entries per list
   uint32_t gslots = 0;   // power of two
   int32_t greq_cap = 0;  // entries of d_gslot
+  // the rows scorer's hand-over: kDeferLists sub-list lengths (one 128-byte
+  // line each) and the sub-lists (dcap entries each)
+  uint32_t* d_dcnt = nullptr;
+  int32_t* d_dlist = nullptr;
+  int64_t dcap = 0;
   uint64_t ggen = 0;
   uint2* d_gplist = nullptr;  // the popular pass's groups
   uint32_t gplist_cap = 0;
@@ -508,6 +514,8 @@ ps_status ps_destroy(ps_ctx* c) {
   dfree(c->d_gkeys);
   dfree(c->d_grec);
   dfree(c->d_gslot);
+  dfree(c->d_dcnt);
+  dfree(c->d_dlist);
   dfree(c->d_gpop);
   dfree(c->d_glist);
   dfree(c->d_gplist);
@@ -719,6 +727,7 @@ ps_status ps_load_instances(ps_ctx* c, const ps_instances* in, const ps_model* m
   c->d_rtop = fresh.d_rtop;
   c->lean_wpc = 0;
   c->rows_wpc = 0;
+  c->score_wpc = 0;
   c->d_lm = fresh.d_lm;
   c->d_lm1 = fresh.d_lm1;
   c->d_csum = fresh.d_csum;
@@ -875,6 +884,9 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   a.sel = c->h_model.sel;
   a.defer_any = nullptr;
   a.defer_only = 0;
+  a.dcnt = nullptr;
+  a.dlist = nullptr;
+  a.dcap = 0;
   a.req_order = nullptr;
   const bool probe_all = d_hits != nullptr;
   if (probe_all) {  // longest chains first
@@ -943,6 +955,38 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
     }
     ev = &c->ev[kTimingEvents * (size_t)c->n_timed];
   }
+  // The lean scorer first when the groups give the requests their hits and
+  // the selector is neither Random nor H-C-Q (persistent grid at its own
+  // occupancy); the general scorer then finishes what it left.
+  const bool lean = !probe_all && a.grp.keys && a.sel != PS_SEL_RANDOM && a.sel != PS_SEL_HCQ;
+  const DevModel& hm = c->h_model;
+  const bool rows = lean && !d_sizes && hm.mono && !(hm.flags & PS_F_TTFT_ADMIT) &&
+                    (a.sel == PS_SEL_DCQ || a.sel == PS_SEL_DQ || a.sel == PS_SEL_DQC) &&
+                    c->n_inst <= kRowsMaxInst;
+  int rows_grid = 0;
+  if (rows) {
+    if (!c->rows_wpc) c->rows_wpc = ps_lean_rows_waves_per_cu(c->n_inst);
+    const int n_batch = (n_req + 3) / 4;
+    rows_grid = std::min(n_batch, c->num_cus * c->rows_wpc);
+    if (!fixed) {
+      // the hand-over sub-lists (the fixed scratch has no room for them):
+      // sub-list q takes the batches of rows waves q, q + kDeferLists, ...
+      const int64_t waves_q = (rows_grid + kDeferLists - 1) / kDeferLists;
+      const int64_t batches_w = (n_batch + rows_grid - 1) / rows_grid;
+      const int64_t cap = waves_q * batches_w * 4;
+      if (!c->d_dcnt)
+        HIP_TRY(c, hipMalloc((void**)&c->d_dcnt, (size_t)kDeferLists * kDeferStride * sizeof(uint32_t)));
+      if (cap > c->dcap) {
+        dfree(c->d_dlist);
+        c->dcap = 0;
+        HIP_TRY(c, hipMalloc((void**)&c->d_dlist, (size_t)kDeferLists * (size_t)cap * sizeof(int32_t)));
+        c->dcap = cap;
+      }
+      a.dcnt = c->d_dcnt;
+      a.dlist = c->d_dlist;
+      a.dcap = (int32_t)c->dcap;
+    }
+  }
   if (ev) HIP_TRY(c, hipEventRecord(ev[0], s));
   // the walk pass over the leaders' lists: a wave per four requests (about
   // two waves per group at the usual group sizes), so the dispatcher
@@ -953,18 +997,8 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   else if (ev)
     HIP_TRY(c, hipEventRecord(ev[1], s));
   if (ev) HIP_TRY(c, hipEventRecord(ev[2], s));
-  // The lean scorer first when the groups give the requests their hits and
-  // the selector is neither Random nor H-C-Q (persistent grid at its own
-  // occupancy); the general scorer then finishes what it left.
-  const bool lean = !probe_all && a.grp.keys && a.sel != PS_SEL_RANDOM && a.sel != PS_SEL_HCQ;
-  const DevModel& hm = c->h_model;
-  const bool rows = lean && !d_sizes && hm.mono && !(hm.flags & PS_F_TTFT_ADMIT) &&
-                    (a.sel == PS_SEL_DCQ || a.sel == PS_SEL_DQ || a.sel == PS_SEL_DQC) &&
-                    c->n_inst <= kRowsMaxInst;
   if (rows) {  // four requests per wave
-    if (!c->rows_wpc) c->rows_wpc = ps_lean_rows_waves_per_cu(c->n_inst);
-    const int resident = c->num_cus * c->rows_wpc;
-    HIP_TRY(c, ps_launch_lean_rows(a, std::min((n_req + 3) / 4, resident), s));
+    HIP_TRY(c, ps_launch_lean_rows(a, rows_grid, s));
     a.defer_only = 1;
   } else if (lean) {
     if (!c->lean_wpc) c->lean_wpc = ps_lean_waves_per_cu(c->n_inst);
@@ -978,9 +1012,16 @@ static ps_status launch_score(ps_ctx* c, const uint64_t* d_pool, int64_t pool_le
   if (ev) HIP_TRY(c, hipEventRecord(ev[3], s));
   // Finishing what the lean kernel left, the general kernel runs on at most
   // four waves per resident slot: enough waves to balance uneven work (the
-  // popular groups), few enough that an empty pass costs little.
-  HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, lean ? std::min(grid, c->num_cus * 64) : grid,
-                             probe_all, s, rows));
+  // popular groups), few enough that an empty pass costs little.  With the
+  // rows scorer's hand-over lists it runs on its resident waves, each taking
+  // an equal share of them.
+  int sgrid = lean ? std::min(grid, c->num_cus * 64) : grid;
+  if (a.dlist) {
+    if (!c->score_wpc) c->score_wpc = ps_score_waves_per_cu(c->n_inst, c->hits_in_lds, rows);
+    sgrid = c->num_cus * c->score_wpc;
+    if (!c->hits_in_lds && !ps_score_small(c->n_inst)) sgrid = std::min(sgrid, c->scratch_rows);
+  }
+  HIP_TRY(c, ps_launch_score(a, c->hits_in_lds, sgrid, probe_all, s, rows));
   if (ev) {
     HIP_TRY(c, hipEventRecord(ev[4], s));
     ++c->n_timed;

@@ -240,7 +240,17 @@ struct ScoreArgs {
   uint32_t sel;          // the model's selector (host copy, picks the kernels)
   uint32_t* defer_any;   // set when the lean kernel left requests to the general one
   int32_t defer_only;    // general kernel: score only requests marked as left to it
+  // Hand-over from the rows scorer (dlist == nullptr: the general kernel
+  // reads every request's mark instead): the requests it left, in
+  // kDeferLists sub-lists of dcap entries (rows wave w appends to sub-list
+  // w % kDeferLists); sub-list q's length in dcnt[q * kDeferStride] (one
+  // 128-byte line each, cleared by the claim pass).
+  uint32_t* dcnt;
+  int32_t* dlist;
+  int32_t dcap;
 };
+constexpr int kDeferLists = 64;
+constexpr int kDeferStride = 32;
 
 // Order of the exhaustive probe: requests by descending chain length in
 // bins of 256 blocks (chains of 16,128 blocks or more share the first bin),
@@ -364,6 +374,8 @@ constexpr int32_t kRowsMaxInst = 4096;
 hipError_t ps_launch_lean_rows(const ps::ScoreArgs& a, int grid, hipStream_t s);
 size_t ps_lean_rows_lds_bytes(int32_t n_inst);
 int32_t ps_lean_rows_waves_per_cu(int32_t n_inst);
+// The general kernel's resident waves per CU.
+int32_t ps_score_waves_per_cu(int32_t n_inst, bool hits_in_lds, bool fast);
 // Lean scorer (requests with group records); its LDS and resident waves per CU.
 hipError_t ps_launch_lean(const ps::ScoreArgs& a, int grid, hipStream_t s);
 size_t ps_lean_lds_bytes(int32_t n_inst);

@@ -537,6 +537,8 @@ __global__ __launch_bounds__(kClaimBlock) void group_claim_kernel(ScoreArgs a) {
   if (blockIdx.x == 0 && threadIdx.x < 2 * kXcds)  // the next window's list lengths and longest segments
     G.lctr_next[(threadIdx.x >> 1) * kListCtrWords + (threadIdx.x & 1u)] = 0u;
   if (blockIdx.x == 0 && threadIdx.x == 0) G.lctr_next[kPopCountWord] = 0u;  // and popular count
+  if (a.dlist && blockIdx.x == 0 && threadIdx.x < kDeferLists)  // the rows scorer's hand-over
+    a.dcnt[threadIdx.x * kDeferStride] = 0u;
   const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   const int lane = threadIdx.x & 63;
   bool want = false;
@@ -1170,9 +1172,39 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
-  if (a.defer_only && *a.defer_any == 0u) return;  // nothing was left to this kernel
+  // With the hand-over lists, only the listed requests: lane l holds the
+  // running total of the sub-lists' lengths through sub-list l.
+  const bool listed = a.defer_only && a.dlist != nullptr;
+  uint32_t lincl = listed ? a.dcnt[lane * kDeferStride] : 0u;
+  static_assert(kDeferLists == 64, "one sub-list per lane");
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = (uint32_t)__shfl_up((int)lincl, d);
+    if (lane >= d) lincl += o;
+  }
+  const uint32_t n_listed = (uint32_t)__builtin_amdgcn_readlane((int)lincl, 63);
+  if (listed ? n_listed == 0u : a.defer_only && *a.defer_any == 0u) return;  // nothing was left
+  // entry i of the concatenated sub-lists (per lane; every lane takes part)
+  auto listed_req = [&](uint32_t i) -> int32_t {
+    int q = 0;  // sub-lists that end at or before i
+#pragma unroll
+    for (int step = 32; step >= 1; step >>= 1)
+      if ((uint32_t)__shfl((int)lincl, q + step - 1) <= i) q += step;
+    const uint32_t before = (uint32_t)__shfl((int)lincl, q > 0 ? q - 1 : 0);
+    return a.dlist[(size_t)q * (size_t)a.dcap + (i - (q > 0 ? before : 0u))];
+  };
   __shared__ DevModel lmodel;
   stage_model(lmodel, a.model, lane, 64);
+  // FAST (pools of at most 4,096 instances: at most 64 chunks of the key
+  // order): the chunk summaries and threshold maxima, window constants, in
+  // LDS for the whole launch
+  __shared__ uint4 lcsum[FAST ? 64 : 1];
+  __shared__ int32_t llm1v[FAST ? 64 : 1];
+  if (FAST) {
+    const int32_t n1c = (n_inst + 63) >> 6;
+    lcsum[lane] = lane < n1c ? a.csum[lane] : make_uint4(0u, 0u, 0u, 0u);
+    llm1v[lane] = lane < n1c ? a.lm1[lane] : -1;
+  }
   __syncthreads();
   const DevModel& m = lmodel;
   uint32_t* const sizes = FAST ? nullptr : a.sizes;
@@ -1194,15 +1226,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
   // Requests are taken in batches of a.batch (<= kBatch) consecutive ones: their
   // descriptors and group slots arrive with one round trip, their group
   // records with a second, into LDS; then each is scored from there.
-  const int32_t B = a.batch;
-  for (int32_t rb = blockIdx.x * B; rb < a.n_req; rb += gridDim.x * B) {
-    const int32_t nb = a.n_req - rb < B ? a.n_req - rb : B;
+  // Listed: this wave takes every gridDim.x-th entry of the concatenated
+  // sub-lists from entry blockIdx.x (equal shares; entries of one group,
+  // which cost alike, spread over the waves), in batches of kBatch (its
+  // entries read 64 at a time into lanes); otherwise batches of
+  // consecutive requests, every gridDim.x-th batch.
+  const int32_t B = listed ? kBatch : a.batch;
+  const int32_t k_lo = listed ? 0 : blockIdx.x * B;
+  const int32_t k_hi = !listed ? a.n_req
+                       : n_listed > blockIdx.x ? (int32_t)((n_listed - 1u - blockIdx.x) / gridDim.x) + 1 : 0;
+  const int32_t k_step = listed ? B : (int32_t)gridDim.x * B;
+  int32_t lbase = k_lo - 64, litem = 0;  // listed: this wave's entries lbase .. lbase + 63 in litem
+  for (int32_t rb = k_lo; rb < k_hi; rb += k_step) {
+    const int32_t nb = k_hi - rb < B ? k_hi - rb : B;
+    int32_t rq = rb + lane;  // the request of the batch's entry `lane` (lane < nb)
+    if (listed) {
+      if (rb + nb > lbase + 64) {
+        lbase = rb;
+        const uint32_t i = blockIdx.x + gridDim.x * (uint32_t)(lbase + lane);
+        const int32_t v = listed_req(i < n_listed ? i : n_listed - 1u);
+        litem = lbase + lane < k_hi ? v : 0;
+      }
+      rq = __shfl(litem, (rb - lbase + lane) & 63);
+    }
+    const int32_t rq3 = __shfl(rq, lane < 3 * nb ? lane / 3 : 0);
     __syncthreads();  // the previous batch is done with the batch buffers
     if (lane < nb) {
-      lgso[lane] = a.grp.keys ? a.grp.slot_of[rb + lane] : kGroupNoSlot;
-      if (a.defer_only) ldef[lane] = a.out[rb + lane].flags & kDeferred;
+      lgso[lane] = a.grp.keys ? a.grp.slot_of[rq] : kGroupNoSlot;
+      if (a.defer_only) ldef[lane] = listed ? kDeferred : a.out[rq].flags & kDeferred;
     }
-    if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rb)[lane];
+    if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rq3)[lane % 3];
     __syncthreads();
     for (int32_t w = lane; w < nb * kGroupRec; w += 64) {
       const uint32_t so = lgso[w / kGroupRec];
@@ -1211,7 +1264,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
     }
     __syncthreads();
     for (int32_t b = 0; b < nb; ++b) {
-      const int32_t r = rb + b;
+      const int32_t r = __builtin_amdgcn_readlane(rq, b);
       if (a.defer_only && __builtin_amdgcn_readfirstlane((int)ldef[b]) == 0) continue;
       // wave-uniform values read from LDS are moved to scalar registers
       const uint32_t gso = (uint32_t)__builtin_amdgcn_readfirstlane((int)lgso[b]);
@@ -1325,7 +1378,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
                 const int32_t cc = c0 + lane;
                 bool may = false;
                 if (cc < n1) {
-                  const uint4 cs = a.csum[cc];
+                  const uint4 cs = FAST ? lcsum[cc] : a.csum[cc];
                   const int64_t rmx = (int64_t)(((uint64_t)cs.w << 32) | cs.z);
                   may = rmx >= L && (notpot || __uint_as_float(cs.x) + xK < m.tau ||
                                      __uint_as_float(cs.y) < m.tau);
@@ -1372,7 +1425,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
               bool found = false;
               for (int32_t c0 = 0; c0 < n1 && !found; c0 += 64) {
                 const int32_t cc = c0 + lane;
-                uint64_t cm = __ballot(cc < n1 && (SMALL || a.lm1[cc] >= ell));
+                uint64_t cm = __ballot(cc < n1 && (SMALL || (FAST ? llm1v[cc] : a.lm1[cc]) >= ell));
                 while (cm && !found) {
                   const int32_t k = (c0 + __builtin_ctzll(cm)) * 64 + lane;
                   cm &= cm - 1;
@@ -1665,7 +1718,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
             const int32_t n1 = (n_inst + 63) >> 6;
             for (int32_t c0 = 0; c0 < n1 && !done0; c0 += 64) {
               const int32_t cc = c0 + lane;
-              uint64_t cm = __ballot(cc < n1 && (SMALL || a.lm1[cc] >= ell));
+              uint64_t cm = __ballot(cc < n1 && (SMALL || (FAST ? llm1v[cc] : a.lm1[cc]) >= ell));
               while (cm && !done0) {
                 const int32_t k0 = (c0 + __builtin_ctzll(cm)) * 64;
                 cm &= cm - 1;
@@ -2155,6 +2208,19 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
   };
   static_assert(sizeof(ps_req) == 24, "a descriptor is 16 + 8 bytes");
   read_desc((int32_t)blockIdx.x * 4 + q);
+  // Hand-over to the general kernel: a batch's left requests (lanes t = 0
+  // of their rows in hdm, their ids in hr) go to this wave's sub-list at
+  // the place the count atomic returned (lane 0's hbase).
+  uint64_t hdm = 0ull;
+  uint32_t hbase = 0u;
+  int32_t hr = 0;
+  int32_t* const hlist = a.dlist ? a.dlist + (size_t)(blockIdx.x % kDeferLists) * (size_t)a.dcap : nullptr;
+  auto hand_over = [&]() {
+    if (hdm != 0ull) {
+      const uint32_t b0 = (uint32_t)__shfl((int)hbase, 0);
+      if ((hdm >> lane) & 1ull) hlist[b0 + (uint32_t)__popcll(hdm & ((1ull << lane) - 1ull))] = hr;
+    }
+  };
 
   for (int32_t rb = blockIdx.x * 4; rb < a.n_req; rb += gridDim.x * 4) {
     const int32_t r = rb + q;
@@ -2340,10 +2406,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
       else a.out[r] = res;
     }
     if (fate == 2u) deferred_any = true;
+    if (a.dlist) {
+      // the previous batch's left requests: their positions have arrived
+      hand_over();
+      // this batch's: places reserved now, written a batch later (the
+      // count atomic's return is not waited for here)
+      hdm = __ballot(t == 0 && fate == 2u);
+      hr = r;
+      if (hdm != 0ull && lane == 0)
+        hbase = atomicAdd(a.dcnt + (blockIdx.x % kDeferLists) * kDeferStride, (uint32_t)__popcll(hdm));
+    }
     __syncthreads();
     if (live && (uint32_t)t < cnt) bmH[id >> 6] = 0ull;
     __syncthreads();
   }
+  if (a.dlist) hand_over();
   if (__ballot(deferred_any) != 0ull && lane == 0) *a.defer_any = 1u;  // (a plain store: every writer writes 1)
 }
 
@@ -2539,6 +2616,22 @@ hipError_t ps_launch_lean_rows(const ScoreArgs& a, int grid, hipStream_t s) {
   else
     hipLaunchKernelGGL(lean_rows_kernel<false>, dim3(grid), dim3(64), lds, s, a);
   return hipGetLastError();
+}
+
+int32_t ps_score_waves_per_cu(int32_t n_inst, bool hits_in_lds, bool fast) {
+  int blocks = 0;
+  const size_t lds = ps_score_lds_bytes(n_inst);
+  hipError_t e;
+  if (ps_score_small(n_inst))
+    e = fast ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, score_kernel<true, true, true>, 64, lds)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, score_kernel<true, true, false>, 64, lds);
+  else if (hits_in_lds)
+    e = fast ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, score_kernel<true, false, true>, 64, lds)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, score_kernel<true, false, false>, 64, lds);
+  else
+    e = fast ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, score_kernel<false, false, true>, 64, lds)
+             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, score_kernel<false, false, false>, 64, lds);
+  return e == hipSuccess && blocks > 0 ? blocks : 12;
 }
 
 hipError_t ps_launch_lmax(const InstState* inst_key, const uint32_t* order0, const DevModel* m,
