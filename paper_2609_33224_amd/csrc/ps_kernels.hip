@@ -1131,7 +1131,10 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
 constexpr int32_t kBatch = 4;  // most requests whose inputs one wave loads together
 // Bytes of the batch buffers: group records, descriptors, group slots,
 // deferral marks (a multiple of 16).
-constexpr size_t kBatchLds = (size_t)kBatch * (kGroupRec * 8 + 3 * 8 + 4 + 4);
+// the general kernel's batch buffers: with the hand-over lists a wave loads
+// up to kListBatch entries of its share together
+constexpr int32_t kListBatch = 16;
+constexpr size_t kBatchLds = (size_t)kListBatch * (kGroupRec * 8 + 3 * 8 + 4 + 4);
 // Result flag of a request the lean scoring kernel left to the general one
 // (never returned: the general kernel overwrites the result).
 constexpr uint32_t kDeferred = 0x80000000u;
@@ -1163,19 +1166,23 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
   uint16_t* cl = reinterpret_cast<uint16_t*>(ch + 64);
   uint16_t* hits = HITS_IN_LDS ? cl + 64 : a.scratch + (size_t)blockIdx.x * (size_t)n_inst;
   uint2* lrec = reinterpret_cast<uint2*>(smem + score_lds_base(n_inst, HITS_IN_LDS));
-  int64_t* lq64 = reinterpret_cast<int64_t*>(lrec + kBatch * kGroupRec);
-  uint32_t* lgso = reinterpret_cast<uint32_t*>(lq64 + 3 * kBatch);
-  uint32_t* ldef = lgso + kBatch;
-  int64_t* lroom = reinterpret_cast<int64_t*>(ldef + kBatch);
+  int64_t* lq64 = reinterpret_cast<int64_t*>(lrec + kListBatch * kGroupRec);
+  uint32_t* lgso = reinterpret_cast<uint32_t*>(lq64 + 3 * kListBatch);
+  uint32_t* ldef = lgso + kListBatch;
+  int64_t* lroom = reinterpret_cast<int64_t*>(ldef + kListBatch);
   InstState* linst = reinterpret_cast<InstState*>(lroom + kSmallPool);
   int4* llm = reinterpret_cast<int4*>(linst + kSmallPool);
   const int lane = threadIdx.x;
   const int g = lane >> 3, s = lane & 7;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
   // With the hand-over lists, only the listed requests: lane l holds the
-  // running total of the sub-lists' lengths through sub-list l.
+  // running total of the sub-lists' lengths through sub-list l.  (Reading
+  // the model and window constants before the test costs the empty pass
+  // more than it saves a full one.)
   const bool listed = a.defer_only && a.dlist != nullptr;
   uint32_t lincl = listed ? a.dcnt[lane * kDeferStride] : 0u;
+  const uint32_t dany = !listed && a.defer_only ? *a.defer_any : 1u;
+
   static_assert(kDeferLists == 64, "one sub-list per lane");
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
@@ -1183,16 +1190,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
     if (lane >= d) lincl += o;
   }
   const uint32_t n_listed = (uint32_t)__builtin_amdgcn_readlane((int)lincl, 63);
-  if (listed ? n_listed == 0u : a.defer_only && *a.defer_any == 0u) return;  // nothing was left
-  // entry i of the concatenated sub-lists (per lane; every lane takes part)
-  auto listed_req = [&](uint32_t i) -> int32_t {
-    int q = 0;  // sub-lists that end at or before i
-#pragma unroll
-    for (int step = 32; step >= 1; step >>= 1)
-      if ((uint32_t)__shfl((int)lincl, q + step - 1) <= i) q += step;
-    const uint32_t before = (uint32_t)__shfl((int)lincl, q > 0 ? q - 1 : 0);
-    return a.dlist[(size_t)q * (size_t)a.dcap + (i - (q > 0 ? before : 0u))];
-  };
+  if (listed ? n_listed == 0u : dany == 0u) return;  // nothing was left
   __shared__ DevModel lmodel;
   stage_model(lmodel, a.model, lane, 64);
   // FAST (pools of at most 4,096 instances: at most 64 chunks of the key
@@ -1205,6 +1203,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
     lcsum[lane] = lane < n1c ? a.csum[lane] : make_uint4(0u, 0u, 0u, 0u);
     llm1v[lane] = lane < n1c ? a.lm1[lane] : -1;
   }
+  // entry i of the concatenated sub-lists (per lane; every lane takes part)
+  auto listed_req = [&](uint32_t i) -> int32_t {
+    int q = 0;  // sub-lists that end at or before i
+#pragma unroll
+    for (int step = 32; step >= 1; step >>= 1)
+      if ((uint32_t)__shfl((int)lincl, q + step - 1) <= i) q += step;
+    const uint32_t before = (uint32_t)__shfl((int)lincl, q > 0 ? q - 1 : 0);
+    return a.dlist[(size_t)q * (size_t)a.dcap + (i - (q > 0 ? before : 0u))];
+  };
   __syncthreads();
   const DevModel& m = lmodel;
   uint32_t* const sizes = FAST ? nullptr : a.sizes;
@@ -1231,7 +1238,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
   // which cost alike, spread over the waves), in batches of kBatch (its
   // entries read 64 at a time into lanes); otherwise batches of
   // consecutive requests, every gridDim.x-th batch.
-  const int32_t B = listed ? kBatch : a.batch;
+  const int32_t B = listed ? kListBatch : a.batch;
   const int32_t k_lo = listed ? 0 : blockIdx.x * B;
   const int32_t k_hi = !listed ? a.n_req
                        : n_listed > blockIdx.x ? (int32_t)((n_listed - 1u - blockIdx.x) / gridDim.x) + 1 : 0;
@@ -1257,10 +1264,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void sc
     }
     if (lane < 3 * nb) lq64[lane] = reinterpret_cast<const int64_t*>(a.reqs + rq3)[lane % 3];
     __syncthreads();
-    for (int32_t w = lane; w < nb * kGroupRec; w += 64) {
-      const uint32_t so = lgso[w / kGroupRec];
-      if (so != kGroupNoSlot)
-        lrec[w] = a.grp.rec[(size_t)(so & ~kGroupLead) * kGroupRec + (uint32_t)(w % kGroupRec)];
+    // the records' words, three loads in flight per lane (loads at slot 0
+    // stand in for requests without one)
+    for (int32_t w0 = lane; w0 < nb * kGroupRec; w0 += 3 * 64) {
+      uint2 rv[3];
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int32_t w = w0 + 64 * u;
+        const uint32_t so = w < nb * kGroupRec ? lgso[w / kGroupRec] : kGroupNoSlot;
+        rv[u] = a.grp.rec[(size_t)(so != kGroupNoSlot ? so & ~kGroupLead : 0u) * kGroupRec + (uint32_t)(w % kGroupRec)];
+      }
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int32_t w = w0 + 64 * u;
+        if (w < nb * kGroupRec && lgso[w / kGroupRec] != kGroupNoSlot) lrec[w] = rv[u];
+      }
     }
     __syncthreads();
     for (int32_t b = 0; b < nb; ++b) {
