@@ -309,13 +309,13 @@ def score_bytes(win, r0, hits, grp=None):
     hits as sparse pairs ("Hk", "Hv").
 
     Requests of a popular group with a shared-hit class below their
-    segment end take the general kernel's class path: descriptor, slot,
-    144 B record, result, the 64 largest rooms (1 KB), the holder bitmap,
-    32 B per exception's state and its resume walk, the 16-byte summaries
-    of the key-ordered chunks, one chunk of 64 key-ordered states with
-    their ids, one chunk of thresholds with the chunk maxima, and the
-    chosen state (a lower bound: later chunks and the fallback scan are
-    not counted).
+    segment end take the general kernel's class path: the hand-over entry
+    (4 B written by the rows kernel, 4 B read), descriptor, slot, 144 B
+    record, result, the 64 largest rooms (1 KB), the holder bitmap, 32 B
+    per exception's state and its resume walk, one chunk of 64 key-ordered
+    states with their ids, one chunk of thresholds, and the chosen state (a
+    lower bound: later chunks and the fallback scan are not counted; the
+    chunk summaries and maxima sit in LDS for a wave's whole launch).
 
     Other requests go through the general kernel: descriptor, slot, result;
     the 64-way search of the sorted rooms; with a popular group row the
@@ -404,8 +404,8 @@ def score_bytes(win, r0, hits, grp=None):
     if clsp.any():
         p_exc = (p_Hg >= 1) & (p_Hg != grp["hs"][pr])    # holders off the class hit
         ex_res = per_row(np.where(p_resume & p_exc, p_rb, 0))
-        cby = (24 + 4 + 8 * 18 + 20 + 64 * 16 + 8 * nw + 32 * per_row(p_exc) + ex_res +
-               16 * n1 + 64 * (4 + 32) + 4 * n1 + 64 * 16 + 32)
+        cby = (4 + 4 + 24 + 4 + 8 * 18 + 20 + 64 * 16 + 8 * nw + 32 * per_row(p_exc) + ex_res +
+               64 * (4 + 32) + 64 * 16 + 32)
         by = np.where(clsp, cby, by)
     # The recomputation filter: W = max(0, T_pf(n, c) - T_pf(0, L)); a
     # non-holder (n = L) has W = max(0, Z).
