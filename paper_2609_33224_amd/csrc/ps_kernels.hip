@@ -746,6 +746,13 @@ __device__ __forceinline__ uint32_t popular_class(const ScoreArgs& a, uint2* rec
   return (nexc <= kGroupHold && hs > 0u && hs < (1u << 24)) ? ((nexc << 24) | hs) : kGroupNone;
 }
 
+// a wave-uniform 64-bit value in scalar registers
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // Prefix groups, pass 2 (a persistent grid over the leaders' lists, which
 // the claim pass wrote): the walk of the group's longest segment on every
 // holder of its first block, into the slot's record (up to kGroupHold
@@ -782,13 +789,11 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
   q0 = q0 < qp ? q0 : qp;
   const uint32_t Q = q0 < 1u ? 1u : (q0 > kGroupSplitMax ? kGroupSplitMax : q0);
   const uint32_t nx = (uint32_t)__builtin_amdgcn_readfirstlane((int)G.lctr[x * kListCtrWords]) * Q;
-  for (uint32_t v = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u); v < nx; v += gridDim.x >> 3) {
-    const uint32_t idx = v / Q, part = v % Q;
-    const unsigned long long ent = G.lists[(size_t)x * G.lcap + idx];
+  auto group_one = [&](uint32_t v, unsigned long long ent, unsigned long long plw, uint64_t key0) {
+    const uint32_t part = v % Q;
     const uint32_t slot = (uint32_t)(ent & 0xFFFFFFull);
     const int64_t pre_off = (int64_t)(ent >> 24) - 1;
-    const int32_t plen =
-        (int32_t)(G.plen[slot] & ((1ull << kGroupGenShift) - 1ull));  // every member lies in the pool
+    const int32_t plen = (int32_t)(plw & ((1ull << kGroupGenShift) - 1ull));  // every member lies in the pool
     // this wave's part of the segment: [s0, s1), at least kGroupPartMin
     // positions and whole 512-position compare steps (a part costs its own
     // preamble of dependent reads)
@@ -796,21 +801,21 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
     const int32_t step = step0 > kGroupPartMin ? step0 : kGroupPartMin;
     const int32_t s0 = (int32_t)part * step;
     const int32_t s1 = s0 + step < plen ? s0 + step : plen;
-    if (part != 0u && s0 >= plen) continue;  // (uniform: no workgroup barrier skipped)
+    if (part != 0u && s0 >= plen) return;  // (uniform: no workgroup barrier skipped)
     const ChainRef c{a.pool + pre_off, a.pool + pre_off, plen, plen};
-    // the segment's first block, read beside its length (the holders' row
-    // walks read the chain directly; only the index walk stages its head)
-    const uint64_t key0 = c.pre[0];
+    // (key0: the segment's first block, read beside its length; the
+    // holders' row walks read the chain directly, only the index walk
+    // stages its head)
     const IdxHit h0 = index_lookup(a.x, key0, g == 0, g, s);
     const bool found0 = __shfl(h0.found ? 1 : 0, 0) != 0;
     const uint32_t off0 = __shfl(h0.off, 0), cnt0 = __shfl(h0.cnt, 0);
     uint2* rec = G.rec + (size_t)slot * kGroupRec;
     uint32_t cnt = 0u;
     if (found0 && cnt0 > kGroupHold) {
-      if (part != 0u) continue;  // a popular group: one wave walks all holders
+      if (part != 0u) return;  // a popular group: one wave walks all holders
       if (cnt0 > kPopular && G.pop_pass &&
           (uint32_t)__builtin_amdgcn_readfirstlane((int)rec[kGroupClsWord].y) != kGroupUnlisted)
-        continue;  // listed by the claim pass: the popular pass's (it writes the record)
+        return;  // listed by the claim pass: the popular pass's (it writes the record)
       const int32_t nst = plen < kStage ? plen : kStage;
       __syncthreads();  // (the previous index walk is done with the stage)
       for (int32_t j = lane; j < nst; j += 64) stage[j] = c.pre[j];
@@ -862,6 +867,35 @@ __global__ __launch_bounds__(64) void group_kernel(ScoreArgs a) {
       cnt = cnt0;
     }
     if (lane == 0 && part == 0u) rec[0] = make_uint2((uint32_t)plen, cnt);
+  };
+  const uint32_t vstep = gridDim.x >> 3;
+  const uint32_t vfirst = (blockIdx.x >> 6) * 8u + (blockIdx.x & 7u);
+  // A group's first reads (its list entry, then its length word and first
+  // block) are issued a group ahead (the entry two ahead): they arrive
+  // while the group before walks.  Entries past the list's end read its
+  // last entry instead (never used).
+  auto entry_at = [&](uint32_t vv) -> unsigned long long {
+    return G.lists[(size_t)x * G.lcap + (vv < nx ? vv : nx - 1u) / Q];
+  };
+  unsigned long long ent_c = 0ull, ent_n = 0ull, plw_c = 0ull;
+  uint64_t key_c = 0ull;
+  if (vfirst < nx) {
+    ent_c = (unsigned long long)uniform64((int64_t)entry_at(vfirst));
+    ent_n = entry_at(vfirst + vstep);
+    plw_c = (unsigned long long)uniform64((int64_t)G.plen[(uint32_t)(ent_c & 0xFFFFFFull)]);
+    key_c = (uint64_t)uniform64((int64_t)a.pool[(int64_t)(ent_c >> 24) - 1]);
+  }
+  for (uint32_t v = vfirst; v < nx; v += vstep) {
+    // the next group's reads (ent_n arrived during this loop's last group)
+    const unsigned long long ent_nu = (unsigned long long)uniform64((int64_t)ent_n);
+    const unsigned long long plw_n = G.plen[(uint32_t)(ent_nu & 0xFFFFFFull)];
+    const uint64_t key_n = a.pool[(int64_t)(ent_nu >> 24) - 1];
+    const unsigned long long ent_nn = entry_at(v + 2u * vstep);
+    group_one(v, ent_c, plw_c, key_c);
+    ent_c = ent_nu;
+    plw_c = (unsigned long long)uniform64((int64_t)plw_n);
+    key_c = (uint64_t)uniform64((int64_t)key_n);
+    ent_n = ent_nn;
   }
 }
 
@@ -1123,11 +1157,6 @@ __global__ __launch_bounds__(64) void popular_member_kernel(ScoreArgs a) {
 // zero-hit thresholds, copied once per launch.
 constexpr int32_t kSmallPool = 64;
 
-__device__ __forceinline__ int64_t uniform64(int64_t v) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
 constexpr int32_t kBatch = 4;  // most requests whose inputs one wave loads together
 // Bytes of the batch buffers: group records, descriptors, group slots,
 // deferral marks (a multiple of 16).
