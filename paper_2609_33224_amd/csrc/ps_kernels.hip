@@ -2398,6 +2398,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void le
         cm &= cm - 1;
         searching = cm != 0ull;
       }
+      if (__ballot(searching) == 0ull) break;  // (no row loads another chunk)
       PS_ROWS_LOAD_CHUNK(searching ? cm : 0ull);
     }
 #undef PS_ROWS_LOAD_CHUNK
