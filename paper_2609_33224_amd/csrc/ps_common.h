@@ -558,8 +558,10 @@ __device__ __forceinline__ uint16_t encode_hit(uint32_t h) {
   return (uint16_t)(h > kHitMax ? kHitOverflow : h);
 }
 
+// bit i of a bitmap of 64-bit words, read as its 32-bit half (a 32-bit
+// shift instead of a 64-bit one: the scorers are bound by VALU issue)
 __device__ __forceinline__ bool test_bit(const uint64_t* bm, uint32_t i) {
-  return ((bm[i >> 6] >> (i & 63)) & 1ull) != 0ull;
+  return ((reinterpret_cast<const uint32_t*>(bm)[i >> 5] >> (i & 31u)) & 1u) != 0u;
 }
 
 // Per-lane accumulation over candidates of A: the selector's key over T
